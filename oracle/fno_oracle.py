@@ -1,0 +1,414 @@
+"""CPU float64 oracle of the FNO spectral-convolution layer.
+
+TEST INFRASTRUCTURE ONLY.  Nothing in the product path may import, call or
+execute this module: only the test suite, the package's smoke check and the
+benchmark's CPU-baseline leg use it.  It shares no code with the HIP library.
+
+What it computes (Tu et al., "Guaranteed Approximation Bounds for
+Mixed-Precision Neural Operators", ICLR 2024):
+
+* The Fourier convolution operator (K v)(x) = F^-1(R . T_K(F v))(x) of Sec. 2
+  ("FNO and extensions"), evaluated with discrete transforms on a regular grid.
+* The forward transform is the Riemann sum of the discretisation error's
+  definition in Sec. 3 (the sum of v(xi_j) phi(xi_j) |Q_j| with |Q_j| = 1/N),
+  i.e. the DFT normalised by 1/N ("forward" normalisation), sign e^{-i theta}
+  (the paper's basis uses e^{+}; for real data this is only conjugation, we
+  take the usual forward-FFT sign).
+* T_K keeps, on every axis but the last, the m_j lowest non-negative and the
+  m_j highest (negative) frequencies in ascending FFT order; on the last,
+  real-FFT axis it keeps k = 0..m_d-1.
+* R is a complex weight per retained mode mixing channels (Sec. 2), dense or
+  Tucker-factorised (the tensorised FNO of Sec. 2; Kolda-Bader mode products).
+* tanh pre-activation before the forward transform in half-precision mode
+  (Sec. 4.3); the full-precision mode has no pre-activation (App. B.8 uses
+  tanh only as an ablation).
+* The inverse takes y = sum_t c(k_d) Re(Yhat_t e^{+i theta}) with c = 1 on the
+  k_d = 0 and Nyquist planes and 2 elsewhere, and no 1/N.
+* The Tucker contraction is split into two-operand steps in the order a greedy
+  rule picks (Sec. 4.2: the next step is the one whose intermediate is
+  smallest).
+* Gradients use the real-gradient convention g = dL/dRe + i dL/dIm.
+
+Everything runs in float64/complex128 on the exact stored input values.
+
+Parity status: every function here is pinned by the oracle tests (brute-force
+sums, a library FFT, Parseval, closed forms, adjoint identities, finite
+differences and hand-derived greedy sequences); none is "parity unpinned".
+"""
+from __future__ import annotations
+
+import itertools
+from typing import Dict, List, Optional, Sequence, Tuple
+
+import numpy as np
+
+PREC_FP32 = "fp32"
+PREC_FP16_TANH = "fp16_tanh"
+
+POLICY_MIN_RESULT = "min_result"
+POLICY_MIN_NET = "min_net"
+
+
+# ---------------------------------------------------------------------------
+# Retained modes (T_K)
+# ---------------------------------------------------------------------------
+
+def mode_freq(n: int, m: int, last: bool) -> np.ndarray:
+    """FFT index k(t) of retained slot t on an axis of length n with m modes.
+
+    Leading axes keep 2m slots: t < m -> k = t, else k = n - 2m + t (the
+    negative frequencies -m..-1).  The last (real-FFT) axis keeps m slots,
+    k = t.  Sec. 2 names the truncation T_K without fixing the set; this is
+    the low-pass set the workloads use.
+    """
+    n, m = int(n), int(m)
+    if last:
+        if not (1 <= m <= n // 2 + 1):
+            raise ValueError("last-axis modes must satisfy 1 <= m <= n/2+1")
+        return np.arange(m, dtype=np.int64)
+    if not (1 <= m and 2 * m <= n):
+        raise ValueError("leading-axis modes must satisfy 1 <= m and 2m <= n")
+    t = np.arange(2 * m, dtype=np.int64)
+    return np.where(t < m, t, n - 2 * m + t)
+
+
+def retained(n: Sequence[int], modes: Sequence[int]) -> List[np.ndarray]:
+    d = len(n)
+    if len(modes) != d:
+        raise ValueError("modes must have one entry per spatial axis")
+    return [mode_freq(n[j], modes[j], j == d - 1) for j in range(d)]
+
+
+def multiplicity(k_last: np.ndarray, n_last: int) -> np.ndarray:
+    """c(k): 1 on the k_d = 0 and Nyquist (2 k_d = N_d) planes, 2 elsewhere."""
+    k = np.asarray(k_last)
+    return np.where((k == 0) | (2 * k == n_last), 1.0, 2.0)
+
+
+def dft_matrix(n: int, ks: np.ndarray, sign: int) -> np.ndarray:
+    """Naive DFT matrix E[t, x] = exp(sign * 2 pi i k_t x / n), phase reduced
+    exactly in integers before the float64 evaluation."""
+    r = np.outer(np.asarray(ks, dtype=np.int64), np.arange(n, dtype=np.int64)) % n
+    return np.exp(sign * 2j * np.pi * r.astype(np.float64) / n)
+
+
+# ---------------------------------------------------------------------------
+# Transforms
+# ---------------------------------------------------------------------------
+
+def _apply_axis(a: np.ndarray, mat: np.ndarray, axis: int) -> np.ndarray:
+    """Contract axis `axis` of a with mat[new, old]; the new axis stays put."""
+    out = np.tensordot(a, mat, axes=([axis], [1]))
+    return np.moveaxis(out, -1, axis)
+
+
+def preactivation(x: np.ndarray, precision: str) -> np.ndarray:
+    """u = tanh(x) in half-precision mode (Sec. 4.3), u = x in full precision."""
+    xf = np.asarray(x, dtype=np.float64)
+    if precision == PREC_FP16_TANH:
+        return np.tanh(xf)
+    if precision == PREC_FP32:
+        return xf
+    raise ValueError(precision)
+
+
+def forward_spectrum(u: np.ndarray, n: Sequence[int], modes: Sequence[int]) -> np.ndarray:
+    """Xhat[..., t] = (1/N) sum_x u[..., x] exp(-i theta(k(t), x)).
+
+    u has leading (batch, channel) axes followed by the d spatial axes.  The
+    sum is the Riemann sum of Sec. 3 with |Q_j| = 1/N, applied axis by axis
+    with naive DFT matrices (the d-dimensional exponential factorises).
+    """
+    d = len(n)
+    ks = retained(n, modes)
+    a = np.asarray(u, dtype=np.float64)
+    lead = a.ndim - d
+    for j in range(d - 1, -1, -1):
+        a = _apply_axis(a, dft_matrix(n[j], ks[j], -1), lead + j)
+    return a / float(np.prod(n))
+
+
+def inverse_spectrum(z: np.ndarray, n: Sequence[int], modes: Sequence[int],
+                     with_c: bool = True) -> np.ndarray:
+    """y[..., x] = sum_t c(k_d(t)) Re(z[..., t] exp(+i theta(k(t), x))), no 1/N.
+
+    with_c=False drops the multiplicity (used by the data gradient)."""
+    d = len(n)
+    ks = retained(n, modes)
+    a = np.asarray(z, dtype=np.complex128)
+    if with_c:
+        a = a * multiplicity(ks[-1], n[-1])
+    lead = a.ndim - d
+    for j in range(d):
+        a = _apply_axis(a, dft_matrix(n[j], ks[j], +1).T, lead + j)
+    return a.real
+
+
+# ---------------------------------------------------------------------------
+# Dense layer: forward and gradients
+# ---------------------------------------------------------------------------
+
+def contract_dense(xh: np.ndarray, w: np.ndarray) -> np.ndarray:
+    """Yhat[b, o, t] = sum_i Xhat[b, i, t] W[i, o, t] (R acting per mode)."""
+    return np.einsum("bi...,io...->bo...", xh, w)
+
+
+def fwd(x, w, n, modes, precision):
+    """y = F^-1(R . T_K(F tanh(x))) for dense complex w[Cin, Cout, K...]."""
+    u = preactivation(x, precision)
+    xh = forward_spectrum(u, n, modes)
+    return inverse_spectrum(contract_dense(xh, w), n, modes, with_c=True)
+
+
+def grad_spectrum(gy, n, modes) -> np.ndarray:
+    """G[b, o, t] = c(k_d) sum_x gy[b, o, x] exp(-i theta): the gradient of the
+    loss with respect to Yhat (unnormalised)."""
+    ks = retained(n, modes)
+    g = forward_spectrum(gy, n, modes) * float(np.prod(n))
+    return g * multiplicity(ks[-1], n[-1])
+
+
+def bwd_data(x, w, gy, n, modes, precision):
+    """gx: G -> gXhat = sum_o G conj(W) -> gu = (1/N) sum_t Re(gXhat e^{+i theta})
+    -> gx = gu (1 - tanh(x)^2) in half-precision mode."""
+    g = grad_spectrum(gy, n, modes)
+    gxh = np.einsum("bo...,io...->bi...", g, np.conj(w))
+    gu = inverse_spectrum(gxh, n, modes, with_c=False) / float(np.prod(n))
+    if precision == PREC_FP16_TANH:
+        t = np.tanh(np.asarray(x, dtype=np.float64))
+        return gu * (1.0 - t * t)
+    return gu
+
+
+def bwd_weight(x, gy, n, modes, precision):
+    """gW[i, o, t] = sum_b conj(Xhat[b, i, t]) G[b, o, t]."""
+    xh = forward_spectrum(preactivation(x, precision), n, modes)
+    g = grad_spectrum(gy, n, modes)
+    return np.einsum("bi...,bo...->io...", np.conj(xh), g)
+
+
+# ---------------------------------------------------------------------------
+# Greedy two-operand contraction order (Sec. 4.2)
+# ---------------------------------------------------------------------------
+
+def _size(idx: str, sizes: Dict[str, int]) -> int:
+    s = 1
+    for ch in idx:
+        s *= int(sizes[ch])
+    return s
+
+
+def pair_result(operands: Sequence[str], p: int, q: int, output: str) -> str:
+    """Indices kept by contracting operands p and q: those still needed by the
+    output or by another remaining operand; p's order first, then q's new
+    indices."""
+    others = set(output)
+    for r, op in enumerate(operands):
+        if r != p and r != q:
+            others.update(op)
+    res = [c for c in operands[p] if c in others]
+    res += [c for c in operands[q] if c in others and c not in res]
+    return "".join(res)
+
+
+def greedy_path(operands: Sequence[str], sizes: Dict[str, int], output: str,
+                policy: str = POLICY_MIN_RESULT) -> List[Tuple[int, int, str]]:
+    """Pairwise contraction order chosen greedily (Sec. 4.2).
+
+    At every step, among pairs that share an index (all pairs if none do),
+    take the one whose result is smallest (policy min_result: element count
+    of the intermediate) or that shrinks memory most (policy min_net: result
+    minus both inputs); ties go to the lexicographically smallest (p, q) of
+    the current list.  The two inputs leave the list and the result is
+    appended.  The final step produces the output index order.
+
+    Returns [(p, q, result_indices)] with p < q positions in the list at the
+    time of the step.
+    """
+    ops = list(operands)
+    steps: List[Tuple[int, int, str]] = []
+    while len(ops) > 1:
+        if len(ops) == 2:
+            steps.append((0, 1, output))
+            break
+        pairs = [(p, q) for p in range(len(ops)) for q in range(p + 1, len(ops))]
+        sharing = [(p, q) for (p, q) in pairs if set(ops[p]) & set(ops[q])]
+        cand = sharing if sharing else pairs
+        best = None
+        for (p, q) in cand:
+            res = pair_result(ops, p, q, output)
+            cost = _size(res, sizes)
+            if policy == POLICY_MIN_NET:
+                cost -= _size(ops[p], sizes) + _size(ops[q], sizes)
+            elif policy != POLICY_MIN_RESULT:
+                raise ValueError(policy)
+            if best is None or cost < best[0]:
+                best = (cost, p, q, res)
+        _, p, q, res = best
+        steps.append((p, q, res))
+        ops = [op for r, op in enumerate(ops) if r not in (p, q)] + [res]
+    return steps
+
+
+def path_macs(operands: Sequence[str], sizes: Dict[str, int],
+              steps: Sequence[Tuple[int, int, str]]) -> int:
+    """Complex multiply-adds of a path: result size x contracted extent."""
+    ops = list(operands)
+    total = 0
+    for p, q, res in steps:
+        shared = (set(ops[p]) | set(ops[q])) - set(res)
+        k = 1
+        for ch in shared:
+            k *= int(sizes[ch])
+        total += _size(res, sizes) * k
+        ops = [op for r, op in enumerate(ops) if r not in (p, q)] + [res]
+    return total
+
+
+def contract_path(arrays: Sequence[np.ndarray], operands: Sequence[str],
+                  steps: Sequence[Tuple[int, int, str]]) -> np.ndarray:
+    """Evaluate a pairwise path with two-operand einsums."""
+    arrs = list(arrays)
+    ops = list(operands)
+    for p, q, res in steps:
+        r = np.einsum(f"{ops[p]},{ops[q]}->{res}", arrs[p], arrs[q])
+        arrs = [a for i, a in enumerate(arrs) if i not in (p, q)] + [r]
+        ops = [o for i, o in enumerate(ops) if i not in (p, q)] + [res]
+    assert len(arrs) == 1
+    return arrs[0]
+
+
+# ---------------------------------------------------------------------------
+# Tucker-factorised weights
+# ---------------------------------------------------------------------------
+
+SPATIAL = "xyz"
+RANKS = "cdf"
+
+
+def tucker_labels(d: int, adjoint: bool = False) -> Tuple[List[str], str]:
+    """Index strings of [spectrum, core, u_in, u_out, u_1..u_d] and the output.
+
+    Forward: Xhat(b i x..) core(a e c..) u_in(i a) u_out(o e) u_j(x_j c_j)
+    -> (b o x..).  Adjoint (data gradient): G(b o x..) with the same factor
+    labels -> (b i x..)."""
+    sp = SPATIAL[:d]
+    rk = RANKS[:d]
+    first = ("bo" if adjoint else "bi") + sp
+    out = ("bi" if adjoint else "bo") + sp
+    ops = [first, "ae" + rk, "ia", "oe"] + [sp[j] + rk[j] for j in range(d)]
+    return ops, out
+
+
+def tucker_sizes(batch, c_in, c_out, kdims, rank) -> Dict[str, int]:
+    d = len(kdims)
+    s = {"b": batch, "i": c_in, "o": c_out, "a": rank[0], "e": rank[1]}
+    for j in range(d):
+        s[SPATIAL[j]] = kdims[j]
+        s[RANKS[j]] = rank[2 + j]
+    return s
+
+
+def tucker_dense(core, u_in, u_out, u_mode) -> np.ndarray:
+    """W[i, o, t_1..t_d] = core x_1 u_in x_2 u_out x_3 u_1 ... (mode products)."""
+    d = len(u_mode)
+    w = np.asarray(core, dtype=np.complex128)
+    # mode product along core axis 0 with u_in[i, a]
+    w = np.tensordot(u_in, w, axes=([1], [0]))               # i, e, r..
+    w = np.moveaxis(np.tensordot(u_out, w, axes=([1], [1])), 0, 1)  # i, o, r..
+    for j in range(d):
+        w = np.tensordot(w, u_mode[j], axes=([2], [1]))      # rank axis -> K_j last
+    return w
+
+
+def tucker_contract(spec, core, u_in, u_out, u_mode, n, modes,
+                    policy: str = POLICY_MIN_RESULT, adjoint: bool = False,
+                    steps=None):
+    """Contract a spectrum with Tucker weights along a greedy path.
+
+    forward:  Yhat[b, o, t] = sum_i spec[b, i, t] W[i, o, t]
+    adjoint:  gXhat[b, i, t] = sum_o spec[b, o, t] conj(W[i, o, t])
+    """
+    d = len(n)
+    ops, out = tucker_labels(d, adjoint)
+    if adjoint:
+        facs = [np.conj(core), np.conj(u_in), np.conj(u_out)] + [np.conj(u) for u in u_mode]
+    else:
+        facs = [core, u_in, u_out] + list(u_mode)
+    b = spec.shape[0]
+    c_first = spec.shape[1]
+    kd = spec.shape[2:]
+    c_in = u_in.shape[0]
+    c_out = u_out.shape[0]
+    rank = (core.shape[0], core.shape[1]) + tuple(core.shape[2:])
+    sizes = tucker_sizes(b, c_in, c_out, kd, rank)
+    if steps is None:
+        steps = greedy_path(ops, sizes, out, policy)
+    return contract_path([spec] + facs, ops, steps)
+
+
+def tucker_fwd(x, core, u_in, u_out, u_mode, n, modes, precision,
+               policy: str = POLICY_MIN_RESULT):
+    xh = forward_spectrum(preactivation(x, precision), n, modes)
+    yh = tucker_contract(xh, core, u_in, u_out, u_mode, n, modes, policy)
+    return inverse_spectrum(yh, n, modes, with_c=True)
+
+
+def tucker_bwd_data(x, core, u_in, u_out, u_mode, gy, n, modes, precision,
+                    policy: str = POLICY_MIN_RESULT):
+    g = grad_spectrum(gy, n, modes)
+    gxh = tucker_contract(g, core, u_in, u_out, u_mode, n, modes, policy, adjoint=True)
+    gu = inverse_spectrum(gxh, n, modes, with_c=False) / float(np.prod(n))
+    if precision == PREC_FP16_TANH:
+        t = np.tanh(np.asarray(x, dtype=np.float64))
+        return gu * (1.0 - t * t)
+    return gu
+
+
+def tucker_bwd_weight(x, gy, core, u_in, u_out, u_mode, n, modes, precision):
+    """Chain rule through the multilinear map W(core, factors):
+    g_F = sum gW * conj(dW/dF) for each factor F, with gW the dense gradient."""
+    d = len(n)
+    gw = bwd_weight(x, gy, n, modes, precision)             # i, o, t..
+    sp = SPATIAL[:d]
+    rk = RANKS[:d]
+    core = np.asarray(core)
+    cu_in, cu_out = np.conj(u_in), np.conj(u_out)
+    cmode = [np.conj(u) for u in u_mode]
+    ccore = np.conj(core)
+    gw_l = "io" + sp
+    mode_terms = ",".join(sp[j] + rk[j] for j in range(d))
+    g_core = np.einsum(f"{gw_l},ia,oe,{mode_terms}->ae{rk}", gw, cu_in, cu_out, *cmode)
+    g_in = np.einsum(f"{gw_l},ae{rk},oe,{mode_terms}->ia", gw, ccore, cu_out, *cmode)
+    g_out = np.einsum(f"{gw_l},ae{rk},ia,{mode_terms}->oe", gw, ccore, cu_in, *cmode)
+    g_mode = []
+    for j in range(d):
+        others = [sp[q] + rk[q] for q in range(d) if q != j]
+        arrs = [cmode[q] for q in range(d) if q != j]
+        spec = ",".join([gw_l, "ae" + rk, "ia", "oe"] + others)
+        g_mode.append(np.einsum(f"{spec}->{sp[j]}{rk[j]}", gw, ccore, cu_in, cu_out, *arrs))
+    return g_core, g_in, g_out, g_mode
+
+
+# ---------------------------------------------------------------------------
+# Comparison
+# ---------------------------------------------------------------------------
+
+def rel_l2(a, b) -> float:
+    """||a - b||_2 / ||b||_2 over the whole tensor in float64 (complex values
+    count as real pairs)."""
+    a = np.asarray(a)
+    b = np.asarray(b)
+    if np.iscomplexobj(a) or np.iscomplexobj(b):
+        a = np.asarray(a, dtype=np.complex128)
+        b = np.asarray(b, dtype=np.complex128)
+        num = np.sqrt(np.sum(np.abs(a - b) ** 2))
+        den = np.sqrt(np.sum(np.abs(b) ** 2))
+    else:
+        a = a.astype(np.float64)
+        b = b.astype(np.float64)
+        num = np.sqrt(np.sum((a - b) ** 2))
+        den = np.sqrt(np.sum(b ** 2))
+    if den == 0.0:
+        return float(num)
+    return float(num / den)

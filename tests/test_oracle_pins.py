@@ -1,0 +1,596 @@
+"""Pins of the CPU oracle against what the paper and the mathematics fix.
+
+None of these re-types the oracle's own formula: each compares it with a
+brute-force sum, a library FFT, an identity (Parseval, shift, adjointness,
+round trip), a closed form, a theorem's bound, finite differences or
+hand-derived integer tables.  The mutation tests at the end plant plausible
+mistakes in the oracle and check that at least one pin catches each.
+"""
+import itertools
+import json
+import os
+
+import numpy as np
+import pytest
+
+from oracle import fno_oracle as O
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+F32, F16T = O.PREC_FP32, O.PREC_FP16_TANH
+
+
+def _rng(seed):
+    return np.random.default_rng(np.random.SeedSequence([77, seed]))
+
+
+def _cplx(rng, shape, scale=1.0):
+    return (rng.standard_normal(shape) + 1j * rng.standard_normal(shape)) * scale
+
+
+# ---------------------------------------------------------------------------
+# Pin functions (return the error; used by tests and by mutation tests)
+# ---------------------------------------------------------------------------
+
+def pin_brute_force_2d():
+    """Quadruple-loop double sum on an 8x8 grid vs the separable oracle."""
+    rng = _rng(1)
+    n, modes = (8, 8), (2, 3)
+    u = rng.standard_normal(n)
+    k1 = [0, 1, 6, 7]
+    k2 = [0, 1, 2]
+    ref = np.zeros((4, 3), dtype=np.complex128)
+    for a, ka in enumerate(k1):
+        for c, kb in enumerate(k2):
+            s = 0j
+            for x1 in range(8):
+                for x2 in range(8):
+                    s += u[x1, x2] * np.exp(-2j * np.pi * (ka * x1 / 8 + kb * x2 / 8))
+            ref[a, c] = s / 64.0
+    got = O.forward_spectrum(u[None, None], n, modes)[0, 0]
+    return np.abs(got - ref).max()
+
+
+def pin_brute_force_3d():
+    rng = _rng(2)
+    n, modes = (4, 6, 8), (1, 2, 3)
+    u = rng.standard_normal(n)
+    ks = [[0, 3], [0, 1, 4, 5], [0, 1, 2]]
+    ref = np.zeros((2, 4, 3), dtype=np.complex128)
+    for ia, ka in enumerate(ks[0]):
+        for ib, kb in enumerate(ks[1]):
+            for ic, kc in enumerate(ks[2]):
+                s = 0j
+                for x1, x2, x3 in itertools.product(range(4), range(6), range(8)):
+                    s += u[x1, x2, x3] * np.exp(
+                        -2j * np.pi * (ka * x1 / 4 + kb * x2 / 6 + kc * x3 / 8))
+                ref[ia, ib, ic] = s / (4 * 6 * 8)
+    got = O.forward_spectrum(u[None, None], n, modes)[0, 0]
+    return np.abs(got - ref).max()
+
+
+def pin_numpy_rfftn(n=(16, 12), modes=(5, 4)):
+    """numpy's real FFT divided by N, read at the retained frequencies."""
+    rng = _rng(3)
+    u = rng.standard_normal((2, 3) + n)
+    lib = np.fft.rfftn(u, axes=tuple(range(2, 2 + len(n)))) / np.prod(n)
+    ks = O.retained(n, modes)
+    sel = lib[np.ix_(range(2), range(3), *ks)]
+    got = O.forward_spectrum(u, n, modes)
+    return np.abs(got - sel).max()
+
+
+def pin_parseval(n=(8, 10)):
+    """(1/N) sum u^2 = sum_k c(k) |Xhat_k|^2 over the half spectrum, all modes."""
+    rng = _rng(4)
+    u = rng.standard_normal(n)
+    modes = (n[0] // 2, n[1] // 2 + 1)
+    xh = O.forward_spectrum(u[None, None], n, modes)[0, 0]
+    c = O.multiplicity(O.retained(n, modes)[-1], n[-1])
+    lhs = np.mean(u * u)
+    rhs = np.sum(c * np.abs(xh) ** 2)
+    return abs(lhs - rhs) / lhs
+
+
+def pin_ramp(n_last=16, m=9):
+    """u[x1, x2] = x2: Xhat[0, k] = -1/2 + (i/2) cot(pi k / N) (k != 0),
+    Xhat[0, 0] = (N - 1)/2, other rows zero.  Imaginary part at k = 1 is the
+    closed form sum_j j sin(2 pi j / m) = -(m/2) cot(pi / m) used in the proof
+    of Thm 3.1."""
+    n = (4, n_last)
+    u = np.tile(np.arange(n_last, dtype=np.float64), (4, 1))
+    xh = O.forward_spectrum(u[None, None], n, (2, m))[0, 0]
+    k = np.arange(m)
+    ref_row = np.empty(m, dtype=np.complex128)
+    ref_row[0] = (n_last - 1) / 2.0
+    with np.errstate(divide="ignore"):
+        ref_row[1:] = -0.5 + 0.5j / np.tan(np.pi * k[1:] / n_last)
+    if 2 * (m - 1) == n_last:
+        ref_row[m - 1] = -0.5           # cot(pi/2) = 0 at Nyquist
+    ref = np.zeros_like(xh)
+    ref[0] = ref_row
+    return np.abs(xh - ref).max()
+
+
+def pin_shift(n=(8, 12), modes=(3, 5), s=(3, 5)):
+    """Circular shift by s multiplies Xhat_k by exp(-2 pi i <k, s/N>)."""
+    rng = _rng(5)
+    u = rng.standard_normal(n)
+    us = np.roll(u, shift=s, axis=(0, 1))
+    ks = O.retained(n, modes)
+    ph = np.exp(-2j * np.pi * (np.outer(ks[0], np.ones_like(ks[1])) * s[0] / n[0]
+                               + np.outer(np.ones_like(ks[0]), ks[1]) * s[1] / n[1]))
+    a = O.forward_spectrum(u[None, None], n, modes)[0, 0] * ph
+    b = O.forward_spectrum(us[None, None], n, modes)[0, 0]
+    return np.abs(a - b).max()
+
+
+def pin_round_trip(n=(8, 6), c=3):
+    """Identity weights with every mode retained reproduce u exactly."""
+    rng = _rng(6)
+    modes = tuple(nj // 2 for nj in n[:-1]) + (n[-1] // 2 + 1,)
+    kd = tuple(2 * m for m in modes[:-1]) + (modes[-1],)
+    u = rng.standard_normal((2, c) + n)
+    w = np.zeros((c, c) + kd, dtype=np.complex128)
+    for i in range(c):
+        w[i, i] = 1.0
+    y = O.fwd(u, w, n, modes, F32)
+    return np.abs(y - u).max()
+
+
+def pin_single_mode(n=(16, 12), modes=(3, 4), a=(14, 2), wv=0.7 - 0.4j):
+    """u = cos(theta_a) with a_d >= 1 retained, W = w delta_io at mode a only:
+    y = Re(w exp(i theta_a)).  Pins the sign, the phase and c(k)."""
+    x1, x2 = np.meshgrid(np.arange(n[0]), np.arange(n[1]), indexing="ij")
+    th = 2 * np.pi * (a[0] * x1 / n[0] + a[1] * x2 / n[1])
+    u = np.cos(th)
+    ks = O.retained(n, modes)
+    t0 = int(np.where(ks[0] == a[0])[0][0])
+    t1 = int(np.where(ks[1] == a[1])[0][0])
+    kd = (len(ks[0]), len(ks[1]))
+    w = np.zeros((1, 1) + kd, dtype=np.complex128)
+    w[0, 0, t0, t1] = wv
+    y = O.fwd(u[None, None], w, n, modes, F32)[0, 0]
+    ref = np.real(wv * np.exp(1j * th))
+    return np.abs(y - ref).max()
+
+
+def pin_irfftn(n=(8, 10), modes=(4, 6)):
+    """With all modes kept and a Hermitian-consistent half spectrum Z (taken
+    from the real FFT of a real field), inverse_spectrum(Z) equals N times
+    numpy's irfftn of Z placed on the full half grid."""
+    rng = _rng(7)
+    v = rng.standard_normal(n)
+    half = np.fft.rfftn(v)                       # consistent half spectrum
+    ks = O.retained(n, modes)
+    z = half[np.ix_(*ks)]
+    y = O.inverse_spectrum(z[None, None], n, modes)[0, 0]
+    ref = np.fft.irfftn(half, s=n, axes=(0, 1)) * np.prod(n)
+    return np.abs(y - ref).max() / np.abs(ref).max()
+
+
+def pin_fd_dense(precision, seed=11):
+    """Central finite differences of L = <gy, y> for x, Re W, Im W."""
+    rng = _rng(seed)
+    n, modes = (8, 8), (2, 2)
+    b, ci, co = 1, 2, 2
+    x = rng.standard_normal((b, ci) + n) * 0.8
+    w = _cplx(rng, (ci, co, 4, 2), 0.5)
+    gy = rng.standard_normal((b, co) + n)
+
+    def loss(xx, ww):
+        return float(np.sum(gy * O.fwd(xx, ww, n, modes, precision)))
+
+    h = 1e-6
+    gx = O.bwd_data(x, w, gy, n, modes, precision)
+    gw = O.bwd_weight(x, gy, n, modes, precision)
+    err = 0.0
+    for idx in [(0, 0, 0, 0), (0, 1, 3, 5), (0, 0, 7, 2), (0, 1, 4, 4)]:
+        e = np.zeros_like(x)
+        e[idx] = h
+        fd = (loss(x + e, w) - loss(x - e, w)) / (2 * h)
+        err = max(err, abs(fd - gx[idx]) / max(1e-3, abs(gx[idx])))
+    for idx in [(0, 0, 0, 0), (1, 0, 3, 1), (0, 1, 2, 0), (1, 1, 1, 1)]:
+        for comp in (1.0, 1j):
+            e = np.zeros_like(w)
+            e[idx] = h * comp
+            fd = (loss(x, w + e) - loss(x, w - e)) / (2 * h)
+            ref = gw[idx].real if comp == 1.0 else gw[idx].imag
+            err = max(err, abs(fd - ref) / max(1e-3, abs(ref)))
+    return err
+
+
+def pin_adjoint(seed=12):
+    """<gy, fwd(dx)> = <bwd_data(gy), dx> and Re<gW, dW> = <gy, y(dW)> in the
+    linear (full-precision) mode."""
+    rng = _rng(seed)
+    n, modes = (8, 12), (3, 4)
+    b, ci, co = 2, 3, 2
+    w = _cplx(rng, (ci, co, 6, 4))
+    dx = rng.standard_normal((b, ci) + n)
+    gy = rng.standard_normal((b, co) + n)
+    lhs = np.sum(gy * O.fwd(dx, w, n, modes, F32))
+    rhs = np.sum(O.bwd_data(dx, w, gy, n, modes, F32) * dx)
+    e1 = abs(lhs - rhs) / abs(lhs)
+    x = rng.standard_normal((b, ci) + n)
+    dw = _cplx(rng, w.shape)
+    lhs2 = np.sum(gy * O.fwd(x, dw, n, modes, F32))
+    rhs2 = np.real(np.sum(np.conj(O.bwd_weight(x, gy, n, modes, F32)) * dw))
+    e2 = abs(lhs2 - rhs2) / abs(lhs2)
+    return max(e1, e2)
+
+
+def pin_identity_self_adjoint(seed=13):
+    """Identity weights: bwd_data(gy) == fwd(gy) in full precision (the
+    truncation projector is self-adjoint)."""
+    rng = _rng(seed)
+    n, modes = (8, 12), (2, 5)
+    c = 3
+    w = np.zeros((c, c, 4, 5), dtype=np.complex128)
+    for i in range(c):
+        w[i, i] = 1.0
+    gy = rng.standard_normal((2, c) + n)
+    a = O.bwd_data(gy, w, gy, n, modes, F32)
+    b = O.fwd(gy, w, n, modes, F32)
+    return np.abs(a - b).max()
+
+
+ALL_PINS = {
+    "brute2d": (pin_brute_force_2d, 1e-13),
+    "brute3d": (pin_brute_force_3d, 1e-13),
+    "rfftn": (pin_numpy_rfftn, 1e-13),
+    "parseval": (pin_parseval, 1e-12),
+    "ramp": (pin_ramp, 1e-12),
+    "shift": (pin_shift, 1e-13),
+    "round_trip": (pin_round_trip, 1e-13),
+    "single_mode": (pin_single_mode, 1e-13),
+    "irfftn": (pin_irfftn, 1e-13),
+    "fd_fp32": (lambda: pin_fd_dense(F32), 1e-7),
+    "fd_tanh": (lambda: pin_fd_dense(F16T), 1e-7),
+    "adjoint": (pin_adjoint, 1e-12),
+    "identity_adjoint": (pin_identity_self_adjoint, 1e-13),
+}
+
+
+@pytest.mark.parametrize("name", sorted(ALL_PINS))
+def test_pin(name):
+    fn, tol = ALL_PINS[name]
+    err = fn()
+    assert err <= tol, f"{name}: {err:.3e} > {tol:.1e}"
+
+
+# ---------------------------------------------------------------------------
+# Further pins
+# ---------------------------------------------------------------------------
+
+def test_mode_maps_golden():
+    with open(os.path.join(GOLDEN, "mode_maps.json")) as f:
+        g = json.load(f)
+    for ax in g["axes"]:
+        k = O.mode_freq(ax["n"], ax["m"], ax["last"])
+        if "k" in ax:
+            assert k.tolist() == ax["k"]
+        else:
+            m = ax["m"]
+            assert [int(k[0]), int(k[m - 1])] == ax["k_low"]
+            if not ax["last"]:
+                assert [int(k[m]), int(k[2 * m - 1])] == ax["k_high"]
+                assert k.tolist() == sorted(k.tolist())   # ascending FFT order
+                assert len(set(k.tolist())) == 2 * m
+    for row in g["multiplicity"]:
+        assert O.multiplicity(np.array(row["k"]), row["n"]).tolist() == row["c"]
+
+
+@pytest.mark.parametrize("n,m,last", [(8, 5, False), (8, 0, False), (8, 6, True),
+                                      (8, 0, True)])
+def test_mode_freq_rejects(n, m, last):
+    with pytest.raises(ValueError):
+        O.mode_freq(n, m, last)
+
+
+def test_ramp_closed_form_odd_and_nyquist():
+    assert pin_ramp(15, 8) < 1e-12
+    assert pin_ramp(16, 9) < 1e-12     # Nyquist bin retained
+
+
+def test_parseval_3d_and_odd():
+    assert pin_parseval((6, 8)) < 1e-12
+    rng = _rng(21)
+    n = (4, 6, 7)
+    u = rng.standard_normal(n)
+    modes = (2, 3, 4)
+    xh = O.forward_spectrum(u[None, None], n, modes)[0, 0]
+    c = O.multiplicity(O.retained(n, modes)[-1], n[-1])
+    assert abs(np.mean(u * u) - np.sum(c * np.abs(xh) ** 2)) < 1e-12
+
+
+def test_rfftn_3d():
+    assert pin_numpy_rfftn((6, 8, 10), (2, 3, 4)) < 1e-13
+    assert pin_numpy_rfftn((16,), (5,)) < 1e-13
+
+
+def test_round_trip_3d_odd():
+    assert pin_round_trip((4, 6, 8), 2) < 1e-13
+    assert pin_round_trip((6, 7), 2) < 1e-13
+
+
+def test_tanh_bounds_spectrum():
+    """|Xhat_k| <= ||tanh(x)||_inf <= 1 for any x, even near the fp16 limit."""
+    rng = _rng(22)
+    n = (16, 16)
+    x = rng.standard_normal((2, 3) + n) * 6e4
+    xh = O.forward_spectrum(O.preactivation(x, F16T), n, (8, 9))
+    assert np.abs(xh).max() <= 1.0 + 1e-15
+    assert np.isfinite(xh).all()
+
+
+@pytest.mark.parametrize("nn", [64, 256])
+def test_thm32_precision_bound(nn):
+    """Thm 3.2: quantising v and the basis values to fp16 (unit roundoff
+    eps = 2^-11) moves every retained coefficient by at most 4 eps ||v||_inf."""
+    rng = _rng(23)
+    n, modes = (nn, nn), (8, 8)
+    v = np.tanh(rng.standard_normal(n) * 2.0)
+    exact = O.forward_spectrum(v[None, None], n, modes)[0, 0]
+    qv = v.astype(np.float16).astype(np.float64)
+    ks = O.retained(n, modes)
+    eps = 2.0 ** -11
+    M = np.abs(v).max()
+    x1, x2 = np.meshgrid(np.arange(nn), np.arange(nn), indexing="ij")
+    worst = 0.0
+    for ka in ks[0][[0, 3, 9, 15]]:
+        for kb in ks[1][[0, 5, 7]]:
+            ph = 2 * np.pi * (((ka * x1) % nn) / nn + ((kb * x2) % nn) / nn)
+            qc = np.cos(ph).astype(np.float16).astype(np.float64)
+            qs = np.sin(ph).astype(np.float16).astype(np.float64)
+            quant = np.sum(qv * (qc - 1j * qs)) / (nn * nn)
+            ta = int(np.where(ks[0] == ka)[0][0])
+            tb = int(np.where(ks[1] == kb)[0][0])
+            err = abs(quant - exact[ta, tb])
+            worst = max(worst, err)
+            assert err <= 4 * eps * M
+    assert worst > 0.0
+
+
+def test_bandlimited_reproduction():
+    """A field supported on the Hermitian-closed part of the retained set is
+    reproduced exactly by identity weights; adding the unpaired k1 = -m1
+    column on the k_d = 0 plane is not."""
+    n, modes = (16, 16), (3, 4)
+    rng = _rng(24)
+    x1, x2 = np.meshgrid(np.arange(16), np.arange(16), indexing="ij")
+    u = np.zeros(n)
+    for k1 in range(-2, 3):            # |k1| <= m1 - 1 on the k_d = 0 plane
+        a = rng.standard_normal()
+        u += a * np.cos(2 * np.pi * k1 * x1 / 16 + 0.3 * k1)
+    for k1 in range(-3, 3):            # any retained k1 for k_d >= 1
+        for k2 in range(1, 4):
+            a = rng.standard_normal()
+            u += a * np.cos(2 * np.pi * (k1 * x1 + k2 * x2) / 16 + 0.1 * k2)
+    w = np.ones((1, 1, 6, 4), dtype=np.complex128)
+    y = O.fwd(u[None, None], w, n, modes, F32)[0, 0]
+    assert np.abs(y - u).max() < 1e-12
+    u2 = u + np.cos(2 * np.pi * (-3) * x1 / 16 + 0.5)
+    y2 = O.fwd(u2[None, None], w, n, modes, F32)[0, 0]
+    assert np.abs(y2 - u2).max() > 1e-3
+
+
+def test_identity_pass_through():
+    rng = _rng(25)
+    xh = _cplx(rng, (2, 3, 4, 5))
+    w = np.zeros((3, 3, 4, 5), dtype=np.complex128)
+    for i in range(3):
+        w[i, i] = 1.0
+    assert np.abs(O.contract_dense(xh, w) - xh).max() == 0.0
+
+
+def test_adjoint_3d():
+    rng = _rng(26)
+    n, modes = (4, 6, 8), (1, 2, 3)
+    w = _cplx(rng, (2, 3, 2, 4, 3))
+    dx = rng.standard_normal((1, 2) + n)
+    gy = rng.standard_normal((1, 3) + n)
+    lhs = np.sum(gy * O.fwd(dx, w, n, modes, F32))
+    rhs = np.sum(O.bwd_data(dx, w, gy, n, modes, F32) * dx)
+    assert abs(lhs - rhs) / abs(lhs) < 1e-12
+
+
+# ---------------------------------------------------------------------------
+# Tucker and the greedy path
+# ---------------------------------------------------------------------------
+
+def _tucker_case(rng, d=2):
+    n = (8, 8) if d == 2 else (4, 4, 6)
+    modes = (2, 3) if d == 2 else (1, 2, 2)
+    kd = tuple(2 * m for m in modes[:-1]) + (modes[-1],)
+    ci, co = 3, 4
+    rank = (2, 3) + tuple([2] * d)
+    core = _cplx(rng, rank, 0.5)
+    u_in = _cplx(rng, (ci, rank[0]), 0.5)
+    u_out = _cplx(rng, (co, rank[1]), 0.5)
+    u_mode = [_cplx(rng, (kd[j], rank[2 + j]), 0.5) for j in range(d)]
+    return n, modes, kd, ci, co, rank, core, u_in, u_out, u_mode
+
+
+@pytest.mark.parametrize("d", [2, 3])
+def test_tucker_all_orders_agree(d):
+    """Dense reconstruction, both greedy policies and random pairwise orders
+    all give the same spectrum product."""
+    rng = _rng(30 + d)
+    n, modes, kd, ci, co, rank, core, u_in, u_out, u_mode = _tucker_case(rng, d)
+    xh = _cplx(rng, (2, ci) + kd)
+    dense = O.contract_dense(xh, O.tucker_dense(core, u_in, u_out, u_mode))
+    scale = np.abs(dense).max()
+    for pol in (O.POLICY_MIN_RESULT, O.POLICY_MIN_NET):
+        got = O.tucker_contract(xh, core, u_in, u_out, u_mode, n, modes, pol)
+        assert np.abs(got - dense).max() <= 1e-12 * scale
+    ops, out = O.tucker_labels(d)
+    for trial in range(6):
+        # random order: repeatedly pick a random pair; result keeps needed indices
+        cur = list(ops)
+        steps = []
+        while len(cur) > 2:
+            p, q = sorted(rng.choice(len(cur), 2, replace=False).tolist())
+            res = O.pair_result(cur, p, q, out)
+            steps.append((p, q, res))
+            cur = [o for r, o in enumerate(cur) if r not in (p, q)] + [res]
+        steps.append((0, 1, out))
+        got = O.tucker_contract(xh, core, u_in, u_out, u_mode, n, modes, steps=steps)
+        assert np.abs(got - dense).max() <= 1e-12 * scale
+
+
+def test_tucker_dense_mode_products():
+    """The dense reconstruction equals explicit sums over the core."""
+    rng = _rng(33)
+    n, modes, kd, ci, co, rank, core, u_in, u_out, u_mode = _tucker_case(rng, 2)
+    w = O.tucker_dense(core, u_in, u_out, u_mode)
+    i, o, t1, t2 = 2, 1, 3, 2
+    s = 0j
+    for a, e, c, dd in itertools.product(*[range(r) for r in rank]):
+        s += core[a, e, c, dd] * u_in[i, a] * u_out[o, e] * u_mode[0][t1, c] * u_mode[1][t2, dd]
+    assert abs(w[i, o, t1, t2] - s) < 1e-13
+
+
+@pytest.mark.parametrize("policy", ["min_result", "min_net"])
+def test_greedy_paths_golden(policy):
+    with open(os.path.join(GOLDEN, "tucker_paths.json")) as f:
+        g = json.load(f)
+    steps = O.greedy_path(g["operands"], g["sizes"], g["output"], policy)
+    exp = g[policy]["steps"]
+    assert len(steps) == len(exp)
+    for (p, q, res), (ep, eq, eres, esize) in zip(steps, exp):
+        assert (p, q) == (ep, eq)
+        assert sorted(res) == sorted(eres)
+        assert O._size(res, g["sizes"]) == esize
+    assert steps[-1][2] == g["output"]
+    assert O.path_macs(g["operands"], g["sizes"], steps) == g[policy]["macs"]
+    peak = max(O._size(r, g["sizes"]) for _, _, r in steps)
+    assert peak == g[policy]["peak"]
+
+
+def test_greedy_adjoint_mirror():
+    """The adjoint einsum swaps i and o; with Cin == Cout and equal ranks its
+    greedy path mirrors the forward one."""
+    ops_f, out_f = O.tucker_labels(2)
+    ops_a, out_a = O.tucker_labels(2, adjoint=True)
+    sz = O.tucker_sizes(16, 128, 128, (64, 32), (13, 13, 6, 3))
+    for pol in ("min_result", "min_net"):
+        a = O.greedy_path(ops_a, sz, out_a, pol)
+        assert len(a) == 5 and a[-1][2] == out_a
+
+
+@pytest.mark.parametrize("precision", [F32, F16T])
+def test_tucker_gradients_fd(precision):
+    """Central finite differences for the core and every factor."""
+    rng = _rng(40)
+    n, modes, kd, ci, co, rank, core, u_in, u_out, u_mode = _tucker_case(rng, 2)
+    x = rng.standard_normal((1, ci) + n) * 0.7
+    gy = rng.standard_normal((1, co) + n)
+
+    def loss(cr, ui, uo, um):
+        return float(np.sum(gy * O.tucker_fwd(x, cr, ui, uo, um, n, modes, precision)))
+
+    g_core, g_in, g_out, g_mode = O.tucker_bwd_weight(x, gy, core, u_in, u_out, u_mode,
+                                                      n, modes, precision)
+    h = 1e-6
+    params = [("core", core, g_core), ("in", u_in, g_in), ("out", u_out, g_out),
+              ("m0", u_mode[0], g_mode[0]), ("m1", u_mode[1], g_mode[1])]
+    for name, arr, grad in params:
+        flat_idx = [0, arr.size - 1, arr.size // 2]
+        for fi in flat_idx:
+            idx = np.unravel_index(fi, arr.shape)
+            for comp in (1.0, 1j):
+                def bump(sgn):
+                    a2 = arr.copy()
+                    a2[idx] += sgn * h * comp
+                    args = {"core": core, "in": u_in, "out": u_out,
+                            "m0": u_mode[0], "m1": u_mode[1]}
+                    args[name] = a2
+                    return loss(args["core"], args["in"], args["out"],
+                                [args["m0"], args["m1"]])
+                fd = (bump(1) - bump(-1)) / (2 * h)
+                ref = grad[idx].real if comp == 1.0 else grad[idx].imag
+                assert abs(fd - ref) <= 1e-7 * max(1.0, abs(ref)), (name, idx, comp)
+
+
+def test_tucker_bwd_data_matches_dense():
+    rng = _rng(41)
+    n, modes, kd, ci, co, rank, core, u_in, u_out, u_mode = _tucker_case(rng, 2)
+    x = rng.standard_normal((2, ci) + n)
+    gy = rng.standard_normal((2, co) + n)
+    w = O.tucker_dense(core, u_in, u_out, u_mode)
+    for pol in ("min_result", "min_net"):
+        a = O.tucker_bwd_data(x, core, u_in, u_out, u_mode, gy, n, modes, F16T, pol)
+        b = O.bwd_data(x, w, gy, n, modes, F16T)
+        assert np.abs(a - b).max() <= 1e-12 * np.abs(b).max()
+
+
+# ---------------------------------------------------------------------------
+# Failure mode the tanh stabiliser addresses (Sec. 4.3), emulated on the CPU
+# ---------------------------------------------------------------------------
+
+def test_fp16_overflow_without_tanh():
+    """An unnormalised DC coefficient accumulated in fp16 with a pairwise
+    (butterfly-like) sum overflows on a 1024^2 grid for a field of mean ~1,
+    whereas the 1/N-normalised spectrum of tanh(x) is bounded by 1."""
+    rng = _rng(50)
+    a = (1.0 + rng.standard_normal(1024 * 1024) * 0.5).astype(np.float16)
+    with np.errstate(over="ignore", invalid="ignore"):
+        while a.size > 1:
+            a = (a[0::2] + a[1::2]).astype(np.float16)
+    assert not np.isfinite(a[0])
+    n = (32, 32)
+    x = (1.0 + rng.standard_normal((1, 1) + n) * 0.5) * 1e4
+    xh = O.forward_spectrum(O.preactivation(x, F16T), n, (4, 4))
+    assert np.abs(xh).max() <= 1.0
+
+
+# ---------------------------------------------------------------------------
+# Planted mistakes: each must make at least one pin fail
+# ---------------------------------------------------------------------------
+
+def _pins_fail():
+    failing = []
+    for name, (fn, tol) in ALL_PINS.items():
+        try:
+            err = fn()
+        except Exception:
+            failing.append(name)
+            continue
+        if not (err <= tol):
+            failing.append(name)
+    return failing
+
+
+MUTATIONS = {
+    "no_multiplicity": ("multiplicity", lambda orig: (lambda k, n: np.ones(np.shape(k)))),
+    "c_everywhere_2": ("multiplicity", lambda orig: (lambda k, n: 2.0 * np.ones(np.shape(k)))),
+    "wrong_sign": ("dft_matrix", lambda orig: (lambda n, ks, s: orig(n, ks, -s))),
+    "high_block_off_by_one": ("mode_freq", lambda orig: (
+        lambda n, m, last: orig(n, m, last) if last else
+        np.where(np.arange(2 * m) < m, np.arange(2 * m), n - 2 * m + np.arange(2 * m) - 1))),
+    "transposed_weight": ("contract_dense", lambda orig: (
+        lambda xh, w: np.einsum("bi...,oi...->bo...", xh, w))),
+    "conj_weight": ("contract_dense", lambda orig: (lambda xh, w: orig(xh, np.conj(w)))),
+    "no_normalisation": ("forward_spectrum", lambda orig: (
+        lambda u, n, m: orig(u, n, m) * float(np.prod(n)))),
+    "drop_imag_in_inverse": ("inverse_spectrum", lambda orig: (
+        lambda z, n, m, with_c=True: orig(np.real(z) + 0j, n, m, with_c))),
+    "tanh_prime_wrong": ("bwd_data", lambda orig: (
+        lambda x, w, gy, n, m, p: orig(x, w, gy, n, m, O.PREC_FP32))),
+    "grad_no_c": ("grad_spectrum", lambda orig: (
+        lambda gy, n, m: O.forward_spectrum(gy, n, m) * float(np.prod(n)))),
+    "wgrad_no_conj": ("bwd_weight", lambda orig: (
+        lambda x, gy, n, m, p: np.einsum(
+            "bi...,bo...->io...",
+            O.forward_spectrum(O.preactivation(x, p), n, m),
+            O.grad_spectrum(gy, n, m)))),
+}
+
+
+@pytest.mark.parametrize("mut", sorted(MUTATIONS))
+def test_planted_mistake_is_caught(mut, monkeypatch):
+    attr, make = MUTATIONS[mut]
+    orig = getattr(O, attr)
+    monkeypatch.setattr(O, attr, make(orig))
+    failing = _pins_fail()
+    assert failing, f"mutation {mut} passed every pin"
