@@ -1,0 +1,244 @@
+"""Benchmark of the FNO spectral-convolution layer (fwd + bwd_data + bwd_weight).
+
+One step = one pass of the whole layer over one batch: forward (writing the
+input-spectrum cache), data gradient (writing the gradient-spectrum cache)
+and weight gradient (reading both caches).  Inputs are seeded synthetic
+Gaussian random fields resident in HBM before the timed region.
+
+Prints one JSON line with the throughput (samples/s), the roofline figure of
+the dominant kernel (HIP events on the launch stream through the library's
+event profiler) and the CPU oracle timed on a bounded sample.
+
+    python bench.py [--steps K] [--warmup W] [--workload 2] [--no-cpu-baseline]
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "spectral-conv fwd+bwd samples/s (fp16+tanh) + achieved HBM GB/s fraction"
+HBM_PEAK_GBS = 8000.0
+
+
+def parse():
+    p = argparse.ArgumentParser()
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=50)
+    p.add_argument("--warmup", type=int, default=10)
+    p.add_argument("--workload", type=int, default=2)
+    p.add_argument("--precision", choices=["fp16_tanh", "fp32"], default="fp16_tanh")
+    p.add_argument("--policy", choices=["min_result", "min_net"], default="min_result")
+    p.add_argument("--no-caches", action="store_true",
+                   help="bwd_weight recomputes both spectra from x and gy")
+    p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--cpu-seconds", type=float, default=12.0)
+    p.add_argument("--profile-steps", type=int, default=20)
+    return p.parse_args()
+
+
+def kernel_bytes(wl, es):
+    """Algorithmic HBM bytes of one launch of each kernel (reads + writes of
+    the tensors it must touch once)."""
+    B, Ci, Co = wl.batch, wl.c_in, wl.c_out
+    N = int(np.prod(wl.n))
+    K = int(np.prod(wl.kdims))
+    spec_in = B * Ci * K * 2 * es
+    spec_out = B * Co * K * 2 * es
+    W = Ci * Co * K * 2 * es
+    out = {
+        "r2c_plane": None,  # depends on the channel count; resolved per launch below
+        "contract": spec_in + W + spec_out,
+        "contract_adjoint": spec_out + W + spec_in,
+        "c2r_plane": spec_out + B * Co * N * es,
+        "c2r_plane_tanh_grad": spec_in + 2 * B * Ci * N * es,
+        "wgrad": spec_in + spec_out + Ci * Co * K * 2 * 4,
+    }
+    # r2c runs once on x (Cin channels) and once on gy (Cout channels)
+    out["r2c_plane"] = ((B * Ci * N * es + spec_in) + (B * Co * N * es + spec_out)) / 2
+    return out
+
+
+def step_bytes(wl, es, caches=True):
+    """Whole-step algorithmic bytes: 5 spatial passes, W twice, gW (fp32),
+    and the two spectral caches written once and read once."""
+    B, Ci, Co = wl.batch, wl.c_in, wl.c_out
+    N = int(np.prod(wl.n))
+    K = int(np.prod(wl.kdims))
+    S_in, S_out = B * Ci * N * es, B * Co * N * es
+    spec = (B * Ci * K + B * Co * K) * 2 * es
+    if wl.weight == "tucker":
+        r = wl.rank
+        nparam = (np.prod(r) + Ci * r[0] + Co * r[1]
+                  + sum(k * rr for k, rr in zip(wl.kdims, r[2:])))
+        W, gW = 2 * nparam * es, 2 * nparam * 4
+    else:
+        W, gW = Ci * Co * K * 2 * es, Ci * Co * K * 2 * 4
+    total = S_in + S_out + (S_out + S_in + S_in) + 2 * W + gW
+    total += 2 * spec if caches else (S_in + S_out)
+    return int(total)
+
+
+def cpu_baseline(wl, x, w, gy, prec, seconds):
+    """The float64 oracle, as it stands, on a bounded sample of the workload:
+    whole batch samples (fwd + bwd_data + bwd_weight), repeated until about
+    `seconds` of CPU time."""
+    from oracle import fno_oracle as O
+    import synth
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
+    except Exception:  # pragma: no cover
+        threads = len(os.sched_getaffinity(0))
+    oprec = O.PREC_FP16_TANH if prec == "fp16_tanh" else O.PREC_FP32
+    done = 0
+    t0 = time.perf_counter()
+    while True:
+        b = done % wl.batch
+        xb, gb = x[b:b + 1], gy[b:b + 1]
+        if wl.weight == "tucker":
+            core = synth.pairs_to_complex(w["core"])
+            u_in = synth.pairs_to_complex(w["u_in"])
+            u_out = synth.pairs_to_complex(w["u_out"])
+            um = [synth.pairs_to_complex(u) for u in w["u_mode"]]
+            O.tucker_fwd(xb, core, u_in, u_out, um, wl.n, wl.modes, oprec)
+            O.tucker_bwd_data(xb, core, u_in, u_out, um, gb, wl.n, wl.modes, oprec)
+            O.tucker_bwd_weight(xb, gb, core, u_in, u_out, um, wl.n, wl.modes, oprec)
+        else:
+            wc = synth.pairs_to_complex(w)
+            O.fwd(xb, wc, wl.n, wl.modes, oprec)
+            O.bwd_data(xb, wc, gb, wl.n, wl.modes, oprec)
+            O.bwd_weight(xb, gb, wl.n, wl.modes, oprec)
+        done += 1
+        el = time.perf_counter() - t0
+        if el >= seconds:
+            break
+    return {"value": done / el, "unit": "samples/s", "cores": int(threads),
+            "kind": "oracle",
+            "sample": f"{done} batch samples of the workload (B=1 slices), float64 oracle "
+                      f"fwd+bwd_data+bwd_weight, {el:.1f} s"}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(json.dumps({"error": "this layer runs on one GPU; multi-GPU runs are not "
+                                   "part of this build (see the sharding design)",
+                          "n_gpus": args.gpus}))
+        sys.exit(2)
+    import torch
+    import synth
+    from paper_2307_15034_amd import binding as B
+    from paper_2307_15034_amd.layer import SpectralConv
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    wl = synth.WORKLOADS[args.workload]
+    npdt = np.float16 if args.precision == "fp16_tanh" else np.float32
+    es = 2 if args.precision == "fp16_tanh" else 4
+    pc = B.FNO_PREC_FP16_TANH if args.precision == "fp16_tanh" else B.FNO_PREC_FP32
+    kind = B.FNO_WEIGHT_TUCKER if wl.weight == "tucker" else B.FNO_WEIGHT_DENSE
+    pol = B.FNO_PATH_MIN_RESULT if args.policy == "min_result" else B.FNO_PATH_MIN_NET
+    x = synth.make_x(wl, npdt)
+    gy = synth.make_gy(wl, npdt)
+    w = synth.make_tucker_weight(wl, npdt) if wl.weight == "tucker" else \
+        synth.make_dense_weight(wl, npdt)
+    layer = SpectralConv(wl.n, wl.modes, wl.batch, wl.c_in, wl.c_out, pc, kind, wl.rank, pol)
+    dev = lambda a: torch.from_numpy(np.ascontiguousarray(a)).cuda()  # noqa: E731
+    xd, gyd = dev(x), dev(gy)
+    wd = ({"core": dev(w["core"]), "u_in": dev(w["u_in"]), "u_out": dev(w["u_out"]),
+           "u_mode": [dev(u) for u in w["u_mode"]]} if isinstance(w, dict) else dev(w))
+    caches = not args.no_caches
+    xh = layer.spectrum_buffer(0) if caches else None
+    gh = layer.spectrum_buffer(1) if caches else None
+    y = torch.empty((wl.batch, wl.c_out) + wl.n, dtype=layer.dtype, device="cuda")
+    gx = torch.empty((wl.batch, wl.c_in) + wl.n, dtype=layer.dtype, device="cuda")
+    gw = layer.alloc_grads()
+    stream = torch.cuda.current_stream()
+    sh = stream.cuda_stream
+    for op in (B.FNO_OP_FWD, B.FNO_OP_BWD_DATA):
+        layer.workspace(op)
+    layer.workspace(B.FNO_OP_BWD_WEIGHT, caches)
+
+    def step():
+        layer.fwd(xd, wd, y=y, x_hat=xh, stream=sh)
+        layer.bwd_data(xd, wd, gyd, gx=gx, gy_hat=gh, stream=sh)
+        if caches:
+            layer.bwd_weight(None, None, wd, x_hat=xh, gy_hat=gh, gw=gw, stream=sh)
+        else:
+            layer.bwd_weight(xd, gyd, wd, gw=gw, stream=sh)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0 = time.perf_counter()
+    ev0.record(stream)
+    for _ in range(args.steps):
+        step()
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms_step = ev0.elapsed_time(ev1) / args.steps
+    value = wl.batch / (ms_step / 1e3)
+    sbytes = step_bytes(wl, es, caches)
+
+    # per-kernel durations: the library brackets each launch with HIP events
+    B.fno_profile_reset()
+    B.fno_profile_enable(True)
+    for _ in range(args.profile_steps):
+        step()
+    torch.cuda.synchronize()
+    prof = B.fno_profile_read()
+    B.fno_profile_enable(False)
+    B.fno_profile_reset()
+    kb = kernel_bytes(wl, es)
+    kernels = {}
+    for name, (n, tot) in prof.items():
+        avg = tot / max(n, 1)
+        per_step = tot / args.profile_steps
+        e = {"launches_per_step": n / args.profile_steps, "avg_ms": avg,
+             "ms_per_step": per_step}
+        if kb.get(name):
+            e["alg_bytes"] = int(kb[name])
+            e["gbs"] = kb[name] / (avg / 1e3) / 1e9
+        kernels[name] = e
+    dom = max(kernels, key=lambda k: kernels[k]["ms_per_step"])
+    dk = kernels[dom]
+    roof = {"bound": "hbm", "kernel": dom, "achieved": round(dk.get("gbs", 0.0), 1),
+            "peak": HBM_PEAK_GBS, "unit": "GB/s",
+            "frac": round(dk.get("gbs", 0.0) / HBM_PEAK_GBS, 4), "traffic": None,
+            "avg_ms": round(dk["avg_ms"], 5), "alg_bytes": dk.get("alg_bytes")}
+
+    out = {
+        "metric": METRIC, "value": round(value, 1), "unit": "samples/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_step, 5),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "f16" if args.precision == "fp16_tanh" else "f32",
+        "data": "synthetic (seeded Gaussian random fields standing in for the paper's PDE "
+                "datasets; random-init weights)",
+        "config": {"workload": wl.name, "batch": wl.batch, "c_in": wl.c_in, "c_out": wl.c_out,
+                   "grid": list(wl.n), "modes": list(wl.modes), "weights": wl.weight,
+                   "precision": args.precision, "spectral_caches": caches,
+                   "path_policy": args.policy if wl.weight == "tucker" else None},
+        "step_alg_bytes": sbytes,
+        "step_hbm_gbs": round(sbytes / (ms_step / 1e3) / 1e9, 1),
+        "step_hbm_frac": round(sbytes / (ms_step / 1e3) / 1e9 / HBM_PEAK_GBS, 4),
+        "roofline": roof,
+        "kernels": {k: {kk: (round(vv, 5) if isinstance(vv, float) else vv)
+                        for kk, vv in v.items()} for k, v in kernels.items()},
+        "wall_s_timed": round(wall, 3),
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(wl, x, w, gy, args.precision, args.cpu_seconds)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,208 @@
+/*
+ * fno_spectral_conv.h — C ABI of the half-precision FNO spectral-convolution
+ * layer for AMD Instinct MI355X (gfx950).
+ *
+ * The layer is the Fourier convolution operator of Tu et al., "Guaranteed
+ * Approximation Bounds for Mixed-Precision Neural Operators" (ICLR 2024),
+ * Sec. 2 ("FNO and extensions"):
+ *
+ *     (K v)(x) = F^-1( R . T_K( F tanh(v) ) )(x)
+ *
+ * with the tanh pre-activation of Sec. 4.3 in half-precision mode, the
+ * forward transform normalised as the Riemann sum of Sec. 3 (1/N), the
+ * truncation T_K keeping the m_j lowest non-negative and m_j highest negative
+ * frequencies on every axis but the last and k = 0..m_d-1 on the last
+ * (real-FFT) axis, a complex per-mode channel mixing R (dense, or Tucker
+ * factorised as in the tensorised FNO of Sec. 2, contracted pairwise in the
+ * greedy order of Sec. 4.2), and the inverse
+ *
+ *     y[x] = sum_t c(k_d(t)) Re( Yhat[t] exp(+2 pi i <k(t), x / N>) ),
+ *
+ * c = 1 on the k_d = 0 and Nyquist planes and 2 elsewhere.  Gradients follow
+ * the real-gradient convention g = dL/dRe + i dL/dIm.
+ *
+ * Conventions for every entry point
+ *   - Tensors are device pointers to contiguous row-major arrays, last axis
+ *     fastest.  Complex values are interleaved (re, im) pairs of the element
+ *     type.  Every device pointer must be 16-byte aligned.
+ *   - Element type: FNO_PREC_FP16_TANH stores x, y, gy, gx and the weights as
+ *     IEEE fp16 (round-to-nearest-even stores, fp32 accumulation inside the
+ *     kernels); FNO_PREC_FP32 stores them as fp32.  Weight gradients are always
+ *     fp32 complex.
+ *   - The caller owns all device memory, including the workspace.  The library
+ *     owns only per-descriptor plan tables (twiddles, index maps, the Tucker
+ *     path); they are built, with a blocking upload, on the first call for a
+ *     descriptor on a device and kept until fno_release_caches() or unload.
+ *     Later calls allocate nothing.  Issue one warm-up call before capturing
+ *     calls into a HIP graph.
+ *   - All argument checks run on the host before anything is enqueued; a
+ *     rejected call enqueues nothing.  Calls are asynchronous on `stream`.
+ *   - The plan cache is mutex-guarded; concurrent calls on different streams
+ *     are safe as long as their workspaces and outputs do not overlap.
+ */
+#ifndef FNO_SPECTRAL_CONV_H_
+#define FNO_SPECTRAL_CONV_H_
+
+#include <stddef.h>
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  FNO_OK = 0,
+  FNO_ERR_INVALID_ARGUMENT = 1,   /* null/misaligned pointer, bad size or mode count */
+  FNO_ERR_UNSUPPORTED = 2,        /* valid request outside what the kernels handle */
+  FNO_ERR_WORKSPACE_TOO_SMALL = 3,
+  FNO_ERR_HIP = 4,                /* a HIP runtime call or launch failed          */
+  FNO_ERR_INTERNAL = 5
+} fno_status;
+
+typedef enum {
+  FNO_PREC_FP32 = 0,        /* fp32 storage and math, no pre-activation        */
+  FNO_PREC_FP16_TANH = 1    /* fp16 storage, fp32 accumulation, tanh (Sec. 4.3) */
+} fno_precision;
+
+typedef enum { FNO_WEIGHT_DENSE = 0, FNO_WEIGHT_TUCKER = 1 } fno_weight_kind;
+
+/* Greedy rule for the Tucker contraction order (Sec. 4.2).  MIN_RESULT takes
+ * the pair whose intermediate has the fewest elements; MIN_NET the pair that
+ * minimises (result - both inputs).  Ties go to the lexicographically smallest
+ * pair of the current operand list. */
+typedef enum { FNO_PATH_MIN_RESULT = 0, FNO_PATH_MIN_NET = 1 } fno_path_policy;
+
+typedef enum { FNO_OP_FWD = 0, FNO_OP_BWD_DATA = 1, FNO_OP_BWD_WEIGHT = 2 } fno_op;
+
+/* Layer descriptor.  Spatial extents n[0..ndim-1] (N_1..N_d), retained mode
+ * counts modes[0..ndim-1]: axes j < d keep K_j = 2 m_j slots (2 m_j <= N_j),
+ * the last axis keeps K_d = m_d slots (1 <= m_d <= N_d/2 + 1).  Retained slot
+ * t on a leading axis is FFT index k = t for t < m, k = N - 2m + t otherwise.
+ * rank = (r_in, r_out, r_1..r_d) for Tucker weights, ignored for dense. */
+typedef struct {
+  int32_t ndim;          /* 1, 2 or 3                      */
+  int32_t precision;     /* fno_precision                  */
+  int32_t weight_kind;   /* fno_weight_kind                */
+  int32_t path_policy;   /* fno_path_policy (Tucker only)  */
+  int64_t batch;
+  int64_t c_in;
+  int64_t c_out;
+  int64_t n[3];
+  int64_t modes[3];
+  int64_t rank[5];
+} fno_conv_desc;
+
+/* Spectral weights R (device pointers, element type of the precision mode).
+ *   dense  : [c_in, c_out, K_1..K_d] complex
+ *   core   : [r_in, r_out, r_1..r_d] complex
+ *   u_in   : [c_in, r_in] complex,  u_out: [c_out, r_out] complex
+ *   u_mode : u_mode[j] is [K_j, r_j] complex
+ * W[i,o,t] = sum core[a,e,c..] u_in[i,a] u_out[o,e] prod_j u_mode[j][t_j,c_j]. */
+typedef struct {
+  const void *dense;
+  const void *core;
+  const void *u_in;
+  const void *u_out;
+  const void *u_mode[3];
+} fno_weights;
+
+/* Weight gradients, same shapes as fno_weights, always fp32 complex.  Dense
+ * uses `dense`; Tucker uses core, u_in, u_out and u_mode[0..d-1]. */
+typedef struct {
+  void *dense;
+  void *core;
+  void *u_in;
+  void *u_out;
+  void *u_mode[3];
+} fno_weight_grads;
+
+/* Bytes of workspace `op` needs for this descriptor (>= 256, multiple of 256).
+ * The size for FNO_OP_BWD_WEIGHT assumes both spectral caches are supplied;
+ * fno_spectral_conv_workspace_size_nocache gives the size when they are not. */
+fno_status fno_spectral_conv_workspace_size(const fno_conv_desc *desc, fno_op op,
+                                            size_t *bytes);
+fno_status fno_spectral_conv_workspace_size_nocache(const fno_conv_desc *desc,
+                                                    fno_op op, size_t *bytes);
+
+/* Bytes of one spectral cache: the truncated spectrum [batch, channels, K...]
+ * of the precision's element type.  `which` is 0 for the input spectrum
+ * Xhat = (1/N) sum_x tanh(x) e^{-i theta} (c_in channels) and 1 for the
+ * gradient spectrum (1/sqrt(N)) sum_x gy e^{-i theta} (c_out channels).  The
+ * contents are produced and consumed by this library only. */
+fno_status fno_spectrum_bytes(const fno_conv_desc *desc, int which, size_t *bytes);
+
+/* Forward: y[batch, c_out, N...] = K x  (x: [batch, c_in, N...]).
+ * x_hat_out: optional (NULL to skip) spectral cache for bwd_weight, written
+ * with the input spectrum.  Errors: FNO_ERR_INVALID_ARGUMENT (bad descriptor,
+ * null or misaligned pointers), FNO_ERR_UNSUPPORTED, FNO_ERR_WORKSPACE_TOO_SMALL,
+ * FNO_ERR_HIP. */
+fno_status fno_spectral_conv_fwd(const fno_conv_desc *desc, const void *x,
+                                 const fno_weights *w, void *y, void *x_hat_out,
+                                 void *workspace, size_t workspace_bytes,
+                                 hipStream_t stream);
+
+/* Data gradient: gx[batch, c_in, N...] from gy[batch, c_out, N...]:
+ * G = c(k) sum_x gy e^{-i theta}, gXhat = sum_o G conj(W),
+ * gx = (1/N) sum_t Re(gXhat e^{+i theta}) * (1 - tanh(x)^2) (tanh mode; x is
+ * read only then and may be NULL in FNO_PREC_FP32).
+ * gy_hat_out: optional spectral cache (gradient spectrum) for bwd_weight. */
+fno_status fno_spectral_conv_bwd_data(const fno_conv_desc *desc, const void *x,
+                                      const fno_weights *w, const void *gy, void *gx,
+                                      void *gy_hat_out, void *workspace,
+                                      size_t workspace_bytes, hipStream_t stream);
+
+/* Weight gradient: dense gW[i,o,t] = sum_b conj(Xhat[b,i,t]) G[b,o,t]; Tucker:
+ * the chain rule through the multilinear map onto core and factors.  Outputs
+ * are overwritten (fp32 complex).  x_hat / gy_hat: spectral caches from fwd /
+ * bwd_data of the same descriptor and inputs, or NULL to recompute them from
+ * x / gy (which may then not be NULL).  The batch reduction has a fixed order:
+ * results are bitwise reproducible. */
+fno_status fno_spectral_conv_bwd_weight(const fno_conv_desc *desc, const void *x,
+                                        const void *gy, const fno_weights *w,
+                                        const void *x_hat, const void *gy_hat,
+                                        fno_weight_grads *gw, void *workspace,
+                                        size_t workspace_bytes, hipStream_t stream);
+
+/* Host-only: FFT index k of retained slot t on `axis` (0-based) — the
+ * truncation map of Sec. 2 as described above. */
+fno_status fno_mode_frequency(const fno_conv_desc *desc, int32_t axis, int64_t t,
+                              int64_t *k);
+
+/* Host-only: the pairwise Tucker contraction order for FNO_OP_FWD or
+ * FNO_OP_BWD_DATA (the greedy rule of Sec. 4.2 under desc->path_policy).
+ * Writes 3 int32 per step: p, q (positions in the current operand list,
+ * p < q; the two leave the list and the result is appended) and the bit mask
+ * of the result's indices: bit 0 batch, 1 c_in, 2 c_out, 3 r_in, 4 r_out,
+ * 5+j spatial axis j, 8+j rank of axis j.  The initial list is
+ * [spectrum, core, u_in, u_out, u_1..u_d].  `cap` is the capacity in steps. */
+fno_status fno_contraction_path(const fno_conv_desc *desc, fno_op op, int32_t *steps,
+                                int32_t cap, int32_t *n_steps);
+
+/* Host-only: total complex multiply-adds of that path and its largest
+ * intermediate (elements). */
+fno_status fno_contraction_path_cost(const fno_conv_desc *desc, fno_op op,
+                                     int64_t *macs, int64_t *peak_elems);
+
+/* Per-kernel timing with HIP events (a profiling aid, off by default).
+ * While enabled, every kernel the library launches is bracketed by a pair of
+ * HIP events recorded on the launch stream (events are created per launch, so
+ * this mode allocates and is not for graph capture).  fno_profile_read
+ * synchronises the pending events and returns, for the index-th kernel name
+ * seen (0-based, in order of first launch), its name, launch count and total
+ * elapsed milliseconds; FNO_ERR_INVALID_ARGUMENT past the last name. */
+fno_status fno_profile_enable(int32_t enable);
+fno_status fno_profile_reset(void);
+fno_status fno_profile_read(int32_t index, char *name, int32_t name_cap, int64_t *launches,
+                            double *total_ms);
+
+/* Frees every cached plan (device tables) of this process. */
+fno_status fno_release_caches(void);
+
+const char *fno_status_string(fno_status status);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* FNO_SPECTRAL_CONV_H_ */

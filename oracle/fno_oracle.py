@@ -378,15 +378,17 @@ def tucker_bwd_weight(x, gy, core, u_in, u_out, u_mode, n, modes, precision):
     ccore = np.conj(core)
     gw_l = "io" + sp
     mode_terms = ",".join(sp[j] + rk[j] for j in range(d))
-    g_core = np.einsum(f"{gw_l},ia,oe,{mode_terms}->ae{rk}", gw, cu_in, cu_out, *cmode)
-    g_in = np.einsum(f"{gw_l},ae{rk},oe,{mode_terms}->ia", gw, ccore, cu_out, *cmode)
-    g_out = np.einsum(f"{gw_l},ae{rk},ia,{mode_terms}->oe", gw, ccore, cu_in, *cmode)
+    opt = dict(optimize=True)   # evaluation order only; the sum is the same
+    g_core = np.einsum(f"{gw_l},ia,oe,{mode_terms}->ae{rk}", gw, cu_in, cu_out, *cmode, **opt)
+    g_in = np.einsum(f"{gw_l},ae{rk},oe,{mode_terms}->ia", gw, ccore, cu_out, *cmode, **opt)
+    g_out = np.einsum(f"{gw_l},ae{rk},ia,{mode_terms}->oe", gw, ccore, cu_in, *cmode, **opt)
     g_mode = []
     for j in range(d):
         others = [sp[q] + rk[q] for q in range(d) if q != j]
         arrs = [cmode[q] for q in range(d) if q != j]
         spec = ",".join([gw_l, "ae" + rk, "ia", "oe"] + others)
-        g_mode.append(np.einsum(f"{spec}->{sp[j]}{rk[j]}", gw, ccore, cu_in, cu_out, *arrs))
+        g_mode.append(np.einsum(f"{spec}->{sp[j]}{rk[j]}", gw, ccore, cu_in, cu_out, *arrs,
+                                **opt))
     return g_core, g_in, g_out, g_mode
 
 

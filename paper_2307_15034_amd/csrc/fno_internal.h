@@ -1,0 +1,132 @@
+// Internal interfaces between the host planner (fno_plan.cpp) and the HIP
+// kernels (fno_kernels.hip).  Not part of the public C ABI.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace fno {
+
+enum Elem { ELEM_F32 = 0, ELEM_F16 = 1 };
+
+// Truncated real-to-complex transform of the last two axes of every plane
+// [planes][Na][Nb] -> spectrum [planes][Ka][Kb] (complex).  Step A runs the
+// last axis (Nb reals -> Kb complex, scaled by sA), step B the other axis
+// (Na -> Ka complex, scaled by sB), both as DFT-by-MFMA with twiddle tables.
+struct R2CArgs {
+  const void* in;
+  void* out;
+  const void* twA;  // [2*Kbp][Nbp]: rows t < Kbp: cos(2 pi t n / Nb), rows Kbp+t: -sin
+  const void* cB;   // [Kap16][Nap]: cos(2 pi k_a(t) n / Na)
+  const void* sB;   // [Kap16][Nap]: sin(2 pi k_a(t) n / Na)
+  int64_t planes;
+  int Na, Nb, Ka, Kb;
+  int Kbp;          // Kb padded: 16 * NCT / 2
+  int Nbp;          // Nb padded to 32
+  int Nap;          // Na padded to a multiple of R
+  int Kap16;        // Ka padded to 16
+  int R;            // rows per chunk (multiple of 32)
+  float scaleA, scaleB;
+  int do_tanh;
+  int vec;          // 1 if Nb allows 16-byte row loads
+};
+
+// Inverse of the above: spectrum [planes][Ka][Kb] -> y [planes][Na][Nb],
+// y = scale * sum_t Re(Z e^{+i theta}) (no multiplicity), optional epilogue
+// y *= 1 - tanh(x)^2.
+struct C2RArgs {
+  const void* in;
+  void* out;
+  const void* x;    // epilogue input or null
+  const void* cI;   // [Nap][Kap]: cos(2 pi k_a(t) n / Na)   (row n, col t)
+  const void* sI;   // [Nap][Kap]: sin(2 pi k_a(t) n / Na)
+  const void* twI;  // [Nbp16][2*Kbp]: cols t < Kbp: cos(2 pi t n / Nb), Kbp+t: -sin
+  int64_t planes;
+  int Na, Nb, Ka, Kb;
+  int Kbp, Kap;     // Kap = Ka padded to 32
+  int Nap;          // Na padded to a multiple of R
+  int R;            // rows per chunk (multiple of 64)
+  float scale;
+  int epilogue;     // 0: none, 1: multiply by 1 - tanh(x)^2
+  int vec;
+};
+
+// Complex DFT along a middle axis: in [outer][Lin][inner] -> out
+// [outer][Lout][inner], out[o][t][j] = scale * sum_l E[t][l] in[o][l][j].
+struct AxisArgs {
+  const void* in;
+  void* out;
+  const void* er;   // [Lout16][Linp] Re E
+  const void* ei;   // [Lout16][Linp] Im E
+  int64_t outer;
+  int Lin, Lout, inner;
+  int Linp;         // Lin padded to 32
+  int Lout16;
+  float scale;
+};
+
+// Per-mode channel contraction:
+//   out[b][p][t] = scale * c(t) * sum_q in[b][q][t] * Wop(q, p, t)
+//   Wop = W[q][p][t] (forward) or conj(W[p][q][t]) (adjoint).
+struct ContractArgs {
+  const void* in;
+  const void* w;
+  void* out;
+  int B, Q, P, K;
+  int wrows, wcols;  // W is [wrows][wcols][K]
+  int adjoint;
+  int Kb, Nb;        // last-axis retained count and length (for c(t))
+  float scale;
+};
+
+// Batch-reduced weight gradient:
+//   gw[q][p][t] = scale * c(t) * sum_b conj(xh[b][q][t]) * gh[b][p][t]   (fp32)
+struct WgradArgs {
+  const void* xh;
+  const void* gh;
+  float* gw;
+  int B, Cin, Cout, K;
+  int Kb, Nb;
+  float scale;
+};
+
+// Generic pairwise complex contraction for the Tucker path (fp32 complex
+// intermediates; operand element type given per operand).
+//   out[m, n, ...] (batch, free-A, free-B index groups, row-major in the
+//   result's own index order) = sum_k A * B, with optional conjugation.
+constexpr int PW_MAXIDX = 8;
+struct PairArgs {
+  const void* a;
+  const void* b;
+  void* out;           // complex of out_elem
+  int a_elem, b_elem;  // Elem of each operand (intermediates are F32)
+  int out_elem;
+  int conj_a, conj_b;
+  int64_t out_size;
+  int n_out;           // number of result indices
+  int64_t out_ext[PW_MAXIDX];     // extents in result order
+  int64_t a_stride_out[PW_MAXIDX];// stride of A per result index (0 if absent)
+  int64_t b_stride_out[PW_MAXIDX];
+  int n_red;           // contracted indices
+  int64_t red_ext[PW_MAXIDX];
+  int64_t a_stride_red[PW_MAXIDX];
+  int64_t b_stride_red[PW_MAXIDX];
+  int64_t red_size;
+  float scale;
+  int scale_c_axis;    // result index position of the last spatial axis for c(t), -1 none
+  int Nb;              // last-axis length for c(t)
+};
+
+hipError_t launch_r2c(int elem, int nct, const R2CArgs& a, size_t lds, hipStream_t s);
+hipError_t launch_c2r(int elem, int nct, const C2RArgs& a, size_t lds, hipStream_t s);
+hipError_t launch_axis(int elem, const AxisArgs& a, size_t lds, hipStream_t s);
+hipError_t launch_contract(int elem, const ContractArgs& a, hipStream_t s);
+hipError_t launch_wgrad(int elem, const WgradArgs& a, hipStream_t s);
+hipError_t launch_pair(const PairArgs& a, hipStream_t s);
+hipError_t launch_scale_complex(float* p, int64_t n, float s, hipStream_t st);
+
+size_t r2c_lds_bytes(int elem, int Kbp, int R);
+size_t c2r_lds_bytes(int elem, int Kbp, int Kap, int R);
+size_t axis_lds_bytes(int elem, int Linp);
+
+}  // namespace fno

@@ -1,0 +1,1302 @@
+// Host side of the FNO spectral-convolution library: descriptor checks, the
+// truncation index map, the greedy Tucker contraction order, plan tables
+// (twiddles) cached per descriptor and device, workspace sizing, and the
+// C ABI entry points that enqueue the HIP kernels.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <array>
+#include <cmath>
+#include <cstdint>
+#include <cstring>
+#include <map>
+#include <memory>
+#include <mutex>
+#include <string>
+#include <vector>
+
+#include "../../include/fno_spectral_conv.h"
+#include "fno_internal.h"
+
+namespace fno {
+namespace {
+
+constexpr double kPi = 3.14159265358979323846;
+
+inline int64_t round_up(int64_t v, int64_t m) { return (v + m - 1) / m * m; }
+
+// --------------------------------------------------------------------------
+// Descriptor checks and the truncation map T_K (Sec. 2)
+// --------------------------------------------------------------------------
+fno_status check_desc(const fno_conv_desc* d) {
+  if (!d) return FNO_ERR_INVALID_ARGUMENT;
+  if (d->ndim < 1 || d->ndim > 3) return FNO_ERR_INVALID_ARGUMENT;
+  if (d->precision != FNO_PREC_FP32 && d->precision != FNO_PREC_FP16_TANH)
+    return FNO_ERR_INVALID_ARGUMENT;
+  if (d->weight_kind != FNO_WEIGHT_DENSE && d->weight_kind != FNO_WEIGHT_TUCKER)
+    return FNO_ERR_INVALID_ARGUMENT;
+  if (d->path_policy != FNO_PATH_MIN_RESULT && d->path_policy != FNO_PATH_MIN_NET)
+    return FNO_ERR_INVALID_ARGUMENT;
+  if (d->batch < 1 || d->c_in < 1 || d->c_out < 1) return FNO_ERR_INVALID_ARGUMENT;
+  const int nd = d->ndim;
+  for (int j = 0; j < nd; ++j) {
+    const int64_t n = d->n[j], m = d->modes[j];
+    if (n < 1 || m < 1) return FNO_ERR_INVALID_ARGUMENT;
+    if (j < nd - 1) {
+      if (2 * m > n) return FNO_ERR_INVALID_ARGUMENT;
+    } else {
+      if (m > n / 2 + 1) return FNO_ERR_INVALID_ARGUMENT;
+    }
+  }
+  if (d->weight_kind == FNO_WEIGHT_TUCKER)
+    for (int j = 0; j < 2 + nd; ++j)
+      if (d->rank[j] < 1) return FNO_ERR_INVALID_ARGUMENT;
+  // Sizes the kernels cover: extents up to 65536 per axis, index math in 64
+  // bits, retained counts per plane within the register tiles.
+  for (int j = 0; j < nd; ++j)
+    if (d->n[j] > 65536) return FNO_ERR_UNSUPPORTED;
+  if (d->batch > (1 << 30) || d->c_in > (1 << 20) || d->c_out > (1 << 20))
+    return FNO_ERR_UNSUPPORTED;
+  const int64_t Kb = d->modes[nd - 1];
+  const int64_t Ka = nd >= 2 ? 2 * d->modes[nd - 2] : 1;
+  if (Kb > 128 || Ka > 128) return FNO_ERR_UNSUPPORTED;
+  if (nd == 3 && 2 * d->modes[0] > 4096) return FNO_ERR_UNSUPPORTED;
+  return FNO_OK;
+}
+
+inline int64_t mode_k(int64_t n, int64_t m, bool last, int64_t t) {
+  if (last) return t;
+  return t < m ? t : n - 2 * m + t;
+}
+
+inline int64_t kextent(const fno_conv_desc* d, int j) {
+  return j < d->ndim - 1 ? 2 * d->modes[j] : d->modes[j];
+}
+
+inline int64_t nspatial(const fno_conv_desc* d) {
+  int64_t s = 1;
+  for (int j = 0; j < d->ndim; ++j) s *= d->n[j];
+  return s;
+}
+
+inline int64_t kmodes(const fno_conv_desc* d) {
+  int64_t s = 1;
+  for (int j = 0; j < d->ndim; ++j) s *= kextent(d, j);
+  return s;
+}
+
+// --------------------------------------------------------------------------
+// Greedy pairwise contraction order (Sec. 4.2)
+// --------------------------------------------------------------------------
+struct PStep {
+  int p, q;
+  std::string res;
+};
+
+using Sizes = std::map<char, int64_t>;
+
+int64_t label_size(const std::string& s, const Sizes& sz) {
+  int64_t v = 1;
+  for (char c : s) v *= sz.at(c);
+  return v;
+}
+
+std::string keep_indices(const std::vector<std::string>& ops, int p, int q,
+                         const std::string& out) {
+  std::string need = out;
+  for (int r = 0; r < (int)ops.size(); ++r)
+    if (r != p && r != q) need += ops[r];
+  std::string res;
+  for (char c : ops[p])
+    if (need.find(c) != std::string::npos && res.find(c) == std::string::npos) res += c;
+  for (char c : ops[q])
+    if (need.find(c) != std::string::npos && res.find(c) == std::string::npos) res += c;
+  return res;
+}
+
+bool share_index(const std::string& a, const std::string& b) {
+  for (char c : a)
+    if (b.find(c) != std::string::npos) return true;
+  return false;
+}
+
+std::vector<PStep> greedy_order(std::vector<std::string> ops, const Sizes& sz,
+                                const std::string& out, int policy) {
+  std::vector<PStep> steps;
+  while (ops.size() > 1) {
+    if (ops.size() == 2) {
+      steps.push_back({0, 1, out});
+      break;
+    }
+    const int n = (int)ops.size();
+    bool any_share = false;
+    for (int p = 0; p < n && !any_share; ++p)
+      for (int q = p + 1; q < n; ++q)
+        if (share_index(ops[p], ops[q])) {
+          any_share = true;
+          break;
+        }
+    bool have = false;
+    int64_t best = 0;
+    PStep pick{0, 1, ""};
+    for (int p = 0; p < n; ++p)
+      for (int q = p + 1; q < n; ++q) {
+        if (any_share && !share_index(ops[p], ops[q])) continue;
+        std::string res = keep_indices(ops, p, q, out);
+        int64_t cost = label_size(res, sz);
+        if (policy == FNO_PATH_MIN_NET) cost -= label_size(ops[p], sz) + label_size(ops[q], sz);
+        if (!have || cost < best) {
+          have = true;
+          best = cost;
+          pick = {p, q, res};
+        }
+      }
+    steps.push_back(pick);
+    std::vector<std::string> next;
+    for (int r = 0; r < n; ++r)
+      if (r != pick.p && r != pick.q) next.push_back(ops[r]);
+    next.push_back(pick.res);
+    ops.swap(next);
+  }
+  return steps;
+}
+
+// Index labels: b batch, i c_in, o c_out, a r_in, e r_out, x y z spatial,
+// c d f ranks of the spatial axes.
+const char kSpatial[3] = {'x', 'y', 'z'};
+const char kRank[3] = {'c', 'd', 'f'};
+
+void tucker_labels(int nd, bool adjoint, std::vector<std::string>* ops, std::string* out) {
+  std::string sp, rk;
+  for (int j = 0; j < nd; ++j) {
+    sp += kSpatial[j];
+    rk += kRank[j];
+  }
+  ops->clear();
+  ops->push_back(std::string(adjoint ? "bo" : "bi") + sp);
+  ops->push_back("ae" + rk);
+  ops->push_back("ia");
+  ops->push_back("oe");
+  for (int j = 0; j < nd; ++j) ops->push_back(std::string(1, kSpatial[j]) + kRank[j]);
+  *out = std::string(adjoint ? "bi" : "bo") + sp;
+}
+
+Sizes tucker_sizes(const fno_conv_desc* d) {
+  Sizes s;
+  s['b'] = d->batch;
+  s['i'] = d->c_in;
+  s['o'] = d->c_out;
+  s['a'] = d->rank[0];
+  s['e'] = d->rank[1];
+  for (int j = 0; j < d->ndim; ++j) {
+    s[kSpatial[j]] = kextent(d, j);
+    s[kRank[j]] = d->rank[2 + j];
+  }
+  return s;
+}
+
+int32_t label_bit(char c) {
+  switch (c) {
+    case 'b': return 0;
+    case 'i': return 1;
+    case 'o': return 2;
+    case 'a': return 3;
+    case 'e': return 4;
+    case 'x': return 5;
+    case 'y': return 6;
+    case 'z': return 7;
+    case 'c': return 8;
+    case 'd': return 9;
+    case 'f': return 10;
+  }
+  return 31;
+}
+
+// --------------------------------------------------------------------------
+// Plans: geometry and device tables
+// --------------------------------------------------------------------------
+struct Geo {
+  int nd;
+  int elem;          // ELEM_F16 / ELEM_F32
+  int es;            // element bytes
+  int64_t B, Cin, Cout;
+  int64_t N;         // prod n
+  int64_t K;         // prod K_j
+  // plane transform (last two axes)
+  int Na, Nb, Ka, Kb;
+  int Kbp, nct;
+  int Nbp, Kap16;
+  int R_f, Nap_f;    // r2c chunking
+  int Kap, R_i, Nap_i, Nb64;  // c2r
+  // leading 3-D axis
+  int N1, K1, Lin_f, Linp_f, Lout16_f, Linp_i, Lout16_i;
+};
+
+struct DevTables {
+  void* base = nullptr;
+  size_t bytes = 0;
+  const void *twA, *cB, *sB, *cI, *sI, *twI;
+  const void *eFr, *eFi, *eIr, *eIi;
+};
+
+struct Plan {
+  Geo g;
+  DevTables t;
+  std::vector<PStep> path_fwd, path_adj;
+  std::vector<std::string> labels_fwd, labels_adj;
+  std::string out_fwd, out_adj;
+  int device = 0;
+};
+
+Geo make_geo(const fno_conv_desc* d) {
+  Geo g{};
+  g.nd = d->ndim;
+  g.elem = d->precision == FNO_PREC_FP16_TANH ? ELEM_F16 : ELEM_F32;
+  g.es = g.elem == ELEM_F16 ? 2 : 4;
+  g.B = d->batch;
+  g.Cin = d->c_in;
+  g.Cout = d->c_out;
+  g.N = nspatial(d);
+  g.K = kmodes(d);
+  const int nd = d->ndim;
+  g.Nb = (int)d->n[nd - 1];
+  g.Kb = (int)d->modes[nd - 1];
+  if (nd >= 2) {
+    g.Na = (int)d->n[nd - 2];
+    g.Ka = (int)(2 * d->modes[nd - 2]);
+  } else {
+    g.Na = 1;
+    g.Ka = 1;
+  }
+  int kb16 = (int)round_up(g.Kb, 16);
+  int kbp = 16;
+  while (kbp < kb16) kbp *= 2;
+  g.Kbp = kbp;
+  g.nct = 2 * kbp / 16;
+  g.Nbp = (int)round_up(g.Nb, 32);
+  g.Kap16 = (int)round_up(g.Ka, 16);
+  // r2c row chunk: step-A result of one chunk stays within ~32 KiB of LDS
+  int rmax = (int)(32768 / (2 * g.Kbp * g.es)) / 32 * 32;
+  rmax = std::max(32, rmax);
+  g.R_f = (int)std::min<int64_t>(round_up(g.Na, 32), rmax);
+  g.Nap_f = (int)round_up(g.Na, g.R_f);
+  // c2r
+  g.Kap = (int)round_up(g.Ka, 32);
+  int rmaxi = (int)(32768 / (2 * g.Kbp * g.es)) / 16 * 16;
+  rmaxi = std::max(16, rmaxi);
+  g.R_i = (int)std::min<int64_t>(round_up(g.Na, 16), rmaxi);
+  g.Nap_i = (int)round_up(g.Na, g.R_i);
+  g.Nb64 = (int)round_up(g.Nb, 64);
+  if (nd == 3) {
+    g.N1 = (int)d->n[0];
+    g.K1 = (int)(2 * d->modes[0]);
+    g.Linp_f = (int)round_up(g.N1, 32);
+    g.Lout16_f = (int)round_up(g.K1, 16);
+    g.Linp_i = (int)round_up(g.K1, 32);
+    g.Lout16_i = (int)round_up(g.N1, 16);
+  }
+  return g;
+}
+
+// cos/sin of 2 pi (k n mod N) / N with the phase reduced exactly in integers.
+inline void twiddle(int64_t k, int64_t n, int64_t N, double* c, double* s) {
+  const int64_t r = ((k % N) * (n % N)) % N;
+  const double ph = 2.0 * kPi * (double)r / (double)N;
+  *c = std::cos(ph);
+  *s = std::sin(ph);
+}
+
+template <typename T>
+void fill_tables(const fno_conv_desc* d, const Geo& g, std::vector<T>& buf,
+                 std::vector<size_t>& off) {
+  auto alloc = [&](size_t n) {
+    size_t o = round_up((int64_t)buf.size(), 64);
+    buf.resize(o + n, (T)0.0f);
+    off.push_back(o);
+    return o;
+  };
+  const int nd = g.nd;
+  const int64_t ma = nd >= 2 ? d->modes[nd - 2] : 1;
+  auto ka_of = [&](int t) -> int64_t {
+    return nd >= 2 ? mode_k(g.Na, ma, false, t) : 0;
+  };
+  // twA [2 Kbp][Nbp]
+  size_t o = alloc((size_t)2 * g.Kbp * g.Nbp);
+  for (int t = 0; t < g.Kb; ++t)
+    for (int n = 0; n < g.Nb; ++n) {
+      double c, s;
+      twiddle(t, n, g.Nb, &c, &s);
+      buf[o + (size_t)t * g.Nbp + n] = (T)c;
+      buf[o + (size_t)(g.Kbp + t) * g.Nbp + n] = (T)(-s);
+    }
+  // cB, sB [Kap16][Nap_f]
+  size_t oc = alloc((size_t)g.Kap16 * g.Nap_f);
+  size_t os = alloc((size_t)g.Kap16 * g.Nap_f);
+  for (int t = 0; t < g.Ka; ++t)
+    for (int n = 0; n < g.Na; ++n) {
+      double c, s;
+      twiddle(ka_of(t), n, g.Na, &c, &s);
+      buf[oc + (size_t)t * g.Nap_f + n] = (T)c;
+      buf[os + (size_t)t * g.Nap_f + n] = (T)s;
+    }
+  // cI, sI [Nap_i][Kap]
+  size_t oci = alloc((size_t)g.Nap_i * g.Kap);
+  size_t osi = alloc((size_t)g.Nap_i * g.Kap);
+  for (int n = 0; n < g.Na; ++n)
+    for (int t = 0; t < g.Ka; ++t) {
+      double c, s;
+      twiddle(ka_of(t), n, g.Na, &c, &s);
+      buf[oci + (size_t)n * g.Kap + t] = (T)c;
+      buf[osi + (size_t)n * g.Kap + t] = (T)s;
+    }
+  // twI [Nb64][2 Kbp]
+  size_t oti = alloc((size_t)g.Nb64 * 2 * g.Kbp);
+  for (int n = 0; n < g.Nb; ++n)
+    for (int t = 0; t < g.Kb; ++t) {
+      double c, s;
+      twiddle(t, n, g.Nb, &c, &s);
+      buf[oti + (size_t)n * 2 * g.Kbp + t] = (T)c;
+      buf[oti + (size_t)n * 2 * g.Kbp + g.Kbp + t] = (T)(-s);
+    }
+  (void)o;
+  (void)oc;
+  (void)os;
+  (void)oci;
+  (void)osi;
+  (void)oti;
+  if (nd == 3) {
+    const int64_t m1 = d->modes[0];
+    // forward E[t][l] = exp(-2 pi i k1(t) l / N1): [Lout16_f][Linp_f]
+    size_t er = alloc((size_t)g.Lout16_f * g.Linp_f);
+    size_t ei = alloc((size_t)g.Lout16_f * g.Linp_f);
+    for (int t = 0; t < g.K1; ++t)
+      for (int l = 0; l < g.N1; ++l) {
+        double c, s;
+        twiddle(mode_k(g.N1, m1, false, t), l, g.N1, &c, &s);
+        buf[er + (size_t)t * g.Linp_f + l] = (T)c;
+        buf[ei + (size_t)t * g.Linp_f + l] = (T)(-s);
+      }
+    // inverse E[n][t] = exp(+2 pi i k1(t) n / N1): [Lout16_i][Linp_i]
+    size_t ir = alloc((size_t)g.Lout16_i * g.Linp_i);
+    size_t ii = alloc((size_t)g.Lout16_i * g.Linp_i);
+    for (int n = 0; n < g.N1; ++n)
+      for (int t = 0; t < g.K1; ++t) {
+        double c, s;
+        twiddle(mode_k(g.N1, m1, false, t), n, g.N1, &c, &s);
+        buf[ir + (size_t)n * g.Linp_i + t] = (T)c;
+        buf[ii + (size_t)n * g.Linp_i + t] = (T)s;
+      }
+  }
+}
+
+struct PlanKey {
+  std::array<int64_t, 24> v;
+  bool operator<(const PlanKey& o) const { return v < o.v; }
+};
+
+PlanKey key_of(const fno_conv_desc* d, int device) {
+  PlanKey k;
+  k.v.fill(0);
+  k.v[0] = device;
+  k.v[1] = d->ndim;
+  k.v[2] = d->precision;
+  k.v[3] = d->weight_kind;
+  k.v[4] = d->path_policy;
+  k.v[5] = d->batch;
+  k.v[6] = d->c_in;
+  k.v[7] = d->c_out;
+  for (int j = 0; j < d->ndim; ++j) {
+    k.v[8 + j] = d->n[j];
+    k.v[11 + j] = d->modes[j];
+  }
+  if (d->weight_kind == FNO_WEIGHT_TUCKER)
+    for (int j = 0; j < 2 + d->ndim; ++j) k.v[14 + j] = d->rank[j];
+  return k;
+}
+
+std::mutex g_mutex;
+std::map<PlanKey, std::unique_ptr<Plan>> g_plans;
+
+fno_status build_tables(const fno_conv_desc* d, Plan* pl) {
+  std::vector<size_t> off;
+  size_t bytes = 0;
+  std::vector<_Float16> b16;
+  std::vector<float> b32;
+  if (pl->g.elem == ELEM_F16) {
+    fill_tables<_Float16>(d, pl->g, b16, off);
+    bytes = b16.size() * 2;
+  } else {
+    fill_tables<float>(d, pl->g, b32, off);
+    bytes = b32.size() * 4;
+  }
+  void* dev = nullptr;
+  if (hipMalloc(&dev, std::max<size_t>(bytes, 256)) != hipSuccess) return FNO_ERR_HIP;
+  const void* src = pl->g.elem == ELEM_F16 ? (const void*)b16.data() : (const void*)b32.data();
+  if (hipMemcpy(dev, src, bytes, hipMemcpyHostToDevice) != hipSuccess) {
+    (void)hipFree(dev);
+    return FNO_ERR_HIP;
+  }
+  pl->t.base = dev;
+  pl->t.bytes = bytes;
+  auto at = [&](int i) -> const void* {
+    return (const void*)((const char*)dev + off[i] * pl->g.es);
+  };
+  pl->t.twA = at(0);
+  pl->t.cB = at(1);
+  pl->t.sB = at(2);
+  pl->t.cI = at(3);
+  pl->t.sI = at(4);
+  pl->t.twI = at(5);
+  if (pl->g.nd == 3) {
+    pl->t.eFr = at(6);
+    pl->t.eFi = at(7);
+    pl->t.eIr = at(8);
+    pl->t.eIi = at(9);
+  }
+  return FNO_OK;
+}
+
+// Geometry and Tucker paths: host-only, no device calls.
+void host_plan(const fno_conv_desc* d, Plan* pl) {
+  pl->g = make_geo(d);
+  if (d->weight_kind == FNO_WEIGHT_TUCKER) {
+    Sizes sz = tucker_sizes(d);
+    tucker_labels(d->ndim, false, &pl->labels_fwd, &pl->out_fwd);
+    tucker_labels(d->ndim, true, &pl->labels_adj, &pl->out_adj);
+    pl->path_fwd = greedy_order(pl->labels_fwd, sz, pl->out_fwd, d->path_policy);
+    pl->path_adj = greedy_order(pl->labels_adj, sz, pl->out_adj, d->path_policy);
+  }
+}
+
+fno_status get_plan(const fno_conv_desc* d, Plan** out) {
+  fno_status st = check_desc(d);
+  if (st != FNO_OK) return st;
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return FNO_ERR_HIP;
+  PlanKey key = key_of(d, dev);
+  std::lock_guard<std::mutex> lock(g_mutex);
+  auto it = g_plans.find(key);
+  if (it != g_plans.end()) {
+    *out = it->second.get();
+    return FNO_OK;
+  }
+  std::unique_ptr<Plan> pl(new Plan());
+  host_plan(d, pl.get());
+  pl->device = dev;
+  st = build_tables(d, pl.get());
+  if (st != FNO_OK) return st;
+  *out = pl.get();
+  g_plans[key] = std::move(pl);
+  return FNO_OK;
+}
+
+// --------------------------------------------------------------------------
+// Workspace layout
+// --------------------------------------------------------------------------
+struct WsLayout {
+  size_t total = 0;
+  size_t add(size_t bytes) {
+    size_t o = total;
+    total += (size_t)round_up((int64_t)std::max<size_t>(bytes, 1), 256);
+    return o;
+  }
+};
+
+size_t spec_bytes(const Geo& g, int64_t C) { return (size_t)g.B * C * g.K * 2 * g.es; }
+
+size_t inter3d_bytes(const Geo& g, int64_t C) {
+  if (g.nd != 3) return 0;
+  return (size_t)g.B * C * g.N1 * g.Ka * g.Kb * 2 * g.es;
+}
+
+struct TuckerWs {
+  std::vector<size_t> step_off;  // one fp32 complex buffer per intermediate
+  size_t total = 0;
+};
+
+// Tucker intermediates of a path (all but the last step, which writes the
+// output spectrum).
+size_t tucker_path_bytes(const fno_conv_desc* d, const std::vector<PStep>& path) {
+  Sizes sz = tucker_sizes(d);
+  size_t t = 0;
+  for (size_t s = 0; s + 1 < path.size(); ++s)
+    t += (size_t)round_up(label_size(path[s].res, sz) * 8, 256);
+  return t;
+}
+
+size_t tucker_wgrad_bytes(const fno_conv_desc* d, const Plan* pl);
+
+size_t ws_bytes(const fno_conv_desc* d, const Plan* pl, fno_op op, bool caches) {
+  const Geo& g = pl->g;
+  WsLayout w;
+  const bool tucker = d->weight_kind == FNO_WEIGHT_TUCKER;
+  if (op == FNO_OP_FWD) {
+    w.add(spec_bytes(g, g.Cin));
+    w.add(spec_bytes(g, g.Cout));
+    w.add(std::max(inter3d_bytes(g, g.Cin), inter3d_bytes(g, g.Cout)));
+    if (tucker) w.add(tucker_path_bytes(d, pl->path_fwd));
+  } else if (op == FNO_OP_BWD_DATA) {
+    w.add(spec_bytes(g, g.Cout));
+    w.add(spec_bytes(g, g.Cin));
+    w.add(std::max(inter3d_bytes(g, g.Cin), inter3d_bytes(g, g.Cout)));
+    if (tucker) w.add(tucker_path_bytes(d, pl->path_adj));
+  } else {
+    if (!caches) {
+      w.add(spec_bytes(g, g.Cin));
+      w.add(spec_bytes(g, g.Cout));
+      w.add(std::max(inter3d_bytes(g, g.Cin), inter3d_bytes(g, g.Cout)));
+    }
+    if (tucker) w.add(tucker_wgrad_bytes(d, pl));
+  }
+  return std::max<size_t>(w.total, 256);
+}
+
+// --------------------------------------------------------------------------
+// Kernel sequences
+// --------------------------------------------------------------------------
+inline bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
+#define FNO_HIP(call)                        \
+  do {                                       \
+    if ((call) != hipSuccess) return FNO_ERR_HIP; \
+  } while (0)
+
+// --------------------------------------------------------------------------
+// Optional per-kernel event timing
+// --------------------------------------------------------------------------
+struct ProfEntry {
+  std::string name;
+  int64_t launches = 0;
+  double total_ms = 0.0;
+};
+struct Pending {
+  int slot;
+  hipEvent_t a, b;
+};
+std::mutex g_prof_mutex;
+bool g_prof_on = false;
+std::vector<ProfEntry> g_prof;
+std::vector<Pending> g_pending;
+
+int prof_slot(const char* name) {
+  for (size_t i = 0; i < g_prof.size(); ++i)
+    if (g_prof[i].name == name) return (int)i;
+  g_prof.push_back(ProfEntry{name, 0, 0.0});
+  return (int)g_prof.size() - 1;
+}
+
+// Runs `launch` bracketed by events when profiling is on.
+template <typename F>
+hipError_t timed(const char* name, hipStream_t s, F launch) {
+  bool on;
+  {
+    std::lock_guard<std::mutex> lk(g_prof_mutex);
+    on = g_prof_on;
+  }
+  if (!on) return launch();
+  hipEvent_t a = nullptr, b = nullptr;
+  if (hipEventCreate(&a) != hipSuccess) return hipErrorOutOfMemory;
+  if (hipEventCreate(&b) != hipSuccess) {
+    (void)hipEventDestroy(a);
+    return hipErrorOutOfMemory;
+  }
+  (void)hipEventRecord(a, s);
+  hipError_t e = launch();
+  (void)hipEventRecord(b, s);
+  std::lock_guard<std::mutex> lk(g_prof_mutex);
+  g_pending.push_back(Pending{prof_slot(name), a, b});
+  return e;
+}
+
+void prof_drain() {
+  for (Pending& p : g_pending) {
+    (void)hipEventSynchronize(p.b);
+    float ms = 0.0f;
+    if (hipEventElapsedTime(&ms, p.a, p.b) == hipSuccess) {
+      g_prof[p.slot].launches += 1;
+      g_prof[p.slot].total_ms += ms;
+    }
+    (void)hipEventDestroy(p.a);
+    (void)hipEventDestroy(p.b);
+  }
+  g_pending.clear();
+}
+
+// Forward truncated transform of planes -> spectrum [B][C][K...].
+// scale_mode 0: 1/N normalisation (input spectrum), 1: 1/sqrt(N) (gradient).
+fno_status run_r2c(const Plan* pl, const void* in, void* spec, void* inter, int64_t C,
+                   int do_tanh, int scale_mode, hipStream_t s) {
+  const Geo& g = pl->g;
+  R2CArgs a{};
+  a.in = in;
+  a.out = g.nd == 3 ? inter : spec;
+  a.twA = pl->t.twA;
+  a.cB = pl->t.cB;
+  a.sB = pl->t.sB;
+  a.planes = g.B * C * (g.nd == 3 ? g.N1 : 1);
+  a.Na = g.Na;
+  a.Nb = g.Nb;
+  a.Ka = g.Ka;
+  a.Kb = g.Kb;
+  a.Kbp = g.Kbp;
+  a.Nbp = g.Nbp;
+  a.Nap = g.Nap_f;
+  a.Kap16 = g.Kap16;
+  a.R = g.R_f;
+  if (scale_mode == 0) {
+    a.scaleA = (float)(1.0 / g.Nb);
+    a.scaleB = (float)(1.0 / g.Na);
+  } else {
+    a.scaleA = (float)(1.0 / std::sqrt((double)g.Nb));
+    a.scaleB = (float)(1.0 / std::sqrt((double)g.Na));
+  }
+  a.do_tanh = do_tanh;
+  a.vec = (g.Nb % 8) == 0;
+  if (a.planes > 0x7fffffff || (g.nd == 3 && g.B * C > 65535)) return FNO_ERR_UNSUPPORTED;
+  FNO_HIP(timed("r2c_plane", s, [&] { return launch_r2c(g.elem, g.nct, a, r2c_lds_bytes(g.elem, g.Kbp, g.R_f), s); }));
+  if (g.nd == 3) {
+    AxisArgs x{};
+    x.in = inter;
+    x.out = spec;
+    x.er = pl->t.eFr;
+    x.ei = pl->t.eFi;
+    x.outer = g.B * C;
+    x.Lin = g.N1;
+    x.Lout = g.K1;
+    x.inner = g.Ka * g.Kb;
+    x.Linp = g.Linp_f;
+    x.Lout16 = g.Lout16_f;
+    x.scale = scale_mode == 0 ? (float)(1.0 / g.N1) : (float)(1.0 / std::sqrt((double)g.N1));
+    FNO_HIP(timed("axis_fwd", s, [&] { return launch_axis(g.elem, x, axis_lds_bytes(g.elem, g.Linp_f), s); }));
+  }
+  return FNO_OK;
+}
+
+// Inverse: spectrum [B][C][K...] -> planes, out = scale * sum Re(Z e^{+i theta}).
+fno_status run_c2r(const Plan* pl, const void* spec, void* out, void* inter, int64_t C,
+                   float scale, const void* x_epi, hipStream_t s) {
+  const Geo& g = pl->g;
+  const void* src = spec;
+  if (g.nd == 3 && g.B * C > 65535) return FNO_ERR_UNSUPPORTED;
+  if (g.nd == 3) {
+    AxisArgs x{};
+    x.in = spec;
+    x.out = inter;
+    x.er = pl->t.eIr;
+    x.ei = pl->t.eIi;
+    x.outer = g.B * C;
+    x.Lin = g.K1;
+    x.Lout = g.N1;
+    x.inner = g.Ka * g.Kb;
+    x.Linp = g.Linp_i;
+    x.Lout16 = g.Lout16_i;
+    x.scale = 1.0f;
+    FNO_HIP(timed("axis_inv", s, [&] { return launch_axis(g.elem, x, axis_lds_bytes(g.elem, g.Linp_i), s); }));
+    src = inter;
+  }
+  C2RArgs a{};
+  a.in = src;
+  a.out = out;
+  a.x = x_epi;
+  a.cI = pl->t.cI;
+  a.sI = pl->t.sI;
+  a.twI = pl->t.twI;
+  a.planes = g.B * C * (g.nd == 3 ? g.N1 : 1);
+  a.Na = g.Na;
+  a.Nb = g.Nb;
+  a.Ka = g.Ka;
+  a.Kb = g.Kb;
+  a.Kbp = g.Kbp;
+  a.Kap = g.Kap;
+  a.Nap = g.Nap_i;
+  a.R = g.R_i;
+  a.scale = scale;
+  a.epilogue = x_epi != nullptr;
+  a.vec = (g.Nb % 8) == 0;
+  if (a.planes > 0x7fffffff) return FNO_ERR_UNSUPPORTED;
+  FNO_HIP(timed(x_epi ? "c2r_plane_tanh_grad" : "c2r_plane", s, [&] { return launch_c2r(g.elem, g.nct, a, c2r_lds_bytes(g.elem, g.Kbp, g.Kap, g.R_i), s); }));
+  return FNO_OK;
+}
+
+fno_status run_contract(const Plan* pl, const void* in, const void* w, void* out,
+                        bool adjoint, hipStream_t s) {
+  const Geo& g = pl->g;
+  ContractArgs a{};
+  a.in = in;
+  a.w = w;
+  a.out = out;
+  a.B = (int)g.B;
+  a.Q = (int)(adjoint ? g.Cout : g.Cin);
+  a.P = (int)(adjoint ? g.Cin : g.Cout);
+  a.K = (int)g.K;
+  a.wrows = (int)g.Cin;
+  a.wcols = (int)g.Cout;
+  a.adjoint = adjoint;
+  a.Kb = g.Kb;
+  a.Nb = g.Nb;
+  a.scale = 1.0f;
+  if (g.K > 0x7fffffff / 2) return FNO_ERR_UNSUPPORTED;
+  FNO_HIP(timed(adjoint ? "contract_adjoint" : "contract", s, [&] { return launch_contract(g.elem, a, s); }));
+  return FNO_OK;
+}
+
+// One pairwise Tucker step.  Operands carry labels, element type, conj flag.
+struct Opnd {
+  const void* ptr;
+  std::string lab;
+  int elem;
+  int conj;
+};
+
+fno_status run_pair(const Sizes& sz, const Opnd& A, const Opnd& Bo, const std::string& res,
+                    void* out, int out_elem, float scale, int c_axis_char, int Nb,
+                    hipStream_t s) {
+  PairArgs a{};
+  a.a = A.ptr;
+  a.b = Bo.ptr;
+  a.out = out;
+  a.a_elem = A.elem;
+  a.b_elem = Bo.elem;
+  a.conj_a = A.conj;
+  a.conj_b = Bo.conj;
+  a.out_elem = out_elem;
+  auto strides = [&](const std::string& lab) {
+    std::map<char, int64_t> st;
+    int64_t acc = 1;
+    for (int i = (int)lab.size() - 1; i >= 0; --i) {
+      st[lab[i]] = acc;
+      acc *= sz.at(lab[i]);
+    }
+    return st;
+  };
+  auto sa = strides(A.lab), sb = strides(Bo.lab);
+  if ((int)res.size() > PW_MAXIDX) return FNO_ERR_UNSUPPORTED;
+  a.n_out = (int)res.size();
+  a.out_size = 1;
+  a.scale_c_axis = -1;
+  for (int k = 0; k < a.n_out; ++k) {
+    char c = res[k];
+    a.out_ext[k] = sz.at(c);
+    a.out_size *= a.out_ext[k];
+    a.a_stride_out[k] = sa.count(c) ? sa[c] : 0;
+    a.b_stride_out[k] = sb.count(c) ? sb[c] : 0;
+    if (c == c_axis_char) a.scale_c_axis = k;
+  }
+  std::string red;
+  for (char c : A.lab + Bo.lab)
+    if (res.find(c) == std::string::npos && red.find(c) == std::string::npos) red += c;
+  if ((int)red.size() > PW_MAXIDX) return FNO_ERR_UNSUPPORTED;
+  a.n_red = (int)red.size();
+  a.red_size = 1;
+  for (int k = 0; k < a.n_red; ++k) {
+    char c = red[k];
+    a.red_ext[k] = sz.at(c);
+    a.red_size *= a.red_ext[k];
+    a.a_stride_red[k] = sa.count(c) ? sa[c] : 0;
+    a.b_stride_red[k] = sb.count(c) ? sb[c] : 0;
+  }
+  a.scale = scale;
+  a.Nb = Nb;
+  FNO_HIP(timed("tucker_pair", s, [&] { return launch_pair(a, s); }));
+  return FNO_OK;
+}
+
+// Evaluate a Tucker path: operands [spec, core, u_in, u_out, u_1..u_d].
+fno_status run_tucker_path(const fno_conv_desc* d, const Plan* pl, bool adjoint,
+                           const void* spec, const fno_weights* w, void* out_spec,
+                           char* scratch, hipStream_t s) {
+  const Geo& g = pl->g;
+  Sizes sz = tucker_sizes(d);
+  const std::vector<PStep>& path = adjoint ? pl->path_adj : pl->path_fwd;
+  const std::vector<std::string>& labs = adjoint ? pl->labels_adj : pl->labels_fwd;
+  std::vector<Opnd> ops;
+  ops.push_back({spec, labs[0], g.elem, 0});
+  const int cj = adjoint ? 1 : 0;
+  ops.push_back({w->core, labs[1], g.elem, cj});
+  ops.push_back({w->u_in, labs[2], g.elem, cj});
+  ops.push_back({w->u_out, labs[3], g.elem, cj});
+  for (int j = 0; j < d->ndim; ++j) ops.push_back({w->u_mode[j], labs[4 + j], g.elem, cj});
+  size_t off = 0;
+  const char clast = kSpatial[d->ndim - 1];
+  for (size_t st = 0; st < path.size(); ++st) {
+    const PStep& ps = path[st];
+    const bool last = st + 1 == path.size();
+    void* dst;
+    int oelem;
+    if (last) {
+      dst = out_spec;
+      oelem = g.elem;
+    } else {
+      dst = scratch + off;
+      off += (size_t)round_up(label_size(ps.res, sz) * 8, 256);
+      oelem = ELEM_F32;
+    }
+    fno_status r = run_pair(sz, ops[ps.p], ops[ps.q], ps.res, dst, oelem, 1.0f,
+                            last ? clast : 0, g.Nb, s);
+    if (r != FNO_OK) return r;
+    std::vector<Opnd> next;
+    for (int k = 0; k < (int)ops.size(); ++k)
+      if (k != ps.p && k != ps.q) next.push_back(ops[k]);
+    next.push_back({dst, ps.res, oelem, 0});
+    ops.swap(next);
+  }
+  return FNO_OK;
+}
+
+// Fixed schedule of the Tucker weight gradient (chain rule through the
+// multilinear map): P = conj(Xhat u_in), Q = sqrt(N) c G conj(u_out),
+// R = sum_b P Q, S = core x u_1 .. x u_d; g_core = R x conj(u_j)...,
+// g_u_j = R . conj(core x_{q != j} u_q), g_u_in = conj(Xhat) . (Q conj S),
+// g_u_out = (sqrt(N) c G) . (P conj S).
+fno_status run_tucker_wgrad(const fno_conv_desc* d, const Plan* pl, const void* xh,
+                            const void* gh, const fno_weights* w, fno_weight_grads* gw,
+                            char* scratch, hipStream_t s, size_t* scratch_used = nullptr) {
+  const bool dry = scratch_used != nullptr;
+  auto run_pair = [&](const Sizes& sz_, const Opnd& A, const Opnd& Bo, const std::string& res,
+                      void* out, int out_elem, float scale, int c_axis_char, int Nb,
+                      hipStream_t st) -> fno_status {
+    if (dry) return FNO_OK;
+    return fno::run_pair(sz_, A, Bo, res, out, out_elem, scale, c_axis_char, Nb, st);
+  };
+  const Geo& g = pl->g;
+  const int nd = d->ndim;
+  Sizes sz = tucker_sizes(d);
+  std::string sp, rk;
+  for (int j = 0; j < nd; ++j) {
+    sp += kSpatial[j];
+    rk += kRank[j];
+  }
+  const char clast = kSpatial[nd - 1];
+  const float sqN = (float)std::sqrt((double)g.N);
+  size_t off = 0;
+  auto buf = [&](const std::string& lab) {
+    void* p = scratch + off;
+    off += (size_t)round_up(label_size(lab, sz) * 8, 256);
+    return p;
+  };
+  auto F = [&](const void* p, const std::string& lab, int conj) {
+    return Opnd{p, lab, ELEM_F32, conj};
+  };
+  auto Wt = [&](const void* p, const std::string& lab, int conj) {
+    return Opnd{p, lab, g.elem, conj};
+  };
+  fno_status r;
+  const std::string lP = "ba" + sp, lQ = "be" + sp, lR = "ae" + sp;
+  void* P = buf(lP);
+  void* Q = buf(lQ);
+  void* Rb = buf(lR);
+  // P[b,a,sp] = sum_i conj(Xhat[b,i,sp]) conj(u_in[i,a])
+  r = run_pair(sz, Wt(xh, "bi" + sp, 1), Wt(w->u_in, "ia", 1), lP, P, ELEM_F32, 1.0f, 0, g.Nb, s);
+  if (r) return r;
+  // Q[b,e,sp] = sqrt(N) c(t) sum_o G[b,o,sp] conj(u_out[o,e])
+  r = run_pair(sz, Wt(gh, "bo" + sp, 0), Wt(w->u_out, "oe", 1), lQ, Q, ELEM_F32, sqN, clast,
+               g.Nb, s);
+  if (r) return r;
+  // R[a,e,sp] = sum_b P Q
+  r = run_pair(sz, F(P, lP, 0), F(Q, lQ, 0), lR, Rb, ELEM_F32, 1.0f, 0, g.Nb, s);
+  if (r) return r;
+  // g_core[a,e,rk] = R contracted with conj(u_j) along every spatial axis
+  {
+    Opnd cur = F(Rb, lR, 0);
+    std::string lab = lR;
+    for (int j = 0; j < nd; ++j) {
+      std::string nl;
+      for (char c : lab) nl += (c == kSpatial[j]) ? kRank[j] : c;
+      const bool last = j == nd - 1;
+      void* dst = last ? gw->core : buf(nl);
+      // reorder the final result to (a, e, rk)
+      std::string res = last ? ("ae" + rk) : nl;
+      r = run_pair(sz, cur, Wt(w->u_mode[j], std::string(1, kSpatial[j]) + kRank[j], 1), res,
+                   dst, ELEM_F32, 1.0f, 0, g.Nb, s);
+      if (r) return r;
+      cur = F(dst, res, 0);
+      lab = res;
+    }
+  }
+  // Per-axis partial cores C_j = core x_{q != j} u_q, labels (a,e, r_j, sp\j)
+  for (int j = 0; j < nd; ++j) {
+    Opnd cur = Wt(w->core, "ae" + rk, 0);
+    std::string lab = "ae" + rk;
+    bool first = true;
+    for (int q = 0; q < nd; ++q) {
+      if (q == j) continue;
+      std::string nl;
+      for (char c : lab) nl += (c == kRank[q]) ? kSpatial[q] : c;
+      void* dst = buf(nl);
+      r = run_pair(sz, cur, Wt(w->u_mode[q], std::string(1, kSpatial[q]) + kRank[q], 0), nl,
+                   dst, ELEM_F32, 1.0f, 0, g.Nb, s);
+      if (r) return r;
+      cur = F(dst, nl, 0);
+      lab = nl;
+      first = false;
+    }
+    // g_u_j[x_j, r_j] = sum R[a,e,sp] conj(C_j[a,e,.., r_j, ..])
+    std::string res = std::string(1, kSpatial[j]) + kRank[j];
+    Opnd cj = first ? Wt(w->core, "ae" + rk, 1) : Opnd{cur.ptr, cur.lab, cur.elem, 1};
+    r = run_pair(sz, F(Rb, lR, 0), cj, res, gw->u_mode[j], ELEM_F32, 1.0f, 0, g.Nb, s);
+    if (r) return r;
+  }
+  // S[a,e,sp] = core x all u_j
+  void* S;
+  {
+    Opnd cur = Wt(w->core, "ae" + rk, 0);
+    std::string lab = "ae" + rk;
+    for (int q = 0; q < nd; ++q) {
+      std::string nl;
+      for (char c : lab) nl += (c == kRank[q]) ? kSpatial[q] : c;
+      void* dst = buf(nl);
+      r = run_pair(sz, cur, Wt(w->u_mode[q], std::string(1, kSpatial[q]) + kRank[q], 0), nl,
+                   dst, ELEM_F32, 1.0f, 0, g.Nb, s);
+      if (r) return r;
+      cur = F(dst, nl, 0);
+      lab = nl;
+    }
+    S = const_cast<void*>(cur.ptr);
+  }
+  const std::string lS = "ae" + sp;
+  // Z1[b,a,sp] = sum_e Q[b,e,sp] conj(S[a,e,sp]);  g_u_in = sum conj(Xhat) Z1
+  void* Z1 = buf("ba" + sp);
+  r = run_pair(sz, F(Q, lQ, 0), F(S, lS, 1), "ba" + sp, Z1, ELEM_F32, 1.0f, 0, g.Nb, s);
+  if (r) return r;
+  r = run_pair(sz, Wt(xh, "bi" + sp, 1), F(Z1, "ba" + sp, 0), "ia", gw->u_in, ELEM_F32, 1.0f, 0,
+               g.Nb, s);
+  if (r) return r;
+  // Z2[b,e,sp] = sqrt(N) c(t) sum_a P[b,a,sp] conj(S[a,e,sp]); g_u_out = sum G Z2
+  void* Z2 = buf("be" + sp);
+  r = run_pair(sz, F(P, lP, 0), F(S, lS, 1), "be" + sp, Z2, ELEM_F32, sqN, clast, g.Nb, s);
+  if (r) return r;
+  r = run_pair(sz, Wt(gh, "bo" + sp, 0), F(Z2, "be" + sp, 0), "oe", gw->u_out, ELEM_F32, 1.0f,
+               0, g.Nb, s);
+  if (r) return r;
+  if (dry) *scratch_used = off;
+  return FNO_OK;
+}
+
+size_t tucker_wgrad_bytes(const fno_conv_desc* d, const Plan* pl) {
+  fno_weights w{};
+  fno_weight_grads gw{};
+  size_t used = 0;
+  char dummy = 0;
+  (void)run_tucker_wgrad(d, pl, &dummy, &dummy, &w, &gw, &dummy, nullptr, &used);
+  return used;
+}
+
+fno_status check_weights(const fno_conv_desc* d, const fno_weights* w) {
+  if (!w) return FNO_ERR_INVALID_ARGUMENT;
+  if (d->weight_kind == FNO_WEIGHT_DENSE) {
+    if (!w->dense || !aligned16(w->dense)) return FNO_ERR_INVALID_ARGUMENT;
+  } else {
+    if (!w->core || !w->u_in || !w->u_out) return FNO_ERR_INVALID_ARGUMENT;
+    if (!aligned16(w->core) || !aligned16(w->u_in) || !aligned16(w->u_out))
+      return FNO_ERR_INVALID_ARGUMENT;
+    for (int j = 0; j < d->ndim; ++j)
+      if (!w->u_mode[j] || !aligned16(w->u_mode[j])) return FNO_ERR_INVALID_ARGUMENT;
+  }
+  return FNO_OK;
+}
+
+inline bool okptr(const void* p) { return p && aligned16(p); }
+
+// Workspace check from the host-only plan: runs before any device call.
+fno_status check_ws(const fno_conv_desc* d, fno_op op, bool caches, const void* ws,
+                    size_t ws_len) {
+  Plan hp;
+  host_plan(d, &hp);
+  if (ws_len < ws_bytes(d, &hp, op, caches)) return FNO_ERR_WORKSPACE_TOO_SMALL;
+  if (!okptr(ws)) return FNO_ERR_INVALID_ARGUMENT;
+  return FNO_OK;
+}
+
+}  // namespace
+}  // namespace fno
+
+using namespace fno;
+
+extern "C" {
+
+const char* fno_status_string(fno_status s) {
+  switch (s) {
+    case FNO_OK: return "FNO_OK";
+    case FNO_ERR_INVALID_ARGUMENT: return "FNO_ERR_INVALID_ARGUMENT";
+    case FNO_ERR_UNSUPPORTED: return "FNO_ERR_UNSUPPORTED";
+    case FNO_ERR_WORKSPACE_TOO_SMALL: return "FNO_ERR_WORKSPACE_TOO_SMALL";
+    case FNO_ERR_HIP: return "FNO_ERR_HIP";
+    case FNO_ERR_INTERNAL: return "FNO_ERR_INTERNAL";
+  }
+  return "FNO_ERR_UNKNOWN";
+}
+
+fno_status fno_mode_frequency(const fno_conv_desc* d, int32_t axis, int64_t t, int64_t* k) {
+  fno_status st = check_desc(d);
+  if (st != FNO_OK && st != FNO_ERR_UNSUPPORTED) return st;
+  if (!k || axis < 0 || axis >= d->ndim) return FNO_ERR_INVALID_ARGUMENT;
+  const bool last = axis == d->ndim - 1;
+  const int64_t ext = last ? d->modes[axis] : 2 * d->modes[axis];
+  if (t < 0 || t >= ext) return FNO_ERR_INVALID_ARGUMENT;
+  *k = mode_k(d->n[axis], d->modes[axis], last, t);
+  return FNO_OK;
+}
+
+static fno_status path_for(const fno_conv_desc* d, fno_op op, std::vector<PStep>* path,
+                           std::vector<std::string>* labs, std::string* out) {
+  fno_status st = check_desc(d);
+  if (st != FNO_OK && st != FNO_ERR_UNSUPPORTED) return st;
+  if (d->weight_kind != FNO_WEIGHT_TUCKER) return FNO_ERR_INVALID_ARGUMENT;
+  if (op != FNO_OP_FWD && op != FNO_OP_BWD_DATA) return FNO_ERR_INVALID_ARGUMENT;
+  tucker_labels(d->ndim, op == FNO_OP_BWD_DATA, labs, out);
+  *path = greedy_order(*labs, tucker_sizes(d), *out, d->path_policy);
+  return FNO_OK;
+}
+
+fno_status fno_contraction_path(const fno_conv_desc* d, fno_op op, int32_t* steps, int32_t cap,
+                                int32_t* n_steps) {
+  if (!n_steps) return FNO_ERR_INVALID_ARGUMENT;
+  std::vector<PStep> path;
+  std::vector<std::string> labs;
+  std::string out;
+  fno_status st = path_for(d, op, &path, &labs, &out);
+  if (st != FNO_OK) return st;
+  *n_steps = (int32_t)path.size();
+  if (!steps || cap < (int32_t)path.size()) return FNO_ERR_INVALID_ARGUMENT;
+  for (size_t i = 0; i < path.size(); ++i) {
+    int32_t mask = 0;
+    for (char c : path[i].res) mask |= 1 << label_bit(c);
+    steps[3 * i] = path[i].p;
+    steps[3 * i + 1] = path[i].q;
+    steps[3 * i + 2] = mask;
+  }
+  return FNO_OK;
+}
+
+fno_status fno_contraction_path_cost(const fno_conv_desc* d, fno_op op, int64_t* macs,
+                                     int64_t* peak) {
+  if (!macs || !peak) return FNO_ERR_INVALID_ARGUMENT;
+  std::vector<PStep> path;
+  std::vector<std::string> labs;
+  std::string out;
+  fno_status st = path_for(d, op, &path, &labs, &out);
+  if (st != FNO_OK) return st;
+  Sizes sz = tucker_sizes(d);
+  int64_t total = 0, pk = 0;
+  std::vector<std::string> ops = labs;
+  for (const PStep& ps : path) {
+    std::string both = ops[ps.p] + ops[ps.q];
+    int64_t kred = 1;
+    std::string seen;
+    for (char c : both)
+      if (ps.res.find(c) == std::string::npos && seen.find(c) == std::string::npos) {
+        seen += c;
+        kred *= sz.at(c);
+      }
+    const int64_t rs = label_size(ps.res, sz);
+    total += rs * kred;
+    pk = std::max(pk, rs);
+    std::vector<std::string> next;
+    for (int r = 0; r < (int)ops.size(); ++r)
+      if (r != ps.p && r != ps.q) next.push_back(ops[r]);
+    next.push_back(ps.res);
+    ops.swap(next);
+  }
+  *macs = total;
+  *peak = pk;
+  return FNO_OK;
+}
+
+fno_status fno_spectrum_bytes(const fno_conv_desc* d, int which, size_t* bytes) {
+  fno_status st = check_desc(d);
+  if (st != FNO_OK) return st;
+  if (!bytes || (which != 0 && which != 1)) return FNO_ERR_INVALID_ARGUMENT;
+  const int64_t es = d->precision == FNO_PREC_FP16_TANH ? 2 : 4;
+  const int64_t C = which == 0 ? d->c_in : d->c_out;
+  *bytes = (size_t)(d->batch * C * kmodes(d) * 2 * es);
+  return FNO_OK;
+}
+
+static fno_status ws_query(const fno_conv_desc* d, fno_op op, size_t* bytes, bool caches) {
+  if (!bytes) return FNO_ERR_INVALID_ARGUMENT;
+  if (op != FNO_OP_FWD && op != FNO_OP_BWD_DATA && op != FNO_OP_BWD_WEIGHT)
+    return FNO_ERR_INVALID_ARGUMENT;
+  fno_status st = check_desc(d);
+  if (st != FNO_OK) return st;
+  Plan pl;
+  host_plan(d, &pl);
+  *bytes = ws_bytes(d, &pl, op, caches);
+  return FNO_OK;
+}
+
+fno_status fno_spectral_conv_workspace_size(const fno_conv_desc* d, fno_op op, size_t* bytes) {
+  return ws_query(d, op, bytes, true);
+}
+
+fno_status fno_spectral_conv_workspace_size_nocache(const fno_conv_desc* d, fno_op op,
+                                                    size_t* bytes) {
+  return ws_query(d, op, bytes, false);
+}
+
+fno_status fno_spectral_conv_fwd(const fno_conv_desc* d, const void* x, const fno_weights* w,
+                                 void* y, void* x_hat_out, void* ws, size_t ws_len,
+                                 hipStream_t s) {
+  fno_status st = check_desc(d);
+  if (st != FNO_OK) return st;
+  if (!okptr(x) || !okptr(y)) return FNO_ERR_INVALID_ARGUMENT;
+  if (x_hat_out && !aligned16(x_hat_out)) return FNO_ERR_INVALID_ARGUMENT;
+  if ((st = check_weights(d, w)) != FNO_OK) return st;
+  if ((st = check_ws(d, FNO_OP_FWD, true, ws, ws_len)) != FNO_OK) return st;
+  Plan* pl = nullptr;
+  if ((st = get_plan(d, &pl)) != FNO_OK) return st;
+  const Geo& g = pl->g;
+  WsLayout L;
+  char* base = (char*)ws;
+  char* xs = base + L.add(spec_bytes(g, g.Cin));
+  char* ys = base + L.add(spec_bytes(g, g.Cout));
+  char* inter = base + L.add(std::max(inter3d_bytes(g, g.Cin), inter3d_bytes(g, g.Cout)));
+  char* tsc = base + L.total;
+  void* xh = x_hat_out ? x_hat_out : (void*)xs;
+  const int tanh_on = d->precision == FNO_PREC_FP16_TANH;
+  if ((st = run_r2c(pl, x, xh, inter, g.Cin, tanh_on, 0, s)) != FNO_OK) return st;
+  if (d->weight_kind == FNO_WEIGHT_DENSE) {
+    if ((st = run_contract(pl, xh, w->dense, ys, false, s)) != FNO_OK) return st;
+  } else {
+    if ((st = run_tucker_path(d, pl, false, xh, w, ys, tsc, s)) != FNO_OK) return st;
+  }
+  return run_c2r(pl, ys, y, inter, g.Cout, 1.0f, nullptr, s);
+}
+
+fno_status fno_spectral_conv_bwd_data(const fno_conv_desc* d, const void* x,
+                                      const fno_weights* w, const void* gy, void* gx,
+                                      void* gy_hat_out, void* ws, size_t ws_len,
+                                      hipStream_t s) {
+  fno_status st = check_desc(d);
+  if (st != FNO_OK) return st;
+  const int tanh_on = d->precision == FNO_PREC_FP16_TANH;
+  if (!okptr(gy) || !okptr(gx)) return FNO_ERR_INVALID_ARGUMENT;
+  if (tanh_on && !okptr(x)) return FNO_ERR_INVALID_ARGUMENT;
+  if (gy_hat_out && !aligned16(gy_hat_out)) return FNO_ERR_INVALID_ARGUMENT;
+  if ((st = check_weights(d, w)) != FNO_OK) return st;
+  if ((st = check_ws(d, FNO_OP_BWD_DATA, true, ws, ws_len)) != FNO_OK) return st;
+  Plan* pl = nullptr;
+  if ((st = get_plan(d, &pl)) != FNO_OK) return st;
+  const Geo& g = pl->g;
+  WsLayout L;
+  char* base = (char*)ws;
+  char* gs = base + L.add(spec_bytes(g, g.Cout));
+  char* gxs = base + L.add(spec_bytes(g, g.Cin));
+  char* inter = base + L.add(std::max(inter3d_bytes(g, g.Cin), inter3d_bytes(g, g.Cout)));
+  char* tsc = base + L.total;
+  void* gh = gy_hat_out ? gy_hat_out : (void*)gs;
+  if ((st = run_r2c(pl, gy, gh, inter, g.Cout, 0, 1, s)) != FNO_OK) return st;
+  if (d->weight_kind == FNO_WEIGHT_DENSE) {
+    if ((st = run_contract(pl, gh, w->dense, gxs, true, s)) != FNO_OK) return st;
+  } else {
+    if ((st = run_tucker_path(d, pl, true, gh, w, gxs, tsc, s)) != FNO_OK) return st;
+  }
+  const float sc = (float)(1.0 / std::sqrt((double)g.N));
+  return run_c2r(pl, gxs, gx, inter, g.Cin, sc, tanh_on ? x : nullptr, s);
+}
+
+fno_status fno_spectral_conv_bwd_weight(const fno_conv_desc* d, const void* x, const void* gy,
+                                        const fno_weights* w, const void* x_hat,
+                                        const void* gy_hat, fno_weight_grads* gw, void* ws,
+                                        size_t ws_len, hipStream_t s) {
+  fno_status st = check_desc(d);
+  if (st != FNO_OK) return st;
+  if (!gw) return FNO_ERR_INVALID_ARGUMENT;
+  if (x_hat ? !aligned16(x_hat) : !okptr(x)) return FNO_ERR_INVALID_ARGUMENT;
+  if (gy_hat ? !aligned16(gy_hat) : !okptr(gy)) return FNO_ERR_INVALID_ARGUMENT;
+  const bool tucker = d->weight_kind == FNO_WEIGHT_TUCKER;
+  if (tucker) {
+    if ((st = check_weights(d, w)) != FNO_OK) return st;
+    if (!okptr(gw->core) || !okptr(gw->u_in) || !okptr(gw->u_out))
+      return FNO_ERR_INVALID_ARGUMENT;
+    for (int j = 0; j < d->ndim; ++j)
+      if (!okptr(gw->u_mode[j])) return FNO_ERR_INVALID_ARGUMENT;
+  } else if (!okptr(gw->dense)) {
+    return FNO_ERR_INVALID_ARGUMENT;
+  }
+  const bool caches = x_hat && gy_hat;
+  if ((st = check_ws(d, FNO_OP_BWD_WEIGHT, caches, ws, ws_len)) != FNO_OK) return st;
+  Plan* pl = nullptr;
+  if ((st = get_plan(d, &pl)) != FNO_OK) return st;
+  const Geo& g = pl->g;
+  WsLayout L;
+  char* base = (char*)ws;
+  const void* xh = x_hat;
+  const void* gh = gy_hat;
+  if (!caches) {
+    char* xs = base + L.add(spec_bytes(g, g.Cin));
+    char* gs = base + L.add(spec_bytes(g, g.Cout));
+    char* inter = base + L.add(std::max(inter3d_bytes(g, g.Cin), inter3d_bytes(g, g.Cout)));
+    if (!xh) {
+      if ((st = run_r2c(pl, x, xs, inter, g.Cin, d->precision == FNO_PREC_FP16_TANH, 0, s)) !=
+          FNO_OK)
+        return st;
+      xh = xs;
+    }
+    if (!gh) {
+      if ((st = run_r2c(pl, gy, gs, inter, g.Cout, 0, 1, s)) != FNO_OK) return st;
+      gh = gs;
+    }
+  }
+  char* tsc = base + L.total;
+  if (!tucker) {
+    WgradArgs a{};
+    a.xh = xh;
+    a.gh = gh;
+    a.gw = (float*)gw->dense;
+    a.B = (int)g.B;
+    a.Cin = (int)g.Cin;
+    a.Cout = (int)g.Cout;
+    a.K = (int)g.K;
+    a.Kb = g.Kb;
+    a.Nb = g.Nb;
+    a.scale = (float)std::sqrt((double)g.N);
+    FNO_HIP(timed("wgrad", s, [&] { return launch_wgrad(g.elem, a, s); }));
+    return FNO_OK;
+  }
+  return run_tucker_wgrad(d, pl, xh, gh, w, gw, tsc, s);
+}
+
+fno_status fno_profile_enable(int32_t enable) {
+  std::lock_guard<std::mutex> lk(g_prof_mutex);
+  g_prof_on = enable != 0;
+  return FNO_OK;
+}
+
+fno_status fno_profile_reset(void) {
+  std::lock_guard<std::mutex> lk(g_prof_mutex);
+  prof_drain();
+  g_prof.clear();
+  return FNO_OK;
+}
+
+fno_status fno_profile_read(int32_t index, char* name, int32_t name_cap, int64_t* launches,
+                            double* total_ms) {
+  std::lock_guard<std::mutex> lk(g_prof_mutex);
+  prof_drain();
+  if (index < 0 || index >= (int32_t)g_prof.size()) return FNO_ERR_INVALID_ARGUMENT;
+  const ProfEntry& e = g_prof[index];
+  if (name && name_cap > 0) {
+    std::strncpy(name, e.name.c_str(), (size_t)name_cap - 1);
+    name[name_cap - 1] = 0;
+  }
+  if (launches) *launches = e.launches;
+  if (total_ms) *total_ms = e.total_ms;
+  return FNO_OK;
+}
+
+fno_status fno_release_caches(void) {
+  std::lock_guard<std::mutex> lock(g_mutex);
+  int cur = 0;
+  (void)hipGetDevice(&cur);
+  for (auto& kv : g_plans) {
+    if (kv.second->t.base) {
+      (void)hipSetDevice(kv.second->device);
+      (void)hipFree(kv.second->t.base);
+    }
+  }
+  (void)hipSetDevice(cur);
+  g_plans.clear();
+  return FNO_OK;
+}
+
+}  // extern "C"

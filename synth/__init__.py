@@ -22,7 +22,7 @@ available here).  Recipe (one independent field per (sample, channel)):
 
   * per-mode variance  lam_k = (|k|^2 + 49)^(-5/2), k the folded integer
     wavenumber (k_j - N_j when k_j > N_j / 2);
-  * u = real(ifftn(sqrt(lam) * fftn(w))) with w iid N(0, 1), divided by
+  * u = irfftn(sqrt(lam) * rfftn(w)) with w iid N(0, 1), divided by
     sqrt(mean_k lam_k) so each field has unit expected variance;
   * workload 2 additionally mixes channels, x[b] = M @ g[b] with
     M_ij ~ N(0, 1/Cin);
@@ -38,9 +38,11 @@ round-to-nearest-even (numpy's float16/float32 casts).
 from __future__ import annotations
 
 import dataclasses
+import os
 from typing import Dict, List, Optional, Sequence, Tuple
 
 import numpy as np
+import scipy.fft
 
 STREAM_X, STREAM_W, STREAM_GY, STREAM_M = 0, 1, 2, 3
 
@@ -105,16 +107,22 @@ def grf_variance(n: Sequence[int]) -> np.ndarray:
 
 def grf_fields(rng: np.random.Generator, count: int, n: Sequence[int],
                chunk: int = 64) -> np.ndarray:
-    """`count` independent unit-variance GRFs of shape n, float64 [count, *n]."""
+    """`count` independent unit-variance GRFs of shape n, float64 [count, *n].
+
+    The amplitude sqrt(lam) is even in k, so shaping the half spectrum of the
+    real noise and transforming back gives the real field directly."""
     n = tuple(int(v) for v in n)
     lam = grf_variance(n)
     amp = np.sqrt(lam / lam.mean())
+    amp_half = amp[..., : n[-1] // 2 + 1]
     axes = tuple(range(1, len(n) + 1))
+    workers = os.cpu_count() or 1
     out = np.empty((count,) + n, dtype=np.float64)
     for s in range(0, count, chunk):
         e = min(count, s + chunk)
         w = rng.standard_normal((e - s,) + n)
-        out[s:e] = np.fft.ifftn(np.fft.fftn(w, axes=axes) * amp, axes=axes).real
+        spec = scipy.fft.rfftn(w, axes=axes, workers=workers) * amp_half
+        out[s:e] = scipy.fft.irfftn(spec, s=n, axes=axes, workers=workers)
     return out
 
 

@@ -1,0 +1,86 @@
+"""Shared helpers of the GPU parity tests: seeded inputs, the HIP path through
+the C ABI, and the float64 oracle on the same stored values."""
+from __future__ import annotations
+
+import sys
+
+import numpy as np
+import torch
+
+from oracle import fno_oracle as O
+import synth
+
+TOL = {"fp32": 1e-5, "fp16_tanh": 3e-3}
+
+
+def say(msg: str) -> None:
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+def prec_codes(prec: str):
+    from paper_2307_15034_amd import binding as B
+    if prec == "fp32":
+        return B.FNO_PREC_FP32, np.float32, O.PREC_FP32
+    return B.FNO_PREC_FP16_TANH, np.float16, O.PREC_FP16_TANH
+
+
+def dev(a: np.ndarray) -> torch.Tensor:
+    return torch.from_numpy(np.ascontiguousarray(a)).to("cuda")
+
+
+def host(t: torch.Tensor) -> np.ndarray:
+    return t.detach().to("cpu").numpy()
+
+
+def cplx(pairs: np.ndarray) -> np.ndarray:
+    return synth.pairs_to_complex(pairs)
+
+
+def make_layer(n, modes, batch, c_in, c_out, prec, tucker_rank=None, policy=0):
+    from paper_2307_15034_amd import binding as B
+    from paper_2307_15034_amd.layer import SpectralConv
+    pc, _, _ = prec_codes(prec)
+    kind = B.FNO_WEIGHT_TUCKER if tucker_rank is not None else B.FNO_WEIGHT_DENSE
+    return SpectralConv(n, modes, batch, c_in, c_out, pc, kind, tucker_rank, policy)
+
+
+def run_all(layer, x, w, gy, caches=True):
+    """fwd, bwd_data and bwd_weight on the GPU; returns host arrays."""
+    xd, gyd = dev(x), dev(gy)
+    if isinstance(w, dict):
+        wd = {"core": dev(w["core"]), "u_in": dev(w["u_in"]), "u_out": dev(w["u_out"]),
+              "u_mode": [dev(u) for u in w["u_mode"]]}
+    else:
+        wd = dev(w)
+    xh = layer.spectrum_buffer(0) if caches else None
+    gh = layer.spectrum_buffer(1) if caches else None
+    say(f"  launch fwd n={layer.n} modes={layer.modes} B={layer.batch} "
+        f"C={layer.c_in}->{layer.c_out} caches={caches}")
+    y = layer.fwd(xd, wd, x_hat=xh)
+    say("  launch bwd_data")
+    gx = layer.bwd_data(xd, wd, gyd, gy_hat=gh)
+    say("  launch bwd_weight")
+    if caches:
+        gw = layer.bwd_weight(None, None, wd, x_hat=xh, gy_hat=gh)
+    else:
+        gw = layer.bwd_weight(xd, gyd, wd)
+    torch.cuda.synchronize()
+    say("  done")
+    if isinstance(gw, dict):
+        gwh = {"core": host(gw["core"]), "u_in": host(gw["u_in"]),
+               "u_out": host(gw["u_out"]), "u_mode": [host(u) for u in gw["u_mode"]]}
+    else:
+        gwh = host(gw)
+    return host(y), host(gx), gwh
+
+
+def rel(a, b) -> float:
+    return O.rel_l2(a, b)
+
+
+def gw_complex(gw):
+    if isinstance(gw, dict):
+        return {"core": cplx(gw["core"]), "u_in": cplx(gw["u_in"]),
+                "u_out": cplx(gw["u_out"]), "u_mode": [cplx(u) for u in gw["u_mode"]]}
+    return cplx(gw)

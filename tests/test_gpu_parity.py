@@ -1,0 +1,281 @@
+"""GPU parity: the HIP path (through the C ABI) against the float64 oracle on
+the same seeded stored inputs.
+
+Tolerances (relative L2 over the whole output): 1e-5 in fp32 mode, 3e-3 in
+fp16+tanh mode.  Full-size workloads that the oracle cannot finish in seconds
+are compared on sampled outputs (a batch sample for y and gx; all modes of gW
+with the spectra computed sample by sample).
+"""
+import numpy as np
+import pytest
+
+torch = pytest.importorskip("torch")
+
+pytestmark = [pytest.mark.gpu,
+              pytest.mark.skipif(not torch.cuda.is_available(), reason="needs a GPU")]
+
+from oracle import fno_oracle as O  # noqa: E402
+import synth  # noqa: E402
+from tests import gpu_util as U  # noqa: E402
+
+PRECS = ["fp32", "fp16_tanh"]
+
+
+def test_native_library_loaded():
+    import os
+    from paper_2307_15034_amd import binding as B
+    here = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    assert os.path.realpath(B.LIB_PATH).startswith(os.path.realpath(here))
+    assert B.lib()._name == B.LIB_PATH
+
+
+def _oracle_dense(x, w, gy, n, modes, oprec):
+    wc = U.cplx(w)
+    y = O.fwd(x, wc, n, modes, oprec)
+    gx = O.bwd_data(x, wc, gy, n, modes, oprec)
+    gw = O.bwd_weight(x, gy, n, modes, oprec)
+    return y, gx, gw
+
+
+def _assert_close(name, got, ref, prec):
+    r = U.rel(got, ref)
+    U.say(f"  {name}: rel_l2 = {r:.3e} (tol {U.TOL[prec]:.0e})")
+    assert np.isfinite(r) and r <= U.TOL[prec], f"{name}: {r:.3e}"
+
+
+EDGE = [
+    # (n, modes, B, Cin, Cout)
+    ((20, 24), (3, 5), 3, 5, 7),        # ragged tiles, K = 30 (scalar mode path)
+    ((12, 18), (2, 10), 2, 3, 4),       # Nyquist retained, row length not a multiple of 8
+    ((8, 6), (4, 4), 2, 3, 3),          # every mode retained
+    ((96,), (17,), 2, 3, 5),            # 1-D
+    ((6, 10, 12), (2, 3, 4), 2, 3, 2),  # 3-D, ragged
+    ((32, 32), (5, 7), 37, 33, 18),     # batch / channels past the 32-wide tiles
+    ((1000, 40), (6, 9), 1, 2, 3),      # several row chunks, rows not a multiple of 32
+    ((16, 256), (8, 100), 1, 2, 2),     # 100 retained last-axis modes (widest tile)
+    ((64, 64), (32, 33), 1, 2, 2),      # 64 leading-axis slots, Nyquist
+]
+
+
+@pytest.mark.parametrize("prec", PRECS)
+@pytest.mark.parametrize("case", range(len(EDGE)))
+def test_dense_edge_cases(case, prec):
+    n, modes, Bt, ci, co = EDGE[case]
+    _, npdt, oprec = U.prec_codes(prec)
+    U.say(f"edge case {case}: n={n} modes={modes} B={Bt} Cin={ci} Cout={co} {prec}")
+    x, w, gy = synth.random_dense_case(case, Bt, ci, co, n, modes, npdt)
+    layer = U.make_layer(n, modes, Bt, ci, co, prec)
+    y, gx, gw = U.run_all(layer, x, w, gy)
+    ry, rgx, rgw = _oracle_dense(x, w, gy, n, modes, oprec)
+    _assert_close("y", y, ry, prec)
+    _assert_close("gx", gx, rgx, prec)
+    _assert_close("gW", U.cplx(gw), rgw, prec)
+
+
+_CACHE = {}
+
+
+def _workload_inputs(wid, prec, batch=None):
+    key = (wid, prec, batch)
+    if key not in _CACHE:
+        wl = synth.WORKLOADS[wid]
+        _, npdt, _ = U.prec_codes(prec)
+        x = synth.make_x(wl, npdt, batch)
+        gy = synth.make_gy(wl, npdt, batch)
+        if wl.weight == "tucker":
+            w = synth.make_tucker_weight(wl, npdt)
+        else:
+            w = synth.make_dense_weight(wl, npdt)
+        _CACHE.clear()
+        _CACHE[key] = (x, w, gy)
+    return _CACHE[key]
+
+
+@pytest.mark.parametrize("prec", PRECS)
+@pytest.mark.parametrize("wid", [1, 2, 4])
+def test_workload_dense_full(wid, prec):
+    wl = synth.WORKLOADS[wid]
+    _, _, oprec = U.prec_codes(prec)
+    U.say(f"workload {wid} {wl.name} {prec}")
+    x, w, gy = _workload_inputs(wid, prec)
+    layer = U.make_layer(wl.n, wl.modes, wl.batch, wl.c_in, wl.c_out, prec)
+    y, gx, gw = U.run_all(layer, x, w, gy)
+    ry, rgx, rgw = _oracle_dense(x, w, gy, wl.n, wl.modes, oprec)
+    _assert_close("y", y, ry, prec)
+    _assert_close("gx", gx, rgx, prec)
+    _assert_close("gW", U.cplx(gw), rgw, prec)
+
+
+def _spectra_by_sample(x, gy, n, modes, oprec):
+    xs = np.concatenate([O.forward_spectrum(O.preactivation(x[b:b + 1], oprec), n, modes)
+                         for b in range(x.shape[0])])
+    gs = np.concatenate([O.grad_spectrum(gy[b:b + 1], n, modes) for b in range(gy.shape[0])])
+    return xs, gs
+
+
+@pytest.mark.parametrize("prec", PRECS)
+def test_workload_hires_sampled(prec):
+    """1024^2 workload at full size: y and gx of batch sample 0 and two output
+    channels compared with the oracle; gW compared over every mode."""
+    wid = 3
+    wl = synth.WORKLOADS[wid]
+    _, _, oprec = U.prec_codes(prec)
+    U.say(f"workload {wid} {wl.name} {prec}")
+    x, w, gy = _workload_inputs(wid, prec)
+    layer = U.make_layer(wl.n, wl.modes, wl.batch, wl.c_in, wl.c_out, prec)
+    y, gx, gw = U.run_all(layer, x, w, gy)
+    wc = U.cplx(w)
+    ry0 = O.fwd(x[0:1], wc, wl.n, wl.modes, oprec)
+    _assert_close("y[b=0]", y[0:1], ry0, prec)
+    rgx0 = O.bwd_data(x[0:1], wc, gy[0:1], wl.n, wl.modes, oprec)
+    _assert_close("gx[b=0]", gx[0:1], rgx0, prec)
+    xs, gs = _spectra_by_sample(x, gy, wl.n, wl.modes, oprec)
+    rgw = np.einsum("bi...,bo...->io...", np.conj(xs), gs)
+    _assert_close("gW", U.cplx(gw), rgw, prec)
+
+
+@pytest.mark.parametrize("policy", ["min_result", "min_net"])
+@pytest.mark.parametrize("prec", PRECS)
+def test_workload_tucker(prec, policy):
+    """Tucker workload at full size: y and gx of batch sample 0; the core and
+    factor gradients from all samples."""
+    wid = 5
+    wl = synth.WORKLOADS[wid]
+    _, _, oprec = U.prec_codes(prec)
+    U.say(f"workload {wid} {wl.name} {prec} {policy}")
+    x, w, gy = _workload_inputs(wid, prec)
+    pol = 0 if policy == "min_result" else 1
+    layer = U.make_layer(wl.n, wl.modes, wl.batch, wl.c_in, wl.c_out, prec, wl.rank, pol)
+    y, gx, gw = U.run_all(layer, x, w, gy)
+    core, u_in, u_out = U.cplx(w["core"]), U.cplx(w["u_in"]), U.cplx(w["u_out"])
+    u_mode = [U.cplx(u) for u in w["u_mode"]]
+    ry0 = O.tucker_fwd(x[0:1], core, u_in, u_out, u_mode, wl.n, wl.modes, oprec, policy)
+    _assert_close("y[b=0]", y[0:1], ry0, prec)
+    rgx0 = O.tucker_bwd_data(x[0:1], core, u_in, u_out, u_mode, gy[0:1], wl.n, wl.modes,
+                             oprec, policy)
+    _assert_close("gx[b=0]", gx[0:1], rgx0, prec)
+    g_core, g_in, g_out, g_mode = O.tucker_bwd_weight(x, gy, core, u_in, u_out, u_mode,
+                                                      wl.n, wl.modes, oprec)
+    gwc = U.gw_complex(gw)
+    _assert_close("g_core", gwc["core"], g_core, prec)
+    _assert_close("g_u_in", gwc["u_in"], g_in, prec)
+    _assert_close("g_u_out", gwc["u_out"], g_out, prec)
+    for j in range(wl.ndim):
+        _assert_close(f"g_u_mode{j}", gwc["u_mode"][j], g_mode[j], prec)
+
+
+TUCKER_EDGE = [
+    ((8, 8), (2, 3), 2, 3, 4, (2, 3, 2, 2)),
+    ((6, 10, 12), (2, 3, 4), 2, 3, 2, (2, 2, 2, 3, 2)),
+    ((40,), (7,), 3, 2, 5, (3, 2, 4)),
+]
+
+
+@pytest.mark.parametrize("policy", ["min_result", "min_net"])
+@pytest.mark.parametrize("prec", PRECS)
+@pytest.mark.parametrize("case", range(len(TUCKER_EDGE)))
+def test_tucker_edge_cases(case, prec, policy):
+    n, modes, Bt, ci, co, rank = TUCKER_EDGE[case]
+    _, npdt, oprec = U.prec_codes(prec)
+    U.say(f"tucker edge {case}: n={n} modes={modes} rank={rank} {prec} {policy}")
+    rng = np.random.default_rng(np.random.SeedSequence([2000 + case]))
+    d = len(n)
+    kd = tuple(2 * m if j < d - 1 else m for j, m in enumerate(modes))
+
+    def cp(shape, std):
+        return (rng.standard_normal(tuple(shape) + (2,)) * std).astype(npdt)
+
+    w = {"core": cp(rank, 0.5), "u_in": cp((ci, rank[0]), 0.5),
+         "u_out": cp((co, rank[1]), 0.5),
+         "u_mode": [cp((kd[j], rank[2 + j]), 0.5) for j in range(d)]}
+    x = rng.standard_normal((Bt, ci) + n).astype(npdt)
+    gy = rng.standard_normal((Bt, co) + n).astype(npdt)
+    pol = 0 if policy == "min_result" else 1
+    layer = U.make_layer(n, modes, Bt, ci, co, prec, rank, pol)
+    y, gx, gw = U.run_all(layer, x, w, gy)
+    core, u_in, u_out = U.cplx(w["core"]), U.cplx(w["u_in"]), U.cplx(w["u_out"])
+    u_mode = [U.cplx(u) for u in w["u_mode"]]
+    _assert_close("y", y, O.tucker_fwd(x, core, u_in, u_out, u_mode, n, modes, oprec, policy),
+                  prec)
+    _assert_close("gx", gx, O.tucker_bwd_data(x, core, u_in, u_out, u_mode, gy, n, modes,
+                                               oprec, policy), prec)
+    g_core, g_in, g_out, g_mode = O.tucker_bwd_weight(x, gy, core, u_in, u_out, u_mode, n,
+                                                      modes, oprec)
+    gwc = U.gw_complex(gw)
+    _assert_close("g_core", gwc["core"], g_core, prec)
+    _assert_close("g_u_in", gwc["u_in"], g_in, prec)
+    _assert_close("g_u_out", gwc["u_out"], g_out, prec)
+    for j in range(d):
+        _assert_close(f"g_u_mode{j}", gwc["u_mode"][j], g_mode[j], prec)
+
+
+# ---------------------------------------------------------------------------
+# Invariants
+# ---------------------------------------------------------------------------
+
+def test_identity_round_trip_fp32():
+    """Identity weights with every mode retained reproduce x (fp32 mode)."""
+    n, modes = (16, 12), (8, 7)
+    c = 4
+    U.say("identity round trip")
+    rng = np.random.default_rng(3)
+    x = rng.standard_normal((2, c) + n).astype(np.float32)
+    w = np.zeros((c, c, 16, 7, 2), dtype=np.float32)
+    for i in range(c):
+        w[i, i, :, :, 0] = 1.0
+    layer = U.make_layer(n, modes, 2, c, c, "fp32")
+    y = U.host(layer.fwd(U.dev(x), U.dev(w)))
+    assert np.abs(y - x).max() < 1e-5
+
+
+@pytest.mark.parametrize("prec", PRECS)
+def test_deterministic_repeat(prec):
+    """Two runs give bitwise-identical outputs (fixed reduction order)."""
+    n, modes, Bt, ci, co = (32, 32), (5, 7), 37, 33, 18
+    _, npdt, _ = U.prec_codes(prec)
+    U.say(f"determinism {prec}")
+    x, w, gy = synth.random_dense_case(77, Bt, ci, co, n, modes, npdt)
+    layer = U.make_layer(n, modes, Bt, ci, co, prec)
+    a = U.run_all(layer, x, w, gy)
+    b = U.run_all(layer, x, w, gy)
+    for u, v in zip(a, b):
+        assert np.array_equal(u, v)
+
+
+@pytest.mark.parametrize("prec", PRECS)
+def test_caches_match_recompute(prec):
+    n, modes, Bt, ci, co = (20, 24), (3, 5), 3, 5, 7
+    _, npdt, _ = U.prec_codes(prec)
+    U.say(f"caches vs recompute {prec}")
+    x, w, gy = synth.random_dense_case(78, Bt, ci, co, n, modes, npdt)
+    layer = U.make_layer(n, modes, Bt, ci, co, prec)
+    a = U.run_all(layer, x, w, gy, caches=True)
+    b = U.run_all(layer, x, w, gy, caches=False)
+    for u, v in zip(a, b):
+        assert np.array_equal(u, v)
+
+
+def test_fp16_extremes_stay_finite():
+    """tanh bounds the transform input: +-65504 and +-inf give finite outputs
+    that still match the oracle."""
+    n, modes, Bt, ci, co = (32, 32), (4, 5), 2, 3, 3
+    U.say("fp16 extremes")
+    x, w, gy = synth.random_dense_case(79, Bt, ci, co, n, modes, np.float16, x_scale=3.0)
+    x[0, 0, 0, :4] = np.array([65504.0, -65504.0, np.inf, -np.inf], dtype=np.float16)
+    layer = U.make_layer(n, modes, Bt, ci, co, "fp16_tanh")
+    y, gx, gw = U.run_all(layer, x, w, gy)
+    assert np.isfinite(y).all() and np.isfinite(gx).all() and np.isfinite(gw).all()
+    ry, rgx, rgw = _oracle_dense(x, w, gy, n, modes, O.PREC_FP16_TANH)
+    _assert_close("y", y, ry, "fp16_tanh")
+    _assert_close("gW", U.cplx(gw), rgw, "fp16_tanh")
+
+
+def test_nan_propagates():
+    n, modes, Bt, ci, co = (32, 32), (4, 5), 2, 3, 3
+    U.say("nan propagation")
+    x, w, gy = synth.random_dense_case(80, Bt, ci, co, n, modes, np.float16)
+    x[0, 1, 5, 7] = np.nan
+    layer = U.make_layer(n, modes, Bt, ci, co, "fp16_tanh")
+    y = U.host(layer.fwd(U.dev(x), U.dev(w)))
+    assert np.isnan(y[0]).any()
+    assert np.isfinite(y[1]).all()
