@@ -79,6 +79,18 @@ __device__ __forceinline__ _Float16 from_f<_Float16>(float v) { return (_Float16
 template <>
 __device__ __forceinline__ float from_f<float>(float v) { return v; }
 
+// One complex value written as a single 4-byte (fp16) or 8-byte (fp32) store.
+template <typename T>
+__device__ __forceinline__ void store_pair(T* d, float re, float im);
+template <>
+__device__ __forceinline__ void store_pair<_Float16>(_Float16* d, float re, float im) {
+  *reinterpret_cast<h2*>(d) = h2{to_h(re), to_h(im)};
+}
+template <>
+__device__ __forceinline__ void store_pair<float>(float* d, float re, float im) {
+  *reinterpret_cast<f2*>(d) = f2{re, im};
+}
+
 // Make LDS writes of one lane visible to the other lanes of its wavefront.
 __device__ __forceinline__ void wave_lds_sync() {
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
@@ -227,9 +239,8 @@ __global__ __launch_bounds__(256) void r2c_plane_kernel(R2CArgs a) {
         for (int i = 0; i < 4; ++i) {
           const int t_a = ta * 16 + 4 * g + i;
           if (t_a < a.Ka && t_b < a.Kb) {
-            T* o = out + ((int64_t)t_a * a.Kb + t_b) * 2;
-            o[0] = from_f<T>(accR[q][tb][i] * a.scaleB);
-            o[1] = from_f<T>(accI[q][tb][i] * a.scaleB);
+            store_pair<T>(out + ((int64_t)t_a * a.Kb + t_b) * 2, accR[q][tb][i] * a.scaleB,
+                          accI[q][tb][i] * a.scaleB);
           }
         }
       }
@@ -401,19 +412,20 @@ __global__ __launch_bounds__(256) void c2r_plane_kernel(C2RArgs a) {
         f4 acc[4];
 #pragma unroll
         for (int c = 0; c < 4; ++c) acc[c] = f4zero();
+        // D = y^T tile: row n_b (4 consecutive per lane), column n_a
         for (int k0 = 0; k0 < 2 * Kbp; k0 += KS) {
           frag vf = M::ld(VL + (rt * 16 + r16) * ldV + k0 + g * KPL);
 #pragma unroll
           for (int c = 0; c < 4; ++c) {
             const int ct = cg * 4 + c;
             frag tf = M::ld(twI + (int64_t)(ct * 16 + r16) * (2 * Kbp) + k0 + g * KPL);
-            acc[c] = M::mma(vf, tf, acc[c]);
+            acc[c] = M::mma(tf, vf, acc[c]);
           }
         }
+        // one 16-byte store per tile: obuf[n_a][n_b .. n_b + 3]
 #pragma unroll
         for (int c = 0; c < 4; ++c)
-#pragma unroll
-          for (int i = 0; i < 4; ++i) obuf[(4 * g + i) * 68 + c * 16 + r16] = acc[c][i];
+          *reinterpret_cast<f4*>(obuf + r16 * 68 + c * 16 + 4 * g) = acc[c];
         wave_lds_sync();
         const int orow = lane >> 2;
         const int ocol = (lane & 3) * 16;
@@ -521,9 +533,8 @@ __global__ __launch_bounds__(256) void axis_kernel(AxisArgs a) {
         for (int i = 0; i < 4; ++i) {
           const int t = tt * 16 + 4 * g + i;
           if (t < a.Lout && j < a.inner) {
-            T* d = out + ((int64_t)t * a.inner + j) * 2;
-            d[0] = from_f<T>(accR[u][i] * a.scale);
-            d[1] = from_f<T>(accI[u][i] * a.scale);
+            store_pair<T>(out + ((int64_t)t * a.inner + j) * 2, accR[u][i] * a.scale,
+                          accI[u][i] * a.scale);
           }
         }
       }
@@ -678,9 +689,7 @@ __global__ __launch_bounds__(256) void contract_kernel(ContractArgs a) {
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int bb = bt * 16 + 4 * g + i, pp = pt * 16 + r16;
-      T* d = so + ((bb * CT_PB + pp) * CT_TM + m) * 2;
-      d[0] = from_f<T>(accR[m][i] * s);
-      d[1] = from_f<T>(accI[m][i] * s);
+      store_pair<T>(so + ((bb * CT_PB + pp) * CT_TM + m) * 2, accR[m][i] * s, accI[m][i] * s);
     }
   }
   __syncthreads();
@@ -792,9 +801,7 @@ __global__ __launch_bounds__(256) void wgrad_kernel(WgradArgs a) {
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int qq = qt * 16 + 4 * g + i, pp = pt * 16 + r16;
-      float* d = so + ((qq * PB + pp) * TM + m) * 2;
-      d[0] = accR[m][i] * s;
-      d[1] = accI[m][i] * s;
+      store_pair<float>(so + ((qq * PB + pp) * TM + m) * 2, accR[m][i] * s, accI[m][i] * s);
     }
   }
   __syncthreads();
@@ -877,14 +884,27 @@ __global__ void scale_kernel(float* p, int64_t n, float s) {
 // ---------------------------------------------------------------------------
 // Launchers
 // ---------------------------------------------------------------------------
+// Dynamic LDS above 64 KiB has to be opted into per kernel.
+static hipError_t allow_lds(const void* kern, size_t lds) {
+  if (lds <= 65536) return hipSuccess;
+  if (lds > 160 * 1024) return hipErrorInvalidValue;
+  return hipFuncSetAttribute(kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+}
+
+#define FNO_LAUNCH(kern, grid, block, lds, s, args)                              \
+  do {                                                                           \
+    hipError_t e_ = allow_lds(reinterpret_cast<const void*>(&kern), lds);        \
+    if (e_ != hipSuccess) return e_;                                             \
+    hipLaunchKernelGGL(kern, grid, block, lds, s, args);                         \
+  } while (0)
 template <typename T>
 static hipError_t r2c_dispatch(int nct, const R2CArgs& a, size_t lds, hipStream_t s) {
   dim3 grid((unsigned)a.planes), block(256);
   switch (nct) {
-    case 2: hipLaunchKernelGGL((r2c_plane_kernel<T, 2>), grid, block, lds, s, a); break;
-    case 4: hipLaunchKernelGGL((r2c_plane_kernel<T, 4>), grid, block, lds, s, a); break;
-    case 8: hipLaunchKernelGGL((r2c_plane_kernel<T, 8>), grid, block, lds, s, a); break;
-    case 16: hipLaunchKernelGGL((r2c_plane_kernel<T, 16>), grid, block, lds, s, a); break;
+    case 2: FNO_LAUNCH((r2c_plane_kernel<T, 2>), grid, block, lds, s, a); break;
+    case 4: FNO_LAUNCH((r2c_plane_kernel<T, 4>), grid, block, lds, s, a); break;
+    case 8: FNO_LAUNCH((r2c_plane_kernel<T, 8>), grid, block, lds, s, a); break;
+    case 16: FNO_LAUNCH((r2c_plane_kernel<T, 16>), grid, block, lds, s, a); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
@@ -899,10 +919,10 @@ template <typename T>
 static hipError_t c2r_dispatch(int nct, const C2RArgs& a, size_t lds, hipStream_t s) {
   dim3 grid((unsigned)a.planes), block(256);
   switch (nct) {
-    case 2: hipLaunchKernelGGL((c2r_plane_kernel<T, 2>), grid, block, lds, s, a); break;
-    case 4: hipLaunchKernelGGL((c2r_plane_kernel<T, 4>), grid, block, lds, s, a); break;
-    case 8: hipLaunchKernelGGL((c2r_plane_kernel<T, 8>), grid, block, lds, s, a); break;
-    case 16: hipLaunchKernelGGL((c2r_plane_kernel<T, 16>), grid, block, lds, s, a); break;
+    case 2: FNO_LAUNCH((c2r_plane_kernel<T, 2>), grid, block, lds, s, a); break;
+    case 4: FNO_LAUNCH((c2r_plane_kernel<T, 4>), grid, block, lds, s, a); break;
+    case 8: FNO_LAUNCH((c2r_plane_kernel<T, 8>), grid, block, lds, s, a); break;
+    case 16: FNO_LAUNCH((c2r_plane_kernel<T, 16>), grid, block, lds, s, a); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
@@ -916,9 +936,9 @@ hipError_t launch_c2r(int elem, int nct, const C2RArgs& a, size_t lds, hipStream
 hipError_t launch_axis(int elem, const AxisArgs& a, size_t lds, hipStream_t s) {
   dim3 grid((unsigned)((a.inner + 63) / 64), (unsigned)a.outer), block(256);
   if (elem == ELEM_F16)
-    hipLaunchKernelGGL((axis_kernel<_Float16>), grid, block, lds, s, a);
+    FNO_LAUNCH((axis_kernel<_Float16>), grid, block, lds, s, a);
   else
-    hipLaunchKernelGGL((axis_kernel<float>), grid, block, lds, s, a);
+    FNO_LAUNCH((axis_kernel<float>), grid, block, lds, s, a);
   return hipGetLastError();
 }
 
