@@ -54,15 +54,14 @@ def kernel_bytes(wl, es):
     spec_out = B * Co * K * 2 * es
     W = Ci * Co * K * 2 * es
     out = {
-        "r2c_plane": None,  # depends on the channel count; resolved per launch below
         "contract": spec_in + W + spec_out,
         "contract_adjoint": spec_out + W + spec_in,
         "c2r_plane": spec_out + B * Co * N * es,
         "c2r_plane_tanh_grad": spec_in + 2 * B * Ci * N * es,
         "wgrad": spec_in + spec_out + Ci * Co * K * 2 * 4,
     }
-    # r2c runs once on x (Cin channels) and once on gy (Cout channels)
-    out["r2c_plane"] = ((B * Ci * N * es + spec_in) + (B * Co * N * es + spec_out)) / 2
+    out["r2c_plane_tanh"] = B * Ci * N * es + spec_in     # input transform (tanh)
+    out["r2c_plane"] = B * Co * N * es + spec_out         # gradient transform
     return out
 
 

@@ -1,0 +1,249 @@
+// Device-side helpers shared by the HIP kernels of the FNO spectral
+// convolution (gfx950): MFMA operand types, conversions, LDS synchronisation,
+// and the staging helpers of the mode-indexed tensors.
+//
+// MFMA 16x16 operand layout used throughout (wave64, lane l, g = l / 16):
+//   A (16 x KSTEP): lane holds A[l % 16][g*KPL .. g*KPL+KPL-1]
+//   B (KSTEP x 16): lane holds B[g*KPL .. g*KPL+KPL-1][l % 16]
+//   D (16 x 16)   : lane holds D[4*g + i][l % 16], i = 0..3
+// The k-ordering within a step only has to agree between A and B.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "fno_internal.h"
+
+namespace fno {
+
+typedef _Float16 h8 __attribute__((ext_vector_type(8)));
+typedef _Float16 h4 __attribute__((ext_vector_type(4)));
+typedef _Float16 h2 __attribute__((ext_vector_type(2)));
+typedef float f4 __attribute__((ext_vector_type(4)));
+typedef float f2 __attribute__((ext_vector_type(2)));
+
+template <typename T>
+struct MM;
+
+template <>
+struct MM<_Float16> {
+  static constexpr int KPL = 8;
+  static constexpr int KSTEP = 32;
+  typedef h8 frag;
+  static __device__ __forceinline__ f4 mma(const frag& a, const frag& b, const f4& c) {
+    return __builtin_amdgcn_mfma_f32_16x16x32_f16(a, b, c, 0, 0, 0);
+  }
+  static __device__ __forceinline__ frag zero() {
+    frag z;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) z[i] = (_Float16)0.0f;
+    return z;
+  }
+  static __device__ __forceinline__ frag ld(const _Float16* p) {
+    return *reinterpret_cast<const frag*>(p);
+  }
+  static __device__ __forceinline__ frag neg(const frag& a) { return -a; }
+};
+
+template <>
+struct MM<float> {
+  static constexpr int KPL = 1;
+  static constexpr int KSTEP = 4;
+  typedef float frag;
+  static __device__ __forceinline__ f4 mma(const frag& a, const frag& b, const f4& c) {
+    return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
+  }
+  static __device__ __forceinline__ frag zero() { return 0.0f; }
+  static __device__ __forceinline__ frag ld(const float* p) { return *p; }
+  static __device__ __forceinline__ frag neg(const frag& a) { return -a; }
+};
+
+__device__ __forceinline__ f4 f4zero() { return f4{0.0f, 0.0f, 0.0f, 0.0f}; }
+
+// tanh in fp32 through the device math library (rounds correctly to fp16 for
+// every fp16 input; limits +-1 at +-inf, NaN propagates).
+__device__ __forceinline__ float tanh_f32(float x) { return tanhf(x); }
+
+// Round-to-nearest-even conversions to the storage type.
+__device__ __forceinline__ _Float16 to_h(float v) { return (_Float16)v; }
+
+template <typename T>
+__device__ __forceinline__ T from_f(float v);
+template <>
+__device__ __forceinline__ _Float16 from_f<_Float16>(float v) { return (_Float16)v; }
+template <>
+__device__ __forceinline__ float from_f<float>(float v) { return v; }
+
+// One complex value written as a single 4-byte (fp16) or 8-byte (fp32) store.
+template <typename T>
+__device__ __forceinline__ void store_pair(T* d, float re, float im);
+template <>
+__device__ __forceinline__ void store_pair<_Float16>(_Float16* d, float re, float im) {
+  *reinterpret_cast<h2*>(d) = h2{to_h(re), to_h(im)};
+}
+template <>
+__device__ __forceinline__ void store_pair<float>(float* d, float re, float im) {
+  *reinterpret_cast<f2*>(d) = f2{re, im};
+}
+
+// Work-groups are dispatched round-robin over the 8 XCDs (each with its own
+// L2): physical block b runs on XCD b % 8.  Returns a logical block id such
+// that consecutive logical ids sit on the same XCD and are dispatched one
+// after the other, so neighbouring tiles that share cache lines share an L2.
+__device__ __forceinline__ int xcd_logical_block(int b, int nblocks) {
+  constexpr int NX = 8;
+  const int full = nblocks - nblocks % NX;
+  if (b >= full) return b;
+  return (b % NX) * (full / NX) + b / NX;
+}
+
+// Make LDS writes of one lane visible to the other lanes of its wavefront.
+__device__ __forceinline__ void wave_lds_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+// ---------------------------------------------------------------------------
+// Input fragment of step A: KPL consecutive row elements, optional tanh.
+// ---------------------------------------------------------------------------
+template <typename T>
+__device__ __forceinline__ typename MM<T>::frag load_row_frag(const T* row, int n0, int Nb,
+                                                              bool vrow, int do_tanh,
+                                                              int vec);
+
+template <>
+__device__ __forceinline__ h8 load_row_frag<_Float16>(const _Float16* row, int n0, int Nb,
+                                                      bool vrow, int do_tanh, int vec) {
+  h8 v = MM<_Float16>::zero();
+  if (vrow) {
+    if (vec) {
+      if (n0 < Nb) v = *reinterpret_cast<const h8*>(row + n0);
+    } else {
+#pragma unroll
+      for (int i = 0; i < 8; ++i)
+        if (n0 + i < Nb) v[i] = row[n0 + i];
+    }
+    if (do_tanh) {
+#pragma unroll
+      for (int i = 0; i < 8; ++i) v[i] = to_h(tanh_f32((float)v[i]));
+    }
+  }
+  return v;
+}
+
+template <>
+__device__ __forceinline__ float load_row_frag<float>(const float* row, int n0, int Nb,
+                                                      bool vrow, int do_tanh, int vec) {
+  float v = 0.0f;
+  if (vrow && n0 < Nb) {
+    v = row[n0];
+    if (do_tanh) v = tanh_f32(v);
+  }
+  return v;
+}
+
+// ---------------------------------------------------------------------------
+// Shared pieces of the per-mode contraction and the weight gradient.
+//
+// Spectra and weights keep the mode index t innermost, so a 16-byte load
+// holds CPL consecutive modes of one (row, channel) pair.  The MFMA reduction
+// runs over a channel (or batch) index, so tiles are staged in LDS with that
+// index innermost: each thread loads 4 rows x CPL modes and writes, per mode,
+// the real and the imaginary parts of the 4 rows as one 8- or 16-byte LDS
+// store (a 4 x CPL transpose done with register moves only).
+// ---------------------------------------------------------------------------
+constexpr int CT_TM = 8;   // modes per tile
+constexpr int CT_PB = 32;  // output channels per tile
+constexpr int CT_BB = 32;  // batch rows per tile
+
+__device__ __forceinline__ float cmult(int t, int Kb, int Nb) {
+  const int tb = t % Kb;
+  return (tb == 0 || 2 * tb == Nb) ? 1.0f : 2.0f;
+}
+
+typedef unsigned int u32;
+typedef u32 u32x4 __attribute__((ext_vector_type(4)));
+typedef u32 u32x2 __attribute__((ext_vector_type(2)));
+
+template <typename T>
+struct CplxIO {
+  static constexpr int CPL = 16 / (2 * (int)sizeof(T));  // complex values per 16 bytes
+};
+
+// 16 bytes of one row starting at mode t (CPL complex values); modes past K
+// (or a row outside the tile) read as zero.  VEC: K is a multiple of CPL, so a
+// full 16-byte load stays inside the row; the load is then issued
+// unconditionally, out-of-range lanes reading from `zeros` (a zero block), so
+// the loaded value needs no fix-up and the wait can sit at its first use.
+template <typename T, bool VEC>
+__device__ __forceinline__ u32x4 load_modes16(const T* zeros, const T* row, int t, int K,
+                                              bool valid) {
+  constexpr int CPL = CplxIO<T>::CPL;
+  if constexpr (VEC) {
+    const bool ok = valid && t < K;
+    const T* p = ok ? row + 2 * t : zeros;
+    return *reinterpret_cast<const u32x4*>(p);
+  } else {
+    u32x4 v = {0u, 0u, 0u, 0u};
+    if (!valid) return v;
+    const u32* r = reinterpret_cast<const u32*>(row);
+    constexpr int WPC = 2 * sizeof(T) / 4;  // 32-bit words per complex value
+#pragma unroll
+    for (int c = 0; c < CPL; ++c)
+      if (t + c < K)
+#pragma unroll
+        for (int w = 0; w < WPC; ++w) v[c * WPC + w] = r[(size_t)(t + c) * WPC + w];
+    return v;
+  }
+}
+
+// From four 16-byte loads (rows r..r+3, modes m0..m0+CPL-1) write, for every
+// mode m, re(rows r..r+3) to dre + m*mstride and im(...) to dim + m*mstride.
+// neg_im flips the sign of the imaginary parts (conjugation).
+template <typename T>
+__device__ __forceinline__ void scatter4(const u32x4 (&L)[4], T* dre, T* dim, int mstride,
+                                         bool neg_im);
+
+template <>
+__device__ __forceinline__ void scatter4<_Float16>(const u32x4 (&L)[4], _Float16* dre,
+                                                   _Float16* dim, int mstride, bool neg_im) {
+  const u32 sign = neg_im ? 0x80008000u : 0u;
+#pragma unroll
+  for (int m = 0; m < 4; ++m) {
+    // dword = (re lo | im hi) of one complex; gather the low / high halves
+    u32x2 re, im;
+    re[0] = __builtin_amdgcn_perm(L[1][m], L[0][m], 0x05040100u);
+    re[1] = __builtin_amdgcn_perm(L[3][m], L[2][m], 0x05040100u);
+    im[0] = __builtin_amdgcn_perm(L[1][m], L[0][m], 0x07060302u) ^ sign;
+    im[1] = __builtin_amdgcn_perm(L[3][m], L[2][m], 0x07060302u) ^ sign;
+    *reinterpret_cast<u32x2*>(dre + m * mstride) = re;
+    *reinterpret_cast<u32x2*>(dim + m * mstride) = im;
+  }
+}
+
+template <>
+__device__ __forceinline__ void scatter4<float>(const u32x4 (&L)[4], float* dre, float* dim,
+                                                int mstride, bool neg_im) {
+  const u32 sign = neg_im ? 0x80000000u : 0u;
+#pragma unroll
+  for (int m = 0; m < 2; ++m) {
+    u32x4 re, im;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      re[j] = L[j][2 * m];
+      im[j] = L[j][2 * m + 1] ^ sign;
+    }
+    *reinterpret_cast<u32x4*>(dre + m * mstride) = re;
+    *reinterpret_cast<u32x4*>(dim + m * mstride) = im;
+  }
+}
+
+// Asynchronous-friendly block barrier for LDS only: waits for this wave's
+// LDS operations, not for outstanding global loads (prefetches stay in flight).
+__device__ __forceinline__ void block_sync_lds() {
+  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
+
+
+}  // namespace fno

@@ -16,6 +16,7 @@ enum Elem { ELEM_F32 = 0, ELEM_F16 = 1 };
 struct R2CArgs {
   const void* in;
   void* out;
+  const void* zeros;  // >= 256 zero bytes: target of out-of-range lanes' loads
   const void* twA;  // [2*Kbp][Nbp]: rows t < Kbp: cos(2 pi t n / Nb), rows Kbp+t: -sin
   const void* cB;   // [Kap16][Nap]: cos(2 pi k_a(t) n / Na)
   const void* sB;   // [Kap16][Nap]: sin(2 pi k_a(t) n / Na)
@@ -37,6 +38,7 @@ struct R2CArgs {
 struct C2RArgs {
   const void* in;
   void* out;
+  const void* zeros;  // >= 256 zero bytes: target of out-of-range lanes' loads
   const void* x;    // epilogue input or null
   const void* cI;   // [Nap][Kap]: cos(2 pi k_a(t) n / Na)   (row n, col t)
   const void* sI;   // [Nap][Kap]: sin(2 pi k_a(t) n / Na)
@@ -72,6 +74,7 @@ struct ContractArgs {
   const void* in;
   const void* w;
   void* out;
+  const void* zeros;  // >= 256 zero bytes: target of out-of-range lanes' loads
   int B, Q, P, K;
   int wrows, wcols;  // W is [wrows][wcols][K]
   int adjoint;
@@ -85,6 +88,7 @@ struct WgradArgs {
   const void* xh;
   const void* gh;
   float* gw;
+  const void* zeros;  // >= 256 zero bytes: target of out-of-range lanes' loads
   int B, Cin, Cout, K;
   int Kb, Nb;
   float scale;
@@ -124,6 +128,15 @@ hipError_t launch_contract(int elem, const ContractArgs& a, hipStream_t s);
 hipError_t launch_wgrad(int elem, const WgradArgs& a, hipStream_t s);
 hipError_t launch_pair(const PairArgs& a, hipStream_t s);
 hipError_t launch_scale_complex(float* p, int64_t n, float s, hipStream_t st);
+
+// Persistent fp16 fast paths (planes up to 128 x 256); hipErrorNotSupported
+// when no instantiation matches the shape.
+hipError_t launch_r2c_fast(const R2CArgs& a, int nct, int nka, int rt, int grid, size_t lds,
+                           hipStream_t s);
+hipError_t launch_c2r_fast(const C2RArgs& a, int nct, int rt, int nbt, int nkz, int grid,
+                           size_t lds, hipStream_t s);
+size_t r2c_fast_lds_bytes(int nct, int nka, int rt, int Kap16, int Nap);
+size_t c2r_fast_lds_bytes(int nct, int rt, int nbt, int nkz);
 
 size_t r2c_lds_bytes(int elem, int Kbp, int R);
 size_t c2r_lds_bytes(int elem, int Kbp, int Kap, int R);

@@ -6,136 +6,12 @@
 // Only retained modes are computed (output-pruned forward transform,
 // input-pruned inverse), which is the truncation T_K of the Fourier
 // convolution operator (Sec. 2) folded into the transform.
-//
-// MFMA 16x16 operand layout used throughout (wave64, lane l, g = l / 16):
-//   A (16 x KSTEP): lane holds A[l % 16][g*KPL .. g*KPL+KPL-1]
-//   B (KSTEP x 16): lane holds B[g*KPL .. g*KPL+KPL-1][l % 16]
-//   D (16 x 16)   : lane holds D[4*g + i][l % 16], i = 0..3
-// The k-ordering within a step only has to agree between A and B.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
-#include "fno_internal.h"
+#include "fno_device.h"
 
 namespace fno {
-
-typedef _Float16 h8 __attribute__((ext_vector_type(8)));
-typedef _Float16 h4 __attribute__((ext_vector_type(4)));
-typedef _Float16 h2 __attribute__((ext_vector_type(2)));
-typedef float f4 __attribute__((ext_vector_type(4)));
-typedef float f2 __attribute__((ext_vector_type(2)));
-
-template <typename T>
-struct MM;
-
-template <>
-struct MM<_Float16> {
-  static constexpr int KPL = 8;
-  static constexpr int KSTEP = 32;
-  typedef h8 frag;
-  static __device__ __forceinline__ f4 mma(const frag& a, const frag& b, const f4& c) {
-    return __builtin_amdgcn_mfma_f32_16x16x32_f16(a, b, c, 0, 0, 0);
-  }
-  static __device__ __forceinline__ frag zero() {
-    frag z;
-#pragma unroll
-    for (int i = 0; i < 8; ++i) z[i] = (_Float16)0.0f;
-    return z;
-  }
-  static __device__ __forceinline__ frag ld(const _Float16* p) {
-    return *reinterpret_cast<const frag*>(p);
-  }
-  static __device__ __forceinline__ frag neg(const frag& a) { return -a; }
-};
-
-template <>
-struct MM<float> {
-  static constexpr int KPL = 1;
-  static constexpr int KSTEP = 4;
-  typedef float frag;
-  static __device__ __forceinline__ f4 mma(const frag& a, const frag& b, const f4& c) {
-    return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
-  }
-  static __device__ __forceinline__ frag zero() { return 0.0f; }
-  static __device__ __forceinline__ frag ld(const float* p) { return *p; }
-  static __device__ __forceinline__ frag neg(const frag& a) { return -a; }
-};
-
-__device__ __forceinline__ f4 f4zero() { return f4{0.0f, 0.0f, 0.0f, 0.0f}; }
-
-// tanh(x) = 1 - 2 / (1 + e^{2x}); exact limits at +-inf, NaN propagates.
-__device__ __forceinline__ float tanh_f32(float x) {
-  float e = __builtin_amdgcn_exp2f(x * 2.8853900817779268f);  // e^{2x}
-  return 1.0f - 2.0f * __builtin_amdgcn_rcpf(1.0f + e);
-}
-
-// Round-to-nearest-even conversions to the storage type.
-__device__ __forceinline__ _Float16 to_h(float v) { return (_Float16)v; }
-
-template <typename T>
-__device__ __forceinline__ T from_f(float v);
-template <>
-__device__ __forceinline__ _Float16 from_f<_Float16>(float v) { return (_Float16)v; }
-template <>
-__device__ __forceinline__ float from_f<float>(float v) { return v; }
-
-// One complex value written as a single 4-byte (fp16) or 8-byte (fp32) store.
-template <typename T>
-__device__ __forceinline__ void store_pair(T* d, float re, float im);
-template <>
-__device__ __forceinline__ void store_pair<_Float16>(_Float16* d, float re, float im) {
-  *reinterpret_cast<h2*>(d) = h2{to_h(re), to_h(im)};
-}
-template <>
-__device__ __forceinline__ void store_pair<float>(float* d, float re, float im) {
-  *reinterpret_cast<f2*>(d) = f2{re, im};
-}
-
-// Make LDS writes of one lane visible to the other lanes of its wavefront.
-__device__ __forceinline__ void wave_lds_sync() {
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-  __builtin_amdgcn_wave_barrier();
-  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-}
-
-// ---------------------------------------------------------------------------
-// Input fragment of step A: KPL consecutive row elements, optional tanh.
-// ---------------------------------------------------------------------------
-template <typename T>
-__device__ __forceinline__ typename MM<T>::frag load_row_frag(const T* row, int n0, int Nb,
-                                                              bool vrow, int do_tanh,
-                                                              int vec);
-
-template <>
-__device__ __forceinline__ h8 load_row_frag<_Float16>(const _Float16* row, int n0, int Nb,
-                                                      bool vrow, int do_tanh, int vec) {
-  h8 v = MM<_Float16>::zero();
-  if (vrow) {
-    if (vec) {
-      if (n0 < Nb) v = *reinterpret_cast<const h8*>(row + n0);
-    } else {
-#pragma unroll
-      for (int i = 0; i < 8; ++i)
-        if (n0 + i < Nb) v[i] = row[n0 + i];
-    }
-    if (do_tanh) {
-#pragma unroll
-      for (int i = 0; i < 8; ++i) v[i] = to_h(tanh_f32((float)v[i]));
-    }
-  }
-  return v;
-}
-
-template <>
-__device__ __forceinline__ float load_row_frag<float>(const float* row, int n0, int Nb,
-                                                      bool vrow, int do_tanh, int vec) {
-  float v = 0.0f;
-  if (vrow && n0 < Nb) {
-    v = row[n0];
-    if (do_tanh) v = tanh_f32(v);
-  }
-  return v;
-}
 
 // ---------------------------------------------------------------------------
 // r2c: truncated forward transform of the last two axes.
@@ -543,134 +419,95 @@ __global__ __launch_bounds__(256) void axis_kernel(AxisArgs a) {
 }
 
 // ---------------------------------------------------------------------------
-// Per-mode channel contraction (forward and adjoint).
-// Work-group: 8 consecutive modes x 32 output channels x 32 batch rows.
+// Per-mode channel contraction (forward and adjoint):
+//   out[b][p][t] = scale c(t) sum_q in[b][q][t] Wop(q, p, t)
+// Tile: 8 modes x 32 batch rows x 32 output channels per work-group; the
+// reduction runs over chunks of QC input channels, the next chunk's loads in
+// flight while the current one is multiplied.
 // ---------------------------------------------------------------------------
-constexpr int CT_TM = 8;
-constexpr int CT_PB = 32;
-constexpr int CT_BB = 32;
-
-__device__ __forceinline__ float cmult(int t, int Kb, int Nb) {
-  const int tb = t % Kb;
-  return (tb == 0 || 2 * tb == Nb) ? 1.0f : 2.0f;
-}
-
-template <typename T>
-__device__ __forceinline__ void load_cplx(const T* src, int n, bool vec, float* re, float* im);
-
-// Loads n (<= 4) consecutive complex values.
-template <>
-__device__ __forceinline__ void load_cplx<_Float16>(const _Float16* src, int n, bool vec,
-                                                    float* re, float* im) {
-  if (vec && n == 4) {
-    h8 v = *reinterpret_cast<const h8*>(src);
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      re[i] = (float)v[2 * i];
-      im[i] = (float)v[2 * i + 1];
-    }
-  } else {
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      re[i] = i < n ? (float)src[2 * i] : 0.0f;
-      im[i] = i < n ? (float)src[2 * i + 1] : 0.0f;
-    }
-  }
-}
-
-template <>
-__device__ __forceinline__ void load_cplx<float>(const float* src, int n, bool vec, float* re,
-                                                 float* im) {
-  if (vec && n == 4) {
-    f4 v0 = *reinterpret_cast<const f4*>(src);
-    f4 v1 = *reinterpret_cast<const f4*>(src + 4);
-    re[0] = v0[0]; im[0] = v0[1]; re[1] = v0[2]; im[1] = v0[3];
-    re[2] = v1[0]; im[2] = v1[1]; re[3] = v1[2]; im[3] = v1[3];
-  } else {
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      re[i] = i < n ? src[2 * i] : 0.0f;
-      im[i] = i < n ? src[2 * i + 1] : 0.0f;
-    }
-  }
-}
-
-template <typename T>
+template <typename T, bool VEC>
 __global__ __launch_bounds__(256) void contract_kernel(ContractArgs a) {
   using M = MM<T>;
   using frag = typename M::frag;
   constexpr int KPL = M::KPL, KS = M::KSTEP;
-  constexpr int QC = (sizeof(T) == 2) ? 32 : 16;  // q per staged chunk
+  constexpr int CPL = CplxIO<T>::CPL;
+  constexpr int TM = CT_TM, BB = CT_BB, PB = CT_PB;
+  constexpr int QC = (sizeof(T) == 2) ? 32 : 16;
   constexpr int LDQ = QC + 16 / (int)sizeof(T);
-  constexpr size_t STAGE = sizeof(T) * 2 * CT_TM * (CT_BB + CT_PB) * LDQ;
-  constexpr size_t OUTB = sizeof(T) * 2 * CT_BB * CT_PB * CT_TM;
+  constexpr int NG = BB * (QC / 4) * (TM / CPL);  // 4-row groups per tile (= 512)
+  constexpr int GPT = NG / 256;                   // groups per thread
+  constexpr size_t SA = (size_t)2 * TM * BB * LDQ, SB = (size_t)2 * TM * PB * LDQ;
+  constexpr size_t STAGE = sizeof(T) * (SA + SB);
+  constexpr size_t OUTB = sizeof(T) * 2 * BB * PB * TM;
+  static_assert(NG % 256 == 0, "staging groups must divide over 256 threads");
   __shared__ __align__(16) unsigned char smem[STAGE > OUTB ? STAGE : OUTB];
-  T(*sIn)[CT_TM][CT_BB][LDQ] = reinterpret_cast<T(*)[CT_TM][CT_BB][LDQ]>(smem);
-  T(*sW)[CT_TM][CT_PB][LDQ] =
-      reinterpret_cast<T(*)[CT_TM][CT_PB][LDQ]>(smem + sizeof(T) * 2 * CT_TM * CT_BB * LDQ);
+  T* sA = reinterpret_cast<T*>(smem);   // [re/im][TM][BB][LDQ]
+  T* sB = sA + SA;                      // [re/im][TM][PB][LDQ]
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int r16 = lane & 15, g = lane >> 4;
-  const int t0 = blockIdx.x * CT_TM;
-  const int p0 = blockIdx.y * CT_PB;
-  const int b0 = blockIdx.z * CT_BB;
+  const int npb = (a.P + PB - 1) / PB, nbb = (a.B + BB - 1) / BB;
+  const int lid = xcd_logical_block(blockIdx.x, gridDim.x);
+  const int t0 = (lid / (npb * nbb)) * TM;
+  const int p0 = (lid % npb) * PB;
+  const int b0 = ((lid / npb) % nbb) * BB;
   const T* in = reinterpret_cast<const T*>(a.in);
   const T* w = reinterpret_cast<const T*>(a.w);
-  const bool vec = (a.K % 4) == 0;
-  // wave -> (b tile, p tile)
+  const T* zr = reinterpret_cast<const T*>(a.zeros);
+  const bool vec = VEC;
   const int bt = wave >> 1, pt = wave & 1;
-  f4 accR[CT_TM], accI[CT_TM];
-#pragma unroll
-  for (int m = 0; m < CT_TM; ++m) accR[m] = accI[m] = f4zero();
 
+  u32x4 LA[GPT][4], LB[GPT][4];
+  auto load_chunk = [&](int q0) {
+#pragma unroll
+    for (int gi = 0; gi < GPT; ++gi) {
+      const int gidx = threadIdx.x + 256 * gi;
+      const int mg = gidx % (TM / CPL);
+      const int q4 = (gidx / (TM / CPL)) % (QC / 4);
+      const int rr = gidx / ((TM / CPL) * (QC / 4));   // b (A) or p (B) within the tile
+      const int tt = t0 + mg * CPL;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int q = q0 + q4 * 4 + j;
+        const int b = b0 + rr;
+        LA[gi][j] = load_modes16<T, VEC>(zr, in + ((int64_t)b * a.Q + q) * a.K * 2, tt, a.K,
+                                         b < a.B && q < a.Q);
+        const int pc = p0 + rr;
+        const int64_t wrow = a.adjoint ? ((int64_t)pc * a.wcols + q) : ((int64_t)q * a.wcols + pc);
+        LB[gi][j] = load_modes16<T, VEC>(zr, w + wrow * a.K * 2, tt, a.K, pc < a.P && q < a.Q);
+      }
+    }
+  };
+  auto store_chunk = [&]() {
+#pragma unroll
+    for (int gi = 0; gi < GPT; ++gi) {
+      const int gidx = threadIdx.x + 256 * gi;
+      const int mg = gidx % (TM / CPL);
+      const int q4 = (gidx / (TM / CPL)) % (QC / 4);
+      const int rr = gidx / ((TM / CPL) * (QC / 4));
+      T* da = sA + ((size_t)(mg * CPL) * BB + rr) * LDQ + q4 * 4;
+      scatter4<T>(LA[gi], da, da + TM * BB * LDQ, BB * LDQ, false);
+      T* db = sB + ((size_t)(mg * CPL) * PB + rr) * LDQ + q4 * 4;
+      scatter4<T>(LB[gi], db, db + TM * PB * LDQ, PB * LDQ, a.adjoint != 0);
+    }
+  };
+
+  f4 accR[TM], accI[TM];
+#pragma unroll
+  for (int m = 0; m < TM; ++m) accR[m] = accI[m] = f4zero();
+
+  load_chunk(0);
   for (int q0 = 0; q0 < a.Q; q0 += QC) {
-    // stage in[b][q][t0..t0+8) -> sIn[.][t][b][q]
-    for (int idx = threadIdx.x; idx < CT_BB * QC * 2; idx += 256) {
-      const int half = idx & 1, rest = idx >> 1;
-      const int qq = rest % QC, bb = rest / QC;
-      const int b = b0 + bb, q = q0 + qq;
-      const int tt = t0 + half * 4;
-      float re[4], im[4];
-      const int n = (b < a.B && q < a.Q) ? max(0, min(4, a.K - tt)) : 0;
-      load_cplx<T>(in + (((int64_t)b * a.Q + q) * a.K + tt) * 2, n, vec, re, im);
+    store_chunk();
+    block_sync_lds();
+    if (q0 + QC < a.Q) load_chunk(q0 + QC);
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        sIn[0][half * 4 + i][bb][qq] = from_f<T>(re[i]);
-        sIn[1][half * 4 + i][bb][qq] = from_f<T>(im[i]);
-      }
-    }
-    // stage Wop(q, p, t) -> sW[.][t][p][q]
-    for (int idx = threadIdx.x; idx < CT_PB * QC * 2; idx += 256) {
-      const int half = idx & 1, rest = idx >> 1;
-      int qq, pp;
-      if (a.adjoint) {  // W[p][q][t]: q fastest
-        qq = rest % QC;
-        pp = rest / QC;
-      } else {          // W[q][p][t]: p fastest
-        pp = rest % CT_PB;
-        qq = rest / CT_PB;
-      }
-      const int q = q0 + qq, pc = p0 + pp;
-      const int tt = t0 + half * 4;
-      float re[4], im[4];
-      const int n = (q < a.Q && pc < a.P) ? max(0, min(4, a.K - tt)) : 0;
-      const int64_t row = a.adjoint ? ((int64_t)pc * a.wcols + q) : ((int64_t)q * a.wcols + pc);
-      load_cplx<T>(w + (row * a.K + tt) * 2, n, vec, re, im);
-      const float sgn = a.adjoint ? -1.0f : 1.0f;
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        sW[0][half * 4 + i][pp][qq] = from_f<T>(re[i]);
-        sW[1][half * 4 + i][pp][qq] = from_f<T>(sgn * im[i]);
-      }
-    }
-    __syncthreads();
-#pragma unroll
-    for (int m = 0; m < CT_TM; ++m) {
+    for (int m = 0; m < TM; ++m) {
 #pragma unroll
       for (int k0 = 0; k0 < QC; k0 += KS) {
-        frag ar = M::ld(&sIn[0][m][bt * 16 + r16][k0 + g * KPL]);
-        frag ai = M::ld(&sIn[1][m][bt * 16 + r16][k0 + g * KPL]);
-        frag br = M::ld(&sW[0][m][pt * 16 + r16][k0 + g * KPL]);
-        frag bi = M::ld(&sW[1][m][pt * 16 + r16][k0 + g * KPL]);
+        const T* pa = sA + ((size_t)m * BB + bt * 16 + r16) * LDQ + k0 + g * KPL;
+        const T* pb = sB + ((size_t)m * PB + pt * 16 + r16) * LDQ + k0 + g * KPL;
+        frag ar = M::ld(pa), ai = M::ld(pa + TM * BB * LDQ);
+        frag br = M::ld(pb), bi = M::ld(pb + TM * PB * LDQ);
         frag nai = M::neg(ai);
         accR[m] = M::mma(ar, br, accR[m]);
         accR[m] = M::mma(nai, bi, accR[m]);
@@ -678,40 +515,35 @@ __global__ __launch_bounds__(256) void contract_kernel(ContractArgs a) {
         accI[m] = M::mma(ai, br, accI[m]);
       }
     }
-    __syncthreads();
+    block_sync_lds();
   }
-  // epilogue: stage [b][p][t] complex in LDS (reuse sIn), then 8-mode rows
-  T* so = reinterpret_cast<T*>(smem);  // [b][p][t] complex
+  // epilogue: [b][p][t] complex staged in LDS, written as rows of 8 modes
+  T* so = reinterpret_cast<T*>(smem);
 #pragma unroll
-  for (int m = 0; m < CT_TM; ++m) {
+  for (int m = 0; m < TM; ++m) {
     const int t = t0 + m;
-    const float s = (t < a.K) ? a.scale * cmult(t, a.Kb, a.Nb) : 0.0f;
+    const float sc = (t < a.K) ? a.scale * cmult(t, a.Kb, a.Nb) : 0.0f;
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int bb = bt * 16 + 4 * g + i, pp = pt * 16 + r16;
-      store_pair<T>(so + ((bb * CT_PB + pp) * CT_TM + m) * 2, accR[m][i] * s, accI[m][i] * s);
+      store_pair<T>(so + ((bb * PB + pp) * TM + m) * 2, accR[m][i] * sc, accI[m][i] * sc);
     }
   }
-  __syncthreads();
+  block_sync_lds();
   T* out = reinterpret_cast<T*>(a.out);
-  for (int idx = threadIdx.x; idx < CT_BB * CT_PB; idx += 256) {
-    const int bb = idx / CT_PB, pp = idx % CT_PB;
+  constexpr int V16 = TM * 2 * (int)sizeof(T) / 16;  // 16-byte pieces per (b, p) row
+  const int nmodes = min(TM, a.K - t0);
+  for (int idx = threadIdx.x; idx < BB * PB * V16; idx += 256) {
+    const int v = idx % V16, bp = idx / V16;
+    const int bb = bp / PB, pp = bp % PB;
     const int b = b0 + bb, pc = p0 + pp;
     if (b < a.B && pc < a.P) {
       T* d = out + (((int64_t)b * a.P + pc) * a.K + t0) * 2;
-      const T* s = so + (bb * CT_PB + pp) * CT_TM * 2;
-      const int n = min(CT_TM, a.K - t0);
-      if (n == CT_TM && vec) {
-        if (sizeof(T) == 2) {
-          *reinterpret_cast<h8*>(d) = *reinterpret_cast<const h8*>(s);
-          *reinterpret_cast<h8*>(d + 8) = *reinterpret_cast<const h8*>(s + 8);
-        } else {
-#pragma unroll
-          for (int i = 0; i < 4; ++i)
-            reinterpret_cast<f4*>(d)[i] = reinterpret_cast<const f4*>(s)[i];
-        }
-      } else {
-        for (int i = 0; i < 2 * n; ++i) d[i] = s[i];
+      const T* sv = so + (size_t)bp * TM * 2;
+      if (nmodes == TM && vec) {
+        reinterpret_cast<u32x4*>(d)[v] = reinterpret_cast<const u32x4*>(sv)[v];
+      } else if (v == 0) {
+        for (int i = 0; i < 2 * nmodes; ++i) d[i] = sv[i];
       }
     }
   }
@@ -719,104 +551,125 @@ __global__ __launch_bounds__(256) void contract_kernel(ContractArgs a) {
 
 // ---------------------------------------------------------------------------
 // Weight gradient: gw[q][p][t] = scale c(t) sum_b conj(xh[b][q][t]) gh[b][p][t]
-// Work-group: 8 modes x 32 (q) x 32 (p); fixed-order reduction over b.
+// Tile: 8 modes x 32 (q) x 32 (p); fixed-order reduction over batch chunks.
 // ---------------------------------------------------------------------------
-template <typename T>
+template <typename T, bool VEC>
 __global__ __launch_bounds__(256) void wgrad_kernel(WgradArgs a) {
   using M = MM<T>;
   using frag = typename M::frag;
   constexpr int KPL = M::KPL, KS = M::KSTEP;
-  constexpr int BC = (sizeof(T) == 2) ? 32 : 16;  // batch rows per chunk
+  constexpr int CPL = CplxIO<T>::CPL;
+  constexpr int TM = CT_TM, QB = 32, PB = 32;
+  constexpr int BC = (sizeof(T) == 2) ? 32 : 16;  // batch rows per chunk (MFMA K)
   constexpr int LDB = BC + 16 / (int)sizeof(T);
-  constexpr int TM = 8, QB = 32, PB = 32;
-  constexpr size_t STAGE = sizeof(T) * 2 * TM * (QB + PB) * LDB;
+  constexpr int NG = QB * (BC / 4) * (TM / CPL);
+  constexpr int GPT = NG / 256;
+  constexpr size_t SX = (size_t)2 * TM * QB * LDB, SG = (size_t)2 * TM * PB * LDB;
+  constexpr size_t STAGE = sizeof(T) * (SX + SG);
   constexpr size_t OUTB = sizeof(float) * 2 * QB * PB * TM;
+  static_assert(NG % 256 == 0, "staging groups must divide over 256 threads");
   __shared__ __align__(16) unsigned char smem[STAGE > OUTB ? STAGE : OUTB];
-  T(*sX)[TM][QB][LDB] = reinterpret_cast<T(*)[TM][QB][LDB]>(smem);
-  T(*sG)[TM][PB][LDB] = reinterpret_cast<T(*)[TM][PB][LDB]>(smem + sizeof(T) * 2 * TM * QB * LDB);
+  T* sX = reinterpret_cast<T*>(smem);   // [re/im][TM][QB][LDB]
+  T* sG = sX + SX;                      // [re/im][TM][PB][LDB]
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int r16 = lane & 15, g = lane >> 4;
-  const int t0 = blockIdx.x * TM;
-  const int q0 = blockIdx.y * QB;
-  const int p0 = blockIdx.z * PB;
+  const int nqb = (a.Cin + QB - 1) / QB, npb = (a.Cout + PB - 1) / PB;
+  const int lid = xcd_logical_block(blockIdx.x, gridDim.x);
+  const int t0 = (lid / (nqb * npb)) * TM;
+  const int q0 = ((lid / npb) % nqb) * QB;
+  const int p0 = (lid % npb) * PB;
   const T* xh = reinterpret_cast<const T*>(a.xh);
   const T* gh = reinterpret_cast<const T*>(a.gh);
-  const bool vec = (a.K % 4) == 0;
+  const T* zr = reinterpret_cast<const T*>(a.zeros);
   const int qt = wave >> 1, pt = wave & 1;
+
+  u32x4 LX[GPT][4], LG[GPT][4];
+  auto load_chunk = [&](int bs) {
+#pragma unroll
+    for (int gi = 0; gi < GPT; ++gi) {
+      const int gidx = threadIdx.x + 256 * gi;
+      const int mg = gidx % (TM / CPL);
+      const int b4 = (gidx / (TM / CPL)) % (BC / 4);
+      const int rr = gidx / ((TM / CPL) * (BC / 4));   // q (X) or p (G) within the tile
+      const int tt = t0 + mg * CPL;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int b = bs + b4 * 4 + j;
+        const int q = q0 + rr, pc = p0 + rr;
+        LX[gi][j] = load_modes16<T, VEC>(zr, xh + ((int64_t)b * a.Cin + q) * a.K * 2, tt,
+                                         a.K, b < a.B && q < a.Cin);
+        LG[gi][j] = load_modes16<T, VEC>(zr, gh + ((int64_t)b * a.Cout + pc) * a.K * 2, tt,
+                                         a.K, b < a.B && pc < a.Cout);
+      }
+    }
+  };
+  auto store_chunk = [&]() {
+#pragma unroll
+    for (int gi = 0; gi < GPT; ++gi) {
+      const int gidx = threadIdx.x + 256 * gi;
+      const int mg = gidx % (TM / CPL);
+      const int b4 = (gidx / (TM / CPL)) % (BC / 4);
+      const int rr = gidx / ((TM / CPL) * (BC / 4));
+      T* dx = sX + ((size_t)(mg * CPL) * QB + rr) * LDB + b4 * 4;
+      scatter4<T>(LX[gi], dx, dx + TM * QB * LDB, QB * LDB, false);
+      T* dg = sG + ((size_t)(mg * CPL) * PB + rr) * LDB + b4 * 4;
+      scatter4<T>(LG[gi], dg, dg + TM * PB * LDB, PB * LDB, false);
+    }
+  };
+
   f4 accR[TM], accI[TM];
 #pragma unroll
   for (int m = 0; m < TM; ++m) accR[m] = accI[m] = f4zero();
 
+  load_chunk(0);
   for (int bs = 0; bs < a.B; bs += BC) {
-    for (int idx = threadIdx.x; idx < BC * QB * 2; idx += 256) {
-      const int half = idx & 1, rest = idx >> 1;
-      const int qq = rest % QB, bb = rest / QB;
-      const int b = bs + bb, q = q0 + qq, tt = t0 + half * 4;
-      float re[4], im[4];
-      const int n = (b < a.B && q < a.Cin) ? max(0, min(4, a.K - tt)) : 0;
-      load_cplx<T>(xh + (((int64_t)b * a.Cin + q) * a.K + tt) * 2, n, vec, re, im);
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        sX[0][half * 4 + i][qq][bb] = from_f<T>(re[i]);
-        sX[1][half * 4 + i][qq][bb] = from_f<T>(im[i]);
-      }
-    }
-    for (int idx = threadIdx.x; idx < BC * PB * 2; idx += 256) {
-      const int half = idx & 1, rest = idx >> 1;
-      const int pp = rest % PB, bb = rest / PB;
-      const int b = bs + bb, pc = p0 + pp, tt = t0 + half * 4;
-      float re[4], im[4];
-      const int n = (b < a.B && pc < a.Cout) ? max(0, min(4, a.K - tt)) : 0;
-      load_cplx<T>(gh + (((int64_t)b * a.Cout + pc) * a.K + tt) * 2, n, vec, re, im);
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        sG[0][half * 4 + i][pp][bb] = from_f<T>(re[i]);
-        sG[1][half * 4 + i][pp][bb] = from_f<T>(im[i]);
-      }
-    }
-    __syncthreads();
+    store_chunk();
+    block_sync_lds();
+    if (bs + BC < a.B) load_chunk(bs + BC);
 #pragma unroll
     for (int m = 0; m < TM; ++m) {
 #pragma unroll
       for (int k0 = 0; k0 < BC; k0 += KS) {
-        frag xr = M::ld(&sX[0][m][qt * 16 + r16][k0 + g * KPL]);
-        frag xi = M::ld(&sX[1][m][qt * 16 + r16][k0 + g * KPL]);
-        frag gr = M::ld(&sG[0][m][pt * 16 + r16][k0 + g * KPL]);
-        frag gi = M::ld(&sG[1][m][pt * 16 + r16][k0 + g * KPL]);
+        const T* px = sX + ((size_t)m * QB + qt * 16 + r16) * LDB + k0 + g * KPL;
+        const T* pg = sG + ((size_t)m * PB + pt * 16 + r16) * LDB + k0 + g * KPL;
+        frag xr = M::ld(px), xi = M::ld(px + TM * QB * LDB);
+        frag gr = M::ld(pg), gi_ = M::ld(pg + TM * PB * LDB);
         frag nxi = M::neg(xi);
-        // conj(x) * g = (xr gr + xi gi) + i (xr gi - xi gr)
+        // conj(x) g = (xr gr + xi gi) + i (xr gi - xi gr)
         accR[m] = M::mma(xr, gr, accR[m]);
-        accR[m] = M::mma(xi, gi, accR[m]);
-        accI[m] = M::mma(xr, gi, accI[m]);
+        accR[m] = M::mma(xi, gi_, accR[m]);
+        accI[m] = M::mma(xr, gi_, accI[m]);
         accI[m] = M::mma(nxi, gr, accI[m]);
       }
     }
-    __syncthreads();
+    block_sync_lds();
   }
   float* so = reinterpret_cast<float*>(smem);  // [QB][PB][TM] complex
 #pragma unroll
   for (int m = 0; m < TM; ++m) {
     const int t = t0 + m;
-    const float s = (t < a.K) ? a.scale * cmult(t, a.Kb, a.Nb) : 0.0f;
+    const float sc = (t < a.K) ? a.scale * cmult(t, a.Kb, a.Nb) : 0.0f;
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int qq = qt * 16 + 4 * g + i, pp = pt * 16 + r16;
-      store_pair<float>(so + ((qq * PB + pp) * TM + m) * 2, accR[m][i] * s, accI[m][i] * s);
+      store_pair<float>(so + ((qq * PB + pp) * TM + m) * 2, accR[m][i] * sc, accI[m][i] * sc);
     }
   }
-  __syncthreads();
-  for (int idx = threadIdx.x; idx < QB * PB; idx += 256) {
-    const int qq = idx / PB, pp = idx % PB;
+  block_sync_lds();
+  constexpr int V16 = TM * 8 / 16;  // 16-byte pieces per (q, p) row of fp32 complex
+  const int nmodes = min(TM, a.K - t0);
+  const bool vout = (a.K % 2) == 0;
+  for (int idx = threadIdx.x; idx < QB * PB * V16; idx += 256) {
+    const int v = idx % V16, qp = idx / V16;
+    const int qq = qp / PB, pp = qp % PB;
     const int q = q0 + qq, pc = p0 + pp;
     if (q < a.Cin && pc < a.Cout) {
       float* d = a.gw + (((int64_t)q * a.Cout + pc) * a.K + t0) * 2;
-      const float* s = so + (qq * PB + pp) * TM * 2;
-      const int n = min(TM, a.K - t0);
-      if (n == TM && vec) {
-#pragma unroll
-        for (int i = 0; i < 4; ++i) reinterpret_cast<f4*>(d)[i] = reinterpret_cast<const f4*>(s)[i];
-      } else {
-        for (int i = 0; i < 2 * n; ++i) d[i] = s[i];
+      const float* sv = so + (size_t)qp * TM * 2;
+      if (nmodes == TM && vout) {
+        reinterpret_cast<f4*>(d)[v] = reinterpret_cast<const f4*>(sv)[v];
+      } else if (v == 0) {
+        for (int i = 0; i < 2 * nmodes; ++i) d[i] = sv[i];
       }
     }
   }
@@ -943,24 +796,41 @@ hipError_t launch_axis(int elem, const AxisArgs& a, size_t lds, hipStream_t s) {
 }
 
 hipError_t launch_contract(int elem, const ContractArgs& a, hipStream_t s) {
-  dim3 grid((unsigned)((a.K + CT_TM - 1) / CT_TM), (unsigned)((a.P + CT_PB - 1) / CT_PB),
-            (unsigned)((a.B + CT_BB - 1) / CT_BB));
+  const int64_t nblk = (int64_t)((a.K + CT_TM - 1) / CT_TM) * ((a.P + CT_PB - 1) / CT_PB) *
+                       ((a.B + CT_BB - 1) / CT_BB);
+  if (nblk > 0x7fffffff) return hipErrorInvalidValue;
+  dim3 grid((unsigned)nblk);
   dim3 block(256);
-  if (elem == ELEM_F16)
-    hipLaunchKernelGGL((contract_kernel<_Float16>), grid, block, 0, s, a);
-  else
-    hipLaunchKernelGGL((contract_kernel<float>), grid, block, 0, s, a);
+  if (elem == ELEM_F16) {
+    if (a.K % 4 == 0)
+      hipLaunchKernelGGL((contract_kernel<_Float16, true>), grid, block, 0, s, a);
+    else
+      hipLaunchKernelGGL((contract_kernel<_Float16, false>), grid, block, 0, s, a);
+  } else {
+    if (a.K % 2 == 0)
+      hipLaunchKernelGGL((contract_kernel<float, true>), grid, block, 0, s, a);
+    else
+      hipLaunchKernelGGL((contract_kernel<float, false>), grid, block, 0, s, a);
+  }
   return hipGetLastError();
 }
 
 hipError_t launch_wgrad(int elem, const WgradArgs& a, hipStream_t s) {
-  dim3 grid((unsigned)((a.K + 7) / 8), (unsigned)((a.Cin + 31) / 32),
-            (unsigned)((a.Cout + 31) / 32));
+  const int64_t nblk = (int64_t)((a.K + 7) / 8) * ((a.Cin + 31) / 32) * ((a.Cout + 31) / 32);
+  if (nblk > 0x7fffffff) return hipErrorInvalidValue;
+  dim3 grid((unsigned)nblk);
   dim3 block(256);
-  if (elem == ELEM_F16)
-    hipLaunchKernelGGL((wgrad_kernel<_Float16>), grid, block, 0, s, a);
-  else
-    hipLaunchKernelGGL((wgrad_kernel<float>), grid, block, 0, s, a);
+  if (elem == ELEM_F16) {
+    if (a.K % 4 == 0)
+      hipLaunchKernelGGL((wgrad_kernel<_Float16, true>), grid, block, 0, s, a);
+    else
+      hipLaunchKernelGGL((wgrad_kernel<_Float16, false>), grid, block, 0, s, a);
+  } else {
+    if (a.K % 2 == 0)
+      hipLaunchKernelGGL((wgrad_kernel<float, true>), grid, block, 0, s, a);
+    else
+      hipLaunchKernelGGL((wgrad_kernel<float, false>), grid, block, 0, s, a);
+  }
   return hipGetLastError();
 }
 

@@ -235,13 +235,14 @@ struct Geo {
 struct DevTables {
   void* base = nullptr;
   size_t bytes = 0;
-  const void *twA, *cB, *sB, *cI, *sI, *twI;
+  const void *zeros, *twA, *cB, *sB, *cI, *sI, *twI;
   const void *eFr, *eFi, *eIr, *eIi;
 };
 
 struct Plan {
   Geo g;
   DevTables t;
+  int num_cu = 256;
   std::vector<PStep> path_fwd, path_adj;
   std::vector<std::string> labels_fwd, labels_adj;
   std::string out_fwd, out_adj;
@@ -315,6 +316,7 @@ void fill_tables(const fno_conv_desc* d, const Geo& g, std::vector<T>& buf,
     off.push_back(o);
     return o;
   };
+  alloc(256 / sizeof(T));  // zero block: loads of out-of-range lanes point here
   const int nd = g.nd;
   const int64_t ma = nd >= 2 ? d->modes[nd - 2] : 1;
   auto ka_of = [&](int t) -> int64_t {
@@ -441,17 +443,18 @@ fno_status build_tables(const fno_conv_desc* d, Plan* pl) {
   auto at = [&](int i) -> const void* {
     return (const void*)((const char*)dev + off[i] * pl->g.es);
   };
-  pl->t.twA = at(0);
-  pl->t.cB = at(1);
-  pl->t.sB = at(2);
-  pl->t.cI = at(3);
-  pl->t.sI = at(4);
-  pl->t.twI = at(5);
+  pl->t.zeros = at(0);
+  pl->t.twA = at(1);
+  pl->t.cB = at(2);
+  pl->t.sB = at(3);
+  pl->t.cI = at(4);
+  pl->t.sI = at(5);
+  pl->t.twI = at(6);
   if (pl->g.nd == 3) {
-    pl->t.eFr = at(6);
-    pl->t.eFi = at(7);
-    pl->t.eIr = at(8);
-    pl->t.eIi = at(9);
+    pl->t.eFr = at(7);
+    pl->t.eFi = at(8);
+    pl->t.eIr = at(9);
+    pl->t.eIi = at(10);
   }
   return FNO_OK;
 }
@@ -483,6 +486,10 @@ fno_status get_plan(const fno_conv_desc* d, Plan** out) {
   std::unique_ptr<Plan> pl(new Plan());
   host_plan(d, pl.get());
   pl->device = dev;
+  int ncu = 0;
+  if (hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess &&
+      ncu > 0)
+    pl->num_cu = ncu;
   st = build_tables(d, pl.get());
   if (st != FNO_OK) return st;
   *out = pl.get();
@@ -628,6 +635,7 @@ fno_status run_r2c(const Plan* pl, const void* in, void* spec, void* inter, int6
                    int do_tanh, int scale_mode, hipStream_t s) {
   const Geo& g = pl->g;
   R2CArgs a{};
+  a.zeros = pl->t.zeros;
   a.in = in;
   a.out = g.nd == 3 ? inter : spec;
   a.twA = pl->t.twA;
@@ -653,7 +661,21 @@ fno_status run_r2c(const Plan* pl, const void* in, void* spec, void* inter, int6
   a.do_tanh = do_tanh;
   a.vec = (g.Nb % 8) == 0;
   if (a.planes > 0x7fffffff || (g.nd == 3 && g.B * C > 65535)) return FNO_ERR_UNSUPPORTED;
-  FNO_HIP(timed("r2c_plane", s, [&] { return launch_r2c(g.elem, g.nct, a, r2c_lds_bytes(g.elem, g.Kbp, g.R_f), s); }));
+  bool done = false;
+  if (g.elem == ELEM_F16 && a.vec && g.Nb <= 256 && g.Na <= 128 && g.nct <= 8) {
+    const int nka = g.Nb <= 32 ? 1 : g.Nb <= 64 ? 2 : g.Nb <= 128 ? 4 : 8;
+    const int rt = g.Na <= 64 ? 1 : 2;
+    const size_t lds = r2c_fast_lds_bytes(g.nct, nka, rt, g.Kap16, g.Nap_f);
+    const int grid = (int)std::min<int64_t>(a.planes, (int64_t)2 * pl->num_cu);
+    if (lds <= 80 * 1024) {
+      hipError_t e = timed(do_tanh ? "r2c_plane_tanh" : "r2c_plane", s, [&] {
+        return launch_r2c_fast(a, g.nct, nka, rt, grid, lds, s);
+      });
+      if (e == hipSuccess) done = true;
+      else if (e != hipErrorNotSupported) return FNO_ERR_HIP;
+    }
+  }
+  if (!done) FNO_HIP(timed(do_tanh ? "r2c_plane_tanh" : "r2c_plane", s, [&] { return launch_r2c(g.elem, g.nct, a, r2c_lds_bytes(g.elem, g.Kbp, g.R_f), s); }));
   if (g.nd == 3) {
     AxisArgs x{};
     x.in = inter;
@@ -695,6 +717,7 @@ fno_status run_c2r(const Plan* pl, const void* spec, void* out, void* inter, int
     src = inter;
   }
   C2RArgs a{};
+  a.zeros = pl->t.zeros;
   a.in = src;
   a.out = out;
   a.x = x_epi;
@@ -714,7 +737,22 @@ fno_status run_c2r(const Plan* pl, const void* spec, void* out, void* inter, int
   a.epilogue = x_epi != nullptr;
   a.vec = (g.Nb % 8) == 0;
   if (a.planes > 0x7fffffff) return FNO_ERR_UNSUPPORTED;
-  FNO_HIP(timed(x_epi ? "c2r_plane_tanh_grad" : "c2r_plane", s, [&] { return launch_c2r(g.elem, g.nct, a, c2r_lds_bytes(g.elem, g.Kbp, g.Kap, g.R_i), s); }));
+  const char* kname = x_epi ? "c2r_plane_tanh_grad" : "c2r_plane";
+  if (g.elem == ELEM_F16 && a.vec && g.Nb <= 256 && g.Na <= 128 && g.nct <= 8 && g.Kap <= 128) {
+    const int nbt = (g.Nb + 63) / 64;
+    const int rt = g.Na <= 64 ? 1 : 2;
+    const int nkz = g.Kap / 32;
+    const size_t lds = c2r_fast_lds_bytes(g.nct, rt, nbt, nkz);
+    const int grid = (int)std::min<int64_t>(a.planes, (int64_t)2 * pl->num_cu);
+    if (lds <= 80 * 1024) {
+      hipError_t e = timed(kname, s, [&] {
+        return launch_c2r_fast(a, g.nct, rt, nbt, nkz, grid, lds, s);
+      });
+      if (e == hipSuccess) return FNO_OK;
+      if (e != hipErrorNotSupported) return FNO_ERR_HIP;
+    }
+  }
+  FNO_HIP(timed(kname, s, [&] { return launch_c2r(g.elem, g.nct, a, c2r_lds_bytes(g.elem, g.Kbp, g.Kap, g.R_i), s); }));
   return FNO_OK;
 }
 
@@ -722,6 +760,7 @@ fno_status run_contract(const Plan* pl, const void* in, const void* w, void* out
                         bool adjoint, hipStream_t s) {
   const Geo& g = pl->g;
   ContractArgs a{};
+  a.zeros = pl->t.zeros;
   a.in = in;
   a.w = w;
   a.out = out;
@@ -1240,6 +1279,7 @@ fno_status fno_spectral_conv_bwd_weight(const fno_conv_desc* d, const void* x, c
   char* tsc = base + L.total;
   if (!tucker) {
     WgradArgs a{};
+    a.zeros = pl->t.zeros;
     a.xh = xh;
     a.gh = gh;
     a.gw = (float*)gw->dense;
