@@ -2,7 +2,7 @@
 
     python -m paper_2307_15034_amd.build
 
-Both sources go through one hipcc invocation; the result lands next to this
+All sources go through one hipcc invocation; the result lands next to this
 file, where the Python binding loads it.
 """
 from __future__ import annotations
@@ -15,7 +15,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 ROOT = os.path.dirname(HERE)
 LIB = os.path.join(HERE, "libfno_spectral_conv.so")
-SOURCES = ["fno_kernels.hip", "fno_fast.hip", "fno_plan.cpp"]
+SOURCES = ["fno_kernels.hip", "fno_fast.hip", "fno_chain.hip", "fno_plan.cpp"]
 ARCH = "gfx950"
 
 

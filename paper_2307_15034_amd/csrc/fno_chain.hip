@@ -1,0 +1,584 @@
+// Chained fp16 truncated transforms: one wavefront per plane, no block
+// barriers after the one-time table staging, no LDS round trip for data.
+//
+// Both axes of a plane transform are DFT-by-MFMA products.  The contraction
+// index of an MFMA may be ordered arbitrarily inside a k-step as long as the
+// two operands agree, so the k-slots of the second product are chosen to be
+// exactly the (row, column) positions that the lane already holds in the
+// result registers of the first product (D lane: rows 4g..4g+3 of a 16x16
+// tile).  The constant twiddle operand is stored with the matching
+// permutation; the data operand never leaves the registers.
+//
+//   forward  (per plane): x[Na][Nb] -> step A (last axis, x . [cos | -sin])
+//            -> step B (leading axis, complex, accumulated over 32-row blocks)
+//            -> spectrum [Ka][Kb]
+//   inverse  (per plane): spectrum -> step B' (leading axis, per 16-row tile
+//            of the output) -> step A' (last axis, real part) -> y[Na][Nb]
+//
+// Output rows of the last products are also permuted so that every lane
+// ends up with contiguous output elements (16-byte stores).
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "fno_device.h"
+
+namespace fno {
+
+namespace {
+
+typedef MM<_Float16> MH;
+constexpr int KS = 32;   // k per MFMA step (v_mfma_f32_16x16x32_f16)
+constexpr int PADH = 8;  // LDS row padding in halves
+constexpr int CH_NW = kChainWaves;  // waves per work-group, one plane each at a time
+
+typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
+
+__device__ __forceinline__ h8 u_as_h8(const u32x4& v) {
+  h8 r;
+  __builtin_memcpy(&r, &v, 16);
+  return r;
+}
+
+__device__ __forceinline__ u32x4 h8_as_u4(const h8& v) {
+  u32x4 r;
+  __builtin_memcpy(&r, &v, 16);
+  return r;
+}
+
+// Copy of a [rows][cols] fp16 table (row stride gstride) into LDS rows of
+// stride lstride (cols, strides multiples of 8), at most MAXP 16-byte pieces
+// per thread.  All loads are issued before any store, so staging costs one
+// memory latency rather than one per piece.
+template <int MAXP>
+struct Stager {
+  u32x4 v[MAXP];
+  __device__ __forceinline__ void load(const _Float16* src, int gstride, int rows, int cols,
+                                       const _Float16* zeros) {
+    const int cpr = cols / 8;
+#pragma unroll
+    for (int k = 0; k < MAXP; ++k) {
+      const int i = threadIdx.x + k * CH_NW * 64;
+      const int r = i / cpr, c = (i - r * cpr) * 8;
+      const bool ok = i < rows * cpr;
+      v[k] = *reinterpret_cast<const u32x4*>(ok ? src + (int64_t)r * gstride + c : zeros);
+    }
+  }
+  __device__ __forceinline__ void store(_Float16* dst, int lstride, int rows, int cols) const {
+    const int cpr = cols / 8;
+#pragma unroll
+    for (int k = 0; k < MAXP; ++k) {
+      const int i = threadIdx.x + k * CH_NW * 64;
+      const int r = i / cpr, c = (i - r * cpr) * 8;
+      if (i < rows * cpr) *reinterpret_cast<u32x4*>(dst + r * lstride + c) = v[k];
+    }
+  }
+};
+
+// Table lookup of two fp16 values packed in w: the LDS table holds f(|x|)
+// for the 32768 non-negative codes; `odd` restores the sign (f odd).
+// 2 * code of the low half is (w << 1) & 0xfffe, of the high half
+// (w >> 15) & 0xfffe.
+template <bool ODD>
+__device__ __forceinline__ unsigned lut_pair(const _Float16* tab, unsigned w) {
+  const unsigned lo = (w << 1) & 0xfffeu, hi = (w >> 15) & 0xfffeu;
+  const char* t = reinterpret_cast<const char*>(tab);
+  const unsigned a = *reinterpret_cast<const unsigned short*>(t + lo);
+  const unsigned b = *reinterpret_cast<const unsigned short*>(t + hi);
+  const unsigned r = a | (b << 16);
+  return ODD ? (r | (w & 0x80008000u)) : r;
+}
+
+template <bool ODD>
+__device__ __forceinline__ u32x4 lut_u4(const _Float16* tab, const u32x4& w) {
+  return u32x4{lut_pair<ODD>(tab, w[0]), lut_pair<ODD>(tab, w[1]), lut_pair<ODD>(tab, w[2]),
+               lut_pair<ODD>(tab, w[3])};
+}
+
+constexpr int LUT_HALVES = 32768;  // one entry per non-negative fp16 code
+
+// Position in a wave's flattened sequence of (plane, block) work items.
+struct Pos {
+  int64_t p;
+  int j;
+};
+
+}  // namespace
+
+// ---------------------------------------------------------------------------
+// Forward.  Template: NKA = ceil(Nb / 32) k-steps of step A, NTB = Kbp / 16
+// spectrum column tiles, NTA = Kap16 / 16 spectrum row tiles.
+//
+// Step A of a 32-row block (two 16-row tiles, rt = 0, 1) gives, per column
+// tile ct, D registers holding Y[32 j + 16 rt + 4 g + i][col(ct, l % 16)].
+// Column tile ct is part ct / NTB (0: cos -> Re, 1: -sin -> Im) of the
+// spectrum columns tb = NTB * (l % 16) + ct % NTB.  Step B takes those eight
+// values (rt = 0, 1; i = 0..3) as the B operand of one k-step; the leading-
+// axis table column 32 j + 8 g + e holds the matching row n_a.
+// ---------------------------------------------------------------------------
+template <int NKA, int NTB, int NTA, bool TANH>
+__global__ __launch_bounds__(CH_NW * 64, 2) void r2c_chain_kernel(R2CArgs a) {
+  constexpr int NCT = 2 * NTB;
+  constexpr int LDT = NKA * KS + PADH;
+  extern __shared__ __align__(16) unsigned char smem[];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int r16 = lane & 15, g = lane >> 4;
+  const int LDE = a.NaC + PADH;
+  constexpr int LUTH = TANH ? LUT_HALVES : 0;
+  _Float16* sLut = reinterpret_cast<_Float16*>(smem);  // tanh of each fp16 code
+  _Float16* sT = sLut + LUTH;                          // [NCT * 16][LDT]
+  _Float16* sEc = sT + NCT * 16 * LDT;                // [NTA * 16][LDE]
+  _Float16* sEs = sEc + NTA * 16 * LDE;
+  const _Float16* x = reinterpret_cast<const _Float16*>(a.in);
+  const _Float16* zr = reinterpret_cast<const _Float16*>(a.zeros);
+  _Float16* out = reinterpret_cast<_Float16*>(a.out);
+
+  // tables: 16 NCT rows x 4 NKA pieces, and 16 NTA rows x NaC / 8 <= 16 pieces
+  constexpr int PT = (NCT * 16 * NKA * 4 + CH_NW * 64 - 1) / (CH_NW * 64);
+  constexpr int PE = (NTA * 16 * 16 + CH_NW * 64 - 1) / (CH_NW * 64);
+  Stager<PT> st;
+  Stager<PE> sc, ss;
+  Stager<TANH ? LUT_HALVES / 8 / (CH_NW * 64) : 1> sl;
+
+  const int NJ = a.NaC / 32;
+  const int64_t plane = (int64_t)a.Na * a.Nb;
+  const int64_t W = (int64_t)gridDim.x * CH_NW;
+  auto next = [&](Pos q) -> Pos { return q.j + 1 < NJ ? Pos{q.p, q.j + 1} : Pos{q.p + W, 0}; };
+
+  // Row block (p, j): lane holds rows 32 j + 16 rt + r16, columns 32 s + 8 g.
+  // Issued unconditionally (past the last plane: the zero block) so the wait
+  // before each use counts all loads issued after it.
+  auto load = [&](Pos q, u32x4 (&buf)[2][NKA]) {
+    const bool pok = q.p < a.planes;
+    const _Float16* base = x + (pok ? q.p : 0) * plane;
+#pragma unroll
+    for (int rt = 0; rt < 2; ++rt) {
+      const int row = 32 * q.j + 16 * rt + r16;
+#pragma unroll
+      for (int s = 0; s < NKA; ++s) {
+        const int col = s * KS + g * 8;
+        const bool ok = pok && row < a.Na && col < a.Nb;
+        buf[rt][s] = *reinterpret_cast<const u32x4*>(ok ? base + (int64_t)row * a.Nb + col : zr);
+      }
+    }
+  };
+
+  f4 zre[NTA][NTB], zim[NTA][NTB];
+
+  // ---- step A: 32 rows x [cos | -sin]; returns the step-B operands ------------
+  auto step_a = [&](const u32x4 (&buf)[2][NKA], h8 (&yf)[NCT]) {
+    f4 acc[2][NCT];
+#pragma unroll
+    for (int rt = 0; rt < 2; ++rt)
+#pragma unroll
+      for (int ct = 0; ct < NCT; ++ct) acc[rt][ct] = f4zero();
+#pragma unroll
+    for (int s = 0; s < NKA; ++s) {
+      h8 v0, v1;
+      if constexpr (TANH) {
+        // tanh rounded to fp16, looked up per fp16 code
+        v0 = u_as_h8(lut_u4<true>(sLut, buf[0][s]));
+        v1 = u_as_h8(lut_u4<true>(sLut, buf[1][s]));
+      } else {
+        v0 = u_as_h8(buf[0][s]);
+        v1 = u_as_h8(buf[1][s]);
+      }
+#pragma unroll
+      for (int ct = 0; ct < NCT; ++ct) {
+        const h8 bf = MH::ld(sT + (ct * 16 + r16) * LDT + s * KS + g * 8);
+        acc[0][ct] = MH::mma(v0, bf, acc[0][ct]);
+        acc[1][ct] = MH::mma(v1, bf, acc[1][ct]);
+      }
+    }
+    // fp16, scaled: slots 0..3 rows 32 j + 4 g + i, slots 4..7 rows + 16
+#pragma unroll
+    for (int ct = 0; ct < NCT; ++ct)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        yf[ct][i] = to_h(acc[0][ct][i] * a.scaleA);
+        yf[ct][4 + i] = to_h(acc[1][ct][i] * a.scaleA);
+      }
+  };
+
+  // ---- step B: Z[t_a][t_b] += (c - i s)[t_a][rows] (Yr + i Yi)[rows][t_b] -----
+  auto step_b = [&](Pos q, const h8 (&yf)[NCT]) {
+    if (q.j == 0) {
+#pragma unroll
+      for (int ta = 0; ta < NTA; ++ta)
+#pragma unroll
+        for (int tb = 0; tb < NTB; ++tb) zre[ta][tb] = zim[ta][tb] = f4zero();
+    }
+#pragma unroll
+    for (int ta = 0; ta < NTA; ++ta) {
+      const int eo = (ta * 16 + r16) * LDE + 32 * q.j + g * 8;
+      const h8 cf = MH::ld(sEc + eo), sf = MH::ld(sEs + eo);
+      const h8 nsf = -sf;
+#pragma unroll
+      for (int tb = 0; tb < NTB; ++tb) {
+        zre[ta][tb] = MH::mma(cf, yf[tb], zre[ta][tb]);
+        zre[ta][tb] = MH::mma(sf, yf[NTB + tb], zre[ta][tb]);
+        zim[ta][tb] = MH::mma(cf, yf[NTB + tb], zim[ta][tb]);
+        zim[ta][tb] = MH::mma(nsf, yf[tb], zim[ta][tb]);
+      }
+    }
+    if (q.j == NJ - 1) {
+      // lane holds Z[16 ta + 4 g + i][NTB r16 + tb]: NTB consecutive complex
+      _Float16* o = out + q.p * (int64_t)a.Ka * a.Kb * 2;
+      const int tb0 = NTB * r16;
+#pragma unroll
+      for (int ta = 0; ta < NTA; ++ta)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int t_a = ta * 16 + 4 * g + i;
+          if (t_a >= a.Ka) continue;
+          _Float16* d = o + ((int64_t)t_a * a.Kb + tb0) * 2;
+          _Float16 v[2 * NTB];
+#pragma unroll
+          for (int tb = 0; tb < NTB; ++tb) {
+            v[2 * tb] = to_h(zre[ta][tb][i] * a.scaleB);
+            v[2 * tb + 1] = to_h(zim[ta][tb][i] * a.scaleB);
+          }
+          // Kb % 4 == 0 (dispatcher) and NTB <= 4: a lane's NTB columns are
+          // either all below Kb or all past it
+          if (tb0 < a.Kb) {
+            if constexpr (NTB == 1) {
+              *reinterpret_cast<h2*>(d) = h2{v[0], v[1]};
+            } else if constexpr (NTB == 2) {
+              *reinterpret_cast<h4*>(d) = h4{v[0], v[1], v[2], v[3]};
+            } else {
+              *reinterpret_cast<h8*>(d) = h8{v[0], v[1], v[2], v[3], v[4], v[5], v[6], v[7]};
+            }
+          }
+        }
+    }
+  };
+
+  // Each wave walks its planes p = wave_id, wave_id + W, ... in 32-row blocks.
+  // Two register buffers in fixed roles (loop unrolled by two): a buffer is
+  // refilled with the block two ahead as soon as step A has consumed it, so
+  // those loads overlap this block's step B and the next block's step A.
+  Pos q0{(int64_t)blockIdx.x * CH_NW + wave, 0};
+  Pos q1 = next(q0);
+  u32x4 b0[2][NKA], b1[2][NKA];
+  h8 yf[NCT];
+  // table loads first: the barrier then waits for them only, while the
+  // first two row blocks stay in flight
+  st.load(reinterpret_cast<const _Float16*>(a.twAc), a.Nbp, NCT * 16, NKA * KS, zr);
+  sc.load(reinterpret_cast<const _Float16*>(a.cBc), a.NaC, NTA * 16, a.NaC, zr);
+  ss.load(reinterpret_cast<const _Float16*>(a.sBc), a.NaC, NTA * 16, a.NaC, zr);
+  if constexpr (TANH) sl.load(reinterpret_cast<const _Float16*>(a.lut), 0, 1, LUT_HALVES, zr);
+  __builtin_amdgcn_sched_barrier(0);
+  load(q0, b0);
+  __builtin_amdgcn_sched_barrier(0);  // keep the two blocks' loads in order
+  load(q1, b1);
+  st.store(sT, LDT, NCT * 16, NKA * KS);
+  sc.store(sEc, LDE, NTA * 16, a.NaC);
+  ss.store(sEs, LDE, NTA * 16, a.NaC);
+  if constexpr (TANH) sl.store(sLut, 0, 1, LUT_HALVES);
+  __syncthreads();  // tables staged
+  for (;;) {
+    if (q0.p >= a.planes) break;
+    step_a(b0, yf);
+    const Pos c0 = q0;
+    q0 = next(q1);
+    load(q0, b0);
+    step_b(c0, yf);
+    if (q1.p >= a.planes) break;
+    step_a(b1, yf);
+    const Pos c1 = q1;
+    q1 = next(q0);
+    load(q1, b1);
+    step_b(c1, yf);
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Inverse.  Template: NG = Nb64 / 64 output column groups, NTB = Kbp / 16,
+// NKZ = Kap / 32 k-steps of step B'.  EPI multiplies by 1 - tanh(x)^2.
+//
+// Step B' for one 16-row output tile computes V^T[t_b][n_a] (complex) with
+// Z^T as the A operand (gathered from global memory, k = t_a) and the
+// leading-axis table as B.  Its D registers hold V^T rows t_b = 16 tt + 4 g
+// + i, which are the k-slots of step A' (y^T = T'^T V'^T); the last-axis
+// table column 32 ks + 8 g + e names (part, t_b) to match.  Row R of output
+// tile T covers n_b = 64 (T / 4) + 16 (R / 4) + 4 (T % 4) + R % 4, so a lane
+// holds 16 consecutive n_b of its row per group of four tiles.
+// ---------------------------------------------------------------------------
+template <int NG, int NTB, int NKZ, bool EPI>
+__global__ __launch_bounds__(CH_NW * 64, 2) void c2r_chain_kernel(C2RArgs a) {
+  constexpr int NYT = 4 * NG;  // output tiles (16 columns each) per row tile
+  constexpr int LDI = 2 * NTB * 16 + PADH;
+  extern __shared__ __align__(16) unsigned char smem[];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int r16 = lane & 15, g = lane >> 4;
+  const int LDK = a.Kap + PADH;
+  const int NAT = (a.Na + 15) / 16;
+  constexpr int LUTH = EPI ? LUT_HALVES : 0;
+  _Float16* sLut = reinterpret_cast<_Float16*>(smem);  // 1 - tanh^2 of each fp16 code
+  _Float16* sTI = sLut + LUTH;                         // [NG * 64][LDI]
+  _Float16* sCI = sTI + NG * 64 * LDI;                 // [NAT * 16][LDK]
+  _Float16* sSI = sCI + NAT * 16 * LDK;
+  const _Float16* zin = reinterpret_cast<const _Float16*>(a.in);
+  const _Float16* xin = reinterpret_cast<const _Float16*>(a.x);
+  const _Float16* zr = reinterpret_cast<const _Float16*>(a.zeros);
+  _Float16* yout = reinterpret_cast<_Float16*>(a.out);
+
+  // tables: 64 NG rows x 4 NTB pieces, and <= 128 rows x 4 NKZ pieces
+  constexpr int PT = (NG * 64 * NTB * 4 + CH_NW * 64 - 1) / (CH_NW * 64);
+  constexpr int PE = (128 * NKZ * 4 + CH_NW * 64 - 1) / (CH_NW * 64);
+  Stager<PT> st;
+  Stager<PE> sc, ss;
+  Stager<EPI ? LUT_HALVES / 8 / (CH_NW * 64) : 1> sl;
+
+  const int64_t plane = (int64_t)a.Na * a.Nb;
+  const int64_t zplane = (int64_t)a.Ka * a.Kb * 2;
+  const int64_t W = (int64_t)gridDim.x * CH_NW;
+  auto next = [&](Pos q) -> Pos { return q.j + 1 < NAT ? Pos{q.p, q.j + 1} : Pos{q.p + W, 0}; };
+
+  // Spectrum plane as MFMA A operands, natural layout: lane (r16, g) holds
+  // row t_a = 16 rt + r16, complex t_b = 16 kz + 4 g .. + 4 (16-byte loads).
+  auto load_z = [&](int64_t p, u32x4 (&buf)[2 * NKZ][NTB]) {
+    const bool pok = p < a.planes;
+    const _Float16* base = zin + (pok ? p : 0) * zplane;
+#pragma unroll
+    for (int rt = 0; rt < 2 * NKZ; ++rt)
+#pragma unroll
+      for (int kz = 0; kz < NTB; ++kz) {
+        const int ta = 16 * rt + r16, tb = 16 * kz + 4 * g;
+        const bool ok = pok && ta < a.Ka && tb < a.Kb;
+        buf[rt][kz] =
+            *reinterpret_cast<const u32x4*>(ok ? base + ((int64_t)ta * a.Kb + tb) * 2 : zr);
+      }
+  };
+  // epilogue input of row tile (p, j): row 16 j + r16, columns 64 G + 16 g + 8 h
+  constexpr int XG = EPI ? NG : 1;
+  auto load_x = [&](Pos q, u32x4 (&buf)[XG][2]) {
+    if constexpr (EPI) {
+      const bool pok = q.p < a.planes;
+      const _Float16* base = xin + (pok ? q.p : 0) * plane;
+      const int row = 16 * q.j + r16;
+#pragma unroll
+      for (int G = 0; G < NG; ++G)
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+          const int col = 64 * G + 16 * g + 8 * h;
+          const bool ok = pok && row < a.Na && col < a.Nb;
+          buf[G][h] = *reinterpret_cast<const u32x4*>(ok ? base + (int64_t)row * a.Nb + col : zr);
+        }
+    }
+  };
+
+  h8 zfr[NTB][NKZ], zfi[NTB][NKZ];
+  // Selection operands that move (re, im) of a 16x32 block of Z into a D
+  // tile of its transpose: B[k][j] = 1 where k = 2 j (re) or 2 j + 1 (im).
+  h8 selr, seli;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    selr[e] = (_Float16)(8 * g + e == 2 * r16 ? 1.0f : 0.0f);
+    seli[e] = (_Float16)(8 * g + e == 2 * r16 + 1 ? 1.0f : 0.0f);
+  }
+
+  auto process = [&](Pos q, const u32x4 (&xb)[XG][2]) {
+    if (q.j == 0) {
+      // this plane's spectrum (its loads overlap the epilogue inputs already
+      // in flight), transposed by the selection products (exact): D lane
+      // (r16, g) gets Re/Im Z[16 rt + 4 g + i][16 kz + r16]; the step-B'
+      // k-step ks takes row tiles 2 ks (slots 0..3) and 2 ks + 1 (4..7)
+      u32x4 zraw[2 * NKZ][NTB];
+      load_z(q.p, zraw);
+#pragma unroll
+      for (int kz = 0; kz < NTB; ++kz)
+#pragma unroll
+        for (int ks = 0; ks < NKZ; ++ks)
+#pragma unroll
+          for (int hh = 0; hh < 2; ++hh) {
+            const h8 av = u_as_h8(zraw[2 * ks + hh][kz]);
+            const f4 dr = MH::mma(av, selr, f4zero());
+            const f4 di = MH::mma(av, seli, f4zero());
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+              zfr[kz][ks][4 * hh + i] = to_h(dr[i]);
+              zfi[kz][ks][4 * hh + i] = to_h(di[i]);
+            }
+          }
+    }
+    // ---- step B': V^T[t_b][n_a] = sum_t_a Z^T[t_b][t_a] (c + i s)[t_a][n_a] -----
+    f4 vr[NTB], vi[NTB];
+#pragma unroll
+    for (int tt = 0; tt < NTB; ++tt) vr[tt] = vi[tt] = f4zero();
+#pragma unroll
+    for (int ks = 0; ks < NKZ; ++ks) {
+      const int eo = (16 * q.j + r16) * LDK + 32 * ks + 8 * g;
+      const h8 cf = MH::ld(sCI + eo), sf = MH::ld(sSI + eo);
+      const h8 nsf = -sf;
+#pragma unroll
+      for (int tt = 0; tt < NTB; ++tt) {
+        vr[tt] = MH::mma(zfr[tt][ks], cf, vr[tt]);
+        vr[tt] = MH::mma(zfi[tt][ks], nsf, vr[tt]);
+        vi[tt] = MH::mma(zfr[tt][ks], sf, vi[tt]);
+        vi[tt] = MH::mma(zfi[tt][ks], cf, vi[tt]);
+      }
+    }
+    // pairs (part, tile) in the order Re tiles, then Im tiles; k-step ks of
+    // step A' takes pairs 2 ks (slots 0..3) and 2 ks + 1 (slots 4..7)
+    h8 vf[NTB];
+#pragma unroll
+    for (int ks = 0; ks < NTB; ++ks)
+#pragma unroll
+      for (int hh = 0; hh < 2; ++hh) {
+        const int pi = 2 * ks + hh;
+        const f4& src = pi < NTB ? vr[pi] : vi[pi - NTB];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) vf[ks][4 * hh + i] = to_h(src[i]);
+      }
+    // ---- step A': y^T[n_b][n_a] = sum_k T'^T[n_b][k] V'^T[k][n_a] --------------
+    f4 yacc[NYT];
+#pragma unroll
+    for (int t = 0; t < NYT; ++t) yacc[t] = f4zero();
+#pragma unroll
+    for (int ks = 0; ks < NTB; ++ks)
+#pragma unroll
+      for (int t = 0; t < NYT; ++t) {
+        const h8 tf = MH::ld(sTI + (16 * t + r16) * LDI + 32 * ks + 8 * g);
+        yacc[t] = MH::mma(tf, vf[ks], yacc[t]);
+      }
+    // ---- epilogue: lane holds y[16 j + r16][64 G + 16 g .. + 16] ---------------
+    const int n_a = 16 * q.j + r16;
+    _Float16* yrow = yout + q.p * plane + (int64_t)n_a * a.Nb;
+#pragma unroll
+    for (int G = 0; G < NG; ++G) {
+      float v[16];
+#pragma unroll
+      for (int tq = 0; tq < 4; ++tq)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) v[4 * tq + i] = yacc[4 * G + tq][i] * a.scale;
+      if constexpr (EPI) {
+        // 1 - tanh(x)^2, rounded to fp16, looked up per fp16 code
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+          const h8 fv = u_as_h8(lut_u4<false>(sLut, xb[G][h]));
+#pragma unroll
+          for (int e = 0; e < 8; ++e) v[8 * h + e] *= (float)fv[e];
+        }
+      }
+      const int n_b = 64 * G + 16 * g;
+      // Nb % 16 == 0 (dispatcher): 16 columns are all in range or all out
+      if (n_a < a.Na && n_b < a.Nb) {
+        h8 o0, o1;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          o0[e] = to_h(v[e]);
+          o1[e] = to_h(v[8 + e]);
+        }
+        *reinterpret_cast<h8*>(yrow + n_b) = o0;
+        *reinterpret_cast<h8*>(yrow + n_b + 8) = o1;
+      }
+    }
+  };
+
+  Pos q0{(int64_t)blockIdx.x * CH_NW + wave, 0};
+  Pos q1 = next(q0), q2 = next(q1);
+  u32x4 x0[XG][2], x1[XG][2], x2[XG][2];
+  st.load(reinterpret_cast<const _Float16*>(a.twIc), 2 * NTB * 16, NG * 64, 2 * NTB * 16, zr);
+  sc.load(reinterpret_cast<const _Float16*>(a.cIc), a.Kap, NAT * 16, a.Kap, zr);
+  ss.load(reinterpret_cast<const _Float16*>(a.sIc), a.Kap, NAT * 16, a.Kap, zr);
+  if constexpr (EPI) sl.load(reinterpret_cast<const _Float16*>(a.lut), 0, 1, LUT_HALVES, zr);
+  __builtin_amdgcn_sched_barrier(0);
+  load_x(q0, x0);
+  __builtin_amdgcn_sched_barrier(0);  // keep the first blocks' loads in order
+  load_x(q1, x1);
+  st.store(sTI, LDI, NG * 64, 2 * NTB * 16);
+  sc.store(sCI, LDK, NAT * 16, a.Kap);
+  ss.store(sSI, LDK, NAT * 16, a.Kap);
+  if constexpr (EPI) sl.store(sLut, 0, 1, LUT_HALVES);
+  __syncthreads();  // tables staged
+  for (;;) {
+    load_x(q2, x2);
+    if (q0.p >= a.planes) break;
+    process(q0, x0);
+    q0 = next(q2);
+    load_x(q0, x0);
+    if (q1.p >= a.planes) break;
+    process(q1, x1);
+    q1 = next(q0);
+    load_x(q1, x1);
+    if (q2.p >= a.planes) break;
+    process(q2, x2);
+    q2 = next(q1);
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Dispatch
+// ---------------------------------------------------------------------------
+size_t r2c_chain_lds_bytes(int nka, int ntb, int nta, int NaC, bool tanh_lut) {
+  return sizeof(_Float16) * ((tanh_lut ? (size_t)LUT_HALVES : 0) +
+                             (size_t)2 * ntb * 16 * (nka * KS + PADH) +
+                             (size_t)2 * nta * 16 * (NaC + PADH));
+}
+
+size_t c2r_chain_lds_bytes(int ng, int ntb, int Kap, int Na, bool sech2_lut) {
+  const int nat = (Na + 15) / 16;
+  return sizeof(_Float16) * ((sech2_lut ? (size_t)LUT_HALVES : 0) +
+                             (size_t)ng * 64 * (2 * ntb * 16 + PADH) +
+                             (size_t)2 * nat * 16 * (Kap + PADH));
+}
+
+// Kernels above 64 KiB of LDS must raise their dynamic-LDS limit first.
+template <typename K>
+static hipError_t allow_lds(K kern, size_t lds) {
+  if (lds <= 64 * 1024) return hipSuccess;
+  return hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
+                             hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+}
+
+#define R2C_CHAIN_SHAPES(X) X(2, 1, 1) X(2, 1, 2) X(2, 2, 2) X(4, 1, 1) X(4, 1, 2) X(4, 2, 2) \
+  X(4, 2, 4)
+#define C2R_CHAIN_SHAPES(X) X(1, 1, 1) X(1, 1, 2) X(2, 1, 1) X(2, 1, 2) X(2, 2, 1) X(2, 2, 2)
+
+bool r2c_chain_has(int nka, int ntb, int nta) {
+#define HAS(A, B, C) if (nka == A && ntb == B && nta == C) return true;
+  R2C_CHAIN_SHAPES(HAS)
+#undef HAS
+  return false;
+}
+
+bool c2r_chain_has(int ng, int ntb, int nkz) {
+#define HAS(A, B, C) if (ng == A && ntb == B && nkz == C) return true;
+  C2R_CHAIN_SHAPES(HAS)
+#undef HAS
+  return false;
+}
+
+hipError_t launch_r2c_chain(const R2CArgs& a, int nka, int ntb, int nta, int grid, size_t lds,
+                            hipStream_t s) {
+#define R2C_CH(NKA_, NTB_, NTA_)                                                      \
+  if (nka == NKA_ && ntb == NTB_ && nta == NTA_) {                                    \
+    auto kern = a.do_tanh ? r2c_chain_kernel<NKA_, NTB_, NTA_, true>                  \
+                          : r2c_chain_kernel<NKA_, NTB_, NTA_, false>;                \
+    hipError_t e = allow_lds(kern, lds);                                              \
+    if (e != hipSuccess) return e;                                                    \
+    hipLaunchKernelGGL(kern, dim3(grid), dim3(CH_NW * 64), lds, s, a);                \
+    return hipGetLastError();                                                         \
+  }
+  R2C_CHAIN_SHAPES(R2C_CH)
+#undef R2C_CH
+  return hipErrorNotSupported;
+}
+
+hipError_t launch_c2r_chain(const C2RArgs& a, int ng, int ntb, int nkz, int grid, size_t lds,
+                            hipStream_t s) {
+#define C2R_CH(NG_, NTB_, NKZ_)                                                       \
+  if (ng == NG_ && ntb == NTB_ && nkz == NKZ_) {                                      \
+    auto kern = a.epilogue ? c2r_chain_kernel<NG_, NTB_, NKZ_, true>                  \
+                           : c2r_chain_kernel<NG_, NTB_, NKZ_, false>;                \
+    hipError_t e = allow_lds(kern, lds);                                              \
+    if (e != hipSuccess) return e;                                                    \
+    hipLaunchKernelGGL(kern, dim3(grid), dim3(CH_NW * 64), lds, s, a);                \
+    return hipGetLastError();                                                         \
+  }
+  C2R_CHAIN_SHAPES(C2R_CH)
+#undef C2R_CH
+  return hipErrorNotSupported;
+}
+
+}  // namespace fno

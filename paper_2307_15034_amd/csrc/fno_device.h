@@ -60,9 +60,21 @@ struct MM<float> {
 
 __device__ __forceinline__ f4 f4zero() { return f4{0.0f, 0.0f, 0.0f, 0.0f}; }
 
-// tanh in fp32 through the device math library (rounds correctly to fp16 for
-// every fp16 input; limits +-1 at +-inf, NaN propagates).
-__device__ __forceinline__ float tanh_f32(float x) { return tanhf(x); }
+// tanh in fp32 without branches (lanes of one wave see mixed magnitudes, and
+// a branchy tanh runs both paths): for |x| < 1/16 the odd series
+// x (1 - x^2/3 + 2 x^4/15) (truncation < 3e-9 relative there), otherwise
+// sign(x) (1 - e) / (1 + e) with e = exp(-2|x|) (no cancellation for
+// |x| >= 1/16).  Both are evaluated and one is selected.  Rounds to the
+// correctly rounded fp16 value for every fp16 input; +-inf -> +-1, NaN -> NaN.
+__device__ __forceinline__ float tanh_f32(float x) {
+  const float ax = __builtin_fabsf(x);
+  const float e = __builtin_amdgcn_exp2f(ax * -2.8853900817779268f);  // exp(-2|x|)
+  const float big = (1.0f - e) * __builtin_amdgcn_rcpf(1.0f + e);
+  const float x2 = x * x;
+  const float small = x * __builtin_fmaf(x2, __builtin_fmaf(x2, 0.13333333333f, -0.33333333333f),
+                                         1.0f);
+  return ax < 0.0625f ? small : __builtin_copysignf(big, x);
+}
 
 // Round-to-nearest-even conversions to the storage type.
 __device__ __forceinline__ _Float16 to_h(float v) { return (_Float16)v; }

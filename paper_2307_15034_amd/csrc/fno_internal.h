@@ -30,6 +30,12 @@ struct R2CArgs {
   float scaleA, scaleB;
   int do_tanh;
   int vec;          // 1 if Nb allows 16-byte row loads
+  // chained fast path (fp16): permuted copies of the tables
+  const void* twAc; // [2*Kbp][Nbp]: row 16 ct + r: part ct / (Kbp/16) of t = (Kbp/16) r + ct % (Kbp/16)
+  const void* cBc;  // [Kap16][NaC]: column 32 j + 8 q + e holds row n = 32 j + 4 q + e (e < 4)
+  const void* sBc;  //   or 32 j + 16 + 4 q + e - 4 (e >= 4)
+  int NaC;          // Na padded to 32
+  const void* lut;  // fp16 tanh of every non-negative fp16 code (32768 entries)
 };
 
 // Inverse of the above: spectrum [planes][Ka][Kb] -> y [planes][Na][Nb],
@@ -51,6 +57,13 @@ struct C2RArgs {
   float scale;
   int epilogue;     // 0: none, 1: multiply by 1 - tanh(x)^2
   int vec;
+  // chained fast path (fp16): [Nb64][2*Kbp], row 16 T + R holds column
+  // n = 64 (T/4) + 16 (R/4) + 4 (T%4) + R%4; column 32 ks + 8 q + e holds
+  // part/tile pair 2 ks + e/4 (Re tiles first) at t = 16 tile + 4 q + e%4
+  const void* twIc;
+  const void* cIc;  // [Nap][Kap] like cI, sI with column 32 ks + 8 q + e holding
+  const void* sIc;  //   t = 32 ks + 4 q + e (e < 4) or 32 ks + 16 + 4 q + e - 4
+  const void* lut;  // fp16 1 - tanh^2 of every non-negative fp16 code (32768 entries)
 };
 
 // Complex DFT along a middle axis: in [outer][Lin][inner] -> out
@@ -131,12 +144,26 @@ hipError_t launch_scale_complex(float* p, int64_t n, float s, hipStream_t st);
 
 // Persistent fp16 fast paths (planes up to 128 x 256); hipErrorNotSupported
 // when no instantiation matches the shape.
-hipError_t launch_r2c_fast(const R2CArgs& a, int nct, int nka, int rt, int grid, size_t lds,
+// nw: waves per work-group, one per 16-row tile of the plane.
+hipError_t launch_r2c_fast(const R2CArgs& a, int nct, int nka, int nw, int grid, size_t lds,
                            hipStream_t s);
-hipError_t launch_c2r_fast(const C2RArgs& a, int nct, int rt, int nbt, int nkz, int grid,
+hipError_t launch_c2r_fast(const C2RArgs& a, int nct, int nw, int nbt, int nkz, int grid,
                            size_t lds, hipStream_t s);
-size_t r2c_fast_lds_bytes(int nct, int nka, int rt, int Kap16, int Nap);
-size_t c2r_fast_lds_bytes(int nct, int rt, int nbt, int nkz);
+size_t r2c_fast_lds_bytes(int nct, int nka, int nw, int Kap16, int Nap);
+size_t c2r_fast_lds_bytes(int nct, int nw, int nbt, int nkz);
+
+// Chained fp16 transforms, one wavefront per plane (Na <= 128, Nb <= 256):
+// nka = Nbp/32, ntb = Kbp/16, nta = Kap16/16 (forward); ng = Nb64/64,
+// nkz = Kap/32 (inverse).  hipErrorNotSupported when not instantiated.
+hipError_t launch_r2c_chain(const R2CArgs& a, int nka, int ntb, int nta, int grid, size_t lds,
+                            hipStream_t s);
+hipError_t launch_c2r_chain(const C2RArgs& a, int ng, int ntb, int nkz, int grid, size_t lds,
+                            hipStream_t s);
+bool r2c_chain_has(int nka, int ntb, int nta);
+bool c2r_chain_has(int ng, int ntb, int nkz);
+size_t r2c_chain_lds_bytes(int nka, int ntb, int nta, int NaC, bool tanh_lut);
+size_t c2r_chain_lds_bytes(int ng, int ntb, int Kap, int Na, bool sech2_lut);
+constexpr int kChainWaves = 8;  // waves per work-group of the chained kernels
 
 size_t r2c_lds_bytes(int elem, int Kbp, int R);
 size_t c2r_lds_bytes(int elem, int Kbp, int Kap, int R);

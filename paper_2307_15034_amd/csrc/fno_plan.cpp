@@ -228,6 +228,7 @@ struct Geo {
   int Nbp, Kap16;
   int R_f, Nap_f;    // r2c chunking
   int Kap, R_i, Nap_i, Nb64;  // c2r
+  int NaC;           // Na padded to 32 (chained forward tables)
   // leading 3-D axis
   int N1, K1, Lin_f, Linp_f, Lout16_f, Linp_i, Lout16_i;
 };
@@ -236,6 +237,8 @@ struct DevTables {
   void* base = nullptr;
   size_t bytes = 0;
   const void *zeros, *twA, *cB, *sB, *cI, *sI, *twI;
+  const void *twAc, *cBc, *sBc, *twIc, *cIc, *sIc;
+  const void *lutTanh, *lutSech2;
   const void *eFr, *eFi, *eIr, *eIi;
 };
 
@@ -288,6 +291,7 @@ Geo make_geo(const fno_conv_desc* d) {
   g.R_i = (int)std::min<int64_t>(round_up(g.Na, 16), rmaxi);
   g.Nap_i = (int)round_up(g.Na, g.R_i);
   g.Nb64 = (int)round_up(g.Nb, 64);
+  g.NaC = (int)round_up(g.Na, 32);
   if (nd == 3) {
     g.N1 = (int)d->n[0];
     g.K1 = (int)(2 * d->modes[0]);
@@ -360,6 +364,83 @@ void fill_tables(const fno_conv_desc* d, const Geo& g, std::vector<T>& buf,
       buf[oti + (size_t)n * 2 * g.Kbp + t] = (T)c;
       buf[oti + (size_t)n * 2 * g.Kbp + g.Kbp + t] = (T)(-s);
     }
+  // Permuted copies for the chained kernels (whose MFMA results feed the
+  // next MFMA directly).  twAc [2 Kbp][Nbp]: row 16 ct + r holds part
+  // ct / ntb (cos, then -sin) of t = ntb r + ct % ntb.
+  const int ntb = g.Kbp / 16;
+  size_t oac = alloc((size_t)2 * g.Kbp * g.Nbp);
+  for (int ct = 0; ct < 2 * ntb; ++ct)
+    for (int r = 0; r < 16; ++r) {
+      const int part = ct / ntb, t = ntb * r + ct % ntb;
+      if (t >= g.Kb) continue;
+      for (int n = 0; n < g.Nb; ++n) {
+        double c, s;
+        twiddle(t, n, g.Nb, &c, &s);
+        buf[oac + (size_t)(ct * 16 + r) * g.Nbp + n] = (T)(part == 0 ? c : -s);
+      }
+    }
+  // cBc, sBc [Kap16][NaC]: column 32 j + 8 q + e holds row
+  // n = 32 j + 4 q + e (e < 4) or 32 j + 16 + 4 q + (e - 4) (e >= 4)
+  size_t obc = alloc((size_t)g.Kap16 * g.NaC);
+  size_t obs = alloc((size_t)g.Kap16 * g.NaC);
+  for (int t = 0; t < g.Ka; ++t)
+    for (int col = 0; col < g.NaC; ++col) {
+      const int j = col / 32, q = (col % 32) / 8, e = col % 8;
+      const int n = 32 * j + (e < 4 ? 4 * q + e : 16 + 4 * q + (e - 4));
+      if (n >= g.Na) continue;
+      double c, s;
+      twiddle(ka_of(t), n, g.Na, &c, &s);
+      buf[obc + (size_t)t * g.NaC + col] = (T)c;
+      buf[obs + (size_t)t * g.NaC + col] = (T)s;
+    }
+  // twIc [Nb64][2 Kbp]: row 16 T + R holds n = 64 (T/4) + 16 (R/4) + 4 (T%4)
+  // + R%4; column 32 ks + 8 q + e holds pair 2 ks + e/4 (pairs: Re tiles
+  // 0..ntb-1, then Im tiles) at t = 16 tile + 4 q + e%4; Re: cos, Im: -sin
+  size_t oic = alloc((size_t)g.Nb64 * 2 * g.Kbp);
+  for (int row = 0; row < g.Nb64; ++row) {
+    const int tile16 = row / 16, R = row % 16;
+    const int n = 64 * (tile16 / 4) + 16 * (R / 4) + 4 * (tile16 % 4) + R % 4;
+    if (n >= g.Nb) continue;
+    for (int col = 0; col < 2 * g.Kbp; ++col) {
+      const int ks = col / 32, q = (col % 32) / 8, e = col % 8;
+      const int pair = 2 * ks + e / 4;
+      const int part = pair / ntb, tile = pair % ntb;
+      const int t = 16 * tile + 4 * q + e % 4;
+      if (t >= g.Kb) continue;
+      double c, s;
+      twiddle(t, n, g.Nb, &c, &s);
+      buf[oic + (size_t)row * 2 * g.Kbp + col] = (T)(part == 0 ? c : -s);
+    }
+  }
+  // cIc, sIc [Nap_i][Kap]: cI, sI with column 32 ks + 8 q + e holding
+  // t = 32 ks + 4 q + e (e < 4) or 32 ks + 16 + 4 q + (e - 4)
+  size_t oicc = alloc((size_t)g.Nap_i * g.Kap);
+  size_t oics = alloc((size_t)g.Nap_i * g.Kap);
+  for (int n = 0; n < g.Na; ++n)
+    for (int col = 0; col < g.Kap; ++col) {
+      const int ks = col / 32, q = (col % 32) / 8, e = col % 8;
+      const int t = 32 * ks + (e < 4 ? 4 * q + e : 16 + 4 * q + (e - 4));
+      if (t >= g.Ka) continue;
+      double c, s;
+      twiddle(ka_of(t), n, g.Na, &c, &s);
+      buf[oicc + (size_t)n * g.Kap + col] = (T)c;
+      buf[oics + (size_t)n * g.Kap + col] = (T)s;
+    }
+  // Lookup tables over the non-negative fp16 codes 0..0x7fff: tanh and
+  // sech^2 = 1 - tanh^2 of the fp16 value, each rounded once to the storage
+  // type (NaN codes give NaN, +inf gives 1 and 0).
+  size_t olt = alloc(32768);
+  size_t ols = alloc(32768);
+  for (int code = 0; code < 32768; ++code) {
+    const uint16_t bits = (uint16_t)code;
+    _Float16 h;
+    std::memcpy(&h, &bits, 2);
+    const double xv = (double)h;
+    const double th = std::tanh(xv);
+    const double ch = std::cosh(xv);
+    buf[olt + code] = (T)th;
+    buf[ols + code] = (T)(1.0 / (ch * ch));
+  }
   (void)o;
   (void)oc;
   (void)os;
@@ -450,11 +531,19 @@ fno_status build_tables(const fno_conv_desc* d, Plan* pl) {
   pl->t.cI = at(4);
   pl->t.sI = at(5);
   pl->t.twI = at(6);
+  pl->t.twAc = at(7);
+  pl->t.cBc = at(8);
+  pl->t.sBc = at(9);
+  pl->t.twIc = at(10);
+  pl->t.cIc = at(11);
+  pl->t.sIc = at(12);
+  pl->t.lutTanh = at(13);
+  pl->t.lutSech2 = at(14);
   if (pl->g.nd == 3) {
-    pl->t.eFr = at(7);
-    pl->t.eFi = at(8);
-    pl->t.eIr = at(9);
-    pl->t.eIi = at(10);
+    pl->t.eFr = at(15);
+    pl->t.eFi = at(16);
+    pl->t.eIr = at(17);
+    pl->t.eIi = at(18);
   }
   return FNO_OK;
 }
@@ -660,16 +749,34 @@ fno_status run_r2c(const Plan* pl, const void* in, void* spec, void* inter, int6
   }
   a.do_tanh = do_tanh;
   a.vec = (g.Nb % 8) == 0;
+  a.twAc = pl->t.twAc;
+  a.cBc = pl->t.cBc;
+  a.sBc = pl->t.sBc;
+  a.NaC = g.NaC;
+  a.lut = pl->t.lutTanh;
   if (a.planes > 0x7fffffff || (g.nd == 3 && g.B * C > 65535)) return FNO_ERR_UNSUPPORTED;
   bool done = false;
-  if (g.elem == ELEM_F16 && a.vec && g.Nb <= 256 && g.Na <= 128 && g.nct <= 8) {
+  if (g.elem == ELEM_F16 && a.vec && g.Kb % 4 == 0 && g.Nb <= 256 && g.Na <= 128) {
+    const int nka = g.Nbp / 32, ntb = g.Kbp / 16, nta = g.Kap16 / 16;
+    const size_t lds = r2c_chain_lds_bytes(nka, ntb, nta, g.NaC, do_tanh != 0);
+    const int64_t waves = (int64_t)kChainWaves;
+    const int grid = (int)std::min<int64_t>((a.planes + waves - 1) / waves, (int64_t)2 * pl->num_cu);
+    if (lds <= 160 * 1024 && grid > 0 && r2c_chain_has(nka, ntb, nta)) {
+      hipError_t e = timed(do_tanh ? "r2c_plane_tanh" : "r2c_plane", s, [&] {
+        return launch_r2c_chain(a, nka, ntb, nta, grid, lds, s);
+      });
+      if (e == hipSuccess) done = true;
+      else if (e != hipErrorNotSupported) return FNO_ERR_HIP;
+    }
+  }
+  if (!done && g.elem == ELEM_F16 && a.vec && g.Nb <= 256 && g.Na <= 128 && g.nct <= 8) {
     const int nka = g.Nb <= 32 ? 1 : g.Nb <= 64 ? 2 : g.Nb <= 128 ? 4 : 8;
-    const int rt = g.Na <= 64 ? 1 : 2;
-    const size_t lds = r2c_fast_lds_bytes(g.nct, nka, rt, g.Kap16, g.Nap_f);
+    const int nw = g.Na <= 64 ? 4 : 8;
+    const size_t lds = r2c_fast_lds_bytes(g.nct, nka, nw, g.Kap16, g.Nap_f);
     const int grid = (int)std::min<int64_t>(a.planes, (int64_t)2 * pl->num_cu);
     if (lds <= 80 * 1024) {
       hipError_t e = timed(do_tanh ? "r2c_plane_tanh" : "r2c_plane", s, [&] {
-        return launch_r2c_fast(a, g.nct, nka, rt, grid, lds, s);
+        return launch_r2c_fast(a, g.nct, nka, nw, grid, lds, s);
       });
       if (e == hipSuccess) done = true;
       else if (e != hipErrorNotSupported) return FNO_ERR_HIP;
@@ -737,16 +844,32 @@ fno_status run_c2r(const Plan* pl, const void* spec, void* out, void* inter, int
   a.epilogue = x_epi != nullptr;
   a.vec = (g.Nb % 8) == 0;
   if (a.planes > 0x7fffffff) return FNO_ERR_UNSUPPORTED;
+  a.twIc = pl->t.twIc;
+  a.cIc = pl->t.cIc;
+  a.sIc = pl->t.sIc;
+  a.lut = pl->t.lutSech2;
   const char* kname = x_epi ? "c2r_plane_tanh_grad" : "c2r_plane";
-  if (g.elem == ELEM_F16 && a.vec && g.Nb <= 256 && g.Na <= 128 && g.nct <= 8 && g.Kap <= 128) {
+  if (g.elem == ELEM_F16 && g.Nb % 16 == 0 && g.Kb % 4 == 0 && g.Nb <= 256 && g.Na <= 128) {
+    const int ng = g.Nb64 / 64, ntb = g.Kbp / 16, nkz = g.Kap / 32;
+    const size_t lds = c2r_chain_lds_bytes(ng, ntb, g.Kap, g.Na, x_epi != nullptr);
+    const int64_t waves = (int64_t)kChainWaves;
+    const int grid = (int)std::min<int64_t>((a.planes + waves - 1) / waves, (int64_t)2 * pl->num_cu);
+    if (lds <= 160 * 1024 && grid > 0 && c2r_chain_has(ng, ntb, nkz)) {
+      hipError_t e = timed(kname, s, [&] { return launch_c2r_chain(a, ng, ntb, nkz, grid, lds, s); });
+      if (e == hipSuccess) return FNO_OK;
+      if (e != hipErrorNotSupported) return FNO_ERR_HIP;
+    }
+  }
+  if (g.elem == ELEM_F16 && a.vec && g.Kb % 4 == 0 && g.Nb <= 256 && g.Na <= 128 && g.nct <= 8 &&
+      g.Kap <= 128) {
     const int nbt = (g.Nb + 63) / 64;
-    const int rt = g.Na <= 64 ? 1 : 2;
+    const int nw = g.Na <= 64 ? 4 : 8;
     const int nkz = g.Kap / 32;
-    const size_t lds = c2r_fast_lds_bytes(g.nct, rt, nbt, nkz);
+    const size_t lds = c2r_fast_lds_bytes(g.nct, nw, nbt, nkz);
     const int grid = (int)std::min<int64_t>(a.planes, (int64_t)2 * pl->num_cu);
     if (lds <= 80 * 1024) {
       hipError_t e = timed(kname, s, [&] {
-        return launch_c2r_fast(a, g.nct, rt, nbt, nkz, grid, lds, s);
+        return launch_c2r_fast(a, g.nct, nw, nbt, nkz, grid, lds, s);
       });
       if (e == hipSuccess) return FNO_OK;
       if (e != hipErrorNotSupported) return FNO_ERR_HIP;
