@@ -85,6 +85,33 @@ def step_bytes(wl, es, caches=True):
     return int(total)
 
 
+def kernel_sources_hash():
+    """Hash of the HIP/C++ sources; counter-derived traffic is reported only
+    while the kernels are the ones the counters were taken on."""
+    import hashlib
+    h = hashlib.sha256()
+    c = os.path.join(ROOT, "paper_2307_15034_amd", "csrc")
+    for f in sorted(os.listdir(c)):
+        h.update(f.encode())
+        with open(os.path.join(c, f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(wl_name, kernel):
+    """HBM bytes per launch of `kernel` from the committed rocprofv3
+    FETCH_SIZE / WRITE_SIZE summary (copy-kernel calibrated), or None."""
+    path = os.path.join(ROOT, "profiles", f"traffic_{wl_name}.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        t = json.load(f)
+    if t.get("src_hash") != kernel_sources_hash():
+        return None
+    k = t.get("kernels", {}).get(kernel)
+    return int(k["bytes"]) if k else None
+
+
 def cpu_baseline(wl, x, w, gy, prec, seconds):
     """The float64 oracle, as it stands, on a bounded sample of the workload:
     whole batch samples (fwd + bwd_data + bwd_weight), repeated until about
@@ -212,7 +239,8 @@ def main():
     dk = kernels[dom]
     roof = {"bound": "hbm", "kernel": dom, "achieved": round(dk.get("gbs", 0.0), 1),
             "peak": HBM_PEAK_GBS, "unit": "GB/s",
-            "frac": round(dk.get("gbs", 0.0) / HBM_PEAK_GBS, 4), "traffic": None,
+            "frac": round(dk.get("gbs", 0.0) / HBM_PEAK_GBS, 4),
+            "traffic": measured_traffic(wl.name, dom),
             "avg_ms": round(dk["avg_ms"], 5), "alg_bytes": dk.get("alg_bytes")}
 
     out = {
