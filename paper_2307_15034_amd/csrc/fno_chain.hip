@@ -260,21 +260,21 @@ __global__ __launch_bounds__(CH_NW * 64, 2) void r2c_chain_kernel(R2CArgs a) {
   Pos q1 = next(q0);
   u32x4 b0[2][NKA], b1[2][NKA];
   h8 yf[NCT];
-  // table loads first: the barrier then waits for them only, while the
-  // first two row blocks stay in flight
+  // Tables first, on their own: every wave needs all of them before its
+  // first block, and row-block loads issued alongside would queue ahead of
+  // other waves' table loads.
   st.load(reinterpret_cast<const _Float16*>(a.twAc), a.Nbp, NCT * 16, NKA * KS, zr);
   sc.load(reinterpret_cast<const _Float16*>(a.cBc), a.NaC, NTA * 16, a.NaC, zr);
   ss.load(reinterpret_cast<const _Float16*>(a.sBc), a.NaC, NTA * 16, a.NaC, zr);
   if constexpr (TANH) sl.load(reinterpret_cast<const _Float16*>(a.lut), 0, 1, LUT_HALVES, zr);
-  __builtin_amdgcn_sched_barrier(0);
-  load(q0, b0);
-  __builtin_amdgcn_sched_barrier(0);  // keep the two blocks' loads in order
-  load(q1, b1);
   st.store(sT, LDT, NCT * 16, NKA * KS);
   sc.store(sEc, LDE, NTA * 16, a.NaC);
   ss.store(sEs, LDE, NTA * 16, a.NaC);
   if constexpr (TANH) sl.store(sLut, 0, 1, LUT_HALVES);
   __syncthreads();  // tables staged
+  load(q0, b0);
+  __builtin_amdgcn_sched_barrier(0);  // keep the two blocks' loads in order
+  load(q1, b1);
   for (;;) {
     if (q0.p >= a.planes) break;
     step_a(b0, yf);
@@ -478,19 +478,19 @@ __global__ __launch_bounds__(CH_NW * 64, 2) void c2r_chain_kernel(C2RArgs a) {
   Pos q0{(int64_t)blockIdx.x * CH_NW + wave, 0};
   Pos q1 = next(q0), q2 = next(q1);
   u32x4 x0[XG][2], x1[XG][2], x2[XG][2];
+  // tables first, on their own (see the forward kernel)
   st.load(reinterpret_cast<const _Float16*>(a.twIc), 2 * NTB * 16, NG * 64, 2 * NTB * 16, zr);
   sc.load(reinterpret_cast<const _Float16*>(a.cIc), a.Kap, NAT * 16, a.Kap, zr);
   ss.load(reinterpret_cast<const _Float16*>(a.sIc), a.Kap, NAT * 16, a.Kap, zr);
   if constexpr (EPI) sl.load(reinterpret_cast<const _Float16*>(a.lut), 0, 1, LUT_HALVES, zr);
-  __builtin_amdgcn_sched_barrier(0);
-  load_x(q0, x0);
-  __builtin_amdgcn_sched_barrier(0);  // keep the first blocks' loads in order
-  load_x(q1, x1);
   st.store(sTI, LDI, NG * 64, 2 * NTB * 16);
   sc.store(sCI, LDK, NAT * 16, a.Kap);
   ss.store(sSI, LDK, NAT * 16, a.Kap);
   if constexpr (EPI) sl.store(sLut, 0, 1, LUT_HALVES);
   __syncthreads();  // tables staged
+  load_x(q0, x0);
+  __builtin_amdgcn_sched_barrier(0);  // keep the first blocks' loads in order
+  load_x(q1, x1);
   for (;;) {
     load_x(q2, x2);
     if (q0.p >= a.planes) break;

@@ -165,6 +165,11 @@ size_t r2c_chain_lds_bytes(int nka, int ntb, int nta, int NaC, bool tanh_lut);
 size_t c2r_chain_lds_bytes(int ng, int ntb, int Kap, int Na, bool sech2_lut);
 constexpr int kChainWaves = 8;  // waves per work-group of the chained kernels
 
+// fp16 contraction / weight gradient on slabs of 16 modes (K % 16 == 0);
+// hipErrorNotSupported otherwise.
+hipError_t launch_contract_slab(const ContractArgs& a, hipStream_t s);
+hipError_t launch_wgrad_slab(const WgradArgs& a, hipStream_t s);
+
 size_t r2c_lds_bytes(int elem, int Kbp, int R);
 size_t c2r_lds_bytes(int elem, int Kbp, int Kap, int R);
 size_t axis_lds_bytes(int elem, int Linp);

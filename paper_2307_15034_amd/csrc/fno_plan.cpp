@@ -898,7 +898,10 @@ fno_status run_contract(const Plan* pl, const void* in, const void* w, void* out
   a.Nb = g.Nb;
   a.scale = 1.0f;
   if (g.K > 0x7fffffff / 2) return FNO_ERR_UNSUPPORTED;
-  FNO_HIP(timed(adjoint ? "contract_adjoint" : "contract", s, [&] { return launch_contract(g.elem, a, s); }));
+  const bool slab = g.elem == ELEM_F16 && g.K % 16 == 0;
+  FNO_HIP(timed(adjoint ? "contract_adjoint" : "contract", s, [&] {
+    return slab ? launch_contract_slab(a, s) : launch_contract(g.elem, a, s);
+  }));
   return FNO_OK;
 }
 
@@ -1413,7 +1416,10 @@ fno_status fno_spectral_conv_bwd_weight(const fno_conv_desc* d, const void* x, c
     a.Kb = g.Kb;
     a.Nb = g.Nb;
     a.scale = (float)std::sqrt((double)g.N);
-    FNO_HIP(timed("wgrad", s, [&] { return launch_wgrad(g.elem, a, s); }));
+    const bool slab = g.elem == ELEM_F16 && g.K % 16 == 0;
+    FNO_HIP(timed("wgrad", s, [&] {
+      return slab ? launch_wgrad_slab(a, s) : launch_wgrad(g.elem, a, s);
+    }));
     return FNO_OK;
   }
   return run_tucker_wgrad(d, pl, xh, gh, w, gw, tsc, s);
