@@ -232,8 +232,11 @@ def main():
         e = {"launches_per_step": n / args.profile_steps, "avg_ms": avg,
              "ms_per_step": per_step}
         if kb.get(name):
-            e["alg_bytes"] = int(kb[name])
-            e["gbs"] = kb[name] / (avg / 1e3) / 1e9
+            # kernel_bytes() is per whole batch; a call may split the batch
+            # into several launches (halves on two streams)
+            per_launch = kb[name] / max(n / args.profile_steps, 1.0)
+            e["alg_bytes"] = int(per_launch)
+            e["gbs"] = per_launch / (avg / 1e3) / 1e9
         kernels[name] = e
     dom = max(kernels, key=lambda k: kernels[k]["ms_per_step"])
     dk = kernels[dom]

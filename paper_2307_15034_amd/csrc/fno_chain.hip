@@ -260,21 +260,22 @@ __global__ __launch_bounds__(CH_NW * 64, 2) void r2c_chain_kernel(R2CArgs a) {
   Pos q1 = next(q0);
   u32x4 b0[2][NKA], b1[2][NKA];
   h8 yf[NCT];
-  // Tables first, on their own: every wave needs all of them before its
-  // first block, and row-block loads issued alongside would queue ahead of
-  // other waves' table loads.
+  // Load order: the first row block, the tables, the second row block.  The
+  // first block and the tables are what the first step needs; the barrier
+  // waits for them only, and the second block streams in behind.
+  load(q0, b0);
+  __builtin_amdgcn_sched_barrier(0);
   st.load(reinterpret_cast<const _Float16*>(a.twAc), a.Nbp, NCT * 16, NKA * KS, zr);
   sc.load(reinterpret_cast<const _Float16*>(a.cBc), a.NaC, NTA * 16, a.NaC, zr);
   ss.load(reinterpret_cast<const _Float16*>(a.sBc), a.NaC, NTA * 16, a.NaC, zr);
   if constexpr (TANH) sl.load(reinterpret_cast<const _Float16*>(a.lut), 0, 1, LUT_HALVES, zr);
+  __builtin_amdgcn_sched_barrier(0);
+  load(q1, b1);
   st.store(sT, LDT, NCT * 16, NKA * KS);
   sc.store(sEc, LDE, NTA * 16, a.NaC);
   ss.store(sEs, LDE, NTA * 16, a.NaC);
   if constexpr (TANH) sl.store(sLut, 0, 1, LUT_HALVES);
   __syncthreads();  // tables staged
-  load(q0, b0);
-  __builtin_amdgcn_sched_barrier(0);  // keep the two blocks' loads in order
-  load(q1, b1);
   for (;;) {
     if (q0.p >= a.planes) break;
     step_a(b0, yf);
@@ -377,29 +378,34 @@ __global__ __launch_bounds__(CH_NW * 64, 2) void c2r_chain_kernel(C2RArgs a) {
     seli[e] = (_Float16)(8 * g + e == 2 * r16 + 1 ? 1.0f : 0.0f);
   }
 
+  // A spectrum plane, transposed by the selection products (exact): D lane
+  // (r16, g) gets Re/Im Z[16 rt + 4 g + i][16 kz + r16]; the step-B' k-step
+  // ks takes row tiles 2 ks (slots 0..3) and 2 ks + 1 (4..7).
+  auto transpose_z = [&](const u32x4 (&zraw)[2 * NKZ][NTB]) {
+#pragma unroll
+    for (int kz = 0; kz < NTB; ++kz)
+#pragma unroll
+      for (int ks = 0; ks < NKZ; ++ks)
+#pragma unroll
+        for (int hh = 0; hh < 2; ++hh) {
+          const h8 av = u_as_h8(zraw[2 * ks + hh][kz]);
+          const f4 dr = MH::mma(av, selr, f4zero());
+          const f4 di = MH::mma(av, seli, f4zero());
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            zfr[kz][ks][4 * hh + i] = to_h(dr[i]);
+            zfi[kz][ks][4 * hh + i] = to_h(di[i]);
+          }
+        }
+  };
+  const int64_t first_plane = (int64_t)blockIdx.x * CH_NW + wave;
+
   auto process = [&](Pos q, const u32x4 (&xb)[XG][2]) {
-    if (q.j == 0) {
-      // this plane's spectrum (its loads overlap the epilogue inputs already
-      // in flight), transposed by the selection products (exact): D lane
-      // (r16, g) gets Re/Im Z[16 rt + 4 g + i][16 kz + r16]; the step-B'
-      // k-step ks takes row tiles 2 ks (slots 0..3) and 2 ks + 1 (4..7)
+    if (q.j == 0 && q.p != first_plane) {
+      // a later plane of this wave (the first one is loaded up front)
       u32x4 zraw[2 * NKZ][NTB];
       load_z(q.p, zraw);
-#pragma unroll
-      for (int kz = 0; kz < NTB; ++kz)
-#pragma unroll
-        for (int ks = 0; ks < NKZ; ++ks)
-#pragma unroll
-          for (int hh = 0; hh < 2; ++hh) {
-            const h8 av = u_as_h8(zraw[2 * ks + hh][kz]);
-            const f4 dr = MH::mma(av, selr, f4zero());
-            const f4 di = MH::mma(av, seli, f4zero());
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-              zfr[kz][ks][4 * hh + i] = to_h(dr[i]);
-              zfi[kz][ks][4 * hh + i] = to_h(di[i]);
-            }
-          }
+      transpose_z(zraw);
     }
     // ---- step B': V^T[t_b][n_a] = sum_t_a Z^T[t_b][t_a] (c + i s)[t_a][n_a] -----
     f4 vr[NTB], vi[NTB];
@@ -478,19 +484,27 @@ __global__ __launch_bounds__(CH_NW * 64, 2) void c2r_chain_kernel(C2RArgs a) {
   Pos q0{(int64_t)blockIdx.x * CH_NW + wave, 0};
   Pos q1 = next(q0), q2 = next(q1);
   u32x4 x0[XG][2], x1[XG][2], x2[XG][2];
-  // tables first, on their own (see the forward kernel)
-  st.load(reinterpret_cast<const _Float16*>(a.twIc), 2 * NTB * 16, NG * 64, 2 * NTB * 16, zr);
-  sc.load(reinterpret_cast<const _Float16*>(a.cIc), a.Kap, NAT * 16, a.Kap, zr);
-  ss.load(reinterpret_cast<const _Float16*>(a.sIc), a.Kap, NAT * 16, a.Kap, zr);
-  if constexpr (EPI) sl.load(reinterpret_cast<const _Float16*>(a.lut), 0, 1, LUT_HALVES, zr);
-  st.store(sTI, LDI, NG * 64, 2 * NTB * 16);
-  sc.store(sCI, LDK, NAT * 16, a.Kap);
-  ss.store(sSI, LDK, NAT * 16, a.Kap);
-  if constexpr (EPI) sl.store(sLut, 0, 1, LUT_HALVES);
+  // Load order: the first plane's spectrum, the tables, then the epilogue
+  // inputs of the first two row tiles (needed last).
+  {
+    u32x4 zraw[2 * NKZ][NTB];
+    load_z(q0.p, zraw);
+    __builtin_amdgcn_sched_barrier(0);
+    st.load(reinterpret_cast<const _Float16*>(a.twIc), 2 * NTB * 16, NG * 64, 2 * NTB * 16, zr);
+    sc.load(reinterpret_cast<const _Float16*>(a.cIc), a.Kap, NAT * 16, a.Kap, zr);
+    ss.load(reinterpret_cast<const _Float16*>(a.sIc), a.Kap, NAT * 16, a.Kap, zr);
+    if constexpr (EPI) sl.load(reinterpret_cast<const _Float16*>(a.lut), 0, 1, LUT_HALVES, zr);
+    __builtin_amdgcn_sched_barrier(0);
+    load_x(q0, x0);
+    __builtin_amdgcn_sched_barrier(0);
+    load_x(q1, x1);
+    st.store(sTI, LDI, NG * 64, 2 * NTB * 16);
+    sc.store(sCI, LDK, NAT * 16, a.Kap);
+    ss.store(sSI, LDK, NAT * 16, a.Kap);
+    if constexpr (EPI) sl.store(sLut, 0, 1, LUT_HALVES);
+    transpose_z(zraw);
+  }
   __syncthreads();  // tables staged
-  load_x(q0, x0);
-  __builtin_amdgcn_sched_barrier(0);  // keep the first blocks' loads in order
-  load_x(q1, x1);
   for (;;) {
     load_x(q2, x2);
     if (q0.p >= a.planes) break;
