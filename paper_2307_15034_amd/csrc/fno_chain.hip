@@ -475,8 +475,9 @@ __global__ __launch_bounds__(CH_NW * 64, 2) void c2r_chain_kernel(C2RArgs a) {
           o0[e] = to_h(v[e]);
           o1[e] = to_h(v[8 + e]);
         }
-        *reinterpret_cast<h8*>(yrow + n_b) = o0;
-        *reinterpret_cast<h8*>(yrow + n_b + 8) = o1;
+        // streaming stores: the layer output is not read again by this layer
+        __builtin_nontemporal_store(h8_as_u4(o0), reinterpret_cast<u32x4*>(yrow + n_b));
+        __builtin_nontemporal_store(h8_as_u4(o1), reinterpret_cast<u32x4*>(yrow + n_b + 8));
       }
     }
   };

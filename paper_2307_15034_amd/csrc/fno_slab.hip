@@ -253,8 +253,9 @@ __global__ __launch_bounds__(SL_NT, 4) void slab_kernel(SlabArgs s) {
     if (row < s.nrow && col < s.ncol) {
       const u32x4 val = *reinterpret_cast<const u32x4*>(so + rr * OT::RSO + cc * OT::PS + 4 * v);
       if constexpr (OP == SLAB_WGRAD) {
+        // streaming store: the weight gradient is not read again here
         float* d = reinterpret_cast<float*>(s.out) + (((int64_t)row * s.ncol + col) * s.K + t0) * 2;
-        reinterpret_cast<u32x4*>(d)[v] = val;
+        __builtin_nontemporal_store(val, reinterpret_cast<u32x4*>(d) + v);
       } else {
         _Float16* d =
             reinterpret_cast<_Float16*>(s.out) + (((int64_t)row * s.ncol + col) * s.K + t0) * 2;
