@@ -318,6 +318,9 @@ __global__ __launch_bounds__(CH_NW * 64, 2) void c2r_chain_kernel(C2RArgs a) {
   _Float16* sTI = sLut + LUTH;                         // [NG * 64][LDI]
   _Float16* sCI = sTI + NG * 64 * LDI;                 // [NAT * 16][LDK]
   _Float16* sSI = sCI + NAT * 16 * LDK;
+  // per-wave output staging: 16 rows x 64 columns (one column group)
+  constexpr int LDO = 64 + PADH;
+  _Float16* sOut = sSI + NAT * 16 * LDK + wave * 16 * LDO;
   const _Float16* zin = reinterpret_cast<const _Float16*>(a.in);
   const _Float16* xin = reinterpret_cast<const _Float16*>(a.x);
   const _Float16* zr = reinterpret_cast<const _Float16*>(a.zeros);
@@ -448,8 +451,6 @@ __global__ __launch_bounds__(CH_NW * 64, 2) void c2r_chain_kernel(C2RArgs a) {
         yacc[t] = MH::mma(tf, vf[ks], yacc[t]);
       }
     // ---- epilogue: lane holds y[16 j + r16][64 G + 16 g .. + 16] ---------------
-    const int n_a = 16 * q.j + r16;
-    _Float16* yrow = yout + q.p * plane + (int64_t)n_a * a.Nb;
 #pragma unroll
     for (int G = 0; G < NG; ++G) {
       float v[16];
@@ -466,19 +467,31 @@ __global__ __launch_bounds__(CH_NW * 64, 2) void c2r_chain_kernel(C2RArgs a) {
           for (int e = 0; e < 8; ++e) v[8 * h + e] *= (float)fv[e];
         }
       }
-      const int n_b = 64 * G + 16 * g;
-      // Nb % 16 == 0 (dispatcher): 16 columns are all in range or all out
-      if (n_a < a.Na && n_b < a.Nb) {
-        h8 o0, o1;
+      // Restage the 16 x 64 block through this wave's LDS so that each
+      // store instruction writes whole 128-byte rows (8 lanes per row):
+      // the streaming stores below bypass the caches that would otherwise
+      // merge partial lines.
+      h8 o0, o1;
 #pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          o0[e] = to_h(v[e]);
-          o1[e] = to_h(v[8 + e]);
-        }
-        // streaming stores: the layer output is not read again by this layer
-        __builtin_nontemporal_store(h8_as_u4(o0), reinterpret_cast<u32x4*>(yrow + n_b));
-        __builtin_nontemporal_store(h8_as_u4(o1), reinterpret_cast<u32x4*>(yrow + n_b + 8));
+      for (int e = 0; e < 8; ++e) {
+        o0[e] = to_h(v[e]);
+        o1[e] = to_h(v[8 + e]);
       }
+      *reinterpret_cast<h8*>(sOut + r16 * LDO + 16 * g) = o0;
+      *reinterpret_cast<h8*>(sOut + r16 * LDO + 16 * g + 8) = o1;
+      wave_lds_sync();
+#pragma unroll
+      for (int k = 0; k < 2; ++k) {
+        const int rr = (lane >> 3) + 8 * k, c8 = (lane & 7) * 8;
+        const u32x4 val = *reinterpret_cast<const u32x4*>(sOut + rr * LDO + c8);
+        const int row = 16 * q.j + rr, col = 64 * G + c8;
+        // Nb % 16 == 0 (dispatcher): a 16-byte piece is all in range or out;
+        // streaming stores: the layer output is not read again by this layer
+        if (row < a.Na && col < a.Nb)
+          __builtin_nontemporal_store(
+              val, reinterpret_cast<u32x4*>(yout + q.p * plane + (int64_t)row * a.Nb + col));
+      }
+      wave_lds_sync();  // staging reads done before the next group's writes
     }
   };
 
@@ -535,7 +548,8 @@ size_t c2r_chain_lds_bytes(int ng, int ntb, int Kap, int Na, bool sech2_lut) {
   const int nat = (Na + 15) / 16;
   return sizeof(_Float16) * ((sech2_lut ? (size_t)LUT_HALVES : 0) +
                              (size_t)ng * 64 * (2 * ntb * 16 + PADH) +
-                             (size_t)2 * nat * 16 * (Kap + PADH));
+                             (size_t)2 * nat * 16 * (Kap + PADH) +
+                             (size_t)CH_NW * 16 * (64 + PADH));
 }
 
 // Kernels above 64 KiB of LDS must raise their dynamic-LDS limit first.
