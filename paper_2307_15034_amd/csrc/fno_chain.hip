@@ -82,10 +82,12 @@ template <bool ODD>
 __device__ __forceinline__ unsigned lut_pair(const _Float16* tab, unsigned w) {
   const unsigned lo = (w << 1) & 0xfffeu, hi = (w >> 15) & 0xfffeu;
   const char* t = reinterpret_cast<const char*>(tab);
-  const unsigned a = *reinterpret_cast<const unsigned short*>(t + lo);
-  const unsigned b = *reinterpret_cast<const unsigned short*>(t + hi);
-  const unsigned r = a | (b << 16);
-  return ODD ? (r | (w & 0x80008000u)) : r;
+  h2 r;
+  r[0] = *reinterpret_cast<const _Float16*>(t + lo);
+  r[1] = *reinterpret_cast<const _Float16*>(t + hi);
+  unsigned u;
+  __builtin_memcpy(&u, &r, 4);
+  return ODD ? (u | (w & 0x80008000u)) : u;
 }
 
 template <bool ODD>
@@ -123,9 +125,10 @@ __global__ __launch_bounds__(CH_NW * 64, 2) void r2c_chain_kernel(R2CArgs a) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int r16 = lane & 15, g = lane >> 4;
   const int LDE = a.NaC + PADH;
-  constexpr int LUTH = TANH ? LUT_HALVES : 0;
-  _Float16* sLut = reinterpret_cast<_Float16*>(smem);  // tanh of each fp16 code
-  _Float16* sT = sLut + LUTH;                          // [NCT * 16][LDT]
+  // the lookup table is a static LDS array (at a known address, so lookups
+  // need no base add); the twiddle tables are dynamic LDS after it
+  __shared__ __align__(16) _Float16 sLut[TANH ? LUT_HALVES : 8];  // tanh of each fp16 code
+  _Float16* sT = reinterpret_cast<_Float16*>(smem);    // [NCT * 16][LDT]
   _Float16* sEc = sT + NCT * 16 * LDT;                // [NTA * 16][LDE]
   _Float16* sEs = sEc + NTA * 16 * LDE;
   const _Float16* x = reinterpret_cast<const _Float16*>(a.in);
@@ -313,9 +316,9 @@ __global__ __launch_bounds__(CH_NW * 64, 2) void c2r_chain_kernel(C2RArgs a) {
   const int r16 = lane & 15, g = lane >> 4;
   const int LDK = a.Kap + PADH;
   const int NAT = (a.Na + 15) / 16;
-  constexpr int LUTH = EPI ? LUT_HALVES : 0;
-  _Float16* sLut = reinterpret_cast<_Float16*>(smem);  // 1 - tanh^2 of each fp16 code
-  _Float16* sTI = sLut + LUTH;                         // [NG * 64][LDI]
+  // static LDS lookup table (see the forward kernel), dynamic tables after
+  __shared__ __align__(16) _Float16 sLut[EPI ? LUT_HALVES : 8];  // 1 - tanh^2 per fp16 code
+  _Float16* sTI = reinterpret_cast<_Float16*>(smem);   // [NG * 64][LDI]
   _Float16* sCI = sTI + NG * 64 * LDI;                 // [NAT * 16][LDK]
   _Float16* sSI = sCI + NAT * 16 * LDK;
   // per-wave output staging: 16 rows x 64 columns (one column group)
@@ -538,16 +541,17 @@ __global__ __launch_bounds__(CH_NW * 64, 2) void c2r_chain_kernel(C2RArgs a) {
 // ---------------------------------------------------------------------------
 // Dispatch
 // ---------------------------------------------------------------------------
+// Dynamic LDS bytes; the lookup table (64 KiB when used) is static LDS.
 size_t r2c_chain_lds_bytes(int nka, int ntb, int nta, int NaC, bool tanh_lut) {
-  return sizeof(_Float16) * ((tanh_lut ? (size_t)LUT_HALVES : 0) +
-                             (size_t)2 * ntb * 16 * (nka * KS + PADH) +
+  (void)tanh_lut;
+  return sizeof(_Float16) * ((size_t)2 * ntb * 16 * (nka * KS + PADH) +
                              (size_t)2 * nta * 16 * (NaC + PADH));
 }
 
 size_t c2r_chain_lds_bytes(int ng, int ntb, int Kap, int Na, bool sech2_lut) {
   const int nat = (Na + 15) / 16;
-  return sizeof(_Float16) * ((sech2_lut ? (size_t)LUT_HALVES : 0) +
-                             (size_t)ng * 64 * (2 * ntb * 16 + PADH) +
+  (void)sech2_lut;
+  return sizeof(_Float16) * ((size_t)ng * 64 * (2 * ntb * 16 + PADH) +
                              (size_t)2 * nat * 16 * (Kap + PADH) +
                              (size_t)CH_NW * 16 * (64 + PADH));
 }

@@ -161,6 +161,7 @@ hipError_t launch_c2r_chain(const C2RArgs& a, int ng, int ntb, int nkz, int grid
                             hipStream_t s);
 bool r2c_chain_has(int nka, int ntb, int nta);
 bool c2r_chain_has(int ng, int ntb, int nkz);
+// dynamic LDS only; a lookup table adds 64 KiB of static LDS
 size_t r2c_chain_lds_bytes(int nka, int ntb, int nta, int NaC, bool tanh_lut);
 size_t c2r_chain_lds_bytes(int ng, int ntb, int Kap, int Na, bool sech2_lut);
 constexpr int kChainWaves = 8;  // waves per work-group of the chained kernels

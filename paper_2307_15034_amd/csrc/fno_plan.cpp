@@ -761,7 +761,8 @@ fno_status run_r2c(const Plan* pl, const void* in, void* spec, void* inter, int6
     const size_t lds = r2c_chain_lds_bytes(nka, ntb, nta, g.NaC, do_tanh != 0);
     const int64_t waves = (int64_t)kChainWaves;
     const int grid = (int)std::min<int64_t>((a.planes + waves - 1) / waves, (int64_t)2 * pl->num_cu);
-    if (lds <= 160 * 1024 && grid > 0 && r2c_chain_has(nka, ntb, nta)) {
+    const size_t lut = do_tanh ? 65536 : 0;  // static LDS of the kernel
+    if (lds + lut <= 160 * 1024 && grid > 0 && r2c_chain_has(nka, ntb, nta)) {
       hipError_t e = timed(do_tanh ? "r2c_plane_tanh" : "r2c_plane", s, [&] {
         return launch_r2c_chain(a, nka, ntb, nta, grid, lds, s);
       });
@@ -854,7 +855,8 @@ fno_status run_c2r(const Plan* pl, const void* spec, void* out, void* inter, int
     const size_t lds = c2r_chain_lds_bytes(ng, ntb, g.Kap, g.Na, x_epi != nullptr);
     const int64_t waves = (int64_t)kChainWaves;
     const int grid = (int)std::min<int64_t>((a.planes + waves - 1) / waves, (int64_t)2 * pl->num_cu);
-    if (lds <= 160 * 1024 && grid > 0 && c2r_chain_has(ng, ntb, nkz)) {
+    const size_t lut = x_epi ? 65536 : 0;  // static LDS of the kernel
+    if (lds + lut <= 160 * 1024 && grid > 0 && c2r_chain_has(ng, ntb, nkz)) {
       hipError_t e = timed(kname, s, [&] { return launch_c2r_chain(a, ng, ntb, nkz, grid, lds, s); });
       if (e == hipSuccess) return FNO_OK;
       if (e != hipErrorNotSupported) return FNO_ERR_HIP;
