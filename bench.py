@@ -38,6 +38,8 @@ def parse():
     p.add_argument("--policy", choices=["min_result", "min_net"], default="min_result")
     p.add_argument("--no-caches", action="store_true",
                    help="bwd_weight recomputes both spectra from x and gy")
+    p.add_argument("--separate-bwd", action="store_true",
+                   help="bwd_data and bwd_weight as two calls instead of the combined one")
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--cpu-seconds", type=float, default=12.0)
     p.add_argument("--profile-steps", type=int, default=20)
@@ -60,6 +62,7 @@ def kernel_bytes(wl, es):
         "c2r_plane_tanh_grad": spec_in + 2 * B * Ci * N * es,
         "wgrad": spec_in + spec_out + Ci * Co * K * 2 * 4,
     }
+    out["contract_adjoint_wgrad"] = out["contract_adjoint"] + out["wgrad"]  # one launch
     out["r2c_plane_tanh"] = B * Ci * N * es + spec_in     # input transform (tanh)
     out["r2c_plane"] = B * Co * N * es + spec_out         # gradient transform
     return out
@@ -191,9 +194,14 @@ def main():
     for op in (B.FNO_OP_FWD, B.FNO_OP_BWD_DATA):
         layer.workspace(op)
     layer.workspace(B.FNO_OP_BWD_WEIGHT, caches)
+    layer.workspace(B.FNO_OP_BWD, caches)
 
     def step():
         layer.fwd(xd, wd, y=y, x_hat=xh, stream=sh)
+        if not args.separate_bwd:
+            # data and weight gradient in one call (the layer's backward)
+            layer.bwd(xd, wd, gyd, x_hat=xh, gx=gx, gw=gw, stream=sh)
+            return
         layer.bwd_data(xd, wd, gyd, gx=gx, gy_hat=gh, stream=sh)
         if caches:
             layer.bwd_weight(None, None, wd, x_hat=xh, gy_hat=gh, gw=gw, stream=sh)
@@ -256,6 +264,7 @@ def main():
         "config": {"workload": wl.name, "batch": wl.batch, "c_in": wl.c_in, "c_out": wl.c_out,
                    "grid": list(wl.n), "modes": list(wl.modes), "weights": wl.weight,
                    "precision": args.precision, "spectral_caches": caches,
+                   "backward": "separate" if args.separate_bwd else "combined",
                    "path_policy": args.policy if wl.weight == "tucker" else None},
         "step_alg_bytes": sbytes,
         "step_hbm_gbs": round(sbytes / (ms_step / 1e3) / 1e9, 1),

@@ -73,7 +73,12 @@ typedef enum { FNO_WEIGHT_DENSE = 0, FNO_WEIGHT_TUCKER = 1 } fno_weight_kind;
  * pair of the current operand list. */
 typedef enum { FNO_PATH_MIN_RESULT = 0, FNO_PATH_MIN_NET = 1 } fno_path_policy;
 
-typedef enum { FNO_OP_FWD = 0, FNO_OP_BWD_DATA = 1, FNO_OP_BWD_WEIGHT = 2 } fno_op;
+typedef enum {
+  FNO_OP_FWD = 0,
+  FNO_OP_BWD_DATA = 1,
+  FNO_OP_BWD_WEIGHT = 2,
+  FNO_OP_BWD = 3      /* data and weight gradient in one call (fno_spectral_conv_bwd) */
+} fno_op;
 
 /* Layer descriptor.  Spatial extents n[0..ndim-1] (N_1..N_d), retained mode
  * counts modes[0..ndim-1]: axes j < d keep K_j = 2 m_j slots (2 m_j <= N_j),
@@ -118,7 +123,8 @@ typedef struct {
 } fno_weight_grads;
 
 /* Bytes of workspace `op` needs for this descriptor (>= 256, multiple of 256).
- * The size for FNO_OP_BWD_WEIGHT assumes both spectral caches are supplied;
+ * The size for FNO_OP_BWD_WEIGHT assumes both spectral caches are supplied
+ * (for FNO_OP_BWD: the input-spectrum cache);
  * fno_spectral_conv_workspace_size_nocache gives the size when they are not. */
 fno_status fno_spectral_conv_workspace_size(const fno_conv_desc *desc, fno_op op,
                                             size_t *bytes);
@@ -163,6 +169,20 @@ fno_status fno_spectral_conv_bwd_weight(const fno_conv_desc *desc, const void *x
                                         const void *x_hat, const void *gy_hat,
                                         fno_weight_grads *gw, void *workspace,
                                         size_t workspace_bytes, hipStream_t stream);
+
+/* Data and weight gradients in one call: the results of
+ * fno_spectral_conv_bwd_data (gx, optional gy_hat_out) followed by
+ * fno_spectral_conv_bwd_weight (gw), with the adjoint contraction and the
+ * dense weight gradient sharing one launch when the element type is fp16 and
+ * the retained-mode count is a multiple of 16 (elsewhere the two run one after
+ * the other, as in the separate calls).  x_hat: the forward's input-spectrum
+ * cache (fno_spectral_conv_fwd's x_hat_out) or NULL to recompute it from x.
+ * Workspace: fno_spectral_conv_workspace_size(desc, FNO_OP_BWD) when x_hat is
+ * given, the _nocache size otherwise.  Errors as for the separate calls. */
+fno_status fno_spectral_conv_bwd(const fno_conv_desc *desc, const void *x,
+                                 const fno_weights *w, const void *gy, const void *x_hat,
+                                 void *gx, fno_weight_grads *gw, void *gy_hat_out,
+                                 void *workspace, size_t workspace_bytes, hipStream_t stream);
 
 /* Host-only: FFT index k of retained slot t on `axis` (0-based) — the
  * truncation map of Sec. 2 as described above. */

@@ -30,6 +30,7 @@ FNO_PATH_MIN_NET = 1
 FNO_OP_FWD = 0
 FNO_OP_BWD_DATA = 1
 FNO_OP_BWD_WEIGHT = 2
+FNO_OP_BWD = 3
 
 LABEL_BITS = {"b": 0, "i": 1, "o": 2, "a": 3, "e": 4, "x": 5, "y": 6, "z": 7,
               "c": 8, "d": 9, "f": 10}
@@ -93,6 +94,9 @@ def _load() -> ctypes.CDLL:
         "fno_spectral_conv_bwd_weight": (ctypes.c_int,
                                          [D, vp, vp, P(FnoWeights), vp, vp,
                                           P(FnoWeightGrads), vp, sz, vp]),
+        "fno_spectral_conv_bwd": (ctypes.c_int,
+                                  [D, vp, P(FnoWeights), vp, vp, vp, P(FnoWeightGrads), vp, vp,
+                                   sz, vp]),
         "fno_release_caches": (ctypes.c_int, []),
         "fno_profile_enable": (ctypes.c_int, [i32]),
         "fno_profile_reset": (ctypes.c_int, []),
@@ -112,7 +116,8 @@ EXPORTED = [
     "fno_status_string", "fno_mode_frequency", "fno_contraction_path",
     "fno_contraction_path_cost", "fno_spectrum_bytes", "fno_spectral_conv_workspace_size",
     "fno_spectral_conv_workspace_size_nocache", "fno_spectral_conv_fwd",
-    "fno_spectral_conv_bwd_data", "fno_spectral_conv_bwd_weight", "fno_release_caches",
+    "fno_spectral_conv_bwd_data", "fno_spectral_conv_bwd_weight", "fno_spectral_conv_bwd",
+    "fno_release_caches",
     "fno_profile_enable", "fno_profile_reset", "fno_profile_read",
 ]
 
@@ -235,6 +240,17 @@ def fno_spectral_conv_bwd_weight(desc, x: int, gy: int, w: FnoWeights, x_hat: in
                                            stream or None)
     if check:
         _check(st, "fno_spectral_conv_bwd_weight")
+    return st
+
+
+def fno_spectral_conv_bwd(desc, x: int, w: FnoWeights, gy: int, x_hat: int, gx: int,
+                          gw: FnoWeightGrads, gy_hat_out: int, ws: int, ws_bytes: int,
+                          stream: int, check: bool = True) -> int:
+    st = _lib.fno_spectral_conv_bwd(ctypes.byref(desc), x or None, ctypes.byref(w), gy or None,
+                                    x_hat or None, gx or None, ctypes.byref(gw),
+                                    gy_hat_out or None, ws or None, ws_bytes, stream or None)
+    if check:
+        _check(st, "fno_spectral_conv_bwd")
     return st
 
 

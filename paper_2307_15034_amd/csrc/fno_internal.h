@@ -170,6 +170,9 @@ constexpr int kChainWaves = 8;  // waves per work-group of the chained kernels
 // hipErrorNotSupported otherwise.
 hipError_t launch_contract_slab(const ContractArgs& a, hipStream_t s);
 hipError_t launch_wgrad_slab(const WgradArgs& a, hipStream_t s);
+// Adjoint contraction and weight gradient in one launch (fp16 slab path).
+bool adj_wgrad_slab_supported(const ContractArgs& adj, const WgradArgs& wg);
+hipError_t launch_adj_wgrad_slab(const ContractArgs& adj, const WgradArgs& wg, hipStream_t s);
 
 size_t r2c_lds_bytes(int elem, int Kbp, int R);
 size_t c2r_lds_bytes(int elem, int Kbp, int Kap, int R);

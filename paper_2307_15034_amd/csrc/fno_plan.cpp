@@ -636,13 +636,19 @@ size_t ws_bytes(const fno_conv_desc* d, const Plan* pl, fno_op op, bool caches) 
     w.add(spec_bytes(g, g.Cin));
     w.add(std::max(inter3d_bytes(g, g.Cin), inter3d_bytes(g, g.Cout)));
     if (tucker) w.add(tucker_path_bytes(d, pl->path_adj));
-  } else {
+  } else if (op == FNO_OP_BWD_WEIGHT) {
     if (!caches) {
       w.add(spec_bytes(g, g.Cin));
       w.add(spec_bytes(g, g.Cout));
       w.add(std::max(inter3d_bytes(g, g.Cin), inter3d_bytes(g, g.Cout)));
     }
     if (tucker) w.add(tucker_wgrad_bytes(d, pl));
+  } else {  // FNO_OP_BWD: gradient spectrum, input spectrum (no cache), then
+            // the data part's workspace and (Tucker) the weight part's
+    w.add(spec_bytes(g, g.Cout));
+    if (!caches) w.add(spec_bytes(g, g.Cin));
+    w.add(ws_bytes(d, pl, FNO_OP_BWD_DATA, true));
+    if (tucker) w.add(ws_bytes(d, pl, FNO_OP_BWD_WEIGHT, true));
   }
   return std::max<size_t>(w.total, 256);
 }
@@ -1281,7 +1287,7 @@ fno_status fno_spectrum_bytes(const fno_conv_desc* d, int which, size_t* bytes) 
 
 static fno_status ws_query(const fno_conv_desc* d, fno_op op, size_t* bytes, bool caches) {
   if (!bytes) return FNO_ERR_INVALID_ARGUMENT;
-  if (op != FNO_OP_FWD && op != FNO_OP_BWD_DATA && op != FNO_OP_BWD_WEIGHT)
+  if (op != FNO_OP_FWD && op != FNO_OP_BWD_DATA && op != FNO_OP_BWD_WEIGHT && op != FNO_OP_BWD)
     return FNO_ERR_INVALID_ARGUMENT;
   fno_status st = check_desc(d);
   if (st != FNO_OK) return st;
@@ -1425,6 +1431,106 @@ fno_status fno_spectral_conv_bwd_weight(const fno_conv_desc* d, const void* x, c
     return FNO_OK;
   }
   return run_tucker_wgrad(d, pl, xh, gh, w, gw, tsc, s);
+}
+
+fno_status fno_spectral_conv_bwd(const fno_conv_desc* d, const void* x, const fno_weights* w,
+                                 const void* gy, const void* x_hat, void* gx,
+                                 fno_weight_grads* gw, void* gy_hat_out, void* ws,
+                                 size_t ws_len, hipStream_t s) {
+  fno_status st = check_desc(d);
+  if (st != FNO_OK) return st;
+  const int tanh_on = d->precision == FNO_PREC_FP16_TANH;
+  const bool tucker = d->weight_kind == FNO_WEIGHT_TUCKER;
+  if (!okptr(gy) || !okptr(gx) || !gw) return FNO_ERR_INVALID_ARGUMENT;
+  if ((tanh_on || !x_hat) && !okptr(x)) return FNO_ERR_INVALID_ARGUMENT;
+  if (x_hat && !aligned16(x_hat)) return FNO_ERR_INVALID_ARGUMENT;
+  if (gy_hat_out && !aligned16(gy_hat_out)) return FNO_ERR_INVALID_ARGUMENT;
+  if ((st = check_weights(d, w)) != FNO_OK) return st;
+  if (tucker) {
+    if (!okptr(gw->core) || !okptr(gw->u_in) || !okptr(gw->u_out))
+      return FNO_ERR_INVALID_ARGUMENT;
+    for (int j = 0; j < d->ndim; ++j)
+      if (!okptr(gw->u_mode[j])) return FNO_ERR_INVALID_ARGUMENT;
+  } else if (!okptr(gw->dense)) {
+    return FNO_ERR_INVALID_ARGUMENT;
+  }
+  const bool cache = x_hat != nullptr;
+  if ((st = check_ws(d, FNO_OP_BWD, cache, ws, ws_len)) != FNO_OK) return st;
+  Plan* pl = nullptr;
+  if ((st = get_plan(d, &pl)) != FNO_OK) return st;
+  const Geo& g = pl->g;
+  WsLayout L;
+  char* base = (char*)ws;
+  char* gs = base + L.add(spec_bytes(g, g.Cout));
+  char* xs = cache ? nullptr : base + L.add(spec_bytes(g, g.Cin));
+  char* wsd = base + L.add(ws_bytes(d, pl, FNO_OP_BWD_DATA, true));
+  void* gh = gy_hat_out ? gy_hat_out : (void*)gs;
+  if (tucker) {
+    char* wsw = base + L.add(ws_bytes(d, pl, FNO_OP_BWD_WEIGHT, true));
+    const size_t nd = ws_bytes(d, pl, FNO_OP_BWD_DATA, true);
+    const size_t nw = ws_bytes(d, pl, FNO_OP_BWD_WEIGHT, true);
+    if ((st = fno_spectral_conv_bwd_data(d, x, w, gy, gx, gh, wsd, nd, s)) != FNO_OK) return st;
+    if (!cache) {
+      // the input spectrum, recomputed into its own region (the 3-D
+      // intermediate is the third region of the data part's workspace)
+      WsLayout Ld;
+      (void)Ld.add(spec_bytes(g, g.Cout));
+      (void)Ld.add(spec_bytes(g, g.Cin));
+      char* inter = wsd + Ld.add(std::max(inter3d_bytes(g, g.Cin), inter3d_bytes(g, g.Cout)));
+      if ((st = run_r2c(pl, x, xs, inter, g.Cin, tanh_on, 0, s)) != FNO_OK) return st;
+    }
+    return fno_spectral_conv_bwd_weight(d, x, gy, w, cache ? x_hat : xs, gh, gw, wsw, nw, s);
+  }
+  // dense: the data part's regions inside wsd, laid out as in bwd_data (its
+  // first region, the gradient spectrum, is unused: gh holds it)
+  WsLayout Ld;
+  (void)Ld.add(spec_bytes(g, g.Cout));
+  char* gxs = wsd + Ld.add(spec_bytes(g, g.Cin));
+  char* inter = wsd + Ld.add(std::max(inter3d_bytes(g, g.Cin), inter3d_bytes(g, g.Cout)));
+  const void* xh = x_hat;
+  if (!cache) {
+    if ((st = run_r2c(pl, x, xs, inter, g.Cin, tanh_on, 0, s)) != FNO_OK) return st;
+    xh = xs;
+  }
+  if ((st = run_r2c(pl, gy, gh, inter, g.Cout, 0, 1, s)) != FNO_OK) return st;
+  ContractArgs a{};
+  a.zeros = pl->t.zeros;
+  a.in = gh;
+  a.w = w->dense;
+  a.out = gxs;
+  a.B = (int)g.B;
+  a.Q = (int)g.Cout;
+  a.P = (int)g.Cin;
+  a.K = (int)g.K;
+  a.wrows = (int)g.Cin;
+  a.wcols = (int)g.Cout;
+  a.adjoint = 1;
+  a.Kb = g.Kb;
+  a.Nb = g.Nb;
+  a.scale = 1.0f;
+  WgradArgs wa{};
+  wa.zeros = pl->t.zeros;
+  wa.xh = xh;
+  wa.gh = gh;
+  wa.gw = (float*)gw->dense;
+  wa.B = (int)g.B;
+  wa.Cin = (int)g.Cin;
+  wa.Cout = (int)g.Cout;
+  wa.K = (int)g.K;
+  wa.Kb = g.Kb;
+  wa.Nb = g.Nb;
+  wa.scale = (float)std::sqrt((double)g.N);
+  if (g.elem == ELEM_F16 && g.K <= 0x7fffffff / 2 && adj_wgrad_slab_supported(a, wa)) {
+    FNO_HIP(timed("contract_adjoint_wgrad", s, [&] { return launch_adj_wgrad_slab(a, wa, s); }));
+  } else {
+    if ((st = run_contract(pl, gh, w->dense, gxs, true, s)) != FNO_OK) return st;
+    const bool slab = g.elem == ELEM_F16 && g.K % 16 == 0;
+    FNO_HIP(timed("wgrad", s, [&] {
+      return slab ? launch_wgrad_slab(wa, s) : launch_wgrad(g.elem, wa, s);
+    }));
+  }
+  const float sc = (float)(1.0 / std::sqrt((double)g.N));
+  return run_c2r(pl, gxs, gx, inter, g.Cin, sc, tanh_on ? x : nullptr, s);
 }
 
 fno_status fno_profile_enable(int32_t enable) {

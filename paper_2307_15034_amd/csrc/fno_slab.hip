@@ -87,17 +87,18 @@ struct SlabArgs {
   float scale;
 };
 
+// One work-group's tile: block `bid` of `nblocks` blocks of this operation.
 template <SlabOp OP>
-__global__ __launch_bounds__(SL_NT, 4) void slab_kernel(SlabArgs s) {
+__device__ __forceinline__ void slab_body(const SlabArgs& s, int bid, int nblocks,
+                                          unsigned char* smem) {
   using OT = SlabOut<OP>;
-  extern __shared__ __align__(16) unsigned char smem[];
   u32* sA = reinterpret_cast<u32*>(smem);  // [mode][A row][reduction]
   u32* sB = sA + A_DW;                      // [mode][B col][reduction]
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6;
   const int r16 = lane & 15, g = lane >> 4;
   const int nrt = (s.nrow + SL_AR - 1) / SL_AR, nct = (s.ncol + SL_BC - 1) / SL_BC;
-  const int lid = xcd_logical_block(blockIdx.x, gridDim.x);
+  const int lid = xcd_logical_block(bid, nblocks);
   const int t0 = (lid / (nrt * nct)) * SL_TM;
   const int row0 = ((lid / nct) % nrt) * SL_AR;
   const int col0 = (lid % nct) * SL_BC;
@@ -265,6 +266,23 @@ __global__ __launch_bounds__(SL_NT, 4) void slab_kernel(SlabArgs s) {
   }
 }
 
+template <SlabOp OP>
+__global__ __launch_bounds__(SL_NT, 4) void slab_kernel(SlabArgs s) {
+  extern __shared__ __align__(16) unsigned char smem[];
+  slab_body<OP>(s, blockIdx.x, gridDim.x, smem);
+}
+
+// The adjoint contraction and the weight gradient of the backward pass in
+// one launch: blocks [0, n1) are adjoint-contraction tiles, the rest weight-
+// gradient tiles (both read the gradient spectrum; one launch instead of two,
+// and each operation's waits are covered by the other's work).
+__global__ __launch_bounds__(SL_NT, 4) void slab_adj_wgrad_kernel(SlabArgs s1, SlabArgs s2,
+                                                                  int n1) {
+  extern __shared__ __align__(16) unsigned char smem[];
+  if ((int)blockIdx.x < n1) slab_body<SLAB_ADJ>(s1, blockIdx.x, n1, smem);
+  else slab_body<SLAB_WGRAD>(s2, blockIdx.x - n1, gridDim.x - n1, smem);
+}
+
 size_t slab_lds_bytes(int op) {
   const int stage_dw = A_DW + B_DW;
   const int out_dw = op == SLAB_WGRAD ? SL_AR * SlabOut<SLAB_WGRAD>::RSO
@@ -292,17 +310,17 @@ static hipError_t slab_launch(int op, const SlabArgs& s, hipStream_t st) {
   return go(slab_kernel<SLAB_WGRAD>);
 }
 
-hipError_t launch_contract_slab(const ContractArgs& a, hipStream_t st) {
+static bool make_contract_slab(const ContractArgs& a, SlabArgs* out) {
+  if ((int64_t)a.B * a.Q * a.K * 4 >= (1ll << 30) - 64 ||
+      (int64_t)a.wrows * a.wcols * a.K * 4 >= (1ll << 30) - 64 ||
+      (int64_t)a.B * a.P * a.K * 2 >= (1ll << 31) || a.K % SL_TM != 0)
+    return false;
   SlabArgs s{};
   s.a = a.in;
   s.b = a.w;
   s.out = a.out;
   s.a_bytes = (int)((int64_t)a.B * a.Q * a.K * 4);
   s.b_bytes = (int)((int64_t)a.wrows * a.wcols * a.K * 4);
-  if ((int64_t)a.B * a.Q * a.K * 4 >= (1ll << 30) - 64 ||
-      (int64_t)a.wrows * a.wcols * a.K * 4 >= (1ll << 30) - 64 ||
-      (int64_t)a.B * a.P * a.K * 2 >= (1ll << 31))
-    return hipErrorNotSupported;
   s.nrow = a.B;
   s.ncol = a.P;
   s.nred = a.Q;
@@ -312,19 +330,20 @@ hipError_t launch_contract_slab(const ContractArgs& a, hipStream_t st) {
   s.Kb = a.Kb;
   s.Nb = a.Nb;
   s.scale = a.scale;
-  return slab_launch(a.adjoint ? SLAB_ADJ : SLAB_FWD, s, st);
+  *out = s;
+  return true;
 }
 
-hipError_t launch_wgrad_slab(const WgradArgs& a, hipStream_t st) {
+static bool make_wgrad_slab(const WgradArgs& a, SlabArgs* out) {
+  if ((int64_t)a.B * a.Cin * a.K * 4 >= (1ll << 30) - 64 ||
+      (int64_t)a.B * a.Cout * a.K * 4 >= (1ll << 30) - 64 || a.K % SL_TM != 0)
+    return false;
   SlabArgs s{};
   s.a = a.xh;
   s.b = a.gh;
   s.out = a.gw;
   s.a_bytes = (int)((int64_t)a.B * a.Cin * a.K * 4);
   s.b_bytes = (int)((int64_t)a.B * a.Cout * a.K * 4);
-  if ((int64_t)a.B * a.Cin * a.K * 4 >= (1ll << 30) - 64 ||
-      (int64_t)a.B * a.Cout * a.K * 4 >= (1ll << 30) - 64)
-    return hipErrorNotSupported;
   s.nrow = a.Cin;
   s.ncol = a.Cout;
   s.nred = a.B;
@@ -334,7 +353,47 @@ hipError_t launch_wgrad_slab(const WgradArgs& a, hipStream_t st) {
   s.Kb = a.Kb;
   s.Nb = a.Nb;
   s.scale = a.scale;
+  *out = s;
+  return true;
+}
+
+static int64_t slab_blocks(const SlabArgs& s) {
+  return (int64_t)(s.K / SL_TM) * ((s.nrow + SL_AR - 1) / SL_AR) *
+         ((s.ncol + SL_BC - 1) / SL_BC);
+}
+
+hipError_t launch_contract_slab(const ContractArgs& a, hipStream_t st) {
+  SlabArgs s;
+  if (!make_contract_slab(a, &s)) return hipErrorNotSupported;
+  return slab_launch(a.adjoint ? SLAB_ADJ : SLAB_FWD, s, st);
+}
+
+hipError_t launch_wgrad_slab(const WgradArgs& a, hipStream_t st) {
+  SlabArgs s;
+  if (!make_wgrad_slab(a, &s)) return hipErrorNotSupported;
   return slab_launch(SLAB_WGRAD, s, st);
+}
+
+bool adj_wgrad_slab_supported(const ContractArgs& adj, const WgradArgs& wg) {
+  SlabArgs s1, s2;
+  return adj.adjoint && make_contract_slab(adj, &s1) && make_wgrad_slab(wg, &s2) &&
+         slab_blocks(s1) > 0 && slab_blocks(s2) > 0 &&
+         slab_blocks(s1) + slab_blocks(s2) <= 0x7fffffff;
+}
+
+hipError_t launch_adj_wgrad_slab(const ContractArgs& adj, const WgradArgs& wg, hipStream_t st) {
+  if (!adj_wgrad_slab_supported(adj, wg)) return hipErrorNotSupported;
+  SlabArgs s1, s2;
+  make_contract_slab(adj, &s1);
+  make_wgrad_slab(wg, &s2);
+  const int64_t n1 = slab_blocks(s1), n2 = slab_blocks(s2);
+  const size_t lds = slab_lds_bytes(SLAB_WGRAD);  // the larger of the two
+  hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(slab_adj_wgrad_kernel),
+                                     hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(slab_adj_wgrad_kernel, dim3((unsigned)(n1 + n2)), dim3(SL_NT), lds, st, s1,
+                     s2, (int)n1);
+  return hipGetLastError();
 }
 
 }  // namespace fno

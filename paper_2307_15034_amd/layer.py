@@ -87,7 +87,7 @@ class SpectralConv:
         return B.grads_struct(core=_addr(g["core"]), u_in=_addr(g["u_in"]),
                               u_out=_addr(g["u_out"]), u_mode=[_addr(u) for u in g["u_mode"]])
 
-    # -- the three calls -------------------------------------------------------
+    # -- the calls ---------------------------------------------------------------
     def fwd(self, x: torch.Tensor, w, y: Optional[torch.Tensor] = None,
             x_hat: Optional[torch.Tensor] = None, stream: Optional[int] = None):
         if y is None:
@@ -123,3 +123,19 @@ class SpectralConv:
                                        _addr(gy_hat), self.grads_struct(gw), _addr(ws),
                                        ws.numel(), s)
         return gw
+
+    def bwd(self, x: Optional[torch.Tensor], w, gy: torch.Tensor,
+            x_hat: Optional[torch.Tensor] = None, gx: Optional[torch.Tensor] = None, gw=None,
+            gy_hat: Optional[torch.Tensor] = None, stream: Optional[int] = None):
+        """Data and weight gradients in one call (returns gx, gw)."""
+        if gx is None:
+            gx = torch.empty((self.batch, self.c_in) + self.n, dtype=self.dtype,
+                             device=self.device)
+        if gw is None:
+            gw = self.alloc_grads()
+        ws = self.workspace(B.FNO_OP_BWD, x_hat is not None)
+        s = torch.cuda.current_stream().cuda_stream if stream is None else stream
+        B.fno_spectral_conv_bwd(self.desc, _addr(x), self.weights_struct(w), _addr(gy),
+                                _addr(x_hat), _addr(gx), self.grads_struct(gw), _addr(gy_hat),
+                                _addr(ws), ws.numel(), s)
+        return gx, gw

@@ -279,3 +279,73 @@ def test_nan_propagates():
     y = U.host(layer.fwd(U.dev(x), U.dev(w)))
     assert np.isnan(y[0]).any()
     assert np.isfinite(y[1]).all()
+
+
+# ---------------------------------------------------------------------------
+# The combined backward call (data + weight gradient in one call)
+# ---------------------------------------------------------------------------
+BWD_CASES = [
+    # (n, modes, B, Cin, Cout, prec): K % 16 == 0 fp16 takes the shared launch
+    ((64, 64), (8, 8), 2, 16, 16, "fp16_tanh"),
+    ((32, 32), (5, 7), 37, 33, 18, "fp16_tanh"),   # K = 70: separate kernels
+    ((32, 32), (8, 8), 17, 20, 36, "fp16_tanh"),   # ragged rows / columns / batch
+    ((6, 10, 12), (2, 3, 4), 2, 3, 2, "fp16_tanh"),
+    ((32, 32), (8, 8), 3, 5, 7, "fp32"),
+]
+
+
+@pytest.mark.parametrize("case", range(len(BWD_CASES)))
+@pytest.mark.parametrize("cache", [True, False])
+def test_combined_bwd(case, cache):
+    """fno_spectral_conv_bwd gives the oracle's gx and gW, and exactly what the
+    separate bwd_data / bwd_weight calls give."""
+    n, modes, Bt, ci, co, prec = BWD_CASES[case]
+    U.say(f"combined bwd case {case}: n={n} modes={modes} B={Bt} {ci}->{co} {prec} "
+          f"cache={cache}")
+    _, npdt, oprec = U.prec_codes(prec)
+    x, w, gy = synth.random_dense_case(500 + case, Bt, ci, co, n, modes, npdt)
+    layer = U.make_layer(n, modes, Bt, ci, co, prec)
+    xd, wd, gyd = U.dev(x), U.dev(w), U.dev(gy)
+    xh = layer.spectrum_buffer(0)
+    gh = layer.spectrum_buffer(1)
+    layer.fwd(xd, wd, x_hat=xh)
+    gx, gw = layer.bwd(xd, wd, gyd, x_hat=xh if cache else None, gy_hat=gh)
+    gx_sep = layer.bwd_data(xd, wd, gyd)
+    gw_sep = layer.bwd_weight(xd, gyd, wd)
+    torch.cuda.synchronize()
+    U.say("  done")
+    ref_gx = O.bwd_data(x, U.cplx(w), gy, n, modes, oprec)
+    ref_gw = O.bwd_weight(x, gy, n, modes, oprec)
+    _assert_close("gx", U.host(gx), ref_gx, prec)
+    _assert_close("gW", U.cplx(U.host(gw)), ref_gw, prec)
+    assert np.array_equal(U.host(gx), U.host(gx_sep))
+    assert np.array_equal(U.host(gw), U.host(gw_sep))
+
+
+@pytest.mark.parametrize("prec", PRECS)
+def test_combined_bwd_tucker(prec):
+    n, modes, Bt, ci, co, rank = (32, 32), (4, 5), 2, 6, 5, (3, 4, 2, 3)
+    U.say(f"combined bwd tucker {prec}")
+    _, npdt, oprec = U.prec_codes(prec)
+    rng = np.random.default_rng(77)
+    x = (rng.standard_normal((Bt, ci) + n)).astype(npdt)
+    gy = (rng.standard_normal((Bt, co) + n)).astype(npdt)
+    kd = (2 * modes[0], modes[1])
+    core = (rng.standard_normal(rank + (2,)) * 0.3).astype(npdt)
+    u_in = (rng.standard_normal((ci, rank[0], 2)) * 0.4).astype(npdt)
+    u_out = (rng.standard_normal((co, rank[1], 2)) * 0.4).astype(npdt)
+    u_mode = [(rng.standard_normal((kd[j], rank[2 + j], 2)) * 0.4).astype(npdt)
+              for j in range(2)]
+    layer = U.make_layer(n, modes, Bt, ci, co, prec, tucker_rank=rank)
+    wd = {"core": U.dev(core), "u_in": U.dev(u_in), "u_out": U.dev(u_out),
+          "u_mode": [U.dev(u) for u in u_mode]}
+    xd, gyd = U.dev(x), U.dev(gy)
+    gx, gw = layer.bwd(xd, wd, gyd)
+    gx_sep = layer.bwd_data(xd, wd, gyd)
+    gw_sep = layer.bwd_weight(xd, gyd, wd)
+    torch.cuda.synchronize()
+    assert np.array_equal(U.host(gx), U.host(gx_sep))
+    for k in ("core", "u_in", "u_out"):
+        assert np.array_equal(U.host(gw[k]), U.host(gw_sep[k]))
+    for a, b in zip(gw["u_mode"], gw_sep["u_mode"]):
+        assert np.array_equal(U.host(a), U.host(b))
