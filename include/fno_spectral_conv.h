@@ -221,6 +221,13 @@ fno_status fno_release_caches(void);
 
 const char *fno_status_string(fno_status status);
 
+/* Detail of the last FNO_ERR_HIP returned on the calling thread: the HIP
+ * error's name and code and the step that failed (a kernel name or a HIP
+ * call).  Empty if no call on this thread has returned FNO_ERR_HIP.  The
+ * string is owned by the library and valid until the thread's next failing
+ * call. */
+const char *fno_last_error(void);
+
 #ifdef __cplusplus
 }
 #endif

@@ -39,7 +39,10 @@ LABEL_BITS = {"b": 0, "i": 1, "o": 2, "a": 3, "e": 4, "x": 5, "y": 6, "z": 7,
 class FnoError(RuntimeError):
     def __init__(self, status: int, where: str):
         self.status = status
-        super().__init__(f"{where}: {status_string(status)} ({status})")
+        msg = f"{where}: {status_string(status)} ({status})"
+        if status == FNO_ERR_HIP:
+            msg += f": {_lib.fno_last_error().decode()}"
+        super().__init__(msg)
 
 
 class FnoConvDesc(ctypes.Structure):
@@ -76,12 +79,21 @@ def _load() -> ctypes.CDLL:
         raise ImportError(
             f"{LIB_PATH} is missing: build it with `python -m paper_2307_15034_amd.build` "
             "(no CPU fallback exists)")
+    # One HIP runtime per process: PyTorch ships its own libamdhip64 with the
+    # same soname as the system one.  Loading torch first makes this library
+    # bind to that copy instead of starting a second runtime (and a second
+    # HSA runtime) beside it.
+    try:
+        import torch  # noqa: F401
+    except ImportError:  # pragma: no cover - the library also works without torch
+        pass
     lib = ctypes.CDLL(LIB_PATH)
     P = ctypes.POINTER
     D = P(FnoConvDesc)
     vp, sz, i32, i64 = ctypes.c_void_p, ctypes.c_size_t, ctypes.c_int32, ctypes.c_int64
     sig = {
         "fno_status_string": (ctypes.c_char_p, [ctypes.c_int]),
+        "fno_last_error": (ctypes.c_char_p, []),
         "fno_mode_frequency": (ctypes.c_int, [D, i32, i64, P(i64)]),
         "fno_contraction_path": (ctypes.c_int, [D, ctypes.c_int, P(i32), i32, P(i32)]),
         "fno_contraction_path_cost": (ctypes.c_int, [D, ctypes.c_int, P(i64), P(i64)]),
@@ -113,7 +125,7 @@ def _load() -> ctypes.CDLL:
 _lib = _load()
 
 EXPORTED = [
-    "fno_status_string", "fno_mode_frequency", "fno_contraction_path",
+    "fno_status_string", "fno_last_error", "fno_mode_frequency", "fno_contraction_path",
     "fno_contraction_path_cost", "fno_spectrum_bytes", "fno_spectral_conv_workspace_size",
     "fno_spectral_conv_workspace_size_nocache", "fno_spectral_conv_fwd",
     "fno_spectral_conv_bwd_data", "fno_spectral_conv_bwd_weight", "fno_spectral_conv_bwd",

@@ -98,6 +98,9 @@ __device__ __forceinline__ u32x4 lut_u4(const _Float16* tab, const u32x4& w) {
 
 constexpr int LUT_HALVES = 32768;  // one entry per non-negative fp16 code
 
+// cache-policy operand of buffer stores: non-temporal (streaming) store
+constexpr int CPOL_NT = 2;
+
 // Position in a wave's flattened sequence of (plane, block) work items.
 struct Pos {
   int64_t p;
@@ -122,7 +125,9 @@ __global__ __launch_bounds__(CH_NW * 64, 2) void r2c_chain_kernel(R2CArgs a) {
   constexpr int NCT = 2 * NTB;
   constexpr int LDT = NKA * KS + PADH;
   extern __shared__ __align__(16) unsigned char smem[];
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  // the wave index is the same on every lane: keep it (and the loop control
+  // derived from it) in scalar registers
+  const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int r16 = lane & 15, g = lane >> 4;
   const int LDE = a.NaC + PADH;
   // the lookup table is a static LDS array (at a known address, so lookups
@@ -148,20 +153,30 @@ __global__ __launch_bounds__(CH_NW * 64, 2) void r2c_chain_kernel(R2CArgs a) {
   auto next = [&](Pos q) -> Pos { return q.j + 1 < NJ ? Pos{q.p, q.j + 1} : Pos{q.p + W, 0}; };
 
   // Row block (p, j): lane holds rows 32 j + 16 rt + r16, columns 32 s + 8 g.
-  // Issued unconditionally (past the last plane: the zero block) so the wait
-  // before each use counts all loads issued after it.
+  // Buffer loads through a per-plane resource (scalar registers); lanes past
+  // the plane's rows or columns, and every lane past the last plane (an empty
+  // resource), read zeros.  All loads are issued, so the wait before each use
+  // counts exactly the loads issued after it.
+  // beyond every plane (planes < 2^29 bytes); a row and a column offset that
+  // are both BIG still add up to less than 2^31
+  constexpr int BIG = 0x20000000;
+  int colo[NKA];
+#pragma unroll
+  for (int s = 0; s < NKA; ++s) {
+    const int col = s * KS + g * 8;
+    colo[s] = col < a.Nb ? col * 2 : BIG;
+  }
   auto load = [&](Pos q, u32x4 (&buf)[2][NKA]) {
     const bool pok = q.p < a.planes;
-    const _Float16* base = x + (pok ? q.p : 0) * plane;
+    const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<_Float16*>(x + (pok ? q.p : 0) * plane), (short)0, pok ? (int)(plane * 2) : 0,
+        0x00020000);
 #pragma unroll
     for (int rt = 0; rt < 2; ++rt) {
       const int row = 32 * q.j + 16 * rt + r16;
+      const int rowo = row < a.Na ? row * a.Nb * 2 : BIG;
 #pragma unroll
-      for (int s = 0; s < NKA; ++s) {
-        const int col = s * KS + g * 8;
-        const bool ok = pok && row < a.Na && col < a.Nb;
-        buf[rt][s] = *reinterpret_cast<const u32x4*>(ok ? base + (int64_t)row * a.Nb + col : zr);
-      }
+      for (int s = 0; s < NKA; ++s) buf[rt][s] = __builtin_amdgcn_raw_buffer_load_b128(rs, rowo + colo[s], 0, 0);
     }
   };
 
@@ -224,42 +239,58 @@ __global__ __launch_bounds__(CH_NW * 64, 2) void r2c_chain_kernel(R2CArgs a) {
       }
     }
     if (q.j == NJ - 1) {
-      // lane holds Z[16 ta + 4 g + i][NTB r16 + tb]: NTB consecutive complex
-      _Float16* o = out + q.p * (int64_t)a.Ka * a.Kb * 2;
+      // lane holds Z[16 ta + 4 g + i][NTB r16 + tb]: NTB consecutive complex.
+      // Buffer stores through the output plane's resource; lanes past Ka or
+      // Kb carry an offset beyond it (the store is dropped), so no branch.
+      const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
+          out + q.p * (int64_t)a.Ka * a.Kb * 2, (short)0, a.Ka * a.Kb * 4, 0x00020000);
+      // Kb % 4 == 0 (dispatcher) and NTB <= 4: a lane's NTB columns are
+      // either all below Kb or all past it.  Row t_a = 16 ta + i + 4 g is
+      // valid iff 16 ta + i < Ka - 4 g.  (The empty asm keeps the compiler
+      // from hoisting the sixteen offsets out of the plane loop.)
       const int tb0 = NTB * r16;
+      int sb = tb0 < a.Kb ? (4 * g * a.Kb + tb0) * 4 : BIG;
+      int glim = a.Ka - 4 * g;
+      asm volatile("" : "+v"(sb), "+v"(glim));
 #pragma unroll
       for (int ta = 0; ta < NTA; ++ta)
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          const int t_a = ta * 16 + 4 * g + i;
-          if (t_a >= a.Ka) continue;
-          _Float16* d = o + ((int64_t)t_a * a.Kb + tb0) * 2;
+          const int r = 16 * ta + i;
+          const int vo = r < glim ? sb + r * a.Kb * 4 : BIG;
           _Float16 v[2 * NTB];
 #pragma unroll
           for (int tb = 0; tb < NTB; ++tb) {
             v[2 * tb] = to_h(zre[ta][tb][i] * a.scaleB);
             v[2 * tb + 1] = to_h(zim[ta][tb][i] * a.scaleB);
           }
-          // Kb % 4 == 0 (dispatcher) and NTB <= 4: a lane's NTB columns are
-          // either all below Kb or all past it
-          if (tb0 < a.Kb) {
-            if constexpr (NTB == 1) {
-              *reinterpret_cast<h2*>(d) = h2{v[0], v[1]};
-            } else if constexpr (NTB == 2) {
-              *reinterpret_cast<h4*>(d) = h4{v[0], v[1], v[2], v[3]};
-            } else {
-              *reinterpret_cast<h8*>(d) = h8{v[0], v[1], v[2], v[3], v[4], v[5], v[6], v[7]};
-            }
+          if constexpr (NTB == 1) {
+            u32 w;
+            __builtin_memcpy(&w, v, 4);
+            __builtin_amdgcn_raw_buffer_store_b32(w, rs, vo, 0, 0);
+          } else if constexpr (NTB == 2) {
+            u32x2 w;
+            __builtin_memcpy(&w, v, 8);
+            __builtin_amdgcn_raw_buffer_store_b64(w, rs, vo, 0, 0);
+          } else {
+            u32x4 w;
+            __builtin_memcpy(&w, v, 16);
+            __builtin_amdgcn_raw_buffer_store_b128(w, rs, vo, 0, 0);
           }
         }
     }
   };
 
-  // Each wave walks its planes p = wave_id, wave_id + W, ... in 32-row blocks.
-  // Two register buffers in fixed roles (loop unrolled by two): a buffer is
-  // refilled with the block two ahead as soon as step A has consumed it, so
-  // those loads overlap this block's step B and the next block's step A.
-  Pos q0{(int64_t)blockIdx.x * CH_NW + wave, 0};
+  // Each wave walks its planes p = wave_id, wave_id + W, ... in 32-row blocks
+  // (nitems blocks in all, a wave-uniform count).  Two register buffers in
+  // fixed roles (loop unrolled by two): a buffer is refilled with the block
+  // two ahead as soon as step A has consumed it, so those loads overlap this
+  // block's step B and the next block's step A.  The loop has one exit test
+  // per pair, so every pass through the loop head has the same loads in
+  // flight and the wait before each step A covers that block only.
+  const int64_t pw = (int64_t)blockIdx.x * CH_NW + wave;
+  const int64_t nitems = pw < a.planes ? ((a.planes - 1 - pw) / W + 1) * NJ : 0;
+  Pos q0{pw, 0};
   Pos q1 = next(q0);
   u32x4 b0[2][NKA], b1[2][NKA];
   h8 yf[NCT];
@@ -279,19 +310,22 @@ __global__ __launch_bounds__(CH_NW * 64, 2) void r2c_chain_kernel(R2CArgs a) {
   ss.store(sEs, LDE, NTA * 16, a.NaC);
   if constexpr (TANH) sl.store(sLut, 0, 1, LUT_HALVES);
   __syncthreads();  // tables staged
-  for (;;) {
-    if (q0.p >= a.planes) break;
+  int64_t it = 0;
+  for (; it + 2 <= nitems; it += 2) {
     step_a(b0, yf);
     const Pos c0 = q0;
     q0 = next(q1);
     load(q0, b0);
     step_b(c0, yf);
-    if (q1.p >= a.planes) break;
     step_a(b1, yf);
     const Pos c1 = q1;
     q1 = next(q0);
     load(q1, b1);
     step_b(c1, yf);
+  }
+  if (it < nitems) {
+    step_a(b0, yf);
+    step_b(q0, yf);
   }
 }
 
@@ -312,7 +346,9 @@ __global__ __launch_bounds__(CH_NW * 64, 2) void c2r_chain_kernel(C2RArgs a) {
   constexpr int NYT = 4 * NG;  // output tiles (16 columns each) per row tile
   constexpr int LDI = 2 * NTB * 16 + PADH;
   extern __shared__ __align__(16) unsigned char smem[];
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  // the wave index is the same on every lane: keep it (and the loop control
+  // derived from it) in scalar registers
+  const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int r16 = lane & 15, g = lane >> 4;
   const int LDK = a.Kap + PADH;
   const int NAT = (a.Na + 15) / 16;
@@ -341,36 +377,51 @@ __global__ __launch_bounds__(CH_NW * 64, 2) void c2r_chain_kernel(C2RArgs a) {
   const int64_t W = (int64_t)gridDim.x * CH_NW;
   auto next = [&](Pos q) -> Pos { return q.j + 1 < NAT ? Pos{q.p, q.j + 1} : Pos{q.p + W, 0}; };
 
+  // Buffer loads and stores through per-plane resources (scalar registers):
+  // lanes past a plane's rows or columns carry an offset beyond it (loads
+  // read zeros, stores are dropped), and a plane past the last has an empty
+  // resource, so every load is issued and no store needs a branch.
+  // beyond every plane (planes < 2^29 bytes); a row and a column offset that
+  // are both BIG still add up to less than 2^31
+  constexpr int BIG = 0x20000000;
+  auto rsrc = [&](const _Float16* base, int64_t p, int64_t halves) {
+    const bool pok = p < a.planes;
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<_Float16*>(base + (pok ? p : 0) * halves),
+                                             (short)0, pok ? (int)(halves * 2) : 0, 0x00020000);
+  };
   // Spectrum plane as MFMA A operands, natural layout: lane (r16, g) holds
   // row t_a = 16 rt + r16, complex t_b = 16 kz + 4 g .. + 4 (16-byte loads).
   auto load_z = [&](int64_t p, u32x4 (&buf)[2 * NKZ][NTB]) {
-    const bool pok = p < a.planes;
-    const _Float16* base = zin + (pok ? p : 0) * zplane;
+    const __amdgpu_buffer_rsrc_t rs = rsrc(zin, p, zplane);
 #pragma unroll
     for (int rt = 0; rt < 2 * NKZ; ++rt)
 #pragma unroll
       for (int kz = 0; kz < NTB; ++kz) {
         const int ta = 16 * rt + r16, tb = 16 * kz + 4 * g;
-        const bool ok = pok && ta < a.Ka && tb < a.Kb;
-        buf[rt][kz] =
-            *reinterpret_cast<const u32x4*>(ok ? base + ((int64_t)ta * a.Kb + tb) * 2 : zr);
+        const int vo = (ta < a.Ka && tb < a.Kb) ? (ta * a.Kb + tb) * 4 : BIG;
+        buf[rt][kz] = __builtin_amdgcn_raw_buffer_load_b128(rs, vo, 0, 0);
       }
   };
   // epilogue input of row tile (p, j): row 16 j + r16, columns 64 G + 16 g + 8 h
   constexpr int XG = EPI ? NG : 1;
+  int colx[XG][2];
+#pragma unroll
+  for (int G = 0; G < XG; ++G)
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const int col = 64 * G + 16 * g + 8 * h;
+      colx[G][h] = col < a.Nb ? col * 2 : BIG;
+    }
   auto load_x = [&](Pos q, u32x4 (&buf)[XG][2]) {
     if constexpr (EPI) {
-      const bool pok = q.p < a.planes;
-      const _Float16* base = xin + (pok ? q.p : 0) * plane;
+      const __amdgpu_buffer_rsrc_t rs = rsrc(xin, q.p, plane);
       const int row = 16 * q.j + r16;
+      const int rowo = row < a.Na ? row * a.Nb * 2 : BIG;
 #pragma unroll
       for (int G = 0; G < NG; ++G)
 #pragma unroll
-        for (int h = 0; h < 2; ++h) {
-          const int col = 64 * G + 16 * g + 8 * h;
-          const bool ok = pok && row < a.Na && col < a.Nb;
-          buf[G][h] = *reinterpret_cast<const u32x4*>(ok ? base + (int64_t)row * a.Nb + col : zr);
-        }
+        for (int h = 0; h < 2; ++h)
+          buf[G][h] = __builtin_amdgcn_raw_buffer_load_b128(rs, rowo + colx[G][h], 0, 0);
     }
   };
 
@@ -454,6 +505,7 @@ __global__ __launch_bounds__(CH_NW * 64, 2) void c2r_chain_kernel(C2RArgs a) {
         yacc[t] = MH::mma(tf, vf[ks], yacc[t]);
       }
     // ---- epilogue: lane holds y[16 j + r16][64 G + 16 g .. + 16] ---------------
+    const __amdgpu_buffer_rsrc_t ry = rsrc(yout, q.p, plane);
 #pragma unroll
     for (int G = 0; G < NG; ++G) {
       float v[16];
@@ -488,17 +540,22 @@ __global__ __launch_bounds__(CH_NW * 64, 2) void c2r_chain_kernel(C2RArgs a) {
         const int rr = (lane >> 3) + 8 * k, c8 = (lane & 7) * 8;
         const u32x4 val = *reinterpret_cast<const u32x4*>(sOut + rr * LDO + c8);
         const int row = 16 * q.j + rr, col = 64 * G + c8;
-        // Nb % 16 == 0 (dispatcher): a 16-byte piece is all in range or out;
-        // streaming stores: the layer output is not read again by this layer
-        if (row < a.Na && col < a.Nb)
-          __builtin_nontemporal_store(
-              val, reinterpret_cast<u32x4*>(yout + q.p * plane + (int64_t)row * a.Nb + col));
+        // Nb % 16 == 0 (dispatcher): a 16-byte piece is all in range or out.
+        // Streaming (non-temporal) stores: the layer does not read y again.
+        const int vo = (row < a.Na && col < a.Nb) ? (row * a.Nb + col) * 2 : BIG;
+        __builtin_amdgcn_raw_buffer_store_b128(val, ry, vo, 0, CPOL_NT);
       }
       wave_lds_sync();  // staging reads done before the next group's writes
     }
   };
 
-  Pos q0{(int64_t)blockIdx.x * CH_NW + wave, 0};
+  // Each wave walks its planes in 16-row tiles (nitems tiles in all, a
+  // wave-uniform count), with the epilogue inputs of three tiles in flight
+  // (loop unrolled by three, one exit test per pass, so every pass through
+  // the loop head has the same loads in flight).
+  const int64_t nitems =
+      first_plane < a.planes ? ((a.planes - 1 - first_plane) / W + 1) * NAT : 0;
+  Pos q0{first_plane, 0};
   Pos q1 = next(q0), q2 = next(q1);
   u32x4 x0[XG][2], x1[XG][2], x2[XG][2];
   // Load order: the first plane's spectrum, the tables, then the epilogue
@@ -522,20 +579,20 @@ __global__ __launch_bounds__(CH_NW * 64, 2) void c2r_chain_kernel(C2RArgs a) {
     transpose_z(zraw);
   }
   __syncthreads();  // tables staged
-  for (;;) {
+  int64_t it = 0;
+  for (; it + 3 <= nitems; it += 3) {
     load_x(q2, x2);
-    if (q0.p >= a.planes) break;
     process(q0, x0);
     q0 = next(q2);
     load_x(q0, x0);
-    if (q1.p >= a.planes) break;
     process(q1, x1);
     q1 = next(q0);
     load_x(q1, x1);
-    if (q2.p >= a.planes) break;
     process(q2, x2);
     q2 = next(q1);
   }
+  if (it < nitems) process(q0, x0);
+  if (it + 1 < nitems) process(q1, x1);
 }
 
 // ---------------------------------------------------------------------------

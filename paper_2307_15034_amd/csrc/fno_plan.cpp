@@ -28,6 +28,14 @@ inline int64_t round_up(int64_t v, int64_t m) { return (v + m - 1) / m * m; }
 // --------------------------------------------------------------------------
 // Descriptor checks and the truncation map T_K (Sec. 2)
 // --------------------------------------------------------------------------
+// Detail of the last FNO_ERR_HIP on this thread (HIP error name and step).
+thread_local std::string g_last_error;
+
+fno_status hip_fail(hipError_t e, const char* what) {
+  g_last_error = std::string(hipGetErrorName(e)) + " (" + std::to_string((int)e) + ") in " + what;
+  return FNO_ERR_HIP;
+}
+
 fno_status check_desc(const fno_conv_desc* d) {
   if (!d) return FNO_ERR_INVALID_ARGUMENT;
   if (d->ndim < 1 || d->ndim > 3) return FNO_ERR_INVALID_ARGUMENT;
@@ -513,11 +521,13 @@ fno_status build_tables(const fno_conv_desc* d, Plan* pl) {
     bytes = b32.size() * 4;
   }
   void* dev = nullptr;
-  if (hipMalloc(&dev, std::max<size_t>(bytes, 256)) != hipSuccess) return FNO_ERR_HIP;
+  hipError_t e = hipMalloc(&dev, std::max<size_t>(bytes, 256));
+  if (e != hipSuccess) return hip_fail(e, "hipMalloc (plan tables)");
   const void* src = pl->g.elem == ELEM_F16 ? (const void*)b16.data() : (const void*)b32.data();
-  if (hipMemcpy(dev, src, bytes, hipMemcpyHostToDevice) != hipSuccess) {
+  e = hipMemcpy(dev, src, bytes, hipMemcpyHostToDevice);
+  if (e != hipSuccess) {
     (void)hipFree(dev);
-    return FNO_ERR_HIP;
+    return hip_fail(e, "hipMemcpy (plan tables)");
   }
   pl->t.base = dev;
   pl->t.bytes = bytes;
@@ -564,7 +574,8 @@ fno_status get_plan(const fno_conv_desc* d, Plan** out) {
   fno_status st = check_desc(d);
   if (st != FNO_OK) return st;
   int dev = 0;
-  if (hipGetDevice(&dev) != hipSuccess) return FNO_ERR_HIP;
+  const hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
   PlanKey key = key_of(d, dev);
   std::lock_guard<std::mutex> lock(g_mutex);
   auto it = g_plans.find(key);
@@ -658,9 +669,10 @@ size_t ws_bytes(const fno_conv_desc* d, const Plan* pl, fno_op op, bool caches) 
 // --------------------------------------------------------------------------
 inline bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
 
-#define FNO_HIP(call)                        \
-  do {                                       \
-    if ((call) != hipSuccess) return FNO_ERR_HIP; \
+#define FNO_HIP(call)                          \
+  do {                                         \
+    const hipError_t fno_e_ = (call);          \
+    if (fno_e_ != hipSuccess) return hip_fail(fno_e_, #call); \
   } while (0)
 
 // --------------------------------------------------------------------------
@@ -773,7 +785,7 @@ fno_status run_r2c(const Plan* pl, const void* in, void* spec, void* inter, int6
         return launch_r2c_chain(a, nka, ntb, nta, grid, lds, s);
       });
       if (e == hipSuccess) done = true;
-      else if (e != hipErrorNotSupported) return FNO_ERR_HIP;
+      else if (e != hipErrorNotSupported) return hip_fail(e, do_tanh ? "r2c_plane_tanh" : "r2c_plane");
     }
   }
   if (!done && g.elem == ELEM_F16 && a.vec && g.Nb <= 256 && g.Na <= 128 && g.nct <= 8) {
@@ -786,7 +798,7 @@ fno_status run_r2c(const Plan* pl, const void* in, void* spec, void* inter, int6
         return launch_r2c_fast(a, g.nct, nka, nw, grid, lds, s);
       });
       if (e == hipSuccess) done = true;
-      else if (e != hipErrorNotSupported) return FNO_ERR_HIP;
+      else if (e != hipErrorNotSupported) return hip_fail(e, do_tanh ? "r2c_plane_tanh" : "r2c_plane");
     }
   }
   if (!done) FNO_HIP(timed(do_tanh ? "r2c_plane_tanh" : "r2c_plane", s, [&] { return launch_r2c(g.elem, g.nct, a, r2c_lds_bytes(g.elem, g.Kbp, g.R_f), s); }));
@@ -865,7 +877,7 @@ fno_status run_c2r(const Plan* pl, const void* spec, void* out, void* inter, int
     if (lds + lut <= 160 * 1024 && grid > 0 && c2r_chain_has(ng, ntb, nkz)) {
       hipError_t e = timed(kname, s, [&] { return launch_c2r_chain(a, ng, ntb, nkz, grid, lds, s); });
       if (e == hipSuccess) return FNO_OK;
-      if (e != hipErrorNotSupported) return FNO_ERR_HIP;
+      if (e != hipErrorNotSupported) return hip_fail(e, kname);
     }
   }
   if (g.elem == ELEM_F16 && a.vec && g.Kb % 4 == 0 && g.Nb <= 256 && g.Na <= 128 && g.nct <= 8 &&
@@ -880,7 +892,7 @@ fno_status run_c2r(const Plan* pl, const void* spec, void* out, void* inter, int
         return launch_c2r_fast(a, g.nct, nw, nbt, nkz, grid, lds, s);
       });
       if (e == hipSuccess) return FNO_OK;
-      if (e != hipErrorNotSupported) return FNO_ERR_HIP;
+      if (e != hipErrorNotSupported) return hip_fail(e, kname);
     }
   }
   FNO_HIP(timed(kname, s, [&] { return launch_c2r(g.elem, g.nct, a, c2r_lds_bytes(g.elem, g.Kbp, g.Kap, g.R_i), s); }));
@@ -1186,6 +1198,8 @@ fno_status check_ws(const fno_conv_desc* d, fno_op op, bool caches, const void* 
 using namespace fno;
 
 extern "C" {
+
+const char* fno_last_error(void) { return g_last_error.c_str(); }
 
 const char* fno_status_string(fno_status s) {
   switch (s) {

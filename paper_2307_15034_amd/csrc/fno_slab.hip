@@ -95,7 +95,7 @@ __device__ __forceinline__ void slab_body(const SlabArgs& s, int bid, int nblock
   u32* sA = reinterpret_cast<u32*>(smem);  // [mode][A row][reduction]
   u32* sB = sA + A_DW;                      // [mode][B col][reduction]
   const int tid = threadIdx.x;
-  const int lane = tid & 63, wave = tid >> 6;
+  const int lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int r16 = lane & 15, g = lane >> 4;
   const int nrt = (s.nrow + SL_AR - 1) / SL_AR, nct = (s.ncol + SL_BC - 1) / SL_BC;
   const int lid = xcd_logical_block(bid, nblocks);
