@@ -31,8 +31,8 @@ HBM_PEAK_GBS = 8000.0
 def parse():
     p = argparse.ArgumentParser()
     p.add_argument("--gpus", type=int, default=1)
-    p.add_argument("--steps", type=int, default=50)
-    p.add_argument("--warmup", type=int, default=10)
+    p.add_argument("--steps", type=int, default=200)
+    p.add_argument("--warmup", type=int, default=20)
     p.add_argument("--workload", type=int, default=2)
     p.add_argument("--precision", choices=["fp16_tanh", "fp32"], default="fp16_tanh")
     p.add_argument("--policy", choices=["min_result", "min_net"], default="min_result")

@@ -45,6 +45,14 @@ __device__ __forceinline__ u32x4 h8_as_u4(const h8& v) {
   return r;
 }
 
+// -v for eight fp16 values: one sign-bit XOR per register
+__device__ __forceinline__ h8 neg_h8(const h8& v) {
+  u32x4 r = h8_as_u4(v);
+#pragma unroll
+  for (int w = 0; w < 4; ++w) r[w] ^= 0x80008000u;
+  return u_as_h8(r);
+}
+
 // Copy of a [rows][cols] fp16 table (row stride gstride) into LDS rows of
 // stride lstride (cols, strides multiples of 8), at most MAXP 16-byte pieces
 // per thread.  All loads are issued before any store, so staging costs one
@@ -229,7 +237,7 @@ __global__ __launch_bounds__(CH_NW * 64, 2) void r2c_chain_kernel(R2CArgs a) {
     for (int ta = 0; ta < NTA; ++ta) {
       const int eo = (ta * 16 + r16) * LDE + 32 * q.j + g * 8;
       const h8 cf = MH::ld(sEc + eo), sf = MH::ld(sEs + eo);
-      const h8 nsf = -sf;
+      const h8 nsf = neg_h8(sf);
 #pragma unroll
       for (int tb = 0; tb < NTB; ++tb) {
         zre[ta][tb] = MH::mma(cf, yf[tb], zre[ta][tb]);
@@ -294,9 +302,11 @@ __global__ __launch_bounds__(CH_NW * 64, 2) void r2c_chain_kernel(R2CArgs a) {
   Pos q1 = next(q0);
   u32x4 b0[2][NKA], b1[2][NKA];
   h8 yf[NCT];
-  // Load order: the first row block, the tables, the second row block.  The
-  // first block and the tables are what the first step needs; the barrier
-  // waits for them only, and the second block streams in behind.
+  // Load order: the first row block, the tables, and (after the barrier) the
+  // second row block.  The first block and the tables are what the first
+  // step needs; requesting the second block only once they have arrived
+  // lets them arrive sooner (all waves start at once, and the memory system
+  // does not serve requests in order).
   load(q0, b0);
   __builtin_amdgcn_sched_barrier(0);
   st.load(reinterpret_cast<const _Float16*>(a.twAc), a.Nbp, NCT * 16, NKA * KS, zr);
@@ -304,12 +314,12 @@ __global__ __launch_bounds__(CH_NW * 64, 2) void r2c_chain_kernel(R2CArgs a) {
   ss.load(reinterpret_cast<const _Float16*>(a.sBc), a.NaC, NTA * 16, a.NaC, zr);
   if constexpr (TANH) sl.load(reinterpret_cast<const _Float16*>(a.lut), 0, 1, LUT_HALVES, zr);
   __builtin_amdgcn_sched_barrier(0);
-  load(q1, b1);
   st.store(sT, LDT, NCT * 16, NKA * KS);
   sc.store(sEc, LDE, NTA * 16, a.NaC);
   ss.store(sEs, LDE, NTA * 16, a.NaC);
   if constexpr (TANH) sl.store(sLut, 0, 1, LUT_HALVES);
   __syncthreads();  // tables staged
+  load(q1, b1);
   int64_t it = 0;
   for (; it + 2 <= nitems; it += 2) {
     step_a(b0, yf);
@@ -472,7 +482,7 @@ __global__ __launch_bounds__(CH_NW * 64, 2) void c2r_chain_kernel(C2RArgs a) {
     for (int ks = 0; ks < NKZ; ++ks) {
       const int eo = (16 * q.j + r16) * LDK + 32 * ks + 8 * g;
       const h8 cf = MH::ld(sCI + eo), sf = MH::ld(sSI + eo);
-      const h8 nsf = -sf;
+      const h8 nsf = neg_h8(sf);
 #pragma unroll
       for (int tt = 0; tt < NTB; ++tt) {
         vr[tt] = MH::mma(zfr[tt][ks], cf, vr[tt]);
