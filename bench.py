@@ -9,6 +9,10 @@ Prints one JSON line with the throughput (samples/s), the roofline figure of
 the dominant kernel (HIP events on the launch stream through the library's
 event profiler) and the CPU oracle timed on a bounded sample.
 
+The timed steps replay the step's launches captured once as a HIP graph
+(--no-graph launches every kernel from the host instead); the per-kernel
+figures come from separate, eagerly launched steps.
+
     python bench.py [--steps K] [--warmup W] [--workload 2] [--no-cpu-baseline]
 """
 from __future__ import annotations
@@ -38,6 +42,9 @@ def parse():
     p.add_argument("--policy", choices=["min_result", "min_net"], default="min_result")
     p.add_argument("--no-caches", action="store_true",
                    help="bwd_weight recomputes both spectra from x and gy")
+    p.add_argument("--no-graph", action="store_true",
+                   help="launch every kernel from the host instead of replaying the step "
+                        "as a HIP graph")
     p.add_argument("--separate-bwd", action="store_true",
                    help="bwd_data and bwd_weight as two calls instead of the combined one")
     p.add_argument("--no-cpu-baseline", action="store_true")
@@ -196,26 +203,45 @@ def main():
     layer.workspace(B.FNO_OP_BWD_WEIGHT, caches)
     layer.workspace(B.FNO_OP_BWD, caches)
 
-    def step():
-        layer.fwd(xd, wd, y=y, x_hat=xh, stream=sh)
+    def step(s=None):
+        s = sh if s is None else s
+        layer.fwd(xd, wd, y=y, x_hat=xh, stream=s)
         if not args.separate_bwd:
             # data and weight gradient in one call (the layer's backward)
-            layer.bwd(xd, wd, gyd, x_hat=xh, gx=gx, gw=gw, stream=sh)
+            layer.bwd(xd, wd, gyd, x_hat=xh, gx=gx, gw=gw, stream=s)
             return
-        layer.bwd_data(xd, wd, gyd, gx=gx, gy_hat=gh, stream=sh)
+        layer.bwd_data(xd, wd, gyd, gx=gx, gy_hat=gh, stream=s)
         if caches:
-            layer.bwd_weight(None, None, wd, x_hat=xh, gy_hat=gh, gw=gw, stream=sh)
+            layer.bwd_weight(None, None, wd, x_hat=xh, gy_hat=gh, gw=gw, stream=s)
         else:
-            layer.bwd_weight(xd, gyd, wd, gw=gw, stream=sh)
+            layer.bwd_weight(xd, gyd, wd, gw=gw, stream=s)
 
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
+    graph, per_graph = None, 1
+    if not args.no_graph:
+        # The step's launches (every kernel of fwd and bwd) captured once in a
+        # HIP graph; a timed step is a replay (per_graph steps per replay).
+        per_graph = 10 if args.steps % 10 == 0 else 1
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            cs = torch.cuda.current_stream().cuda_stream
+            for _ in range(per_graph):
+                step(cs)
+        torch.cuda.synchronize()
+        for _ in range(2):
+            graph.replay()
+        torch.cuda.synchronize()
     ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     t0 = time.perf_counter()
     ev0.record(stream)
-    for _ in range(args.steps):
-        step()
+    if graph is not None:
+        for _ in range(args.steps // per_graph):
+            graph.replay()
+    else:
+        for _ in range(args.steps):
+            step()
     ev1.record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
@@ -265,6 +291,7 @@ def main():
                    "grid": list(wl.n), "modes": list(wl.modes), "weights": wl.weight,
                    "precision": args.precision, "spectral_caches": caches,
                    "backward": "separate" if args.separate_bwd else "combined",
+                   "launch": "stream" if args.no_graph else "hip_graph",
                    "path_policy": args.policy if wl.weight == "tucker" else None},
         "step_alg_bytes": sbytes,
         "step_hbm_gbs": round(sbytes / (ms_step / 1e3) / 1e9, 1),
