@@ -568,17 +568,23 @@ __global__ __launch_bounds__(CH_NW * 64, 2) void c2r_chain_kernel(C2RArgs a) {
   Pos q0{first_plane, 0};
   Pos q1 = next(q0), q2 = next(q1);
   u32x4 x0[XG][2], x1[XG][2], x2[XG][2];
-  // Load order: the first plane's spectrum and the tables; the epilogue
-  // inputs of the first two row tiles (needed last) only after the barrier,
-  // so that they do not compete with what the first tile needs first.
+  // Load order: the tables (cache hits, all work-groups read the same
+  // ones), the first plane's spectrum, then the epilogue inputs of the first
+  // two row tiles.  Waits count loads in issue order, so staging the tables
+  // waits for the tables only, and the first transposition for the spectrum
+  // but not the epilogue inputs.
   {
     u32x4 zraw[2 * NKZ][NTB];
-    load_z(q0.p, zraw);
-    __builtin_amdgcn_sched_barrier(0);
     st.load(reinterpret_cast<const _Float16*>(a.twIc), 2 * NTB * 16, NG * 64, 2 * NTB * 16, zr);
     sc.load(reinterpret_cast<const _Float16*>(a.cIc), a.Kap, NAT * 16, a.Kap, zr);
     ss.load(reinterpret_cast<const _Float16*>(a.sIc), a.Kap, NAT * 16, a.Kap, zr);
     if constexpr (EPI) sl.load(reinterpret_cast<const _Float16*>(a.lut), 0, 1, LUT_HALVES, zr);
+    __builtin_amdgcn_sched_barrier(0);
+    load_z(q0.p, zraw);
+    __builtin_amdgcn_sched_barrier(0);
+    load_x(q0, x0);
+    __builtin_amdgcn_sched_barrier(0);
+    load_x(q1, x1);
     __builtin_amdgcn_sched_barrier(0);
     st.store(sTI, LDI, NG * 64, 2 * NTB * 16);
     sc.store(sCI, LDK, NAT * 16, a.Kap);
@@ -587,9 +593,6 @@ __global__ __launch_bounds__(CH_NW * 64, 2) void c2r_chain_kernel(C2RArgs a) {
     transpose_z(zraw);
   }
   __syncthreads();  // tables staged
-  load_x(q0, x0);
-  __builtin_amdgcn_sched_barrier(0);
-  load_x(q1, x1);
   int64_t it = 0;
   for (; it + 3 <= nitems; it += 3) {
     load_x(q2, x2);
