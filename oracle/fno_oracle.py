@@ -17,15 +17,17 @@ Mixed-Precision Neural Operators", ICLR 2024):
 * T_K keeps, on every axis but the last, the m_j lowest non-negative and the
   m_j highest (negative) frequencies in ascending FFT order; on the last,
   real-FFT axis it keeps k = 0..m_d-1.
-* R is a complex weight per retained mode mixing channels (Sec. 2), dense or
-  Tucker-factorised (the tensorised FNO of Sec. 2; Kolda-Bader mode products).
+* R is a complex weight per retained mode mixing channels (Sec. 2), dense,
+  Tucker-factorised (the tensorised FNO of Sec. 2; Kolda-Bader mode products)
+  or CP-factorised (the factorisation of the Navier-Stokes and Darcy runs,
+  Sec. 4.6).
 * tanh pre-activation before the forward transform in half-precision mode
   (Sec. 4.3); the full-precision mode has no pre-activation (App. B.8 uses
   tanh only as an ablation).
 * The inverse takes y = sum_t c(k_d) Re(Yhat_t e^{+i theta}) with c = 1 on the
   k_d = 0 and Nyquist planes and 2 elsewhere, and no 1/N.
-* The Tucker contraction is split into two-operand steps in the order a greedy
-  rule picks (Sec. 4.2: the next step is the one whose intermediate is
+* The Tucker and CP contractions are split into two-operand steps in the
+  order a greedy rule picks (Sec. 4.2: the next step is the one whose intermediate is
   smallest).
 * Gradients use the real-gradient convention g = dL/dRe + i dL/dIm.
 
@@ -390,6 +392,112 @@ def tucker_bwd_weight(x, gy, core, u_in, u_out, u_mode, n, modes, precision):
         g_mode.append(np.einsum(f"{spec}->{sp[j]}{rk[j]}", gw, ccore, cu_in, cu_out, *arrs,
                                 **opt))
     return g_core, g_in, g_out, g_mode
+
+
+# ---------------------------------------------------------------------------
+# CP-factorised weights
+# ---------------------------------------------------------------------------
+
+CP_RANK = "r"
+
+
+def cp_labels(d: int, adjoint: bool = False) -> Tuple[List[str], str]:
+    """Index strings of [spectrum, lambda, u_in, u_out, u_1..u_d] and the output.
+
+    CP (canonical polyadic) form of the weight tensor, the factorisation the
+    paper uses on Navier-Stokes and Darcy flow (Sec. 4.6; Kolda-Bader, cited in
+    Sec. 2): W[i, o, t_1..t_d] = sum_r lambda[r] u_in[i, r] u_out[o, r]
+    prod_j u_j[t_j, r], one rank index r shared by every factor.
+    Forward: Xhat(b i x..) lambda(r) u_in(i r) u_out(o r) u_j(x_j r) -> (b o x..);
+    adjoint: G(b o x..) with the same factor labels -> (b i x..)."""
+    sp = SPATIAL[:d]
+    first = ("bo" if adjoint else "bi") + sp
+    out = ("bi" if adjoint else "bo") + sp
+    ops = [first, CP_RANK, "i" + CP_RANK, "o" + CP_RANK] + [sp[j] + CP_RANK for j in range(d)]
+    return ops, out
+
+
+def cp_sizes(batch, c_in, c_out, kdims, rank: int) -> Dict[str, int]:
+    s = {"b": batch, "i": c_in, "o": c_out, CP_RANK: int(rank)}
+    for j in range(len(kdims)):
+        s[SPATIAL[j]] = kdims[j]
+    return s
+
+
+def cp_dense(lam, u_in, u_out, u_mode) -> np.ndarray:
+    """W[i, o, t_1..t_d] = sum_r lam[r] u_in[i, r] u_out[o, r] prod_j u_j[t_j, r]."""
+    w = np.asarray(lam, dtype=np.complex128)[None, None, :] * \
+        np.asarray(u_in, dtype=np.complex128)[:, None, :] * \
+        np.asarray(u_out, dtype=np.complex128)[None, :, :]          # i, o, r
+    for u in u_mode:
+        u = np.asarray(u, dtype=np.complex128)
+        w = w[..., None, :] * u.reshape((1,) * (w.ndim - 1) + u.shape)  # ..., t_j, r
+    return w.sum(axis=-1)
+
+
+def cp_contract(spec, lam, u_in, u_out, u_mode, policy: str = POLICY_MIN_RESULT,
+                adjoint: bool = False, steps=None):
+    """Contract a spectrum with CP weights along a greedy two-operand path
+    (Sec. 4.2), the same rule as for Tucker weights.
+
+    forward:  Yhat[b, o, t] = sum_i spec[b, i, t] W[i, o, t]
+    adjoint:  gXhat[b, i, t] = sum_o spec[b, o, t] conj(W[i, o, t])
+    """
+    d = len(u_mode)
+    ops, out = cp_labels(d, adjoint)
+    facs = [lam, u_in, u_out] + list(u_mode)
+    if adjoint:
+        facs = [np.conj(f) for f in facs]
+    sizes = cp_sizes(spec.shape[0], u_in.shape[0], u_out.shape[0], spec.shape[2:],
+                     np.asarray(lam).shape[0])
+    if steps is None:
+        steps = greedy_path(ops, sizes, out, policy)
+    return contract_path([spec] + facs, ops, steps)
+
+
+def cp_fwd(x, lam, u_in, u_out, u_mode, n, modes, precision,
+           policy: str = POLICY_MIN_RESULT):
+    xh = forward_spectrum(preactivation(x, precision), n, modes)
+    yh = cp_contract(xh, lam, u_in, u_out, u_mode, policy)
+    return inverse_spectrum(yh, n, modes, with_c=True)
+
+
+def cp_bwd_data(x, lam, u_in, u_out, u_mode, gy, n, modes, precision,
+                policy: str = POLICY_MIN_RESULT):
+    g = grad_spectrum(gy, n, modes)
+    gxh = cp_contract(g, lam, u_in, u_out, u_mode, policy, adjoint=True)
+    gu = inverse_spectrum(gxh, n, modes, with_c=False) / float(np.prod(n))
+    if precision == PREC_FP16_TANH:
+        t = np.tanh(np.asarray(x, dtype=np.float64))
+        return gu * (1.0 - t * t)
+    return gu
+
+
+def cp_bwd_weight(x, gy, lam, u_in, u_out, u_mode, n, modes, precision):
+    """Chain rule through W(lambda, factors): g_F = sum gW * conj(dW/dF) for
+    each parameter F, with gW the dense weight gradient."""
+    d = len(n)
+    gw = bwd_weight(x, gy, n, modes, precision)             # i, o, t..
+    sp = SPATIAL[:d]
+    r = CP_RANK
+    clam, cu_in, cu_out = np.conj(lam), np.conj(u_in), np.conj(u_out)
+    cmode = [np.conj(u) for u in u_mode]
+    gw_l = "io" + sp
+    mode_terms = [sp[j] + r for j in range(d)]
+    opt = dict(optimize=True)   # evaluation order only; the sum is the same
+    g_lam = np.einsum(",".join([gw_l, "i" + r, "o" + r] + mode_terms) + "->" + r,
+                      gw, cu_in, cu_out, *cmode, **opt)
+    g_in = np.einsum(",".join([gw_l, r, "o" + r] + mode_terms) + "->i" + r,
+                     gw, clam, cu_out, *cmode, **opt)
+    g_out = np.einsum(",".join([gw_l, r, "i" + r] + mode_terms) + "->o" + r,
+                      gw, clam, cu_in, *cmode, **opt)
+    g_mode = []
+    for j in range(d):
+        others = [mode_terms[q] for q in range(d) if q != j]
+        arrs = [cmode[q] for q in range(d) if q != j]
+        spec = ",".join([gw_l, r, "i" + r, "o" + r] + others)
+        g_mode.append(np.einsum(f"{spec}->{sp[j]}{r}", gw, clam, cu_in, cu_out, *arrs, **opt))
+    return g_lam, g_in, g_out, g_mode
 
 
 # ---------------------------------------------------------------------------

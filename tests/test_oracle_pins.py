@@ -234,7 +234,60 @@ def pin_identity_self_adjoint(seed=13):
     return np.abs(a - b).max()
 
 
+def _cp_small(seed, d=2, rank=3):
+    rng = _rng(seed)
+    n = (8, 8) if d == 2 else (4, 4, 6)
+    modes = (2, 3) if d == 2 else (1, 2, 2)
+    kd = tuple(2 * m for m in modes[:-1]) + (modes[-1],)
+    ci, co = 3, 4
+    lam = _cplx(rng, (rank,), 0.5)
+    u_in, u_out = _cplx(rng, (ci, rank), 0.5), _cplx(rng, (co, rank), 0.5)
+    u_mode = [_cplx(rng, (kd[j], rank), 0.5) for j in range(d)]
+    x = rng.standard_normal((2, ci) + n) * 0.7
+    gy = rng.standard_normal((2, co) + n)
+    return rng, n, modes, kd, lam, u_in, u_out, u_mode, x, gy
+
+
+def pin_cp_explicit(seed=80):
+    """CP reconstruction against the rank-one sum written out (relative)."""
+    _, n, modes, kd, lam, u_in, u_out, u_mode, _, _ = _cp_small(seed)
+    w = O.cp_dense(lam, u_in, u_out, u_mode)
+    err = 0.0
+    for (i, o, t1, t2) in [(0, 0, 0, 0), (2, 1, 3, 2), (1, 3, 2, 1)]:
+        ref = sum(lam[r] * u_in[i, r] * u_out[o, r] * u_mode[0][t1, r] * u_mode[1][t2, r]
+                  for r in range(lam.shape[0]))
+        err = max(err, abs(w[i, o, t1, t2] - ref) / abs(ref))
+    return err
+
+
+def pin_cp_tucker(seed=81):
+    """The CP layer equals the Tucker layer with lambda on the core's
+    superdiagonal: outputs, data gradients, and lambda = the core gradient's
+    superdiagonal (relative errors)."""
+    _, n, modes, kd, lam, u_in, u_out, u_mode, x, gy = _cp_small(seed)
+    r = lam.shape[0]
+    core = np.zeros((r,) * 4, dtype=np.complex128)
+    for k in range(r):
+        core[k, k, k, k] = lam[k]
+    rel = lambda a, b: np.abs(a - b).max() / np.abs(b).max()  # noqa: E731
+    err = 0.0
+    for prec in (F32, F16T):
+        err = max(err, rel(O.cp_fwd(x, lam, u_in, u_out, u_mode, n, modes, prec),
+                           O.tucker_fwd(x, core, u_in, u_out, u_mode, n, modes, prec)))
+        err = max(err, rel(O.cp_bwd_data(x, lam, u_in, u_out, u_mode, gy, n, modes, prec),
+                           O.tucker_bwd_data(x, core, u_in, u_out, u_mode, gy, n, modes,
+                                             prec)))
+        g = O.cp_bwd_weight(x, gy, lam, u_in, u_out, u_mode, n, modes, prec)
+        t = O.tucker_bwd_weight(x, gy, core, u_in, u_out, u_mode, n, modes, prec)
+        err = max(err, rel(g[0], np.array([t[0][k, k, k, k] for k in range(r)])))
+        err = max(err, rel(g[1], t[1]), rel(g[2], t[2]), rel(g[3][0], t[3][0]),
+                  rel(g[3][1], t[3][1]))
+    return err
+
+
 ALL_PINS = {
+    "cp_explicit": (pin_cp_explicit, 1e-13),
+    "cp_tucker": (pin_cp_tucker, 1e-12),
     "brute2d": (pin_brute_force_2d, 1e-13),
     "brute3d": (pin_brute_force_3d, 1e-13),
     "rfftn": (pin_numpy_rfftn, 1e-13),
@@ -525,6 +578,169 @@ def test_tucker_bwd_data_matches_dense():
 
 
 # ---------------------------------------------------------------------------
+# CP-factorised weights (Sec. 4.6)
+# ---------------------------------------------------------------------------
+
+def _cp_case(rng, d=2, rank=3):
+    n = (8, 8) if d == 2 else (4, 4, 6)
+    modes = (2, 3) if d == 2 else (1, 2, 2)
+    kd = tuple(2 * m for m in modes[:-1]) + (modes[-1],)
+    ci, co = 3, 4
+    lam = _cplx(rng, (rank,), 0.5)
+    u_in = _cplx(rng, (ci, rank), 0.5)
+    u_out = _cplx(rng, (co, rank), 0.5)
+    u_mode = [_cplx(rng, (kd[j], rank), 0.5) for j in range(d)]
+    return n, modes, kd, ci, co, rank, lam, u_in, u_out, u_mode
+
+
+def _superdiagonal_core(lam, d):
+    """The Tucker core of a CP tensor: lam[r] on the superdiagonal."""
+    r = lam.shape[0]
+    core = np.zeros((r,) * (2 + d), dtype=np.complex128)
+    for k in range(r):
+        core[(k,) * (2 + d)] = lam[k]
+    return core
+
+
+def test_cp_dense_explicit_sum():
+    """The dense reconstruction equals the rank-one sum written out."""
+    rng = _rng(60)
+    n, modes, kd, ci, co, rank, lam, u_in, u_out, u_mode = _cp_case(rng, 2)
+    w = O.cp_dense(lam, u_in, u_out, u_mode)
+    assert w.shape == (ci, co) + kd
+    for (i, o, t1, t2) in [(0, 0, 0, 0), (2, 1, 3, 2), (1, 3, 2, 1)]:
+        s = sum(lam[r] * u_in[i, r] * u_out[o, r] * u_mode[0][t1, r] * u_mode[1][t2, r]
+                for r in range(rank))
+        assert abs(w[i, o, t1, t2] - s) < 1e-13
+
+
+@pytest.mark.parametrize("d", [2, 3])
+def test_cp_is_superdiagonal_tucker(d):
+    """A CP tensor is a Tucker tensor whose core holds lambda on its
+    superdiagonal (Kolda-Bader): the CP layer equals the Tucker layer with
+    that core, and the lambda gradient is the core gradient's superdiagonal
+    while the factor gradients coincide."""
+    rng = _rng(61 + d)
+    n, modes, kd, ci, co, rank, lam, u_in, u_out, u_mode = _cp_case(rng, d)
+    core = _superdiagonal_core(lam, d)
+    x = rng.standard_normal((2, ci) + n) * 0.7
+    gy = rng.standard_normal((2, co) + n)
+    wt = O.tucker_dense(core, u_in, u_out, u_mode)
+    wc = O.cp_dense(lam, u_in, u_out, u_mode)
+    assert np.abs(wt - wc).max() <= 1e-13
+    for prec in (F32, F16T):
+        a = O.cp_fwd(x, lam, u_in, u_out, u_mode, n, modes, prec)
+        b = O.tucker_fwd(x, core, u_in, u_out, u_mode, n, modes, prec)
+        assert np.abs(a - b).max() <= 1e-12 * np.abs(b).max()
+        a = O.cp_bwd_data(x, lam, u_in, u_out, u_mode, gy, n, modes, prec)
+        b = O.tucker_bwd_data(x, core, u_in, u_out, u_mode, gy, n, modes, prec)
+        assert np.abs(a - b).max() <= 1e-12 * np.abs(b).max()
+        g_lam, g_in, g_out, g_mode = O.cp_bwd_weight(x, gy, lam, u_in, u_out, u_mode, n,
+                                                     modes, prec)
+        t_core, t_in, t_out, t_mode = O.tucker_bwd_weight(x, gy, core, u_in, u_out, u_mode,
+                                                          n, modes, prec)
+        diag = np.array([t_core[(k,) * (2 + d)] for k in range(rank)])
+        for got, ref in [(g_lam, diag), (g_in, t_in), (g_out, t_out)] + \
+                list(zip(g_mode, t_mode)):
+            assert np.abs(got - ref).max() <= 1e-12 * max(np.abs(ref).max(), 1e-30)
+
+
+@pytest.mark.parametrize("d", [2, 3])
+def test_cp_all_orders_agree(d):
+    """Dense reconstruction, both greedy policies and random pairwise orders
+    all give the same spectrum product (forward and adjoint)."""
+    rng = _rng(64 + d)
+    n, modes, kd, ci, co, rank, lam, u_in, u_out, u_mode = _cp_case(rng, d)
+    w = O.cp_dense(lam, u_in, u_out, u_mode)
+    for adjoint in (False, True):
+        spec = _cplx(rng, (2, co if adjoint else ci) + kd)
+        if adjoint:
+            ref = np.einsum("bo...,io...->bi...", spec, np.conj(w))
+        else:
+            ref = O.contract_dense(spec, w)
+        scale = np.abs(ref).max()
+        for pol in (O.POLICY_MIN_RESULT, O.POLICY_MIN_NET):
+            got = O.cp_contract(spec, lam, u_in, u_out, u_mode, pol, adjoint)
+            assert np.abs(got - ref).max() <= 1e-12 * scale
+        ops, out = O.cp_labels(d, adjoint)
+        for trial in range(6):
+            cur = list(ops)
+            steps = []
+            while len(cur) > 2:
+                p, q = sorted(rng.choice(len(cur), 2, replace=False).tolist())
+                res = O.pair_result(cur, p, q, out)
+                steps.append((p, q, res))
+                cur = [o for r, o in enumerate(cur) if r not in (p, q)] + [res]
+            steps.append((0, 1, out))
+            got = O.cp_contract(spec, lam, u_in, u_out, u_mode, adjoint=adjoint, steps=steps)
+            assert np.abs(got - ref).max() <= 1e-12 * scale
+
+
+@pytest.mark.parametrize("policy", ["min_result", "min_net"])
+def test_cp_greedy_paths_golden(policy):
+    with open(os.path.join(GOLDEN, "cp_paths.json")) as f:
+        g = json.load(f)
+    ops, out = O.cp_labels(2)
+    assert ops == g["operands"] and out == g["output"]
+    steps = O.greedy_path(g["operands"], g["sizes"], g["output"], policy)
+    exp = g[policy]["steps"]
+    assert len(steps) == len(exp)
+    for (p, q, res), (ep, eq, eres, esize) in zip(steps, exp):
+        assert (p, q) == (ep, eq)
+        assert sorted(res) == sorted(eres)
+        assert O._size(res, g["sizes"]) == esize
+    assert steps[-1][2] == g["output"]
+    assert O.path_macs(g["operands"], g["sizes"], steps) == g[policy]["macs"]
+    peak = max(O._size(r, g["sizes"]) for _, _, r in steps)
+    assert peak == g[policy]["peak"]
+
+
+@pytest.mark.parametrize("precision", [F32, F16T])
+def test_cp_gradients_fd(precision):
+    """Central finite differences for lambda and every factor."""
+    rng = _rng(70)
+    n, modes, kd, ci, co, rank, lam, u_in, u_out, u_mode = _cp_case(rng, 2)
+    x = rng.standard_normal((1, ci) + n) * 0.7
+    gy = rng.standard_normal((1, co) + n)
+
+    def loss(lm, ui, uo, um):
+        return float(np.sum(gy * O.cp_fwd(x, lm, ui, uo, um, n, modes, precision)))
+
+    g_lam, g_in, g_out, g_mode = O.cp_bwd_weight(x, gy, lam, u_in, u_out, u_mode, n, modes,
+                                                 precision)
+    h = 1e-6
+    params = [("lam", lam, g_lam), ("in", u_in, g_in), ("out", u_out, g_out),
+              ("m0", u_mode[0], g_mode[0]), ("m1", u_mode[1], g_mode[1])]
+    for name, arr, grad in params:
+        for fi in [0, arr.size - 1, arr.size // 2]:
+            idx = np.unravel_index(fi, arr.shape)
+            for comp in (1.0, 1j):
+                def bump(sgn):
+                    a2 = arr.copy()
+                    a2[idx] += sgn * h * comp
+                    args = {"lam": lam, "in": u_in, "out": u_out,
+                            "m0": u_mode[0], "m1": u_mode[1]}
+                    args[name] = a2
+                    return loss(args["lam"], args["in"], args["out"],
+                                [args["m0"], args["m1"]])
+                fd = (bump(1) - bump(-1)) / (2 * h)
+                ref = grad[idx].real if comp == 1.0 else grad[idx].imag
+                assert abs(fd - ref) <= 1e-7 * max(1.0, abs(ref)), (name, idx, comp)
+
+
+def test_cp_bwd_data_matches_dense():
+    rng = _rng(71)
+    n, modes, kd, ci, co, rank, lam, u_in, u_out, u_mode = _cp_case(rng, 2)
+    x = rng.standard_normal((2, ci) + n)
+    gy = rng.standard_normal((2, co) + n)
+    w = O.cp_dense(lam, u_in, u_out, u_mode)
+    for pol in ("min_result", "min_net"):
+        a = O.cp_bwd_data(x, lam, u_in, u_out, u_mode, gy, n, modes, F16T, pol)
+        b = O.bwd_data(x, w, gy, n, modes, F16T)
+        assert np.abs(a - b).max() <= 1e-12 * np.abs(b).max()
+
+
+# ---------------------------------------------------------------------------
 # Failure mode the tanh stabiliser addresses (Sec. 4.3), emulated on the CPU
 # ---------------------------------------------------------------------------
 
@@ -579,6 +795,19 @@ MUTATIONS = {
         lambda x, w, gy, n, m, p: orig(x, w, gy, n, m, O.PREC_FP32))),
     "grad_no_c": ("grad_spectrum", lambda orig: (
         lambda gy, n, m: O.forward_spectrum(gy, n, m) * float(np.prod(n)))),
+    "cp_drop_lambda": ("cp_dense", lambda orig: (
+        lambda lam, ui, uo, um: orig(np.ones_like(lam), ui, uo, um))),
+    "cp_adjoint_no_conj": ("cp_contract", lambda orig: (
+        lambda spec, lam, ui, uo, um, policy=O.POLICY_MIN_RESULT, adjoint=False, steps=None:
+        O.contract_path([spec, lam, ui, uo] + list(um), O.cp_labels(len(um), adjoint)[0],
+                        O.greedy_path(O.cp_labels(len(um), adjoint)[0],
+                                      O.cp_sizes(spec.shape[0], ui.shape[0], uo.shape[0],
+                                                 spec.shape[2:], lam.shape[0]),
+                                      O.cp_labels(len(um), adjoint)[1], policy)))),
+    "cp_wgrad_lambda_no_conj": ("cp_bwd_weight", lambda orig: (
+        lambda x, gy, lam, ui, uo, um, n, m, p: (
+            np.conj(orig(x, gy, lam, ui, uo, um, n, m, p)[0]),) +
+        tuple(orig(x, gy, lam, ui, uo, um, n, m, p)[1:]))),
     "wgrad_no_conj": ("bwd_weight", lambda orig: (
         lambda x, gy, n, m, p: np.einsum(
             "bi...,bo...->io...",
