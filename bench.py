@@ -88,6 +88,10 @@ def step_bytes(wl, es, caches=True):
         nparam = (np.prod(r) + Ci * r[0] + Co * r[1]
                   + sum(k * rr for k, rr in zip(wl.kdims, r[2:])))
         W, gW = 2 * nparam * es, 2 * nparam * 4
+    elif wl.weight == "cp":
+        r = wl.rank[0]
+        nparam = r * (1 + Ci + Co + sum(wl.kdims))
+        W, gW = 2 * nparam * es, 2 * nparam * 4
     else:
         W, gW = Ci * Co * K * 2 * es, Ci * Co * K * 2 * 4
     total = S_in + S_out + (S_out + S_in + S_in) + 2 * W + gW
@@ -139,14 +143,17 @@ def cpu_baseline(wl, x, w, gy, prec, seconds):
     while True:
         b = done % wl.batch
         xb, gb = x[b:b + 1], gy[b:b + 1]
-        if wl.weight == "tucker":
+        if wl.weight in ("tucker", "cp"):
             core = synth.pairs_to_complex(w["core"])
             u_in = synth.pairs_to_complex(w["u_in"])
             u_out = synth.pairs_to_complex(w["u_out"])
             um = [synth.pairs_to_complex(u) for u in w["u_mode"]]
-            O.tucker_fwd(xb, core, u_in, u_out, um, wl.n, wl.modes, oprec)
-            O.tucker_bwd_data(xb, core, u_in, u_out, um, gb, wl.n, wl.modes, oprec)
-            O.tucker_bwd_weight(xb, gb, core, u_in, u_out, um, wl.n, wl.modes, oprec)
+            fw, bd, bw = ((O.tucker_fwd, O.tucker_bwd_data, O.tucker_bwd_weight)
+                          if wl.weight == "tucker" else
+                          (O.cp_fwd, O.cp_bwd_data, O.cp_bwd_weight))
+            fw(xb, core, u_in, u_out, um, wl.n, wl.modes, oprec)
+            bd(xb, core, u_in, u_out, um, gb, wl.n, wl.modes, oprec)
+            bw(xb, gb, core, u_in, u_out, um, wl.n, wl.modes, oprec)
         else:
             wc = synth.pairs_to_complex(w)
             O.fwd(xb, wc, wl.n, wl.modes, oprec)
@@ -179,12 +186,12 @@ def main():
     npdt = np.float16 if args.precision == "fp16_tanh" else np.float32
     es = 2 if args.precision == "fp16_tanh" else 4
     pc = B.FNO_PREC_FP16_TANH if args.precision == "fp16_tanh" else B.FNO_PREC_FP32
-    kind = B.FNO_WEIGHT_TUCKER if wl.weight == "tucker" else B.FNO_WEIGHT_DENSE
+    kind = {"tucker": B.FNO_WEIGHT_TUCKER, "cp": B.FNO_WEIGHT_CP}.get(wl.weight,
+                                                                    B.FNO_WEIGHT_DENSE)
     pol = B.FNO_PATH_MIN_RESULT if args.policy == "min_result" else B.FNO_PATH_MIN_NET
     x = synth.make_x(wl, npdt)
     gy = synth.make_gy(wl, npdt)
-    w = synth.make_tucker_weight(wl, npdt) if wl.weight == "tucker" else \
-        synth.make_dense_weight(wl, npdt)
+    w = synth.make_weight(wl, npdt)
     layer = SpectralConv(wl.n, wl.modes, wl.batch, wl.c_in, wl.c_out, pc, kind, wl.rank, pol)
     dev = lambda a: torch.from_numpy(np.ascontiguousarray(a)).cuda()  # noqa: E731
     xd, gyd = dev(x), dev(gy)
@@ -292,7 +299,7 @@ def main():
                    "precision": args.precision, "spectral_caches": caches,
                    "backward": "separate" if args.separate_bwd else "combined",
                    "launch": "stream" if args.no_graph else "hip_graph",
-                   "path_policy": args.policy if wl.weight == "tucker" else None},
+                   "path_policy": args.policy if wl.weight != "dense" else None},
         "step_alg_bytes": sbytes,
         "step_hbm_gbs": round(sbytes / (ms_step / 1e3) / 1e9, 1),
         "step_hbm_frac": round(sbytes / (ms_step / 1e3) / 1e9 / HBM_PEAK_GBS, 4),

@@ -65,9 +65,16 @@ typedef enum {
   FNO_PREC_FP16_TANH = 1    /* fp16 storage, fp32 accumulation, tanh (Sec. 4.3) */
 } fno_precision;
 
-typedef enum { FNO_WEIGHT_DENSE = 0, FNO_WEIGHT_TUCKER = 1 } fno_weight_kind;
+/* Spectral weight parameterisation: dense, Tucker (the tensorised FNO of
+ * Sec. 2) or CP (canonical polyadic, the factorisation of the Navier-Stokes
+ * and Darcy runs of Sec. 4.6). */
+typedef enum {
+  FNO_WEIGHT_DENSE = 0,
+  FNO_WEIGHT_TUCKER = 1,
+  FNO_WEIGHT_CP = 2
+} fno_weight_kind;
 
-/* Greedy rule for the Tucker contraction order (Sec. 4.2).  MIN_RESULT takes
+/* Greedy rule for the Tucker and CP contraction order (Sec. 4.2).  MIN_RESULT takes
  * the pair whose intermediate has the fewest elements; MIN_NET the pair that
  * minimises (result - both inputs).  Ties go to the lexicographically smallest
  * pair of the current operand list. */
@@ -84,12 +91,13 @@ typedef enum {
  * counts modes[0..ndim-1]: axes j < d keep K_j = 2 m_j slots (2 m_j <= N_j),
  * the last axis keeps K_d = m_d slots (1 <= m_d <= N_d/2 + 1).  Retained slot
  * t on a leading axis is FFT index k = t for t < m, k = N - 2m + t otherwise.
- * rank = (r_in, r_out, r_1..r_d) for Tucker weights, ignored for dense. */
+ * rank = (r_in, r_out, r_1..r_d) for Tucker weights, rank[0] = R for CP
+ * weights, ignored for dense. */
 typedef struct {
   int32_t ndim;          /* 1, 2 or 3                      */
   int32_t precision;     /* fno_precision                  */
   int32_t weight_kind;   /* fno_weight_kind                */
-  int32_t path_policy;   /* fno_path_policy (Tucker only)  */
+  int32_t path_policy;   /* fno_path_policy (Tucker, CP)   */
   int64_t batch;
   int64_t c_in;
   int64_t c_out;
@@ -100,10 +108,15 @@ typedef struct {
 
 /* Spectral weights R (device pointers, element type of the precision mode).
  *   dense  : [c_in, c_out, K_1..K_d] complex
+ * Tucker:
  *   core   : [r_in, r_out, r_1..r_d] complex
  *   u_in   : [c_in, r_in] complex,  u_out: [c_out, r_out] complex
  *   u_mode : u_mode[j] is [K_j, r_j] complex
- * W[i,o,t] = sum core[a,e,c..] u_in[i,a] u_out[o,e] prod_j u_mode[j][t_j,c_j]. */
+ *   W[i,o,t] = sum core[a,e,c..] u_in[i,a] u_out[o,e] prod_j u_mode[j][t_j,c_j]
+ * CP (rank R = rank[0]; `core` holds the weights lambda):
+ *   core   : lambda [R] complex
+ *   u_in   : [c_in, R], u_out: [c_out, R], u_mode[j]: [K_j, R], all complex
+ *   W[i,o,t] = sum_r lambda[r] u_in[i,r] u_out[o,r] prod_j u_mode[j][t_j,r] */
 typedef struct {
   const void *dense;
   const void *core;
@@ -113,7 +126,8 @@ typedef struct {
 } fno_weights;
 
 /* Weight gradients, same shapes as fno_weights, always fp32 complex.  Dense
- * uses `dense`; Tucker uses core, u_in, u_out and u_mode[0..d-1]. */
+ * uses `dense`; Tucker and CP use core (CP: the lambda gradient), u_in, u_out
+ * and u_mode[0..d-1]. */
 typedef struct {
   void *dense;
   void *core;
@@ -189,13 +203,15 @@ fno_status fno_spectral_conv_bwd(const fno_conv_desc *desc, const void *x,
 fno_status fno_mode_frequency(const fno_conv_desc *desc, int32_t axis, int64_t t,
                               int64_t *k);
 
-/* Host-only: the pairwise Tucker contraction order for FNO_OP_FWD or
- * FNO_OP_BWD_DATA (the greedy rule of Sec. 4.2 under desc->path_policy).
- * Writes 3 int32 per step: p, q (positions in the current operand list,
- * p < q; the two leave the list and the result is appended) and the bit mask
- * of the result's indices: bit 0 batch, 1 c_in, 2 c_out, 3 r_in, 4 r_out,
- * 5+j spatial axis j, 8+j rank of axis j.  The initial list is
- * [spectrum, core, u_in, u_out, u_1..u_d].  `cap` is the capacity in steps. */
+/* Host-only: the pairwise contraction order of Tucker or CP weights for
+ * FNO_OP_FWD or FNO_OP_BWD_DATA (the greedy rule of Sec. 4.2 under
+ * desc->path_policy).  Writes 3 int32 per step: p, q (positions in the
+ * current operand list, p < q; the two leave the list and the result is
+ * appended) and the bit mask of the result's indices: bit 0 batch, 1 c_in,
+ * 2 c_out, 3 r_in, 4 r_out, 5+j spatial axis j, 8+j rank of axis j (Tucker),
+ * 11 the CP rank.  The initial list is [spectrum, core (CP: lambda), u_in,
+ * u_out, u_1..u_d].  FNO_ERR_INVALID_ARGUMENT for dense weights.  `cap` is
+ * the capacity in steps. */
 fno_status fno_contraction_path(const fno_conv_desc *desc, fno_op op, int32_t *steps,
                                 int32_t cap, int32_t *n_steps);
 

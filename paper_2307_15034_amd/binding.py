@@ -25,6 +25,7 @@ FNO_PREC_FP32 = 0
 FNO_PREC_FP16_TANH = 1
 FNO_WEIGHT_DENSE = 0
 FNO_WEIGHT_TUCKER = 1
+FNO_WEIGHT_CP = 2
 FNO_PATH_MIN_RESULT = 0
 FNO_PATH_MIN_NET = 1
 FNO_OP_FWD = 0
@@ -33,7 +34,7 @@ FNO_OP_BWD_WEIGHT = 2
 FNO_OP_BWD = 3
 
 LABEL_BITS = {"b": 0, "i": 1, "o": 2, "a": 3, "e": 4, "x": 5, "y": 6, "z": 7,
-              "c": 8, "d": 9, "f": 10}
+              "c": 8, "d": 9, "f": 10, "r": 11}
 
 
 class FnoError(RuntimeError):

@@ -676,8 +676,12 @@ __global__ __launch_bounds__(256) void wgrad_kernel(WgradArgs a) {
 }
 
 // ---------------------------------------------------------------------------
-// Generic pairwise complex contraction (Tucker path steps), fp32 accumulate.
-// One thread per result element; strides decode the index groups.
+// Generic pairwise complex contraction (Tucker and CP path steps), fp32
+// accumulate.  The result index is decoded once into the two operands'
+// offsets; the contracted indices are walked with an odometer (counters and
+// offsets stepped in place by a mixed-radix addition, no division per
+// element).  Two launch shapes: one thread per result element, or, for few
+// results with long reductions, one work-group per result element.
 // ---------------------------------------------------------------------------
 __device__ __forceinline__ f2 load_elem(const void* p, int elem, int64_t off) {
   if (elem == ELEM_F16) {
@@ -687,12 +691,13 @@ __device__ __forceinline__ f2 load_elem(const void* p, int elem, int64_t off) {
   return reinterpret_cast<const f2*>(p)[off];
 }
 
-__global__ __launch_bounds__(256) void pair_kernel(PairArgs a) {
-  const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (idx >= a.out_size) return;
+// Offsets of result element idx in A and B, and its last-spatial-axis slot.
+__device__ __forceinline__ void pair_decode(const PairArgs& a, int64_t idx, int64_t& aoff,
+                                            int64_t& boff, int64_t& cidx) {
   int64_t rem = idx;
-  int64_t aoff = 0, boff = 0;
-  int64_t cidx = 0;
+  aoff = 0;
+  boff = 0;
+  cidx = 0;
   for (int k = a.n_out - 1; k >= 0; --k) {
     const int64_t e = a.out_ext[k];
     const int64_t v = rem % e;
@@ -701,31 +706,139 @@ __global__ __launch_bounds__(256) void pair_kernel(PairArgs a) {
     boff += v * a.b_stride_out[k];
     if (k == a.scale_c_axis) cidx = v;
   }
-  float sr = 0.0f, si = 0.0f;
-  for (int64_t r = 0; r < a.red_size; ++r) {
-    int64_t rr = r, ao = aoff, bo = boff;
-    for (int k = a.n_red - 1; k >= 0; --k) {
-      const int64_t e = a.red_ext[k];
-      const int64_t v = rr % e;
-      rr /= e;
-      ao += v * a.a_stride_red[k];
-      bo += v * a.b_stride_red[k];
+}
+
+// Advance the contracted-index counters by `dig` (digits of the step in the
+// radix of the contracted extents, innermost last), carrying outwards, and
+// move the two offsets along.
+__device__ __forceinline__ void pair_step(const PairArgs& a, const int64_t (&dig)[PW_MAXIDX],
+                                          int64_t (&cnt)[PW_MAXIDX], int64_t& ao,
+                                          int64_t& bo) {
+  int64_t carry = 0;
+#pragma unroll
+  for (int k = PW_MAXIDX - 1; k >= 0; --k) {
+    if (k < a.n_red) {
+      const int64_t add = dig[k] + carry;
+      cnt[k] += add;
+      ao += add * a.a_stride_red[k];
+      bo += add * a.b_stride_red[k];
+      carry = 0;
+      if (cnt[k] >= a.red_ext[k]) {
+        cnt[k] -= a.red_ext[k];
+        ao -= a.red_ext[k] * a.a_stride_red[k];
+        bo -= a.red_ext[k] * a.b_stride_red[k];
+        carry = 1;
+      }
     }
-    f2 x = load_elem(a.a, a.a_elem, ao);
-    f2 y = load_elem(a.b, a.b_elem, bo);
-    if (a.conj_a) x[1] = -x[1];
-    if (a.conj_b) y[1] = -y[1];
-    sr = fmaf(x[0], y[0], sr);
-    sr = fmaf(-x[1], y[1], sr);
-    si = fmaf(x[0], y[1], si);
-    si = fmaf(x[1], y[0], si);
   }
+}
+
+// Counters of contracted element r0 and the digits of `step`; offsets move
+// to element r0.
+__device__ __forceinline__ void pair_start(const PairArgs& a, int64_t r0, int64_t step,
+                                           int64_t (&dig)[PW_MAXIDX], int64_t (&cnt)[PW_MAXIDX],
+                                           int64_t& ao, int64_t& bo) {
+  int64_t q = step, rr = r0;
+#pragma unroll
+  for (int k = PW_MAXIDX - 1; k >= 0; --k) {
+    dig[k] = 0;
+    cnt[k] = 0;
+    if (k < a.n_red) {
+      const int64_t e = a.red_ext[k];
+      dig[k] = q % e;
+      q /= e;
+      cnt[k] = rr % e;
+      rr /= e;
+      ao += cnt[k] * a.a_stride_red[k];
+      bo += cnt[k] * a.b_stride_red[k];
+    }
+  }
+}
+
+__device__ __forceinline__ void pair_fma(const PairArgs& a, f2 x, f2 y, float& sr, float& si) {
+  if (a.conj_a) x[1] = -x[1];
+  if (a.conj_b) y[1] = -y[1];
+  sr = fmaf(x[0], y[0], sr);
+  sr = fmaf(-x[1], y[1], sr);
+  si = fmaf(x[0], y[1], si);
+  si = fmaf(x[1], y[0], si);
+}
+
+// Sum over contracted elements r0, r0 + step, ... below r1, starting from
+// the result element's offsets.  Eight elements' loads are issued before
+// their products (in the same order, so the sum is the plain sequential one).
+__device__ __forceinline__ void pair_reduce(const PairArgs& a, int64_t r0, int64_t r1,
+                                            int64_t step, int64_t ao, int64_t bo, float& sr,
+                                            float& si) {
+  if (r0 >= r1) return;
+  int64_t dig[PW_MAXIDX], cnt[PW_MAXIDX];
+  pair_start(a, r0, step, dig, cnt, ao, bo);
+  constexpr int UN = 8;
+  int64_t r = r0;
+  for (; r + (UN - 1) * step < r1; r += UN * step) {
+    f2 xs[UN], ys[UN];
+#pragma unroll
+    for (int u = 0; u < UN; ++u) {
+      xs[u] = load_elem(a.a, a.a_elem, ao);
+      ys[u] = load_elem(a.b, a.b_elem, bo);
+      pair_step(a, dig, cnt, ao, bo);
+    }
+#pragma unroll
+    for (int u = 0; u < UN; ++u) pair_fma(a, xs[u], ys[u], sr, si);
+  }
+  for (; r < r1; r += step) {
+    pair_fma(a, load_elem(a.a, a.a_elem, ao), load_elem(a.b, a.b_elem, bo), sr, si);
+    pair_step(a, dig, cnt, ao, bo);
+  }
+}
+
+__device__ __forceinline__ void pair_store(const PairArgs& a, int64_t idx, int64_t cidx,
+                                           float sr, float si) {
   float s = a.scale;
   if (a.scale_c_axis >= 0) s *= (cidx == 0 || 2 * cidx == a.Nb) ? 1.0f : 2.0f;
   if (a.out_elem == ELEM_F16) {
     reinterpret_cast<h2*>(a.out)[idx] = h2{to_h(sr * s), to_h(si * s)};
   } else {
     reinterpret_cast<f2*>(a.out)[idx] = f2{sr * s, si * s};
+  }
+}
+
+__global__ __launch_bounds__(256) void pair_kernel(PairArgs a) {
+  const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (idx >= a.out_size) return;
+  int64_t aoff, boff, cidx;
+  pair_decode(a, idx, aoff, boff, cidx);
+  float sr = 0.0f, si = 0.0f;
+  pair_reduce(a, 0, a.red_size, 1, aoff, boff, sr, si);
+  pair_store(a, idx, cidx, sr, si);
+}
+
+// One work-group per result element: thread t takes the contracted elements
+// t, t + 256, ... (consecutive threads read consecutive elements of the
+// innermost contracted index); the 256 partial sums are added in a fixed
+// order (bit-reproducible).
+__global__ __launch_bounds__(256) void pair_block_kernel(PairArgs a) {
+  __shared__ float red[2][4];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int64_t idx = blockIdx.x;
+  int64_t aoff, boff, cidx;
+  pair_decode(a, idx, aoff, boff, cidx);
+  float sr = 0.0f, si = 0.0f;
+  pair_reduce(a, tid, a.red_size, 256, aoff, boff, sr, si);
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) {
+    sr += __shfl_xor(sr, off, 64);
+    si += __shfl_xor(si, off, 64);
+  }
+  if (lane == 0) {
+    red[0][wave] = sr;
+    red[1][wave] = si;
+  }
+  __syncthreads();
+  if (tid == 0) {
+    const float tr = (red[0][0] + red[0][1]) + (red[0][2] + red[0][3]);
+    const float ti = (red[1][0] + red[1][1]) + (red[1][2] + red[1][3]);
+    pair_store(a, idx, cidx, tr, ti);
   }
 }
 
@@ -836,8 +949,15 @@ hipError_t launch_wgrad(int elem, const WgradArgs& a, hipStream_t s) {
 
 hipError_t launch_pair(const PairArgs& a, hipStream_t s) {
   if (a.out_size <= 0) return hipSuccess;
-  dim3 grid((unsigned)((a.out_size + 255) / 256)), block(256);
-  hipLaunchKernelGGL(pair_kernel, grid, block, 0, s, a);
+  // Few results with long reductions (weight-gradient steps): a work-group
+  // per result.  Otherwise a thread per result.
+  if (a.red_size >= 2048 && a.out_size <= (int64_t)1 << 20) {
+    dim3 grid((unsigned)a.out_size), block(256);
+    hipLaunchKernelGGL(pair_block_kernel, grid, block, 0, s, a);
+  } else {
+    dim3 grid((unsigned)((a.out_size + 255) / 256)), block(256);
+    hipLaunchKernelGGL(pair_kernel, grid, block, 0, s, a);
+  }
   return hipGetLastError();
 }
 

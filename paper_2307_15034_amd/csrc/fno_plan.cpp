@@ -41,7 +41,8 @@ fno_status check_desc(const fno_conv_desc* d) {
   if (d->ndim < 1 || d->ndim > 3) return FNO_ERR_INVALID_ARGUMENT;
   if (d->precision != FNO_PREC_FP32 && d->precision != FNO_PREC_FP16_TANH)
     return FNO_ERR_INVALID_ARGUMENT;
-  if (d->weight_kind != FNO_WEIGHT_DENSE && d->weight_kind != FNO_WEIGHT_TUCKER)
+  if (d->weight_kind != FNO_WEIGHT_DENSE && d->weight_kind != FNO_WEIGHT_TUCKER &&
+      d->weight_kind != FNO_WEIGHT_CP)
     return FNO_ERR_INVALID_ARGUMENT;
   if (d->path_policy != FNO_PATH_MIN_RESULT && d->path_policy != FNO_PATH_MIN_NET)
     return FNO_ERR_INVALID_ARGUMENT;
@@ -59,6 +60,7 @@ fno_status check_desc(const fno_conv_desc* d) {
   if (d->weight_kind == FNO_WEIGHT_TUCKER)
     for (int j = 0; j < 2 + nd; ++j)
       if (d->rank[j] < 1) return FNO_ERR_INVALID_ARGUMENT;
+  if (d->weight_kind == FNO_WEIGHT_CP && d->rank[0] < 1) return FNO_ERR_INVALID_ARGUMENT;
   // Sizes the kernels cover: extents up to 65536 per axis, index math in 64
   // bits, retained counts per plane within the register tiles.
   for (int j = 0; j < nd; ++j)
@@ -169,6 +171,34 @@ std::vector<PStep> greedy_order(std::vector<std::string> ops, const Sizes& sz,
   return steps;
 }
 
+// Memory order of the intermediates of a path (the greedy rule fixes which
+// indices a result keeps, not their order): the indices of the larger input
+// keep that input's order, innermost last, and the others go outermost.
+// Consecutive result elements then step through the larger input
+// contiguously.  The last step keeps the output's order.
+std::vector<PStep> memory_order(std::vector<PStep> path, std::vector<std::string> ops,
+                                const Sizes& sz) {
+  for (size_t st = 0; st < path.size(); ++st) {
+    PStep& ps = path[st];
+    if (st + 1 < path.size()) {
+      const std::string& big =
+          label_size(ops[ps.p], sz) >= label_size(ops[ps.q], sz) ? ops[ps.p] : ops[ps.q];
+      std::string outer, inner;
+      for (char c : ps.res)
+        if (big.find(c) == std::string::npos) outer += c;
+      for (char c : big)
+        if (ps.res.find(c) != std::string::npos) inner += c;
+      ps.res = outer + inner;
+    }
+    std::vector<std::string> next;
+    for (int r = 0; r < (int)ops.size(); ++r)
+      if (r != ps.p && r != ps.q) next.push_back(ops[r]);
+    next.push_back(ps.res);
+    ops.swap(next);
+  }
+  return path;
+}
+
 // Index labels: b batch, i c_in, o c_out, a r_in, e r_out, x y z spatial,
 // c d f ranks of the spatial axes.
 const char kSpatial[3] = {'x', 'y', 'z'};
@@ -189,6 +219,30 @@ void tucker_labels(int nd, bool adjoint, std::vector<std::string>* ops, std::str
   *out = std::string(adjoint ? "bi" : "bo") + sp;
 }
 
+// CP weights (Sec. 4.6): one rank index r shared by lambda and every factor.
+//   Xhat(b i x..) lambda(r) u_in(i r) u_out(o r) u_j(x_j r) -> (b o x..)
+void cp_labels(int nd, bool adjoint, std::vector<std::string>* ops, std::string* out) {
+  std::string sp;
+  for (int j = 0; j < nd; ++j) sp += kSpatial[j];
+  ops->clear();
+  ops->push_back(std::string(adjoint ? "bo" : "bi") + sp);
+  ops->push_back("r");
+  ops->push_back("ir");
+  ops->push_back("or");
+  for (int j = 0; j < nd; ++j) ops->push_back(std::string(1, kSpatial[j]) + "r");
+  *out = std::string(adjoint ? "bi" : "bo") + sp;
+}
+
+Sizes cp_sizes(const fno_conv_desc* d) {
+  Sizes s;
+  s['b'] = d->batch;
+  s['i'] = d->c_in;
+  s['o'] = d->c_out;
+  s['r'] = d->rank[0];
+  for (int j = 0; j < d->ndim; ++j) s[kSpatial[j]] = kextent(d, j);
+  return s;
+}
+
 Sizes tucker_sizes(const fno_conv_desc* d) {
   Sizes s;
   s['b'] = d->batch;
@@ -203,8 +257,24 @@ Sizes tucker_sizes(const fno_conv_desc* d) {
   return s;
 }
 
+inline bool factorized(const fno_conv_desc* d) {
+  return d->weight_kind == FNO_WEIGHT_TUCKER || d->weight_kind == FNO_WEIGHT_CP;
+}
+
+// Labels and sizes of the factorised contraction (Tucker or CP).
+void weight_labels(const fno_conv_desc* d, bool adjoint, std::vector<std::string>* ops,
+                   std::string* out) {
+  if (d->weight_kind == FNO_WEIGHT_CP) cp_labels(d->ndim, adjoint, ops, out);
+  else tucker_labels(d->ndim, adjoint, ops, out);
+}
+
+Sizes weight_sizes(const fno_conv_desc* d) {
+  return d->weight_kind == FNO_WEIGHT_CP ? cp_sizes(d) : tucker_sizes(d);
+}
+
 int32_t label_bit(char c) {
   switch (c) {
+    case 'r': return 11;
     case 'b': return 0;
     case 'i': return 1;
     case 'o': return 2;
@@ -502,6 +572,7 @@ PlanKey key_of(const fno_conv_desc* d, int device) {
   }
   if (d->weight_kind == FNO_WEIGHT_TUCKER)
     for (int j = 0; j < 2 + d->ndim; ++j) k.v[14 + j] = d->rank[j];
+  if (d->weight_kind == FNO_WEIGHT_CP) k.v[14] = d->rank[0];
   return k;
 }
 
@@ -561,12 +632,14 @@ fno_status build_tables(const fno_conv_desc* d, Plan* pl) {
 // Geometry and Tucker paths: host-only, no device calls.
 void host_plan(const fno_conv_desc* d, Plan* pl) {
   pl->g = make_geo(d);
-  if (d->weight_kind == FNO_WEIGHT_TUCKER) {
-    Sizes sz = tucker_sizes(d);
-    tucker_labels(d->ndim, false, &pl->labels_fwd, &pl->out_fwd);
-    tucker_labels(d->ndim, true, &pl->labels_adj, &pl->out_adj);
-    pl->path_fwd = greedy_order(pl->labels_fwd, sz, pl->out_fwd, d->path_policy);
-    pl->path_adj = greedy_order(pl->labels_adj, sz, pl->out_adj, d->path_policy);
+  if (factorized(d)) {
+    Sizes sz = weight_sizes(d);
+    weight_labels(d, false, &pl->labels_fwd, &pl->out_fwd);
+    weight_labels(d, true, &pl->labels_adj, &pl->out_adj);
+    pl->path_fwd = memory_order(
+        greedy_order(pl->labels_fwd, sz, pl->out_fwd, d->path_policy), pl->labels_fwd, sz);
+    pl->path_adj = memory_order(
+        greedy_order(pl->labels_adj, sz, pl->out_adj, d->path_policy), pl->labels_adj, sz);
   }
 }
 
@@ -624,7 +697,7 @@ struct TuckerWs {
 // Tucker intermediates of a path (all but the last step, which writes the
 // output spectrum).
 size_t tucker_path_bytes(const fno_conv_desc* d, const std::vector<PStep>& path) {
-  Sizes sz = tucker_sizes(d);
+  Sizes sz = weight_sizes(d);
   size_t t = 0;
   for (size_t s = 0; s + 1 < path.size(); ++s)
     t += (size_t)round_up(label_size(path[s].res, sz) * 8, 256);
@@ -632,11 +705,12 @@ size_t tucker_path_bytes(const fno_conv_desc* d, const std::vector<PStep>& path)
 }
 
 size_t tucker_wgrad_bytes(const fno_conv_desc* d, const Plan* pl);
+size_t cp_wgrad_bytes(const fno_conv_desc* d, const Plan* pl);
 
 size_t ws_bytes(const fno_conv_desc* d, const Plan* pl, fno_op op, bool caches) {
   const Geo& g = pl->g;
   WsLayout w;
-  const bool tucker = d->weight_kind == FNO_WEIGHT_TUCKER;
+  const bool tucker = factorized(d);
   if (op == FNO_OP_FWD) {
     w.add(spec_bytes(g, g.Cin));
     w.add(spec_bytes(g, g.Cout));
@@ -653,7 +727,8 @@ size_t ws_bytes(const fno_conv_desc* d, const Plan* pl, fno_op op, bool caches) 
       w.add(spec_bytes(g, g.Cout));
       w.add(std::max(inter3d_bytes(g, g.Cin), inter3d_bytes(g, g.Cout)));
     }
-    if (tucker) w.add(tucker_wgrad_bytes(d, pl));
+    if (tucker)
+      w.add(d->weight_kind == FNO_WEIGHT_CP ? cp_wgrad_bytes(d, pl) : tucker_wgrad_bytes(d, pl));
   } else {  // FNO_OP_BWD: gradient spectrum, input spectrum (no cache), then
             // the data part's workspace and (Tucker) the weight part's
     w.add(spec_bytes(g, g.Cout));
@@ -986,12 +1061,13 @@ fno_status run_pair(const Sizes& sz, const Opnd& A, const Opnd& Bo, const std::s
   return FNO_OK;
 }
 
-// Evaluate a Tucker path: operands [spec, core, u_in, u_out, u_1..u_d].
+// Evaluate a Tucker or CP path: operands [spec, core (CP: lambda), u_in,
+// u_out, u_1..u_d].
 fno_status run_tucker_path(const fno_conv_desc* d, const Plan* pl, bool adjoint,
                            const void* spec, const fno_weights* w, void* out_spec,
                            char* scratch, hipStream_t s) {
   const Geo& g = pl->g;
-  Sizes sz = tucker_sizes(d);
+  Sizes sz = weight_sizes(d);
   const std::vector<PStep>& path = adjoint ? pl->path_adj : pl->path_fwd;
   const std::vector<std::string>& labs = adjoint ? pl->labels_adj : pl->labels_fwd;
   std::vector<Opnd> ops;
@@ -1166,6 +1242,115 @@ size_t tucker_wgrad_bytes(const fno_conv_desc* d, const Plan* pl) {
   return used;
 }
 
+// Fixed schedule of the CP weight gradient (chain rule through
+// W = sum_r lambda_r u_in(r) u_out(r) prod_j u_j(r)), with G' = sqrt(N) c G:
+//   P[b,r,sp] = sum_i conj(Xhat) conj(u_in),  Q[b,r,sp] = sum_o G' conj(u_out),
+//   R[r,sp] = sum_b P Q,  S[r,sp] = lambda prod_j u_j,
+//   g_lambda = sum_sp R prod_j conj(u_j),
+//   g_u_j = conj(lambda) sum_{sp except j} R prod_{q != j} conj(u_q),
+//   g_u_in = sum_{b,sp} conj(Xhat) (Q conj(S)),  g_u_out = sum_{b,sp} G' (P conj(S)).
+fno_status run_cp_wgrad(const fno_conv_desc* d, const Plan* pl, const void* xh, const void* gh,
+                        const fno_weights* w, fno_weight_grads* gw, char* scratch,
+                        hipStream_t s, size_t* scratch_used = nullptr) {
+  const bool dry = scratch_used != nullptr;
+  auto pair = [&](const Sizes& sz_, const Opnd& A, const Opnd& Bo, const std::string& res,
+                  void* out, float scale, int c_axis_char) -> fno_status {
+    if (dry) return FNO_OK;
+    return run_pair(sz_, A, Bo, res, out, ELEM_F32, scale, c_axis_char, pl->g.Nb, s);
+  };
+  const Geo& g = pl->g;
+  const int nd = d->ndim;
+  Sizes sz = cp_sizes(d);
+  std::string sp;
+  for (int j = 0; j < nd; ++j) sp += kSpatial[j];
+  const char clast = kSpatial[nd - 1];
+  const float sqN = (float)std::sqrt((double)g.N);
+  size_t off = 0;
+  auto buf = [&](const std::string& lab) {
+    void* p = scratch + off;
+    off += (size_t)round_up(label_size(lab, sz) * 8, 256);
+    return p;
+  };
+  auto F = [&](const void* p, const std::string& lab, int conj) {
+    return Opnd{p, lab, ELEM_F32, conj};
+  };
+  auto Wt = [&](const void* p, const std::string& lab, int conj) {
+    return Opnd{p, lab, g.elem, conj};
+  };
+  auto U = [&](int j, int conj) { return Wt(w->u_mode[j], std::string(1, kSpatial[j]) + "r", conj); };
+  fno_status r;
+  const std::string lP = "br" + sp, lR = "r" + sp;
+  void* P = buf(lP);
+  void* Q = buf(lP);
+  void* Rb = buf(lR);
+  if ((r = pair(sz, Wt(xh, "bi" + sp, 1), Wt(w->u_in, "ir", 1), lP, P, 1.0f, 0))) return r;
+  if ((r = pair(sz, Wt(gh, "bo" + sp, 0), Wt(w->u_out, "or", 1), lP, Q, sqN, clast))) return r;
+  if ((r = pair(sz, F(P, lP, 0), F(Q, lP, 0), lR, Rb, 1.0f, 0))) return r;
+  // g_lambda: contract R with conj(u_j) along every spatial axis
+  {
+    Opnd cur = F(Rb, lR, 0);
+    std::string lab = lR;
+    for (int j = 0; j < nd; ++j) {
+      std::string nl;
+      for (char c : lab)
+        if (c != kSpatial[j]) nl += c;
+      const bool last = j == nd - 1;
+      void* dst = last ? gw->core : buf(nl);
+      if ((r = pair(sz, cur, U(j, 1), nl, dst, 1.0f, 0))) return r;
+      cur = F(dst, nl, 0);
+      lab = nl;
+    }
+  }
+  // g_u_j: R contracted with conj(u_q) for q != j, then times conj(lambda)
+  for (int j = 0; j < nd; ++j) {
+    Opnd cur = F(Rb, lR, 0);
+    std::string lab = lR;
+    for (int q = 0; q < nd; ++q) {
+      if (q == j) continue;
+      std::string nl;
+      for (char c : lab)
+        if (c != kSpatial[q]) nl += c;
+      void* dst = buf(nl);
+      if ((r = pair(sz, cur, U(q, 1), nl, dst, 1.0f, 0))) return r;
+      cur = F(dst, nl, 0);
+      lab = nl;
+    }
+    if ((r = pair(sz, cur, Wt(w->core, "r", 1), std::string(1, kSpatial[j]) + "r",
+                  gw->u_mode[j], 1.0f, 0)))
+      return r;
+  }
+  // S[r, sp] = lambda[r] prod_j u_j[sp_j, r]
+  Opnd S = Wt(w->core, "r", 0);
+  {
+    std::string lab = "r";
+    for (int j = 0; j < nd; ++j) {
+      const std::string nl = lab + kSpatial[j];
+      void* dst = buf(nl);
+      if ((r = pair(sz, S, U(j, 0), nl, dst, 1.0f, 0))) return r;
+      S = F(dst, nl, 0);
+      lab = nl;
+    }
+  }
+  const Opnd Sc{S.ptr, S.lab, S.elem, 1};
+  void* Z1 = buf(lP);
+  if ((r = pair(sz, F(Q, lP, 0), Sc, lP, Z1, 1.0f, 0))) return r;
+  if ((r = pair(sz, Wt(xh, "bi" + sp, 1), F(Z1, lP, 0), "ir", gw->u_in, 1.0f, 0))) return r;
+  void* Z2 = buf(lP);
+  if ((r = pair(sz, F(P, lP, 0), Sc, lP, Z2, sqN, clast))) return r;
+  if ((r = pair(sz, Wt(gh, "bo" + sp, 0), F(Z2, lP, 0), "or", gw->u_out, 1.0f, 0))) return r;
+  if (dry) *scratch_used = off;
+  return FNO_OK;
+}
+
+size_t cp_wgrad_bytes(const fno_conv_desc* d, const Plan* pl) {
+  fno_weights w{};
+  fno_weight_grads gw{};
+  size_t used = 0;
+  char dummy = 0;
+  (void)run_cp_wgrad(d, pl, &dummy, &dummy, &w, &gw, &dummy, nullptr, &used);
+  return used;
+}
+
 fno_status check_weights(const fno_conv_desc* d, const fno_weights* w) {
   if (!w) return FNO_ERR_INVALID_ARGUMENT;
   if (d->weight_kind == FNO_WEIGHT_DENSE) {
@@ -1228,10 +1413,10 @@ static fno_status path_for(const fno_conv_desc* d, fno_op op, std::vector<PStep>
                            std::vector<std::string>* labs, std::string* out) {
   fno_status st = check_desc(d);
   if (st != FNO_OK && st != FNO_ERR_UNSUPPORTED) return st;
-  if (d->weight_kind != FNO_WEIGHT_TUCKER) return FNO_ERR_INVALID_ARGUMENT;
+  if (!factorized(d)) return FNO_ERR_INVALID_ARGUMENT;
   if (op != FNO_OP_FWD && op != FNO_OP_BWD_DATA) return FNO_ERR_INVALID_ARGUMENT;
-  tucker_labels(d->ndim, op == FNO_OP_BWD_DATA, labs, out);
-  *path = greedy_order(*labs, tucker_sizes(d), *out, d->path_policy);
+  weight_labels(d, op == FNO_OP_BWD_DATA, labs, out);
+  *path = greedy_order(*labs, weight_sizes(d), *out, d->path_policy);
   return FNO_OK;
 }
 
@@ -1263,7 +1448,7 @@ fno_status fno_contraction_path_cost(const fno_conv_desc* d, fno_op op, int64_t*
   std::string out;
   fno_status st = path_for(d, op, &path, &labs, &out);
   if (st != FNO_OK) return st;
-  Sizes sz = tucker_sizes(d);
+  Sizes sz = weight_sizes(d);
   int64_t total = 0, pk = 0;
   std::vector<std::string> ops = labs;
   for (const PStep& ps : path) {
@@ -1390,7 +1575,7 @@ fno_status fno_spectral_conv_bwd_weight(const fno_conv_desc* d, const void* x, c
   if (!gw) return FNO_ERR_INVALID_ARGUMENT;
   if (x_hat ? !aligned16(x_hat) : !okptr(x)) return FNO_ERR_INVALID_ARGUMENT;
   if (gy_hat ? !aligned16(gy_hat) : !okptr(gy)) return FNO_ERR_INVALID_ARGUMENT;
-  const bool tucker = d->weight_kind == FNO_WEIGHT_TUCKER;
+  const bool tucker = factorized(d);
   if (tucker) {
     if ((st = check_weights(d, w)) != FNO_OK) return st;
     if (!okptr(gw->core) || !okptr(gw->u_in) || !okptr(gw->u_out))
@@ -1444,6 +1629,7 @@ fno_status fno_spectral_conv_bwd_weight(const fno_conv_desc* d, const void* x, c
     }));
     return FNO_OK;
   }
+  if (d->weight_kind == FNO_WEIGHT_CP) return run_cp_wgrad(d, pl, xh, gh, w, gw, tsc, s);
   return run_tucker_wgrad(d, pl, xh, gh, w, gw, tsc, s);
 }
 
@@ -1454,7 +1640,7 @@ fno_status fno_spectral_conv_bwd(const fno_conv_desc* d, const void* x, const fn
   fno_status st = check_desc(d);
   if (st != FNO_OK) return st;
   const int tanh_on = d->precision == FNO_PREC_FP16_TANH;
-  const bool tucker = d->weight_kind == FNO_WEIGHT_TUCKER;
+  const bool tucker = factorized(d);
   if (!okptr(gy) || !okptr(gx) || !gw) return FNO_ERR_INVALID_ARGUMENT;
   if ((tanh_on || !x_hat) && !okptr(x)) return FNO_ERR_INVALID_ARGUMENT;
   if (x_hat && !aligned16(x_hat)) return FNO_ERR_INVALID_ARGUMENT;

@@ -30,6 +30,8 @@ class SpectralConv:
       dense: [c_in, c_out, K_1..K_d, 2]
       tucker: core [r_in, r_out, r_1..r_d, 2], u_in [c_in, r_in, 2],
               u_out [c_out, r_out, 2], u_mode[j] [K_j, r_j, 2]
+      cp (rank R): core = lambda [R, 2], u_in [c_in, R, 2], u_out [c_out, R, 2],
+              u_mode[j] [K_j, R, 2]
     The storage dtype is float16 in fp16+tanh mode and float32 in fp32 mode.
     """
 
@@ -76,6 +78,12 @@ class SpectralConv:
             return torch.empty((self.c_in, self.c_out) + self.kdims + (2,), **f)
         r = self.rank
         d = len(self.n)
+        if self.weight_kind == B.FNO_WEIGHT_CP:
+            # the lambda gradient travels in the "core" slot
+            return {"core": torch.empty((r[0], 2), **f),
+                    "u_in": torch.empty((self.c_in, r[0], 2), **f),
+                    "u_out": torch.empty((self.c_out, r[0], 2), **f),
+                    "u_mode": [torch.empty((k, r[0], 2), **f) for k in self.kdims]}
         return {"core": torch.empty(tuple(r[:2]) + tuple(r[2:2 + d]) + (2,), **f),
                 "u_in": torch.empty((self.c_in, r[0], 2), **f),
                 "u_out": torch.empty((self.c_out, r[1], 2), **f),

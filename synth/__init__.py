@@ -16,6 +16,9 @@ Workloads (the five layer shapes the paper's PDE settings suggest):
      (the 64^3 latent grid of the GINO setting, Sec. 4.1)
   5  2-D 256x256,  B=16, Cin=Cout=128, modes (32, 32),  Tucker core (13,13,6,3)
      (a tensorised FNO, Sec. 2 "FNO and extensions")
+  6  2-D 128x128,  B=32, Cin=Cout=64,  modes (32, 32),  CP rank 16, GRF + mixing
+     (the CP-factorised Navier-Stokes setting of Sec. 4.6; the paper does not
+     give the rank: 16 keeps the parameter count near the Tucker workload's)
 
 Synthetic Gaussian random fields stand in for the paper's datasets (none are
 available here).  Recipe (one independent field per (sample, channel)):
@@ -29,6 +32,8 @@ available here).  Recipe (one independent field per (sample, channel)):
   * dense weights: real and imaginary parts iid N(0, 1/(Cin*Cout));
   * Tucker: factor entries re, im ~ N(0, 1/(2 r)), core entries re, im ~
     N(0, 1/(Cin*Cout));
+  * CP (rank R): factor entries re, im ~ N(0, 1/2), lambda re, im ~
+    N(0, 1/(Cin*Cout*R)), so that W has the dense weights' variance;
   * upstream gradient gy: iid N(0, 1).
 
 Seeds: numpy SeedSequence([workload_id, stream]) with streams x=0, W=1, gy=2,
@@ -59,8 +64,8 @@ class Workload:
     c_out: int
     n: Tuple[int, ...]
     modes: Tuple[int, ...]
-    weight: str = "dense"            # "dense" | "tucker"
-    rank: Optional[Tuple[int, ...]] = None   # (r_in, r_out, r_1..r_d) for tucker
+    weight: str = "dense"            # "dense" | "tucker" | "cp"
+    rank: Optional[Tuple[int, ...]] = None   # (r_in, r_out, r_1..r_d) tucker; (R,) cp
     mixing: bool = False
 
     @property
@@ -86,6 +91,8 @@ WORKLOADS: Dict[int, Workload] = {
                 (16, 16, 16)),
     5: Workload(5, "tfno2d-256x256-b16-c128-m32x32-tucker13x13x6x3", 16, 128, 128,
                 (256, 256), (32, 32), weight="tucker", rank=(13, 13, 6, 3)),
+    6: Workload(6, "cpfno2d-128x128-b32-c64-m32x32-cp16", 32, 64, 64, (128, 128), (32, 32),
+                weight="cp", rank=(16,), mixing=True),
 }
 
 
@@ -193,6 +200,28 @@ def make_tucker_weight(wl: Workload, dtype=np.float16) -> Dict[str, object]:
     u_mode = [_complex_pairs(rng, (k, r), 1.0 / np.sqrt(2 * r), dtype)
               for k, r in zip(wl.kdims, rm)]
     return {"core": core, "u_in": u_in, "u_out": u_out, "u_mode": u_mode}
+
+
+def make_cp_weight(wl: Workload, dtype=np.float16) -> Dict[str, object]:
+    """CP weights of rank R: lambda ("core" slot) [R], u_in[Cin, R],
+    u_out[Cout, R], u_mode[j][K_j, R], all as (re, im) pairs."""
+    assert wl.rank is not None
+    rng = rng_for(wl.wid, STREAM_W)
+    r = wl.rank[0]
+    lam = _complex_pairs(rng, (r,), 1.0 / np.sqrt(wl.c_in * wl.c_out * r), dtype)
+    u_in = _complex_pairs(rng, (wl.c_in, r), np.sqrt(0.5), dtype)
+    u_out = _complex_pairs(rng, (wl.c_out, r), np.sqrt(0.5), dtype)
+    u_mode = [_complex_pairs(rng, (k, r), np.sqrt(0.5), dtype) for k in wl.kdims]
+    return {"core": lam, "u_in": u_in, "u_out": u_out, "u_mode": u_mode}
+
+
+def make_weight(wl: Workload, dtype=np.float16):
+    """The workload's weights: dense array, or dict of Tucker / CP factors."""
+    if wl.weight == "tucker":
+        return make_tucker_weight(wl, dtype)
+    if wl.weight == "cp":
+        return make_cp_weight(wl, dtype)
+    return make_dense_weight(wl, dtype)
 
 
 def pairs_to_complex(a: np.ndarray) -> np.ndarray:

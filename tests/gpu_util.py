@@ -37,10 +37,13 @@ def cplx(pairs: np.ndarray) -> np.ndarray:
     return synth.pairs_to_complex(pairs)
 
 
-def make_layer(n, modes, batch, c_in, c_out, prec, tucker_rank=None, policy=0):
+def make_layer(n, modes, batch, c_in, c_out, prec, tucker_rank=None, policy=0, cp_rank=None):
     from paper_2307_15034_amd import binding as B
     from paper_2307_15034_amd.layer import SpectralConv
     pc, _, _ = prec_codes(prec)
+    if cp_rank is not None:
+        return SpectralConv(n, modes, batch, c_in, c_out, pc, B.FNO_WEIGHT_CP, (cp_rank,),
+                            policy)
     kind = B.FNO_WEIGHT_TUCKER if tucker_rank is not None else B.FNO_WEIGHT_DENSE
     return SpectralConv(n, modes, batch, c_in, c_out, pc, kind, tucker_rank, policy)
 

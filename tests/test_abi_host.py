@@ -46,7 +46,8 @@ def test_status_strings():
 
 
 def _desc_for(wl, precision=B.FNO_PREC_FP16_TANH, policy=B.FNO_PATH_MIN_RESULT, batch=None):
-    kind = B.FNO_WEIGHT_TUCKER if wl.weight == "tucker" else B.FNO_WEIGHT_DENSE
+    kind = {"tucker": B.FNO_WEIGHT_TUCKER, "cp": B.FNO_WEIGHT_CP}.get(wl.weight,
+                                                                    B.FNO_WEIGHT_DENSE)
     return B.make_desc(wl.n, wl.modes, batch or wl.batch, wl.c_in, wl.c_out, precision, kind,
                        wl.rank, policy)
 
@@ -81,15 +82,20 @@ def test_mode_frequency_random_shapes():
 
 def _mask_to_set(mask):
     inv = {v: k for k, v in B.LABEL_BITS.items()}
-    return {inv[b] for b in range(11) if mask >> b & 1}
+    return {inv[b] for b in range(12) if mask >> b & 1}
 
 
-def _check_path(d, wl_like, op, policy):
+def _check_path(d, wl_like, op, policy, cp=False):
     nd = len(wl_like["n"])
     kd = tuple(2 * m if j < nd - 1 else m for j, m in enumerate(wl_like["modes"]))
-    ops, out = O.tucker_labels(nd, adjoint=(op == B.FNO_OP_BWD_DATA))
-    sizes = O.tucker_sizes(wl_like["batch"], wl_like["c_in"], wl_like["c_out"], kd,
-                           wl_like["rank"])
+    if cp:
+        ops, out = O.cp_labels(nd, adjoint=(op == B.FNO_OP_BWD_DATA))
+        sizes = O.cp_sizes(wl_like["batch"], wl_like["c_in"], wl_like["c_out"], kd,
+                           wl_like["rank"][0])
+    else:
+        ops, out = O.tucker_labels(nd, adjoint=(op == B.FNO_OP_BWD_DATA))
+        sizes = O.tucker_sizes(wl_like["batch"], wl_like["c_in"], wl_like["c_out"], kd,
+                               wl_like["rank"])
     ref = O.greedy_path(ops, sizes, out, policy)
     got = B.fno_contraction_path(d, op)
     assert len(got) == len(ref)
@@ -127,6 +133,63 @@ def test_tucker_path_matches_oracle_random():
             for op in (B.FNO_OP_FWD, B.FNO_OP_BWD_DATA):
                 _check_path(d, dict(n=n, modes=modes, batch=b, c_in=ci, c_out=co, rank=rank),
                             op, pol)
+
+
+@pytest.mark.parametrize("policy", [B.FNO_PATH_MIN_RESULT, B.FNO_PATH_MIN_NET])
+@pytest.mark.parametrize("op", [B.FNO_OP_FWD, B.FNO_OP_BWD_DATA])
+def test_cp_path_matches_oracle_workload(policy, op):
+    wl = synth.WORKLOADS[6]
+    d = _desc_for(wl, policy=policy)
+    pol = "min_result" if policy == B.FNO_PATH_MIN_RESULT else "min_net"
+    _check_path(d, dict(n=wl.n, modes=wl.modes, batch=wl.batch, c_in=wl.c_in,
+                        c_out=wl.c_out, rank=wl.rank), op, pol, cp=True)
+
+
+def test_cp_path_golden():
+    """The library's CP path for the workload the golden sequences were worked
+    out for (hand-derived, tests/golden/cp_paths.json)."""
+    import json
+    with open(os.path.join(ROOT, "tests", "golden", "cp_paths.json")) as f:
+        g = json.load(f)
+    sz = g["sizes"]
+    for policy, pol in [(B.FNO_PATH_MIN_RESULT, "min_result"), (B.FNO_PATH_MIN_NET, "min_net")]:
+        d = B.make_desc((128, 128), (32, 32), sz["b"], sz["i"], sz["o"], B.FNO_PREC_FP16_TANH,
+                        B.FNO_WEIGHT_CP, (sz["r"],), policy)
+        got = B.fno_contraction_path(d, B.FNO_OP_FWD)
+        exp = g[pol]["steps"]
+        assert len(got) == len(exp)
+        for (p, q, mask), (ep, eq, eres, _) in zip(got, exp):
+            assert (p, q) == (ep, eq)
+            assert _mask_to_set(mask) == set(eres)
+        macs, peak = B.fno_contraction_path_cost(d, B.FNO_OP_FWD)
+        assert (macs, peak) == (g[pol]["macs"], g[pol]["peak"])
+
+
+def test_cp_path_matches_oracle_random():
+    rng = np.random.default_rng(19)
+    for trial in range(150):
+        nd = int(rng.integers(1, 4))
+        n = [int(rng.choice([8, 16, 32, 64])) for _ in range(nd)]
+        modes = [int(rng.integers(1, v // 2 + 1)) for v in n]
+        modes[-1] = int(rng.integers(1, n[-1] // 2 + 2))
+        rank = [int(rng.integers(1, 40))]
+        b, ci, co = (int(rng.integers(1, 40)) for _ in range(3))
+        for policy, pol in [(B.FNO_PATH_MIN_RESULT, "min_result"),
+                            (B.FNO_PATH_MIN_NET, "min_net")]:
+            d = B.make_desc(n, modes, b, ci, co, B.FNO_PREC_FP16_TANH, B.FNO_WEIGHT_CP,
+                            rank, policy)
+            for op in (B.FNO_OP_FWD, B.FNO_OP_BWD_DATA):
+                _check_path(d, dict(n=n, modes=modes, batch=b, c_in=ci, c_out=co, rank=rank),
+                            op, pol, cp=True)
+
+
+def test_cp_rank_checked():
+    d = B.make_desc((16, 16), (4, 4), 2, 3, 3, B.FNO_PREC_FP16_TANH, B.FNO_WEIGHT_CP, (0,))
+    with pytest.raises(B.FnoError):
+        B.fno_spectral_conv_workspace_size(d, B.FNO_OP_FWD)
+    d = B.make_desc((16, 16), (4, 4), 2, 3, 3, B.FNO_PREC_FP16_TANH, B.FNO_WEIGHT_DENSE)
+    with pytest.raises(B.FnoError):
+        B.fno_contraction_path(d, B.FNO_OP_FWD)
 
 
 def test_spectrum_bytes():

@@ -82,10 +82,7 @@ def _workload_inputs(wid, prec, batch=None):
         _, npdt, _ = U.prec_codes(prec)
         x = synth.make_x(wl, npdt, batch)
         gy = synth.make_gy(wl, npdt, batch)
-        if wl.weight == "tucker":
-            w = synth.make_tucker_weight(wl, npdt)
-        else:
-            w = synth.make_dense_weight(wl, npdt)
+        w = synth.make_weight(wl, npdt)
         _CACHE.clear()
         _CACHE[key] = (x, w, gy)
     return _CACHE[key]
@@ -339,6 +336,125 @@ def test_combined_bwd_tucker(prec):
     layer = U.make_layer(n, modes, Bt, ci, co, prec, tucker_rank=rank)
     wd = {"core": U.dev(core), "u_in": U.dev(u_in), "u_out": U.dev(u_out),
           "u_mode": [U.dev(u) for u in u_mode]}
+    xd, gyd = U.dev(x), U.dev(gy)
+    gx, gw = layer.bwd(xd, wd, gyd)
+    gx_sep = layer.bwd_data(xd, wd, gyd)
+    gw_sep = layer.bwd_weight(xd, gyd, wd)
+    torch.cuda.synchronize()
+    assert np.array_equal(U.host(gx), U.host(gx_sep))
+    for k in ("core", "u_in", "u_out"):
+        assert np.array_equal(U.host(gw[k]), U.host(gw_sep[k]))
+    for a, b in zip(gw["u_mode"], gw_sep["u_mode"]):
+        assert np.array_equal(U.host(a), U.host(b))
+
+
+# ---------------------------------------------------------------------------
+# CP-factorised weights (Sec. 4.6)
+# ---------------------------------------------------------------------------
+
+def _cp_check(w, x, gy, n, modes, y, gx, gw, prec, oprec, policy):
+    lam, u_in, u_out = U.cplx(w["core"]), U.cplx(w["u_in"]), U.cplx(w["u_out"])
+    u_mode = [U.cplx(u) for u in w["u_mode"]]
+    _assert_close("y", y, O.cp_fwd(x, lam, u_in, u_out, u_mode, n, modes, oprec, policy), prec)
+    _assert_close("gx", gx, O.cp_bwd_data(x, lam, u_in, u_out, u_mode, gy, n, modes, oprec,
+                                          policy), prec)
+    g_lam, g_in, g_out, g_mode = O.cp_bwd_weight(x, gy, lam, u_in, u_out, u_mode, n, modes,
+                                                 oprec)
+    gwc = U.gw_complex(gw)
+    _assert_close("g_lambda", gwc["core"], g_lam, prec)
+    _assert_close("g_u_in", gwc["u_in"], g_in, prec)
+    _assert_close("g_u_out", gwc["u_out"], g_out, prec)
+    for j in range(len(n)):
+        _assert_close(f"g_u_mode{j}", gwc["u_mode"][j], g_mode[j], prec)
+
+
+CP_EDGE = [
+    # (n, modes, B, Cin, Cout, R)
+    ((8, 8), (2, 3), 2, 3, 4, 3),
+    ((6, 10, 12), (2, 3, 4), 2, 3, 2, 5),
+    ((40,), (7,), 3, 2, 5, 4),
+    ((32, 48), (5, 9), 3, 7, 6, 1),      # rank one
+    ((64, 64), (16, 16), 4, 32, 32, 24),  # chained-transform shapes, K % 32 == 0
+]
+
+
+@pytest.mark.parametrize("policy", ["min_result", "min_net"])
+@pytest.mark.parametrize("prec", PRECS)
+@pytest.mark.parametrize("case", range(len(CP_EDGE)))
+def test_cp_edge_cases(case, prec, policy):
+    n, modes, Bt, ci, co, r = CP_EDGE[case]
+    _, npdt, oprec = U.prec_codes(prec)
+    U.say(f"cp edge {case}: n={n} modes={modes} B={Bt} C={ci}->{co} R={r} {prec} {policy}")
+    rng = np.random.default_rng(np.random.SeedSequence([3000 + case]))
+    d = len(n)
+    kd = tuple(2 * m if j < d - 1 else m for j, m in enumerate(modes))
+
+    def cpx(shape, std):
+        return (rng.standard_normal(tuple(shape) + (2,)) * std).astype(npdt)
+
+    w = {"core": cpx((r,), 0.5), "u_in": cpx((ci, r), 0.5), "u_out": cpx((co, r), 0.5),
+         "u_mode": [cpx((kd[j], r), 0.5) for j in range(d)]}
+    x = rng.standard_normal((Bt, ci) + n).astype(npdt)
+    gy = rng.standard_normal((Bt, co) + n).astype(npdt)
+    pol = 0 if policy == "min_result" else 1
+    layer = U.make_layer(n, modes, Bt, ci, co, prec, policy=pol, cp_rank=r)
+    y, gx, gw = U.run_all(layer, x, w, gy)
+    _cp_check(w, x, gy, n, modes, y, gx, gw, prec, oprec, policy)
+    if case == 0:
+        # bwd_weight recomputing both spectra (no caches) gives the same grads
+        _, _, gw2 = U.run_all(layer, x, w, gy, caches=False)
+        for k in ("core", "u_in", "u_out"):
+            assert np.array_equal(gw[k], gw2[k]), k
+
+
+@pytest.mark.parametrize("policy", ["min_result", "min_net"])
+@pytest.mark.parametrize("prec", PRECS)
+def test_workload_cp(prec, policy):
+    """CP workload at full size: y and gx of batch sample 0; lambda and factor
+    gradients from all samples."""
+    wid = 6
+    wl = synth.WORKLOADS[wid]
+    _, _, oprec = U.prec_codes(prec)
+    U.say(f"workload {wid} {wl.name} {prec} {policy}")
+    x, w, gy = _workload_inputs(wid, prec)
+    pol = 0 if policy == "min_result" else 1
+    layer = U.make_layer(wl.n, wl.modes, wl.batch, wl.c_in, wl.c_out, prec, policy=pol,
+                         cp_rank=wl.rank[0])
+    y, gx, gw = U.run_all(layer, x, w, gy)
+    lam, u_in, u_out = U.cplx(w["core"]), U.cplx(w["u_in"]), U.cplx(w["u_out"])
+    u_mode = [U.cplx(u) for u in w["u_mode"]]
+    ry0 = O.cp_fwd(x[0:1], lam, u_in, u_out, u_mode, wl.n, wl.modes, oprec, policy)
+    _assert_close("y[b=0]", y[0:1], ry0, prec)
+    rgx0 = O.cp_bwd_data(x[0:1], lam, u_in, u_out, u_mode, gy[0:1], wl.n, wl.modes, oprec,
+                         policy)
+    _assert_close("gx[b=0]", gx[0:1], rgx0, prec)
+    g_lam, g_in, g_out, g_mode = O.cp_bwd_weight(x, gy, lam, u_in, u_out, u_mode, wl.n,
+                                                 wl.modes, oprec)
+    gwc = U.gw_complex(gw)
+    _assert_close("g_lambda", gwc["core"], g_lam, prec)
+    _assert_close("g_u_in", gwc["u_in"], g_in, prec)
+    _assert_close("g_u_out", gwc["u_out"], g_out, prec)
+    for j in range(wl.ndim):
+        _assert_close(f"g_u_mode{j}", gwc["u_mode"][j], g_mode[j], prec)
+
+
+@pytest.mark.parametrize("prec", PRECS)
+def test_combined_bwd_cp(prec):
+    """fno_spectral_conv_bwd with CP weights equals the two separate calls."""
+    n, modes, Bt, ci, co, r = (32, 32), (4, 5), 2, 6, 5, 7
+    U.say(f"combined bwd cp {prec}")
+    _, npdt, oprec = U.prec_codes(prec)
+    rng = np.random.default_rng(78)
+    x = (rng.standard_normal((Bt, ci) + n)).astype(npdt)
+    gy = (rng.standard_normal((Bt, co) + n)).astype(npdt)
+    kd = (2 * modes[0], modes[1])
+    w = {"core": (rng.standard_normal((r, 2)) * 0.3).astype(npdt),
+         "u_in": (rng.standard_normal((ci, r, 2)) * 0.4).astype(npdt),
+         "u_out": (rng.standard_normal((co, r, 2)) * 0.4).astype(npdt),
+         "u_mode": [(rng.standard_normal((kd[j], r, 2)) * 0.4).astype(npdt) for j in range(2)]}
+    layer = U.make_layer(n, modes, Bt, ci, co, prec, cp_rank=r)
+    wd = {"core": U.dev(w["core"]), "u_in": U.dev(w["u_in"]), "u_out": U.dev(w["u_out"]),
+          "u_mode": [U.dev(u) for u in w["u_mode"]]}
     xd, gyd = U.dev(x), U.dev(gy)
     gx, gw = layer.bwd(xd, wd, gyd)
     gx_sep = layer.bwd_data(xd, wd, gyd)
