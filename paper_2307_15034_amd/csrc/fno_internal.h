@@ -132,6 +132,12 @@ struct PairArgs {
   float scale;
   int scale_c_axis;    // result index position of the last spatial axis for c(t), -1 none
   int Nb;              // last-axis length for c(t)
+  // Register blocking (set by launch_pair): result index blk_k, absent from
+  // A, is covered PB_NB values per thread so each A element loaded serves
+  // them all; -1 for one result per thread.  res_stride: the result's own
+  // strides.
+  int blk_k;
+  int64_t res_stride[PW_MAXIDX];
 };
 
 hipError_t launch_r2c(int elem, int nct, const R2CArgs& a, size_t lds, hipStream_t s);

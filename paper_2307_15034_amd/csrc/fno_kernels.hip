@@ -813,6 +813,65 @@ __global__ __launch_bounds__(256) void pair_kernel(PairArgs a) {
   pair_store(a, idx, cidx, sr, si);
 }
 
+// PB_NB results per thread along result index blk_k (absent from A): the
+// thread walks the contraction once, loads each A element once and the PB_NB
+// matching B elements, and keeps PB_NB sums.  Each sum runs over the
+// contracted elements in the same order as in pair_kernel, so the results
+// are the same bits.
+constexpr int PB_NB = 16;
+
+__global__ __launch_bounds__(256) void pair_blocked_kernel(PairArgs a, int64_t items) {
+  const int64_t it = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (it >= items) return;
+  const int kb = a.blk_k;
+  // decode the item over the result indices with blk_k in blocks of PB_NB
+  int64_t rem = it, ao = 0, bo = 0, oo = 0, cidx = 0, j0 = 0;
+  for (int k = a.n_out - 1; k >= 0; --k) {
+    const int64_t e = k == kb ? (a.out_ext[k] + PB_NB - 1) / PB_NB : a.out_ext[k];
+    int64_t v = rem % e;
+    rem /= e;
+    if (k == kb) {
+      v *= PB_NB;
+      j0 = v;
+    }
+    ao += v * a.a_stride_out[k];
+    bo += v * a.b_stride_out[k];
+    oo += v * a.res_stride[k];
+    if (k == a.scale_c_axis) cidx = v;
+  }
+  const int nj = (int)min((int64_t)PB_NB, a.out_ext[kb] - j0);
+  const int64_t bstep = a.b_stride_out[kb];
+  float sr[PB_NB], si[PB_NB];
+#pragma unroll
+  for (int j = 0; j < PB_NB; ++j) sr[j] = si[j] = 0.0f;
+  int64_t dig[PW_MAXIDX], cnt[PW_MAXIDX];
+  pair_start(a, 0, 1, dig, cnt, ao, bo);
+  for (int64_t r = 0; r < a.red_size; ++r) {
+    f2 x = load_elem(a.a, a.a_elem, ao);
+    if (a.conj_a) x[1] = -x[1];
+#pragma unroll
+    for (int j = 0; j < PB_NB; ++j) {
+      if (j < nj) {
+        f2 y = load_elem(a.b, a.b_elem, bo + j * bstep);
+        if (a.conj_b) y[1] = -y[1];
+        sr[j] = fmaf(x[0], y[0], sr[j]);
+        sr[j] = fmaf(-x[1], y[1], sr[j]);
+        si[j] = fmaf(x[0], y[1], si[j]);
+        si[j] = fmaf(x[1], y[0], si[j]);
+      }
+    }
+    pair_step(a, dig, cnt, ao, bo);
+  }
+  const int64_t ostep = a.res_stride[kb];
+#pragma unroll
+  for (int j = 0; j < PB_NB; ++j) {
+    if (j < nj) {
+      const int64_t ci = kb == a.scale_c_axis ? j0 + j : cidx;
+      pair_store(a, oo + j * ostep, ci, sr[j], si[j]);
+    }
+  }
+}
+
 // One work-group per result element: thread t takes the contracted elements
 // t, t + 256, ... (consecutive threads read consecutive elements of the
 // innermost contracted index); the 256 partial sums are added in a fixed
@@ -947,13 +1006,37 @@ hipError_t launch_wgrad(int elem, const WgradArgs& a, hipStream_t s) {
   return hipGetLastError();
 }
 
-hipError_t launch_pair(const PairArgs& a, hipStream_t s) {
+hipError_t launch_pair(const PairArgs& a_in, hipStream_t s) {
+  PairArgs a = a_in;
   if (a.out_size <= 0) return hipSuccess;
+  int64_t st = 1;
+  for (int k = a.n_out - 1; k >= 0; --k) {
+    a.res_stride[k] = st;
+    st *= a.out_ext[k];
+  }
+  // Register blocking: the widest result index that A (the larger operand)
+  // does not carry, if at least 4 wide.
+  a.blk_k = -1;
+  int64_t best = 3;
+  for (int k = 0; k < a.n_out; ++k)
+    if (a.a_stride_out[k] == 0 && a.out_ext[k] > best) {
+      best = a.out_ext[k];
+      a.blk_k = k;
+    }
   // Few results with long reductions (weight-gradient steps): a work-group
-  // per result.  Otherwise a thread per result.
+  // per result.  Otherwise a thread per PB_NB results or per result.
   if (a.red_size >= 2048 && a.out_size <= (int64_t)1 << 20) {
     dim3 grid((unsigned)a.out_size), block(256);
     hipLaunchKernelGGL(pair_block_kernel, grid, block, 0, s, a);
+  } else if (a.blk_k >= 0 &&
+             a.out_size / a.out_ext[a.blk_k] * ((a.out_ext[a.blk_k] + PB_NB - 1) / PB_NB) >=
+                 ((int64_t)1 << 17)) {
+    // (only with enough blocked items left to fill the chip: >= 2048 waves)
+    const int64_t items = a.out_size / a.out_ext[a.blk_k] *
+                          ((a.out_ext[a.blk_k] + PB_NB - 1) / PB_NB);
+    if ((items + 255) / 256 > 0xffffffffll) return hipErrorInvalidValue;
+    dim3 grid((unsigned)((items + 255) / 256)), block(256);
+    hipLaunchKernelGGL(pair_blocked_kernel, grid, block, 0, s, a, items);
   } else {
     dim3 grid((unsigned)((a.out_size + 255) / 256)), block(256);
     hipLaunchKernelGGL(pair_kernel, grid, block, 0, s, a);

@@ -1008,9 +1008,14 @@ struct Opnd {
   int conj;
 };
 
-fno_status run_pair(const Sizes& sz, const Opnd& A, const Opnd& Bo, const std::string& res,
+fno_status run_pair(const Sizes& sz, const Opnd& A0, const Opnd& B0, const std::string& res,
                     void* out, int out_elem, float scale, int c_axis_char, int Nb,
                     hipStream_t s) {
+  // the larger operand goes first (the kernels share its loads across a
+  // result index it does not carry); the product commutes
+  const bool swap = label_size(B0.lab, sz) > label_size(A0.lab, sz);
+  const Opnd& A = swap ? B0 : A0;
+  const Opnd& Bo = swap ? A0 : B0;
   PairArgs a{};
   a.a = A.ptr;
   a.b = Bo.ptr;
