@@ -25,6 +25,10 @@ size_t r2c_lds_bytes(int elem, int Kbp, int R) {
   return (size_t)2 * Kbp * (R + pad) * es;
 }
 
+// row tiles per wave and pass in the generic transforms' last-axis products
+constexpr int R2C_NRT = 2;
+constexpr int C2R_NRT = 2;
+
 template <typename T, int NCT>
 __global__ __launch_bounds__(256) void r2c_plane_kernel(R2CArgs a) {
   using M = MM<T>;
@@ -53,28 +57,46 @@ __global__ __launch_bounds__(256) void r2c_plane_kernel(R2CArgs a) {
 
   for (int c0 = 0; c0 < a.Na; c0 += a.R) {
     // ---- step A: rows c0 .. c0+R-1, last axis -> 2*Kbp real columns -------
+    // A wave takes NRT row tiles (rt, rt + 4, ...) at once, so each twiddle
+    // fragment it loads serves NRT products.
     const int nrt = a.R >> 4;
-    for (int rt = wave; rt < nrt; rt += 4) {
-      f4 acc[NCT];
+    for (int rt0 = wave; rt0 < nrt; rt0 += 4 * R2C_NRT) {
+      f4 acc[R2C_NRT][NCT];
+      const T* rp[R2C_NRT];
+      bool vrow[R2C_NRT];
 #pragma unroll
-      for (int ct = 0; ct < NCT; ++ct) acc[ct] = f4zero();
-      const int row = c0 + rt * 16 + r16;
-      const bool vrow = row < a.Na;
-      const T* rp = in + (int64_t)(vrow ? row : 0) * a.Nb;
+      for (int u = 0; u < R2C_NRT; ++u) {
+#pragma unroll
+        for (int ct = 0; ct < NCT; ++ct) acc[u][ct] = f4zero();
+        const int row = c0 + (rt0 + 4 * u) * 16 + r16;
+        vrow[u] = rt0 + 4 * u < nrt && row < a.Na;
+        rp[u] = in + (int64_t)(vrow[u] ? row : 0) * a.Nb;
+      }
       for (int k0 = 0; k0 < a.Nbp; k0 += KS) {
-        frag af = load_row_frag<T>(rp, k0 + g * KPL, a.Nb, vrow, a.do_tanh, a.vec);
+        frag af[R2C_NRT];
+#pragma unroll
+        for (int u = 0; u < R2C_NRT; ++u)
+          if (rt0 + 4 * u < nrt)
+            af[u] = load_row_frag<T>(rp[u], k0 + g * KPL, a.Nb, vrow[u], a.do_tanh, a.vec);
 #pragma unroll
         for (int ct = 0; ct < NCT; ++ct) {
           frag bf = M::ld(twA + (int64_t)(ct * 16 + r16) * a.Nbp + k0 + g * KPL);
-          acc[ct] = M::mma(af, bf, acc[ct]);
+#pragma unroll
+          for (int u = 0; u < R2C_NRT; ++u)
+            if (rt0 + 4 * u < nrt) acc[u][ct] = M::mma(af[u], bf, acc[u][ct]);
         }
       }
 #pragma unroll
-      for (int ct = 0; ct < NCT; ++ct) {
-        const int col = ct * 16 + r16;
-        T* dst = (col < Kbp ? ATr + col * ldA : ATi + (col - Kbp) * ldA) + rt * 16 + 4 * g;
+      for (int u = 0; u < R2C_NRT; ++u) {
+        if (rt0 + 4 * u >= nrt) continue;
 #pragma unroll
-        for (int i = 0; i < 4; ++i) dst[i] = from_f<T>(acc[ct][i] * a.scaleA);
+        for (int ct = 0; ct < NCT; ++ct) {
+          const int col = ct * 16 + r16;
+          T* dst = (col < Kbp ? ATr + col * ldA : ATi + (col - Kbp) * ldA) +
+                   (rt0 + 4 * u) * 16 + 4 * g;
+#pragma unroll
+          for (int i = 0; i < 4; ++i) dst[i] = from_f<T>(acc[u][ct][i] * a.scaleA);
+        }
       }
     }
     __syncthreads();
@@ -282,54 +304,68 @@ __global__ __launch_bounds__(256) void c2r_plane_kernel(C2RArgs a) {
     }
     __syncthreads();
     // ---- step A': y[n][m] = sum_k VL[n][k] twI[m][k] ------------------------
-    for (int rt = wave; rt < nnt; rt += 4) {
-      const int row0 = c0 + rt * 16;
+    // A wave takes C2R_NRT row tiles (rt, rt + 4, ...) per column group, so
+    // each twiddle fragment it loads serves C2R_NRT products.
+    for (int rt0 = wave; rt0 < nnt; rt0 += 4 * C2R_NRT) {
       for (int cg = 0; cg < ncg; ++cg) {
-        f4 acc[4];
+        f4 acc[C2R_NRT][4];
 #pragma unroll
-        for (int c = 0; c < 4; ++c) acc[c] = f4zero();
+        for (int u = 0; u < C2R_NRT; ++u)
+#pragma unroll
+          for (int c = 0; c < 4; ++c) acc[u][c] = f4zero();
         // D = y^T tile: row n_b (4 consecutive per lane), column n_a
         for (int k0 = 0; k0 < 2 * Kbp; k0 += KS) {
-          frag vf = M::ld(VL + (rt * 16 + r16) * ldV + k0 + g * KPL);
+          frag vf[C2R_NRT];
+#pragma unroll
+          for (int u = 0; u < C2R_NRT; ++u)
+            if (rt0 + 4 * u < nnt)
+              vf[u] = M::ld(VL + ((rt0 + 4 * u) * 16 + r16) * ldV + k0 + g * KPL);
 #pragma unroll
           for (int c = 0; c < 4; ++c) {
             const int ct = cg * 4 + c;
             frag tf = M::ld(twI + (int64_t)(ct * 16 + r16) * (2 * Kbp) + k0 + g * KPL);
-            acc[c] = M::mma(tf, vf, acc[c]);
+#pragma unroll
+            for (int u = 0; u < C2R_NRT; ++u)
+              if (rt0 + 4 * u < nnt) acc[u][c] = M::mma(tf, vf[u], acc[u][c]);
           }
         }
-        // one 16-byte store per tile: obuf[n_a][n_b .. n_b + 3]
 #pragma unroll
-        for (int c = 0; c < 4; ++c)
-          *reinterpret_cast<f4*>(obuf + r16 * 68 + c * 16 + 4 * g) = acc[c];
-        wave_lds_sync();
-        const int orow = lane >> 2;
-        const int ocol = (lane & 3) * 16;
-        const int n_a = row0 + orow;
-        const int n_b = cg * 64 + ocol;
-        float v[16];
+        for (int u = 0; u < C2R_NRT; ++u) {
+          if (rt0 + 4 * u >= nnt) continue;
+          const int row0 = c0 + (rt0 + 4 * u) * 16;
+          // one 16-byte store per tile: obuf[n_a][n_b .. n_b + 3]
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          f4 t = *reinterpret_cast<const f4*>(obuf + orow * 68 + ocol + 4 * i);
-          v[4 * i] = t[0] * a.scale;
-          v[4 * i + 1] = t[1] * a.scale;
-          v[4 * i + 2] = t[2] * a.scale;
-          v[4 * i + 3] = t[3] * a.scale;
-        }
-        wave_lds_sync();
-        if (n_a < a.Na && n_b < a.Nb) {
-          const int nval = min(16, a.Nb - n_b);
-          const int64_t off = (int64_t)n_a * a.Nb + n_b;
-          if (a.epilogue) {
-            float xv[16];
-            load16<T>(xin + off, xv, nval, a.vec);
+          for (int c = 0; c < 4; ++c)
+            *reinterpret_cast<f4*>(obuf + r16 * 68 + c * 16 + 4 * g) = acc[u][c];
+          wave_lds_sync();
+          const int orow = lane >> 2;
+          const int ocol = (lane & 3) * 16;
+          const int n_a = row0 + orow;
+          const int n_b = cg * 64 + ocol;
+          float v[16];
 #pragma unroll
-            for (int i = 0; i < 16; ++i) {
-              const float t = tanh_f32(xv[i]);
-              v[i] *= (1.0f - t * t);
+          for (int i = 0; i < 4; ++i) {
+            f4 t = *reinterpret_cast<const f4*>(obuf + orow * 68 + ocol + 4 * i);
+            v[4 * i] = t[0] * a.scale;
+            v[4 * i + 1] = t[1] * a.scale;
+            v[4 * i + 2] = t[2] * a.scale;
+            v[4 * i + 3] = t[3] * a.scale;
+          }
+          wave_lds_sync();
+          if (n_a < a.Na && n_b < a.Nb) {
+            const int nval = min(16, a.Nb - n_b);
+            const int64_t off = (int64_t)n_a * a.Nb + n_b;
+            if (a.epilogue) {
+              float xv[16];
+              load16<T>(xin + off, xv, nval, a.vec);
+#pragma unroll
+              for (int i = 0; i < 16; ++i) {
+                const float t = tanh_f32(xv[i]);
+                v[i] *= (1.0f - t * t);
+              }
             }
+            store16<T>(yout + off, v, nval, a.vec);
           }
-          store16<T>(yout + off, v, nval, a.vec);
         }
       }
     }
