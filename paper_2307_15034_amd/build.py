@@ -15,7 +15,8 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 ROOT = os.path.dirname(HERE)
 LIB = os.path.join(HERE, "libfno_spectral_conv.so")
-SOURCES = ["fno_kernels.hip", "fno_fast.hip", "fno_chain.hip", "fno_slab.hip", "fno_plan.cpp"]
+SOURCES = ["fno_kernels.hip", "fno_fast.hip", "fno_chain.hip", "fno_slab.hip", "fno_gemm.hip",
+           "fno_plan.cpp"]
 ARCH = "gfx950"
 
 

@@ -1,0 +1,469 @@
+// Pairwise contraction steps of the factorised weights (the greedy two-
+// operand order of Sec. 4.2) as batched complex GEMMs on the matrix cores.
+//
+// A step R[res] = sum_red A[..] B[..] sorts its indices into four classes:
+// batch (in A, B and R), M (in A and R only), N (in B and R only) and K (the
+// contracted ones).  Each class is flattened in mixed radix (innermost last),
+// so the step reads R[bt][m][n] = sum_k A[bt][m][k] B[bt][n][k], and every
+// operand is reached through per-class strides: any index order, no
+// transposed copies.  A work-group owns a TM x TN tile of one batch entry and
+// walks K in stages of 16 through LDS (operands converted to fp32 and
+// conjugated on the way in); each complex product is four real
+// v_mfma_f32_16x16x4_f32 (Re += ar br - ai bi, Im += ar bi + ai br), fp32
+// accumulation.  Long reductions over few results are split over work-groups
+// (split-K); the partial sums are then added in split order by a second
+// kernel, so the result does not depend on scheduling.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include <algorithm>
+#include <climits>
+#include <utility>
+#include <vector>
+
+#include "fno_device.h"
+
+namespace fno {
+
+namespace {
+
+constexpr int GM_SUB = PW_MAXIDX;  // sub-indices per class
+constexpr int GM_TK = 16;          // k per LDS stage (four MFMA k-steps)
+constexpr int GM_LS = GM_TK + 4;   // LDS row stride (floats): 16 rows of a
+                                   // fragment read start in disjoint banks
+constexpr int GM_KCHUNK = 2048;    // most contracted elements per work-group
+enum { CL_BT = 0, CL_M = 1, CL_N = 2, CL_K = 3 };
+
+struct GemmClass {
+  int n;                                     // sub-indices, innermost last
+  int32_t ext[GM_SUB];
+  int64_t sa[GM_SUB], sb[GM_SUB], sr[GM_SUB];  // element strides (0: absent)
+  int csub;                                  // last spatial axis (c(t)), -1 none
+  int64_t size;
+};
+
+struct GemmArgs {
+  const void* a;
+  const void* b;
+  void* out;
+  float* part;  // split-K partial sums [splits][Bt][M][N] complex, or null
+  int a_elem, b_elem, out_elem, conj_a, conj_b;
+  GemmClass c[4];
+  int a_kfast, b_kfast;  // staging order: lanes along k (else along m / n)
+  int tiles_m, tiles_n, splits, kchunk;
+  float scale;
+  int Nb;
+};
+
+// Offsets of flat index v of class c in A, B and R, and the c(t) factor.
+__device__ __forceinline__ void cls_decode(const GemmClass& c, uint32_t v, int Nb, int32_t& oa,
+                                           int32_t& ob, int64_t& orr, float& mult) {
+  oa = 0;
+  ob = 0;
+  orr = 0;
+  mult = 1.0f;
+#pragma unroll
+  for (int j = GM_SUB - 1; j >= 0; --j) {
+    if (j < c.n) {
+      const uint32_t e = (uint32_t)c.ext[j];
+      const uint32_t d = v % e;
+      v /= e;
+      oa += (int32_t)(d * c.sa[j]);
+      ob += (int32_t)(d * c.sb[j]);
+      orr += (int64_t)d * c.sr[j];
+      if (j == c.csub) mult = (d == 0 || 2 * (int)d == Nb) ? 1.0f : 2.0f;
+    }
+  }
+}
+
+__device__ __forceinline__ f2 load_c(const void* p, int elem, int32_t off) {
+  if (elem == ELEM_F16) {
+    const h2 v = reinterpret_cast<const h2*>(p)[off];
+    return f2{(float)v[0], (float)v[1]};
+  }
+  return reinterpret_cast<const f2*>(p)[off];
+}
+
+__device__ __forceinline__ void store_c(void* p, int elem, int64_t off, float re, float im) {
+  if (elem == ELEM_F16)
+    reinterpret_cast<h2*>(p)[off] = h2{to_h(re), to_h(im)};
+  else
+    reinterpret_cast<f2*>(p)[off] = f2{re, im};
+}
+
+// One operand tile (rows x GM_TK) of a stage into registers: NE elements
+// per thread, lanes along k (KFAST) or along the rows.
+template <int ROWS>
+struct TileLoader {
+  static constexpr int NE = ROWS * GM_TK / 256;
+  float re[NE], im[NE];
+  __device__ __forceinline__ static void slot(bool kfast, int e, int& r, int& kk) {
+    const int t = threadIdx.x;
+    if (kfast) {
+      kk = t & (GM_TK - 1);
+      r = (t >> 4) + 16 * e;
+    } else {
+      r = t % ROWS;
+      kk = t / ROWS + (256 / ROWS) * e;
+    }
+  }
+  __device__ __forceinline__ void load(const void* p, int elem, int conj, bool kfast, int32_t base,
+                                       const int32_t* roff, const int32_t* koff, int k0,
+                                       int klen) {
+#pragma unroll
+    for (int e = 0; e < NE; ++e) {
+      int r, kk;
+      slot(kfast, e, r, kk);
+      const int32_t ro = roff[r];
+      f2 v = f2{0.0f, 0.0f};
+      if (ro >= 0 && k0 + kk < klen) v = load_c(p, elem, base + ro + koff[k0 + kk]);
+      re[e] = v[0];
+      im[e] = conj ? -v[1] : v[1];
+    }
+  }
+  __device__ __forceinline__ void store(bool kfast, float* lre, float* lim) const {
+#pragma unroll
+    for (int e = 0; e < NE; ++e) {
+      int r, kk;
+      slot(kfast, e, r, kk);
+      lre[r * GM_LS + kk] = re[e];
+      lim[r * GM_LS + kk] = im[e];
+    }
+  }
+};
+
+// TM x TN result tile per work-group of four waves, WGM of them along M.
+template <int TM, int TN, int WGM>
+__global__ __launch_bounds__(256) void pair_gemm_kernel(GemmArgs g) {
+  constexpr int WGN = 4 / WGM;
+  constexpr int WM = TM / WGM, WN = TN / WGN;
+  constexpr int FM = WM / 16, FN = WN / 16;
+  static_assert(FM >= 1 && FN >= 1 && WM % 16 == 0 && WN % 16 == 0, "tile shape");
+  __shared__ __align__(16) float As[2][TM * GM_LS];
+  __shared__ __align__(16) float Bs[2][TN * GM_LS];
+  __shared__ int32_t moA[TM], noB[TN];
+  __shared__ int64_t moR[TM], noR[TN];
+  __shared__ float mmul[TM], nmul[TN];
+  __shared__ int32_t koA[GM_KCHUNK], koB[GM_KCHUNK];
+
+  const int tid = threadIdx.x;
+  uint32_t bid = blockIdx.x;
+  const int tn = (int)(bid % (uint32_t)g.tiles_n);
+  bid /= (uint32_t)g.tiles_n;
+  const int tm = (int)(bid % (uint32_t)g.tiles_m);
+  bid /= (uint32_t)g.tiles_m;
+  const uint32_t bt = bid % (uint32_t)g.c[CL_BT].size;
+  const int sp = (int)(bid / (uint32_t)g.c[CL_BT].size);
+  const int64_t M = g.c[CL_M].size, N = g.c[CL_N].size, K = g.c[CL_K].size;
+  const int64_t m0 = (int64_t)tm * TM, n0 = (int64_t)tn * TN;
+  const int64_t kb = (int64_t)sp * g.kchunk;
+  const int klen = (int)std::min<int64_t>(g.kchunk, K - kb);
+
+  int32_t baA, baB;
+  int64_t baR;
+  float bmul;
+  cls_decode(g.c[CL_BT], bt, g.Nb, baA, baB, baR, bmul);
+  for (int i = tid; i < TM; i += 256) {
+    int32_t oa = -1, ob;
+    int64_t orr = 0;
+    float mu = 1.0f;
+    if (m0 + i < M) cls_decode(g.c[CL_M], (uint32_t)(m0 + i), g.Nb, oa, ob, orr, mu);
+    moA[i] = oa;
+    moR[i] = orr;
+    mmul[i] = mu;
+  }
+  for (int i = tid; i < TN; i += 256) {
+    int32_t oa, ob = -1;
+    int64_t orr = 0;
+    float mu = 1.0f;
+    if (n0 + i < N) cls_decode(g.c[CL_N], (uint32_t)(n0 + i), g.Nb, oa, ob, orr, mu);
+    noB[i] = ob;
+    noR[i] = orr;
+    nmul[i] = mu;
+  }
+  for (int i = tid; i < klen; i += 256) {
+    int32_t oa, ob;
+    int64_t orr;
+    float mu;
+    cls_decode(g.c[CL_K], (uint32_t)(kb + i), g.Nb, oa, ob, orr, mu);
+    koA[i] = oa;
+    koB[i] = ob;
+  }
+  __syncthreads();
+
+  const int lane = tid & 63, wave = tid >> 6, r16 = lane & 15, gq = lane >> 4;
+  const int wm = wave % WGM, wn = wave / WGM;
+  f4 cr[FM][FN], ci[FM][FN];
+#pragma unroll
+  for (int i = 0; i < FM; ++i)
+#pragma unroll
+    for (int j = 0; j < FN; ++j) cr[i][j] = ci[i][j] = f4zero();
+
+  TileLoader<TM> la;
+  TileLoader<TN> lb;
+  const bool akf = g.a_kfast != 0, bkf = g.b_kfast != 0;
+  const int nst = (klen + GM_TK - 1) / GM_TK;
+  la.load(g.a, g.a_elem, g.conj_a, akf, baA, moA, koA, 0, klen);
+  lb.load(g.b, g.b_elem, g.conj_b, bkf, baB, noB, koB, 0, klen);
+  for (int st = 0; st < nst; ++st) {
+    la.store(akf, As[0], As[1]);
+    lb.store(bkf, Bs[0], Bs[1]);
+    __syncthreads();
+    if (st + 1 < nst) {  // next stage in flight during this one's products
+      la.load(g.a, g.a_elem, g.conj_a, akf, baA, moA, koA, (st + 1) * GM_TK, klen);
+      lb.load(g.b, g.b_elem, g.conj_b, bkf, baB, noB, koB, (st + 1) * GM_TK, klen);
+    }
+    // lane (r16, gq) holds k = 4 gq + s of MFMA k-step s (A and B alike)
+    f4 ar[FM], ai[FM], an[FM], br[FN], bi[FN];
+#pragma unroll
+    for (int i = 0; i < FM; ++i) {
+      const int row = wm * WM + i * 16 + r16;
+      ar[i] = *reinterpret_cast<const f4*>(&As[0][row * GM_LS + 4 * gq]);
+      ai[i] = *reinterpret_cast<const f4*>(&As[1][row * GM_LS + 4 * gq]);
+      an[i] = -ai[i];
+    }
+#pragma unroll
+    for (int j = 0; j < FN; ++j) {
+      const int col = wn * WN + j * 16 + r16;
+      br[j] = *reinterpret_cast<const f4*>(&Bs[0][col * GM_LS + 4 * gq]);
+      bi[j] = *reinterpret_cast<const f4*>(&Bs[1][col * GM_LS + 4 * gq]);
+    }
+#pragma unroll
+    for (int s = 0; s < 4; ++s)
+#pragma unroll
+      for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int j = 0; j < FN; ++j) {
+          cr[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(ar[i][s], br[j][s], cr[i][j], 0, 0, 0);
+          cr[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(an[i][s], bi[j][s], cr[i][j], 0, 0, 0);
+          ci[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(ar[i][s], bi[j][s], ci[i][j], 0, 0, 0);
+          ci[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(ai[i][s], br[j][s], ci[i][j], 0, 0, 0);
+        }
+    __syncthreads();
+  }
+
+  // D: lane holds rows 4 gq + v, column r16 of each 16 x 16 tile
+  const int64_t total = (int64_t)g.c[CL_BT].size * M * N;
+#pragma unroll
+  for (int i = 0; i < FM; ++i)
+#pragma unroll
+    for (int j = 0; j < FN; ++j)
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        const int rr = wm * WM + i * 16 + 4 * gq + v;
+        const int cc = wn * WN + j * 16 + r16;
+        if (m0 + rr >= M || n0 + cc >= N) continue;
+        if (g.splits > 1) {
+          const int64_t e = ((int64_t)bt * M + m0 + rr) * N + n0 + cc;
+          reinterpret_cast<f2*>(g.part)[(int64_t)sp * total + e] = f2{cr[i][j][v], ci[i][j][v]};
+        } else {
+          const float sc = g.scale * bmul * mmul[rr] * nmul[cc];
+          store_c(g.out, g.out_elem, baR + moR[rr] + noR[cc], cr[i][j][v] * sc, ci[i][j][v] * sc);
+        }
+      }
+}
+
+// Split-K: result = scale * sum of the partial sums.  A work-group of 16
+// waves takes 64 results (one per lane); wave w adds its contiguous run of
+// splits in order, then the 16 wave sums are added in wave order, so the
+// result does not depend on scheduling.
+constexpr int GR_WAVES = 16;
+
+__global__ __launch_bounds__(GR_WAVES * 64) void pair_gemm_reduce_kernel(GemmArgs g) {
+  __shared__ f2 red[GR_WAVES][64];
+  const int64_t M = g.c[CL_M].size, N = g.c[CL_N].size;
+  const int64_t total = (int64_t)g.c[CL_BT].size * M * N;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int64_t e = (int64_t)blockIdx.x * 64 + lane;
+  const int per = (g.splits + GR_WAVES - 1) / GR_WAVES;
+  const int s0 = wave * per, s1 = min(g.splits, s0 + per);
+  const f2* part = reinterpret_cast<const f2*>(g.part);
+  float sr = 0.0f, si = 0.0f;
+  if (e < total) {
+    int s = s0;
+    for (; s + 4 <= s1; s += 4) {  // four loads in flight, added in order
+      f2 v[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) v[u] = part[(int64_t)(s + u) * total + e];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        sr += v[u][0];
+        si += v[u][1];
+      }
+    }
+    for (; s < s1; ++s) {
+      const f2 v = part[(int64_t)s * total + e];
+      sr += v[0];
+      si += v[1];
+    }
+  }
+  red[wave][lane] = f2{sr, si};
+  __syncthreads();
+  if (wave != 0 || e >= total) return;
+  sr = 0.0f;
+  si = 0.0f;
+  for (int w = 0; w < GR_WAVES; ++w) {
+    sr += red[w][lane][0];
+    si += red[w][lane][1];
+  }
+  const int64_t n = e % N, t = e / N;
+  const int64_t m = t % M, bt = t / M;
+  int32_t oa, ob;
+  int64_t r0, r1, r2;
+  float u0, u1, u2;
+  cls_decode(g.c[CL_BT], (uint32_t)bt, g.Nb, oa, ob, r0, u0);
+  cls_decode(g.c[CL_M], (uint32_t)m, g.Nb, oa, ob, r1, u1);
+  cls_decode(g.c[CL_N], (uint32_t)n, g.Nb, oa, ob, r2, u2);
+  const float sc = g.scale * u0 * u1 * u2;
+  store_c(g.out, g.out_elem, r0 + r1 + r2, sr * sc, si * sc);
+}
+
+// Largest element offset an operand reaches through the classes.
+int64_t max_offset(const GemmArgs& g, int which) {
+  int64_t m = 0;
+  for (int c = 0; c < 4; ++c)
+    for (int j = 0; j < g.c[c].n; ++j) {
+      const int64_t s = which == 0 ? g.c[c].sa[j] : which == 1 ? g.c[c].sb[j] : g.c[c].sr[j];
+      m += (int64_t)(g.c[c].ext[j] - 1) * s;
+    }
+  return m;
+}
+
+}  // namespace
+
+// Returns hipErrorNotSupported when the step does not map onto the GEMM
+// (an index in the result only, sizes past 32-bit offsets, no room for the
+// split-K partial sums) or wastes most of a tile on it; the caller then uses
+// the generic kernels.
+hipError_t launch_pair_gemm(const PairArgs& p, hipStream_t s) {
+  GemmArgs g{};
+  g.a = p.a;
+  g.b = p.b;
+  g.out = p.out;
+  g.part = reinterpret_cast<float*>(p.part);
+  g.a_elem = p.a_elem;
+  g.b_elem = p.b_elem;
+  g.out_elem = p.out_elem;
+  g.conj_a = p.conj_a;
+  g.conj_b = p.conj_b;
+  g.scale = p.scale;
+  g.Nb = p.Nb;
+  struct Sub {
+    int64_t ext, sa, sb, sr;
+    bool c;
+  };
+  std::vector<Sub> cls[4];
+  int64_t rs = 1;
+  std::vector<int64_t> res_stride(p.n_out);
+  for (int k = p.n_out - 1; k >= 0; --k) {
+    res_stride[k] = rs;
+    rs *= p.out_ext[k];
+  }
+  for (int k = 0; k < p.n_out; ++k) {
+    const bool ina = p.a_stride_out[k] != 0, inb = p.b_stride_out[k] != 0;
+    if (!ina && !inb) return hipErrorNotSupported;
+    const int c = ina && inb ? CL_BT : ina ? CL_M : CL_N;
+    cls[c].push_back({p.out_ext[k], p.a_stride_out[k], p.b_stride_out[k], res_stride[k],
+                      k == p.scale_c_axis});
+  }
+  for (int k = 0; k < p.n_red; ++k)
+    cls[CL_K].push_back({p.red_ext[k], p.a_stride_red[k], p.b_stride_red[k], 0, false});
+  // innermost sub-index = smallest stride of the operand that streams along
+  // the class (absent indices, stride 0, go outermost)
+  auto key = [](int64_t st) { return st == 0 ? INT64_MAX : st; };
+  auto min_stride = [&](const std::vector<Sub>& v, bool a) {
+    int64_t m = INT64_MAX;
+    for (const Sub& u : v) m = std::min(m, key(a ? u.sa : u.sb));
+    return m;
+  };
+  // the smaller class goes to N (operands swap roles; the product commutes)
+  auto csize = [&](const std::vector<Sub>& v) {
+    int64_t z = 1;
+    for (const Sub& u : v) z *= u.ext;
+    return z;
+  };
+  if (csize(cls[CL_N]) > csize(cls[CL_M])) {
+    std::swap(cls[CL_M], cls[CL_N]);
+    for (auto& v : cls)
+      for (Sub& u : v) std::swap(u.sa, u.sb);
+    std::swap(g.a, g.b);
+    std::swap(g.a_elem, g.b_elem);
+    std::swap(g.conj_a, g.conj_b);
+  }
+  g.a_kfast = min_stride(cls[CL_K], true) < min_stride(cls[CL_M], true);
+  g.b_kfast = min_stride(cls[CL_K], false) < min_stride(cls[CL_N], false);
+  auto sort_by = [&](std::vector<Sub>& v, int which) {
+    std::stable_sort(v.begin(), v.end(), [&](const Sub& x, const Sub& y) {
+      const int64_t sx = which == 0 ? key(x.sa) : which == 1 ? key(x.sb) : key(x.sr);
+      const int64_t sy = which == 0 ? key(y.sa) : which == 1 ? key(y.sb) : key(y.sr);
+      return sx > sy;
+    });
+  };
+  sort_by(cls[CL_BT], 2);
+  sort_by(cls[CL_M], 0);
+  sort_by(cls[CL_N], 1);
+  sort_by(cls[CL_K], g.a_kfast || !g.b_kfast ? 0 : 1);
+  for (int c = 0; c < 4; ++c) {
+    if ((int)cls[c].size() > GM_SUB) return hipErrorNotSupported;
+    GemmClass& C = g.c[c];
+    C.n = (int)cls[c].size();
+    C.csub = -1;
+    C.size = 1;
+    for (int j = 0; j < C.n; ++j) {
+      C.ext[j] = (int32_t)cls[c][j].ext;
+      C.sa[j] = cls[c][j].sa;
+      C.sb[j] = cls[c][j].sb;
+      C.sr[j] = cls[c][j].sr;
+      if (cls[c][j].c) C.csub = j;
+      C.size *= cls[c][j].ext;
+    }
+    if (C.size >= ((int64_t)1 << 31)) return hipErrorNotSupported;
+  }
+  if (max_offset(g, 0) >= ((int64_t)1 << 31) || max_offset(g, 1) >= ((int64_t)1 << 31))
+    return hipErrorNotSupported;
+  const int64_t M = g.c[CL_M].size, N = g.c[CL_N].size, K = g.c[CL_K].size;
+  const int64_t Bt = g.c[CL_BT].size;
+  // Elementwise and outer products (K < 4) and batched dot products (tiny
+  // M x N) waste the tile: the generic kernels take those.
+  if (K < 4 || M * N < 64) return hipErrorNotSupported;
+  int cfg, TM, TN;
+  if (N <= 16) {
+    cfg = 0, TM = 128, TN = 16;
+  } else if (N <= 32) {
+    cfg = 1, TM = 128, TN = 32;
+  } else {
+    cfg = 2, TM = 64, TN = 64;
+  }
+  g.tiles_m = (int)((M + TM - 1) / TM);
+  g.tiles_n = (int)((N + TN - 1) / TN);
+  const int64_t tiles = (int64_t)g.tiles_m * g.tiles_n * Bt;
+  const int64_t nst = (K + GM_TK - 1) / GM_TK;
+  const int64_t total = Bt * M * N;
+  // split-K: at least enough splits for the per-work-group offset table,
+  // more while the tiles alone leave the chip idle (>= 4 stages a split),
+  // as many as the partial-sum area holds
+  const int64_t need = (K + GM_KCHUNK - 1) / GM_KCHUNK;
+  int64_t want = need;
+  if (tiles < 512) want = std::max(want, std::min<int64_t>(nst / 4, (1024 + tiles - 1) / tiles));
+  const int64_t cap = p.part ? (int64_t)(p.part_cap / (size_t)(total * 8)) : 0;
+  if (need > 1 && cap < need) return hipErrorNotSupported;
+  const int64_t splits = want > 1 ? std::max(need, std::min(want, cap)) : 1;
+  const int64_t kst = (nst + splits - 1) / splits;
+  g.kchunk = (int)(kst * GM_TK);
+  g.splits = (int)std::max<int64_t>(1, (K + g.kchunk - 1) / g.kchunk);
+  const int64_t blocks = tiles * g.splits;
+  if (blocks <= 0 || blocks > 0x7fffffffll) return hipErrorNotSupported;
+  dim3 grid((unsigned)blocks), block(256);
+  switch (cfg) {
+    case 0: hipLaunchKernelGGL((pair_gemm_kernel<128, 16, 4>), grid, block, 0, s, g); break;
+    case 1: hipLaunchKernelGGL((pair_gemm_kernel<128, 32, 4>), grid, block, 0, s, g); break;
+    default: hipLaunchKernelGGL((pair_gemm_kernel<64, 64, 2>), grid, block, 0, s, g); break;
+  }
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || g.splits == 1) return e;
+  dim3 rgrid((unsigned)((total + 63) / 64)), rblock(GR_WAVES * 64);
+  hipLaunchKernelGGL(pair_gemm_reduce_kernel, rgrid, rblock, 0, s, g);
+  return hipGetLastError();
+}
+
+}  // namespace fno

@@ -138,7 +138,14 @@ struct PairArgs {
   // strides.
   int blk_k;
   int64_t res_stride[PW_MAXIDX];
+  // Room for split-K partial sums of the GEMM form (null: no split-K).
+  void* part;
+  size_t part_cap;
 };
+
+// Bytes of every factorised-weight scratch area reserved for the split-K
+// partial sums of one pairwise step.
+constexpr size_t kPairPartBytes = (size_t)8 << 20;
 
 hipError_t launch_r2c(int elem, int nct, const R2CArgs& a, size_t lds, hipStream_t s);
 hipError_t launch_c2r(int elem, int nct, const C2RArgs& a, size_t lds, hipStream_t s);
@@ -146,6 +153,7 @@ hipError_t launch_axis(int elem, const AxisArgs& a, size_t lds, hipStream_t s);
 hipError_t launch_contract(int elem, const ContractArgs& a, hipStream_t s);
 hipError_t launch_wgrad(int elem, const WgradArgs& a, hipStream_t s);
 hipError_t launch_pair(const PairArgs& a, hipStream_t s);
+hipError_t launch_pair_gemm(const PairArgs& a, hipStream_t s);
 hipError_t launch_scale_complex(float* p, int64_t n, float s, hipStream_t st);
 
 // Persistent fp16 fast paths (planes up to 128 x 256); hipErrorNotSupported

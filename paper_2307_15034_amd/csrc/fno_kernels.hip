@@ -728,12 +728,26 @@ __device__ __forceinline__ f2 load_elem(const void* p, int elem, int64_t off) {
 }
 
 // Offsets of result element idx in A and B, and its last-spatial-axis slot.
+// (32-bit division while the result has fewer than 2^32 elements: a 64-bit
+// divide costs several times more and runs once per index per element)
 __device__ __forceinline__ void pair_decode(const PairArgs& a, int64_t idx, int64_t& aoff,
                                             int64_t& boff, int64_t& cidx) {
-  int64_t rem = idx;
   aoff = 0;
   boff = 0;
   cidx = 0;
+  if (a.out_size <= 0xffffffffll) {
+    uint32_t rem = (uint32_t)idx;
+    for (int k = a.n_out - 1; k >= 0; --k) {
+      const uint32_t e = (uint32_t)a.out_ext[k];
+      const uint32_t v = rem % e;
+      rem /= e;
+      aoff += (int64_t)v * a.a_stride_out[k];
+      boff += (int64_t)v * a.b_stride_out[k];
+      if (k == a.scale_c_axis) cidx = v;
+    }
+    return;
+  }
+  int64_t rem = idx;
   for (int k = a.n_out - 1; k >= 0; --k) {
     const int64_t e = a.out_ext[k];
     const int64_t v = rem % e;
@@ -861,9 +875,12 @@ __global__ __launch_bounds__(256) void pair_blocked_kernel(PairArgs a, int64_t i
   if (it >= items) return;
   const int kb = a.blk_k;
   // decode the item over the result indices with blk_k in blocks of PB_NB
-  int64_t rem = it, ao = 0, bo = 0, oo = 0, cidx = 0, j0 = 0;
+  // (items < 2^32: launch_pair checks; 32-bit division as in pair_decode)
+  uint32_t rem = (uint32_t)it;
+  int64_t ao = 0, bo = 0, oo = 0, cidx = 0, j0 = 0;
   for (int k = a.n_out - 1; k >= 0; --k) {
-    const int64_t e = k == kb ? (a.out_ext[k] + PB_NB - 1) / PB_NB : a.out_ext[k];
+    const uint32_t e =
+        (uint32_t)(k == kb ? (a.out_ext[k] + PB_NB - 1) / PB_NB : a.out_ext[k]);
     int64_t v = rem % e;
     rem /= e;
     if (k == kb) {
@@ -1045,6 +1062,10 @@ hipError_t launch_wgrad(int elem, const WgradArgs& a, hipStream_t s) {
 hipError_t launch_pair(const PairArgs& a_in, hipStream_t s) {
   PairArgs a = a_in;
   if (a.out_size <= 0) return hipSuccess;
+  {
+    const hipError_t e = launch_pair_gemm(a, s);
+    if (e != hipErrorNotSupported) return e;
+  }
   int64_t st = 1;
   for (int k = a.n_out - 1; k >= 0; --k) {
     a.res_stride[k] = st;
@@ -1070,7 +1091,7 @@ hipError_t launch_pair(const PairArgs& a_in, hipStream_t s) {
     // (only with enough blocked items left to fill the chip: >= 2048 waves)
     const int64_t items = a.out_size / a.out_ext[a.blk_k] *
                           ((a.out_ext[a.blk_k] + PB_NB - 1) / PB_NB);
-    if ((items + 255) / 256 > 0xffffffffll) return hipErrorInvalidValue;
+    if (items > 0xffffffffll) return hipErrorInvalidValue;
     dim3 grid((unsigned)((items + 255) / 256)), block(256);
     hipLaunchKernelGGL(pair_blocked_kernel, grid, block, 0, s, a, items);
   } else {

@@ -698,7 +698,7 @@ struct TuckerWs {
 // output spectrum).
 size_t tucker_path_bytes(const fno_conv_desc* d, const std::vector<PStep>& path) {
   Sizes sz = weight_sizes(d);
-  size_t t = 0;
+  size_t t = kPairPartBytes;  // split-K partial sums
   for (size_t s = 0; s + 1 < path.size(); ++s)
     t += (size_t)round_up(label_size(path[s].res, sz) * 8, 256);
   return t;
@@ -1010,7 +1010,7 @@ struct Opnd {
 
 fno_status run_pair(const Sizes& sz, const Opnd& A0, const Opnd& B0, const std::string& res,
                     void* out, int out_elem, float scale, int c_axis_char, int Nb,
-                    hipStream_t s) {
+                    hipStream_t s, void* part = nullptr) {
   // the larger operand goes first (the kernels share its loads across a
   // result index it does not carry); the product commutes
   const bool swap = label_size(B0.lab, sz) > label_size(A0.lab, sz);
@@ -1062,6 +1062,8 @@ fno_status run_pair(const Sizes& sz, const Opnd& A0, const Opnd& B0, const std::
   }
   a.scale = scale;
   a.Nb = Nb;
+  a.part = part;
+  a.part_cap = part ? kPairPartBytes : 0;
   FNO_HIP(timed("tucker_pair", s, [&] { return launch_pair(a, s); }));
   return FNO_OK;
 }
@@ -1082,7 +1084,9 @@ fno_status run_tucker_path(const fno_conv_desc* d, const Plan* pl, bool adjoint,
   ops.push_back({w->u_in, labs[2], g.elem, cj});
   ops.push_back({w->u_out, labs[3], g.elem, cj});
   for (int j = 0; j < d->ndim; ++j) ops.push_back({w->u_mode[j], labs[4 + j], g.elem, cj});
-  size_t off = 0;
+  // split-K partial sums first, then one fp32 buffer per intermediate
+  void* part = scratch;
+  size_t off = kPairPartBytes;
   const char clast = kSpatial[d->ndim - 1];
   for (size_t st = 0; st < path.size(); ++st) {
     const PStep& ps = path[st];
@@ -1098,7 +1102,7 @@ fno_status run_tucker_path(const fno_conv_desc* d, const Plan* pl, bool adjoint,
       oelem = ELEM_F32;
     }
     fno_status r = run_pair(sz, ops[ps.p], ops[ps.q], ps.res, dst, oelem, 1.0f,
-                            last ? clast : 0, g.Nb, s);
+                            last ? clast : 0, g.Nb, s, part);
     if (r != FNO_OK) return r;
     std::vector<Opnd> next;
     for (int k = 0; k < (int)ops.size(); ++k)
@@ -1122,7 +1126,7 @@ fno_status run_tucker_wgrad(const fno_conv_desc* d, const Plan* pl, const void* 
                       void* out, int out_elem, float scale, int c_axis_char, int Nb,
                       hipStream_t st) -> fno_status {
     if (dry) return FNO_OK;
-    return fno::run_pair(sz_, A, Bo, res, out, out_elem, scale, c_axis_char, Nb, st);
+    return fno::run_pair(sz_, A, Bo, res, out, out_elem, scale, c_axis_char, Nb, st, scratch);
   };
   const Geo& g = pl->g;
   const int nd = d->ndim;
@@ -1134,7 +1138,7 @@ fno_status run_tucker_wgrad(const fno_conv_desc* d, const Plan* pl, const void* 
   }
   const char clast = kSpatial[nd - 1];
   const float sqN = (float)std::sqrt((double)g.N);
-  size_t off = 0;
+  size_t off = kPairPartBytes;  // split-K partial sums at the start
   auto buf = [&](const std::string& lab) {
     void* p = scratch + off;
     off += (size_t)round_up(label_size(lab, sz) * 8, 256);
@@ -1261,7 +1265,7 @@ fno_status run_cp_wgrad(const fno_conv_desc* d, const Plan* pl, const void* xh, 
   auto pair = [&](const Sizes& sz_, const Opnd& A, const Opnd& Bo, const std::string& res,
                   void* out, float scale, int c_axis_char) -> fno_status {
     if (dry) return FNO_OK;
-    return run_pair(sz_, A, Bo, res, out, ELEM_F32, scale, c_axis_char, pl->g.Nb, s);
+    return run_pair(sz_, A, Bo, res, out, ELEM_F32, scale, c_axis_char, pl->g.Nb, s, scratch);
   };
   const Geo& g = pl->g;
   const int nd = d->ndim;
@@ -1270,7 +1274,7 @@ fno_status run_cp_wgrad(const fno_conv_desc* d, const Plan* pl, const void* xh, 
   for (int j = 0; j < nd; ++j) sp += kSpatial[j];
   const char clast = kSpatial[nd - 1];
   const float sqN = (float)std::sqrt((double)g.N);
-  size_t off = 0;
+  size_t off = kPairPartBytes;  // split-K partial sums at the start
   auto buf = [&](const std::string& lab) {
     void* p = scratch + off;
     off += (size_t)round_up(label_size(lab, sz) * 8, 256);
