@@ -60,6 +60,11 @@ struct MM<float> {
 
 __device__ __forceinline__ f4 f4zero() { return f4{0.0f, 0.0f, 0.0f, 0.0f}; }
 
+// n / d for a 32-bit n, with (m, s) from div_magic(d).
+__device__ __forceinline__ uint32_t fast_div(uint32_t n, uint32_t m, uint32_t s) {
+  return (uint32_t)(((uint64_t)__umulhi(n, m) + n) >> s);
+}
+
 // tanh in fp32 without branches (lanes of one wave see mixed magnitudes, and
 // a branchy tanh runs both paths): for |x| < 1/16 the odd series
 // x (1 - x^2/3 + 2 x^4/15) (truncation < 3e-9 relative there), otherwise

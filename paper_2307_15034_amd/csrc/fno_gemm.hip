@@ -37,6 +37,7 @@ enum { CL_BT = 0, CL_M = 1, CL_N = 2, CL_K = 3 };
 struct GemmClass {
   int n;                                     // sub-indices, innermost last
   int32_t ext[GM_SUB];
+  uint32_t mag[GM_SUB], shr[GM_SUB];           // division by ext (div_magic)
   int64_t sa[GM_SUB], sb[GM_SUB], sr[GM_SUB];  // element strides (0: absent)
   int csub;                                  // last spatial axis (c(t)), -1 none
   int64_t size;
@@ -65,9 +66,9 @@ __device__ __forceinline__ void cls_decode(const GemmClass& c, uint32_t v, int N
 #pragma unroll
   for (int j = GM_SUB - 1; j >= 0; --j) {
     if (j < c.n) {
-      const uint32_t e = (uint32_t)c.ext[j];
-      const uint32_t d = v % e;
-      v /= e;
+      const uint32_t q = fast_div(v, c.mag[j], c.shr[j]);
+      const uint32_t d = v - q * (uint32_t)c.ext[j];
+      v = q;
       oa += (int32_t)(d * c.sa[j]);
       ob += (int32_t)(d * c.sb[j]);
       orr += (int64_t)d * c.sr[j];
@@ -263,9 +264,9 @@ __global__ __launch_bounds__(256) void pair_gemm_kernel(GemmArgs g) {
       }
 }
 
-// Split-K: result = scale * sum of the partial sums.  A work-group of 16
-// waves takes 64 results (one per lane); wave w adds its contiguous run of
-// splits in order, then the 16 wave sums are added in wave order, so the
+// Split-K: result = scale * sum of the partial sums.  A work-group of up to
+// GR_WAVES waves takes 64 results (one per lane); wave w adds its contiguous
+// run of splits in order, then the wave sums are added in wave order, so the
 // result does not depend on scheduling.
 constexpr int GR_WAVES = 16;
 
@@ -274,8 +275,9 @@ __global__ __launch_bounds__(GR_WAVES * 64) void pair_gemm_reduce_kernel(GemmArg
   const int64_t M = g.c[CL_M].size, N = g.c[CL_N].size;
   const int64_t total = (int64_t)g.c[CL_BT].size * M * N;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int nw = blockDim.x >> 6;
   const int64_t e = (int64_t)blockIdx.x * 64 + lane;
-  const int per = (g.splits + GR_WAVES - 1) / GR_WAVES;
+  const int per = (g.splits + nw - 1) / nw;
   const int s0 = wave * per, s1 = min(g.splits, s0 + per);
   const f2* part = reinterpret_cast<const f2*>(g.part);
   float sr = 0.0f, si = 0.0f;
@@ -302,7 +304,7 @@ __global__ __launch_bounds__(GR_WAVES * 64) void pair_gemm_reduce_kernel(GemmArg
   if (wave != 0 || e >= total) return;
   sr = 0.0f;
   si = 0.0f;
-  for (int w = 0; w < GR_WAVES; ++w) {
+  for (int w = 0; w < nw; ++w) {
     sr += red[w][lane][0];
     si += red[w][lane][1];
   }
@@ -411,6 +413,7 @@ hipError_t launch_pair_gemm(const PairArgs& p, hipStream_t s) {
     C.size = 1;
     for (int j = 0; j < C.n; ++j) {
       C.ext[j] = (int32_t)cls[c][j].ext;
+      div_magic((uint32_t)cls[c][j].ext, &C.mag[j], &C.shr[j]);
       C.sa[j] = cls[c][j].sa;
       C.sb[j] = cls[c][j].sb;
       C.sr[j] = cls[c][j].sr;
@@ -423,9 +426,9 @@ hipError_t launch_pair_gemm(const PairArgs& p, hipStream_t s) {
     return hipErrorNotSupported;
   const int64_t M = g.c[CL_M].size, N = g.c[CL_N].size, K = g.c[CL_K].size;
   const int64_t Bt = g.c[CL_BT].size;
-  // Elementwise and outer products (K < 4) and batched dot products (tiny
-  // M x N) waste the tile: the generic kernels take those.
-  if (K < 4 || M * N < 64) return hipErrorNotSupported;
+  // Elementwise and outer products (K < 4) and large batches of tiny dot
+  // products waste the tile: the generic kernels take those.
+  if (K < 4 || (M * N < 16 && Bt * M * N > 4096)) return hipErrorNotSupported;
   int cfg, TM, TN;
   if (N <= 16) {
     cfg = 0, TM = 128, TN = 16;
@@ -461,7 +464,7 @@ hipError_t launch_pair_gemm(const PairArgs& p, hipStream_t s) {
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || g.splits == 1) return e;
-  dim3 rgrid((unsigned)((total + 63) / 64)), rblock(GR_WAVES * 64);
+  dim3 rgrid((unsigned)((total + 63) / 64)), rblock(64 * std::min(GR_WAVES, g.splits));
   hipLaunchKernelGGL(pair_gemm_reduce_kernel, rgrid, rblock, 0, s, g);
   return hipGetLastError();
 }

@@ -141,7 +141,22 @@ struct PairArgs {
   // Room for split-K partial sums of the GEMM form (null: no split-K).
   void* part;
   size_t part_cap;
+  // Division by out_ext[k] (and by the blocked index's block count) as a
+  // multiply-high and shift (set by launch_pair; see div_magic).
+  uint32_t out_mag[PW_MAXIDX], out_shr[PW_MAXIDX];
+  uint32_t blk_mag, blk_shr;
 };
+
+// Division by an invariant integer (Granlund and Montgomery, "Division by
+// invariant integers using multiplication", 1994): for 1 <= d < 2^32 with
+// s = ceil(log2 d) and m = floor(2^32 (2^s - d) / d) + 1, every 32-bit n has
+// n / d = (n + mulhi(n, m)) >> s, the sum taken in 64 bits.
+inline void div_magic(uint32_t d, uint32_t* m, uint32_t* s) {
+  uint32_t l = 0;
+  while (l < 32 && ((uint64_t)1 << l) < d) ++l;
+  *s = l;
+  *m = (uint32_t)((((uint64_t)1 << 32) * (((uint64_t)1 << l) - d)) / d + 1);
+}
 
 // Bytes of every factorised-weight scratch area reserved for the split-K
 // partial sums of one pairwise step.

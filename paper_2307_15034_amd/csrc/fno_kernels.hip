@@ -728,8 +728,9 @@ __device__ __forceinline__ f2 load_elem(const void* p, int elem, int64_t off) {
 }
 
 // Offsets of result element idx in A and B, and its last-spatial-axis slot.
-// (32-bit division while the result has fewer than 2^32 elements: a 64-bit
-// divide costs several times more and runs once per index per element)
+// (while the result has fewer than 2^32 elements, 32-bit division by
+// multiply-high: a true divide costs tens of instructions and runs once per
+// index per element)
 __device__ __forceinline__ void pair_decode(const PairArgs& a, int64_t idx, int64_t& aoff,
                                             int64_t& boff, int64_t& cidx) {
   aoff = 0;
@@ -738,9 +739,9 @@ __device__ __forceinline__ void pair_decode(const PairArgs& a, int64_t idx, int6
   if (a.out_size <= 0xffffffffll) {
     uint32_t rem = (uint32_t)idx;
     for (int k = a.n_out - 1; k >= 0; --k) {
-      const uint32_t e = (uint32_t)a.out_ext[k];
-      const uint32_t v = rem % e;
-      rem /= e;
+      const uint32_t q = fast_div(rem, a.out_mag[k], a.out_shr[k]);
+      const uint32_t v = rem - q * (uint32_t)a.out_ext[k];
+      rem = q;
       aoff += (int64_t)v * a.a_stride_out[k];
       boff += (int64_t)v * a.b_stride_out[k];
       if (k == a.scale_c_axis) cidx = v;
@@ -863,6 +864,33 @@ __global__ __launch_bounds__(256) void pair_kernel(PairArgs a) {
   pair_store(a, idx, cidx, sr, si);
 }
 
+// Products without a contracted index (elementwise and outer products):
+// PE_NV consecutive results along the innermost result index per thread,
+// decoded once; each is the same single product as in pair_kernel.
+constexpr int PE_NV = 4;
+
+__global__ __launch_bounds__(256) void pair_ew_kernel(PairArgs a, int64_t items) {
+  const int64_t it = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (it >= items) return;
+  const int64_t idx = it * PE_NV;
+  int64_t ao, bo, cidx;
+  pair_decode(a, idx, ao, bo, cidx);
+  const int kin = a.n_out - 1;
+  const int64_t sa = a.a_stride_out[kin], sb = a.b_stride_out[kin];
+  f2 x[PE_NV], y[PE_NV];
+#pragma unroll
+  for (int j = 0; j < PE_NV; ++j) {
+    x[j] = load_elem(a.a, a.a_elem, ao + j * sa);
+    y[j] = load_elem(a.b, a.b_elem, bo + j * sb);
+  }
+#pragma unroll
+  for (int j = 0; j < PE_NV; ++j) {
+    float sr = 0.0f, si = 0.0f;
+    pair_fma(a, x[j], y[j], sr, si);
+    pair_store(a, idx + j, kin == a.scale_c_axis ? cidx + j : cidx, sr, si);
+  }
+}
+
 // PB_NB results per thread along result index blk_k (absent from A): the
 // thread walks the contraction once, loads each A element once and the PB_NB
 // matching B elements, and keeps PB_NB sums.  Each sum runs over the
@@ -879,10 +907,12 @@ __global__ __launch_bounds__(256) void pair_blocked_kernel(PairArgs a, int64_t i
   uint32_t rem = (uint32_t)it;
   int64_t ao = 0, bo = 0, oo = 0, cidx = 0, j0 = 0;
   for (int k = a.n_out - 1; k >= 0; --k) {
+    const bool blk = k == kb;
     const uint32_t e =
-        (uint32_t)(k == kb ? (a.out_ext[k] + PB_NB - 1) / PB_NB : a.out_ext[k]);
-    int64_t v = rem % e;
-    rem /= e;
+        (uint32_t)(blk ? (a.out_ext[k] + PB_NB - 1) / PB_NB : a.out_ext[k]);
+    const uint32_t q = fast_div(rem, blk ? a.blk_mag : a.out_mag[k], blk ? a.blk_shr : a.out_shr[k]);
+    int64_t v = rem - q * e;
+    rem = q;
     if (k == kb) {
       v *= PB_NB;
       j0 = v;
@@ -1070,6 +1100,8 @@ hipError_t launch_pair(const PairArgs& a_in, hipStream_t s) {
   for (int k = a.n_out - 1; k >= 0; --k) {
     a.res_stride[k] = st;
     st *= a.out_ext[k];
+    div_magic((uint32_t)std::min<int64_t>(a.out_ext[k], 0xffffffffll), &a.out_mag[k],
+              &a.out_shr[k]);
   }
   // Register blocking: the widest result index that A (the larger operand)
   // does not carry, if at least 4 wide.
@@ -1080,9 +1112,16 @@ hipError_t launch_pair(const PairArgs& a_in, hipStream_t s) {
       best = a.out_ext[k];
       a.blk_k = k;
     }
+  if (a.blk_k >= 0)
+    div_magic((uint32_t)((a.out_ext[a.blk_k] + PB_NB - 1) / PB_NB), &a.blk_mag, &a.blk_shr);
   // Few results with long reductions (weight-gradient steps): a work-group
   // per result.  Otherwise a thread per PB_NB results or per result.
-  if (a.red_size >= 2048 && a.out_size <= (int64_t)1 << 20) {
+  if (a.red_size == 1 && a.n_out > 0 && a.out_ext[a.n_out - 1] % PE_NV == 0 &&
+      a.out_size / PE_NV <= 0xffffffffll * 256) {
+    const int64_t items = a.out_size / PE_NV;
+    dim3 grid((unsigned)((items + 255) / 256)), block(256);
+    hipLaunchKernelGGL(pair_ew_kernel, grid, block, 0, s, a, items);
+  } else if (a.red_size >= 2048 && a.out_size <= (int64_t)1 << 20) {
     dim3 grid((unsigned)a.out_size), block(256);
     hipLaunchKernelGGL(pair_block_kernel, grid, block, 0, s, a);
   } else if (a.blk_k >= 0 &&
