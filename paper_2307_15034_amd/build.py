@@ -16,7 +16,7 @@ CSRC = os.path.join(HERE, "csrc")
 ROOT = os.path.dirname(HERE)
 LIB = os.path.join(HERE, "libfno_spectral_conv.so")
 SOURCES = ["fno_kernels.hip", "fno_fast.hip", "fno_chain.hip", "fno_slab.hip", "fno_gemm.hip",
-           "fno_plan.cpp"]
+           "fno_wide.hip", "fno_plan.cpp"]
 ARCH = "gfx950"
 
 

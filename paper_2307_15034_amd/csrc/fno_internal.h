@@ -36,6 +36,7 @@ struct R2CArgs {
   const void* sBc;  //   or 32 j + 16 + 4 q + e - 4 (e >= 4)
   int NaC;          // Na padded to 32
   const void* lut;  // fp16 tanh of every non-negative fp16 code (32768 entries)
+  int lut_sat;      // first code from which tanh stays at its +inf value
 };
 
 // Inverse of the above: spectrum [planes][Ka][Kb] -> y [planes][Na][Nb],
@@ -64,6 +65,7 @@ struct C2RArgs {
   const void* cIc;  // [Nap][Kap] like cI, sI with column 32 ks + 8 q + e holding
   const void* sIc;  //   t = 32 ks + 4 q + e (e < 4) or 32 ks + 16 + 4 q + e - 4
   const void* lut;  // fp16 1 - tanh^2 of every non-negative fp16 code (32768 entries)
+  int lut_sat;      // first code from which 1 - tanh^2 stays at its +inf value
 };
 
 // Complex DFT along a middle axis: in [outer][Lin][inner] -> out
@@ -169,6 +171,10 @@ hipError_t launch_contract(int elem, const ContractArgs& a, hipStream_t s);
 hipError_t launch_wgrad(int elem, const WgradArgs& a, hipStream_t s);
 hipError_t launch_pair(const PairArgs& a, hipStream_t s);
 hipError_t launch_pair_gemm(const PairArgs& a, hipStream_t s);
+size_t r2c_wide_lds_bytes(int nct, bool tanh, int lut_sat);
+size_t c2r_wide_lds_bytes(int nct, int Kap, bool epi, int lut_sat);
+hipError_t launch_r2c_wide(const R2CArgs& a, int nct, int grid, size_t lds, hipStream_t s);
+hipError_t launch_c2r_wide(const C2RArgs& a, int nct, int grid, size_t lds, hipStream_t s);
 hipError_t launch_scale_complex(float* p, int64_t n, float s, hipStream_t st);
 
 // Persistent fp16 fast paths (planes up to 128 x 256); hipErrorNotSupported

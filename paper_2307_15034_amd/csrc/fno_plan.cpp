@@ -317,6 +317,7 @@ struct DevTables {
   const void *zeros, *twA, *cB, *sB, *cI, *sI, *twI;
   const void *twAc, *cBc, *sBc, *twIc, *cIc, *sIc;
   const void *lutTanh, *lutSech2;
+  int tanhSat = 0, sech2Sat = 0;  // first codes of the saturated tails (fp16 plans)
   const void *eFr, *eFi, *eIr, *eIi;
 };
 
@@ -587,6 +588,20 @@ fno_status build_tables(const fno_conv_desc* d, Plan* pl) {
   if (pl->g.elem == ELEM_F16) {
     fill_tables<_Float16>(d, pl->g, b16, off);
     bytes = b16.size() * 2;
+    // the tanh and sech^2 tables are constant from some code up to +inf
+    // (0x7c00): the wide-plane kernels keep only the codes below in LDS
+    auto sat_of = [&](size_t o) {
+      uint16_t top, v;
+      std::memcpy(&top, &b16[o + 0x7c00], 2);
+      int c = 0x7c00;
+      for (; c > 0; --c) {
+        std::memcpy(&v, &b16[o + c - 1], 2);
+        if (v != top) break;
+      }
+      return c;
+    };
+    pl->t.tanhSat = sat_of(off[13]);
+    pl->t.sech2Sat = sat_of(off[14]);
   } else {
     fill_tables<float>(d, pl->g, b32, off);
     bytes = b32.size() * 4;
@@ -876,6 +891,19 @@ fno_status run_r2c(const Plan* pl, const void* in, void* spec, void* inter, int6
       else if (e != hipErrorNotSupported) return hip_fail(e, do_tanh ? "r2c_plane_tanh" : "r2c_plane");
     }
   }
+  if (!done && g.elem == ELEM_F16 && g.Nb % 128 == 0 && g.Na % 256 == 0 && g.Nbp == g.Nb &&
+      (g.nct == 4 || g.nct == 8) && g.Kap16 <= 128 && 128 % g.Kap16 == 0 &&
+      g.Na * (int64_t)g.Nb * 2 < ((int64_t)1 << 30)) {
+    // large planes: persistent eight-wave work-groups, one per compute unit
+    a.lut_sat = pl->t.tanhSat;
+    const size_t lds = r2c_wide_lds_bytes(g.nct, do_tanh != 0, a.lut_sat);
+    const int grid = (int)std::min<int64_t>(a.planes, (int64_t)pl->num_cu);
+    hipError_t e = timed(do_tanh ? "r2c_plane_tanh" : "r2c_plane", s, [&] {
+      return launch_r2c_wide(a, g.nct, grid, lds, s);
+    });
+    if (e == hipSuccess) done = true;
+    else if (e != hipErrorNotSupported) return hip_fail(e, do_tanh ? "r2c_plane_tanh" : "r2c_plane");
+  }
   if (!done) FNO_HIP(timed(do_tanh ? "r2c_plane_tanh" : "r2c_plane", s, [&] { return launch_r2c(g.elem, g.nct, a, r2c_lds_bytes(g.elem, g.Kbp, g.R_f), s); }));
   if (g.nd == 3) {
     AxisArgs x{};
@@ -894,6 +922,11 @@ fno_status run_r2c(const Plan* pl, const void* in, void* spec, void* inter, int6
   }
   return FNO_OK;
 }
+
+// The wide-plane inverse kernel writes 32-byte row pieces per lane (partial
+// cache lines); the generic inverse, which writes whole lines through an LDS
+// transpose, is faster on every measured shape, so the wide one stays off.
+constexpr bool kWideInverse = false;
 
 // Inverse: spectrum [B][C][K...] -> planes, out = scale * sum Re(Z e^{+i theta}).
 fno_status run_c2r(const Plan* pl, const void* spec, void* out, void* inter, int64_t C,
@@ -969,6 +1002,16 @@ fno_status run_c2r(const Plan* pl, const void* spec, void* out, void* inter, int
       if (e == hipSuccess) return FNO_OK;
       if (e != hipErrorNotSupported) return hip_fail(e, kname);
     }
+  }
+  if (kWideInverse && g.elem == ELEM_F16 && g.Nb % 128 == 0 && g.Na % 256 == 0 &&
+      (g.nct == 4 || g.nct == 8) && g.Kap <= 128 && g.Na * (int64_t)g.Nb * 2 < ((int64_t)1 << 30)) {
+    // large planes: persistent eight-wave work-groups, one per compute unit
+    a.lut_sat = pl->t.sech2Sat;
+    const size_t lds = c2r_wide_lds_bytes(g.nct, g.Kap, x_epi != nullptr, a.lut_sat);
+    const int grid = (int)std::min<int64_t>(a.planes, (int64_t)pl->num_cu);
+    hipError_t e = timed(kname, s, [&] { return launch_c2r_wide(a, g.nct, grid, lds, s); });
+    if (e == hipSuccess) return FNO_OK;
+    if (e != hipErrorNotSupported) return hip_fail(e, kname);
   }
   FNO_HIP(timed(kname, s, [&] { return launch_c2r(g.elem, g.nct, a, c2r_lds_bytes(g.elem, g.Kbp, g.Kap, g.R_i), s); }));
   return FNO_OK;

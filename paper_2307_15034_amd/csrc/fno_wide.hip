@@ -1,0 +1,622 @@
+// Truncated transforms of large fp16 planes: Na a multiple of 256, Nb a
+// multiple of 128, 2*Kbp in {64, 128} real last-axis columns, up to 128
+// retained leading-axis modes (the 256^2 and 1024^2 workloads).  Same
+// arithmetic as the generic plane kernels (DFT-by-MFMA with the twiddle
+// tables of the plan, v_mfma_f32_16x16x32_f16, fp32 accumulation), laid out
+// for bandwidth:
+//   - persistent work-groups of eight waves walk (plane, 256-row chunk)
+//     items; each wave owns two 16-row tiles, so each twiddle fragment it
+//     loads serves two products;
+//   - the next k-step's (forward) or the next column tiles' (inverse) global
+//     data is in flight while the current one is multiplied (register double
+//     buffering, loads issued unconditionally so the waits stay exact); rows
+//     are read with buffer loads, rows past the plane reading zero;
+//   - tanh (forward pre-activation) and sech^2 (backward epilogue) come from
+//     a table in LDS of the fp16 codes up to the code where the function
+//     saturates, plus one NaN entry (three packed 16-bit operations pick the
+//     entry), instead of fp32 arithmetic per element.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "fno_device.h"
+
+namespace fno {
+
+namespace {
+
+constexpr int WD_WAVES = 8;
+constexpr int WD_R = 256;   // rows per chunk: 8 waves x 2 tiles x 16
+constexpr int WD_PAD = 8;   // LDS row padding in halves
+constexpr int WD_BIG = 0x40000000;  // buffer offset past every plane
+constexpr int WD_NT = 2;    // cache policy of the inverse's stores: streaming
+constexpr int WD_XD = 8;    // column tiles of x in flight (inverse epilogue)
+constexpr int WD_AD = 4;    // k-steps of row data in flight (forward)
+
+typedef unsigned short us2 __attribute__((ext_vector_type(2)));
+
+__device__ __forceinline__ h8 w_as_h8(const u32x4& v) {
+  h8 r;
+  __builtin_memcpy(&r, &v, 16);
+  return r;
+}
+
+// f(|x|) of the two fp16 values packed in w, from the LDS table tab:
+// tab[0..sat] holds f of the non-negative codes (every code from sat up to
+// +inf has the value tab[sat]) and tab[sat + 1] is NaN.  ODD: f odd, the
+// sign of x is restored.
+template <bool ODD>
+__device__ __forceinline__ uint32_t lut2(const _Float16* tab, uint32_t w, us2 sat) {
+  const uint32_t aw = w & 0x7fff7fffu;
+  us2 ax;
+  __builtin_memcpy(&ax, &aw, 4);
+  const us2 nan =
+      __builtin_elementwise_min(__builtin_elementwise_sub_sat(ax, (us2){0x7c00, 0x7c00}), (us2){1, 1});
+  const us2 idx = __builtin_elementwise_min(ax, sat) + nan;
+  h2 r;
+  r[0] = tab[idx[0]];
+  r[1] = tab[idx[1]];
+  uint32_t u;
+  __builtin_memcpy(&u, &r, 4);
+  return ODD ? (u | (w & 0x80008000u)) : u;
+}
+
+// Stage tab[0..sat] of a global table and the NaN entry.
+__device__ __forceinline__ void stage_lut(_Float16* dst, const void* src, int sat) {
+  const _Float16* s = reinterpret_cast<const _Float16*>(src);
+  for (int i = threadIdx.x; i <= sat; i += WD_WAVES * 64) dst[i] = s[i];
+  if (threadIdx.x == 0) {
+    const uint16_t qnan = 0x7e00;
+    __builtin_memcpy(&dst[sat + 1], &qnan, 2);
+  }
+}
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t plane_rsrc(const void* base, int64_t p,
+                                                             int64_t plane_bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<char*>(reinterpret_cast<const char*>(base) + p * plane_bytes), (short)0,
+      (int)plane_bytes, 0x00020000);
+}
+
+}  // namespace
+
+// ---------------------------------------------------------------------------
+// Forward: plane [Na][Nb] -> spectrum [Ka][Kb].  Step A (last axis) per
+// chunk: Y[row][c] = sum_n u[row][n] twA[c][n] (c < Kbp: cos, else -sin),
+// into LDS (transposed, fp16); step B (leading axis) accumulates
+// X[t_a][t_b] += sum_rows (cB - i sB)[t_a][row] Y[row][t_b] over the chunks.
+// ---------------------------------------------------------------------------
+template <int NCT, bool TANH>
+__global__ __launch_bounds__(WD_WAVES * 64, 1) void r2c_wide_kernel(R2CArgs a) {
+  typedef MM<_Float16> M;
+  constexpr int KS = 32, NTB = NCT / 2, KBP = NCT * 8;
+  constexpr int LDA = WD_R + WD_PAD;
+  extern __shared__ __align__(16) unsigned char smem[];
+  _Float16* ATr = reinterpret_cast<_Float16*>(smem);
+  _Float16* ATi = ATr + KBP * LDA;
+  _Float16* lut = ATi + KBP * LDA;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int r16 = lane & 15, g = lane >> 4;
+  const _Float16* twA = reinterpret_cast<const _Float16*>(a.twA);
+  const _Float16* cB = reinterpret_cast<const _Float16*>(a.cB);
+  const _Float16* sB = reinterpret_cast<const _Float16*>(a.sB);
+  const us2 sat = {(unsigned short)a.lut_sat, (unsigned short)a.lut_sat};
+  if (TANH) stage_lut(lut, a.lut, a.lut_sat);
+  __syncthreads();
+
+  const int64_t plane_bytes = (int64_t)a.Na * a.Nb * 2;
+  const int nks = a.Nb / KS;
+  const int nch = a.Na / WD_R;
+  // step-B share of this wave: spectrum row tile ta, column tiles tb0 + j*tbs
+  const int nta = a.Kap16 >> 4;
+  const int ta = wave % nta, tb0 = wave / nta, tbs = WD_WAVES / nta;
+
+  // work items (plane, chunk) of this work-group, in order
+  const int64_t nitems = a.planes > (int64_t)blockIdx.x
+                             ? ((a.planes - 1 - blockIdx.x) / gridDim.x + 1) * nch
+                             : 0;
+  auto item_plane = [&](int64_t it) { return (int64_t)blockIdx.x + (it / nch) * gridDim.x; };
+  auto item_chunk = [&](int64_t it) { return (int)(it % nch) * WD_R; };
+
+  // Lane parts of the buffer offsets (row data: the wave's first row tile,
+  // the second is 128 rows on, in the scalar offset; twiddles: the column
+  // tile's part in the scalar offset).  Formed from an opaque copy of the
+  // thread index where they are used, so they are recomputed rather than
+  // held in registers through the loops.
+  auto row_lane = [&](int c0) {
+    int t = threadIdx.x;
+    asm volatile("" : "+v"(t));
+    return (c0 + wave * 16 + (t & 15)) * a.Nb * 2 + ((t >> 4) & 3) * 16;
+  };
+  auto tw_lane = [&]() {
+    int t = threadIdx.x;
+    asm volatile("" : "+v"(t));
+    return ((t & 15) * a.Nbp + ((t >> 4) & 3) * 8) * 2;
+  };
+  const int rstep = WD_WAVES * 16 * a.Nb * 2;  // second row tile
+  auto ldA = [&](const __amdgpu_buffer_rsrc_t& rs, int rb, int s, u32x4 (&v)[2]) {
+#pragma unroll
+    for (int u = 0; u < 2; ++u)
+      v[u] = __builtin_amdgcn_raw_buffer_load_b128(rs, rb + s * KS * 2, u * rstep, 0);
+  };
+  const __amdgpu_buffer_rsrc_t rt = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<_Float16*>(twA), (short)0, 2 * KBP * a.Nbp * 2, 0x00020000);
+  auto ldB1 = [&](int tl, int s, int ct) {
+    return w_as_h8(__builtin_amdgcn_raw_buffer_load_b128(rt, tl + s * KS * 2,
+                                                         ct * 16 * a.Nbp * 2, 0));
+  };
+  auto ldB = [&](int s, h8 (&b)[NCT]) {
+    const int tl = tw_lane();
+#pragma unroll
+    for (int ct = 0; ct < NCT; ++ct) b[ct] = ldB1(tl, s, ct);
+  };
+
+  f4 accR[NTB], accI[NTB];
+  // row fragments of k-steps s .. s+3 (slot s % 4): each is requested four
+  // k-steps before it is multiplied, the twiddles one k-step before
+  u32x4 va[WD_AD][2];
+  h8 bq[NCT];  // twiddles of the k-step being multiplied, refilled with the
+               // next k-step's as each is consumed
+  __amdgpu_buffer_rsrc_t rs = plane_rsrc(a.in, nitems > 0 ? item_plane(0) : 0, plane_bytes);
+  if (nitems > 0) {
+    const int rb = row_lane(0);
+#pragma unroll
+    for (int d = 0; d < WD_AD; ++d) ldA(rs, rb, d, va[d]);
+    ldB(0, bq);
+  }
+  for (int64_t it = 0; it < nitems; ++it) {
+    const int64_t p = item_plane(it);
+    const int c0 = item_chunk(it);
+    if (c0 == 0) {
+#pragma unroll
+      for (int j = 0; j < NTB; ++j) accR[j] = accI[j] = f4zero();
+    }
+    // the item after this one: its first k-steps are requested after this
+    // chunk's step-B tables; past the end, this item's last k-step again
+    const bool more = it + 1 < nitems;
+    const __amdgpu_buffer_rsrc_t rsn = more ? plane_rsrc(a.in, item_plane(it + 1), plane_bytes) : rs;
+    const int cn = more ? item_chunk(it + 1) : c0;
+
+    // ---- step A ------------------------------------------------------------
+    f4 acc[2][NCT];
+#pragma unroll
+    for (int u = 0; u < 2; ++u)
+#pragma unroll
+      for (int ct = 0; ct < NCT; ++ct) acc[u][ct] = f4zero();
+    auto mul = [&](const u32x4 (&v)[2], int tl, int snext, bool reload) {
+      h8 af[2];
+#pragma unroll
+      for (int u = 0; u < 2; ++u) {
+        u32x4 w = v[u];
+        if (TANH) {
+#pragma unroll
+          for (int e = 0; e < 4; ++e) w[e] = lut2<true>(lut, w[e], sat);
+        }
+        af[u] = w_as_h8(w);
+      }
+#pragma unroll
+      for (int ct = 0; ct < NCT; ++ct) {
+#pragma unroll
+        for (int u = 0; u < 2; ++u) acc[u][ct] = M::mma(af[u], bq[ct], acc[u][ct]);
+        if (reload) bq[ct] = ldB1(tl, snext, ct);
+      }
+    };
+    // nks is a multiple of WD_AD on this path.  Row fragments are requested
+    // WD_AD k-steps ahead within the item; the next item's are requested
+    // only after this chunk's step-B tables, so waiting for those tables
+    // never waits for rows from memory (outstanding loads complete in order).
+#pragma nounroll
+    for (int s0 = 0; s0 < nks - WD_AD; s0 += WD_AD) {
+      const int rb = row_lane(c0), tl = tw_lane();
+#pragma unroll
+      for (int d = 0; d < WD_AD; ++d) {
+        const int s = s0 + d;
+        mul(va[d], tl, s + 1, true);
+        ldA(rs, rb, s + WD_AD, va[d]);
+      }
+    }
+    {
+      const int tl = tw_lane();
+#pragma unroll
+      for (int d = 0; d < WD_AD; ++d) {
+        // (the next item's first twiddles are requested after step B:
+        // register pressure)
+        mul(va[d], tl, nks - WD_AD + d + 1, d + 1 < WD_AD);
+      }
+    }
+    {
+      // LDS offsets formed here, not hoisted out of the item loop (registers)
+      int lb = r16 * LDA + wave * 16 + 4 * g;
+      asm volatile("" : "+v"(lb));
+#pragma unroll
+      for (int u = 0; u < 2; ++u)
+#pragma unroll
+        for (int ct = 0; ct < NCT; ++ct) {
+          // column ct * 16 + r16: rows ct * 16 of [ATr | ATi] (ATi = ATr + KBP * LDA)
+          _Float16* dst = ATr + lb + ct * 16 * LDA + WD_WAVES * 16 * u;
+#pragma unroll
+          for (int i = 0; i < 4; ++i) dst[i] = to_h(acc[u][ct][i] * a.scaleA);
+        }
+    }
+    __builtin_amdgcn_sched_barrier(0);  // accumulators dead before the tables load
+    // step-B tables of this chunk, then the next item's first row fragments
+    // (operands selected, not branched on: one load sequence, exact waits)
+    constexpr int NKB = WD_R / KS;
+    h8 cfs[NKB], sfs[NKB];
+#pragma unroll
+    for (int k = 0; k < NKB; ++k) {
+      const int64_t toff = (int64_t)(ta * 16 + r16) * a.Nap + c0 + k * KS + g * 8;
+      cfs[k] = M::ld(cB + toff);
+      sfs[k] = M::ld(sB + toff);
+    }
+    {
+      const int rb = row_lane(cn);
+#pragma unroll
+      for (int d = 0; d < WD_AD; ++d) ldA(more ? rsn : rs, rb, more ? d : nks - 1, va[d]);
+    }
+    __syncthreads();
+
+    // ---- step B ------------------------------------------------------------
+#pragma unroll
+    for (int k = 0; k < NKB; ++k) {
+      const int k0 = k * KS;
+      const h8 nsf = M::neg(sfs[k]);
+#pragma unroll
+      for (int j = 0; j < NTB; ++j) {
+        const int tb = tb0 + j * tbs;
+        if (tb < NTB) {
+          const h8 ar = M::ld(ATr + (tb * 16 + r16) * LDA + k0 + g * 8);
+          const h8 ai = M::ld(ATi + (tb * 16 + r16) * LDA + k0 + g * 8);
+          accR[j] = M::mma(cfs[k], ar, accR[j]);
+          accR[j] = M::mma(sfs[k], ai, accR[j]);
+          accI[j] = M::mma(cfs[k], ai, accI[j]);
+          accI[j] = M::mma(nsf, ar, accI[j]);
+        }
+      }
+      __builtin_amdgcn_sched_barrier(0);  // bound the hoisting of LDS reads
+    }
+    ldB(0, bq);
+    __syncthreads();
+
+    if (c0 + WD_R >= a.Na) {  // last chunk of the plane: store its spectrum
+      const __amdgpu_buffer_rsrc_t ro = plane_rsrc(a.out, p, (int64_t)a.Ka * a.Kb * 4);
+      // offsets formed here, not hoisted out of the item loop (registers)
+      int ta0 = ta * 16 + 4 * g;
+      asm volatile("" : "+v"(ta0));
+#pragma unroll
+      for (int j = 0; j < NTB; ++j) {
+        const int tb = tb0 + j * tbs;
+        if (tb >= NTB) continue;
+        const int t_b = tb * 16 + r16;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int t_a = ta0 + i;
+          if (t_a < a.Ka && t_b < a.Kb) {
+            h2 v = {to_h(accR[j][i] * a.scaleB), to_h(accI[j][i] * a.scaleB)};
+            uint32_t w;
+            __builtin_memcpy(&w, &v, 4);
+            __builtin_amdgcn_raw_buffer_store_b32(w, ro, (t_a * a.Kb + t_b) * 4, 0, 0);
+          }
+        }
+      }
+    }
+    rs = rsn;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Inverse: spectrum [Ka][Kb] -> plane [Na][Nb], y = scale * sum Re(Z e^{+i
+// theta}), optional epilogue y *= sech^2(x).  Per plane the spectrum is
+// staged transposed in LDS (ZT[kb][ka]: real rows, then imaginary); per
+// chunk step B' gives V[row][kb] = sum_ka (cI + i sI)[row][ka] Z[ka][kb] into
+// LDS as [Re V | Im V] (each wave two 16-row tiles), and step A' sums
+// y[row][m] = sum_k V[row][k] twI[m][k]: each wave takes Nb / 128 column
+// tiles of 16 m, holds one tile's twiddles in registers and sweeps the
+// chunk's 16 row tiles (V from LDS), each lane storing 4 consecutive outputs
+// of one row.  All global loads are issued ahead of their use in the order
+// their waits come (the counter of outstanding loads completes in order):
+// the next item's V-step table rows and spectrum first, then per column
+// tile the next tile's twiddles, then per row tile the x of the row tile 16
+// iterations ahead.
+// ---------------------------------------------------------------------------
+template <int NCT, int NKZ, bool EPI>
+__global__ __launch_bounds__(WD_WAVES * 64, 1) void c2r_wide_kernel(C2RArgs a) {
+  typedef MM<_Float16> M;
+  constexpr int KS = 32, NTB = NCT / 2, KBP = NCT * 8;
+  constexpr int NKV = NCT / 2;          // k-steps of step A' (2 Kbp / 32)
+  constexpr int LDV = 2 * KBP + WD_PAD;
+  constexpr int LDZ = NKZ * KS + WD_PAD;
+  constexpr int NRT = WD_R / 16;        // row tiles per chunk
+  constexpr int ZQ = 4;                 // 16-byte spectrum pieces per thread
+  // the next item's V-step table rows requested before step A' while they
+  // take at most 32 registers, else after it
+  constexpr bool EARLYC = 2 * NKZ * 2 * 4 <= 32;
+  extern __shared__ __align__(16) unsigned char smem[];
+  _Float16* ZT = reinterpret_cast<_Float16*>(smem);  // [2 KBP][LDZ]
+  _Float16* VL = ZT + 2 * KBP * LDZ;                  // [WD_R][LDV]
+  _Float16* lut = VL + WD_R * LDV;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int r16 = lane & 15, g = lane >> 4;
+  const _Float16* cI = reinterpret_cast<const _Float16*>(a.cI);
+  const _Float16* sI = reinterpret_cast<const _Float16*>(a.sI);
+  const _Float16* twI = reinterpret_cast<const _Float16*>(a.twI);
+  const us2 sat = {(unsigned short)a.lut_sat, (unsigned short)a.lut_sat};
+
+  const int64_t plane_bytes = (int64_t)a.Na * a.Nb * 2;
+  const int spec_bytes = a.Ka * a.Kb * 4;
+  const int nch = a.Na / WD_R;
+  const int ctw = a.Nb / 16 / WD_WAVES;  // column tiles per wave
+  const int ct0 = wave * ctw;
+  const int nq = a.Ka * a.Kb / 4;        // 16-byte spectrum pieces
+  const int64_t nitems = a.planes > (int64_t)blockIdx.x
+                             ? ((a.planes - 1 - blockIdx.x) / gridDim.x + 1) * nch
+                             : 0;
+  auto item_plane = [&](int64_t it) { return (int64_t)blockIdx.x + (it / nch) * gridDim.x; };
+  auto item_chunk = [&](int64_t it) { return (int)(it % nch) * WD_R; };
+
+  // the padding of ZT stays zero: every plane writes the same positions
+  for (int i = tid; i < 2 * KBP * LDZ; i += WD_WAVES * 64) ZT[i] = (_Float16)0.0f;
+  if (EPI) stage_lut(lut, a.lut, a.lut_sat);
+
+  auto ldZ = [&](int64_t p, u32x4 (&zq)[ZQ]) {
+    const __amdgpu_buffer_rsrc_t rz = plane_rsrc(a.in, p, spec_bytes);
+#pragma unroll
+    for (int q = 0; q < ZQ; ++q) {
+      const int i = tid + q * WD_WAVES * 64;
+      zq[q] = __builtin_amdgcn_raw_buffer_load_b128(rz, i < nq ? i * 16 : WD_BIG, 0, 0);
+    }
+  };
+  auto stZ = [&](const u32x4 (&zq)[ZQ]) {
+    const int qpr = a.Kb / 4;
+#pragma unroll
+    for (int q = 0; q < ZQ; ++q) {
+      const int i = tid + q * WD_WAVES * 64;
+      if (i < nq) {
+        const int ka = i / qpr, kb0 = (i - ka * qpr) * 4;
+        const h8 v = w_as_h8(zq[q]);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          ZT[(kb0 + e) * LDZ + ka] = v[2 * e];
+          ZT[(KBP + kb0 + e) * LDZ + ka] = v[2 * e + 1];
+        }
+      }
+    }
+  };
+  auto ldC = [&](int c0, h8 (&cf)[2][NKZ], h8 (&sf)[2][NKZ]) {
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      const int64_t row = c0 + (wave + WD_WAVES * u) * 16 + r16;
+#pragma unroll
+      for (int k = 0; k < NKZ; ++k) {
+        cf[u][k] = M::ld(cI + row * a.Kap + k * KS + g * 8);
+        sf[u][k] = M::ld(sI + row * a.Kap + k * KS + g * 8);
+      }
+    }
+  };
+  auto ldT = [&](int ct, h8 (&t)[NKV]) {
+#pragma unroll
+    for (int k = 0; k < NKV; ++k)
+      t[k] = M::ld(twI + (int64_t)(ct * 16 + r16) * (2 * KBP) + k * KS + g * 8);
+  };
+  // x of iteration j (column tile ct0 + j / NRT, row tile j % NRT) of the
+  // item with buffer rx and first row c0
+  auto ldX = [&](const __amdgpu_buffer_rsrc_t& rx, int c0, int j) {
+    const int ct = ct0 + j / NRT, rt = j % NRT;
+    const int off = (c0 + rt * 16 + r16) * a.Nb * 2 + (ct * 16 + 4 * g) * 2;
+    return __builtin_amdgcn_raw_buffer_load_b64(rx, off, 0, 0);
+  };
+
+  u32x4 zq[ZQ];
+  h8 cf[2][NKZ], sf[2][NKZ];
+  h8 tq[NKV];              // twiddles of the next column tile
+  u32x2 xq[NRT];           // x of the next NRT iterations (slot j % NRT)
+  if (nitems > 0) {
+    ldZ(item_plane(0), zq);
+    ldC(0, cf, sf);
+    ldT(ct0, tq);
+    if (EPI) {
+      const __amdgpu_buffer_rsrc_t rx = plane_rsrc(a.x, item_plane(0), plane_bytes);
+#pragma unroll
+      for (int j = 0; j < NRT; ++j) xq[j] = ldX(rx, 0, j);
+    }
+  }
+  __syncthreads();  // ZT cleared, table staged
+
+  for (int64_t it = 0; it < nitems; ++it) {
+    const int64_t p = item_plane(it);
+    const int c0 = item_chunk(it);
+    const bool more = it + 1 < nitems;
+    const int64_t pn = more ? item_plane(it + 1) : p;
+    const int cn = more ? item_chunk(it + 1) : c0;
+    if (c0 == 0) {
+      stZ(zq);
+      __syncthreads();
+    }
+
+    // ---- step B': V for rows c0 + (wave + 8u) * 16 + [0, 16), two column
+    // tiles of kb at a time (register pressure) ------------------------------
+    constexpr int TBH = NTB < 2 ? NTB : 2;
+#pragma unroll
+    for (int tbh = 0; tbh < NTB; tbh += TBH) {
+      f4 vr[2][TBH], vi[2][TBH];
+#pragma unroll
+      for (int u = 0; u < 2; ++u)
+#pragma unroll
+        for (int t = 0; t < TBH; ++t) vr[u][t] = vi[u][t] = f4zero();
+#pragma unroll
+      for (int ks = 0; ks < NKZ; ++ks) {
+        h8 nsf[2];
+#pragma unroll
+        for (int u = 0; u < 2; ++u) nsf[u] = M::neg(sf[u][ks]);
+#pragma unroll
+        for (int t = 0; t < TBH; ++t) {
+          const int tb = tbh + t;
+          const h8 zr = M::ld(ZT + (tb * 16 + r16) * LDZ + ks * KS + g * 8);
+          const h8 zi = M::ld(ZT + (KBP + tb * 16 + r16) * LDZ + ks * KS + g * 8);
+#pragma unroll
+          for (int u = 0; u < 2; ++u) {
+            vr[u][t] = M::mma(cf[u][ks], zr, vr[u][t]);
+            vr[u][t] = M::mma(nsf[u], zi, vr[u][t]);
+            vi[u][t] = M::mma(cf[u][ks], zi, vi[u][t]);
+            vi[u][t] = M::mma(sf[u][ks], zr, vi[u][t]);
+          }
+        }
+      }
+      // D: lane holds rows 4 g + i, column kb = tb * 16 + r16
+#pragma unroll
+      for (int u = 0; u < 2; ++u)
+#pragma unroll
+        for (int t = 0; t < TBH; ++t)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            const int rl = (wave + WD_WAVES * u) * 16 + 4 * g + i;
+            const int kb = (tbh + t) * 16 + r16;
+            VL[rl * LDV + kb] = to_h(vr[u][t][i]);
+            VL[rl * LDV + KBP + kb] = to_h(vi[u][t][i]);
+          }
+    }
+    __syncthreads();
+
+    // next item's V-step rows and (new plane) spectrum, before this item's
+    // column-tile and x requests (with many of them, after step A' instead:
+    // register pressure)
+    if (EARLYC) {
+      ldC(cn, cf, sf);
+      if (more && cn == 0) ldZ(pn, zq);
+    }
+
+    // ---- step A' ---------------------------------------------------------------
+    const __amdgpu_buffer_rsrc_t ry = plane_rsrc(a.out, p, plane_bytes);
+    const __amdgpu_buffer_rsrc_t rx = plane_rsrc(EPI ? a.x : a.out, p, plane_bytes);
+    const __amdgpu_buffer_rsrc_t rxn = plane_rsrc(EPI ? a.x : a.out, pn, plane_bytes);
+    const int J = ctw * NRT;
+#pragma nounroll
+    for (int j0 = 0; j0 < J; j0 += NRT) {
+      const int ct = ct0 + j0 / NRT;
+      h8 tf[NKV];
+#pragma unroll
+      for (int k = 0; k < NKV; ++k) tf[k] = tq[k];
+      ldT(ct + 1 < ct0 + ctw ? ct + 1 : ct0, tq);  // next tile (next item: first)
+      const bool last = j0 + NRT >= J;
+      h8 vf[NKV];
+#pragma unroll
+      for (int k = 0; k < NKV; ++k) vf[k] = M::ld(VL + r16 * LDV + k * KS + g * 8);
+#pragma unroll
+      for (int rt = 0; rt < NRT; ++rt) {
+        // V fragments of the next row tile requested before this one's
+        // products; the barrier at the end keeps the scheduler from hoisting
+        // further (register pressure)
+        h8 vn[NKV];
+        const int rn = rt + 1 < NRT ? rt + 1 : rt;
+#pragma unroll
+        for (int k = 0; k < NKV; ++k) vn[k] = M::ld(VL + (rn * 16 + r16) * LDV + k * KS + g * 8);
+        f4 acc = f4zero();
+#pragma unroll
+        for (int k = 0; k < NKV; ++k) acc = M::mma(tf[k], vf[k], acc);
+        float v[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) v[i] = acc[i] * a.scale;
+        if (EPI) {
+          const u32x2 xs = xq[rt];
+          // x of iteration j0 + rt + NRT: this item's, else the next item's
+          // first (late mode: those are requested after the next item's
+          // V-step rows, and this slot re-reads the current tile).  Operands
+          // selected, not branched on: one load sequence, exact waits.
+          const bool nxt = last && EARLYC;
+          xq[rt] = ldX(nxt ? rxn : rx, nxt ? cn : c0,
+                       last ? (EARLYC ? rt : j0 + rt) : j0 + NRT + rt);
+          const uint32_t s0 = lut2<false>(lut, xs[0], sat);
+          const uint32_t s1 = lut2<false>(lut, xs[1], sat);
+          h2 h0, h1;
+          __builtin_memcpy(&h0, &s0, 4);
+          __builtin_memcpy(&h1, &s1, 4);
+          v[0] *= (float)h0[0];
+          v[1] *= (float)h0[1];
+          v[2] *= (float)h1[0];
+          v[3] *= (float)h1[1];
+        }
+        h4 o = {to_h(v[0]), to_h(v[1]), to_h(v[2]), to_h(v[3])};
+        u32x2 w;
+        __builtin_memcpy(&w, &o, 8);
+        const int off = (c0 + rt * 16 + r16) * a.Nb * 2 + (ct * 16 + 4 * g) * 2;
+        __builtin_amdgcn_raw_buffer_store_b64(w, ry, off, 0, WD_NT);
+#pragma unroll
+        for (int k = 0; k < NKV; ++k) vf[k] = vn[k];
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    }
+    if (!EARLYC) {
+      ldC(cn, cf, sf);
+      if (more && cn == 0) ldZ(pn, zq);
+      if (EPI) {
+#pragma unroll
+        for (int rt = 0; rt < NRT; ++rt) xq[rt] = ldX(rxn, cn, rt);
+      }
+    }
+    __syncthreads();
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Launchers (hipErrorNotSupported: the shape is not one of this path's)
+// ---------------------------------------------------------------------------
+size_t r2c_wide_lds_bytes(int nct, bool tanh, int lut_sat) {
+  const size_t at = (size_t)2 * (nct * 8) * (WD_R + WD_PAD) * 2;
+  return at + (tanh ? (size_t)(lut_sat + 2) * 2 : 0);
+}
+
+size_t c2r_wide_lds_bytes(int nct, int Kap, bool epi, int lut_sat) {
+  const size_t zt = (size_t)2 * (nct * 8) * (Kap + WD_PAD) * 2;
+  const size_t vl = (size_t)WD_R * (2 * nct * 8 + WD_PAD) * 2;
+  return zt + vl + (epi ? (size_t)(lut_sat + 2) * 2 : 0);
+}
+
+hipError_t launch_r2c_wide(const R2CArgs& a, int nct, int grid, size_t lds, hipStream_t s) {
+  const bool t = a.do_tanh != 0;
+  const void* k = nullptr;
+  if (nct == 4) k = t ? (const void*)&r2c_wide_kernel<4, true> : (const void*)&r2c_wide_kernel<4, false>;
+  if (nct == 8) k = t ? (const void*)&r2c_wide_kernel<8, true> : (const void*)&r2c_wide_kernel<8, false>;
+  if (!k || lds > 160 * 1024) return hipErrorNotSupported;
+  hipError_t e = hipFuncSetAttribute(k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+  if (e != hipSuccess) return e;
+  dim3 gr(grid), bl(WD_WAVES * 64);
+  if (nct == 4) {
+    if (t) hipLaunchKernelGGL((r2c_wide_kernel<4, true>), gr, bl, lds, s, a);
+    else hipLaunchKernelGGL((r2c_wide_kernel<4, false>), gr, bl, lds, s, a);
+  } else {
+    if (t) hipLaunchKernelGGL((r2c_wide_kernel<8, true>), gr, bl, lds, s, a);
+    else hipLaunchKernelGGL((r2c_wide_kernel<8, false>), gr, bl, lds, s, a);
+  }
+  return hipGetLastError();
+}
+
+template <int NCT, int NKZ>
+static hipError_t c2r_wide_go(const C2RArgs& a, int grid, size_t lds, hipStream_t s) {
+  const void* k = a.epilogue ? (const void*)&c2r_wide_kernel<NCT, NKZ, true>
+                             : (const void*)&c2r_wide_kernel<NCT, NKZ, false>;
+  hipError_t e = hipFuncSetAttribute(k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+  if (e != hipSuccess) return e;
+  dim3 gr(grid), bl(WD_WAVES * 64);
+  if (a.epilogue) hipLaunchKernelGGL((c2r_wide_kernel<NCT, NKZ, true>), gr, bl, lds, s, a);
+  else hipLaunchKernelGGL((c2r_wide_kernel<NCT, NKZ, false>), gr, bl, lds, s, a);
+  return hipGetLastError();
+}
+
+// Shapes: nct in {4, 8}, Kap in {32, 64, 128}, Ka * Kb <= 8192, Nb a multiple
+// of 128, Na a multiple of 256.
+hipError_t launch_c2r_wide(const C2RArgs& a, int nct, int grid, size_t lds, hipStream_t s) {
+  if (lds > 160 * 1024 || a.Ka * a.Kb > 8192 || a.Nb % 128 != 0 || a.Na % WD_R != 0 ||
+      a.Kb % 4 != 0)
+    return hipErrorNotSupported;
+  const int nkz = a.Kap / 32;
+  if (nct == 4 && nkz == 1) return c2r_wide_go<4, 1>(a, grid, lds, s);
+  if (nct == 4 && nkz == 2) return c2r_wide_go<4, 2>(a, grid, lds, s);
+  if (nct == 4 && nkz == 4) return c2r_wide_go<4, 4>(a, grid, lds, s);
+  if (nct == 8 && nkz == 1) return c2r_wide_go<8, 1>(a, grid, lds, s);
+  if (nct == 8 && nkz == 2) return c2r_wide_go<8, 2>(a, grid, lds, s);
+  if (nct == 8 && nkz == 4) return c2r_wide_go<8, 4>(a, grid, lds, s);
+  return hipErrorNotSupported;
+}
+
+}  // namespace fno

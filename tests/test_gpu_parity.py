@@ -54,6 +54,9 @@ EDGE = [
     ((1000, 40), (6, 9), 1, 2, 3),      # several row chunks, rows not a multiple of 32
     ((16, 256), (8, 100), 1, 2, 2),     # 100 retained last-axis modes (widest tile)
     ((64, 64), (32, 33), 1, 2, 2),      # 64 leading-axis slots, Nyquist
+    ((256, 256), (32, 32), 2, 3, 2),    # wide-plane transforms: one 256-row chunk
+    ((512, 128), (16, 64), 1, 2, 3),    # wide-plane transforms: two chunks, 64 last-axis modes
+    ((256, 256), (32, 32), 9, 30, 31),  # wide-plane transforms: more planes than work-groups
 ]
 
 
@@ -252,11 +255,16 @@ def test_caches_match_recompute(prec):
         assert np.array_equal(u, v)
 
 
-def test_fp16_extremes_stay_finite():
+# small planes, and planes that take the wide-plane transforms
+SPECIAL_SHAPES = [((32, 32), (4, 5)), ((256, 256), (32, 32))]
+
+
+@pytest.mark.parametrize("shape", range(len(SPECIAL_SHAPES)))
+def test_fp16_extremes_stay_finite(shape):
     """tanh bounds the transform input: +-65504 and +-inf give finite outputs
     that still match the oracle."""
-    n, modes, Bt, ci, co = (32, 32), (4, 5), 2, 3, 3
-    U.say("fp16 extremes")
+    (n, modes), Bt, ci, co = SPECIAL_SHAPES[shape], 2, 3, 3
+    U.say(f"fp16 extremes n={n}")
     x, w, gy = synth.random_dense_case(79, Bt, ci, co, n, modes, np.float16, x_scale=3.0)
     x[0, 0, 0, :4] = np.array([65504.0, -65504.0, np.inf, -np.inf], dtype=np.float16)
     layer = U.make_layer(n, modes, Bt, ci, co, "fp16_tanh")
@@ -267,9 +275,10 @@ def test_fp16_extremes_stay_finite():
     _assert_close("gW", U.cplx(gw), rgw, "fp16_tanh")
 
 
-def test_nan_propagates():
-    n, modes, Bt, ci, co = (32, 32), (4, 5), 2, 3, 3
-    U.say("nan propagation")
+@pytest.mark.parametrize("shape", range(len(SPECIAL_SHAPES)))
+def test_nan_propagates(shape):
+    (n, modes), Bt, ci, co = SPECIAL_SHAPES[shape], 2, 3, 3
+    U.say(f"nan propagation n={n}")
     x, w, gy = synth.random_dense_case(80, Bt, ci, co, n, modes, np.float16)
     x[0, 1, 5, 7] = np.nan
     layer = U.make_layer(n, modes, Bt, ci, co, "fp16_tanh")
