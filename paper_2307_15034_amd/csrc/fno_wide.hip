@@ -84,16 +84,32 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t plane_rsrc(const void* base, i
 // chunk: Y[row][c] = sum_n u[row][n] twA[c][n] (c < Kbp: cos, else -sin),
 // into LDS (transposed, fp16); step B (leading axis) accumulates
 // X[t_a][t_b] += sum_rows (cB - i sB)[t_a][row] Y[row][t_b] over the chunks.
+//
+// The twiddles of step A go through LDS in slices of two k-steps (all 2 Kbp
+// rows x 64 columns), double buffered: the whole work-group loads slice
+// g + 2 into registers while slice g is multiplied, and writes slice g + 1
+// to LDS before the barrier that ends slice g.  The slice sequence is the
+// same for every item, so it simply wraps around at the item boundary.  The
+// per-wave global loads are then the row stream (four k-steps ahead) and,
+// once per chunk, the step-B tables; every load is waited for about four
+// k-steps after its request (outstanding loads complete in order, so a
+// short-latency load waited for early would also wait for the rows).
 // ---------------------------------------------------------------------------
+constexpr int WD_SK = 64;             // columns (n) per twiddle slice
+constexpr int WD_LDT = WD_SK + WD_PAD;
+
 template <int NCT, bool TANH>
 __global__ __launch_bounds__(WD_WAVES * 64, 1) void r2c_wide_kernel(R2CArgs a) {
   typedef MM<_Float16> M;
   constexpr int KS = 32, NTB = NCT / 2, KBP = NCT * 8;
   constexpr int LDA = WD_R + WD_PAD;
+  constexpr int TWP = 2 * KBP * WD_SK / 8 / (WD_WAVES * 64);  // 16-byte pieces per thread
+  static_assert(TWP >= 1, "slice pieces");
   extern __shared__ __align__(16) unsigned char smem[];
   _Float16* ATr = reinterpret_cast<_Float16*>(smem);
   _Float16* ATi = ATr + KBP * LDA;
-  _Float16* lut = ATi + KBP * LDA;
+  _Float16* TWb = ATi + KBP * LDA;                  // [2][2 KBP][WD_LDT]
+  _Float16* lut = TWb + 2 * 2 * KBP * WD_LDT;
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int r16 = lane & 15, g = lane >> 4;
@@ -102,10 +118,10 @@ __global__ __launch_bounds__(WD_WAVES * 64, 1) void r2c_wide_kernel(R2CArgs a) {
   const _Float16* sB = reinterpret_cast<const _Float16*>(a.sB);
   const us2 sat = {(unsigned short)a.lut_sat, (unsigned short)a.lut_sat};
   if (TANH) stage_lut(lut, a.lut, a.lut_sat);
-  __syncthreads();
 
   const int64_t plane_bytes = (int64_t)a.Na * a.Nb * 2;
-  const int nks = a.Nb / KS;
+  const int nks = a.Nb / KS;        // a multiple of 4 on this path
+  const int ngr = nks / 2;          // twiddle slices per item (even)
   const int nch = a.Na / WD_R;
   // step-B share of this wave: spectrum row tile ta, column tiles tb0 + j*tbs
   const int nta = a.Kap16 >> 4;
@@ -118,52 +134,57 @@ __global__ __launch_bounds__(WD_WAVES * 64, 1) void r2c_wide_kernel(R2CArgs a) {
   auto item_plane = [&](int64_t it) { return (int64_t)blockIdx.x + (it / nch) * gridDim.x; };
   auto item_chunk = [&](int64_t it) { return (int)(it % nch) * WD_R; };
 
-  // Lane parts of the buffer offsets (row data: the wave's first row tile,
-  // the second is 128 rows on, in the scalar offset; twiddles: the column
-  // tile's part in the scalar offset).  Formed from an opaque copy of the
-  // thread index where they are used, so they are recomputed rather than
-  // held in registers through the loops.
+  // Lane part of the row-data offset (the second row tile, 128 rows on, in
+  // the scalar offset), formed from an opaque copy of the thread index where
+  // it is used, so it is recomputed rather than held through the loops.
   auto row_lane = [&](int c0) {
     int t = threadIdx.x;
     asm volatile("" : "+v"(t));
     return (c0 + wave * 16 + (t & 15)) * a.Nb * 2 + ((t >> 4) & 3) * 16;
   };
-  auto tw_lane = [&]() {
-    int t = threadIdx.x;
-    asm volatile("" : "+v"(t));
-    return ((t & 15) * a.Nbp + ((t >> 4) & 3) * 8) * 2;
-  };
-  const int rstep = WD_WAVES * 16 * a.Nb * 2;  // second row tile
+  const int rstep = WD_WAVES * 16 * a.Nb * 2;
   auto ldA = [&](const __amdgpu_buffer_rsrc_t& rs, int rb, int s, u32x4 (&v)[2]) {
 #pragma unroll
     for (int u = 0; u < 2; ++u)
       v[u] = __builtin_amdgcn_raw_buffer_load_b128(rs, rb + s * KS * 2, u * rstep, 0);
   };
+  // twiddle slice gs: rows c < 2 KBP, columns gs * 64 + [0, 64); thread t
+  // takes pieces t + 512 e (row piece / 8, 8 halves at (piece % 8) * 8)
   const __amdgpu_buffer_rsrc_t rt = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<_Float16*>(twA), (short)0, 2 * KBP * a.Nbp * 2, 0x00020000);
-  auto ldB1 = [&](int tl, int s, int ct) {
-    return w_as_h8(__builtin_amdgcn_raw_buffer_load_b128(rt, tl + s * KS * 2,
-                                                         ct * 16 * a.Nbp * 2, 0));
-  };
-  auto ldB = [&](int s, h8 (&b)[NCT]) {
-    const int tl = tw_lane();
+  auto ldTW = [&](int gs, u32x4 (&v)[TWP]) {
 #pragma unroll
-    for (int ct = 0; ct < NCT; ++ct) b[ct] = ldB1(tl, s, ct);
+    for (int e = 0; e < TWP; ++e) {
+      const int pc = tid + e * WD_WAVES * 64;
+      v[e] = __builtin_amdgcn_raw_buffer_load_b128(rt, ((pc >> 3) * a.Nbp + (pc & 7) * 8) * 2,
+                                                   gs * WD_SK * 2, 0);
+    }
+  };
+  auto stTW = [&](const u32x4 (&v)[TWP], int buf) {
+    _Float16* d = TWb + buf * (2 * KBP * WD_LDT);
+#pragma unroll
+    for (int e = 0; e < TWP; ++e) {
+      const int pc = tid + e * WD_WAVES * 64;
+      *reinterpret_cast<u32x4*>(d + (pc >> 3) * WD_LDT + (pc & 7) * 8) = v[e];
+    }
   };
 
   f4 accR[NTB], accI[NTB];
-  // row fragments of k-steps s .. s+3 (slot s % 4): each is requested four
-  // k-steps before it is multiplied, the twiddles one k-step before
+  // row fragments of k-steps s .. s+3 (slot s % 4), each requested four
+  // k-steps before it is multiplied; twiddle slices g + 1, g + 2 in flight
   u32x4 va[WD_AD][2];
-  h8 bq[NCT];  // twiddles of the k-step being multiplied, refilled with the
-               // next k-step's as each is consumed
+  u32x4 twr[2][TWP];
   __amdgpu_buffer_rsrc_t rs = plane_rsrc(a.in, nitems > 0 ? item_plane(0) : 0, plane_bytes);
   if (nitems > 0) {
+    ldTW(0, twr[0]);
+    ldTW(1, twr[1]);
     const int rb = row_lane(0);
 #pragma unroll
     for (int d = 0; d < WD_AD; ++d) ldA(rs, rb, d, va[d]);
-    ldB(0, bq);
+    stTW(twr[0], 0);
   }
+  __syncthreads();  // table and first slice staged
+
   for (int64_t it = 0; it < nitems; ++it) {
     const int64_t p = item_plane(it);
     const int c0 = item_chunk(it);
@@ -171,8 +192,6 @@ __global__ __launch_bounds__(WD_WAVES * 64, 1) void r2c_wide_kernel(R2CArgs a) {
 #pragma unroll
       for (int j = 0; j < NTB; ++j) accR[j] = accI[j] = f4zero();
     }
-    // the item after this one: its first k-steps are requested after this
-    // chunk's step-B tables; past the end, this item's last k-step again
     const bool more = it + 1 < nitems;
     const __amdgpu_buffer_rsrc_t rsn = more ? plane_rsrc(a.in, item_plane(it + 1), plane_bytes) : rs;
     const int cn = more ? item_chunk(it + 1) : c0;
@@ -183,7 +202,8 @@ __global__ __launch_bounds__(WD_WAVES * 64, 1) void r2c_wide_kernel(R2CArgs a) {
     for (int u = 0; u < 2; ++u)
 #pragma unroll
       for (int ct = 0; ct < NCT; ++ct) acc[u][ct] = f4zero();
-    auto mul = [&](const u32x4 (&v)[2], int tl, int snext, bool reload) {
+    // k-step k of the slice in LDS buffer buf
+    auto mul = [&](const u32x4 (&v)[2], int buf, int k) {
       h8 af[2];
 #pragma unroll
       for (int u = 0; u < 2; ++u) {
@@ -194,36 +214,36 @@ __global__ __launch_bounds__(WD_WAVES * 64, 1) void r2c_wide_kernel(R2CArgs a) {
         }
         af[u] = w_as_h8(w);
       }
+      const _Float16* tb = TWb + buf * (2 * KBP * WD_LDT) + r16 * WD_LDT + k * KS + g * 8;
 #pragma unroll
       for (int ct = 0; ct < NCT; ++ct) {
+        const h8 bf = M::ld(tb + ct * 16 * WD_LDT);
 #pragma unroll
-        for (int u = 0; u < 2; ++u) acc[u][ct] = M::mma(af[u], bq[ct], acc[u][ct]);
-        if (reload) bq[ct] = ldB1(tl, snext, ct);
+        for (int u = 0; u < 2; ++u) acc[u][ct] = M::mma(af[u], bf, acc[u][ct]);
       }
     };
-    // nks is a multiple of WD_AD on this path.  Row fragments are requested
-    // WD_AD k-steps ahead within the item; the next item's are requested
-    // only after this chunk's step-B tables, so waiting for those tables
-    // never waits for rows from memory (outstanding loads complete in order).
+    // one slice: its two k-steps, then the next slice into LDS and a barrier
+    auto slice = [&](int gs, int par, int rb, bool rows) {
+      ldTW(gs + 2 < ngr ? gs + 2 : gs + 2 - ngr, twr[par]);
+#pragma unroll
+      for (int k = 0; k < 2; ++k) {
+        const int s = 2 * gs + k;
+        mul(va[(2 * par + k) % WD_AD], par, k);
+        if (rows) ldA(rs, rb, s + WD_AD, va[(2 * par + k) % WD_AD]);
+      }
+      stTW(twr[1 - par], 1 - par);
+      __syncthreads();
+    };
 #pragma nounroll
-    for (int s0 = 0; s0 < nks - WD_AD; s0 += WD_AD) {
-      const int rb = row_lane(c0), tl = tw_lane();
-#pragma unroll
-      for (int d = 0; d < WD_AD; ++d) {
-        const int s = s0 + d;
-        mul(va[d], tl, s + 1, true);
-        ldA(rs, rb, s + WD_AD, va[d]);
-      }
+    for (int gs = 0; gs < ngr - 2; gs += 2) {
+      const int rb = row_lane(c0);
+      slice(gs, 0, rb, true);
+      slice(gs + 1, 1, rb, true);
     }
-    {
-      const int tl = tw_lane();
-#pragma unroll
-      for (int d = 0; d < WD_AD; ++d) {
-        // (the next item's first twiddles are requested after step B:
-        // register pressure)
-        mul(va[d], tl, nks - WD_AD + d + 1, d + 1 < WD_AD);
-      }
-    }
+    // last two slices: the next item's rows are requested after the step-B
+    // tables
+    slice(ngr - 2, 0, 0, false);
+    slice(ngr - 1, 1, 0, false);
     {
       // LDS offsets formed here, not hoisted out of the item loop (registers)
       int lb = r16 * LDA + wave * 16 + 4 * g;
@@ -263,19 +283,18 @@ __global__ __launch_bounds__(WD_WAVES * 64, 1) void r2c_wide_kernel(R2CArgs a) {
       const h8 nsf = M::neg(sfs[k]);
 #pragma unroll
       for (int j = 0; j < NTB; ++j) {
-        const int tb = tb0 + j * tbs;
-        if (tb < NTB) {
-          const h8 ar = M::ld(ATr + (tb * 16 + r16) * LDA + k0 + g * 8);
-          const h8 ai = M::ld(ATi + (tb * 16 + r16) * LDA + k0 + g * 8);
-          accR[j] = M::mma(cfs[k], ar, accR[j]);
-          accR[j] = M::mma(sfs[k], ai, accR[j]);
-          accI[j] = M::mma(cfs[k], ai, accI[j]);
-          accI[j] = M::mma(nsf, ar, accI[j]);
-        }
+        // (column tiles past NTB are computed from a clamped tile and never
+        // stored: no branch, so no copies of the accumulators)
+        const int tb = min(tb0 + j * tbs, NTB - 1);
+        const h8 ar = M::ld(ATr + (tb * 16 + r16) * LDA + k0 + g * 8);
+        const h8 ai = M::ld(ATi + (tb * 16 + r16) * LDA + k0 + g * 8);
+        accR[j] = M::mma(cfs[k], ar, accR[j]);
+        accR[j] = M::mma(sfs[k], ai, accR[j]);
+        accI[j] = M::mma(cfs[k], ai, accI[j]);
+        accI[j] = M::mma(nsf, ar, accI[j]);
       }
       __builtin_amdgcn_sched_barrier(0);  // bound the hoisting of LDS reads
     }
-    ldB(0, bq);
     __syncthreads();
 
     if (c0 + WD_R >= a.Na) {  // last chunk of the plane: store its spectrum
@@ -563,7 +582,8 @@ __global__ __launch_bounds__(WD_WAVES * 64, 1) void c2r_wide_kernel(C2RArgs a) {
 // ---------------------------------------------------------------------------
 size_t r2c_wide_lds_bytes(int nct, bool tanh, int lut_sat) {
   const size_t at = (size_t)2 * (nct * 8) * (WD_R + WD_PAD) * 2;
-  return at + (tanh ? (size_t)(lut_sat + 2) * 2 : 0);
+  const size_t tw = (size_t)2 * 2 * (nct * 8) * WD_LDT * 2;
+  return at + tw + (tanh ? (size_t)(lut_sat + 2) * 2 : 0);
 }
 
 size_t c2r_wide_lds_bytes(int nct, int Kap, bool epi, int lut_sat) {
