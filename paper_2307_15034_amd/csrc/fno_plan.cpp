@@ -923,11 +923,6 @@ fno_status run_r2c(const Plan* pl, const void* in, void* spec, void* inter, int6
   return FNO_OK;
 }
 
-// The wide-plane inverse kernel writes 32-byte row pieces per lane (partial
-// cache lines); the generic inverse, which writes whole lines through an LDS
-// transpose, is faster on every measured shape, so the wide one stays off.
-constexpr bool kWideInverse = false;
-
 // Inverse: spectrum [B][C][K...] -> planes, out = scale * sum Re(Z e^{+i theta}).
 fno_status run_c2r(const Plan* pl, const void* spec, void* out, void* inter, int64_t C,
                    float scale, const void* x_epi, hipStream_t s) {
@@ -1003,7 +998,7 @@ fno_status run_c2r(const Plan* pl, const void* spec, void* out, void* inter, int
       if (e != hipErrorNotSupported) return hip_fail(e, kname);
     }
   }
-  if (kWideInverse && g.elem == ELEM_F16 && g.Nb % 128 == 0 && g.Na % 256 == 0 &&
+  if (g.elem == ELEM_F16 && g.Nb % 128 == 0 && g.Na % 256 == 0 &&
       (g.nct == 4 || g.nct == 8) && g.Kap <= 128 && g.Na * (int64_t)g.Nb * 2 < ((int64_t)1 << 30)) {
     // large planes: persistent eight-wave work-groups, one per compute unit
     a.lut_sat = pl->t.sech2Sat;

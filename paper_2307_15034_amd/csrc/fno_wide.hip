@@ -328,32 +328,52 @@ __global__ __launch_bounds__(WD_WAVES * 64, 1) void r2c_wide_kernel(R2CArgs a) {
 // theta}), optional epilogue y *= sech^2(x).  Per plane the spectrum is
 // staged transposed in LDS (ZT[kb][ka]: real rows, then imaginary); per
 // chunk step B' gives V[row][kb] = sum_ka (cI + i sI)[row][ka] Z[ka][kb] into
-// LDS as [Re V | Im V] (each wave two 16-row tiles), and step A' sums
-// y[row][m] = sum_k V[row][k] twI[m][k]: each wave takes Nb / 128 column
-// tiles of 16 m, holds one tile's twiddles in registers and sweeps the
-// chunk's 16 row tiles (V from LDS), each lane storing 4 consecutive outputs
-// of one row.  All global loads are issued ahead of their use in the order
-// their waits come (the counter of outstanding loads completes in order):
-// the next item's V-step table rows and spectrum first, then per column
-// tile the next tile's twiddles, then per row tile the x of the row tile 16
-// iterations ahead.
+// LDS as [Re V | Im V] (each wave two 16-row tiles), and each wave then holds
+// its rows of V in registers for step A', y[row][m] = sum_k V[row][k]
+// twI[m][k], over blocks of 64 columns m.  The twiddles of a block go
+// through LDS (double buffered, in the space V used: the whole work-group
+// loads block b + 2 into registers while block b is multiplied and writes
+// block b + 1 before the barrier that ends block b).  Each wave's 16 x 64
+// result of a row tile passes through a per-wave fp32 LDS buffer so that a
+// lane stores 16 consecutive outputs of one row (four lanes write a whole
+// 128-byte line), and x of the epilogue is read in the same layout two
+// blocks ahead.  The next item's step-B' table rows and spectrum are
+// requested before this item's blocks (outstanding loads complete in
+// order).
 // ---------------------------------------------------------------------------
+constexpr int WD_MB = 64;      // output columns per block of step A'
+constexpr int WD_LDO = 68;     // transpose buffer row stride (floats)
+
+template <int NCT, int NKZ>
+struct C2RWide {
+  static constexpr int KBP = NCT * 8;
+  static constexpr int LDV = 2 * KBP + WD_PAD;
+  static constexpr int LDZ = NKZ * 32 + WD_PAD;
+  static constexpr int LDT = 2 * KBP + WD_PAD;
+  static constexpr size_t zt_bytes = (size_t)2 * KBP * LDZ * 2;
+  static constexpr size_t vl_bytes = (size_t)WD_R * LDV * 2;
+  static constexpr size_t tw_bytes = (size_t)2 * WD_MB * LDT * 2;
+  static constexpr size_t ob_bytes = (size_t)WD_WAVES * 16 * WD_LDO * 4;
+  static constexpr size_t reg_bytes = vl_bytes > tw_bytes + ob_bytes ? vl_bytes : tw_bytes + ob_bytes;
+};
+
 template <int NCT, int NKZ, bool EPI>
 __global__ __launch_bounds__(WD_WAVES * 64, 1) void c2r_wide_kernel(C2RArgs a) {
   typedef MM<_Float16> M;
+  typedef C2RWide<NCT, NKZ> L;
   constexpr int KS = 32, NTB = NCT / 2, KBP = NCT * 8;
   constexpr int NKV = NCT / 2;          // k-steps of step A' (2 Kbp / 32)
-  constexpr int LDV = 2 * KBP + WD_PAD;
-  constexpr int LDZ = NKZ * KS + WD_PAD;
-  constexpr int NRT = WD_R / 16;        // row tiles per chunk
+  constexpr int LDV = L::LDV, LDZ = L::LDZ, LDT = L::LDT;
   constexpr int ZQ = 4;                 // 16-byte spectrum pieces per thread
-  // the next item's V-step table rows requested before step A' while they
-  // take at most 32 registers, else after it
-  constexpr bool EARLYC = 2 * NKZ * 2 * 4 <= 32;
+  constexpr int TWP = 2 * KBP * WD_MB / 8 / (WD_WAVES * 64);  // twiddle pieces per thread
+  static_assert(TWP >= 1, "block pieces");
   extern __shared__ __align__(16) unsigned char smem[];
-  _Float16* ZT = reinterpret_cast<_Float16*>(smem);  // [2 KBP][LDZ]
-  _Float16* VL = ZT + 2 * KBP * LDZ;                  // [WD_R][LDV]
-  _Float16* lut = VL + WD_R * LDV;
+  _Float16* ZT = reinterpret_cast<_Float16*>(smem);                      // [2 KBP][LDZ]
+  unsigned char* reg = smem + L::zt_bytes;
+  _Float16* VL = reinterpret_cast<_Float16*>(reg);                       // [WD_R][LDV]
+  _Float16* TW = reinterpret_cast<_Float16*>(reg);                       // [2][WD_MB][LDT]
+  float* OB = reinterpret_cast<float*>(reg + L::tw_bytes);               // [8][16][WD_LDO]
+  _Float16* lut = reinterpret_cast<_Float16*>(reg + L::reg_bytes);
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int r16 = lane & 15, g = lane >> 4;
@@ -361,12 +381,12 @@ __global__ __launch_bounds__(WD_WAVES * 64, 1) void c2r_wide_kernel(C2RArgs a) {
   const _Float16* sI = reinterpret_cast<const _Float16*>(a.sI);
   const _Float16* twI = reinterpret_cast<const _Float16*>(a.twI);
   const us2 sat = {(unsigned short)a.lut_sat, (unsigned short)a.lut_sat};
+  float* ob = OB + wave * 16 * WD_LDO;
 
   const int64_t plane_bytes = (int64_t)a.Na * a.Nb * 2;
   const int spec_bytes = a.Ka * a.Kb * 4;
   const int nch = a.Na / WD_R;
-  const int ctw = a.Nb / 16 / WD_WAVES;  // column tiles per wave
-  const int ct0 = wave * ctw;
+  const int nmb = a.Nb / WD_MB;          // even on this path
   const int nq = a.Ka * a.Kb / 4;        // 16-byte spectrum pieces
   const int64_t nitems = a.planes > (int64_t)blockIdx.x
                              ? ((a.planes - 1 - blockIdx.x) / gridDim.x + 1) * nch
@@ -413,31 +433,55 @@ __global__ __launch_bounds__(WD_WAVES * 64, 1) void c2r_wide_kernel(C2RArgs a) {
       }
     }
   };
-  auto ldT = [&](int ct, h8 (&t)[NKV]) {
+  // twiddle block b: rows m = b * 64 + [0, 64), all 2 KBP columns; thread t
+  // takes pieces t + 512 e (row piece / (KBP / 4), 8 halves at the rest * 8)
+  const __amdgpu_buffer_rsrc_t rt = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<_Float16*>(twI), (short)0, a.Nb * 2 * KBP * 2, 0x00020000);
+  constexpr int PPR = 2 * KBP / 8;  // pieces per twiddle row
+  auto ldTW = [&](int b, u32x4 (&v)[TWP]) {
 #pragma unroll
-    for (int k = 0; k < NKV; ++k)
-      t[k] = M::ld(twI + (int64_t)(ct * 16 + r16) * (2 * KBP) + k * KS + g * 8);
+    for (int e = 0; e < TWP; ++e) {
+      const int pc = tid + e * WD_WAVES * 64;
+      v[e] = __builtin_amdgcn_raw_buffer_load_b128(rt, ((pc / PPR) * 2 * KBP + (pc % PPR) * 8) * 2,
+                                                   b * WD_MB * 2 * KBP * 2, 0);
+    }
   };
-  // x of iteration j (column tile ct0 + j / NRT, row tile j % NRT) of the
-  // item with buffer rx and first row c0
-  auto ldX = [&](const __amdgpu_buffer_rsrc_t& rx, int c0, int j) {
-    const int ct = ct0 + j / NRT, rt = j % NRT;
-    const int off = (c0 + rt * 16 + r16) * a.Nb * 2 + (ct * 16 + 4 * g) * 2;
-    return __builtin_amdgcn_raw_buffer_load_b64(rx, off, 0, 0);
+  auto stTW = [&](const u32x4 (&v)[TWP], int buf) {
+    _Float16* d = TW + buf * (WD_MB * LDT);
+#pragma unroll
+    for (int e = 0; e < TWP; ++e) {
+      const int pc = tid + e * WD_WAVES * 64;
+      *reinterpret_cast<u32x4*>(d + (pc / PPR) * LDT + (pc % PPR) * 8) = v[e];
+    }
+  };
+  // x (or y) offset of this lane in the transposed layout: row lane / 4 of
+  // row tile u, 16 columns at (lane % 4) * 16 of block b
+  auto xoff = [&](int c0, int u, int b) {
+    return (c0 + (wave + WD_WAVES * u) * 16 + (lane >> 2)) * a.Nb * 2 +
+           (b * WD_MB + (lane & 3) * 16) * 2;
+  };
+  auto ldX = [&](const __amdgpu_buffer_rsrc_t& rx, int c0, int b, u32x4 (&v)[2][2]) {
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      const int o = xoff(c0, u, b);
+      v[u][0] = __builtin_amdgcn_raw_buffer_load_b128(rx, o, 0, 0);
+      v[u][1] = __builtin_amdgcn_raw_buffer_load_b128(rx, o + 16, 0, 0);
+    }
   };
 
   u32x4 zq[ZQ];
   h8 cf[2][NKZ], sf[2][NKZ];
-  h8 tq[NKV];              // twiddles of the next column tile
-  u32x2 xq[NRT];           // x of the next NRT iterations (slot j % NRT)
+  u32x4 twr[2][TWP];   // twiddle blocks b + 1, b + 2 in flight
+  u32x4 xr[2][2][2];   // x of blocks b + 1, b + 2 (slot b % 2)
   if (nitems > 0) {
     ldZ(item_plane(0), zq);
     ldC(0, cf, sf);
-    ldT(ct0, tq);
+    ldTW(0, twr[0]);
+    ldTW(1, twr[1]);
     if (EPI) {
       const __amdgpu_buffer_rsrc_t rx = plane_rsrc(a.x, item_plane(0), plane_bytes);
-#pragma unroll
-      for (int j = 0; j < NRT; ++j) xq[j] = ldX(rx, 0, j);
+      ldX(rx, 0, 0, xr[0]);
+      ldX(rx, 0, 1, xr[1]);
     }
   }
   __syncthreads();  // ZT cleared, table staged
@@ -497,83 +541,97 @@ __global__ __launch_bounds__(WD_WAVES * 64, 1) void c2r_wide_kernel(C2RArgs a) {
     }
     __syncthreads();
 
-    // next item's V-step rows and (new plane) spectrum, before this item's
-    // column-tile and x requests (with many of them, after step A' instead:
-    // register pressure)
-    if (EARLYC) {
-      ldC(cn, cf, sf);
-      if (more && cn == 0) ldZ(pn, zq);
-    }
+    // this wave's rows of V, as B operands of step A'
+    h8 vf[2][NKV];
+#pragma unroll
+    for (int u = 0; u < 2; ++u)
+#pragma unroll
+      for (int k = 0; k < NKV; ++k)
+        vf[u][k] = M::ld(VL + ((wave + WD_WAVES * u) * 16 + r16) * LDV + k * KS + g * 8);
+    // next item's step-B' table rows and (new plane) spectrum, before this
+    // item's block requests
+    ldC(cn, cf, sf);
+    if (more && cn == 0) ldZ(pn, zq);
+    __syncthreads();  // V read: its space takes the twiddle blocks
+    stTW(twr[0], 0);
+    __syncthreads();
 
     // ---- step A' ---------------------------------------------------------------
     const __amdgpu_buffer_rsrc_t ry = plane_rsrc(a.out, p, plane_bytes);
     const __amdgpu_buffer_rsrc_t rx = plane_rsrc(EPI ? a.x : a.out, p, plane_bytes);
     const __amdgpu_buffer_rsrc_t rxn = plane_rsrc(EPI ? a.x : a.out, pn, plane_bytes);
-    const int J = ctw * NRT;
-#pragma nounroll
-    for (int j0 = 0; j0 < J; j0 += NRT) {
-      const int ct = ct0 + j0 / NRT;
-      h8 tf[NKV];
-#pragma unroll
-      for (int k = 0; k < NKV; ++k) tf[k] = tq[k];
-      ldT(ct + 1 < ct0 + ctw ? ct + 1 : ct0, tq);  // next tile (next item: first)
-      const bool last = j0 + NRT >= J;
-      h8 vf[NKV];
-#pragma unroll
-      for (int k = 0; k < NKV; ++k) vf[k] = M::ld(VL + r16 * LDV + k * KS + g * 8);
-#pragma unroll
-      for (int rt = 0; rt < NRT; ++rt) {
-        // V fragments of the next row tile requested before this one's
-        // products; the barrier at the end keeps the scheduler from hoisting
-        // further (register pressure)
-        h8 vn[NKV];
-        const int rn = rt + 1 < NRT ? rt + 1 : rt;
-#pragma unroll
-        for (int k = 0; k < NKV; ++k) vn[k] = M::ld(VL + (rn * 16 + r16) * LDV + k * KS + g * 8);
-        f4 acc = f4zero();
-#pragma unroll
-        for (int k = 0; k < NKV; ++k) acc = M::mma(tf[k], vf[k], acc);
-        float v[4];
-#pragma unroll
-        for (int i = 0; i < 4; ++i) v[i] = acc[i] * a.scale;
-        if (EPI) {
-          const u32x2 xs = xq[rt];
-          // x of iteration j0 + rt + NRT: this item's, else the next item's
-          // first (late mode: those are requested after the next item's
-          // V-step rows, and this slot re-reads the current tile).  Operands
-          // selected, not branched on: one load sequence, exact waits.
-          const bool nxt = last && EARLYC;
-          xq[rt] = ldX(nxt ? rxn : rx, nxt ? cn : c0,
-                       last ? (EARLYC ? rt : j0 + rt) : j0 + NRT + rt);
-          const uint32_t s0 = lut2<false>(lut, xs[0], sat);
-          const uint32_t s1 = lut2<false>(lut, xs[1], sat);
-          h2 h0, h1;
-          __builtin_memcpy(&h0, &s0, 4);
-          __builtin_memcpy(&h1, &s1, 4);
-          v[0] *= (float)h0[0];
-          v[1] *= (float)h0[1];
-          v[2] *= (float)h1[0];
-          v[3] *= (float)h1[1];
-        }
-        h4 o = {to_h(v[0]), to_h(v[1]), to_h(v[2]), to_h(v[3])};
-        u32x2 w;
-        __builtin_memcpy(&w, &o, 8);
-        const int off = (c0 + rt * 16 + r16) * a.Nb * 2 + (ct * 16 + 4 * g) * 2;
-        __builtin_amdgcn_raw_buffer_store_b64(w, ry, off, 0, WD_NT);
-#pragma unroll
-        for (int k = 0; k < NKV; ++k) vf[k] = vn[k];
-        __builtin_amdgcn_sched_barrier(0);
-      }
-    }
-    if (!EARLYC) {
-      ldC(cn, cf, sf);
-      if (more && cn == 0) ldZ(pn, zq);
+    auto block = [&](int b, int par) {
+      // requests two blocks ahead (the next item's first ones at the end);
+      // operands selected, not branched on: one load sequence, exact waits
+      ldTW(b + 2 < nmb ? b + 2 : b + 2 - nmb, twr[par]);
+      u32x4 xs[2][2];
       if (EPI) {
 #pragma unroll
-        for (int rt = 0; rt < NRT; ++rt) xq[rt] = ldX(rxn, cn, rt);
+        for (int u = 0; u < 2; ++u) {
+          xs[u][0] = xr[par][u][0];
+          xs[u][1] = xr[par][u][1];
+        }
+        const bool nxt = b + 2 >= nmb;
+        ldX(nxt ? rxn : rx, nxt ? cn : c0, nxt ? b + 2 - nmb : b + 2, xr[par]);
       }
+      const _Float16* tb = TW + par * (WD_MB * LDT) + r16 * LDT + g * 8;
+#pragma unroll
+      for (int u = 0; u < 2; ++u) {
+        f4 acc[4];
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+          acc[c] = f4zero();
+#pragma unroll
+          for (int k = 0; k < NKV; ++k)
+            acc[c] = M::mma(M::ld(tb + c * 16 * LDT + k * KS), vf[u][k], acc[c]);
+        }
+        // D: lane holds column n = r16 (row of y), rows m = c * 16 + 4 g + i
+#pragma unroll
+        for (int c = 0; c < 4; ++c)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) ob[r16 * WD_LDO + c * 16 + 4 * g + i] = acc[c][i] * a.scale;
+        wave_lds_sync();
+        float v[16];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const f4 t = *reinterpret_cast<const f4*>(ob + (lane >> 2) * WD_LDO + (lane & 3) * 16 + 4 * q);
+          v[4 * q] = t[0];
+          v[4 * q + 1] = t[1];
+          v[4 * q + 2] = t[2];
+          v[4 * q + 3] = t[3];
+        }
+        wave_lds_sync();
+        if (EPI) {
+#pragma unroll
+          for (int h = 0; h < 2; ++h)
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+              const uint32_t sw = lut2<false>(lut, xs[u][h][e], sat);
+              h2 s2;
+              __builtin_memcpy(&s2, &sw, 4);
+              v[8 * h + 2 * e] *= (float)s2[0];
+              v[8 * h + 2 * e + 1] *= (float)s2[1];
+            }
+        }
+        const int o = xoff(c0, u, b);
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+          h8 w;
+#pragma unroll
+          for (int e = 0; e < 8; ++e) w[e] = to_h(v[8 * h + e]);
+          u32x4 wv;
+          __builtin_memcpy(&wv, &w, 16);
+          __builtin_amdgcn_raw_buffer_store_b128(wv, ry, o + 16 * h, 0, WD_NT);
+        }
+      }
+      stTW(twr[1 - par], 1 - par);
+      __syncthreads();
+    };
+#pragma nounroll
+    for (int b = 0; b < nmb; b += 2) {
+      block(b, 0);
+      block(b + 1, 1);
     }
-    __syncthreads();
   }
 }
 
@@ -587,9 +645,15 @@ size_t r2c_wide_lds_bytes(int nct, bool tanh, int lut_sat) {
 }
 
 size_t c2r_wide_lds_bytes(int nct, int Kap, bool epi, int lut_sat) {
-  const size_t zt = (size_t)2 * (nct * 8) * (Kap + WD_PAD) * 2;
-  const size_t vl = (size_t)WD_R * (2 * nct * 8 + WD_PAD) * 2;
-  return zt + vl + (epi ? (size_t)(lut_sat + 2) * 2 : 0);
+  size_t base = 0;
+  const int nkz = Kap / 32;
+#define FNO_C2RW_BYTES(N, K) \
+  if (nct == N && nkz == K) base = C2RWide<N, K>::zt_bytes + C2RWide<N, K>::reg_bytes;
+  FNO_C2RW_BYTES(4, 1) FNO_C2RW_BYTES(4, 2) FNO_C2RW_BYTES(4, 4)
+  FNO_C2RW_BYTES(8, 1) FNO_C2RW_BYTES(8, 2) FNO_C2RW_BYTES(8, 4)
+#undef FNO_C2RW_BYTES
+  if (base == 0) return (size_t)1 << 30;  // not a shape of this path
+  return base + (epi ? (size_t)(lut_sat + 2) * 2 : 0);
 }
 
 hipError_t launch_r2c_wide(const R2CArgs& a, int nct, int grid, size_t lds, hipStream_t s) {
@@ -626,7 +690,7 @@ static hipError_t c2r_wide_go(const C2RArgs& a, int grid, size_t lds, hipStream_
 // Shapes: nct in {4, 8}, Kap in {32, 64, 128}, Ka * Kb <= 8192, Nb a multiple
 // of 128, Na a multiple of 256.
 hipError_t launch_c2r_wide(const C2RArgs& a, int nct, int grid, size_t lds, hipStream_t s) {
-  if (lds > 160 * 1024 || a.Ka * a.Kb > 8192 || a.Nb % 128 != 0 || a.Na % WD_R != 0 ||
+  if (lds > 160 * 1024 || a.Ka * a.Kb > 8192 || a.Nb % (2 * WD_MB) != 0 || a.Na % WD_R != 0 ||
       a.Kb % 4 != 0)
     return hipErrorNotSupported;
   const int nkz = a.Kap / 32;
