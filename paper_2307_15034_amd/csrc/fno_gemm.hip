@@ -8,9 +8,9 @@
 // operand is reached through per-class strides: any index order, no
 // transposed copies.  A work-group owns a TM x TN tile of one batch entry and
 // walks K in stages of 16 through LDS (operands converted to fp32 and
-// conjugated on the way in); each complex product is four real
-// v_mfma_f32_16x16x4_f32 (Re += ar br - ai bi, Im += ar bi + ai br), fp32
-// accumulation.  Long reductions over few results are split over work-groups
+// conjugated on the way in); each complex product is three real
+// v_mfma_f32_16x16x4_f32 products (Gauss: ar br, ai bi, (ar + ai)(br + bi)),
+// fp32 accumulation.  Long reductions over few results are split over work-groups
 // (split-K); the partial sums are then added in split order by a second
 // kernel, so the result does not depend on scheduling.
 #include <hip/hip_runtime.h>
@@ -92,15 +92,28 @@ __device__ __forceinline__ void store_c(void* p, int elem, int64_t off, float re
     reinterpret_cast<f2*>(p)[off] = f2{re, im};
 }
 
-// One operand tile (rows x GM_TK) of a stage into registers: NE elements
-// per thread, lanes along k (KFAST) or along the rows.
+// One operand tile (rows x GM_TK) of a stage into registers.  With 64 or
+// more rows a thread takes four consecutive k of one row (four loads) and
+// writes them to LDS as one 16-byte access in the layout the MFMA fragments
+// are read in (no bank conflicts); lanes run along the row's k quads
+// (KFAST) or along the rows.  Smaller tiles: one element per thread.
 template <int ROWS>
 struct TileLoader {
   static constexpr int NE = ROWS * GM_TK / 256;
+  static constexpr bool QUAD = ROWS >= 64;
   float re[NE], im[NE];
   __device__ __forceinline__ static void slot(bool kfast, int e, int& r, int& kk) {
     const int t = threadIdx.x;
-    if (kfast) {
+    if (QUAD) {
+      const int q = e >> 2, j = e & 3;  // quad q of this thread, element j
+      if (kfast) {
+        kk = (t & 3) * 4 + j;
+        r = (t >> 2) + 64 * q;
+      } else {
+        r = t % ROWS;
+        kk = (t / ROWS + (256 / ROWS) * q) * 4 + j;
+      }
+    } else if (kfast) {
       kk = t & (GM_TK - 1);
       r = (t >> 4) + 16 * e;
     } else {
@@ -123,12 +136,24 @@ struct TileLoader {
     }
   }
   __device__ __forceinline__ void store(bool kfast, float* lre, float* lim) const {
+    if (QUAD) {
 #pragma unroll
-    for (int e = 0; e < NE; ++e) {
-      int r, kk;
-      slot(kfast, e, r, kk);
-      lre[r * GM_LS + kk] = re[e];
-      lim[r * GM_LS + kk] = im[e];
+      for (int q = 0; q < NE / 4; ++q) {
+        int r, kk;
+        slot(kfast, 4 * q, r, kk);
+        *reinterpret_cast<f4*>(lre + r * GM_LS + kk) =
+            f4{re[4 * q], re[4 * q + 1], re[4 * q + 2], re[4 * q + 3]};
+        *reinterpret_cast<f4*>(lim + r * GM_LS + kk) =
+            f4{im[4 * q], im[4 * q + 1], im[4 * q + 2], im[4 * q + 3]};
+      }
+    } else {
+#pragma unroll
+      for (int e = 0; e < NE; ++e) {
+        int r, kk;
+        slot(kfast, e, r, kk);
+        lre[r * GM_LS + kk] = re[e];
+        lim[r * GM_LS + kk] = im[e];
+      }
     }
   }
 };
@@ -194,11 +219,11 @@ __global__ __launch_bounds__(256) void pair_gemm_kernel(GemmArgs g) {
 
   const int lane = tid & 63, wave = tid >> 6, r16 = lane & 15, gq = lane >> 4;
   const int wm = wave % WGM, wn = wave / WGM;
-  f4 cr[FM][FN], ci[FM][FN];
+  f4 t1[FM][FN], t2[FM][FN], t3[FM][FN];
 #pragma unroll
   for (int i = 0; i < FM; ++i)
 #pragma unroll
-    for (int j = 0; j < FN; ++j) cr[i][j] = ci[i][j] = f4zero();
+    for (int j = 0; j < FN; ++j) t1[i][j] = t2[i][j] = t3[i][j] = f4zero();
 
   TileLoader<TM> la;
   TileLoader<TN> lb;
@@ -214,20 +239,23 @@ __global__ __launch_bounds__(256) void pair_gemm_kernel(GemmArgs g) {
       la.load(g.a, g.a_elem, g.conj_a, akf, baA, moA, koA, (st + 1) * GM_TK, klen);
       lb.load(g.b, g.b_elem, g.conj_b, bkf, baB, noB, koB, (st + 1) * GM_TK, klen);
     }
-    // lane (r16, gq) holds k = 4 gq + s of MFMA k-step s (A and B alike)
-    f4 ar[FM], ai[FM], an[FM], br[FN], bi[FN];
+    // lane (r16, gq) holds k = 4 gq + s of MFMA k-step s (A and B alike).
+    // Complex product with three real products (Gauss): t1 = ar br,
+    // t2 = ai bi, t3 = (ar + ai)(br + bi); Re = t1 - t2, Im = t3 - t1 - t2.
+    f4 ar[FM], ai[FM], as[FM], br[FN], bi[FN], bs[FN];
 #pragma unroll
     for (int i = 0; i < FM; ++i) {
       const int row = wm * WM + i * 16 + r16;
       ar[i] = *reinterpret_cast<const f4*>(&As[0][row * GM_LS + 4 * gq]);
       ai[i] = *reinterpret_cast<const f4*>(&As[1][row * GM_LS + 4 * gq]);
-      an[i] = -ai[i];
+      as[i] = ar[i] + ai[i];
     }
 #pragma unroll
     for (int j = 0; j < FN; ++j) {
       const int col = wn * WN + j * 16 + r16;
       br[j] = *reinterpret_cast<const f4*>(&Bs[0][col * GM_LS + 4 * gq]);
       bi[j] = *reinterpret_cast<const f4*>(&Bs[1][col * GM_LS + 4 * gq]);
+      bs[j] = br[j] + bi[j];
     }
 #pragma unroll
     for (int s = 0; s < 4; ++s)
@@ -235,13 +263,20 @@ __global__ __launch_bounds__(256) void pair_gemm_kernel(GemmArgs g) {
       for (int i = 0; i < FM; ++i)
 #pragma unroll
         for (int j = 0; j < FN; ++j) {
-          cr[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(ar[i][s], br[j][s], cr[i][j], 0, 0, 0);
-          cr[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(an[i][s], bi[j][s], cr[i][j], 0, 0, 0);
-          ci[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(ar[i][s], bi[j][s], ci[i][j], 0, 0, 0);
-          ci[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(ai[i][s], br[j][s], ci[i][j], 0, 0, 0);
+          t1[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(ar[i][s], br[j][s], t1[i][j], 0, 0, 0);
+          t2[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(ai[i][s], bi[j][s], t2[i][j], 0, 0, 0);
+          t3[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(as[i][s], bs[j][s], t3[i][j], 0, 0, 0);
         }
     __syncthreads();
   }
+  f4 cr[FM][FN], ci[FM][FN];
+#pragma unroll
+  for (int i = 0; i < FM; ++i)
+#pragma unroll
+    for (int j = 0; j < FN; ++j) {
+      cr[i][j] = t1[i][j] - t2[i][j];
+      ci[i][j] = t3[i][j] - t1[i][j] - t2[i][j];
+    }
 
   // D: lane holds rows 4 gq + v, column r16 of each 16 x 16 tile
   const int64_t total = (int64_t)g.c[CL_BT].size * M * N;
