@@ -382,7 +382,7 @@ size_t axis_lds_bytes(int elem, int Linp) {
   return (size_t)2 * 64 * (Linp + pad) * es;
 }
 
-template <typename T>
+template <typename T, bool VEC>
 __global__ __launch_bounds__(256) void axis_kernel(AxisArgs a) {
   using M = MM<T>;
   using frag = typename M::frag;
@@ -400,16 +400,31 @@ __global__ __launch_bounds__(256) void axis_kernel(AxisArgs a) {
   const T* er = reinterpret_cast<const T*>(a.er);
   const T* ei = reinterpret_cast<const T*>(a.ei);
 
-  for (int idx = threadIdx.x; idx < a.Linp * 64; idx += 256) {
-    const int l = idx >> 6, jj = idx & 63;
-    T re = from_f<T>(0.0f), im = from_f<T>(0.0f);
-    if (l < a.Lin && j0 + jj < a.inner) {
-      const T* s = in + ((int64_t)l * a.inner + j0 + jj) * 2;
-      re = s[0];
-      im = s[1];
+  if constexpr (VEC) {
+    // fp16 with inner % 4 == 0: 16-byte loads of four consecutive columns
+    for (int idx = threadIdx.x; idx < a.Linp * 16; idx += 256) {
+      const int l = idx >> 4, jj = (idx & 15) * 4;
+      h8 v = MM<_Float16>::zero();
+      if (l < a.Lin && j0 + jj < a.inner)
+        v = *reinterpret_cast<const h8*>(in + ((int64_t)l * a.inner + j0 + jj) * 2);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        Ir[(jj + e) * ld + l] = v[2 * e];
+        Ii[(jj + e) * ld + l] = v[2 * e + 1];
+      }
     }
-    Ir[jj * ld + l] = re;
-    Ii[jj * ld + l] = im;
+  } else {
+    for (int idx = threadIdx.x; idx < a.Linp * 64; idx += 256) {
+      const int l = idx >> 6, jj = idx & 63;
+      T re = from_f<T>(0.0f), im = from_f<T>(0.0f);
+      if (l < a.Lin && j0 + jj < a.inner) {
+        const T* s = in + ((int64_t)l * a.inner + j0 + jj) * 2;
+        re = s[0];
+        im = s[1];
+      }
+      Ir[jj * ld + l] = re;
+      Ii[jj * ld + l] = im;
+    }
   }
   __syncthreads();
   const int jt = wave;  // each wave owns 16 of the 64 columns
@@ -1043,10 +1058,12 @@ hipError_t launch_c2r(int elem, int nct, const C2RArgs& a, size_t lds, hipStream
 
 hipError_t launch_axis(int elem, const AxisArgs& a, size_t lds, hipStream_t s) {
   dim3 grid((unsigned)((a.inner + 63) / 64), (unsigned)a.outer), block(256);
-  if (elem == ELEM_F16)
-    FNO_LAUNCH((axis_kernel<_Float16>), grid, block, lds, s, a);
+  if (elem == ELEM_F16 && a.inner % 4 == 0)
+    FNO_LAUNCH((axis_kernel<_Float16, true>), grid, block, lds, s, a);
+  else if (elem == ELEM_F16)
+    FNO_LAUNCH((axis_kernel<_Float16, false>), grid, block, lds, s, a);
   else
-    FNO_LAUNCH((axis_kernel<float>), grid, block, lds, s, a);
+    FNO_LAUNCH((axis_kernel<float, false>), grid, block, lds, s, a);
   return hipGetLastError();
 }
 
