@@ -50,6 +50,10 @@ def parse():
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--cpu-seconds", type=float, default=12.0)
     p.add_argument("--profile-steps", type=int, default=20)
+    p.add_argument("--copy-probe", action="store_true",
+                   help="only run a plain elementwise kernel that reads 1 GiB and writes "
+                        "1 GiB, three times (the calibration of the FETCH_SIZE / WRITE_SIZE "
+                        "counters)")
     return p.parse_args()
 
 
@@ -169,6 +173,21 @@ def cpu_baseline(wl, x, w, gy, prec, seconds):
                       f"fwd+bwd_data+bwd_weight, {el:.1f} s"}
 
 
+def copy_probe(torch):
+    """A plain elementwise kernel that reads 1 GiB and writes 1 GiB (int32
+    negation, torch's own kernel), three times: what FETCH_SIZE and
+    WRITE_SIZE read for it calibrates them in bytes."""
+    assert torch.cuda.is_available(), "the copy probe needs a GPU"
+    n = (1 << 30) // 4
+    a = torch.ones(n, dtype=torch.int32, device="cuda")
+    b = torch.empty_like(a)
+    for _ in range(3):
+        torch.neg(a, out=b)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_probe_bytes_read": n * 4, "copy_probe_bytes_written": n * 4,
+                      "dispatches": 3}))
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -177,6 +196,9 @@ def main():
                           "n_gpus": args.gpus}))
         sys.exit(2)
     import torch
+    if args.copy_probe:
+        copy_probe(torch)
+        return
     import synth
     from paper_2307_15034_amd import binding as B
     from paper_2307_15034_amd.layer import SpectralConv
