@@ -334,10 +334,10 @@ __global__ __launch_bounds__(WD_WAVES * 64, 1) void r2c_wide_kernel(R2CArgs a) {
 // through LDS (double buffered, in the space V used: the whole work-group
 // loads block b + 2 into registers while block b is multiplied and writes
 // block b + 1 before the barrier that ends block b).  Each wave's 16 x 64
-// result of a row tile passes through a per-wave fp32 LDS buffer so that a
-// lane stores 16 consecutive outputs of one row (four lanes write a whole
-// 128-byte line), and x of the epilogue is read in the same layout two
-// blocks ahead.  The next item's step-B' table rows and spectrum are
+// result of a row tile passes through a per-wave fp32 LDS buffer so that
+// every 16-byte store instruction writes eight whole 128-byte lines (a lane
+// takes 8 consecutive outputs of two rows), and x of the epilogue is read in
+// the same layout two blocks ahead.  The next item's step-B' table rows and spectrum are
 // requested before this item's blocks (outstanding loads complete in
 // order).
 // ---------------------------------------------------------------------------
@@ -454,19 +454,19 @@ __global__ __launch_bounds__(WD_WAVES * 64, 1) void c2r_wide_kernel(C2RArgs a) {
       *reinterpret_cast<u32x4*>(d + (pc / PPR) * LDT + (pc % PPR) * 8) = v[e];
     }
   };
-  // x (or y) offset of this lane in the transposed layout: row lane / 4 of
-  // row tile u, 16 columns at (lane % 4) * 16 of block b
-  auto xoff = [&](int c0, int u, int b) {
-    return (c0 + (wave + WD_WAVES * u) * 16 + (lane >> 2)) * a.Nb * 2 +
-           (b * WD_MB + (lane & 3) * 16) * 2;
+  // x (or y) offset of this lane in the transposed layout: row
+  // lane / 8 + 8 h of row tile u, 8 columns at (lane % 8) * 8 of block b, so
+  // that each 16-byte access instruction covers eight whole 128-byte lines
+  auto xoff = [&](int c0, int u, int b, int h) {
+    return (c0 + (wave + WD_WAVES * u) * 16 + (lane >> 3) + 8 * h) * a.Nb * 2 +
+           (b * WD_MB + (lane & 7) * 8) * 2;
   };
   auto ldX = [&](const __amdgpu_buffer_rsrc_t& rx, int c0, int b, u32x4 (&v)[2][2]) {
 #pragma unroll
-    for (int u = 0; u < 2; ++u) {
-      const int o = xoff(c0, u, b);
-      v[u][0] = __builtin_amdgcn_raw_buffer_load_b128(rx, o, 0, 0);
-      v[u][1] = __builtin_amdgcn_raw_buffer_load_b128(rx, o + 16, 0, 0);
-    }
+    for (int u = 0; u < 2; ++u)
+#pragma unroll
+      for (int h = 0; h < 2; ++h)
+        v[u][h] = __builtin_amdgcn_raw_buffer_load_b128(rx, xoff(c0, u, b, h), 0, 0);
   };
 
   u32x4 zq[ZQ];
@@ -591,10 +591,12 @@ __global__ __launch_bounds__(WD_WAVES * 64, 1) void c2r_wide_kernel(C2RArgs a) {
 #pragma unroll
           for (int i = 0; i < 4; ++i) ob[r16 * WD_LDO + c * 16 + 4 * g + i] = acc[c][i] * a.scale;
         wave_lds_sync();
-        float v[16];
+        float v[16];  // v[8 h + e]: row lane / 8 + 8 h, column (lane % 8) * 8 + e
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
-          const f4 t = *reinterpret_cast<const f4*>(ob + (lane >> 2) * WD_LDO + (lane & 3) * 16 + 4 * q);
+          const int h = q >> 1, e0 = (q & 1) * 4;
+          const f4 t = *reinterpret_cast<const f4*>(ob + ((lane >> 3) + 8 * h) * WD_LDO +
+                                                    (lane & 7) * 8 + e0);
           v[4 * q] = t[0];
           v[4 * q + 1] = t[1];
           v[4 * q + 2] = t[2];
@@ -613,7 +615,6 @@ __global__ __launch_bounds__(WD_WAVES * 64, 1) void c2r_wide_kernel(C2RArgs a) {
               v[8 * h + 2 * e + 1] *= (float)s2[1];
             }
         }
-        const int o = xoff(c0, u, b);
 #pragma unroll
         for (int h = 0; h < 2; ++h) {
           h8 w;
@@ -621,7 +622,7 @@ __global__ __launch_bounds__(WD_WAVES * 64, 1) void c2r_wide_kernel(C2RArgs a) {
           for (int e = 0; e < 8; ++e) w[e] = to_h(v[8 * h + e]);
           u32x4 wv;
           __builtin_memcpy(&wv, &w, 16);
-          __builtin_amdgcn_raw_buffer_store_b128(wv, ry, o + 16 * h, 0, WD_NT);
+          __builtin_amdgcn_raw_buffer_store_b128(wv, ry, xoff(c0, u, b, h), 0, WD_NT);
         }
       }
       stTW(twr[1 - par], 1 - par);
