@@ -881,8 +881,11 @@ __global__ __launch_bounds__(256) void pair_kernel(PairArgs a) {
 
 // Products without a contracted index (elementwise and outer products):
 // PE_NV consecutive results along the innermost result index per thread,
-// decoded once; each is the same single product as in pair_kernel.
-constexpr int PE_NV = 4;
+// decoded once; each is the same single product as in pair_kernel.  The
+// two results of a thread are stored with one access (16 bytes fp32, 8 bytes
+// fp16), so consecutive lanes write consecutive bytes and every store
+// instruction covers whole cache lines.
+constexpr int PE_NV = 2;
 
 __global__ __launch_bounds__(256) void pair_ew_kernel(PairArgs a, int64_t items) {
   const int64_t it = (int64_t)blockIdx.x * 256 + threadIdx.x;
@@ -898,11 +901,24 @@ __global__ __launch_bounds__(256) void pair_ew_kernel(PairArgs a, int64_t items)
     x[j] = load_elem(a.a, a.a_elem, ao + j * sa);
     y[j] = load_elem(a.b, a.b_elem, bo + j * sb);
   }
+  float r[2 * PE_NV];
 #pragma unroll
   for (int j = 0; j < PE_NV; ++j) {
     float sr = 0.0f, si = 0.0f;
     pair_fma(a, x[j], y[j], sr, si);
-    pair_store(a, idx + j, kin == a.scale_c_axis ? cidx + j : cidx, sr, si);
+    float s = a.scale;
+    if (a.scale_c_axis >= 0) {
+      const int64_t ci = kin == a.scale_c_axis ? cidx + j : cidx;
+      s *= (ci == 0 || 2 * ci == a.Nb) ? 1.0f : 2.0f;
+    }
+    r[2 * j] = sr * s;
+    r[2 * j + 1] = si * s;
+  }
+  if (a.out_elem == ELEM_F16) {
+    h4 v = {to_h(r[0]), to_h(r[1]), to_h(r[2]), to_h(r[3])};
+    reinterpret_cast<h4*>(a.out)[it] = v;
+  } else {
+    reinterpret_cast<f4*>(a.out)[it] = f4{r[0], r[1], r[2], r[3]};
   }
 }
 
