@@ -413,13 +413,24 @@ hipError_t launch_pair_gemm(const PairArgs& p, hipStream_t s) {
     for (const Sub& u : v) m = std::min(m, key(a ? u.sa : u.sb));
     return m;
   };
-  // the smaller class goes to N (operands swap roles; the product commutes)
+  // The class holding the result's contiguous index goes to N: lanes run
+  // along N in the D fragments, so each store instruction then writes
+  // consecutive elements.  Otherwise the smaller class goes to N.  (The
+  // operands swap roles; the product commutes.)
   auto csize = [&](const std::vector<Sub>& v) {
     int64_t z = 1;
     for (const Sub& u : v) z *= u.ext;
     return z;
   };
-  if (csize(cls[CL_N]) > csize(cls[CL_M])) {
+  auto has_unit = [&](const std::vector<Sub>& v) {
+    for (const Sub& u : v)
+      if (u.sr == 1) return true;
+    return false;
+  };
+  const bool swap_mn = has_unit(cls[CL_M])   ? true
+                       : has_unit(cls[CL_N]) ? false
+                                             : csize(cls[CL_N]) > csize(cls[CL_M]);
+  if (swap_mn) {
     std::swap(cls[CL_M], cls[CL_N]);
     for (auto& v : cls)
       for (Sub& u : v) std::swap(u.sa, u.sb);
@@ -469,6 +480,10 @@ hipError_t launch_pair_gemm(const PairArgs& p, hipStream_t s) {
     cfg = 0, TM = 128, TN = 16;
   } else if (N <= 32) {
     cfg = 1, TM = 128, TN = 32;
+  } else if (M <= 16) {
+    cfg = 3, TM = 16, TN = 128;
+  } else if (M <= 32) {
+    cfg = 4, TM = 32, TN = 128;
   } else {
     cfg = 2, TM = 64, TN = 64;
   }
@@ -495,6 +510,8 @@ hipError_t launch_pair_gemm(const PairArgs& p, hipStream_t s) {
   switch (cfg) {
     case 0: hipLaunchKernelGGL((pair_gemm_kernel<128, 16, 4>), grid, block, 0, s, g); break;
     case 1: hipLaunchKernelGGL((pair_gemm_kernel<128, 32, 4>), grid, block, 0, s, g); break;
+    case 3: hipLaunchKernelGGL((pair_gemm_kernel<16, 128, 1>), grid, block, 0, s, g); break;
+    case 4: hipLaunchKernelGGL((pair_gemm_kernel<32, 128, 1>), grid, block, 0, s, g); break;
     default: hipLaunchKernelGGL((pair_gemm_kernel<64, 64, 2>), grid, block, 0, s, g); break;
   }
   hipError_t e = hipGetLastError();
