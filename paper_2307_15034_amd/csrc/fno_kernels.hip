@@ -469,6 +469,95 @@ __global__ __launch_bounds__(256) void axis_kernel(AxisArgs a) {
   }
 }
 
+// fp16 variant for small tables (Lout padded to 16 <= 128, Lin padded to 32
+// <= 128, inner a multiple of 4): the twiddle table is staged in LDS next to
+// the data (no global loads between the products), and the 16-row x 64-column
+// result tiles are staged in LDS too, so that every store instruction writes
+// whole 256-byte row segments (consecutive lanes, consecutive 16 bytes).
+size_t axis_f16_lds_bytes(int Linp, int Lout16) {
+  const int ldl = Linp + 8;
+  return (size_t)2 * 64 * ldl * 2 + (size_t)2 * Lout16 * ldl * 2 + (size_t)Lout16 * 68 * 4;
+}
+
+template <int NTT>
+__global__ __launch_bounds__(256) void axis_f16_kernel(AxisArgs a) {
+  typedef MM<_Float16> M;
+  constexpr int KS = 32;
+  extern __shared__ __align__(16) unsigned char smem[];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int r16 = lane & 15, g = lane >> 4;
+  const int ldl = a.Linp + 8;
+  _Float16* Ir = reinterpret_cast<_Float16*>(smem);
+  _Float16* Ii = Ir + 64 * ldl;
+  _Float16* Er = Ii + 64 * ldl;
+  _Float16* Ei = Er + NTT * 16 * ldl;
+  uint32_t* Ob = reinterpret_cast<uint32_t*>(Ei + NTT * 16 * ldl);  // [NTT*16][68]
+  const int j0 = blockIdx.x * 64;
+  const int64_t o = blockIdx.y;
+  const _Float16* in = reinterpret_cast<const _Float16*>(a.in) + o * (int64_t)a.Lin * a.inner * 2;
+  _Float16* out = reinterpret_cast<_Float16*>(a.out) + o * (int64_t)a.Lout * a.inner * 2;
+  const _Float16* er = reinterpret_cast<const _Float16*>(a.er);
+  const _Float16* ei = reinterpret_cast<const _Float16*>(a.ei);
+
+  // table: [NTT*16][Linp] twice, 16-byte pieces; data: Linp rows x 16 quads
+  const int tpr = a.Linp / 8;
+  for (int i = tid; i < 2 * NTT * 16 * tpr; i += 256) {
+    const int tab = i / (NTT * 16 * tpr), rem = i - tab * (NTT * 16 * tpr);
+    const int t = rem / tpr, c = (rem - t * tpr) * 8;
+    const h8 v = *reinterpret_cast<const h8*>((tab ? ei : er) + (int64_t)t * a.Linp + c);
+    *reinterpret_cast<h8*>((tab ? Ei : Er) + t * ldl + c) = v;
+  }
+  for (int idx = tid; idx < a.Linp * 16; idx += 256) {
+    const int l = idx >> 4, jj = (idx & 15) * 4;
+    h8 v = M::zero();
+    if (l < a.Lin && j0 + jj < a.inner)
+      v = *reinterpret_cast<const h8*>(in + ((int64_t)l * a.inner + j0 + jj) * 2);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      Ir[(jj + e) * ldl + l] = v[2 * e];
+      Ii[(jj + e) * ldl + l] = v[2 * e + 1];
+    }
+  }
+  __syncthreads();
+  // D[t][j] = sum_l E[t][l] X[l][j]; wave owns columns 16 wave .. + 16
+  f4 accR[NTT], accI[NTT];
+#pragma unroll
+  for (int u = 0; u < NTT; ++u) accR[u] = accI[u] = f4zero();
+  for (int k0 = 0; k0 < a.Linp; k0 += KS) {
+    const h8 br = M::ld(Ir + (wave * 16 + r16) * ldl + k0 + g * 8);
+    const h8 bi = M::ld(Ii + (wave * 16 + r16) * ldl + k0 + g * 8);
+#pragma unroll
+    for (int u = 0; u < NTT; ++u) {
+      const h8 xr = M::ld(Er + (u * 16 + r16) * ldl + k0 + g * 8);
+      const h8 xi = M::ld(Ei + (u * 16 + r16) * ldl + k0 + g * 8);
+      const h8 nxi = M::neg(xi);
+      accR[u] = M::mma(xr, br, accR[u]);
+      accR[u] = M::mma(nxi, bi, accR[u]);
+      accI[u] = M::mma(xr, bi, accI[u]);
+      accI[u] = M::mma(xi, br, accI[u]);
+    }
+  }
+  // D: lane holds rows t = 16 u + 4 g + i, column j = 16 wave + r16
+#pragma unroll
+  for (int u = 0; u < NTT; ++u)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      h2 v = {to_h(accR[u][i] * a.scale), to_h(accI[u][i] * a.scale)};
+      uint32_t w;
+      __builtin_memcpy(&w, &v, 4);
+      Ob[(u * 16 + 4 * g + i) * 68 + wave * 16 + r16] = w;
+    }
+  __syncthreads();
+  // rows t < Lout, 64 complex (256 bytes) each: 16 pieces of 16 bytes
+  for (int i = tid; i < a.Lout * 16; i += 256) {
+    const int t = i >> 4, q = i & 15;
+    if (j0 + 4 * q < a.inner) {
+      const u32x4 v = *reinterpret_cast<const u32x4*>(Ob + t * 68 + 4 * q);
+      *reinterpret_cast<u32x4*>(out + ((int64_t)t * a.inner + j0 + 4 * q) * 2) = v;
+    }
+  }
+}
+
 // ---------------------------------------------------------------------------
 // Per-mode channel contraction (forward and adjoint):
 //   out[b][p][t] = scale c(t) sum_q in[b][q][t] Wop(q, p, t)
@@ -1074,6 +1163,19 @@ hipError_t launch_c2r(int elem, int nct, const C2RArgs& a, size_t lds, hipStream
 
 hipError_t launch_axis(int elem, const AxisArgs& a, size_t lds, hipStream_t s) {
   dim3 grid((unsigned)((a.inner + 63) / 64), (unsigned)a.outer), block(256);
+  if (elem == ELEM_F16 && a.inner % 4 == 0 && a.Linp <= 128 && a.Lout16 <= 128) {
+    const size_t l2 = axis_f16_lds_bytes(a.Linp, a.Lout16);
+    switch (a.Lout16 / 16) {
+#define FNO_AXIS_F16(N)                                                            \
+  case N:                                                                          \
+    FNO_LAUNCH((axis_f16_kernel<N>), grid, block, l2, s, a);                       \
+    return hipGetLastError();
+      FNO_AXIS_F16(1) FNO_AXIS_F16(2) FNO_AXIS_F16(3) FNO_AXIS_F16(4)
+      FNO_AXIS_F16(5) FNO_AXIS_F16(6) FNO_AXIS_F16(7) FNO_AXIS_F16(8)
+#undef FNO_AXIS_F16
+      default: break;
+    }
+  }
   if (elem == ELEM_F16 && a.inner % 4 == 0)
     FNO_LAUNCH((axis_kernel<_Float16, true>), grid, block, lds, s, a);
   else if (elem == ELEM_F16)
