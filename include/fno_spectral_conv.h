@@ -60,10 +60,32 @@ typedef enum {
   FNO_ERR_INTERNAL = 5
 } fno_status;
 
+/* Storage precision, and the pre-activation that FNO_PREACT_DEFAULT selects. */
 typedef enum {
   FNO_PREC_FP32 = 0,        /* fp32 storage and math, no pre-activation        */
   FNO_PREC_FP16_TANH = 1    /* fp16 storage, fp32 accumulation, tanh (Sec. 4.3) */
 } fno_precision;
+
+/* Pre-activation u = f(x) applied to the input before the forward transform
+ * (the stabiliser of Sec. 4.3, and the pre-FFT alternatives compared in
+ * App. B.6); bwd_data multiplies the transformed gradient by f'(x).  Any
+ * choice combines with either storage precision: FP32 with TANH is the
+ * full-precision + tanh ablation of App. B.8, FP16_TANH with NONE the
+ * unstabilised half-precision baseline, and HARD_CLIP with clip = 57344 the
+ * clipping of out-of-range values to the FP8-E5M2 limits (Sec. 4.6,
+ * App. B.11).
+ *   NONE      : f(x) = x
+ *   TANH      : f(x) = tanh(x),  f'(x) = 1 - tanh(x)^2
+ *   HARD_CLIP : f(x) = min(max(x, -clip), clip),  f'(x) = 1 for |x| <= clip,
+ *               0 otherwise (the bound's own point counts as inside)
+ * NaN inputs give NaN in f and f'.  In fp16 storage f(x) is rounded once to
+ * fp16 before the transform. */
+typedef enum {
+  FNO_PREACT_DEFAULT = 0,   /* TANH for FNO_PREC_FP16_TANH, NONE for FNO_PREC_FP32 */
+  FNO_PREACT_NONE = 1,
+  FNO_PREACT_TANH = 2,
+  FNO_PREACT_HARD_CLIP = 3
+} fno_preactivation;
 
 /* Spectral weight parameterisation: dense, Tucker (the tensorised FNO of
  * Sec. 2) or CP (canonical polyadic, the factorisation of the Navier-Stokes
@@ -92,7 +114,9 @@ typedef enum {
  * the last axis keeps K_d = m_d slots (1 <= m_d <= N_d/2 + 1).  Retained slot
  * t on a leading axis is FFT index k = t for t < m, k = N - 2m + t otherwise.
  * rank = (r_in, r_out, r_1..r_d) for Tucker weights, rank[0] = R for CP
- * weights, ignored for dense. */
+ * weights, ignored for dense.  preact: fno_preactivation (0 = the precision's
+ * default); clip: the HARD_CLIP bound, positive and finite (at most 65504 in
+ * fp16 storage), ignored otherwise; FNO_ERR_INVALID_ARGUMENT when out of range. */
 typedef struct {
   int32_t ndim;          /* 1, 2 or 3                      */
   int32_t precision;     /* fno_precision                  */
@@ -104,6 +128,8 @@ typedef struct {
   int64_t n[3];
   int64_t modes[3];
   int64_t rank[5];
+  int32_t preact;        /* fno_preactivation              */
+  float clip;            /* bound of FNO_PREACT_HARD_CLIP  */
 } fno_conv_desc;
 
 /* Spectral weights R (device pointers, element type of the precision mode).
@@ -147,7 +173,7 @@ fno_status fno_spectral_conv_workspace_size_nocache(const fno_conv_desc *desc,
 
 /* Bytes of one spectral cache: the truncated spectrum [batch, channels, K...]
  * of the precision's element type.  `which` is 0 for the input spectrum
- * Xhat = (1/N) sum_x tanh(x) e^{-i theta} (c_in channels) and 1 for the
+ * Xhat = (1/N) sum_x f(x) e^{-i theta} (c_in channels, f the pre-activation) and 1 for the
  * gradient spectrum (1/sqrt(N)) sum_x gy e^{-i theta} (c_out channels).  The
  * contents are produced and consumed by this library only. */
 fno_status fno_spectrum_bytes(const fno_conv_desc *desc, int which, size_t *bytes);
@@ -164,8 +190,8 @@ fno_status fno_spectral_conv_fwd(const fno_conv_desc *desc, const void *x,
 
 /* Data gradient: gx[batch, c_in, N...] from gy[batch, c_out, N...]:
  * G = c(k) sum_x gy e^{-i theta}, gXhat = sum_o G conj(W),
- * gx = (1/N) sum_t Re(gXhat e^{+i theta}) * (1 - tanh(x)^2) (tanh mode; x is
- * read only then and may be NULL in FNO_PREC_FP32).
+ * gx = (1/N) sum_t Re(gXhat e^{+i theta}) * f'(x) with f the pre-activation
+ * (x is read only for f' and may be NULL when the pre-activation is NONE).
  * gy_hat_out: optional spectral cache (gradient spectrum) for bwd_weight. */
 fno_status fno_spectral_conv_bwd_data(const fno_conv_desc *desc, const void *x,
                                       const fno_weights *w, const void *gy, void *gx,

@@ -21,9 +21,11 @@ Mixed-Precision Neural Operators", ICLR 2024):
   Tucker-factorised (the tensorised FNO of Sec. 2; Kolda-Bader mode products)
   or CP-factorised (the factorisation of the Navier-Stokes and Darcy runs,
   Sec. 4.6).
-* tanh pre-activation before the forward transform in half-precision mode
-  (Sec. 4.3); the full-precision mode has no pre-activation (App. B.8 uses
-  tanh only as an ablation).
+* A pre-activation u = f(x) before the forward transform: tanh in
+  half-precision mode (Sec. 4.3), none in full precision; as variants, tanh in
+  full precision (the ablation of App. B.8), none in half precision (the
+  unstabilised baseline) and the hard clip to [-c, c] of the pre-FFT
+  comparison (App. B.6; with c = 57344 the FP8-E5M2 clipping of Sec. 4.6).
 * The inverse takes y = sum_t c(k_d) Re(Yhat_t e^{+i theta}) with c = 1 on the
   k_d = 0 and Nyquist planes and 2 elsewhere, and no 1/N.
 * The Tucker and CP contractions are split into two-operand steps in the
@@ -44,8 +46,35 @@ from typing import Dict, List, Optional, Sequence, Tuple
 
 import numpy as np
 
-PREC_FP32 = "fp32"
-PREC_FP16_TANH = "fp16_tanh"
+# A mode names the storage precision and the pre-activation f.  The storage
+# precision does not change this module's arithmetic (it works on the stored
+# values in float64); it only names which library mode a result stands for.
+PREC_FP32 = "fp32"            # f(x) = x
+PREC_FP16_TANH = "fp16_tanh"  # f(x) = tanh(x)
+PREC_FP32_TANH = "fp32_tanh"  # f(x) = tanh(x)
+PREC_FP16 = "fp16"            # f(x) = x
+# "fp16_clip:<c>" / "fp32_clip:<c>": f(x) = min(max(x, -c), c), built by clip_mode
+
+
+def clip_mode(storage: str, c: float) -> str:
+    """Mode string of the hard clip to [-c, c] with the given storage."""
+    if storage not in ("fp16", "fp32"):
+        raise ValueError(storage)
+    return f"{storage}_clip:{float(c)!r}"
+
+
+def preact_kind(precision: str) -> Tuple[str, Optional[float]]:
+    """("none" | "tanh" | "clip", the clip bound or None) of a mode."""
+    if precision in (PREC_FP32, PREC_FP16):
+        return "none", None
+    if precision in (PREC_FP16_TANH, PREC_FP32_TANH):
+        return "tanh", None
+    if isinstance(precision, str) and precision.split(":")[0] in ("fp16_clip", "fp32_clip"):
+        c = float(precision.split(":", 1)[1])
+        if not (c > 0.0 and np.isfinite(c)):
+            raise ValueError(precision)
+        return "clip", c
+    raise ValueError(precision)
 
 POLICY_MIN_RESULT = "min_result"
 POLICY_MIN_NET = "min_net"
@@ -105,13 +134,29 @@ def _apply_axis(a: np.ndarray, mat: np.ndarray, axis: int) -> np.ndarray:
 
 
 def preactivation(x: np.ndarray, precision: str) -> np.ndarray:
-    """u = tanh(x) in half-precision mode (Sec. 4.3), u = x in full precision."""
+    """u = f(x): tanh (Sec. 4.3), the identity, or the hard clip that moves
+    every value outside [-c, c] to the nearer bound (App. B.6).  NaN stays NaN."""
     xf = np.asarray(x, dtype=np.float64)
-    if precision == PREC_FP16_TANH:
+    kind, c = preact_kind(precision)
+    if kind == "tanh":
         return np.tanh(xf)
-    if precision == PREC_FP32:
-        return xf
-    raise ValueError(precision)
+    if kind == "clip":
+        return np.where(np.abs(xf) > c, np.copysign(c, xf), xf)
+    return xf
+
+
+def preactivation_grad(x: np.ndarray, precision: str) -> Optional[np.ndarray]:
+    """f'(x), or None for the identity.  tanh: 1 - tanh(x)^2.  Hard clip: 1
+    where |x| <= c (a value on the bound counts as inside, as for a clamp whose
+    gradient passes at its limits), 0 beyond, NaN where x is NaN."""
+    xf = np.asarray(x, dtype=np.float64)
+    kind, c = preact_kind(precision)
+    if kind == "tanh":
+        t = np.tanh(xf)
+        return 1.0 - t * t
+    if kind == "clip":
+        return np.where(np.isnan(xf), np.nan, np.where(np.abs(xf) <= c, 1.0, 0.0))
+    return None
 
 
 def forward_spectrum(u: np.ndarray, n: Sequence[int], modes: Sequence[int]) -> np.ndarray:
@@ -172,14 +217,12 @@ def grad_spectrum(gy, n, modes) -> np.ndarray:
 
 def bwd_data(x, w, gy, n, modes, precision):
     """gx: G -> gXhat = sum_o G conj(W) -> gu = (1/N) sum_t Re(gXhat e^{+i theta})
-    -> gx = gu (1 - tanh(x)^2) in half-precision mode."""
+    -> gx = gu f'(x) (the chain rule through the pre-activation)."""
     g = grad_spectrum(gy, n, modes)
     gxh = np.einsum("bo...,io...->bi...", g, np.conj(w))
     gu = inverse_spectrum(gxh, n, modes, with_c=False) / float(np.prod(n))
-    if precision == PREC_FP16_TANH:
-        t = np.tanh(np.asarray(x, dtype=np.float64))
-        return gu * (1.0 - t * t)
-    return gu
+    fp = preactivation_grad(x, precision)
+    return gu if fp is None else gu * fp
 
 
 def bwd_weight(x, gy, n, modes, precision):
@@ -361,10 +404,8 @@ def tucker_bwd_data(x, core, u_in, u_out, u_mode, gy, n, modes, precision,
     g = grad_spectrum(gy, n, modes)
     gxh = tucker_contract(g, core, u_in, u_out, u_mode, n, modes, policy, adjoint=True)
     gu = inverse_spectrum(gxh, n, modes, with_c=False) / float(np.prod(n))
-    if precision == PREC_FP16_TANH:
-        t = np.tanh(np.asarray(x, dtype=np.float64))
-        return gu * (1.0 - t * t)
-    return gu
+    fp = preactivation_grad(x, precision)
+    return gu if fp is None else gu * fp
 
 
 def tucker_bwd_weight(x, gy, core, u_in, u_out, u_mode, n, modes, precision):
@@ -467,10 +508,8 @@ def cp_bwd_data(x, lam, u_in, u_out, u_mode, gy, n, modes, precision,
     g = grad_spectrum(gy, n, modes)
     gxh = cp_contract(g, lam, u_in, u_out, u_mode, policy, adjoint=True)
     gu = inverse_spectrum(gxh, n, modes, with_c=False) / float(np.prod(n))
-    if precision == PREC_FP16_TANH:
-        t = np.tanh(np.asarray(x, dtype=np.float64))
-        return gu * (1.0 - t * t)
-    return gu
+    fp = preactivation_grad(x, precision)
+    return gu if fp is None else gu * fp
 
 
 def cp_bwd_weight(x, gy, lam, u_in, u_out, u_mode, n, modes, precision):

@@ -23,6 +23,10 @@ FNO_ERR_INTERNAL = 5
 
 FNO_PREC_FP32 = 0
 FNO_PREC_FP16_TANH = 1
+FNO_PREACT_DEFAULT = 0
+FNO_PREACT_NONE = 1
+FNO_PREACT_TANH = 2
+FNO_PREACT_HARD_CLIP = 3
 FNO_WEIGHT_DENSE = 0
 FNO_WEIGHT_TUCKER = 1
 FNO_WEIGHT_CP = 2
@@ -58,6 +62,8 @@ class FnoConvDesc(ctypes.Structure):
         ("n", ctypes.c_int64 * 3),
         ("modes", ctypes.c_int64 * 3),
         ("rank", ctypes.c_int64 * 5),
+        ("preact", ctypes.c_int32),
+        ("clip", ctypes.c_float),
     ]
 
 
@@ -151,12 +157,15 @@ def _check(status: int, where: str) -> None:
 def make_desc(n: Sequence[int], modes: Sequence[int], batch: int, c_in: int, c_out: int,
               precision: int = FNO_PREC_FP16_TANH, weight_kind: int = FNO_WEIGHT_DENSE,
               rank: Optional[Sequence[int]] = None,
-              path_policy: int = FNO_PATH_MIN_RESULT) -> FnoConvDesc:
+              path_policy: int = FNO_PATH_MIN_RESULT, preact: int = FNO_PREACT_DEFAULT,
+              clip: float = 0.0) -> FnoConvDesc:
     d = FnoConvDesc()
     d.ndim = len(n)
     d.precision = precision
     d.weight_kind = weight_kind
     d.path_policy = path_policy
+    d.preact = preact
+    d.clip = clip
     d.batch, d.c_in, d.c_out = batch, c_in, c_out
     for j, v in enumerate(n):
         d.n[j] = int(v)

@@ -128,7 +128,7 @@ struct Pos {
 // values (rt = 0, 1; i = 0..3) as the B operand of one k-step; the leading-
 // axis table column 32 j + 8 g + e holds the matching row n_a.
 // ---------------------------------------------------------------------------
-template <int NKA, int NTB, int NTA, bool TANH>
+template <int NKA, int NTB, int NTA, bool PRE>
 __global__ __launch_bounds__(CH_NW * 64, 2) void r2c_chain_kernel(R2CArgs a) {
   constexpr int NCT = 2 * NTB;
   constexpr int LDT = NKA * KS + PADH;
@@ -140,7 +140,7 @@ __global__ __launch_bounds__(CH_NW * 64, 2) void r2c_chain_kernel(R2CArgs a) {
   const int LDE = a.NaC + PADH;
   // the lookup table is a static LDS array (at a known address, so lookups
   // need no base add); the twiddle tables are dynamic LDS after it
-  __shared__ __align__(16) _Float16 sLut[TANH ? LUT_HALVES : 8];  // tanh of each fp16 code
+  __shared__ __align__(16) _Float16 sLut[PRE ? LUT_HALVES : 8];  // f(x) of each fp16 code
   _Float16* sT = reinterpret_cast<_Float16*>(smem);    // [NCT * 16][LDT]
   _Float16* sEc = sT + NCT * 16 * LDT;                // [NTA * 16][LDE]
   _Float16* sEs = sEc + NTA * 16 * LDE;
@@ -153,7 +153,7 @@ __global__ __launch_bounds__(CH_NW * 64, 2) void r2c_chain_kernel(R2CArgs a) {
   constexpr int PE = (NTA * 16 * 16 + CH_NW * 64 - 1) / (CH_NW * 64);
   Stager<PT> st;
   Stager<PE> sc, ss;
-  Stager<TANH ? LUT_HALVES / 8 / (CH_NW * 64) : 1> sl;
+  Stager<PRE ? LUT_HALVES / 8 / (CH_NW * 64) : 1> sl;
 
   const int NJ = a.NaC / 32;
   const int64_t plane = (int64_t)a.Na * a.Nb;
@@ -200,8 +200,9 @@ __global__ __launch_bounds__(CH_NW * 64, 2) void r2c_chain_kernel(R2CArgs a) {
 #pragma unroll
     for (int s = 0; s < NKA; ++s) {
       h8 v0, v1;
-      if constexpr (TANH) {
-        // tanh rounded to fp16, looked up per fp16 code
+      if constexpr (PRE) {
+        // the pre-activation f (odd: tanh or the hard clip) rounded to fp16,
+        // looked up per fp16 code
         v0 = u_as_h8(lut_u4<true>(sLut, buf[0][s]));
         v1 = u_as_h8(lut_u4<true>(sLut, buf[1][s]));
       } else {
@@ -312,12 +313,12 @@ __global__ __launch_bounds__(CH_NW * 64, 2) void r2c_chain_kernel(R2CArgs a) {
   st.load(reinterpret_cast<const _Float16*>(a.twAc), a.Nbp, NCT * 16, NKA * KS, zr);
   sc.load(reinterpret_cast<const _Float16*>(a.cBc), a.NaC, NTA * 16, a.NaC, zr);
   ss.load(reinterpret_cast<const _Float16*>(a.sBc), a.NaC, NTA * 16, a.NaC, zr);
-  if constexpr (TANH) sl.load(reinterpret_cast<const _Float16*>(a.lut), 0, 1, LUT_HALVES, zr);
+  if constexpr (PRE) sl.load(reinterpret_cast<const _Float16*>(a.lut), 0, 1, LUT_HALVES, zr);
   __builtin_amdgcn_sched_barrier(0);
   st.store(sT, LDT, NCT * 16, NKA * KS);
   sc.store(sEc, LDE, NTA * 16, a.NaC);
   ss.store(sEs, LDE, NTA * 16, a.NaC);
-  if constexpr (TANH) sl.store(sLut, 0, 1, LUT_HALVES);
+  if constexpr (PRE) sl.store(sLut, 0, 1, LUT_HALVES);
   __syncthreads();  // tables staged
   load(q1, b1);
   int64_t it = 0;
@@ -341,7 +342,8 @@ __global__ __launch_bounds__(CH_NW * 64, 2) void r2c_chain_kernel(R2CArgs a) {
 
 // ---------------------------------------------------------------------------
 // Inverse.  Template: NG = Nb64 / 64 output column groups, NTB = Kbp / 16,
-// NKZ = Kap / 32 k-steps of step B'.  EPI multiplies by 1 - tanh(x)^2.
+// NKZ = Kap / 32 k-steps of step B'.  EPI multiplies by f'(x), the
+// derivative of the pre-activation.
 //
 // Step B' for one 16-row output tile computes V^T[t_b][n_a] (complex) with
 // Z^T as the A operand (gathered from global memory, k = t_a) and the
@@ -363,7 +365,7 @@ __global__ __launch_bounds__(CH_NW * 64, 2) void c2r_chain_kernel(C2RArgs a) {
   const int LDK = a.Kap + PADH;
   const int NAT = (a.Na + 15) / 16;
   // static LDS lookup table (see the forward kernel), dynamic tables after
-  __shared__ __align__(16) _Float16 sLut[EPI ? LUT_HALVES : 8];  // 1 - tanh^2 per fp16 code
+  __shared__ __align__(16) _Float16 sLut[EPI ? LUT_HALVES : 8];  // f'(x) per fp16 code
   _Float16* sTI = reinterpret_cast<_Float16*>(smem);   // [NG * 64][LDI]
   _Float16* sCI = sTI + NG * 64 * LDI;                 // [NAT * 16][LDK]
   _Float16* sSI = sCI + NAT * 16 * LDK;
@@ -524,7 +526,7 @@ __global__ __launch_bounds__(CH_NW * 64, 2) void c2r_chain_kernel(C2RArgs a) {
 #pragma unroll
         for (int i = 0; i < 4; ++i) v[4 * tq + i] = yacc[4 * G + tq][i] * a.scale;
       if constexpr (EPI) {
-        // 1 - tanh(x)^2, rounded to fp16, looked up per fp16 code
+        // f'(x) (even), rounded to fp16, looked up per fp16 code
 #pragma unroll
         for (int h = 0; h < 2; ++h) {
           const h8 fv = u_as_h8(lut_u4<false>(sLut, xb[G][h]));
@@ -613,15 +615,15 @@ __global__ __launch_bounds__(CH_NW * 64, 2) void c2r_chain_kernel(C2RArgs a) {
 // Dispatch
 // ---------------------------------------------------------------------------
 // Dynamic LDS bytes; the lookup table (64 KiB when used) is static LDS.
-size_t r2c_chain_lds_bytes(int nka, int ntb, int nta, int NaC, bool tanh_lut) {
-  (void)tanh_lut;
+size_t r2c_chain_lds_bytes(int nka, int ntb, int nta, int NaC, bool pre_lut) {
+  (void)pre_lut;
   return sizeof(_Float16) * ((size_t)2 * ntb * 16 * (nka * KS + PADH) +
                              (size_t)2 * nta * 16 * (NaC + PADH));
 }
 
-size_t c2r_chain_lds_bytes(int ng, int ntb, int Kap, int Na, bool sech2_lut) {
+size_t c2r_chain_lds_bytes(int ng, int ntb, int Kap, int Na, bool grad_lut) {
   const int nat = (Na + 15) / 16;
-  (void)sech2_lut;
+  (void)grad_lut;
   return sizeof(_Float16) * ((size_t)ng * 64 * (2 * ntb * 16 + PADH) +
                              (size_t)2 * nat * 16 * (Kap + PADH) +
                              (size_t)CH_NW * 16 * (64 + PADH));

@@ -81,6 +81,24 @@ __device__ __forceinline__ float tanh_f32(float x) {
   return ax < 0.0625f ? small : __builtin_copysignf(big, x);
 }
 
+// Pre-activation u = f(x) of the arithmetic (table-free) kernels and its
+// derivative f'(x) for the data gradient.  act 1: tanh, f' = 1 - tanh^2;
+// act 2: the hard clip to [-clip, clip], f' = 1 for |x| <= clip and 0
+// beyond.  NaN stays NaN in both (the clip's comparisons are false for it).
+__device__ __forceinline__ float preact_f32(float x, int act, float clip) {
+  if (act == 2) return __builtin_fabsf(x) > clip ? __builtin_copysignf(clip, x) : x;
+  return tanh_f32(x);
+}
+
+__device__ __forceinline__ float preact_grad_f32(float x, int act, float clip) {
+  if (act == 2) {
+    const float ax = __builtin_fabsf(x);
+    return ax <= clip ? 1.0f : (ax > clip ? 0.0f : x);
+  }
+  const float t = tanh_f32(x);
+  return 1.0f - t * t;
+}
+
 // Round-to-nearest-even conversions to the storage type.
 __device__ __forceinline__ _Float16 to_h(float v) { return (_Float16)v; }
 
@@ -122,16 +140,18 @@ __device__ __forceinline__ void wave_lds_sync() {
 }
 
 // ---------------------------------------------------------------------------
-// Input fragment of step A: KPL consecutive row elements, optional tanh.
+// Input fragment of step A: KPL consecutive row elements, optional
+// pre-activation (act as for preact_f32, 0: none).
 // ---------------------------------------------------------------------------
 template <typename T>
 __device__ __forceinline__ typename MM<T>::frag load_row_frag(const T* row, int n0, int Nb,
-                                                              bool vrow, int do_tanh,
-                                                              int vec);
+                                                              bool vrow, int act,
+                                                              float clip, int vec);
 
 template <>
 __device__ __forceinline__ h8 load_row_frag<_Float16>(const _Float16* row, int n0, int Nb,
-                                                      bool vrow, int do_tanh, int vec) {
+                                                      bool vrow, int act, float clip,
+                                                      int vec) {
   h8 v = MM<_Float16>::zero();
   if (vrow) {
     if (vec) {
@@ -141,9 +161,9 @@ __device__ __forceinline__ h8 load_row_frag<_Float16>(const _Float16* row, int n
       for (int i = 0; i < 8; ++i)
         if (n0 + i < Nb) v[i] = row[n0 + i];
     }
-    if (do_tanh) {
+    if (act) {
 #pragma unroll
-      for (int i = 0; i < 8; ++i) v[i] = to_h(tanh_f32((float)v[i]));
+      for (int i = 0; i < 8; ++i) v[i] = to_h(preact_f32((float)v[i], act, clip));
     }
   }
   return v;
@@ -151,11 +171,12 @@ __device__ __forceinline__ h8 load_row_frag<_Float16>(const _Float16* row, int n
 
 template <>
 __device__ __forceinline__ float load_row_frag<float>(const float* row, int n0, int Nb,
-                                                      bool vrow, int do_tanh, int vec) {
+                                                      bool vrow, int act, float clip,
+                                                      int vec) {
   float v = 0.0f;
   if (vrow && n0 < Nb) {
     v = row[n0];
-    if (do_tanh) v = tanh_f32(v);
+    if (act) v = preact_f32(v, act, clip);
   }
   return v;
 }

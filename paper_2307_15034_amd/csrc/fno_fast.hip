@@ -112,9 +112,9 @@ __global__ __launch_bounds__(NW * 64, 2) void r2c_fast_kernel(R2CArgs a) {
 #pragma unroll
       for (int s = 0; s < NKA; ++s) {
         h8 v = as_h8(cur[s]);
-        if (a.do_tanh) {
+        if (a.act) {
 #pragma unroll
-          for (int i = 0; i < 8; ++i) v[i] = to_h(tanh_f32((float)v[i]));
+          for (int i = 0; i < 8; ++i) v[i] = to_h(preact_f32((float)v[i], a.act, a.clip));
         }
 #pragma unroll
         for (int ct = 0; ct < NCT; ++ct) {
@@ -185,7 +185,7 @@ __global__ __launch_bounds__(NW * 64, 2) void r2c_fast_kernel(R2CArgs a) {
 // ---------------------------------------------------------------------------
 // Inverse: spectrum [Ka][Kb] -> plane [Na][Nb]; one wave per 16-row tile
 // (Na <= 16*NW), Nb <= 64*NBT, Ka <= 32*NKZ, Kb <= 8*NCT.  EPI multiplies by
-// 1 - tanh(x)^2.
+// the pre-activation's derivative f'(x).
 // ---------------------------------------------------------------------------
 template <int NCT, int NW, int NBT, int NKZ, bool EPI>
 __global__ __launch_bounds__(NW * 64, 2) void c2r_fast_kernel(C2RArgs a) {
@@ -344,10 +344,7 @@ __global__ __launch_bounds__(NW * 64, 2) void c2r_fast_kernel(C2RArgs a) {
         for (int h = 0; h < 2; ++h) {
           h8 xv = as_h8(xc[c][h]);
 #pragma unroll
-          for (int e = 0; e < 8; ++e) {
-            const float t = tanh_f32((float)xv[e]);
-            v[8 * h + e] *= (1.0f - t * t);
-          }
+          for (int e = 0; e < 8; ++e) v[8 * h + e] *= preact_grad_f32((float)xv[e], a.act, a.clip);
         }
       }
       const int n_a = wave * 16 + orow, n_b = c * 64 + ocol;

@@ -8,6 +8,8 @@
 namespace fno {
 
 enum Elem { ELEM_F32 = 0, ELEM_F16 = 1 };
+// Pre-activation of a plan (the `act` codes of the kernel arguments).
+enum Act { ACT_NONE = 0, ACT_TANH = 1, ACT_CLIP = 2 };
 
 // Truncated real-to-complex transform of the last two axes of every plane
 // [planes][Na][Nb] -> spectrum [planes][Ka][Kb] (complex).  Step A runs the
@@ -28,20 +30,22 @@ struct R2CArgs {
   int Kap16;        // Ka padded to 16
   int R;            // rows per chunk (multiple of 32)
   float scaleA, scaleB;
-  int do_tanh;
+  int do_tanh;      // 1 if the pre-activation u = f(x) is applied (any act)
+  int act;          // arithmetic kernels: 0 none, 1 tanh, 2 hard clip to [-clip, clip]
+  float clip;
   int vec;          // 1 if Nb allows 16-byte row loads
   // chained fast path (fp16): permuted copies of the tables
   const void* twAc; // [2*Kbp][Nbp]: row 16 ct + r: part ct / (Kbp/16) of t = (Kbp/16) r + ct % (Kbp/16)
   const void* cBc;  // [Kap16][NaC]: column 32 j + 8 q + e holds row n = 32 j + 4 q + e (e < 4)
   const void* sBc;  //   or 32 j + 16 + 4 q + e - 4 (e >= 4)
   int NaC;          // Na padded to 32
-  const void* lut;  // fp16 tanh of every non-negative fp16 code (32768 entries)
-  int lut_sat;      // first code from which tanh stays at its +inf value
+  const void* lut;  // fp16 f(x) of every non-negative fp16 code (32768 entries; f odd)
+  int lut_sat;      // first code from which f stays at its +inf value
 };
 
 // Inverse of the above: spectrum [planes][Ka][Kb] -> y [planes][Na][Nb],
 // y = scale * sum_t Re(Z e^{+i theta}) (no multiplicity), optional epilogue
-// y *= 1 - tanh(x)^2.
+// y *= f'(x), the derivative of the pre-activation.
 struct C2RArgs {
   const void* in;
   void* out;
@@ -56,7 +60,9 @@ struct C2RArgs {
   int Nap;          // Na padded to a multiple of R
   int R;            // rows per chunk (multiple of 64)
   float scale;
-  int epilogue;     // 0: none, 1: multiply by 1 - tanh(x)^2
+  int epilogue;     // 0: none, 1: multiply by f'(x)
+  int act;          // arithmetic kernels: 1 tanh, 2 hard clip to [-clip, clip]
+  float clip;
   int vec;
   // chained fast path (fp16): [Nb64][2*Kbp], row 16 T + R holds column
   // n = 64 (T/4) + 16 (R/4) + 4 (T%4) + R%4; column 32 ks + 8 q + e holds
@@ -64,8 +70,8 @@ struct C2RArgs {
   const void* twIc;
   const void* cIc;  // [Nap][Kap] like cI, sI with column 32 ks + 8 q + e holding
   const void* sIc;  //   t = 32 ks + 4 q + e (e < 4) or 32 ks + 16 + 4 q + e - 4
-  const void* lut;  // fp16 1 - tanh^2 of every non-negative fp16 code (32768 entries)
-  int lut_sat;      // first code from which 1 - tanh^2 stays at its +inf value
+  const void* lut;  // fp16 f'(x) of every non-negative fp16 code (32768 entries; f' even)
+  int lut_sat;      // first code from which f' stays at its +inf value
 };
 
 // Complex DFT along a middle axis: in [outer][Lin][inner] -> out
@@ -171,7 +177,7 @@ hipError_t launch_contract(int elem, const ContractArgs& a, hipStream_t s);
 hipError_t launch_wgrad(int elem, const WgradArgs& a, hipStream_t s);
 hipError_t launch_pair(const PairArgs& a, hipStream_t s);
 hipError_t launch_pair_gemm(const PairArgs& a, hipStream_t s);
-size_t r2c_wide_lds_bytes(int nct, bool tanh, int lut_sat);
+size_t r2c_wide_lds_bytes(int nct, bool pre, int lut_sat);
 size_t c2r_wide_lds_bytes(int nct, int Kap, bool epi, int lut_sat);
 hipError_t launch_r2c_wide(const R2CArgs& a, int nct, int grid, size_t lds, hipStream_t s);
 hipError_t launch_c2r_wide(const C2RArgs& a, int nct, int grid, size_t lds, hipStream_t s);
@@ -197,8 +203,8 @@ hipError_t launch_c2r_chain(const C2RArgs& a, int ng, int ntb, int nkz, int grid
 bool r2c_chain_has(int nka, int ntb, int nta);
 bool c2r_chain_has(int ng, int ntb, int nkz);
 // dynamic LDS only; a lookup table adds 64 KiB of static LDS
-size_t r2c_chain_lds_bytes(int nka, int ntb, int nta, int NaC, bool tanh_lut);
-size_t c2r_chain_lds_bytes(int ng, int ntb, int Kap, int Na, bool sech2_lut);
+size_t r2c_chain_lds_bytes(int nka, int ntb, int nta, int NaC, bool pre_lut);
+size_t c2r_chain_lds_bytes(int ng, int ntb, int Kap, int Na, bool grad_lut);
 constexpr int kChainWaves = 8;  // waves per work-group of the chained kernels
 
 // fp16 contraction / weight gradient on slabs of 16 modes (K % 16 == 0);

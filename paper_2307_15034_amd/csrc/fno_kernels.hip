@@ -77,7 +77,8 @@ __global__ __launch_bounds__(256) void r2c_plane_kernel(R2CArgs a) {
 #pragma unroll
         for (int u = 0; u < R2C_NRT; ++u)
           if (rt0 + 4 * u < nrt)
-            af[u] = load_row_frag<T>(rp[u], k0 + g * KPL, a.Nb, vrow[u], a.do_tanh, a.vec);
+            af[u] = load_row_frag<T>(rp[u], k0 + g * KPL, a.Nb, vrow[u], a.act, a.clip,
+                                    a.vec);
 #pragma unroll
         for (int ct = 0; ct < NCT; ++ct) {
           frag bf = M::ld(twA + (int64_t)(ct * 16 + r16) * a.Nbp + k0 + g * KPL);
@@ -359,10 +360,7 @@ __global__ __launch_bounds__(256) void c2r_plane_kernel(C2RArgs a) {
               float xv[16];
               load16<T>(xin + off, xv, nval, a.vec);
 #pragma unroll
-              for (int i = 0; i < 16; ++i) {
-                const float t = tanh_f32(xv[i]);
-                v[i] *= (1.0f - t * t);
-              }
+              for (int i = 0; i < 16; ++i) v[i] *= preact_grad_f32(xv[i], a.act, a.clip);
             }
             store16<T>(yout + off, v, nval, a.vec);
           }

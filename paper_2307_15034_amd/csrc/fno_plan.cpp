@@ -36,11 +36,27 @@ fno_status hip_fail(hipError_t e, const char* what) {
   return FNO_ERR_HIP;
 }
 
+int act_of(const fno_conv_desc* d) {
+  switch (d->preact) {
+    case FNO_PREACT_NONE: return ACT_NONE;
+    case FNO_PREACT_TANH: return ACT_TANH;
+    case FNO_PREACT_HARD_CLIP: return ACT_CLIP;
+    default: return d->precision == FNO_PREC_FP16_TANH ? ACT_TANH : ACT_NONE;
+  }
+}
+
 fno_status check_desc(const fno_conv_desc* d) {
   if (!d) return FNO_ERR_INVALID_ARGUMENT;
   if (d->ndim < 1 || d->ndim > 3) return FNO_ERR_INVALID_ARGUMENT;
   if (d->precision != FNO_PREC_FP32 && d->precision != FNO_PREC_FP16_TANH)
     return FNO_ERR_INVALID_ARGUMENT;
+  if (d->preact < FNO_PREACT_DEFAULT || d->preact > FNO_PREACT_HARD_CLIP)
+    return FNO_ERR_INVALID_ARGUMENT;
+  if (d->preact == FNO_PREACT_HARD_CLIP) {
+    // a positive finite bound, one that fp16 storage can hold in fp16 mode
+    const float lim = d->precision == FNO_PREC_FP16_TANH ? 65504.0f : 3.4028235e38f;
+    if (!(d->clip > 0.0f && d->clip <= lim)) return FNO_ERR_INVALID_ARGUMENT;
+  }
   if (d->weight_kind != FNO_WEIGHT_DENSE && d->weight_kind != FNO_WEIGHT_TUCKER &&
       d->weight_kind != FNO_WEIGHT_CP)
     return FNO_ERR_INVALID_ARGUMENT;
@@ -297,6 +313,8 @@ struct Geo {
   int nd;
   int elem;          // ELEM_F16 / ELEM_F32
   int es;            // element bytes
+  int act;           // pre-activation: ACT_NONE / ACT_TANH / ACT_CLIP
+  float clip;        // bound of ACT_CLIP
   int64_t B, Cin, Cout;
   int64_t N;         // prod n
   int64_t K;         // prod K_j
@@ -316,8 +334,8 @@ struct DevTables {
   size_t bytes = 0;
   const void *zeros, *twA, *cB, *sB, *cI, *sI, *twI;
   const void *twAc, *cBc, *sBc, *twIc, *cIc, *sIc;
-  const void *lutTanh, *lutSech2;
-  int tanhSat = 0, sech2Sat = 0;  // first codes of the saturated tails (fp16 plans)
+  const void *lutAct, *lutGrad;
+  int actSat = 0, gradSat = 0;  // first codes of the saturated tails (fp16 plans)
   const void *eFr, *eFi, *eIr, *eIi;
 };
 
@@ -336,6 +354,8 @@ Geo make_geo(const fno_conv_desc* d) {
   g.nd = d->ndim;
   g.elem = d->precision == FNO_PREC_FP16_TANH ? ELEM_F16 : ELEM_F32;
   g.es = g.elem == ELEM_F16 ? 2 : 4;
+  g.act = act_of(d);
+  g.clip = g.act == ACT_CLIP ? d->clip : 0.0f;
   g.B = d->batch;
   g.Cin = d->c_in;
   g.Cout = d->c_out;
@@ -505,20 +525,33 @@ void fill_tables(const fno_conv_desc* d, const Geo& g, std::vector<T>& buf,
       buf[oicc + (size_t)n * g.Kap + col] = (T)c;
       buf[oics + (size_t)n * g.Kap + col] = (T)s;
     }
-  // Lookup tables over the non-negative fp16 codes 0..0x7fff: tanh and
-  // sech^2 = 1 - tanh^2 of the fp16 value, each rounded once to the storage
-  // type (NaN codes give NaN, +inf gives 1 and 0).
+  // Lookup tables over the non-negative fp16 codes 0..0x7fff: the
+  // pre-activation f and its derivative f' of the fp16 value, each rounded
+  // once to the storage type.  tanh: f = tanh, f' = sech^2 = 1 - tanh^2
+  // (+inf gives 1 and 0); hard clip: f = min(x, clip), f' = 1 up to clip and
+  // 0 beyond.  NaN codes give NaN in both.  f is odd and f' even, so the
+  // kernels look up |x| and restore the sign of f.
   size_t olt = alloc(32768);
   size_t ols = alloc(32768);
+  const double cb = (double)g.clip;
   for (int code = 0; code < 32768; ++code) {
     const uint16_t bits = (uint16_t)code;
     _Float16 h;
     std::memcpy(&h, &bits, 2);
     const double xv = (double)h;
-    const double th = std::tanh(xv);
-    const double ch = std::cosh(xv);
-    buf[olt + code] = (T)th;
-    buf[ols + code] = (T)(1.0 / (ch * ch));
+    double f, fp;
+    if (std::isnan(xv)) {
+      f = fp = xv;
+    } else if (g.act == ACT_CLIP) {
+      f = xv > cb ? cb : xv;
+      fp = xv <= cb ? 1.0 : 0.0;
+    } else {
+      const double ch = std::cosh(xv);
+      f = std::tanh(xv);
+      fp = 1.0 / (ch * ch);
+    }
+    buf[olt + code] = (T)f;
+    buf[ols + code] = (T)fp;
   }
   (void)o;
   (void)oc;
@@ -574,6 +607,13 @@ PlanKey key_of(const fno_conv_desc* d, int device) {
   if (d->weight_kind == FNO_WEIGHT_TUCKER)
     for (int j = 0; j < 2 + d->ndim; ++j) k.v[14 + j] = d->rank[j];
   if (d->weight_kind == FNO_WEIGHT_CP) k.v[14] = d->rank[0];
+  const int act = act_of(d);
+  k.v[19] = act;
+  if (act == ACT_CLIP) {
+    uint32_t bits;
+    std::memcpy(&bits, &d->clip, 4);
+    k.v[20] = bits;
+  }
   return k;
 }
 
@@ -600,8 +640,8 @@ fno_status build_tables(const fno_conv_desc* d, Plan* pl) {
       }
       return c;
     };
-    pl->t.tanhSat = sat_of(off[13]);
-    pl->t.sech2Sat = sat_of(off[14]);
+    pl->t.actSat = sat_of(off[13]);
+    pl->t.gradSat = sat_of(off[14]);
   } else {
     fill_tables<float>(d, pl->g, b32, off);
     bytes = b32.size() * 4;
@@ -633,8 +673,8 @@ fno_status build_tables(const fno_conv_desc* d, Plan* pl) {
   pl->t.twIc = at(10);
   pl->t.cIc = at(11);
   pl->t.sIc = at(12);
-  pl->t.lutTanh = at(13);
-  pl->t.lutSech2 = at(14);
+  pl->t.lutAct = at(13);
+  pl->t.lutGrad = at(14);
   if (pl->g.nd == 3) {
     pl->t.eFr = at(15);
     pl->t.eFi = at(16);
@@ -828,8 +868,9 @@ void prof_drain() {
 
 // Forward truncated transform of planes -> spectrum [B][C][K...].
 // scale_mode 0: 1/N normalisation (input spectrum), 1: 1/sqrt(N) (gradient).
+// pre: apply the plan's pre-activation (if it has one) to the input.
 fno_status run_r2c(const Plan* pl, const void* in, void* spec, void* inter, int64_t C,
-                   int do_tanh, int scale_mode, hipStream_t s) {
+                   int pre, int scale_mode, hipStream_t s) {
   const Geo& g = pl->g;
   R2CArgs a{};
   a.zeros = pl->t.zeros;
@@ -855,27 +896,31 @@ fno_status run_r2c(const Plan* pl, const void* in, void* spec, void* inter, int6
     a.scaleA = (float)(1.0 / std::sqrt((double)g.Nb));
     a.scaleB = (float)(1.0 / std::sqrt((double)g.Na));
   }
-  a.do_tanh = do_tanh;
+  a.do_tanh = pre && g.act != ACT_NONE;
+  a.act = a.do_tanh ? g.act : ACT_NONE;
+  a.clip = g.clip;
+  const bool do_tanh = a.do_tanh;
+  const char* kname = !do_tanh ? "r2c_plane" : g.act == ACT_TANH ? "r2c_plane_tanh" : "r2c_plane_clip";
   a.vec = (g.Nb % 8) == 0;
   a.twAc = pl->t.twAc;
   a.cBc = pl->t.cBc;
   a.sBc = pl->t.sBc;
   a.NaC = g.NaC;
-  a.lut = pl->t.lutTanh;
+  a.lut = pl->t.lutAct;
   if (a.planes > 0x7fffffff || (g.nd == 3 && g.B * C > 65535)) return FNO_ERR_UNSUPPORTED;
   bool done = false;
   if (g.elem == ELEM_F16 && a.vec && g.Kb % 4 == 0 && g.Nb <= 256 && g.Na <= 128) {
     const int nka = g.Nbp / 32, ntb = g.Kbp / 16, nta = g.Kap16 / 16;
-    const size_t lds = r2c_chain_lds_bytes(nka, ntb, nta, g.NaC, do_tanh != 0);
+    const size_t lds = r2c_chain_lds_bytes(nka, ntb, nta, g.NaC, do_tanh);
     const int64_t waves = (int64_t)kChainWaves;
     const int grid = (int)std::min<int64_t>((a.planes + waves - 1) / waves, (int64_t)2 * pl->num_cu);
     const size_t lut = do_tanh ? 65536 : 0;  // static LDS of the kernel
     if (lds + lut <= 160 * 1024 && grid > 0 && r2c_chain_has(nka, ntb, nta)) {
-      hipError_t e = timed(do_tanh ? "r2c_plane_tanh" : "r2c_plane", s, [&] {
+      hipError_t e = timed(kname, s, [&] {
         return launch_r2c_chain(a, nka, ntb, nta, grid, lds, s);
       });
       if (e == hipSuccess) done = true;
-      else if (e != hipErrorNotSupported) return hip_fail(e, do_tanh ? "r2c_plane_tanh" : "r2c_plane");
+      else if (e != hipErrorNotSupported) return hip_fail(e, kname);
     }
   }
   if (!done && g.elem == ELEM_F16 && a.vec && g.Nb <= 256 && g.Na <= 128 && g.nct <= 8) {
@@ -884,27 +929,27 @@ fno_status run_r2c(const Plan* pl, const void* in, void* spec, void* inter, int6
     const size_t lds = r2c_fast_lds_bytes(g.nct, nka, nw, g.Kap16, g.Nap_f);
     const int grid = (int)std::min<int64_t>(a.planes, (int64_t)2 * pl->num_cu);
     if (lds <= 80 * 1024) {
-      hipError_t e = timed(do_tanh ? "r2c_plane_tanh" : "r2c_plane", s, [&] {
+      hipError_t e = timed(kname, s, [&] {
         return launch_r2c_fast(a, g.nct, nka, nw, grid, lds, s);
       });
       if (e == hipSuccess) done = true;
-      else if (e != hipErrorNotSupported) return hip_fail(e, do_tanh ? "r2c_plane_tanh" : "r2c_plane");
+      else if (e != hipErrorNotSupported) return hip_fail(e, kname);
     }
   }
   if (!done && g.elem == ELEM_F16 && g.Nb % 128 == 0 && g.Na % 256 == 0 && g.Nbp == g.Nb &&
       (g.nct == 4 || g.nct == 8) && g.Kap16 <= 128 && 128 % g.Kap16 == 0 &&
       g.Na * (int64_t)g.Nb * 2 < ((int64_t)1 << 30)) {
     // large planes: persistent eight-wave work-groups, one per compute unit
-    a.lut_sat = pl->t.tanhSat;
-    const size_t lds = r2c_wide_lds_bytes(g.nct, do_tanh != 0, a.lut_sat);
+    a.lut_sat = pl->t.actSat;
+    const size_t lds = r2c_wide_lds_bytes(g.nct, do_tanh, a.lut_sat);
     const int grid = (int)std::min<int64_t>(a.planes, (int64_t)pl->num_cu);
-    hipError_t e = timed(do_tanh ? "r2c_plane_tanh" : "r2c_plane", s, [&] {
+    hipError_t e = timed(kname, s, [&] {
       return launch_r2c_wide(a, g.nct, grid, lds, s);
     });
     if (e == hipSuccess) done = true;
-    else if (e != hipErrorNotSupported) return hip_fail(e, do_tanh ? "r2c_plane_tanh" : "r2c_plane");
+    else if (e != hipErrorNotSupported) return hip_fail(e, kname);
   }
-  if (!done) FNO_HIP(timed(do_tanh ? "r2c_plane_tanh" : "r2c_plane", s, [&] { return launch_r2c(g.elem, g.nct, a, r2c_lds_bytes(g.elem, g.Kbp, g.R_f), s); }));
+  if (!done) FNO_HIP(timed(kname, s, [&] { return launch_r2c(g.elem, g.nct, a, r2c_lds_bytes(g.elem, g.Kbp, g.R_f), s); }));
   if (g.nd == 3) {
     AxisArgs x{};
     x.in = inter;
@@ -964,13 +1009,16 @@ fno_status run_c2r(const Plan* pl, const void* spec, void* out, void* inter, int
   a.R = g.R_i;
   a.scale = scale;
   a.epilogue = x_epi != nullptr;
+  a.act = g.act;
+  a.clip = g.clip;
   a.vec = (g.Nb % 8) == 0;
   if (a.planes > 0x7fffffff) return FNO_ERR_UNSUPPORTED;
   a.twIc = pl->t.twIc;
   a.cIc = pl->t.cIc;
   a.sIc = pl->t.sIc;
-  a.lut = pl->t.lutSech2;
-  const char* kname = x_epi ? "c2r_plane_tanh_grad" : "c2r_plane";
+  a.lut = pl->t.lutGrad;
+  const char* kname = !x_epi ? "c2r_plane"
+                      : g.act == ACT_TANH ? "c2r_plane_tanh_grad" : "c2r_plane_clip_grad";
   if (g.elem == ELEM_F16 && g.Nb % 16 == 0 && g.Kb % 4 == 0 && g.Nb <= 256 && g.Na <= 128) {
     const int ng = g.Nb64 / 64, ntb = g.Kbp / 16, nkz = g.Kap / 32;
     const size_t lds = c2r_chain_lds_bytes(ng, ntb, g.Kap, g.Na, x_epi != nullptr);
@@ -1001,7 +1049,7 @@ fno_status run_c2r(const Plan* pl, const void* spec, void* out, void* inter, int
   if (g.elem == ELEM_F16 && g.Nb % 128 == 0 && g.Na % 256 == 0 &&
       (g.nct == 4 || g.nct == 8) && g.Kap <= 128 && g.Na * (int64_t)g.Nb * 2 < ((int64_t)1 << 30)) {
     // large planes: persistent eight-wave work-groups, one per compute unit
-    a.lut_sat = pl->t.sech2Sat;
+    a.lut_sat = pl->t.gradSat;
     const size_t lds = c2r_wide_lds_bytes(g.nct, g.Kap, x_epi != nullptr, a.lut_sat);
     const int grid = (int)std::min<int64_t>(a.planes, (int64_t)pl->num_cu);
     hipError_t e = timed(kname, s, [&] { return launch_c2r_wide(a, g.nct, grid, lds, s); });
@@ -1571,8 +1619,7 @@ fno_status fno_spectral_conv_fwd(const fno_conv_desc* d, const void* x, const fn
   char* inter = base + L.add(std::max(inter3d_bytes(g, g.Cin), inter3d_bytes(g, g.Cout)));
   char* tsc = base + L.total;
   void* xh = x_hat_out ? x_hat_out : (void*)xs;
-  const int tanh_on = d->precision == FNO_PREC_FP16_TANH;
-  if ((st = run_r2c(pl, x, xh, inter, g.Cin, tanh_on, 0, s)) != FNO_OK) return st;
+  if ((st = run_r2c(pl, x, xh, inter, g.Cin, 1, 0, s)) != FNO_OK) return st;
   if (d->weight_kind == FNO_WEIGHT_DENSE) {
     if ((st = run_contract(pl, xh, w->dense, ys, false, s)) != FNO_OK) return st;
   } else {
@@ -1587,9 +1634,9 @@ fno_status fno_spectral_conv_bwd_data(const fno_conv_desc* d, const void* x,
                                       hipStream_t s) {
   fno_status st = check_desc(d);
   if (st != FNO_OK) return st;
-  const int tanh_on = d->precision == FNO_PREC_FP16_TANH;
+  const int pre_on = act_of(d) != ACT_NONE;  // x is read for f'(x)
   if (!okptr(gy) || !okptr(gx)) return FNO_ERR_INVALID_ARGUMENT;
-  if (tanh_on && !okptr(x)) return FNO_ERR_INVALID_ARGUMENT;
+  if (pre_on && !okptr(x)) return FNO_ERR_INVALID_ARGUMENT;
   if (gy_hat_out && !aligned16(gy_hat_out)) return FNO_ERR_INVALID_ARGUMENT;
   if ((st = check_weights(d, w)) != FNO_OK) return st;
   if ((st = check_ws(d, FNO_OP_BWD_DATA, true, ws, ws_len)) != FNO_OK) return st;
@@ -1610,7 +1657,7 @@ fno_status fno_spectral_conv_bwd_data(const fno_conv_desc* d, const void* x,
     if ((st = run_tucker_path(d, pl, true, gh, w, gxs, tsc, s)) != FNO_OK) return st;
   }
   const float sc = (float)(1.0 / std::sqrt((double)g.N));
-  return run_c2r(pl, gxs, gx, inter, g.Cin, sc, tanh_on ? x : nullptr, s);
+  return run_c2r(pl, gxs, gx, inter, g.Cin, sc, pre_on ? x : nullptr, s);
 }
 
 fno_status fno_spectral_conv_bwd_weight(const fno_conv_desc* d, const void* x, const void* gy,
@@ -1646,7 +1693,7 @@ fno_status fno_spectral_conv_bwd_weight(const fno_conv_desc* d, const void* x, c
     char* gs = base + L.add(spec_bytes(g, g.Cout));
     char* inter = base + L.add(std::max(inter3d_bytes(g, g.Cin), inter3d_bytes(g, g.Cout)));
     if (!xh) {
-      if ((st = run_r2c(pl, x, xs, inter, g.Cin, d->precision == FNO_PREC_FP16_TANH, 0, s)) !=
+      if ((st = run_r2c(pl, x, xs, inter, g.Cin, 1, 0, s)) !=
           FNO_OK)
         return st;
       xh = xs;
@@ -1686,10 +1733,10 @@ fno_status fno_spectral_conv_bwd(const fno_conv_desc* d, const void* x, const fn
                                  size_t ws_len, hipStream_t s) {
   fno_status st = check_desc(d);
   if (st != FNO_OK) return st;
-  const int tanh_on = d->precision == FNO_PREC_FP16_TANH;
+  const int pre_on = act_of(d) != ACT_NONE;  // x is read for f'(x)
   const bool tucker = factorized(d);
   if (!okptr(gy) || !okptr(gx) || !gw) return FNO_ERR_INVALID_ARGUMENT;
-  if ((tanh_on || !x_hat) && !okptr(x)) return FNO_ERR_INVALID_ARGUMENT;
+  if ((pre_on || !x_hat) && !okptr(x)) return FNO_ERR_INVALID_ARGUMENT;
   if (x_hat && !aligned16(x_hat)) return FNO_ERR_INVALID_ARGUMENT;
   if (gy_hat_out && !aligned16(gy_hat_out)) return FNO_ERR_INVALID_ARGUMENT;
   if ((st = check_weights(d, w)) != FNO_OK) return st;
@@ -1724,7 +1771,7 @@ fno_status fno_spectral_conv_bwd(const fno_conv_desc* d, const void* x, const fn
       (void)Ld.add(spec_bytes(g, g.Cout));
       (void)Ld.add(spec_bytes(g, g.Cin));
       char* inter = wsd + Ld.add(std::max(inter3d_bytes(g, g.Cin), inter3d_bytes(g, g.Cout)));
-      if ((st = run_r2c(pl, x, xs, inter, g.Cin, tanh_on, 0, s)) != FNO_OK) return st;
+      if ((st = run_r2c(pl, x, xs, inter, g.Cin, 1, 0, s)) != FNO_OK) return st;
     }
     return fno_spectral_conv_bwd_weight(d, x, gy, w, cache ? x_hat : xs, gh, gw, wsw, nw, s);
   }
@@ -1736,7 +1783,7 @@ fno_status fno_spectral_conv_bwd(const fno_conv_desc* d, const void* x, const fn
   char* inter = wsd + Ld.add(std::max(inter3d_bytes(g, g.Cin), inter3d_bytes(g, g.Cout)));
   const void* xh = x_hat;
   if (!cache) {
-    if ((st = run_r2c(pl, x, xs, inter, g.Cin, tanh_on, 0, s)) != FNO_OK) return st;
+    if ((st = run_r2c(pl, x, xs, inter, g.Cin, 1, 0, s)) != FNO_OK) return st;
     xh = xs;
   }
   if ((st = run_r2c(pl, gy, gh, inter, g.Cout, 0, 1, s)) != FNO_OK) return st;
@@ -1777,7 +1824,7 @@ fno_status fno_spectral_conv_bwd(const fno_conv_desc* d, const void* x, const fn
     }));
   }
   const float sc = (float)(1.0 / std::sqrt((double)g.N));
-  return run_c2r(pl, gxs, gx, inter, g.Cin, sc, tanh_on ? x : nullptr, s);
+  return run_c2r(pl, gxs, gx, inter, g.Cin, sc, pre_on ? x : nullptr, s);
 }
 
 fno_status fno_profile_enable(int32_t enable) {

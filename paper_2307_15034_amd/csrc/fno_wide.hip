@@ -11,8 +11,8 @@
 //     data is in flight while the current one is multiplied (register double
 //     buffering, loads issued unconditionally so the waits stay exact); rows
 //     are read with buffer loads, rows past the plane reading zero;
-//   - tanh (forward pre-activation) and sech^2 (backward epilogue) come from
-//     a table in LDS of the fp16 codes up to the code where the function
+//   - the pre-activation f (tanh or the hard clip, forward) and its
+//     derivative f' (backward epilogue) come from a table in LDS of the fp16 codes up to the code where the function
 //     saturates, plus one NaN entry (three packed 16-bit operations pick the
 //     entry), instead of fp32 arithmetic per element.
 #include <hip/hip_runtime.h>
@@ -98,7 +98,7 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t plane_rsrc(const void* base, i
 constexpr int WD_SK = 64;             // columns (n) per twiddle slice
 constexpr int WD_LDT = WD_SK + WD_PAD;
 
-template <int NCT, bool TANH>
+template <int NCT, bool PRE>
 __global__ __launch_bounds__(WD_WAVES * 64, 1) void r2c_wide_kernel(R2CArgs a) {
   typedef MM<_Float16> M;
   constexpr int KS = 32, NTB = NCT / 2, KBP = NCT * 8;
@@ -117,7 +117,7 @@ __global__ __launch_bounds__(WD_WAVES * 64, 1) void r2c_wide_kernel(R2CArgs a) {
   const _Float16* cB = reinterpret_cast<const _Float16*>(a.cB);
   const _Float16* sB = reinterpret_cast<const _Float16*>(a.sB);
   const us2 sat = {(unsigned short)a.lut_sat, (unsigned short)a.lut_sat};
-  if (TANH) stage_lut(lut, a.lut, a.lut_sat);
+  if (PRE) stage_lut(lut, a.lut, a.lut_sat);
 
   const int64_t plane_bytes = (int64_t)a.Na * a.Nb * 2;
   const int nks = a.Nb / KS;        // a multiple of 4 on this path
@@ -208,7 +208,7 @@ __global__ __launch_bounds__(WD_WAVES * 64, 1) void r2c_wide_kernel(R2CArgs a) {
 #pragma unroll
       for (int u = 0; u < 2; ++u) {
         u32x4 w = v[u];
-        if (TANH) {
+        if (PRE) {
 #pragma unroll
           for (int e = 0; e < 4; ++e) w[e] = lut2<true>(lut, w[e], sat);
         }
@@ -325,7 +325,7 @@ __global__ __launch_bounds__(WD_WAVES * 64, 1) void r2c_wide_kernel(R2CArgs a) {
 
 // ---------------------------------------------------------------------------
 // Inverse: spectrum [Ka][Kb] -> plane [Na][Nb], y = scale * sum Re(Z e^{+i
-// theta}), optional epilogue y *= sech^2(x).  Per plane the spectrum is
+// theta}), optional epilogue y *= f'(x).  Per plane the spectrum is
 // staged transposed in LDS (ZT[kb][ka]: real rows, then imaginary); per
 // chunk step B' gives V[row][kb] = sum_ka (cI + i sI)[row][ka] Z[ka][kb] into
 // LDS as [Re V | Im V] (each wave two 16-row tiles), and each wave then holds
@@ -639,10 +639,10 @@ __global__ __launch_bounds__(WD_WAVES * 64, 1) void c2r_wide_kernel(C2RArgs a) {
 // ---------------------------------------------------------------------------
 // Launchers (hipErrorNotSupported: the shape is not one of this path's)
 // ---------------------------------------------------------------------------
-size_t r2c_wide_lds_bytes(int nct, bool tanh, int lut_sat) {
+size_t r2c_wide_lds_bytes(int nct, bool pre, int lut_sat) {
   const size_t at = (size_t)2 * (nct * 8) * (WD_R + WD_PAD) * 2;
   const size_t tw = (size_t)2 * 2 * (nct * 8) * WD_LDT * 2;
-  return at + tw + (tanh ? (size_t)(lut_sat + 2) * 2 : 0);
+  return at + tw + (pre ? (size_t)(lut_sat + 2) * 2 : 0);
 }
 
 size_t c2r_wide_lds_bytes(int nct, int Kap, bool epi, int lut_sat) {

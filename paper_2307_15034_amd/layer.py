@@ -32,13 +32,15 @@ class SpectralConv:
               u_out [c_out, r_out, 2], u_mode[j] [K_j, r_j, 2]
       cp (rank R): core = lambda [R, 2], u_in [c_in, R, 2], u_out [c_out, R, 2],
               u_mode[j] [K_j, R, 2]
-    The storage dtype is float16 in fp16+tanh mode and float32 in fp32 mode.
+    The storage dtype is float16 in fp16+tanh mode and float32 in fp32 mode;
+    `preact` / `clip` choose the pre-activation (the precision's own by default).
     """
 
     def __init__(self, n: Sequence[int], modes: Sequence[int], batch: int, c_in: int,
                  c_out: int, precision: int = B.FNO_PREC_FP16_TANH,
                  weight_kind: int = B.FNO_WEIGHT_DENSE, rank: Optional[Sequence[int]] = None,
-                 path_policy: int = B.FNO_PATH_MIN_RESULT, device: str = "cuda"):
+                 path_policy: int = B.FNO_PATH_MIN_RESULT, device: str = "cuda",
+                 preact: int = B.FNO_PREACT_DEFAULT, clip: float = 0.0):
         self.n = tuple(int(v) for v in n)
         self.modes = tuple(int(v) for v in modes)
         self.batch, self.c_in, self.c_out = int(batch), int(c_in), int(c_out)
@@ -46,7 +48,7 @@ class SpectralConv:
         self.weight_kind = weight_kind
         self.rank = tuple(rank) if rank is not None else None
         self.desc = B.make_desc(self.n, self.modes, batch, c_in, c_out, precision,
-                                weight_kind, rank, path_policy)
+                                weight_kind, rank, path_policy, preact, clip)
         self.dtype = torch.float16 if precision == B.FNO_PREC_FP16_TANH else torch.float32
         self.device = torch.device(device)
         d = len(self.n)

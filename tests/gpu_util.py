@@ -10,7 +10,14 @@ import torch
 from oracle import fno_oracle as O
 import synth
 
-TOL = {"fp32": 1e-5, "fp16_tanh": 3e-3}
+class _Tol(dict):
+    """Relative L2 tolerance of a mode: 1e-5 for fp32 storage, 3e-3 for fp16."""
+
+    def __missing__(self, prec):
+        return 1e-5 if prec.startswith("fp32") else 3e-3
+
+
+TOL = _Tol({"fp32": 1e-5, "fp16_tanh": 3e-3})
 
 
 def say(msg: str) -> None:
@@ -19,10 +26,25 @@ def say(msg: str) -> None:
 
 
 def prec_codes(prec: str):
+    """(library precision code, numpy storage dtype, oracle mode) of a mode
+    name: "fp32", "fp16_tanh", "fp32_tanh", "fp16" or "fp16_clip:<c>" /
+    "fp32_clip:<c>" (the oracle's mode strings)."""
     from paper_2307_15034_amd import binding as B
-    if prec == "fp32":
-        return B.FNO_PREC_FP32, np.float32, O.PREC_FP32
-    return B.FNO_PREC_FP16_TANH, np.float16, O.PREC_FP16_TANH
+    O.preact_kind(prec)  # rejects unknown names
+    if prec.startswith("fp32"):
+        return B.FNO_PREC_FP32, np.float32, prec
+    return B.FNO_PREC_FP16_TANH, np.float16, prec
+
+
+def preact_codes(prec: str):
+    """(library pre-activation code, clip bound) of a mode name."""
+    from paper_2307_15034_amd import binding as B
+    kind, c = O.preact_kind(prec)
+    if prec in ("fp32", "fp16_tanh"):
+        return B.FNO_PREACT_DEFAULT, 0.0
+    if kind == "clip":
+        return B.FNO_PREACT_HARD_CLIP, float(c)
+    return (B.FNO_PREACT_TANH if kind == "tanh" else B.FNO_PREACT_NONE), 0.0
 
 
 def dev(a: np.ndarray) -> torch.Tensor:
@@ -41,11 +63,13 @@ def make_layer(n, modes, batch, c_in, c_out, prec, tucker_rank=None, policy=0, c
     from paper_2307_15034_amd import binding as B
     from paper_2307_15034_amd.layer import SpectralConv
     pc, _, _ = prec_codes(prec)
+    pa, clip = preact_codes(prec)
     if cp_rank is not None:
         return SpectralConv(n, modes, batch, c_in, c_out, pc, B.FNO_WEIGHT_CP, (cp_rank,),
-                            policy)
+                            policy, preact=pa, clip=clip)
     kind = B.FNO_WEIGHT_TUCKER if tucker_rank is not None else B.FNO_WEIGHT_DENSE
-    return SpectralConv(n, modes, batch, c_in, c_out, pc, kind, tucker_rank, policy)
+    return SpectralConv(n, modes, batch, c_in, c_out, pc, kind, tucker_rank, policy,
+                        preact=pa, clip=clip)
 
 
 def run_all(layer, x, w, gy, caches=True):

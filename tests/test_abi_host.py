@@ -240,6 +240,37 @@ def test_invalid_enums_and_counts():
         assert e.value.status == B.FNO_ERR_INVALID_ARGUMENT, field
 
 
+def test_preactivation_descriptor_checks():
+    P16, P32 = B.FNO_PREC_FP16_TANH, B.FNO_PREC_FP32
+    bad = [(P16, 4, 1.0), (P16, -1, 1.0), (P16, B.FNO_PREACT_HARD_CLIP, 0.0),
+           (P16, B.FNO_PREACT_HARD_CLIP, -1.0), (P16, B.FNO_PREACT_HARD_CLIP, float("nan")),
+           (P32, B.FNO_PREACT_HARD_CLIP, float("inf")),
+           (P16, B.FNO_PREACT_HARD_CLIP, 70000.0)]       # beyond fp16's largest value
+    for prec, pa, clip in bad:
+        d = B.make_desc((16, 16), (4, 4), 2, 4, 4, prec, preact=pa, clip=clip)
+        with pytest.raises(B.FnoError) as e:
+            B.fno_spectral_conv_workspace_size(d, B.FNO_OP_FWD)
+        assert e.value.status == B.FNO_ERR_INVALID_ARGUMENT, (prec, pa, clip)
+    good = [(P32, B.FNO_PREACT_HARD_CLIP, 70000.0), (P16, B.FNO_PREACT_HARD_CLIP, 65504.0),
+            (P16, B.FNO_PREACT_TANH, float("nan")), (P32, B.FNO_PREACT_NONE, -3.0),
+            (P32, B.FNO_PREACT_TANH, 0.0)]             # the bound is ignored unless clipping
+    for prec, pa, clip in good:
+        d = B.make_desc((16, 16), (4, 4), 2, 4, 4, prec, preact=pa, clip=clip)
+        assert B.fno_spectral_conv_workspace_size(d, B.FNO_OP_FWD) > 0
+
+
+def test_preactivation_decides_whether_bwd_data_reads_x():
+    """x may be null exactly when there is no pre-activation (no f'(x))."""
+    w = B.weights_struct(dense=FAKE)
+    for prec, pa, needs_x in [(B.FNO_PREC_FP32, B.FNO_PREACT_TANH, True),
+                              (B.FNO_PREC_FP32, B.FNO_PREACT_HARD_CLIP, True),
+                              (B.FNO_PREC_FP16_TANH, B.FNO_PREACT_NONE, False),
+                              (B.FNO_PREC_FP32, B.FNO_PREACT_DEFAULT, False)]:
+        d = B.make_desc((32, 32), (4, 4), 2, 4, 4, prec, preact=pa, clip=1.0)
+        st = B.fno_spectral_conv_bwd_data(d, 0, w, FAKE, FAKE, 0, FAKE, 16, 0, check=False)
+        assert st == (B.FNO_ERR_INVALID_ARGUMENT if needs_x else B.FNO_ERR_WORKSPACE_TOO_SMALL)
+
+
 def test_unsupported_sizes():
     d = B.make_desc((512, 512), (8, 200), 1, 1, 1)
     with pytest.raises(B.FnoError) as e:

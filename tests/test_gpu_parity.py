@@ -297,6 +297,8 @@ BWD_CASES = [
     ((32, 32), (8, 8), 17, 20, 36, "fp16_tanh"),   # ragged rows / columns / batch
     ((6, 10, 12), (2, 3, 4), 2, 3, 2, "fp16_tanh"),
     ((32, 32), (8, 8), 3, 5, 7, "fp32"),
+    ((64, 64), (8, 8), 2, 16, 16, "fp16_clip:0.75"),   # shared launch, clip derivative
+    ((32, 32), (8, 8), 3, 5, 7, "fp32_tanh"),
 ]
 
 

@@ -234,6 +234,81 @@ def pin_identity_self_adjoint(seed=13):
     return np.abs(a - b).max()
 
 
+def pin_fd_clip(seed=14, c=0.5):
+    """Central finite differences of L = <gy, y> in x through the hard clip,
+    at points inside and outside [-c, c] (none within 1e-3 of the bound)."""
+    rng = _rng(seed)
+    n, modes = (8, 8), (2, 2)
+    prec = O.clip_mode("fp16", c)
+    x = rng.standard_normal((1, 2) + n) * 0.8
+    w = _cplx(rng, (2, 2, 4, 2), 0.5)
+    gy = rng.standard_normal((1, 2) + n)
+    gx = O.bwd_data(x, w, gy, n, modes, prec)
+    far = np.abs(np.abs(x) - c) > 1e-3
+    inside = np.argwhere(far & (np.abs(x) < c))[:3]
+    outside = np.argwhere(far & (np.abs(x) > c))[:3]
+    if len(inside) < 3 or len(outside) < 3:
+        return np.inf
+    h = 1e-6
+    err = 0.0
+    for idx in [tuple(i) for i in inside] + [tuple(i) for i in outside]:
+        e = np.zeros_like(x)
+        e[idx] = h
+        fd = (np.sum(gy * O.fwd(x + e, w, n, modes, prec)) -
+              np.sum(gy * O.fwd(x - e, w, n, modes, prec))) / (2 * h)
+        err = max(err, abs(fd - gx[idx]) / max(1e-3, abs(gx[idx])))
+    # outside the bound the input does not reach the output
+    err = max(err, float(np.abs(gx[far & (np.abs(x) > c)]).max()))
+    return err
+
+
+def pin_clip_saturated(seed=15, c=0.25):
+    """Every |x| > c: the clipped input is c sign(x), so the layer output is
+    c times the full-precision output for sign(x)."""
+    rng = _rng(seed)
+    n, modes = (8, 6), (2, 3)
+    x = rng.standard_normal((2, 3) + n)
+    x = np.where(np.abs(x) < 2 * c, np.copysign(2 * c, x), x)
+    w = _cplx(rng, (3, 2, 4, 3), 0.5)
+    got = O.fwd(x, w, n, modes, O.clip_mode("fp32", c))
+    ref = c * O.fwd(np.sign(x), w, n, modes, F32)
+    return np.abs(got - ref).max() / np.abs(ref).max()
+
+
+def pin_clip_wide_is_identity(seed=16):
+    """A bound above every |x| leaves the layer and its gradients as in
+    full precision without pre-activation."""
+    rng = _rng(seed)
+    n, modes = (8, 6), (2, 3)
+    x = rng.standard_normal((2, 3) + n)
+    w = _cplx(rng, (3, 2, 4, 3), 0.5)
+    gy = rng.standard_normal((2, 2) + n)
+    prec = O.clip_mode("fp16", float(np.abs(x).max()) * 1.01)
+    err = np.abs(O.fwd(x, w, n, modes, prec) - O.fwd(x, w, n, modes, F32)).max()
+    err = max(err, np.abs(O.bwd_data(x, w, gy, n, modes, prec) -
+                          O.bwd_data(x, w, gy, n, modes, F32)).max())
+    return err
+
+
+def pin_tanh_constant_field(seed=17):
+    """A constant input a_i per channel has only the zero mode: y[o] =
+    sum_i Re(W[i, o, 0, 0]) tanh(a_i) at every point, for the tanh modes of
+    both storage precisions (scalar math.tanh as the closed form)."""
+    import math
+    rng = _rng(seed)
+    n, modes = (8, 6), (2, 3)
+    a = np.array([-3.0, -0.4, 0.7, 5.0])
+    x = np.broadcast_to(a[None, :, None, None], (1, 4) + n).copy()
+    w = _cplx(rng, (4, 3, 4, 3), 0.5)
+    ref = np.array([sum(w[i, o, 0, 0].real * math.tanh(a[i]) for i in range(4))
+                    for o in range(3)])
+    err = 0.0
+    for prec in (O.PREC_FP32_TANH, F16T):
+        y = O.fwd(x, w, n, modes, prec)[0]
+        err = max(err, np.abs(y - ref[:, None, None]).max())
+    return err
+
+
 def _cp_small(seed, d=2, rank=3):
     rng = _rng(seed)
     n = (8, 8) if d == 2 else (4, 4, 6)
@@ -299,6 +374,11 @@ ALL_PINS = {
     "irfftn": (pin_irfftn, 1e-13),
     "fd_fp32": (lambda: pin_fd_dense(F32), 1e-7),
     "fd_tanh": (lambda: pin_fd_dense(F16T), 1e-7),
+    "fd_fp32_tanh": (lambda: pin_fd_dense(O.PREC_FP32_TANH), 1e-7),
+    "fd_clip": (pin_fd_clip, 1e-7),
+    "clip_saturated": (pin_clip_saturated, 1e-13),
+    "tanh_constant": (pin_tanh_constant_field, 1e-13),
+    "clip_wide_identity": (pin_clip_wide_is_identity, 1e-13),
     "adjoint": (pin_adjoint, 1e-12),
     "identity_adjoint": (pin_identity_self_adjoint, 1e-13),
 }
@@ -793,6 +873,13 @@ MUTATIONS = {
         lambda z, n, m, with_c=True: orig(np.real(z) + 0j, n, m, with_c))),
     "tanh_prime_wrong": ("bwd_data", lambda orig: (
         lambda x, w, gy, n, m, p: orig(x, w, gy, n, m, O.PREC_FP32))),
+    "clip_one_sided": ("preactivation", lambda orig: (
+        lambda x, p: np.minimum(np.asarray(x, dtype=np.float64), O.preact_kind(p)[1])
+        if O.preact_kind(p)[0] == "clip" else orig(x, p))),
+    "clip_grad_ones": ("preactivation_grad", lambda orig: (
+        lambda x, p: np.ones(np.shape(x)) if O.preact_kind(p)[0] == "clip" else orig(x, p))),
+    "fp32_tanh_as_identity": ("preact_kind", lambda orig: (
+        lambda p: ("none", None) if p == O.PREC_FP32_TANH else orig(p))),
     "grad_no_c": ("grad_spectrum", lambda orig: (
         lambda gy, n, m: O.forward_spectrum(gy, n, m) * float(np.prod(n)))),
     "cp_drop_lambda": ("cp_dense", lambda orig: (
