@@ -242,3 +242,18 @@ def random_dense_case(seed: int, batch: int, c_in: int, c_out: int,
     w = _complex_pairs(rng, (c_in, c_out) + kd, 1.0 / np.sqrt(c_in * c_out), dtype)
     gy = _round(rng.standard_normal((batch, c_out) + n), dtype)
     return x, w, gy
+
+
+def decaying_sinusoids(seed: int, count: int, length: int, kmax: int = 10,
+                       decay: float = 1.0) -> np.ndarray:
+    """`count` 1-D signals of `length` samples, float64 [count, length]: sums of
+    a cosine and a sine at each integer frequency k = 1..kmax (cycles per
+    signal), with amplitudes r 2^(-decay (k-1)), r ~ U(0.5, 1) drawn per wave
+    (the synthetic signal of the frequency-mode ablation, App. B.10)."""
+    rng = np.random.default_rng(np.random.SeedSequence([3000 + int(seed)]))
+    x = np.arange(length, dtype=np.float64) / length
+    out = np.zeros((count, length))
+    for k in range(1, kmax + 1):
+        a = rng.uniform(0.5, 1.0, (count, 2)) * 2.0 ** (-decay * (k - 1))
+        out += a[:, :1] * np.cos(2 * np.pi * k * x) + a[:, 1:] * np.sin(2 * np.pi * k * x)
+    return out

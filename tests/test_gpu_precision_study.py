@@ -1,0 +1,86 @@
+"""Precision study on the GPU path (synthetic inputs only).
+
+1. Theorem 3.2 (Sec. 3): the half-precision forward transform moves every
+   retained coefficient by at most a constant times eps ||v||_inf, whatever
+   the grid size.  The theorem's model quantises v and the basis values and
+   sums exactly (c = 4 in its proof).  The fp16 kernels also round the first
+   axis's result and the final coefficient to fp16 and accumulate in fp32.
+   Per real or imaginary part that gives:
+     - first axis: q(v) and the twiddles, 2 eps M; its stored result, eps M;
+     - second axis: the propagated 3 eps M times |cos| + |sin| <= sqrt 2,
+       plus the twiddles, sqrt 2 eps M;
+     - the final store, eps M;
+     - fp32 sums, under 0.2 eps M at these lengths.
+   That is (1 + 4 sqrt 2) eps M + 0.4 eps M < 7.1 eps M per part, so under
+   10 eps M in modulus (eps = 2^-11).  The measured maximum is printed per
+   grid size; the test holds each to that bound.
+2. The frequency-mode ablation (App. B.10): for signals whose amplitudes
+   decay exponentially with frequency, the half-precision spectrum's error
+   relative to each amplitude grows with frequency.  The fp32 GPU path is the
+   full-precision reference, as in the paper's comparison.
+"""
+import numpy as np
+import pytest
+
+torch = pytest.importorskip("torch")
+
+pytestmark = [pytest.mark.gpu,
+              pytest.mark.skipif(not torch.cuda.is_available(), reason="needs a GPU")]
+
+from oracle import fno_oracle as O  # noqa: E402
+import synth  # noqa: E402
+from tests import gpu_util as U  # noqa: E402
+
+EPS16 = 2.0 ** -11
+
+
+def _spectrum(layer, x: np.ndarray) -> np.ndarray:
+    """The input spectrum the forward call leaves in its cache (complex128)."""
+    w = np.zeros((layer.c_in, layer.c_out) + layer.kdims + (2,),
+                 dtype=np.float16 if layer.dtype == torch.float16 else np.float32)
+    xh = layer.spectrum_buffer(0)
+    layer.fwd(U.dev(x), U.dev(w), x_hat=xh)
+    torch.cuda.synchronize()
+    raw = U.host(xh).view(np.float16 if layer.dtype == torch.float16 else np.float32)
+    k = int(np.prod(layer.kdims))
+    pairs = raw[: layer.batch * layer.c_in * k * 2].reshape(
+        (layer.batch, layer.c_in) + layer.kdims + (2,))
+    return U.cplx(pairs.astype(np.float64))
+
+
+def test_thm32_bound_on_gpu_spectrum():
+    rows = []
+    for nn in (64, 128, 256, 512, 1024):
+        n, modes, Bt, C = (nn, nn), (16, 16), 2, 2
+        U.say(f"Thm 3.2 grid {nn}x{nn}")
+        rng = np.random.default_rng(np.random.SeedSequence([4100, nn]))
+        x = (synth.grf_fields(rng, Bt * C, n) * 2.0).reshape((Bt, C) + n).astype(np.float16)
+        layer = U.make_layer(n, modes, Bt, C, C, "fp16_tanh")
+        got = _spectrum(layer, x)
+        v = np.tanh(x.astype(np.float64))
+        exact = O.forward_spectrum(v, n, modes)
+        M = float(np.abs(v).max())
+        err = float(np.abs(got - exact).max()) / (EPS16 * M)
+        rows.append((nn, err))
+        U.say(f"  max |error| = {err:.3f} eps M")
+        assert err <= 10.0, (nn, err)
+    U.say("grid  max|err|/(eps M): " + ", ".join(f"{a}: {b:.3f}" for a, b in rows))
+
+
+def test_frequency_error_grows_with_frequency():
+    N, kmax, Bt = 1024, 10, 64
+    x64 = synth.decaying_sinusoids(0, Bt, N, kmax)
+    spec = {}
+    for prec in ("fp16", "fp32"):
+        _, npdt, _ = U.prec_codes(prec)
+        layer = U.make_layer((N,), (16,), Bt, 1, 1, prec)
+        spec[prec] = _spectrum(layer, x64.astype(npdt))[:, 0]
+    # the reference of each precision's stored input: fp16 rounding of the
+    # signal is part of the half-precision error, as in the paper's comparison
+    amp = np.abs(spec["fp32"][:, 1:kmax + 1])
+    pct = 100.0 * np.abs(spec["fp16"][:, 1:kmax + 1] - spec["fp32"][:, 1:kmax + 1]) / amp
+    mean_pct = pct.mean(axis=0)
+    U.say("frequency  mean amplitude  mean error %: " + "; ".join(
+        f"{k}: {amp[:, k - 1].mean():.2e} {mean_pct[k - 1]:.3f}" for k in range(1, kmax + 1)))
+    assert mean_pct[-3:].mean() > 10.0 * mean_pct[:3].mean()
+    assert np.all(np.diff(np.log(mean_pct[1:])) > -0.5)
