@@ -39,6 +39,9 @@ def parse():
     p.add_argument("--warmup", type=int, default=20)
     p.add_argument("--workload", type=int, default=2)
     p.add_argument("--precision", choices=["fp16_tanh", "fp32"], default="fp16_tanh")
+    p.add_argument("--preact", choices=["default", "none", "tanh", "clip"], default="default",
+                   help="pre-activation (default: tanh in fp16_tanh, none in fp32)")
+    p.add_argument("--clip", type=float, default=1.0, help="bound of --preact clip")
     p.add_argument("--policy", choices=["min_result", "min_net"], default="min_result")
     p.add_argument("--no-caches", action="store_true",
                    help="bwd_weight recomputes both spectra from x and gy")
@@ -57,9 +60,11 @@ def parse():
     return p.parse_args()
 
 
-def kernel_bytes(wl, es):
-    """Algorithmic HBM bytes of one launch of each kernel (reads + writes of
-    the tensors it must touch once)."""
+def kernel_bytes(wl, es, preact="tanh"):
+    """Algorithmic HBM bytes of each kernel per step (reads + writes of the
+    tensors it must touch once).  Without a pre-activation the input and
+    gradient transforms are both "r2c_plane" and both inverses "c2r_plane"
+    (the data gradient's inverse then reads no x)."""
     B, Ci, Co = wl.batch, wl.c_in, wl.c_out
     N = int(np.prod(wl.n))
     K = int(np.prod(wl.kdims))
@@ -76,12 +81,18 @@ def kernel_bytes(wl, es):
     out["contract_adjoint_wgrad"] = out["contract_adjoint"] + out["wgrad"]  # one launch
     out["r2c_plane_tanh"] = B * Ci * N * es + spec_in     # input transform (tanh)
     out["r2c_plane"] = B * Co * N * es + spec_out         # gradient transform
+    out["r2c_plane_clip"] = out["r2c_plane_tanh"]
+    out["c2r_plane_clip_grad"] = out["c2r_plane_tanh_grad"]
+    if preact == "none":
+        out["r2c_plane"] += out["r2c_plane_tanh"]
+        out["c2r_plane"] += spec_in + B * Ci * N * es
     return out
 
 
-def step_bytes(wl, es, caches=True):
-    """Whole-step algorithmic bytes: 5 spatial passes, W twice, gW (fp32),
-    and the two spectral caches written once and read once."""
+def step_bytes(wl, es, caches=True, preact="tanh"):
+    """Whole-step algorithmic bytes: 5 spatial passes (4 without a
+    pre-activation, whose data gradient reads no x), W twice, gW (fp32), and
+    the two spectral caches written once and read once."""
     B, Ci, Co = wl.batch, wl.c_in, wl.c_out
     N = int(np.prod(wl.n))
     K = int(np.prod(wl.kdims))
@@ -99,6 +110,8 @@ def step_bytes(wl, es, caches=True):
     else:
         W, gW = Ci * Co * K * 2 * es, Ci * Co * K * 2 * 4
     total = S_in + S_out + (S_out + S_in + S_in) + 2 * W + gW
+    if preact == "none":
+        total -= S_in
     total += 2 * spec if caches else (S_in + S_out)
     return int(total)
 
@@ -141,7 +154,7 @@ def cpu_baseline(wl, x, w, gy, prec, seconds):
         threads = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
     except Exception:  # pragma: no cover
         threads = len(os.sched_getaffinity(0))
-    oprec = O.PREC_FP16_TANH if prec == "fp16_tanh" else O.PREC_FP32
+    oprec = prec
     done = 0
     t0 = time.perf_counter()
     while True:
@@ -208,13 +221,22 @@ def main():
     npdt = np.float16 if args.precision == "fp16_tanh" else np.float32
     es = 2 if args.precision == "fp16_tanh" else 4
     pc = B.FNO_PREC_FP16_TANH if args.precision == "fp16_tanh" else B.FNO_PREC_FP32
+    preact = args.preact if args.preact != "default" else (
+        "tanh" if args.precision == "fp16_tanh" else "none")
+    pa = {"default": B.FNO_PREACT_DEFAULT, "none": B.FNO_PREACT_NONE,
+          "tanh": B.FNO_PREACT_TANH, "clip": B.FNO_PREACT_HARD_CLIP}[args.preact]
+    storage = "fp16" if args.precision == "fp16_tanh" else "fp32"
+    # the oracle's name of this mode (cpu_baseline leg)
+    omode = {"none": storage, "tanh": storage + "_tanh",
+             "clip": f"{storage}_clip:{float(np.float32(args.clip))!r}"}[preact]
     kind = {"tucker": B.FNO_WEIGHT_TUCKER, "cp": B.FNO_WEIGHT_CP}.get(wl.weight,
                                                                     B.FNO_WEIGHT_DENSE)
     pol = B.FNO_PATH_MIN_RESULT if args.policy == "min_result" else B.FNO_PATH_MIN_NET
     x = synth.make_x(wl, npdt)
     gy = synth.make_gy(wl, npdt)
     w = synth.make_weight(wl, npdt)
-    layer = SpectralConv(wl.n, wl.modes, wl.batch, wl.c_in, wl.c_out, pc, kind, wl.rank, pol)
+    layer = SpectralConv(wl.n, wl.modes, wl.batch, wl.c_in, wl.c_out, pc, kind, wl.rank, pol,
+                         preact=pa, clip=args.clip)
     dev = lambda a: torch.from_numpy(np.ascontiguousarray(a)).cuda()  # noqa: E731
     xd, gyd = dev(x), dev(gy)
     wd = ({"core": dev(w["core"]), "u_in": dev(w["u_in"]), "u_out": dev(w["u_out"]),
@@ -276,7 +298,7 @@ def main():
     wall = time.perf_counter() - t0
     ms_step = ev0.elapsed_time(ev1) / args.steps
     value = wl.batch / (ms_step / 1e3)
-    sbytes = step_bytes(wl, es, caches)
+    sbytes = step_bytes(wl, es, caches, preact)
 
     # per-kernel durations: the library brackets each launch with HIP events
     B.fno_profile_reset()
@@ -287,7 +309,7 @@ def main():
     prof = B.fno_profile_read()
     B.fno_profile_enable(False)
     B.fno_profile_reset()
-    kb = kernel_bytes(wl, es)
+    kb = kernel_bytes(wl, es, preact)
     kernels = {}
     for name, (n, tot) in prof.items():
         avg = tot / max(n, 1)
@@ -318,7 +340,9 @@ def main():
                 "datasets; random-init weights)",
         "config": {"workload": wl.name, "batch": wl.batch, "c_in": wl.c_in, "c_out": wl.c_out,
                    "grid": list(wl.n), "modes": list(wl.modes), "weights": wl.weight,
-                   "precision": args.precision, "spectral_caches": caches,
+                   "precision": args.precision, "preactivation": preact,
+                   **({"clip": args.clip} if preact == "clip" else {}),
+                   "spectral_caches": caches,
                    "backward": "separate" if args.separate_bwd else "combined",
                    "launch": "stream" if args.no_graph else "hip_graph",
                    "path_policy": args.policy if wl.weight != "dense" else None},
@@ -331,7 +355,7 @@ def main():
         "wall_s_timed": round(wall, 3),
     }
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(wl, x, w, gy, args.precision, args.cpu_seconds)
+        out["cpu_baseline"] = cpu_baseline(wl, x, w, gy, omode, args.cpu_seconds)
     print(json.dumps(out), flush=True)
 
 
