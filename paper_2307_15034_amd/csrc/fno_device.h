@@ -45,16 +45,25 @@ struct MM<_Float16> {
   static __device__ __forceinline__ frag neg(const frag& a) { return -a; }
 };
 
+// fp32: one fragment is four k-steps of v_mfma_f32_16x16x4_f32 over a
+// 16-wide k-block, lane group g holding k = 4 g + s at sub-step s (A and B
+// agree, so the four steps sum the whole block).  Each lane then reads its
+// four k-values of a row with one 16-byte load.
 template <>
 struct MM<float> {
-  static constexpr int KPL = 1;
-  static constexpr int KSTEP = 4;
-  typedef float frag;
+  static constexpr int KPL = 4;
+  static constexpr int KSTEP = 16;
+  typedef f4 frag;
   static __device__ __forceinline__ f4 mma(const frag& a, const frag& b, const f4& c) {
-    return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
+    f4 d = __builtin_amdgcn_mfma_f32_16x16x4f32(a[0], b[0], c, 0, 0, 0);
+    d = __builtin_amdgcn_mfma_f32_16x16x4f32(a[1], b[1], d, 0, 0, 0);
+    d = __builtin_amdgcn_mfma_f32_16x16x4f32(a[2], b[2], d, 0, 0, 0);
+    return __builtin_amdgcn_mfma_f32_16x16x4f32(a[3], b[3], d, 0, 0, 0);
   }
-  static __device__ __forceinline__ frag zero() { return 0.0f; }
-  static __device__ __forceinline__ frag ld(const float* p) { return *p; }
+  static __device__ __forceinline__ frag zero() { return f4{0.0f, 0.0f, 0.0f, 0.0f}; }
+  static __device__ __forceinline__ frag ld(const float* p) {
+    return *reinterpret_cast<const f4*>(p);
+  }
   static __device__ __forceinline__ frag neg(const frag& a) { return -a; }
 };
 
@@ -170,13 +179,21 @@ __device__ __forceinline__ h8 load_row_frag<_Float16>(const _Float16* row, int n
 }
 
 template <>
-__device__ __forceinline__ float load_row_frag<float>(const float* row, int n0, int Nb,
-                                                      bool vrow, int act, float clip,
-                                                      int vec) {
-  float v = 0.0f;
-  if (vrow && n0 < Nb) {
-    v = row[n0];
-    if (act) v = preact_f32(v, act, clip);
+__device__ __forceinline__ f4 load_row_frag<float>(const float* row, int n0, int Nb,
+                                                   bool vrow, int act, float clip, int vec) {
+  f4 v = f4{0.0f, 0.0f, 0.0f, 0.0f};
+  if (vrow) {
+    if (vec) {
+      if (n0 < Nb) v = *reinterpret_cast<const f4*>(row + n0);
+    } else {
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        if (n0 + i < Nb) v[i] = row[n0 + i];
+    }
+    if (act) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) v[i] = preact_f32(v[i], act, clip);
+    }
   }
   return v;
 }
