@@ -53,6 +53,10 @@ def parse():
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--cpu-seconds", type=float, default=12.0)
     p.add_argument("--profile-steps", type=int, default=20)
+    p.add_argument("--summarize", metavar="DIR",
+                   help="write profiles/ summaries of the workload from rocprofv3 output "
+                        "under DIR (trace/, FETCH_SIZE/, WRITE_SIZE/, copy_FETCH_SIZE/, "
+                        "copy_WRITE_SIZE/, each holding run_*.csv); no GPU")
     p.add_argument("--copy-probe", action="store_true",
                    help="only run a plain elementwise kernel that reads 1 GiB and writes "
                         "1 GiB, three times (the calibration of the FETCH_SIZE / WRITE_SIZE "
@@ -201,8 +205,130 @@ def copy_probe(torch):
                       "dispatches": 3}))
 
 
+# rocprofv3 kernel symbols -> the names the library times its launches under
+# (first match wins; the template flag "true" marks the pre-activation
+# variant of a transform)
+KERNEL_NAMES = [
+    (r"r2c_\w+<[^>]*true>", "r2c_plane_tanh"),
+    (r"r2c_\w+<", "r2c_plane"),
+    (r"slab_adj_wgrad_kernel", "contract_adjoint_wgrad"),
+    (r"slab_kernel<", "contract"),
+    (r"c2r_\w+<[^>]*true>", "c2r_plane_tanh_grad"),
+    (r"c2r_\w+<", "c2r_plane"),
+]
+
+
+def _logical(kname):
+    import re
+    for pat, name in KERNEL_NAMES:
+        if re.search(pat, kname):
+            return name
+    return kname
+
+
+def _csv(path):
+    import csv
+    with open(path, newline="") as f:
+        return list(csv.DictReader(f))
+
+
+def summarize(args):
+    """profiles/traffic_<workload>.json and profiles/layer_step_<workload>.md
+    from the rocprofv3 runs listed in the summary: durations from the kernel
+    trace, HBM bytes from FETCH_SIZE / WRITE_SIZE (KiB per dispatch, median
+    over the dispatches of a kernel) scaled by what the same counters read for
+    the copy probe (1 GiB read, 1 GiB written)."""
+    import statistics
+    wl = __import__("synth").WORKLOADS[args.workload]
+    d = args.summarize
+    trace = _csv(os.path.join(d, "trace", "run_kernel_trace.csv"))
+    stats = _csv(os.path.join(d, "trace", "run_kernel_stats.csv"))
+
+    def counter(sub, name):
+        per = {}
+        for r in _csv(os.path.join(d, sub, "run_counter_collection.csv")):
+            if r["Counter_Name"] == name:
+                per.setdefault(r["Kernel_Name"], []).append(float(r["Counter_Value"]) * 1024)
+        return per
+
+    gib = float(1 << 30)
+    cf = counter("copy_FETCH_SIZE", "FETCH_SIZE")
+    cw = counter("copy_WRITE_SIZE", "WRITE_SIZE")
+    # the probe's kernel is the one that moves the most bytes
+    f_cal = gib / statistics.median(max(cf.values(), key=statistics.median))
+    w_cal = gib / statistics.median(max(cw.values(), key=statistics.median))
+    fetch = counter("FETCH_SIZE", "FETCH_SIZE")
+    write = counter("WRITE_SIZE", "WRITE_SIZE")
+    dur = {}
+    for r in trace:
+        dur.setdefault(r["Kernel_Name"], []).append(
+            (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3)
+    es = 2 if args.precision == "fp16_tanh" else 4
+    kb = kernel_bytes(wl, es)
+    tr = {"workload": wl.name, "src_hash": kernel_sources_hash(),
+          "calibration": {"fetch": f_cal, "write": w_cal}, "kernels": {}}
+    rows = []
+    for kname, ds in sorted(dur.items(), key=lambda kv: -sum(kv[1])):
+        name = _logical(kname)
+        if name not in kb or kname not in fetch or kname not in write:
+            continue
+        fb = statistics.median(fetch[kname]) * f_cal
+        wb = statistics.median(write[kname]) * w_cal
+        tr["kernels"][name] = {"fetch_bytes": int(fb), "write_bytes": int(wb),
+                               "bytes": int(fb + wb)}
+        avg = sum(ds) / len(ds)
+        rows.append(f"| {name} | {len(ds)} | {avg:.1f} | {min(ds):.1f} | {max(ds):.1f} | "
+                    f"{kb[name] / 1e6:.1f} | {kb[name] / avg / 1e3:.0f} | {fb / 1e6:.1f} | "
+                    f"{wb / 1e6:.1f} | {(fb + wb) / kb[name]:.2f} |")
+    os.makedirs(os.path.join(ROOT, "profiles"), exist_ok=True)
+    with open(os.path.join(ROOT, "profiles", f"traffic_{wl.name}.json"), "w") as f:
+        json.dump(tr, f, indent=1)
+    cmd = ("cd /tmp && export TMPDIR=/tmp && rocprofv3 {what} --output-format csv "
+           "-d <out>/{sub} -o run -- python3 /root/repo/bench.py {extra}")
+    wk = f"--workload {args.workload} " if args.workload != 2 else ""
+    cmds = [
+        cmd.format(what="--kernel-trace --stats", sub="trace",
+                   extra=f"{wk}--steps 20 --warmup 5 --no-cpu-baseline"),
+        cmd.format(what="--pmc FETCH_SIZE", sub="FETCH_SIZE",
+                   extra=f"{wk}--steps 2 --warmup 1 --profile-steps 1 --no-cpu-baseline"),
+        cmd.format(what="--pmc WRITE_SIZE", sub="WRITE_SIZE",
+                   extra=f"{wk}--steps 2 --warmup 1 --profile-steps 1 --no-cpu-baseline"),
+        cmd.format(what="--pmc FETCH_SIZE", sub="copy_FETCH_SIZE", extra="--copy-probe"),
+        cmd.format(what="--pmc WRITE_SIZE", sub="copy_WRITE_SIZE", extra="--copy-probe"),
+        f"python3 bench.py {wk}--summarize <out>",
+    ]
+    total_avg = sum(sum(ds) / len(ds) for k, ds in dur.items() if _logical(k) in kb)
+    lines = [
+        f"# Layer step kernels, workload {wl.name} (fp16+tanh, {wl.weight}, spectral caches, "
+        "combined backward)", "",
+        "MI355X, one GPU. Durations from the rocprofv3 kernel trace of the timed benchmark",
+        "(kernel begin/end timestamps, all dispatches of the run); HBM traffic from the",
+        "FETCH_SIZE and WRITE_SIZE counters (KiB per dispatch, median over dispatches) scaled",
+        "by the factors that an elementwise probe kernel reading 1 GiB and writing 1 GiB",
+        f"(bench.py --copy-probe) gives for the same counters (FETCH x{f_cal:.3f}, "
+        f"WRITE x{w_cal:.3f}).",
+        f"Kernel sources hash {tr['src_hash']}.", "", "Commands:", ""]
+    lines += ["    " + c for c in cmds]
+    lines += ["", "| kernel | dispatches | avg us | min us | max us | alg MB | alg GB/s (avg) | "
+                  "HBM fetch MB | HBM write MB | traffic / alg |",
+              "|---|---|---|---|---|---|---|---|---|---|"] + rows
+    lines += ["", f"Sum of kernel averages per step: {total_avg:.1f} us.", "",
+              "rocprofv3 --stats summary (all dispatches):", "",
+              "| name | calls | avg ns | min ns | max ns | % |", "|---|---|---|---|---|---|"]
+    for r in stats:
+        lines.append(f"| {r['Name'][:70]} | {r['Calls']} | {float(r['AverageNs']):.0f} | "
+                     f"{float(r['MinNs']):.0f} | {float(r['MaxNs']):.0f} | "
+                     f"{float(r['Percentage']):.2f} |")
+    with open(os.path.join(ROOT, "profiles", f"layer_step_{wl.name}.md"), "w") as f:
+        f.write("\n".join(lines) + "\n")
+    print(json.dumps(tr))
+
+
 def main():
     args = parse()
+    if args.summarize:
+        summarize(args)
+        return
     if args.gpus != 1:
         print(json.dumps({"error": "this layer runs on one GPU; multi-GPU runs are not "
                                    "part of this build (see the sharding design)",

@@ -10,7 +10,12 @@
 // walks K in stages of 16 through LDS (operands converted to fp32 and
 // conjugated on the way in); each complex product is three real
 // v_mfma_f32_16x16x4_f32 products (Gauss: ar br, ai bi, (ar + ai)(br + bi)),
-// fp32 accumulation.  Long reductions over few results are split over work-groups
+// fp32 accumulation.  When both operands are stored in fp16 (the spectra,
+// the factors and the fp16 intermediates of the half-precision mode) the
+// tiles stay fp16 in LDS and each complex product is four real
+// v_mfma_f32_16x16x16_f16 products (ar br - ai bi, ar bi + ai br): the
+// products of fp16 values are exact in the fp32 accumulator, so this equals
+// the fp32 form up to summation order, with a quarter of its matrix-core time.  Long reductions over few results are split over work-groups
 // (split-K); the partial sums are then added in split order by a second
 // kernel, so the result does not depend on scheduling.
 #include <hip/hip_runtime.h>
@@ -18,6 +23,7 @@
 
 #include <algorithm>
 #include <climits>
+#include <type_traits>
 #include <utility>
 #include <vector>
 
@@ -28,9 +34,12 @@ namespace fno {
 namespace {
 
 constexpr int GM_SUB = PW_MAXIDX;  // sub-indices per class
-constexpr int GM_TK = 16;          // k per LDS stage (four MFMA k-steps)
-constexpr int GM_LS = GM_TK + 4;   // LDS row stride (floats): 16 rows of a
-                                   // fragment read start in disjoint banks
+constexpr int GM_TK = 16;          // k per LDS stage, fp32 tiles (four MFMA k-steps)
+constexpr int GM_TKH = 16;         // k per LDS stage, fp16 tiles (one MFMA k-step;
+                                   // 32 measured slower)
+// LDS row stride (elements) of a stage tk deep: 16 rows of a fragment read
+// start in disjoint banks
+__host__ __device__ constexpr int gm_ls(int tk) { return tk + 4; }
 constexpr int GM_KCHUNK = 2048;    // most contracted elements per work-group
 enum { CL_BT = 0, CL_M = 1, CL_N = 2, CL_K = 3 };
 
@@ -92,30 +101,33 @@ __device__ __forceinline__ void store_c(void* p, int elem, int64_t off, float re
     reinterpret_cast<f2*>(p)[off] = f2{re, im};
 }
 
-// One operand tile (rows x GM_TK) of a stage into registers.  With 64 or
+// One operand tile (rows x TK) of a stage into registers.  With 64 or
 // more rows a thread takes four consecutive k of one row (four loads) and
-// writes them to LDS as one 16-byte access in the layout the MFMA fragments
+// writes them to LDS as one 16-byte (fp32) or 8-byte (fp16) access in the layout the MFMA fragments
 // are read in (no bank conflicts); lanes run along the row's k quads
 // (KFAST) or along the rows.  Smaller tiles: one element per thread.
-template <int ROWS>
+template <int ROWS, int TK>
 struct TileLoader {
-  static constexpr int NE = ROWS * GM_TK / 256;
+  static constexpr int NE = ROWS * TK / 256;
   static constexpr bool QUAD = ROWS >= 64;
+  static constexpr int QPR = TK / 4;  // k quads per row
+  static constexpr int LS = gm_ls(TK);
+  static_assert(NE >= 1 && (!QUAD || NE % 4 == 0), "tile shape");
   float re[NE], im[NE];
   __device__ __forceinline__ static void slot(bool kfast, int e, int& r, int& kk) {
     const int t = threadIdx.x;
     if (QUAD) {
       const int q = e >> 2, j = e & 3;  // quad q of this thread, element j
       if (kfast) {
-        kk = (t & 3) * 4 + j;
-        r = (t >> 2) + 64 * q;
+        kk = (t % QPR) * 4 + j;
+        r = t / QPR + (256 / QPR) * q;
       } else {
         r = t % ROWS;
         kk = (t / ROWS + (256 / ROWS) * q) * 4 + j;
       }
     } else if (kfast) {
-      kk = t & (GM_TK - 1);
-      r = (t >> 4) + 16 * e;
+      kk = t % TK;
+      r = t / TK + (256 / TK) * e;
     } else {
       r = t % ROWS;
       kk = t / ROWS + (256 / ROWS) * e;
@@ -135,38 +147,46 @@ struct TileLoader {
       im[e] = conj ? -v[1] : v[1];
     }
   }
-  __device__ __forceinline__ void store(bool kfast, float* lre, float* lim) const {
+  // ST float: the fp32 tiles; ST _Float16: fp16 tiles (values loaded from
+  // fp16 storage, so the conversion back is exact).
+  template <typename ST>
+  __device__ __forceinline__ void store(bool kfast, ST* lre, ST* lim) const {
+    typedef ST v4 __attribute__((ext_vector_type(4)));
     if (QUAD) {
 #pragma unroll
       for (int q = 0; q < NE / 4; ++q) {
         int r, kk;
         slot(kfast, 4 * q, r, kk);
-        *reinterpret_cast<f4*>(lre + r * GM_LS + kk) =
-            f4{re[4 * q], re[4 * q + 1], re[4 * q + 2], re[4 * q + 3]};
-        *reinterpret_cast<f4*>(lim + r * GM_LS + kk) =
-            f4{im[4 * q], im[4 * q + 1], im[4 * q + 2], im[4 * q + 3]};
+        *reinterpret_cast<v4*>(lre + r * LS + kk) =
+            v4{(ST)re[4 * q], (ST)re[4 * q + 1], (ST)re[4 * q + 2], (ST)re[4 * q + 3]};
+        *reinterpret_cast<v4*>(lim + r * LS + kk) =
+            v4{(ST)im[4 * q], (ST)im[4 * q + 1], (ST)im[4 * q + 2], (ST)im[4 * q + 3]};
       }
     } else {
 #pragma unroll
       for (int e = 0; e < NE; ++e) {
         int r, kk;
         slot(kfast, e, r, kk);
-        lre[r * GM_LS + kk] = re[e];
-        lim[r * GM_LS + kk] = im[e];
+        lre[r * LS + kk] = (ST)re[e];
+        lim[r * LS + kk] = (ST)im[e];
       }
     }
   }
 };
 
 // TM x TN result tile per work-group of four waves, WGM of them along M.
-template <int TM, int TN, int WGM>
+// H: both operands stored in fp16 (fp16 tiles, fp16 matrix-core products).
+template <int TM, int TN, int WGM, bool H>
 __global__ __launch_bounds__(256) void pair_gemm_kernel(GemmArgs g) {
   constexpr int WGN = 4 / WGM;
   constexpr int WM = TM / WGM, WN = TN / WGN;
   constexpr int FM = WM / 16, FN = WN / 16;
   static_assert(FM >= 1 && FN >= 1 && WM % 16 == 0 && WN % 16 == 0, "tile shape");
-  __shared__ __align__(16) float As[2][TM * GM_LS];
-  __shared__ __align__(16) float Bs[2][TN * GM_LS];
+  typedef typename std::conditional<H, _Float16, float>::type ST;
+  constexpr int TK = H ? GM_TKH : GM_TK;
+  constexpr int LS = gm_ls(TK);
+  __shared__ __align__(16) ST As[2][TM * LS];
+  __shared__ __align__(16) ST Bs[2][TN * LS];
   __shared__ int32_t moA[TM], noB[TN];
   __shared__ int64_t moR[TM], noR[TN];
   __shared__ float mmul[TM], nmul[TN];
@@ -225,10 +245,10 @@ __global__ __launch_bounds__(256) void pair_gemm_kernel(GemmArgs g) {
 #pragma unroll
     for (int j = 0; j < FN; ++j) t1[i][j] = t2[i][j] = t3[i][j] = f4zero();
 
-  TileLoader<TM> la;
-  TileLoader<TN> lb;
+  TileLoader<TM, TK> la;
+  TileLoader<TN, TK> lb;
   const bool akf = g.a_kfast != 0, bkf = g.b_kfast != 0;
-  const int nst = (klen + GM_TK - 1) / GM_TK;
+  const int nst = (klen + TK - 1) / TK;
   la.load(g.a, g.a_elem, g.conj_a, akf, baA, moA, koA, 0, klen);
   lb.load(g.b, g.b_elem, g.conj_b, bkf, baB, noB, koB, 0, klen);
   for (int st = 0; st < nst; ++st) {
@@ -236,8 +256,41 @@ __global__ __launch_bounds__(256) void pair_gemm_kernel(GemmArgs g) {
     lb.store(bkf, Bs[0], Bs[1]);
     __syncthreads();
     if (st + 1 < nst) {  // next stage in flight during this one's products
-      la.load(g.a, g.a_elem, g.conj_a, akf, baA, moA, koA, (st + 1) * GM_TK, klen);
-      lb.load(g.b, g.b_elem, g.conj_b, bkf, baB, noB, koB, (st + 1) * GM_TK, klen);
+      la.load(g.a, g.a_elem, g.conj_a, akf, baA, moA, koA, (st + 1) * TK, klen);
+      lb.load(g.b, g.b_elem, g.conj_b, bkf, baB, noB, koB, (st + 1) * TK, klen);
+    }
+    if constexpr (H) {
+      // lane (r16, gq) holds k = 16 ks + 4 gq .. + 3 of k-step ks (A and B
+      // alike), one v_mfma_f32_16x16x16_f16 per real product:
+      // t1 = Re = ar br + (-ai) bi, t2 = Im = ar bi + ai br.
+#pragma unroll
+      for (int ks = 0; ks < TK / 16; ++ks) {
+        h4 ar[FM], ai[FM], nai[FM], br[FN], bi[FN];
+#pragma unroll
+        for (int i = 0; i < FM; ++i) {
+          const int row = wm * WM + i * 16 + r16;
+          ar[i] = *reinterpret_cast<const h4*>(&As[0][row * LS + 16 * ks + 4 * gq]);
+          ai[i] = *reinterpret_cast<const h4*>(&As[1][row * LS + 16 * ks + 4 * gq]);
+          nai[i] = -ai[i];
+        }
+#pragma unroll
+        for (int j = 0; j < FN; ++j) {
+          const int col = wn * WN + j * 16 + r16;
+          br[j] = *reinterpret_cast<const h4*>(&Bs[0][col * LS + 16 * ks + 4 * gq]);
+          bi[j] = *reinterpret_cast<const h4*>(&Bs[1][col * LS + 16 * ks + 4 * gq]);
+        }
+#pragma unroll
+        for (int i = 0; i < FM; ++i)
+#pragma unroll
+          for (int j = 0; j < FN; ++j) {
+            t1[i][j] = __builtin_amdgcn_mfma_f32_16x16x16f16(ar[i], br[j], t1[i][j], 0, 0, 0);
+            t1[i][j] = __builtin_amdgcn_mfma_f32_16x16x16f16(nai[i], bi[j], t1[i][j], 0, 0, 0);
+            t2[i][j] = __builtin_amdgcn_mfma_f32_16x16x16f16(ar[i], bi[j], t2[i][j], 0, 0, 0);
+            t2[i][j] = __builtin_amdgcn_mfma_f32_16x16x16f16(ai[i], br[j], t2[i][j], 0, 0, 0);
+          }
+      }
+      __syncthreads();
+      continue;
     }
     // lane (r16, gq) holds k = 4 gq + s of MFMA k-step s (A and B alike).
     // Complex product with three real products (Gauss): t1 = ar br,
@@ -246,15 +299,15 @@ __global__ __launch_bounds__(256) void pair_gemm_kernel(GemmArgs g) {
 #pragma unroll
     for (int i = 0; i < FM; ++i) {
       const int row = wm * WM + i * 16 + r16;
-      ar[i] = *reinterpret_cast<const f4*>(&As[0][row * GM_LS + 4 * gq]);
-      ai[i] = *reinterpret_cast<const f4*>(&As[1][row * GM_LS + 4 * gq]);
+      ar[i] = *reinterpret_cast<const f4*>(&As[0][row * LS + 4 * gq]);
+      ai[i] = *reinterpret_cast<const f4*>(&As[1][row * LS + 4 * gq]);
       as[i] = ar[i] + ai[i];
     }
 #pragma unroll
     for (int j = 0; j < FN; ++j) {
       const int col = wn * WN + j * 16 + r16;
-      br[j] = *reinterpret_cast<const f4*>(&Bs[0][col * GM_LS + 4 * gq]);
-      bi[j] = *reinterpret_cast<const f4*>(&Bs[1][col * GM_LS + 4 * gq]);
+      br[j] = *reinterpret_cast<const f4*>(&Bs[0][col * LS + 4 * gq]);
+      bi[j] = *reinterpret_cast<const f4*>(&Bs[1][col * LS + 4 * gq]);
       bs[j] = br[j] + bi[j];
     }
 #pragma unroll
@@ -274,8 +327,13 @@ __global__ __launch_bounds__(256) void pair_gemm_kernel(GemmArgs g) {
   for (int i = 0; i < FM; ++i)
 #pragma unroll
     for (int j = 0; j < FN; ++j) {
-      cr[i][j] = t1[i][j] - t2[i][j];
-      ci[i][j] = t3[i][j] - t1[i][j] - t2[i][j];
+      if constexpr (H) {
+        cr[i][j] = t1[i][j];
+        ci[i][j] = t2[i][j];
+      } else {
+        cr[i][j] = t1[i][j] - t2[i][j];
+        ci[i][j] = t3[i][j] - t1[i][j] - t2[i][j];
+      }
     }
 
   // D: lane holds rows 4 gq + v, column r16 of each 16 x 16 tile
@@ -487,10 +545,12 @@ hipError_t launch_pair_gemm(const PairArgs& p, hipStream_t s) {
   } else {
     cfg = 2, TM = 64, TN = 64;
   }
+  const bool half = g.a_elem == ELEM_F16 && g.b_elem == ELEM_F16;
+  const int tk = half ? GM_TKH : GM_TK;
   g.tiles_m = (int)((M + TM - 1) / TM);
   g.tiles_n = (int)((N + TN - 1) / TN);
   const int64_t tiles = (int64_t)g.tiles_m * g.tiles_n * Bt;
-  const int64_t nst = (K + GM_TK - 1) / GM_TK;
+  const int64_t nst = (K + tk - 1) / tk;
   const int64_t total = Bt * M * N;
   // split-K: at least enough splits for the per-work-group offset table,
   // more while the tiles alone leave the chip idle (>= 4 stages a split),
@@ -502,17 +562,27 @@ hipError_t launch_pair_gemm(const PairArgs& p, hipStream_t s) {
   if (need > 1 && cap < need) return hipErrorNotSupported;
   const int64_t splits = want > 1 ? std::max(need, std::min(want, cap)) : 1;
   const int64_t kst = (nst + splits - 1) / splits;
-  g.kchunk = (int)(kst * GM_TK);
+  g.kchunk = (int)(kst * tk);
   g.splits = (int)std::max<int64_t>(1, (K + g.kchunk - 1) / g.kchunk);
   const int64_t blocks = tiles * g.splits;
   if (blocks <= 0 || blocks > 0x7fffffffll) return hipErrorNotSupported;
   dim3 grid((unsigned)blocks), block(256);
-  switch (cfg) {
-    case 0: hipLaunchKernelGGL((pair_gemm_kernel<128, 16, 4>), grid, block, 0, s, g); break;
-    case 1: hipLaunchKernelGGL((pair_gemm_kernel<128, 32, 4>), grid, block, 0, s, g); break;
-    case 3: hipLaunchKernelGGL((pair_gemm_kernel<16, 128, 1>), grid, block, 0, s, g); break;
-    case 4: hipLaunchKernelGGL((pair_gemm_kernel<32, 128, 1>), grid, block, 0, s, g); break;
-    default: hipLaunchKernelGGL((pair_gemm_kernel<64, 64, 2>), grid, block, 0, s, g); break;
+  if (half) {
+    switch (cfg) {
+      case 0: hipLaunchKernelGGL((pair_gemm_kernel<128, 16, 4, true>), grid, block, 0, s, g); break;
+      case 1: hipLaunchKernelGGL((pair_gemm_kernel<128, 32, 4, true>), grid, block, 0, s, g); break;
+      case 3: hipLaunchKernelGGL((pair_gemm_kernel<16, 128, 1, true>), grid, block, 0, s, g); break;
+      case 4: hipLaunchKernelGGL((pair_gemm_kernel<32, 128, 1, true>), grid, block, 0, s, g); break;
+      default: hipLaunchKernelGGL((pair_gemm_kernel<64, 64, 2, true>), grid, block, 0, s, g); break;
+    }
+  } else {
+    switch (cfg) {
+      case 0: hipLaunchKernelGGL((pair_gemm_kernel<128, 16, 4, false>), grid, block, 0, s, g); break;
+      case 1: hipLaunchKernelGGL((pair_gemm_kernel<128, 32, 4, false>), grid, block, 0, s, g); break;
+      case 3: hipLaunchKernelGGL((pair_gemm_kernel<16, 128, 1, false>), grid, block, 0, s, g); break;
+      case 4: hipLaunchKernelGGL((pair_gemm_kernel<32, 128, 1, false>), grid, block, 0, s, g); break;
+      default: hipLaunchKernelGGL((pair_gemm_kernel<64, 64, 2, false>), grid, block, 0, s, g); break;
+    }
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || g.splits == 1) return e;

@@ -115,7 +115,7 @@ struct WgradArgs {
   float scale;
 };
 
-// Generic pairwise complex contraction for the Tucker path (fp32 complex
+// Generic pairwise complex contraction for the Tucker path (fp32 or fp16 complex
 // intermediates; operand element type given per operand).
 //   out[m, n, ...] (batch, free-A, free-B index groups, row-major in the
 //   result's own index order) = sum_k A * B, with optional conjugation.
@@ -124,7 +124,7 @@ struct PairArgs {
   const void* a;
   const void* b;
   void* out;           // complex of out_elem
-  int a_elem, b_elem;  // Elem of each operand (intermediates are F32)
+  int a_elem, b_elem;  // Elem of each operand
   int out_elem;
   int conj_a, conj_b;
   int64_t out_size;

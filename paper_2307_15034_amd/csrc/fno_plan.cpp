@@ -1170,7 +1170,11 @@ fno_status run_tucker_path(const fno_conv_desc* d, const Plan* pl, bool adjoint,
   ops.push_back({w->u_in, labs[2], g.elem, cj});
   ops.push_back({w->u_out, labs[3], g.elem, cj});
   for (int j = 0; j < d->ndim; ++j) ops.push_back({w->u_mode[j], labs[4 + j], g.elem, cj});
-  // split-K partial sums first, then one fp32 buffer per intermediate
+  // split-K partial sums first, then one buffer per intermediate (sized for
+  // fp32 complex).  Intermediates take the storage type: fp32 in the fp32
+  // mode, fp16 in the half-precision mode, where the whole contraction runs
+  // in half precision as the paper's mixed-precision layer does (products
+  // exact in fp32 accumulators, each intermediate rounded once to fp16).
   void* part = scratch;
   size_t off = kPairPartBytes;
   const char clast = kSpatial[d->ndim - 1];
@@ -1185,7 +1189,7 @@ fno_status run_tucker_path(const fno_conv_desc* d, const Plan* pl, bool adjoint,
     } else {
       dst = scratch + off;
       off += (size_t)round_up(label_size(ps.res, sz) * 8, 256);
-      oelem = ELEM_F32;
+      oelem = g.elem;
     }
     fno_status r = run_pair(sz, ops[ps.p], ops[ps.q], ps.res, dst, oelem, 1.0f,
                             last ? clast : 0, g.Nb, s, part);
