@@ -530,9 +530,14 @@ hipError_t launch_pair_gemm(const PairArgs& p, hipStream_t s) {
     return hipErrorNotSupported;
   const int64_t M = g.c[CL_M].size, N = g.c[CL_N].size, K = g.c[CL_K].size;
   const int64_t Bt = g.c[CL_BT].size;
-  // Elementwise and outer products (K < 4) and large batches of tiny dot
-  // products waste the tile: the generic kernels take those.
-  if (K < 4 || (M * N < 16 && Bt * M * N > 4096)) return hipErrorNotSupported;
+  // Elementwise and outer products (K < 4), large batches of tiny dot
+  // products, and large batches of small products with short reductions
+  // (at most 16 x 16 results and 64 contracted elements per batch entry:
+  // most of a 128 x 16 tile would be padding, one stage per work-group)
+  // waste the tile: the generic kernels take those.
+  if (K < 4 || (M * N < 16 && Bt * M * N > 4096) ||
+      (M <= 16 && N <= 16 && K <= 64 && Bt * M * N > 4096))
+    return hipErrorNotSupported;
   int cfg, TM, TN;
   if (N <= 16) {
     cfg = 0, TM = 128, TN = 16;
