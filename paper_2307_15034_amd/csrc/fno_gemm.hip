@@ -60,6 +60,7 @@ struct GemmArgs {
   int a_elem, b_elem, out_elem, conj_a, conj_b;
   GemmClass c[4];
   int a_kfast, b_kfast;  // staging order: lanes along k (else along m / n)
+  int a_vec, b_vec;      // quads of k consecutive and 4-aligned in memory
   int tiles_m, tiles_n, splits, kchunk;
   float scale;
   int Nb;
@@ -133,9 +134,42 @@ struct TileLoader {
       kk = t / ROWS + (256 / ROWS) * e;
     }
   }
-  __device__ __forceinline__ void load(const void* p, int elem, int conj, bool kfast, int32_t base,
-                                       const int32_t* roff, const int32_t* koff, int k0,
-                                       int klen) {
+  // vec: the four k of a quad are consecutive elements in memory, starting
+  // at an offset that is a multiple of four (checked on the host): one 16-byte
+  // (fp16) or two 16-byte (fp32) loads per quad instead of four, so the
+  // address unit sees a quarter of the instructions.
+  __device__ __forceinline__ void load(const void* p, int elem, int conj, bool kfast, bool vec,
+                                       int32_t base, const int32_t* roff, const int32_t* koff,
+                                       int k0, int klen) {
+    if (QUAD && kfast && vec) {
+#pragma unroll
+      for (int q = 0; q < NE / 4; ++q) {
+        int r, kk;
+        slot(kfast, 4 * q, r, kk);
+        const int32_t ro = roff[r];
+        f4 vr = f4zero(), vi = f4zero();
+        // klen is a multiple of four, so a quad is either whole or outside
+        if (ro >= 0 && k0 + kk < klen) {
+          const int32_t off = base + ro + koff[k0 + kk];
+          if (elem == ELEM_F16) {
+            const h8 v = *reinterpret_cast<const h8*>(reinterpret_cast<const h2*>(p) + off);
+            vr = f4{(float)v[0], (float)v[2], (float)v[4], (float)v[6]};
+            vi = f4{(float)v[1], (float)v[3], (float)v[5], (float)v[7]};
+          } else {
+            const f4* fp = reinterpret_cast<const f4*>(reinterpret_cast<const f2*>(p) + off);
+            const f4 v0 = fp[0], v1 = fp[1];
+            vr = f4{v0[0], v0[2], v1[0], v1[2]};
+            vi = f4{v0[1], v0[3], v1[1], v1[3]};
+          }
+        }
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          re[4 * q + j] = vr[j];
+          im[4 * q + j] = conj ? -vi[j] : vi[j];
+        }
+      }
+      return;
+    }
 #pragma unroll
     for (int e = 0; e < NE; ++e) {
       int r, kk;
@@ -249,15 +283,16 @@ __global__ __launch_bounds__(256) void pair_gemm_kernel(GemmArgs g) {
   TileLoader<TN, TK> lb;
   const bool akf = g.a_kfast != 0, bkf = g.b_kfast != 0;
   const int nst = (klen + TK - 1) / TK;
-  la.load(g.a, g.a_elem, g.conj_a, akf, baA, moA, koA, 0, klen);
-  lb.load(g.b, g.b_elem, g.conj_b, bkf, baB, noB, koB, 0, klen);
+  const bool avc = g.a_vec != 0, bvc = g.b_vec != 0;
+  la.load(g.a, g.a_elem, g.conj_a, akf, avc, baA, moA, koA, 0, klen);
+  lb.load(g.b, g.b_elem, g.conj_b, bkf, bvc, baB, noB, koB, 0, klen);
   for (int st = 0; st < nst; ++st) {
     la.store(akf, As[0], As[1]);
     lb.store(bkf, Bs[0], Bs[1]);
     __syncthreads();
     if (st + 1 < nst) {  // next stage in flight during this one's products
-      la.load(g.a, g.a_elem, g.conj_a, akf, baA, moA, koA, (st + 1) * TK, klen);
-      lb.load(g.b, g.b_elem, g.conj_b, bkf, baB, noB, koB, (st + 1) * TK, klen);
+      la.load(g.a, g.a_elem, g.conj_a, akf, avc, baA, moA, koA, (st + 1) * TK, klen);
+      lb.load(g.b, g.b_elem, g.conj_b, bkf, bvc, baB, noB, koB, (st + 1) * TK, klen);
     }
     if constexpr (H) {
       // lane (r16, gq) holds k = 16 ks + 4 gq .. + 3 of k-step ks (A and B
@@ -530,6 +565,26 @@ hipError_t launch_pair_gemm(const PairArgs& p, hipStream_t s) {
     return hipErrorNotSupported;
   const int64_t M = g.c[CL_M].size, N = g.c[CL_N].size, K = g.c[CL_K].size;
   const int64_t Bt = g.c[CL_BT].size;
+  // 16-byte quad loads for an operand staged along k: the innermost
+  // contracted sub-index has unit stride in it and an extent that is a
+  // multiple of four, and every other stride of it is a multiple of four (so
+  // quads start 16-byte aligned; operands are 16-byte aligned)
+  auto quad_vec = [&](bool kfast, int which) {
+    const GemmClass& ck = g.c[CL_K];
+    if (!kfast || ck.n == 0) return 0;
+    const int in = ck.n - 1;
+    const int64_t s_in = which == 0 ? ck.sa[in] : ck.sb[in];
+    if (s_in != 1 || ck.ext[in] % 4 != 0) return 0;
+    for (int c = 0; c < 4; ++c)
+      for (int j = 0; j < g.c[c].n; ++j) {
+        if (c == CL_K && j == in) continue;
+        const int64_t st = which == 0 ? g.c[c].sa[j] : g.c[c].sb[j];
+        if (st % 4 != 0) return 0;
+      }
+    return 1;
+  };
+  g.a_vec = quad_vec(g.a_kfast != 0, 0);
+  g.b_vec = quad_vec(g.b_kfast != 0, 1);
   // Elementwise and outer products (K < 4), large batches of tiny dot
   // products, and large batches of small products with short reductions
   // (at most 16 x 16 results and 64 contracted elements per batch entry:

@@ -1191,13 +1191,26 @@ fno_status run_tucker_path(const fno_conv_desc* d, const Plan* pl, bool adjoint,
       off += (size_t)round_up(label_size(ps.res, sz) * 8, 256);
       oelem = g.elem;
     }
-    fno_status r = run_pair(sz, ops[ps.p], ops[ps.q], ps.res, dst, oelem, 1.0f,
+    // Storage order of an intermediate: the path's index order with the
+    // last spatial index moved innermost where present, so that rows of the
+    // spectrum stay contiguous (an outer product with the last axis' factor
+    // would otherwise put the rank index, a few elements wide, innermost and
+    // scatter the next step's loads).  The path itself is unchanged.
+    std::string store = ps.res;
+    if (!last) {
+      const size_t pos = store.find(clast);
+      if (pos != std::string::npos && pos + 1 != store.size()) {
+        store.erase(pos, 1);
+        store += clast;
+      }
+    }
+    fno_status r = run_pair(sz, ops[ps.p], ops[ps.q], store, dst, oelem, 1.0f,
                             last ? clast : 0, g.Nb, s, part);
     if (r != FNO_OK) return r;
     std::vector<Opnd> next;
     for (int k = 0; k < (int)ops.size(); ++k)
       if (k != ps.p && k != ps.q) next.push_back(ops[k]);
-    next.push_back({dst, ps.res, oelem, 0});
+    next.push_back({dst, store, oelem, 0});
     ops.swap(next);
   }
   return FNO_OK;
