@@ -252,13 +252,18 @@ def summarize(args):
         return per
 
     gib = float(1 << 30)
-    cf = counter("copy_FETCH_SIZE", "FETCH_SIZE")
-    cw = counter("copy_WRITE_SIZE", "WRITE_SIZE")
-    # the probe's kernel is the one that moves the most bytes
-    f_cal = gib / statistics.median(max(cf.values(), key=statistics.median))
-    w_cal = gib / statistics.median(max(cw.values(), key=statistics.median))
-    fetch = counter("FETCH_SIZE", "FETCH_SIZE")
-    write = counter("WRITE_SIZE", "WRITE_SIZE")
+    # counter runs are optional: without them only the trace is summarised
+    have_pmc = os.path.isdir(os.path.join(d, "FETCH_SIZE"))
+    f_cal = w_cal = 1.0
+    fetch, write = {}, {}
+    if have_pmc:
+        cf = counter("copy_FETCH_SIZE", "FETCH_SIZE")
+        cw = counter("copy_WRITE_SIZE", "WRITE_SIZE")
+        # the probe's kernel is the one that moves the most bytes
+        f_cal = gib / statistics.median(max(cf.values(), key=statistics.median))
+        w_cal = gib / statistics.median(max(cw.values(), key=statistics.median))
+        fetch = counter("FETCH_SIZE", "FETCH_SIZE")
+        write = counter("WRITE_SIZE", "WRITE_SIZE")
     dur = {}
     for r in trace:
         dur.setdefault(r["Kernel_Name"], []).append(
@@ -271,6 +276,10 @@ def summarize(args):
     for kname, ds in sorted(dur.items(), key=lambda kv: -sum(kv[1])):
         name = _logical(kname)
         if name not in kb or kname not in fetch or kname not in write:
+            if name in kb:
+                avg = sum(ds) / len(ds)
+                rows.append(f"| {name} | {len(ds)} | {avg:.1f} | {min(ds):.1f} | {max(ds):.1f} | "
+                            f"{kb[name] / 1e6:.1f} | {kb[name] / avg / 1e3:.0f} | - | - | - |")
             continue
         fb = statistics.median(fetch[kname]) * f_cal
         wb = statistics.median(write[kname]) * w_cal
@@ -281,11 +290,14 @@ def summarize(args):
                     f"{kb[name] / 1e6:.1f} | {kb[name] / avg / 1e3:.0f} | {fb / 1e6:.1f} | "
                     f"{wb / 1e6:.1f} | {(fb + wb) / kb[name]:.2f} |")
     os.makedirs(os.path.join(ROOT, "profiles"), exist_ok=True)
-    with open(os.path.join(ROOT, "profiles", f"traffic_{wl.name}.json"), "w") as f:
-        json.dump(tr, f, indent=1)
+    if have_pmc:
+        with open(os.path.join(ROOT, "profiles", f"traffic_{wl.name}.json"), "w") as f:
+            json.dump(tr, f, indent=1)
     cmd = ("cd /tmp && export TMPDIR=/tmp && rocprofv3 {what} --output-format csv "
            "-d <out>/{sub} -o run -- python3 /root/repo/bench.py {extra}")
     wk = f"--workload {args.workload} " if args.workload != 2 else ""
+    if wl.weight != "dense":
+        wk += f"--policy {args.policy} "
     cmds = [
         cmd.format(what="--kernel-trace --stats", sub="trace",
                    extra=f"{wk}--steps 20 --warmup 5 --no-cpu-baseline"),
@@ -297,29 +309,40 @@ def summarize(args):
         cmd.format(what="--pmc WRITE_SIZE", sub="copy_WRITE_SIZE", extra="--copy-probe"),
         f"python3 bench.py {wk}--summarize <out>",
     ]
+    if not have_pmc:
+        cmds = [cmds[0], cmds[-1]]
     total_avg = sum(sum(ds) / len(ds) for k, ds in dur.items() if _logical(k) in kb)
+    pol = f", {args.policy} path" if wl.weight != "dense" else ""
     lines = [
-        f"# Layer step kernels, workload {wl.name} (fp16+tanh, {wl.weight}, spectral caches, "
-        "combined backward)", "",
+        f"# Layer step kernels, workload {wl.name} (fp16+tanh, {wl.weight}{pol}, spectral "
+        "caches, combined backward)", "",
         "MI355X, one GPU. Durations from the rocprofv3 kernel trace of the timed benchmark",
-        "(kernel begin/end timestamps, all dispatches of the run); HBM traffic from the",
-        "FETCH_SIZE and WRITE_SIZE counters (KiB per dispatch, median over dispatches) scaled",
-        "by the factors that an elementwise probe kernel reading 1 GiB and writing 1 GiB",
-        f"(bench.py --copy-probe) gives for the same counters (FETCH x{f_cal:.3f}, "
-        f"WRITE x{w_cal:.3f}).",
-        f"Kernel sources hash {tr['src_hash']}.", "", "Commands:", ""]
+        "(kernel begin/end timestamps, all dispatches of the run)" + (
+            "; HBM traffic from the" if have_pmc else "."),
+    ]
+    if have_pmc:
+        lines += [
+            "FETCH_SIZE and WRITE_SIZE counters (KiB per dispatch, median over dispatches) "
+            "scaled",
+            "by the factors that an elementwise probe kernel reading 1 GiB and writing 1 GiB",
+            f"(bench.py --copy-probe) gives for the same counters (FETCH x{f_cal:.3f}, "
+            f"WRITE x{w_cal:.3f})."]
+    lines += [f"Kernel sources hash {tr['src_hash']}.", "", "Commands:", ""]
     lines += ["    " + c for c in cmds]
     lines += ["", "| kernel | dispatches | avg us | min us | max us | alg MB | alg GB/s (avg) | "
                   "HBM fetch MB | HBM write MB | traffic / alg |",
               "|---|---|---|---|---|---|---|---|---|---|"] + rows
-    lines += ["", f"Sum of kernel averages per step: {total_avg:.1f} us.", "",
+    lines += ["", f"Sum of the averages of the kernels in the table: {total_avg:.1f} us"
+                  + (" (the whole step)." if wl.weight == "dense" and wl.ndim < 3 else
+                     " (the other kernels of the step are in the summary below)."), "",
               "rocprofv3 --stats summary (all dispatches):", "",
               "| name | calls | avg ns | min ns | max ns | % |", "|---|---|---|---|---|---|"]
     for r in stats:
         lines.append(f"| {r['Name'][:70]} | {r['Calls']} | {float(r['AverageNs']):.0f} | "
                      f"{float(r['MinNs']):.0f} | {float(r['MaxNs']):.0f} | "
                      f"{float(r['Percentage']):.2f} |")
-    with open(os.path.join(ROOT, "profiles", f"layer_step_{wl.name}.md"), "w") as f:
+    suffix = f"_{args.policy}" if wl.weight != "dense" else ""
+    with open(os.path.join(ROOT, "profiles", f"layer_step_{wl.name}{suffix}.md"), "w") as f:
         f.write("\n".join(lines) + "\n")
     print(json.dumps(tr))
 
