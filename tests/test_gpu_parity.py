@@ -168,6 +168,10 @@ TUCKER_EDGE = [
     ((8, 8), (2, 3), 2, 3, 4, (2, 3, 2, 2)),
     ((6, 10, 12), (2, 3, 4), 2, 3, 2, (2, 2, 2, 3, 2)),
     ((40,), (7,), 3, 2, 5, (3, 2, 4)),
+    # ranks and C_in multiples of 4 but not of 16: GEMM steps whose operands
+    # are staged as 16-byte quads of contiguous contracted elements, with
+    # contractions that end in a partial stage
+    ((16, 24), (4, 5), 3, 12, 20, (4, 8, 2, 4)),
 ]
 
 
