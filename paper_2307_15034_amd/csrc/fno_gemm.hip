@@ -613,11 +613,11 @@ hipError_t launch_pair_gemm(const PairArgs& p, hipStream_t s) {
   const int64_t nst = (K + tk - 1) / tk;
   const int64_t total = Bt * M * N;
   // split-K: at least enough splits for the per-work-group offset table,
-  // more while the tiles alone leave the chip idle (>= 4 stages a split),
+  // more while the tiles alone leave the chip idle (>= 2 stages a split),
   // as many as the partial-sum area holds
   const int64_t need = (K + GM_KCHUNK - 1) / GM_KCHUNK;
   int64_t want = need;
-  if (tiles < 512) want = std::max(want, std::min<int64_t>(nst / 4, (1024 + tiles - 1) / tiles));
+  if (tiles < 512) want = std::max(want, std::min<int64_t>(nst / 2, (1024 + tiles - 1) / tiles));
   const int64_t cap = p.part ? (int64_t)(p.part_cap / (size_t)(total * 8)) : 0;
   if (need > 1 && cap < need) return hipErrorNotSupported;
   const int64_t splits = want > 1 ? std::max(need, std::min(want, cap)) : 1;
