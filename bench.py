@@ -13,7 +13,11 @@ The timed steps replay the step's launches captured once as a HIP graph
 (--no-graph launches every kernel from the host instead); the per-kernel
 figures come from separate, eagerly launched steps.
 
-    python bench.py [--steps K] [--warmup W] [--workload 2] [--no-cpu-baseline]
+    python bench.py [--steps K] [--warmup W] [--workload 3] [--no-cpu-baseline]
+
+The default workload is the largest single-GPU one, the 2-D 1024 x 1024 layer
+(B = 8, C_in = C_out = 64, 64 x 64 retained modes): 5.97 GB of algorithmic
+HBM traffic per step.
 """
 from __future__ import annotations
 
@@ -37,7 +41,7 @@ def parse():
     p.add_argument("--gpus", type=int, default=1)
     p.add_argument("--steps", type=int, default=200)
     p.add_argument("--warmup", type=int, default=20)
-    p.add_argument("--workload", type=int, default=2)
+    p.add_argument("--workload", type=int, default=3)
     p.add_argument("--precision", choices=["fp16_tanh", "fp32"], default="fp16_tanh")
     p.add_argument("--preact", choices=["default", "none", "tanh", "clip"], default="default",
                    help="pre-activation (default: tanh in fp16_tanh, none in fp32)")
@@ -57,6 +61,9 @@ def parse():
                    help="write profiles/ summaries of the workload from rocprofv3 output "
                         "under DIR (trace/, FETCH_SIZE/, WRITE_SIZE/, copy_FETCH_SIZE/, "
                         "copy_WRITE_SIZE/, each holding run_*.csv); no GPU")
+    p.add_argument("--summarize-sq", metavar="DIR",
+                   help="write profiles/sq_counters_<workload>.md from the two SQ counter "
+                        "runs under DIR (sq1/, sq2/) and the kernel trace (trace/); no GPU")
     p.add_argument("--copy-probe", action="store_true",
                    help="only run a plain elementwise kernel that reads 1 GiB and writes "
                         "1 GiB, three times (the calibration of the FETCH_SIZE / WRITE_SIZE "
@@ -82,7 +89,9 @@ def kernel_bytes(wl, es, preact="tanh"):
         "c2r_plane_tanh_grad": spec_in + 2 * B * Ci * N * es,
         "wgrad": spec_in + spec_out + Ci * Co * K * 2 * 4,
     }
-    out["contract_adjoint_wgrad"] = out["contract_adjoint"] + out["wgrad"]  # one launch
+    # one launch: G read once (shared by both products), W read, gXhat
+    # written, Xhat read, gW written
+    out["contract_adjoint_wgrad"] = spec_out + W + spec_in + spec_in + Ci * Co * K * 2 * 4
     out["r2c_plane_tanh"] = B * Ci * N * es + spec_in     # input transform (tanh)
     out["r2c_plane"] = B * Co * N * es + spec_out         # gradient transform
     out["r2c_plane_clip"] = out["r2c_plane_tanh"]
@@ -153,11 +162,12 @@ def cpu_baseline(wl, x, w, gy, prec, seconds):
     `seconds` of CPU time."""
     from oracle import fno_oracle as O
     import synth
+    host_cores = len(os.sched_getaffinity(0))
     try:
         from threadpoolctl import threadpool_info
         threads = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
     except Exception:  # pragma: no cover
-        threads = len(os.sched_getaffinity(0))
+        threads = host_cores
     oprec = prec
     done = 0
     t0 = time.perf_counter()
@@ -185,7 +195,7 @@ def cpu_baseline(wl, x, w, gy, prec, seconds):
         if el >= seconds:
             break
     return {"value": done / el, "unit": "samples/s", "cores": int(threads),
-            "kind": "oracle",
+            "host_cores": int(host_cores), "kind": "oracle",
             "sample": f"{done} batch samples of the workload (B=1 slices), float64 oracle "
                       f"fwd+bwd_data+bwd_weight, {el:.1f} s"}
 
@@ -203,6 +213,28 @@ def copy_probe(torch):
     torch.cuda.synchronize()
     print(json.dumps({"copy_probe_bytes_read": n * 4, "copy_probe_bytes_written": n * 4,
                       "dispatches": 3}))
+
+
+def copy_bandwidth(torch, nbytes=1 << 30, reps=10):
+    """A plain device-to-device copy of `nbytes` (torch's copy kernel), timed
+    with HIP events: (read + written bytes) / time, in GB/s.  The practical
+    streaming rate of this GPU, reported beside the 8 TB/s peak."""
+    a = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
+    a.fill_(1)
+    b = torch.empty_like(a)
+    for _ in range(2):
+        b.copy_(a)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        b.copy_(a)
+    e1.record()
+    torch.cuda.synchronize()
+    gbs = 2.0 * nbytes * reps / (e0.elapsed_time(e1) / 1e3) / 1e9
+    del a, b
+    torch.cuda.empty_cache()
+    return gbs
 
 
 # rocprofv3 kernel symbols -> the names the library times its launches under
@@ -264,6 +296,14 @@ def summarize(args):
         w_cal = gib / statistics.median(max(cw.values(), key=statistics.median))
         fetch = counter("FETCH_SIZE", "FETCH_SIZE")
         write = counter("WRITE_SIZE", "WRITE_SIZE")
+    # the HIP-event figures bench.py printed in the same (traced) run
+    ev = {}
+    tlog = os.path.join(d, "trace.log")
+    if os.path.exists(tlog):
+        for line in open(tlog):
+            line = line.strip()
+            if line.startswith("{") and '"kernels"' in line:
+                ev = {k: v["avg_ms"] * 1e3 for k, v in json.loads(line)["kernels"].items()}
     dur = {}
     for r in trace:
         dur.setdefault(r["Kernel_Name"], []).append(
@@ -275,19 +315,22 @@ def summarize(args):
     rows = []
     for kname, ds in sorted(dur.items(), key=lambda kv: -sum(kv[1])):
         name = _logical(kname)
+        evs = f"{ev[name]:.1f}" if name in ev else "-"
         if name not in kb or kname not in fetch or kname not in write:
             if name in kb:
                 avg = sum(ds) / len(ds)
-                rows.append(f"| {name} | {len(ds)} | {avg:.1f} | {min(ds):.1f} | {max(ds):.1f} | "
-                            f"{kb[name] / 1e6:.1f} | {kb[name] / avg / 1e3:.0f} | - | - | - |")
+                rows.append(f"| {name} | {len(ds)} | {avg:.1f} | {evs} | {min(ds):.1f} | "
+                            f"{max(ds):.1f} | {kb[name] / 1e6:.1f} | {kb[name] / avg / 1e3:.0f} | "
+                            f"{kb[name] / avg / 1e3 / HBM_PEAK_GBS:.3f} | - | - | - |")
             continue
         fb = statistics.median(fetch[kname]) * f_cal
         wb = statistics.median(write[kname]) * w_cal
         tr["kernels"][name] = {"fetch_bytes": int(fb), "write_bytes": int(wb),
                                "bytes": int(fb + wb)}
         avg = sum(ds) / len(ds)
-        rows.append(f"| {name} | {len(ds)} | {avg:.1f} | {min(ds):.1f} | {max(ds):.1f} | "
-                    f"{kb[name] / 1e6:.1f} | {kb[name] / avg / 1e3:.0f} | {fb / 1e6:.1f} | "
+        rows.append(f"| {name} | {len(ds)} | {avg:.1f} | {evs} | {min(ds):.1f} | {max(ds):.1f} | "
+                    f"{kb[name] / 1e6:.1f} | {kb[name] / avg / 1e3:.0f} | "
+                    f"{kb[name] / avg / 1e3 / HBM_PEAK_GBS:.3f} | {fb / 1e6:.1f} | "
                     f"{wb / 1e6:.1f} | {(fb + wb) / kb[name]:.2f} |")
     os.makedirs(os.path.join(ROOT, "profiles"), exist_ok=True)
     if have_pmc:
@@ -295,12 +338,12 @@ def summarize(args):
             json.dump(tr, f, indent=1)
     cmd = ("cd /tmp && export TMPDIR=/tmp && rocprofv3 {what} --output-format csv "
            "-d <out>/{sub} -o run -- python3 /root/repo/bench.py {extra}")
-    wk = f"--workload {args.workload} " if args.workload != 2 else ""
+    wk = f"--workload {args.workload} " if args.workload != 3 else ""
     if wl.weight != "dense":
         wk += f"--policy {args.policy} "
     cmds = [
         cmd.format(what="--kernel-trace --stats", sub="trace",
-                   extra=f"{wk}--steps 20 --warmup 5 --no-cpu-baseline"),
+                   extra=f"{wk}--steps 20 --warmup 5 --no-cpu-baseline") + " > <out>/trace.log",
         cmd.format(what="--pmc FETCH_SIZE", sub="FETCH_SIZE",
                    extra=f"{wk}--steps 2 --warmup 1 --profile-steps 1 --no-cpu-baseline"),
         cmd.format(what="--pmc WRITE_SIZE", sub="WRITE_SIZE",
@@ -329,9 +372,12 @@ def summarize(args):
             f"WRITE x{w_cal:.3f})."]
     lines += [f"Kernel sources hash {tr['src_hash']}.", "", "Commands:", ""]
     lines += ["    " + c for c in cmds]
-    lines += ["", "| kernel | dispatches | avg us | min us | max us | alg MB | alg GB/s (avg) | "
-                  "HBM fetch MB | HBM write MB | traffic / alg |",
-              "|---|---|---|---|---|---|---|---|---|---|"] + rows
+    lines += ["", "\"avg us\" is the trace's average over all dispatches; \"events us\" the "
+                  "average that", "bench.py's own HIP events measured in the same run (the "
+                  "figure its JSON line uses);", "\"frac\" = alg MB / trace avg / 8 TB/s.", "",
+              "| kernel | dispatches | avg us | events us | min us | max us | alg MB | "
+              "alg GB/s (avg) | frac | HBM fetch MB | HBM write MB | traffic / alg |",
+              "|---|---|---|---|---|---|---|---|---|---|---|---|"] + rows
     lines += ["", f"Sum of the averages of the kernels in the table: {total_avg:.1f} us"
                   + (" (the whole step)." if wl.weight == "dense" and wl.ndim < 3 else
                      " (the other kernels of the step are in the summary below)."), "",
@@ -347,10 +393,90 @@ def summarize(args):
     print(json.dumps(tr))
 
 
+SQ_PASSES = {
+    "sq1": "SQ_WAVES SQ_INSTS_VALU SQ_INSTS_LDS SQ_INSTS_MFMA SQ_VALU_MFMA_BUSY_CYCLES "
+           "SQ_INSTS_VALU_MFMA_MOPS_F16 SQ_WAVE_CYCLES SQ_BUSY_CYCLES GRBM_GUI_ACTIVE",
+    "sq2": "SQ_WAIT_ANY SQ_WAIT_INST_ANY SQ_ACTIVE_INST_VALU SQ_ACTIVE_INST_LDS "
+           "SQ_ACTIVE_INST_VMEM SQ_LDS_BANK_CONFLICT SQ_INSTS_SALU SQ_INSTS_VMEM_RD",
+}
+SIMDS = 256 * 4          # MI355X: 256 compute units of four SIMDs
+MFMA_F16_PEAK_TFS = 2500.0
+
+
+def summarize_sq(args):
+    """profiles/sq_counters_<workload>.md: instruction, stall and matrix-core
+    counters of one profiled step per kernel (chip-wide sums per dispatch,
+    median over a kernel's dispatches).  Matrix-core utilisation is
+    SQ_VALU_MFMA_BUSY_CYCLES / (GRBM_GUI_ACTIVE x SIMDs); the fp16 matrix rate
+    is 512 x SQ_INSTS_VALU_MFMA_MOPS_F16 flops over the kernel's trace
+    duration, against the 2.5 PFLOP/s dense fp16 peak."""
+    import statistics
+    wl = __import__("synth").WORKLOADS[args.workload]
+    d = args.summarize_sq
+    vals = {}
+    for sub in SQ_PASSES:
+        for r in _csv(os.path.join(d, sub, "run_counter_collection.csv")):
+            key = (r["Kernel_Name"], r.get("Grid_Size", ""))
+            vals.setdefault(key, {}).setdefault(r["Counter_Name"], {}).setdefault(
+                r.get("Dispatch_Id", "0"), 0.0)
+            vals[key][r["Counter_Name"]][r.get("Dispatch_Id", "0")] += float(r["Counter_Value"])
+    dur = {}
+    tpath = os.path.join(d, "trace", "run_kernel_trace.csv")
+    if os.path.exists(tpath):
+        for r in _csv(tpath):
+            dur.setdefault(r["Kernel_Name"], []).append(
+                (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3)
+    med = lambda m, c: statistics.median(m[c].values()) if c in m else float("nan")  # noqa
+    rows = []
+    for (kname, grid), m in sorted(vals.items(), key=lambda kv: -med(kv[1], "SQ_WAVE_CYCLES")):
+        if _logical(kname) == kname and "fno::" not in kname:
+            continue
+        wc = med(m, "SQ_WAVE_CYCLES")
+        util = 100.0 * med(m, "SQ_VALU_MFMA_BUSY_CYCLES") / (med(m, "GRBM_GUI_ACTIVE") * SIMDS)
+        flops = 512.0 * med(m, "SQ_INSTS_VALU_MFMA_MOPS_F16")
+        avg = (sum(dur[kname]) / len(dur[kname])) if kname in dur else float("nan")
+        tfs = flops / (avg * 1e-6) / 1e12
+        short = kname.replace("void ", "").replace("fno::", "").split("(")[0][:48]
+        rows.append(
+            f"| {short} | {grid} | {avg:.1f} | {util:.1f} | {flops / 1e9:.2f} | {tfs:.0f} | "
+            f"{100 * tfs / MFMA_F16_PEAK_TFS:.1f} | {med(m, 'SQ_INSTS_VALU'):.3g} | "
+            f"{med(m, 'SQ_INSTS_MFMA'):.3g} | {med(m, 'SQ_INSTS_LDS'):.3g} | "
+            f"{med(m, 'SQ_LDS_BANK_CONFLICT'):.3g} | "
+            f"{100 * med(m, 'SQ_WAIT_ANY') / wc:.0f} | "
+            f"{100 * med(m, 'SQ_ACTIVE_INST_VALU') / wc:.0f} | "
+            f"{100 * med(m, 'SQ_ACTIVE_INST_LDS') / wc:.0f} |")
+    wk = f"--workload {args.workload} " if args.workload != 3 else ""
+    cmd = ("cd /tmp && export TMPDIR=/tmp && rocprofv3 --pmc {c} --output-format csv "
+           "-d <out>/{sub} -o run -- python3 /root/repo/bench.py {wk}--steps 2 --warmup 1 "
+           "--profile-steps 1 --no-cpu-baseline")
+    lines = [f"# SQ and matrix-core counters, workload {wl.name} (fp16+tanh, one step)", "",
+             "MI355X, one GPU. Chip-wide counter sums per dispatch, median over the "
+             "dispatches of a", "kernel with the same grid. Durations from the kernel "
+             "trace of the same sources.", f"Kernel sources hash {kernel_sources_hash()}.", "",
+             "Commands:", ""]
+    lines += ["    " + cmd.format(c=c, sub=sub, wk=wk) for sub, c in SQ_PASSES.items()]
+    lines += ["    (trace: the kernel-trace command of the layer-step summary, same sources)",
+              f"    python3 bench.py {wk}--summarize-sq <out>", "",
+              "Columns: trace average (us); MFMA busy = SQ_VALU_MFMA_BUSY_CYCLES / "
+              "(GRBM_GUI_ACTIVE x 1024 SIMDs);", "fp16 MFMA GFLOP per dispatch = 512 x "
+              "SQ_INSTS_VALU_MFMA_MOPS_F16, its rate over the trace average and the",
+              "fraction of the 2.5 PFLOP/s dense fp16 peak; instruction counts; LDS bank-"
+              "conflict cycles;", "wait / VALU-active / LDS-active as % of SQ_WAVE_CYCLES.", "",
+              "| kernel | grid | avg us | MFMA busy % | fp16 MFMA GFLOP | TFLOP/s | % of fp16 "
+              "peak | VALU insts | MFMA insts | LDS insts | LDS bank confl. | wait % | "
+              "VALU % | LDS % |",
+              "|---|---|---|---|---|---|---|---|---|---|---|---|---|---|"] + rows
+    with open(os.path.join(ROOT, "profiles", f"sq_counters_{wl.name}.md"), "w") as f:
+        f.write("\n".join(lines) + "\n")
+
+
 def main():
     args = parse()
     if args.summarize:
         summarize(args)
+        return
+    if args.summarize_sq:
+        summarize_sq(args)
         return
     if args.gpus != 1:
         print(json.dumps({"error": "this layer runs on one GPU; multi-GPU runs are not "
@@ -474,11 +600,14 @@ def main():
         kernels[name] = e
     dom = max(kernels, key=lambda k: kernels[k]["ms_per_step"])
     dk = kernels[dom]
+    copy_gbs = copy_bandwidth(torch)
     roof = {"bound": "hbm", "kernel": dom, "achieved": round(dk.get("gbs", 0.0), 1),
             "peak": HBM_PEAK_GBS, "unit": "GB/s",
             "frac": round(dk.get("gbs", 0.0) / HBM_PEAK_GBS, 4),
             "traffic": measured_traffic(wl.name, dom),
-            "avg_ms": round(dk["avg_ms"], 5), "alg_bytes": dk.get("alg_bytes")}
+            "avg_ms": round(dk["avg_ms"], 5), "alg_bytes": dk.get("alg_bytes"),
+            "copy_gbs": round(copy_gbs, 1),
+            "frac_of_copy": round(dk.get("gbs", 0.0) / copy_gbs, 4)}
 
     out = {
         "metric": METRIC, "value": round(value, 1), "unit": "samples/s", "n_gpus": 1,
@@ -498,6 +627,7 @@ def main():
         "step_alg_bytes": sbytes,
         "step_hbm_gbs": round(sbytes / (ms_step / 1e3) / 1e9, 1),
         "step_hbm_frac": round(sbytes / (ms_step / 1e3) / 1e9 / HBM_PEAK_GBS, 4),
+        "step_copy_frac": round(sbytes / (ms_step / 1e3) / 1e9 / copy_gbs, 4),
         "roofline": roof,
         "kernels": {k: {kk: (round(vv, 5) if isinstance(vv, float) else vv)
                         for kk, vv in v.items()} for k, v in kernels.items()},

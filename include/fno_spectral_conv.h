@@ -258,7 +258,13 @@ fno_status fno_profile_reset(void);
 fno_status fno_profile_read(int32_t index, char *name, int32_t name_cap, int64_t *launches,
                             double *total_ms);
 
-/* Frees every cached plan (device tables) of this process. */
+/* Drops every cached plan (device tables) of this process.  A plan that a
+ * call on another thread is using stays alive until that call returns;
+ * every other plan's tables are freed here.  The tables may still be read by
+ * kernels already enqueued: call this only when no work issued through the
+ * library is in flight (after a device or stream synchronisation).  HIP
+ * graphs captured earlier hold the freed table addresses: re-capture them
+ * (after one warm-up call) once the caches have been released. */
 fno_status fno_release_caches(void);
 
 const char *fno_status_string(fno_status status);

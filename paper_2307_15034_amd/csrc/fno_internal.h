@@ -207,8 +207,12 @@ size_t r2c_chain_lds_bytes(int nka, int ntb, int nta, int NaC, bool pre_lut);
 size_t c2r_chain_lds_bytes(int ng, int ntb, int Kap, int Na, bool grad_lut);
 constexpr int kChainWaves = 8;  // waves per work-group of the chained kernels
 
-// fp16 contraction / weight gradient on slabs of 16 modes (K % 16 == 0);
-// hipErrorNotSupported otherwise.
+// fp16 contraction / weight gradient on slabs of 16 modes (K % 16 == 0,
+// operands under 1 GiB: 32-bit buffer offsets); hipErrorNotSupported
+// otherwise.  The *_supported predicates say beforehand whether a launch
+// would be taken, so that callers pick the generic kernels instead.
+bool contract_slab_supported(const ContractArgs& a);
+bool wgrad_slab_supported(const WgradArgs& a);
 hipError_t launch_contract_slab(const ContractArgs& a, hipStream_t s);
 hipError_t launch_wgrad_slab(const WgradArgs& a, hipStream_t s);
 // Adjoint contraction and weight gradient in one launch (fp16 slab path).

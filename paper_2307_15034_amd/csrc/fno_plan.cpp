@@ -87,6 +87,16 @@ fno_status check_desc(const fno_conv_desc* d) {
   const int64_t Ka = nd >= 2 ? 2 * d->modes[nd - 2] : 1;
   if (Kb > 128 || Ka > 128) return FNO_ERR_UNSUPPORTED;
   if (nd == 3 && 2 * d->modes[0] > 4096) return FNO_ERR_UNSUPPORTED;
+  // launch-shape limits, checked here so that a call that cannot run is
+  // rejected before anything is enqueued: the 3-D leading-axis kernels put
+  // batch x channels on the second grid dimension, and the plane transforms
+  // count planes (batch x channels x the extents before the last two axes)
+  // in 31 bits
+  const int64_t cmax = d->c_in > d->c_out ? d->c_in : d->c_out;
+  if (nd == 3 && d->batch * cmax > 65535) return FNO_ERR_UNSUPPORTED;
+  int64_t planes = d->batch * cmax;
+  for (int j = 0; j + 2 < nd; ++j) planes *= d->n[j];
+  if (planes > 0x7fffffff) return FNO_ERR_UNSUPPORTED;
   return FNO_OK;
 }
 
@@ -347,6 +357,19 @@ struct Plan {
   std::vector<std::string> labels_fwd, labels_adj;
   std::string out_fwd, out_adj;
   int device = 0;
+  Plan() = default;
+  Plan(const Plan&) = delete;
+  Plan& operator=(const Plan&) = delete;
+  // the device tables go with the last reference (the cache's, or that of a
+  // call still running on another thread when the cache is released)
+  ~Plan() {
+    if (!t.base) return;
+    int cur = 0;
+    (void)hipGetDevice(&cur);
+    (void)hipSetDevice(device);
+    (void)hipFree(t.base);
+    (void)hipSetDevice(cur);
+  }
 };
 
 Geo make_geo(const fno_conv_desc* d) {
@@ -618,7 +641,7 @@ PlanKey key_of(const fno_conv_desc* d, int device) {
 }
 
 std::mutex g_mutex;
-std::map<PlanKey, std::unique_ptr<Plan>> g_plans;
+std::map<PlanKey, std::shared_ptr<Plan>> g_plans;
 
 fno_status build_tables(const fno_conv_desc* d, Plan* pl) {
   std::vector<size_t> off;
@@ -698,7 +721,10 @@ void host_plan(const fno_conv_desc* d, Plan* pl) {
   }
 }
 
-fno_status get_plan(const fno_conv_desc* d, Plan** out) {
+// The plan of a descriptor on the current device, built on first use.  The
+// caller holds a reference for the duration of its call, so a concurrent
+// fno_release_caches cannot free the tables under it.
+fno_status get_plan(const fno_conv_desc* d, std::shared_ptr<Plan>* out) {
   fno_status st = check_desc(d);
   if (st != FNO_OK) return st;
   int dev = 0;
@@ -708,10 +734,10 @@ fno_status get_plan(const fno_conv_desc* d, Plan** out) {
   std::lock_guard<std::mutex> lock(g_mutex);
   auto it = g_plans.find(key);
   if (it != g_plans.end()) {
-    *out = it->second.get();
+    *out = it->second;
     return FNO_OK;
   }
-  std::unique_ptr<Plan> pl(new Plan());
+  std::shared_ptr<Plan> pl = std::make_shared<Plan>();
   host_plan(d, pl.get());
   pl->device = dev;
   int ncu = 0;
@@ -720,7 +746,7 @@ fno_status get_plan(const fno_conv_desc* d, Plan** out) {
     pl->num_cu = ncu;
   st = build_tables(d, pl.get());
   if (st != FNO_OK) return st;
-  *out = pl.get();
+  *out = pl;
   g_plans[key] = std::move(pl);
   return FNO_OK;
 }
@@ -1079,7 +1105,7 @@ fno_status run_contract(const Plan* pl, const void* in, const void* w, void* out
   a.Nb = g.Nb;
   a.scale = 1.0f;
   if (g.K > 0x7fffffff / 2) return FNO_ERR_UNSUPPORTED;
-  const bool slab = g.elem == ELEM_F16 && g.K % 16 == 0;
+  const bool slab = g.elem == ELEM_F16 && g.K % 16 == 0 && contract_slab_supported(a);
   FNO_HIP(timed(adjoint ? "contract_adjoint" : "contract", s, [&] {
     return slab ? launch_contract_slab(a, s) : launch_contract(g.elem, a, s);
   }));
@@ -1626,8 +1652,9 @@ fno_status fno_spectral_conv_fwd(const fno_conv_desc* d, const void* x, const fn
   if (x_hat_out && !aligned16(x_hat_out)) return FNO_ERR_INVALID_ARGUMENT;
   if ((st = check_weights(d, w)) != FNO_OK) return st;
   if ((st = check_ws(d, FNO_OP_FWD, true, ws, ws_len)) != FNO_OK) return st;
-  Plan* pl = nullptr;
-  if ((st = get_plan(d, &pl)) != FNO_OK) return st;
+  std::shared_ptr<Plan> plan_ref;
+  if ((st = get_plan(d, &plan_ref)) != FNO_OK) return st;
+  Plan* pl = plan_ref.get();
   const Geo& g = pl->g;
   WsLayout L;
   char* base = (char*)ws;
@@ -1657,8 +1684,9 @@ fno_status fno_spectral_conv_bwd_data(const fno_conv_desc* d, const void* x,
   if (gy_hat_out && !aligned16(gy_hat_out)) return FNO_ERR_INVALID_ARGUMENT;
   if ((st = check_weights(d, w)) != FNO_OK) return st;
   if ((st = check_ws(d, FNO_OP_BWD_DATA, true, ws, ws_len)) != FNO_OK) return st;
-  Plan* pl = nullptr;
-  if ((st = get_plan(d, &pl)) != FNO_OK) return st;
+  std::shared_ptr<Plan> plan_ref;
+  if ((st = get_plan(d, &plan_ref)) != FNO_OK) return st;
+  Plan* pl = plan_ref.get();
   const Geo& g = pl->g;
   WsLayout L;
   char* base = (char*)ws;
@@ -1698,8 +1726,9 @@ fno_status fno_spectral_conv_bwd_weight(const fno_conv_desc* d, const void* x, c
   }
   const bool caches = x_hat && gy_hat;
   if ((st = check_ws(d, FNO_OP_BWD_WEIGHT, caches, ws, ws_len)) != FNO_OK) return st;
-  Plan* pl = nullptr;
-  if ((st = get_plan(d, &pl)) != FNO_OK) return st;
+  std::shared_ptr<Plan> plan_ref;
+  if ((st = get_plan(d, &plan_ref)) != FNO_OK) return st;
+  Plan* pl = plan_ref.get();
   const Geo& g = pl->g;
   WsLayout L;
   char* base = (char*)ws;
@@ -1734,7 +1763,7 @@ fno_status fno_spectral_conv_bwd_weight(const fno_conv_desc* d, const void* x, c
     a.Kb = g.Kb;
     a.Nb = g.Nb;
     a.scale = (float)std::sqrt((double)g.N);
-    const bool slab = g.elem == ELEM_F16 && g.K % 16 == 0;
+    const bool slab = g.elem == ELEM_F16 && g.K % 16 == 0 && wgrad_slab_supported(a);
     FNO_HIP(timed("wgrad", s, [&] {
       return slab ? launch_wgrad_slab(a, s) : launch_wgrad(g.elem, a, s);
     }));
@@ -1767,8 +1796,9 @@ fno_status fno_spectral_conv_bwd(const fno_conv_desc* d, const void* x, const fn
   }
   const bool cache = x_hat != nullptr;
   if ((st = check_ws(d, FNO_OP_BWD, cache, ws, ws_len)) != FNO_OK) return st;
-  Plan* pl = nullptr;
-  if ((st = get_plan(d, &pl)) != FNO_OK) return st;
+  std::shared_ptr<Plan> plan_ref;
+  if ((st = get_plan(d, &plan_ref)) != FNO_OK) return st;
+  Plan* pl = plan_ref.get();
   const Geo& g = pl->g;
   WsLayout L;
   char* base = (char*)ws;
@@ -1835,7 +1865,7 @@ fno_status fno_spectral_conv_bwd(const fno_conv_desc* d, const void* x, const fn
     FNO_HIP(timed("contract_adjoint_wgrad", s, [&] { return launch_adj_wgrad_slab(a, wa, s); }));
   } else {
     if ((st = run_contract(pl, gh, w->dense, gxs, true, s)) != FNO_OK) return st;
-    const bool slab = g.elem == ELEM_F16 && g.K % 16 == 0;
+    const bool slab = g.elem == ELEM_F16 && g.K % 16 == 0 && wgrad_slab_supported(wa);
     FNO_HIP(timed("wgrad", s, [&] {
       return slab ? launch_wgrad_slab(wa, s) : launch_wgrad(g.elem, wa, s);
     }));
@@ -1873,17 +1903,14 @@ fno_status fno_profile_read(int32_t index, char* name, int32_t name_cap, int64_t
 }
 
 fno_status fno_release_caches(void) {
-  std::lock_guard<std::mutex> lock(g_mutex);
-  int cur = 0;
-  (void)hipGetDevice(&cur);
-  for (auto& kv : g_plans) {
-    if (kv.second->t.base) {
-      (void)hipSetDevice(kv.second->device);
-      (void)hipFree(kv.second->t.base);
-    }
+  std::map<PlanKey, std::shared_ptr<Plan>> gone;
+  {
+    std::lock_guard<std::mutex> lock(g_mutex);
+    gone.swap(g_plans);
   }
-  (void)hipSetDevice(cur);
-  g_plans.clear();
+  // plans no call holds are destroyed here (their tables freed); a plan in
+  // use by a call on another thread goes when that call returns
+  gone.clear();
   return FNO_OK;
 }
 

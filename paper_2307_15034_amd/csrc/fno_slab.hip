@@ -374,6 +374,16 @@ hipError_t launch_wgrad_slab(const WgradArgs& a, hipStream_t st) {
   return slab_launch(SLAB_WGRAD, s, st);
 }
 
+bool contract_slab_supported(const ContractArgs& a) {
+  SlabArgs s;
+  return make_contract_slab(a, &s) && slab_blocks(s) > 0 && slab_blocks(s) <= 0x7fffffff;
+}
+
+bool wgrad_slab_supported(const WgradArgs& a) {
+  SlabArgs s;
+  return make_wgrad_slab(a, &s) && slab_blocks(s) > 0 && slab_blocks(s) <= 0x7fffffff;
+}
+
 bool adj_wgrad_slab_supported(const ContractArgs& adj, const WgradArgs& wg) {
   SlabArgs s1, s2;
   return adj.adjoint && make_contract_slab(adj, &s1) && make_wgrad_slab(wg, &s2) &&

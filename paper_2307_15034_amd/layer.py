@@ -13,13 +13,30 @@ import torch
 from . import binding as B
 
 
-def _addr(t: Optional[torch.Tensor]) -> int:
+def _addr(t: Optional[torch.Tensor], shape=None, dtype=None, name: str = "tensor",
+          device: Optional[torch.device] = None, min_bytes: Optional[int] = None) -> int:
+    """Device address of t after checking what the kernels assume of it: its
+    dtype and exact shape (or, for raw byte buffers, a minimum size), that it
+    is contiguous, and that it lives on the layer's GPU.  None gives 0."""
     if t is None:
         return 0
-    if not t.is_cuda:
-        raise ValueError("tensor must live on the GPU")
+    if not isinstance(t, torch.Tensor):
+        raise ValueError(f"{name}: expected a torch.Tensor, got {type(t).__name__}")
+    if dtype is not None and t.dtype != dtype:
+        raise ValueError(f"{name}: dtype {t.dtype}, expected {dtype}")
+    if shape is not None and tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name}: shape {tuple(t.shape)}, expected {tuple(shape)}")
+    if min_bytes is not None and t.numel() * t.element_size() < min_bytes:
+        raise ValueError(f"{name}: {t.numel() * t.element_size()} bytes, "
+                         f"at least {min_bytes} needed")
     if not t.is_contiguous():
-        raise ValueError("tensor must be contiguous")
+        raise ValueError(f"{name}: tensor must be contiguous")
+    if device is False:      # layout checks only (the caller checks devices later)
+        return 0
+    if not t.is_cuda:
+        raise ValueError(f"{name}: tensor must live on the GPU")
+    if device is not None and device.index is not None and t.device.index != device.index:
+        raise ValueError(f"{name}: on {t.device}, the layer runs on {device}")
     return t.data_ptr()
 
 
@@ -67,12 +84,65 @@ class SpectralConv:
         nbytes = B.fno_spectrum_bytes(self.desc, which)
         return torch.empty(max(nbytes, 16), dtype=torch.uint8, device=self.device)
 
-    def weights_struct(self, w) -> B.FnoWeights:
+    def _param_shapes(self):
+        """Shapes (without the trailing (re, im) axis) of the weight tensors:
+        {"dense": ...} or {"core", "u_in", "u_out", "u_mode": [...]}."""
         if self.weight_kind == B.FNO_WEIGHT_DENSE:
-            return B.weights_struct(dense=_addr(w))
-        return B.weights_struct(core=_addr(w["core"]), u_in=_addr(w["u_in"]),
-                                u_out=_addr(w["u_out"]),
-                                u_mode=[_addr(u) for u in w["u_mode"]])
+            return {"dense": (self.c_in, self.c_out) + self.kdims}
+        r = self.rank
+        d = len(self.n)
+        if self.weight_kind == B.FNO_WEIGHT_CP:
+            return {"core": (r[0],), "u_in": (self.c_in, r[0]), "u_out": (self.c_out, r[0]),
+                    "u_mode": [(k, r[0]) for k in self.kdims]}
+        return {"core": tuple(r[:2]) + tuple(r[2:2 + d]), "u_in": (self.c_in, r[0]),
+                "u_out": (self.c_out, r[1]),
+                "u_mode": [(self.kdims[j], r[2 + j]) for j in range(d)]}
+
+    def _params(self, w, dtype, what, device=None):
+        """Checked addresses of a weight (or gradient) set of this layer
+        (device=False: the layout checks only)."""
+        sh = self._param_shapes()
+        dev = self.device if device is None else device
+        chk = lambda t, shp, nm: _addr(t, shp + (2,), dtype, f"{what}.{nm}", dev)  # noqa: E731
+        if self.weight_kind == B.FNO_WEIGHT_DENSE:
+            if isinstance(w, dict):
+                raise ValueError(f"{what}: a dense layer takes one tensor")
+            return {"dense": chk(w, sh["dense"], "dense")}
+        if not isinstance(w, dict) or len(w.get("u_mode", [])) != len(self.n):
+            raise ValueError(f"{what}: expected core, u_in, u_out and {len(self.n)} u_mode")
+        return {"core": chk(w["core"], sh["core"], "core"),
+                "u_in": chk(w["u_in"], sh["u_in"], "u_in"),
+                "u_out": chk(w["u_out"], sh["u_out"], "u_out"),
+                "u_mode": [chk(u, shp, f"u_mode[{j}]")
+                           for j, (u, shp) in enumerate(zip(w["u_mode"], sh["u_mode"]))]}
+
+    def weights_struct(self, w) -> B.FnoWeights:
+        return B.weights_struct(**self._params(w, self.dtype, "w"))
+
+    def _x(self, t, name, c, device=None):
+        return _addr(t, (self.batch, c) + self.n, self.dtype, name,
+                     self.device if device is None else device)
+
+    def _spec(self, t, name, which, device=None):
+        return _addr(t, None, None, name, self.device if device is None else device,
+                     min_bytes=B.fno_spectrum_bytes(self.desc, which))
+
+    def _validate(self, x=None, w=None, gy=None, y=None, gx=None, x_hat=None, gy_hat=None,
+                  gw=None):
+        """Layout checks (dtype, shape, size, contiguity) of every argument of a
+        call, then device checks of every argument: a mistake in any argument
+        is reported before anything is allocated or enqueued."""
+        for dev in (False, None):
+            self._x(x, "x", self.c_in, dev)
+            self._x(gy, "gy", self.c_out, dev)
+            self._x(y, "y", self.c_out, dev)
+            self._x(gx, "gx", self.c_in, dev)
+            if w is not None:
+                self._params(w, self.dtype, "w", dev)
+            if gw is not None:
+                self._params(gw, torch.float32, "gw", dev)
+            self._spec(x_hat, "x_hat", 0, dev)
+            self._spec(gy_hat, "gy_hat", 1, dev)
 
     def alloc_grads(self):
         f = dict(dtype=torch.float32, device=self.device)
@@ -92,60 +162,66 @@ class SpectralConv:
                 "u_mode": [torch.empty((self.kdims[j], r[2 + j], 2), **f) for j in range(d)]}
 
     def grads_struct(self, g) -> B.FnoWeightGrads:
-        if self.weight_kind == B.FNO_WEIGHT_DENSE:
-            return B.grads_struct(dense=_addr(g))
-        return B.grads_struct(core=_addr(g["core"]), u_in=_addr(g["u_in"]),
-                              u_out=_addr(g["u_out"]), u_mode=[_addr(u) for u in g["u_mode"]])
+        return B.grads_struct(**self._params(g, torch.float32, "gw"))
 
     # -- the calls ---------------------------------------------------------------
+    # Every tensor argument is checked (dtype, shape, device) before anything
+    # is allocated or enqueued; outputs left as None are allocated afterwards.
+    def _out(self, t, c):
+        if t is None:
+            t = torch.empty((self.batch, c) + self.n, dtype=self.dtype, device=self.device)
+        return t
+
     def fwd(self, x: torch.Tensor, w, y: Optional[torch.Tensor] = None,
             x_hat: Optional[torch.Tensor] = None, stream: Optional[int] = None):
-        if y is None:
-            y = torch.empty((self.batch, self.c_out) + self.n, dtype=self.dtype,
-                            device=self.device)
+        self._validate(x=x, w=w, y=y, x_hat=x_hat)
+        y = self._out(y, self.c_out)
         ws = self.workspace(B.FNO_OP_FWD)
         s = torch.cuda.current_stream().cuda_stream if stream is None else stream
-        B.fno_spectral_conv_fwd(self.desc, _addr(x), self.weights_struct(w), _addr(y),
-                                _addr(x_hat), _addr(ws), ws.numel(), s)
+        B.fno_spectral_conv_fwd(self.desc, self._x(x, "x", self.c_in), self.weights_struct(w),
+                                self._x(y, "y", self.c_out), self._spec(x_hat, "x_hat", 0),
+                                _addr(ws), ws.numel(), s)
         return y
 
     def bwd_data(self, x: torch.Tensor, w, gy: torch.Tensor, gx: Optional[torch.Tensor] = None,
                  gy_hat: Optional[torch.Tensor] = None, stream: Optional[int] = None):
-        if gx is None:
-            gx = torch.empty((self.batch, self.c_in) + self.n, dtype=self.dtype,
-                             device=self.device)
+        self._validate(x=x, w=w, gy=gy, gx=gx, gy_hat=gy_hat)
+        gx = self._out(gx, self.c_in)
         ws = self.workspace(B.FNO_OP_BWD_DATA)
         s = torch.cuda.current_stream().cuda_stream if stream is None else stream
-        B.fno_spectral_conv_bwd_data(self.desc, _addr(x), self.weights_struct(w), _addr(gy),
-                                     _addr(gx), _addr(gy_hat), _addr(ws), ws.numel(), s)
+        B.fno_spectral_conv_bwd_data(self.desc, self._x(x, "x", self.c_in),
+                                     self.weights_struct(w), self._x(gy, "gy", self.c_out),
+                                     self._x(gx, "gx", self.c_in),
+                                     self._spec(gy_hat, "gy_hat", 1), _addr(ws), ws.numel(), s)
         return gx
 
     def bwd_weight(self, x: Optional[torch.Tensor], gy: Optional[torch.Tensor], w=None,
                    x_hat: Optional[torch.Tensor] = None, gy_hat: Optional[torch.Tensor] = None,
                    gw=None, stream: Optional[int] = None):
-        if gw is None:
-            gw = self.alloc_grads()
+        self._validate(x=x, w=w, gy=gy, x_hat=x_hat, gy_hat=gy_hat, gw=gw)
+        gw = self.alloc_grads() if gw is None else gw
         caches = x_hat is not None and gy_hat is not None
         ws = self.workspace(B.FNO_OP_BWD_WEIGHT, caches)
         s = torch.cuda.current_stream().cuda_stream if stream is None else stream
-        wstruct = self.weights_struct(w) if w is not None else B.weights_struct()
-        B.fno_spectral_conv_bwd_weight(self.desc, _addr(x), _addr(gy), wstruct, _addr(x_hat),
-                                       _addr(gy_hat), self.grads_struct(gw), _addr(ws),
-                                       ws.numel(), s)
+        wst = self.weights_struct(w) if w is not None else B.weights_struct()
+        B.fno_spectral_conv_bwd_weight(self.desc, self._x(x, "x", self.c_in),
+                                       self._x(gy, "gy", self.c_out), wst,
+                                       self._spec(x_hat, "x_hat", 0),
+                                       self._spec(gy_hat, "gy_hat", 1), self.grads_struct(gw),
+                                       _addr(ws), ws.numel(), s)
         return gw
 
     def bwd(self, x: Optional[torch.Tensor], w, gy: torch.Tensor,
             x_hat: Optional[torch.Tensor] = None, gx: Optional[torch.Tensor] = None, gw=None,
             gy_hat: Optional[torch.Tensor] = None, stream: Optional[int] = None):
         """Data and weight gradients in one call (returns gx, gw)."""
-        if gx is None:
-            gx = torch.empty((self.batch, self.c_in) + self.n, dtype=self.dtype,
-                             device=self.device)
-        if gw is None:
-            gw = self.alloc_grads()
+        self._validate(x=x, w=w, gy=gy, gx=gx, x_hat=x_hat, gy_hat=gy_hat, gw=gw)
+        gx = self._out(gx, self.c_in)
+        gw = self.alloc_grads() if gw is None else gw
         ws = self.workspace(B.FNO_OP_BWD, x_hat is not None)
         s = torch.cuda.current_stream().cuda_stream if stream is None else stream
-        B.fno_spectral_conv_bwd(self.desc, _addr(x), self.weights_struct(w), _addr(gy),
-                                _addr(x_hat), _addr(gx), self.grads_struct(gw), _addr(gy_hat),
-                                _addr(ws), ws.numel(), s)
+        B.fno_spectral_conv_bwd(self.desc, self._x(x, "x", self.c_in), self.weights_struct(w),
+                                self._x(gy, "gy", self.c_out), self._spec(x_hat, "x_hat", 0),
+                                self._x(gx, "gx", self.c_in), self.grads_struct(gw),
+                                self._spec(gy_hat, "gy_hat", 1), _addr(ws), ws.numel(), s)
         return gx, gw

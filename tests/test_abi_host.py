@@ -165,6 +165,28 @@ def test_cp_path_golden():
         assert (macs, peak) == (g[pol]["macs"], g[pol]["peak"])
 
 
+def test_tucker_path_golden_both_ops():
+    """The library's Tucker paths for the workload the golden sequences were
+    worked out for (hand-derived, tests/golden/tucker_paths.json): the
+    forward contraction and the data gradient's adjoint contraction."""
+    import json
+    with open(os.path.join(ROOT, "tests", "golden", "tucker_paths.json")) as f:
+        g = json.load(f)
+    sz = g["sizes"]
+    for policy, pol in [(B.FNO_PATH_MIN_RESULT, "min_result"), (B.FNO_PATH_MIN_NET, "min_net")]:
+        d = B.make_desc((256, 256), (32, 32), sz["b"], sz["i"], sz["o"], B.FNO_PREC_FP16_TANH,
+                        B.FNO_WEIGHT_TUCKER, (sz["a"], sz["e"], sz["c"], sz["d"]), policy)
+        for op, gg in [(B.FNO_OP_FWD, g), (B.FNO_OP_BWD_DATA, g["adjoint"])]:
+            got = B.fno_contraction_path(d, op)
+            exp = gg[pol]["steps"]
+            assert len(got) == len(exp)
+            for (p, q, mask), (ep, eq, eres, _) in zip(got, exp):
+                assert (p, q) == (ep, eq)
+                assert _mask_to_set(mask) == set(eres)
+            macs, peak = B.fno_contraction_path_cost(d, op)
+            assert (macs, peak) == (gg[pol]["macs"], gg[pol]["peak"])
+
+
 def test_cp_path_matches_oracle_random():
     rng = np.random.default_rng(19)
     for trial in range(150):
@@ -278,6 +300,23 @@ def test_unsupported_sizes():
     assert e.value.status == B.FNO_ERR_UNSUPPORTED
 
 
+@pytest.mark.parametrize("batch,c_in,c_out,ok", [
+    (1, 65535, 3, True), (1, 3, 65535, True), (1, 65536, 3, False), (1, 3, 65536, False),
+    (2, 32768, 1, False), (256, 255, 255, True), (256, 256, 2, False)])
+def test_3d_channel_batch_limit(batch, c_in, c_out, ok):
+    """The 3-D leading-axis kernels hold batch x channels on a grid axis of at
+    most 65535 entries (for the larger of the two channel counts); a
+    descriptor beyond that is rejected by the descriptor check, before any
+    call enqueues work."""
+    d = B.make_desc((8, 8, 8), (2, 2, 2), batch, c_in, c_out)
+    if ok:
+        B.fno_spectral_conv_workspace_size(d, B.FNO_OP_FWD)
+    else:
+        with pytest.raises(B.FnoError) as e:
+            B.fno_spectral_conv_workspace_size(d, B.FNO_OP_FWD)
+        assert e.value.status == B.FNO_ERR_UNSUPPORTED
+
+
 # Fake device addresses are only ever paired with a request that the host
 # rejects first (null / misaligned pointer or too small a workspace), so no
 # call below can reach a device.
@@ -335,3 +374,85 @@ def test_binding_has_no_cpu_fallback():
             if fn.endswith((".py", ".hip", ".cpp", ".h")):
                 txt = open(os.path.join(dirpath, fn)).read()
                 assert not pat.search(txt), fn
+
+
+# ---------------------------------------------------------------------------
+# The torch wrapper checks every tensor before anything reaches the library
+# (CPU tensors here: the dtype and shape checks come before the device check,
+# and every rejection happens before any allocation or call)
+# ---------------------------------------------------------------------------
+
+def _layer(**kw):
+    from paper_2307_15034_amd.layer import SpectralConv
+    args = dict(n=(16, 16), modes=(4, 4), batch=2, c_in=3, c_out=5)
+    args.update(kw)
+    return SpectralConv(**args)
+
+
+def _good(layer):
+    import torch
+    x = torch.zeros((2, 3, 16, 16), dtype=torch.float16)
+    w = torch.zeros((3, 5, 8, 4, 2), dtype=torch.float16)
+    gy = torch.zeros((2, 5, 16, 16), dtype=torch.float16)
+    return x, w, gy
+
+
+def test_layer_rejects_wrong_dtype():
+    import torch
+    layer = _layer()
+    x, w, gy = _good(layer)
+    with pytest.raises(ValueError, match="dtype"):
+        layer.fwd(x.float(), w)
+    with pytest.raises(ValueError, match="dtype"):
+        layer.fwd(x, w.float())
+    with pytest.raises(ValueError, match="dtype"):
+        layer.bwd_data(x, w, gy.to(torch.float64))
+    with pytest.raises(ValueError, match="dtype"):
+        layer.bwd(x, w, gy, gw=torch.zeros((3, 5, 8, 4, 2), dtype=torch.float16))
+
+
+def test_layer_rejects_wrong_shape():
+    layer = _layer()
+    x, w, gy = _good(layer)
+    with pytest.raises(ValueError, match="shape"):
+        layer.fwd(x[:1], w)                               # batch smaller than the layer's
+    with pytest.raises(ValueError, match="shape"):
+        layer.fwd(x, w[:, :, :4])                         # fewer modes
+    with pytest.raises(ValueError, match="shape"):
+        layer.fwd(x, w[..., 0].contiguous())              # no (re, im) axis
+    with pytest.raises(ValueError, match="shape"):
+        layer.bwd_data(x, w, gy[:, :3].contiguous())      # gradient with C_in channels
+    with pytest.raises(ValueError, match="shape"):
+        layer.fwd(x, w, y=gy[:, :4].contiguous())
+
+
+def test_layer_rejects_factor_shapes_and_kinds():
+    import torch
+    from paper_2307_15034_amd import binding as B
+    layer = _layer(weight_kind=B.FNO_WEIGHT_TUCKER, rank=(2, 3, 2, 2))
+    x, _, _ = _good(layer)
+    h = dict(dtype=torch.float16)
+    w = {"core": torch.zeros((2, 3, 2, 2, 2), **h), "u_in": torch.zeros((3, 2, 2), **h),
+         "u_out": torch.zeros((5, 3, 2), **h),
+         "u_mode": [torch.zeros((8, 2, 2), **h), torch.zeros((4, 2, 2), **h)]}
+    bad = dict(w, u_out=torch.zeros((5, 2, 2), **h))
+    with pytest.raises(ValueError, match="u_out.*shape"):
+        layer.fwd(x, bad)
+    with pytest.raises(ValueError, match="u_mode"):
+        layer.fwd(x, dict(w, u_mode=w["u_mode"][:1]))
+    with pytest.raises(ValueError, match="one tensor|expected core"):
+        layer.fwd(x, torch.zeros((3, 5, 8, 4, 2), **h))
+    with pytest.raises(ValueError, match="GPU"):
+        layer.fwd(x, w)                                   # right shapes, but on the host
+
+
+def test_layer_rejects_host_tensors_and_short_spectra():
+    import torch
+    layer = _layer()
+    x, w, gy = _good(layer)
+    with pytest.raises(ValueError, match="GPU"):
+        layer.fwd(x, w)
+    with pytest.raises(ValueError, match="contiguous"):
+        layer.fwd(x.transpose(2, 3), w)
+    with pytest.raises(ValueError, match="bytes"):
+        layer.fwd(x, w, x_hat=torch.zeros(16, dtype=torch.uint8))

@@ -16,8 +16,11 @@
    grid size; the test holds each to that bound.
 2. The frequency-mode ablation (App. B.10): for signals whose amplitudes
    decay exponentially with frequency, the half-precision spectrum's error
-   relative to each amplitude grows with frequency.  The fp32 GPU path is the
-   full-precision reference, as in the paper's comparison.
+   relative to each amplitude grows with frequency.  The error is measured
+   against the true spectrum of the signal: the float64 oracle's transform of
+   the unrounded float64 samples (the paper reports the error as a
+   percentage of the true amplitudes).  The fp32 GPU path is measured the
+   same way and must stay orders of magnitude below the fp16 one.
 """
 import numpy as np
 import pytest
@@ -70,17 +73,24 @@ def test_thm32_bound_on_gpu_spectrum():
 def test_frequency_error_grows_with_frequency():
     N, kmax, Bt = 1024, 10, 64
     x64 = synth.decaying_sinusoids(0, Bt, N, kmax)
-    spec = {}
+    # the true spectrum: the float64 signal itself (before any rounding to the
+    # storage type) through the oracle's transform
+    true = O.forward_spectrum(x64[:, None, :], (N,), (16,))[:, 0]
+    amp = np.abs(true[:, 1:kmax + 1])
+    pct = {}
     for prec in ("fp16", "fp32"):
         _, npdt, _ = U.prec_codes(prec)
         layer = U.make_layer((N,), (16,), Bt, 1, 1, prec)
-        spec[prec] = _spectrum(layer, x64.astype(npdt))[:, 0]
-    # the reference of each precision's stored input: fp16 rounding of the
-    # signal is part of the half-precision error, as in the paper's comparison
-    amp = np.abs(spec["fp32"][:, 1:kmax + 1])
-    pct = 100.0 * np.abs(spec["fp16"][:, 1:kmax + 1] - spec["fp32"][:, 1:kmax + 1]) / amp
-    mean_pct = pct.mean(axis=0)
-    U.say("frequency  mean amplitude  mean error %: " + "; ".join(
-        f"{k}: {amp[:, k - 1].mean():.2e} {mean_pct[k - 1]:.3f}" for k in range(1, kmax + 1)))
+        got = _spectrum(layer, x64.astype(npdt))[:, 0]
+        err = np.abs(got[:, 1:kmax + 1] - true[:, 1:kmax + 1])
+        pct[prec] = (100.0 * err / amp).mean(axis=0)
+    for prec in ("fp16", "fp32"):
+        U.say(f"{prec}: frequency  mean amplitude  mean error %: " + "; ".join(
+            f"{k}: {amp[:, k - 1].mean():.2e} {pct[prec][k - 1]:.4f}"
+            for k in range(1, kmax + 1)))
+    mean_pct = pct["fp16"]
     assert mean_pct[-3:].mean() > 10.0 * mean_pct[:3].mean()
     assert np.all(np.diff(np.log(mean_pct[1:])) > -0.5)
+    # full precision is the reference the paper compares against: its error
+    # stays far below half precision's at every frequency
+    assert np.all(pct["fp32"] < 0.02 * mean_pct)

@@ -360,7 +360,45 @@ def pin_cp_tucker(seed=81):
     return err
 
 
+def pin_rel_l2_hand():
+    """rel_l2 against values worked by hand: a real vector, a 2-D tensor (the
+    norm runs over the whole tensor), complex values and the same values as
+    (re, im) pairs, fp16 inputs whose squares overflow fp16, the zero
+    reference, and scale invariance.  Returns the largest deviation."""
+    f16 = np.float16
+    cases = [
+        (np.array([1.0, 2.0, 2.0]), np.array([1.0, 0.0, 0.0]), np.sqrt(8.0)),
+        (np.array([[3.0, 0.0], [0.0, 0.0]]), np.array([[0.0, 0.0], [0.0, 4.0]]), 1.25),
+        (np.array([1 + 1j, 0j]), np.array([1 + 0j, 1j]), 1.0),
+        (np.array([2 + 0j]), np.array([1j]), np.sqrt(5.0)),
+        (np.array([[2.0, 0.0]]), np.array([[0.0, 1.0]]), np.sqrt(5.0)),
+        (np.full(4, 60000, f16), np.full(4, 30000, f16), 1.0),
+        (np.array([3.0, 4.0]), np.zeros(2), 5.0),
+        (np.zeros(3), np.zeros(3), 0.0),
+        (np.array([4.0, 8.0, 8.0]), np.array([4.0, 0.0, 0.0]), np.sqrt(8.0)),
+    ]
+    err = 0.0
+    for a, b, want in cases:
+        got = O.rel_l2(a, b)
+        err = max(err, abs(got - want)) if np.isfinite(got) else np.inf
+    return err
+
+
+def pin_max_plane_hand():
+    """max_plane_rel_l2 on a [2, 2, 3] tensor of ones with one element of
+    plane (1, 0) off by 3: that plane's error is 3 / sqrt(3) = sqrt(3), while
+    the whole-tensor figure is only 3 / sqrt(12)."""
+    b = np.ones((2, 2, 3))
+    a = b.copy()
+    a[1, 0, 2] += 3.0
+    return max(abs(O.max_plane_rel_l2(a, b) - np.sqrt(3.0)),
+               abs(O.max_plane_rel_l2(b, b) - 0.0),
+               abs(O.rel_l2(a, b) - 3.0 / np.sqrt(12.0)))
+
+
 ALL_PINS = {
+    "rel_l2_hand": (pin_rel_l2_hand, 1e-15),
+    "max_plane_hand": (pin_max_plane_hand, 1e-15),
     "cp_explicit": (pin_cp_explicit, 1e-13),
     "cp_tucker": (pin_cp_tucker, 1e-12),
     "brute2d": (pin_brute_force_2d, 1e-13),
@@ -600,15 +638,28 @@ def test_greedy_paths_golden(policy):
     assert peak == g[policy]["peak"]
 
 
-def test_greedy_adjoint_mirror():
-    """The adjoint einsum swaps i and o; with Cin == Cout and equal ranks its
-    greedy path mirrors the forward one."""
-    ops_f, out_f = O.tucker_labels(2)
+@pytest.mark.parametrize("policy", ["min_result", "min_net"])
+def test_greedy_adjoint_golden(policy):
+    """The data gradient's contraction (G with the conjugated factors) follows
+    its own hand-derived greedy sequence (tests/golden/tucker_paths.json,
+    "adjoint"), ties included."""
+    with open(os.path.join(GOLDEN, "tucker_paths.json")) as f:
+        g = json.load(f)
     ops_a, out_a = O.tucker_labels(2, adjoint=True)
+    ga = g["adjoint"]
+    assert ops_a == ga["operands"] and out_a == ga["output"]
     sz = O.tucker_sizes(16, 128, 128, (64, 32), (13, 13, 6, 3))
-    for pol in ("min_result", "min_net"):
-        a = O.greedy_path(ops_a, sz, out_a, pol)
-        assert len(a) == 5 and a[-1][2] == out_a
+    assert sz == g["sizes"]
+    steps = O.greedy_path(ops_a, sz, out_a, policy)
+    exp = ga[policy]["steps"]
+    assert len(steps) == len(exp)
+    for (p, q, res), (ep, eq, eres, esize) in zip(steps, exp):
+        assert (p, q) == (ep, eq)
+        assert sorted(res) == sorted(eres)
+        assert O._size(res, sz) == esize
+    assert steps[-1][2] == out_a
+    assert O.path_macs(ops_a, sz, steps) == ga[policy]["macs"]
+    assert max(O._size(r, sz) for _, _, r in steps) == ga[policy]["peak"]
 
 
 @pytest.mark.parametrize("precision", [F32, F16T])
@@ -857,7 +908,37 @@ def _pins_fail():
     return failing
 
 
+def _rel_l2_abs_not_squared(a, b):
+    a = np.asarray(a, dtype=np.complex128)
+    b = np.asarray(b, dtype=np.complex128)
+    den = np.sqrt(np.sum(np.abs(b)))
+    num = np.sqrt(np.sum(np.abs(a - b)))
+    return float(num / den) if den else float(num)
+
+
+def _rel_l2_in_input_dtype(a, b):
+    a = np.asarray(a)
+    b = np.asarray(b)
+    with np.errstate(over="ignore", invalid="ignore"):
+        num = np.sqrt(np.sum((a - b) * np.conj(a - b)).real)
+        den = np.sqrt(np.sum(b * np.conj(b)).real)
+    return float(num / den) if den else float(num)
+
+
 MUTATIONS = {
+    "rel_l2_divides_by_a": ("rel_l2", lambda orig: (lambda a, b: orig(b, a))),
+    "rel_l2_no_sqrt": ("rel_l2", lambda orig: (lambda a, b: orig(a, b) ** 2)),
+    "rel_l2_real_part_only": ("rel_l2", lambda orig: (
+        lambda a, b: orig(np.real(a), np.real(b)))),
+    "rel_l2_abs_not_squared": ("rel_l2", lambda orig: _rel_l2_abs_not_squared),
+    "rel_l2_squares_in_fp16": ("rel_l2", lambda orig: _rel_l2_in_input_dtype),
+    "rel_l2_max_norm": ("rel_l2", lambda orig: (
+        lambda a, b: float(np.abs(np.asarray(a, dtype=np.complex128) - b).max()
+                           / max(np.abs(np.asarray(b, dtype=np.complex128)).max(), 1e-300)))),
+    "rel_l2_zero_ref_is_zero": ("rel_l2", lambda orig: (
+        lambda a, b: 0.0 if not np.any(np.asarray(b)) else orig(a, b))),
+    "max_plane_is_whole_tensor": ("max_plane_rel_l2", lambda orig: (
+        lambda a, b, nlead=2: O.rel_l2(a, b))),
     "no_multiplicity": ("multiplicity", lambda orig: (lambda k, n: np.ones(np.shape(k)))),
     "c_everywhere_2": ("multiplicity", lambda orig: (lambda k, n: 2.0 * np.ones(np.shape(k)))),
     "wrong_sign": ("dft_matrix", lambda orig: (lambda n, ks, s: orig(n, ks, -s))),
