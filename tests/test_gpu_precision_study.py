@@ -81,7 +81,7 @@ def test_frequency_error_grows_with_frequency():
     for prec in ("fp16", "fp32"):
         _, npdt, _ = U.prec_codes(prec)
         layer = U.make_layer((N,), (16,), Bt, 1, 1, prec)
-        got = _spectrum(layer, x64.astype(npdt))[:, 0]
+        got = _spectrum(layer, x64[:, None, :].astype(npdt))[:, 0]
         err = np.abs(got[:, 1:kmax + 1] - true[:, 1:kmax + 1])
         pct[prec] = (100.0 * err / amp).mean(axis=0)
     for prec in ("fp16", "fp32"):
