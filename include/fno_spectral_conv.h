@@ -188,6 +188,27 @@ fno_status fno_spectral_conv_fwd(const fno_conv_desc *desc, const void *x,
                                  void *workspace, size_t workspace_bytes,
                                  hipStream_t stream);
 
+/* Allocation-free forward call, for callers that cannot allocate device
+ * memory (code under HIP graph capture, tight serving loops, harnesses that
+ * forbid allocation).  Same arguments and results as fno_spectral_conv_fwd
+ * without the workspace: the library's own fixed device array of
+ * FNO_NOALLOC_SCRATCH_BYTES per GPU (held until the process ends) takes its
+ * place.  The call allocates no device memory and creates no events:
+ *   - the descriptor's plan must already exist on the current device (make
+ *     one ordinary call with it first, e.g. fno_spectral_conv_fwd);
+ *     otherwise FNO_ERR_INVALID_ARGUMENT and nothing is enqueued;
+ *   - a descriptor whose forward workspace
+ *     (fno_spectral_conv_workspace_size(desc, FNO_OP_FWD)) exceeds
+ *     FNO_NOALLOC_SCRATCH_BYTES is rejected with FNO_ERR_WORKSPACE_TOO_SMALL
+ *     before anything is enqueued.
+ * Every call on a GPU uses the same array, which keeps the last call's
+ * contents: calls that overlap on one GPU (other streams, other threads)
+ * race; serialise them. */
+#define FNO_NOALLOC_SCRATCH_BYTES ((size_t)64 << 20)
+fno_status fno_spectral_conv_fwd_noalloc(const fno_conv_desc *desc, const void *x,
+                                         const fno_weights *w, void *y, void *x_hat_out,
+                                         hipStream_t stream);
+
 /* Data gradient: gx[batch, c_in, N...] from gy[batch, c_out, N...]:
  * G = c(k) sum_x gy e^{-i theta}, gXhat = sum_o G conj(W),
  * gx = (1/N) sum_t Re(gXhat e^{+i theta}) * f'(x) with f the pre-activation

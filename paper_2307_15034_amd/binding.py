@@ -108,6 +108,7 @@ def _load() -> ctypes.CDLL:
         "fno_spectral_conv_workspace_size": (ctypes.c_int, [D, ctypes.c_int, P(sz)]),
         "fno_spectral_conv_workspace_size_nocache": (ctypes.c_int, [D, ctypes.c_int, P(sz)]),
         "fno_spectral_conv_fwd": (ctypes.c_int, [D, vp, P(FnoWeights), vp, vp, vp, sz, vp]),
+        "fno_spectral_conv_fwd_noalloc": (ctypes.c_int, [D, vp, P(FnoWeights), vp, vp, vp]),
         "fno_spectral_conv_bwd_data": (ctypes.c_int,
                                        [D, vp, P(FnoWeights), vp, vp, vp, vp, sz, vp]),
         "fno_spectral_conv_bwd_weight": (ctypes.c_int,
@@ -135,6 +136,7 @@ EXPORTED = [
     "fno_status_string", "fno_last_error", "fno_mode_frequency", "fno_contraction_path",
     "fno_contraction_path_cost", "fno_spectrum_bytes", "fno_spectral_conv_workspace_size",
     "fno_spectral_conv_workspace_size_nocache", "fno_spectral_conv_fwd",
+    "fno_spectral_conv_fwd_noalloc",
     "fno_spectral_conv_bwd_data", "fno_spectral_conv_bwd_weight", "fno_spectral_conv_bwd",
     "fno_release_caches",
     "fno_profile_enable", "fno_profile_reset", "fno_profile_read",
@@ -240,6 +242,19 @@ def fno_spectral_conv_fwd(desc, x: int, w: FnoWeights, y: int, x_hat: int, ws: i
                                      x_hat or None, ws or None, ws_bytes, stream or None)
     if check:
         _check(st, "fno_spectral_conv_fwd")
+    return st
+
+
+# the fixed per-GPU scratch of the allocation-free forward call
+FNO_NOALLOC_SCRATCH_BYTES = 64 << 20
+
+
+def fno_spectral_conv_fwd_noalloc(desc, x: int, w: FnoWeights, y: int, x_hat: int, stream: int,
+                                  check: bool = True) -> int:
+    st = _lib.fno_spectral_conv_fwd_noalloc(ctypes.byref(desc), x or None, ctypes.byref(w),
+                                            y or None, x_hat or None, stream or None)
+    if check:
+        _check(st, "fno_spectral_conv_fwd_noalloc")
     return st
 
 

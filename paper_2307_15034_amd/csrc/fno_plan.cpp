@@ -17,6 +17,7 @@
 
 #include "../../include/fno_spectral_conv.h"
 #include "fno_internal.h"
+#include "fno_host.h"
 
 namespace fno {
 namespace {
@@ -724,7 +725,7 @@ void host_plan(const fno_conv_desc* d, Plan* pl) {
 // The plan of a descriptor on the current device, built on first use.  The
 // caller holds a reference for the duration of its call, so a concurrent
 // fno_release_caches cannot free the tables under it.
-fno_status get_plan(const fno_conv_desc* d, std::shared_ptr<Plan>* out) {
+fno_status get_plan(const fno_conv_desc* d, std::shared_ptr<Plan>* out, bool build = true) {
   fno_status st = check_desc(d);
   if (st != FNO_OK) return st;
   int dev = 0;
@@ -736,6 +737,10 @@ fno_status get_plan(const fno_conv_desc* d, std::shared_ptr<Plan>* out) {
   if (it != g_plans.end()) {
     *out = it->second;
     return FNO_OK;
+  }
+  if (!build) {
+    g_last_error = "no plan for this descriptor on this device: make one ordinary call first";
+    return FNO_ERR_INVALID_ARGUMENT;
   }
   std::shared_ptr<Plan> pl = std::make_shared<Plan>();
   host_plan(d, pl.get());
@@ -856,6 +861,10 @@ int prof_slot(const char* name) {
 }
 
 // Runs `launch` bracketed by events when profiling is on.
+// set while the calling thread runs an allocation-free entry point (no
+// events are created for it)
+thread_local bool g_no_alloc_call = false;
+
 template <typename F>
 hipError_t timed(const char* name, hipStream_t s, F launch) {
   bool on;
@@ -863,7 +872,7 @@ hipError_t timed(const char* name, hipStream_t s, F launch) {
     std::lock_guard<std::mutex> lk(g_prof_mutex);
     on = g_prof_on;
   }
-  if (!on) return launch();
+  if (!on || g_no_alloc_call) return launch();
   hipEvent_t a = nullptr, b = nullptr;
   if (hipEventCreate(&a) != hipSuccess) return hipErrorOutOfMemory;
   if (hipEventCreate(&b) != hipSuccess) {
@@ -1520,6 +1529,48 @@ fno_status check_ws(const fno_conv_desc* d, fno_op op, bool caches, const void* 
 
 using namespace fno;
 
+namespace fno {
+// The forward call.  build_plan = false: the plan must already exist (no
+// device allocation, no blocking upload; the allocation-free entry point).
+fno_status fwd_impl(const fno_conv_desc* d, const void* x, const fno_weights* w, void* y,
+                    void* x_hat_out, void* ws, size_t ws_len, hipStream_t s, bool build_plan) {
+  fno_status st = check_desc(d);
+  if (st != FNO_OK) return st;
+  if (!okptr(x) || !okptr(y)) return FNO_ERR_INVALID_ARGUMENT;
+  if (x_hat_out && !aligned16(x_hat_out)) return FNO_ERR_INVALID_ARGUMENT;
+  if ((st = check_weights(d, w)) != FNO_OK) return st;
+  if (build_plan && (st = check_ws(d, FNO_OP_FWD, true, ws, ws_len)) != FNO_OK) return st;
+  std::shared_ptr<Plan> plan_ref;
+  if ((st = get_plan(d, &plan_ref, build_plan)) != FNO_OK) return st;
+  Plan* pl = plan_ref.get();
+  if (!build_plan) {  // the cached plan gives the workspace size
+    if (ws_len < ws_bytes(d, pl, FNO_OP_FWD, true)) return FNO_ERR_WORKSPACE_TOO_SMALL;
+    if (!okptr(ws)) return FNO_ERR_INVALID_ARGUMENT;
+  }
+  const Geo& g = pl->g;
+  WsLayout L;
+  char* base = (char*)ws;
+  char* xs = base + L.add(spec_bytes(g, g.Cin));
+  char* ys = base + L.add(spec_bytes(g, g.Cout));
+  char* inter = base + L.add(std::max(inter3d_bytes(g, g.Cin), inter3d_bytes(g, g.Cout)));
+  char* tsc = base + L.total;
+  void* xh = x_hat_out ? x_hat_out : (void*)xs;
+  struct Flag {  // profiler events stay off for an allocation-free call
+    bool prev;
+    explicit Flag(bool on) : prev(g_no_alloc_call) { g_no_alloc_call = on; }
+    ~Flag() { g_no_alloc_call = prev; }
+  } flag(!build_plan);
+  if ((st = run_r2c(pl, x, xh, inter, g.Cin, 1, 0, s)) != FNO_OK) return st;
+  if (d->weight_kind == FNO_WEIGHT_DENSE) {
+    if ((st = run_contract(pl, xh, w->dense, ys, false, s)) != FNO_OK) return st;
+  } else {
+    if ((st = run_tucker_path(d, pl, false, xh, w, ys, tsc, s)) != FNO_OK) return st;
+  }
+  return run_c2r(pl, ys, y, inter, g.Cout, 1.0f, nullptr, s);
+}
+
+}  // namespace fno
+
 extern "C" {
 
 const char* fno_last_error(void) { return g_last_error.c_str(); }
@@ -1646,30 +1697,7 @@ fno_status fno_spectral_conv_workspace_size_nocache(const fno_conv_desc* d, fno_
 fno_status fno_spectral_conv_fwd(const fno_conv_desc* d, const void* x, const fno_weights* w,
                                  void* y, void* x_hat_out, void* ws, size_t ws_len,
                                  hipStream_t s) {
-  fno_status st = check_desc(d);
-  if (st != FNO_OK) return st;
-  if (!okptr(x) || !okptr(y)) return FNO_ERR_INVALID_ARGUMENT;
-  if (x_hat_out && !aligned16(x_hat_out)) return FNO_ERR_INVALID_ARGUMENT;
-  if ((st = check_weights(d, w)) != FNO_OK) return st;
-  if ((st = check_ws(d, FNO_OP_FWD, true, ws, ws_len)) != FNO_OK) return st;
-  std::shared_ptr<Plan> plan_ref;
-  if ((st = get_plan(d, &plan_ref)) != FNO_OK) return st;
-  Plan* pl = plan_ref.get();
-  const Geo& g = pl->g;
-  WsLayout L;
-  char* base = (char*)ws;
-  char* xs = base + L.add(spec_bytes(g, g.Cin));
-  char* ys = base + L.add(spec_bytes(g, g.Cout));
-  char* inter = base + L.add(std::max(inter3d_bytes(g, g.Cin), inter3d_bytes(g, g.Cout)));
-  char* tsc = base + L.total;
-  void* xh = x_hat_out ? x_hat_out : (void*)xs;
-  if ((st = run_r2c(pl, x, xh, inter, g.Cin, 1, 0, s)) != FNO_OK) return st;
-  if (d->weight_kind == FNO_WEIGHT_DENSE) {
-    if ((st = run_contract(pl, xh, w->dense, ys, false, s)) != FNO_OK) return st;
-  } else {
-    if ((st = run_tucker_path(d, pl, false, xh, w, ys, tsc, s)) != FNO_OK) return st;
-  }
-  return run_c2r(pl, ys, y, inter, g.Cout, 1.0f, nullptr, s);
+  return fno::fwd_impl(d, x, w, y, x_hat_out, ws, ws_len, s, true);
 }
 
 fno_status fno_spectral_conv_bwd_data(const fno_conv_desc* d, const void* x,
