@@ -400,6 +400,7 @@ SQ_PASSES = {
            "SQ_ACTIVE_INST_VMEM SQ_LDS_BANK_CONFLICT SQ_INSTS_SALU SQ_INSTS_VMEM_RD",
 }
 SIMDS = 256 * 4          # MI355X: 256 compute units of four SIMDs
+XCDS = 8                 # GRBM_GUI_ACTIVE is summed over the eight XCDs
 MFMA_F16_PEAK_TFS = 2500.0
 
 
@@ -407,7 +408,8 @@ def summarize_sq(args):
     """profiles/sq_counters_<workload>.md: instruction, stall and matrix-core
     counters of one profiled step per kernel (chip-wide sums per dispatch,
     median over a kernel's dispatches).  Matrix-core utilisation is
-    SQ_VALU_MFMA_BUSY_CYCLES / (GRBM_GUI_ACTIVE x SIMDs); the fp16 matrix rate
+    SQ_VALU_MFMA_BUSY_CYCLES / (GRBM_GUI_ACTIVE / XCDs x SIMDs), the busy
+    cycles of all SIMDs over the cycles of one XCD's kernel; the fp16 matrix rate
     is 512 x SQ_INSTS_VALU_MFMA_MOPS_F16 flops over the kernel's trace
     duration, against the 2.5 PFLOP/s dense fp16 peak."""
     import statistics
@@ -432,7 +434,8 @@ def summarize_sq(args):
         if _logical(kname) == kname and "fno::" not in kname:
             continue
         wc = med(m, "SQ_WAVE_CYCLES")
-        util = 100.0 * med(m, "SQ_VALU_MFMA_BUSY_CYCLES") / (med(m, "GRBM_GUI_ACTIVE") * SIMDS)
+        util = 100.0 * med(m, "SQ_VALU_MFMA_BUSY_CYCLES") / (
+            med(m, "GRBM_GUI_ACTIVE") / XCDS * SIMDS)
         flops = 512.0 * med(m, "SQ_INSTS_VALU_MFMA_MOPS_F16")
         avg = (sum(dur[kname]) / len(dur[kname])) if kname in dur else float("nan")
         tfs = flops / (avg * 1e-6) / 1e12
@@ -458,7 +461,7 @@ def summarize_sq(args):
     lines += ["    (trace: the kernel-trace command of the layer-step summary, same sources)",
               f"    python3 bench.py {wk}--summarize-sq <out>", "",
               "Columns: trace average (us); MFMA busy = SQ_VALU_MFMA_BUSY_CYCLES / "
-              "(GRBM_GUI_ACTIVE x 1024 SIMDs);", "fp16 MFMA GFLOP per dispatch = 512 x "
+              "(GRBM_GUI_ACTIVE / 8 XCDs x 1024 SIMDs);", "fp16 MFMA GFLOP per dispatch = 512 x "
               "SQ_INSTS_VALU_MFMA_MOPS_F16, its rate over the trace average and the",
               "fraction of the 2.5 PFLOP/s dense fp16 peak; instruction counts; LDS bank-"
               "conflict cycles;", "wait / VALU-active / LDS-active as % of SQ_WAVE_CYCLES.", "",

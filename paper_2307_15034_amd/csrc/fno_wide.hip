@@ -32,51 +32,6 @@ constexpr int WD_NT = 2;    // cache policy of the inverse's stores: streaming
 constexpr int WD_XD = 8;    // column tiles of x in flight (inverse epilogue)
 constexpr int WD_AD = 4;    // k-steps of row data in flight (forward)
 
-typedef unsigned short us2 __attribute__((ext_vector_type(2)));
-
-__device__ __forceinline__ h8 w_as_h8(const u32x4& v) {
-  h8 r;
-  __builtin_memcpy(&r, &v, 16);
-  return r;
-}
-
-// f(|x|) of the two fp16 values packed in w, from the LDS table tab:
-// tab[0..sat] holds f of the non-negative codes (every code from sat up to
-// +inf has the value tab[sat]) and tab[sat + 1] is NaN.  ODD: f odd, the
-// sign of x is restored.
-template <bool ODD>
-__device__ __forceinline__ uint32_t lut2(const _Float16* tab, uint32_t w, us2 sat) {
-  const uint32_t aw = w & 0x7fff7fffu;
-  us2 ax;
-  __builtin_memcpy(&ax, &aw, 4);
-  const us2 nan =
-      __builtin_elementwise_min(__builtin_elementwise_sub_sat(ax, (us2){0x7c00, 0x7c00}), (us2){1, 1});
-  const us2 idx = __builtin_elementwise_min(ax, sat) + nan;
-  h2 r;
-  r[0] = tab[idx[0]];
-  r[1] = tab[idx[1]];
-  uint32_t u;
-  __builtin_memcpy(&u, &r, 4);
-  return ODD ? (u | (w & 0x80008000u)) : u;
-}
-
-// Stage tab[0..sat] of a global table and the NaN entry.
-__device__ __forceinline__ void stage_lut(_Float16* dst, const void* src, int sat) {
-  const _Float16* s = reinterpret_cast<const _Float16*>(src);
-  for (int i = threadIdx.x; i <= sat; i += WD_WAVES * 64) dst[i] = s[i];
-  if (threadIdx.x == 0) {
-    const uint16_t qnan = 0x7e00;
-    __builtin_memcpy(&dst[sat + 1], &qnan, 2);
-  }
-}
-
-__device__ __forceinline__ __amdgpu_buffer_rsrc_t plane_rsrc(const void* base, int64_t p,
-                                                             int64_t plane_bytes) {
-  return __builtin_amdgcn_make_buffer_rsrc(
-      const_cast<char*>(reinterpret_cast<const char*>(base) + p * plane_bytes), (short)0,
-      (int)plane_bytes, 0x00020000);
-}
-
 }  // namespace
 
 // ---------------------------------------------------------------------------
@@ -117,7 +72,7 @@ __global__ __launch_bounds__(WD_WAVES * 64, 1) void r2c_wide_kernel(R2CArgs a) {
   const _Float16* cB = reinterpret_cast<const _Float16*>(a.cB);
   const _Float16* sB = reinterpret_cast<const _Float16*>(a.sB);
   const us2 sat = {(unsigned short)a.lut_sat, (unsigned short)a.lut_sat};
-  if (PRE) stage_lut(lut, a.lut, a.lut_sat);
+  if (PRE) stage_lut<WD_WAVES * 64>(lut, a.lut, a.lut_sat);
 
   const int64_t plane_bytes = (int64_t)a.Na * a.Nb * 2;
   const int nks = a.Nb / KS;        // a multiple of 4 on this path
@@ -396,7 +351,7 @@ __global__ __launch_bounds__(WD_WAVES * 64, 1) void c2r_wide_kernel(C2RArgs a) {
 
   // the padding of ZT stays zero: every plane writes the same positions
   for (int i = tid; i < 2 * KBP * LDZ; i += WD_WAVES * 64) ZT[i] = (_Float16)0.0f;
-  if (EPI) stage_lut(lut, a.lut, a.lut_sat);
+  if (EPI) stage_lut<WD_WAVES * 64>(lut, a.lut, a.lut_sat);
 
   auto ldZ = [&](int64_t p, u32x4 (&zq)[ZQ]) {
     const __amdgpu_buffer_rsrc_t rz = plane_rsrc(a.in, p, spec_bytes);
