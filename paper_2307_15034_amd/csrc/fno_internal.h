@@ -219,6 +219,13 @@ hipError_t launch_wgrad_slab(const WgradArgs& a, hipStream_t s);
 bool adj_wgrad_slab_supported(const ContractArgs& adj, const WgradArgs& wg);
 hipError_t launch_adj_wgrad_slab(const ContractArgs& adj, const WgradArgs& wg, hipStream_t s);
 
+// Radix-2 wide-plane transforms (fno_wide2.hip): the radix-2 tables in the
+// table fields; hipErrorNotSupported when the shape is not one of the path's.
+size_t r2c_wide2_lds_bytes(int nctc, bool pre, int lut_sat);
+size_t c2r_wide2_lds_bytes(int nctc, int nkzh, bool epi, int lut_sat);
+hipError_t launch_r2c_wide2(const R2CArgs& a, int nctc, int grid, size_t lds, hipStream_t s);
+hipError_t launch_c2r_wide2(const C2RArgs& a, int nctc, int grid, size_t lds, hipStream_t s);
+
 size_t r2c_lds_bytes(int elem, int Kbp, int R);
 size_t c2r_lds_bytes(int elem, int Kbp, int Kap, int R);
 size_t axis_lds_bytes(int elem, int Linp);

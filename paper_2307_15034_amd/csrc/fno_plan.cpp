@@ -338,6 +338,10 @@ struct Geo {
   int NaC;           // Na padded to 32 (chained forward tables)
   // leading 3-D axis
   int N1, K1, Lin_f, Linp_f, Lout16_f, Linp_i, Lout16_i;
+  // radix-2 wide-plane transforms (fp16 planes with both extents multiples
+  // of 256): column tiles per class, leading-axis tiles per class, and the
+  // leading-axis slots per class padded to 32
+  int w2, w2_nctc, w2_nta, w2_kah;
 };
 
 struct DevTables {
@@ -348,6 +352,7 @@ struct DevTables {
   const void *lutAct, *lutGrad;
   int actSat = 0, gradSat = 0;  // first codes of the saturated tails (fp16 plans)
   const void *eFr, *eFi, *eIr, *eIi;
+  const void *twA2, *cB2, *sB2, *cI2, *sI2, *twI2;  // radix-2 wide-plane tables
 };
 
 struct Plan {
@@ -422,6 +427,17 @@ Geo make_geo(const fno_conv_desc* d) {
     g.Lout16_f = (int)round_up(g.K1, 16);
     g.Linp_i = (int)round_up(g.K1, 32);
     g.Lout16_i = (int)round_up(g.N1, 16);
+  }
+  g.w2 = 0;
+  if (g.elem == ELEM_F16 && nd == 2 && g.Na % 256 == 0 && g.Nb % 256 == 0 && g.Kb <= 64 &&
+      g.Kb % 4 == 0 && g.Ka <= 128 && g.Ka * g.Kb <= 8192 &&
+      (int64_t)g.Na * g.Nb * 2 < ((int64_t)1 << 30)) {
+    const int kbe = (g.Kb + 1) / 2, m = g.Ka / 2;
+    const int nta = (m + 15) / 16;
+    g.w2 = 1;
+    g.w2_nctc = kbe <= 16 ? 2 : 4;
+    g.w2_nta = nta <= 1 ? 1 : nta <= 2 ? 2 : 4;
+    g.w2_kah = (int)round_up(m, 32);
   }
   return g;
 }
@@ -583,6 +599,43 @@ void fill_tables(const fno_conv_desc* d, const Geo& g, std::vector<T>& buf,
   (void)oci;
   (void)osi;
   (void)oti;
+  if (g.w2) {
+    // radix-2 wide-plane tables (even and odd slots of each axis as classes)
+    const int kbpc = g.w2_nctc * 8, nh = g.Nb / 2, nha = g.Na / 2, m = g.Ka / 2;
+    const int nta16 = g.w2_nta * 16, kah = g.w2_kah;
+    // twA2 [4 kbpc][nh]: row cls 2 kbpc + c: cos, + kbpc: -sin of 2 pi k n / Nb
+    size_t a2 = alloc((size_t)4 * kbpc * nh);
+    // twI2 [nh][4 kbpc]: the same values, transposed
+    size_t i2 = alloc((size_t)nh * 4 * kbpc);
+    for (int cls = 0; cls < 2; ++cls)
+      for (int c = 0; c < kbpc; ++c) {
+        const int k = 2 * c + cls;
+        if (k >= g.Kb) continue;
+        for (int n = 0; n < nh; ++n) {
+          double cv, sv;
+          twiddle(k, n, g.Nb, &cv, &sv);
+          buf[a2 + (size_t)(cls * 2 * kbpc + c) * nh + n] = (T)cv;
+          buf[a2 + (size_t)(cls * 2 * kbpc + kbpc + c) * nh + n] = (T)(-sv);
+          buf[i2 + (size_t)n * 4 * kbpc + cls * 2 * kbpc + c] = (T)cv;
+          buf[i2 + (size_t)n * 4 * kbpc + cls * 2 * kbpc + kbpc + c] = (T)(-sv);
+        }
+      }
+    // cB2, sB2 [2][nta16][nha]; cI2, sI2 [2][nha][kah]: slot t_a = 2 t + cls
+    size_t cb2 = alloc((size_t)2 * nta16 * nha), sb2 = alloc((size_t)2 * nta16 * nha);
+    size_t ci2 = alloc((size_t)2 * nha * kah), si2 = alloc((size_t)2 * nha * kah);
+    for (int cls = 0; cls < 2; ++cls)
+      for (int t = 0; t < m; ++t) {
+        const int64_t ka = ka_of(2 * t + cls);
+        for (int r = 0; r < nha; ++r) {
+          double cv, sv;
+          twiddle(ka, r, g.Na, &cv, &sv);
+          buf[cb2 + ((size_t)cls * nta16 + t) * nha + r] = (T)cv;
+          buf[sb2 + ((size_t)cls * nta16 + t) * nha + r] = (T)sv;
+          buf[ci2 + ((size_t)cls * nha + r) * kah + t] = (T)cv;
+          buf[si2 + ((size_t)cls * nha + r) * kah + t] = (T)sv;
+        }
+      }
+  }
   if (nd == 3) {
     const int64_t m1 = d->modes[0];
     // forward E[t][l] = exp(-2 pi i k1(t) l / N1): [Lout16_f][Linp_f]
@@ -699,6 +752,14 @@ fno_status build_tables(const fno_conv_desc* d, Plan* pl) {
   pl->t.sIc = at(12);
   pl->t.lutAct = at(13);
   pl->t.lutGrad = at(14);
+  if (pl->g.w2) {  // allocated after the lookup tables (2-D plans only)
+    pl->t.twA2 = at(15);
+    pl->t.twI2 = at(16);
+    pl->t.cB2 = at(17);
+    pl->t.sB2 = at(18);
+    pl->t.cI2 = at(19);
+    pl->t.sI2 = at(20);
+  }
   if (pl->g.nd == 3) {
     pl->t.eFr = at(15);
     pl->t.eFi = at(16);
@@ -971,6 +1032,21 @@ fno_status run_r2c(const Plan* pl, const void* in, void* spec, void* inter, int6
       else if (e != hipErrorNotSupported) return hip_fail(e, kname);
     }
   }
+  if (!done && g.w2) {
+    // large planes, one radix-2 stage per axis: persistent eight-wave
+    // work-groups, one per compute unit
+    R2CArgs b = a;
+    b.twA = pl->t.twA2;
+    b.cB = pl->t.cB2;
+    b.sB = pl->t.sB2;
+    b.Kap16 = g.w2_nta * 16;
+    b.lut_sat = pl->t.actSat;
+    const size_t lds = r2c_wide2_lds_bytes(g.w2_nctc, do_tanh, b.lut_sat);
+    const int grid = (int)std::min<int64_t>(a.planes, (int64_t)pl->num_cu);
+    hipError_t e = timed(kname, s, [&] { return launch_r2c_wide2(b, g.w2_nctc, grid, lds, s); });
+    if (e == hipSuccess) done = true;
+    else if (e != hipErrorNotSupported) return hip_fail(e, kname);
+  }
   if (!done && g.elem == ELEM_F16 && g.Nb % 128 == 0 && g.Na % 256 == 0 && g.Nbp == g.Nb &&
       (g.nct == 4 || g.nct == 8) && g.Kap16 <= 128 && 128 % g.Kap16 == 0 &&
       g.Na * (int64_t)g.Nb * 2 < ((int64_t)1 << 30)) {
@@ -1080,6 +1156,20 @@ fno_status run_c2r(const Plan* pl, const void* spec, void* out, void* inter, int
       if (e == hipSuccess) return FNO_OK;
       if (e != hipErrorNotSupported) return hip_fail(e, kname);
     }
+  }
+  if (g.w2) {
+    // large planes, one radix-2 stage per axis
+    C2RArgs b = a;
+    b.cI = pl->t.cI2;
+    b.sI = pl->t.sI2;
+    b.twI = pl->t.twI2;
+    b.Kap = g.w2_kah;
+    b.lut_sat = pl->t.gradSat;
+    const size_t lds = c2r_wide2_lds_bytes(g.w2_nctc, g.w2_kah / 32, x_epi != nullptr, b.lut_sat);
+    const int grid = (int)std::min<int64_t>(a.planes, (int64_t)pl->num_cu);
+    hipError_t e = timed(kname, s, [&] { return launch_c2r_wide2(b, g.w2_nctc, grid, lds, s); });
+    if (e == hipSuccess) return FNO_OK;
+    if (e != hipErrorNotSupported) return hip_fail(e, kname);
   }
   if (g.elem == ELEM_F16 && g.Nb % 128 == 0 && g.Na % 256 == 0 &&
       (g.nct == 4 || g.nct == 8) && g.Kap <= 128 && g.Na * (int64_t)g.Nb * 2 < ((int64_t)1 << 30)) {

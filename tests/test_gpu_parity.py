@@ -67,6 +67,11 @@ EDGE = [
     ((256, 256), (32, 32), 2, 3, 2),    # wide-plane transforms: one 256-row chunk
     ((512, 128), (16, 64), 1, 2, 3),    # wide-plane transforms: two chunks, 64 last-axis modes
     ((256, 256), (32, 32), 9, 30, 31),  # wide-plane transforms: more planes than work-groups
+    # radix-2 wide-plane transforms: odd and even slot classes of unequal
+    # padding, several items per plane, leading-axis tiles padded per class
+    ((512, 256), (20, 20), 2, 3, 2),    # 10 + 10 last-axis slots, 2 x 20 leading
+    ((256, 512), (40, 36), 1, 2, 3),    # 18 + 18 last-axis slots (four column tiles)
+    ((1024, 256), (8, 12), 3, 2, 2),    # four items per plane, 6 + 6 slots
 ]
 
 
