@@ -146,15 +146,15 @@ __global__ __launch_bounds__(W2_NT, 1) void r2c_wide2_kernel(R2CArgs a) {
   };
 
   f4 accR[NTBW], accI[NTBW];
-  u32x4 va[2][2][2];   // row fragments of the two k-steps of the next slice
+  u32x4 va[4][2][2];   // row fragments of k-steps s .. s + 3 (slot s % 4)
   u32x4 twr[2][TWP];   // twiddle slices g + 1, g + 2 in flight
   __amdgpu_buffer_rsrc_t rs = plane_rsrc(a.in, nitems > 0 ? item_plane(0) : 0, plane_bytes);
   if (nitems > 0) {
     ldTW(0, twr[0]);
     ldTW(1, twr[1]);
     const int rb = row_lane(0);
-    ldA(rs, rb, 0, va[0]);
-    ldA(rs, rb, 1, va[1]);
+#pragma unroll
+    for (int d = 0; d < 4; ++d) ldA(rs, rb, d, va[d]);
     stTW(twr[0], 0);
   }
   __syncthreads();  // table and first slice staged
@@ -209,14 +209,14 @@ __global__ __launch_bounds__(W2_NT, 1) void r2c_wide2_kernel(R2CArgs a) {
         }
       }
     };
-    // one slice: its two k-steps (the next slice's rows requested as each
+    // one slice: its two k-steps (the rows two slices on requested as each
     // k-step's registers free up), then the next slice into LDS and a barrier
     auto slice = [&](int gs, int par, int rb, bool rows) {
       ldTW(gs + 2 < ngr ? gs + 2 : gs + 2 - ngr, twr[par]);
 #pragma unroll
       for (int k = 0; k < 2; ++k) {
-        mul(va[k], par, k);
-        if (rows) ldA(rs, rb, 2 * gs + 2 + k, va[k]);
+        mul(va[2 * par + k], par, k);
+        if (rows) ldA(rs, rb, 2 * gs + k + 4, va[2 * par + k]);
       }
       stTW(twr[1 - par], 1 - par);
       __syncthreads();
@@ -227,11 +227,9 @@ __global__ __launch_bounds__(W2_NT, 1) void r2c_wide2_kernel(R2CArgs a) {
       slice(gs, 0, rb, true);
       slice(gs + 1, 1, rb, true);
     }
-    {
-      const int rb = row_lane(c0);
-      slice(ngr - 2, 0, rb, true);
-    }
-    // last slice: the next item's rows are requested after the step-B tables
+    // last two slices: the next item's rows are requested after the step-B
+    // tables
+    slice(ngr - 2, 0, 0, false);
     slice(ngr - 1, 1, 0, false);
     {
       // row butterfly, scale (twice the step-A scale: the last-axis stage
@@ -270,7 +268,7 @@ __global__ __launch_bounds__(W2_NT, 1) void r2c_wide2_kernel(R2CArgs a) {
     {
       const int rb = row_lane(cn);
 #pragma unroll
-      for (int d = 0; d < 2; ++d) ldA(more ? rsn : rs, rb, more ? d : nks - 1, va[d]);
+      for (int d = 0; d < 4; ++d) ldA(more ? rsn : rs, rb, more ? d : nks - 1, va[d]);
     }
     __syncthreads();
 
