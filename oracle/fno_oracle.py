@@ -25,7 +25,10 @@ Mixed-Precision Neural Operators", ICLR 2024):
   half-precision mode (Sec. 4.3), none in full precision; as variants, tanh in
   full precision (the ablation of App. B.8), none in half precision (the
   unstabilised baseline) and the hard clip to [-c, c] of the pre-FFT
-  comparison (App. B.6; with c = 57344 the FP8-E5M2 clipping of Sec. 4.6).
+  comparison (App. B.6; with c = 57344 the FP8-E5M2 clipping of Sec. 4.6),
+  and the 2-sigma clip of the same comparison: each (batch, channel) plane
+  clipped to its mean plus or minus two (population) standard deviations,
+  the bounds held constant in the gradient.
 * The inverse takes y = sum_t c(k_d) Re(Yhat_t e^{+i theta}) with c = 1 on the
   k_d = 0 and Nyquist planes and 2 elsewhere, and no 1/N.
 * The Tucker and CP contractions are split into two-operand steps in the
@@ -56,6 +59,9 @@ PREC_FP16_TANH = "fp16_tanh"  # f(x) = tanh(x)
 PREC_FP32_TANH = "fp32_tanh"  # f(x) = tanh(x)
 PREC_FP16 = "fp16"            # f(x) = x
 # "fp16_clip:<c>" / "fp32_clip:<c>": f(x) = min(max(x, -c), c), built by clip_mode
+# "fp16_sigma:<k>" / "fp32_sigma:<k>": the statistics-based clip to
+# [mu - k sigma, mu + k sigma] per (batch, channel) plane (k = 2: the 2-sigma
+# clip), built by sigma_mode
 
 
 def clip_mode(storage: str, c: float) -> str:
@@ -65,8 +71,16 @@ def clip_mode(storage: str, c: float) -> str:
     return f"{storage}_clip:{float(c)!r}"
 
 
+def sigma_mode(storage: str, k: float = 2.0) -> str:
+    """Mode string of the k-sigma clip with the given storage."""
+    if storage not in ("fp16", "fp32"):
+        raise ValueError(storage)
+    return f"{storage}_sigma:{float(k)!r}"
+
+
 def preact_kind(precision: str) -> Tuple[str, Optional[float]]:
-    """("none" | "tanh" | "clip", the clip bound or None) of a mode."""
+    """("none" | "tanh" | "clip" | "sigma", the clip bound / the number of
+    standard deviations, or None) of a mode."""
     if precision in (PREC_FP32, PREC_FP16):
         return "none", None
     if precision in (PREC_FP16_TANH, PREC_FP32_TANH):
@@ -76,6 +90,11 @@ def preact_kind(precision: str) -> Tuple[str, Optional[float]]:
         if not (c > 0.0 and np.isfinite(c)):
             raise ValueError(precision)
         return "clip", c
+    if isinstance(precision, str) and precision.split(":")[0] in ("fp16_sigma", "fp32_sigma"):
+        k = float(precision.split(":", 1)[1])
+        if not (k > 0.0 and np.isfinite(k)):
+            raise ValueError(precision)
+        return "sigma", k
     raise ValueError(precision)
 
 POLICY_MIN_RESULT = "min_result"
@@ -135,15 +154,42 @@ def _apply_axis(a: np.ndarray, mat: np.ndarray, axis: int) -> np.ndarray:
     return np.moveaxis(out, -1, axis)
 
 
+def sigma_bounds(x: np.ndarray, k: float) -> Tuple[np.ndarray, np.ndarray]:
+    """Bounds of the statistics-based clip (App. B.6: clipping from the data's
+    mean and standard deviation): for every (batch, channel) plane of x
+    [B, C, N...], mu - k sigma and mu + k sigma with mu the plane's mean and
+    sigma its population standard deviation (divide by the number of points).
+    A plane holding a non-finite value has NaN bounds.  Returned with the
+    spatial axes kept (size 1) for broadcasting."""
+    xf = np.asarray(x, dtype=np.float64)
+    if xf.ndim < 3:
+        raise ValueError("the sigma clip needs [batch, channel, spatial...] input")
+    axes = tuple(range(2, xf.ndim))
+    with np.errstate(invalid="ignore", over="ignore"):
+        mu = xf.mean(axis=axes, keepdims=True)
+        sd = np.sqrt(((xf - mu) ** 2).mean(axis=axes, keepdims=True))
+        lo, hi = mu - k * sd, mu + k * sd
+    bad = ~(np.isfinite(lo) & np.isfinite(hi))
+    lo = np.where(bad, np.nan, lo)
+    hi = np.where(bad, np.nan, hi)
+    return lo, hi
+
+
 def preactivation(x: np.ndarray, precision: str) -> np.ndarray:
-    """u = f(x): tanh (Sec. 4.3), the identity, or the hard clip that moves
-    every value outside [-c, c] to the nearer bound (App. B.6).  NaN stays NaN."""
+    """u = f(x): tanh (Sec. 4.3), the identity, the hard clip that moves
+    every value outside [-c, c] to the nearer bound, or the statistics-based
+    clip to each plane's [mu - k sigma, mu + k sigma] (App. B.6).  NaN stays
+    NaN; a plane whose statistics are not finite is NaN throughout."""
     xf = np.asarray(x, dtype=np.float64)
     kind, c = preact_kind(precision)
     if kind == "tanh":
         return np.tanh(xf)
     if kind == "clip":
         return np.where(np.abs(xf) > c, np.copysign(c, xf), xf)
+    if kind == "sigma":
+        lo, hi = sigma_bounds(xf, c)
+        u = np.where(xf < lo, lo, np.where(xf > hi, hi, xf))
+        return np.where(np.isnan(lo), np.nan, u)
     return xf
 
 
@@ -158,6 +204,13 @@ def preactivation_grad(x: np.ndarray, precision: str) -> Optional[np.ndarray]:
         return 1.0 - t * t
     if kind == "clip":
         return np.where(np.isnan(xf), np.nan, np.where(np.abs(xf) <= c, 1.0, 0.0))
+    if kind == "sigma":
+        # the bounds depend on x too; this reading holds them constant (no
+        # gradient through the mean and the standard deviation), as for a
+        # clip with given bounds
+        lo, hi = sigma_bounds(xf, c)
+        inside = (xf >= lo) & (xf <= hi)
+        return np.where(np.isnan(xf) | np.isnan(lo), np.nan, np.where(inside, 1.0, 0.0))
     return None
 
 

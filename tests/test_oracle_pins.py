@@ -396,7 +396,69 @@ def pin_max_plane_hand():
                abs(O.rel_l2(a, b) - 3.0 / np.sqrt(12.0)))
 
 
+def pin_sigma_closed_form():
+    """The 2-sigma clip on planes whose statistics are known in closed form:
+    63 zeros and one value A (mean A/64, population deviation A sqrt(63)/64,
+    so A clips to A (1 + 2 sqrt 63) / 64 and the zeros stay), the same with
+    -A, values +-1 alternating (mean 0, deviation 1: nothing clips), and the
+    first plane scaled by 1000 (each plane's own statistics: the result
+    scales with it).  Returns the largest relative deviation."""
+    A = 10.0
+    x = np.zeros((1, 4, 8, 8))
+    x[0, 0, 2, 5] = A
+    x[0, 1, 7, 0] = -A
+    x[0, 2] = np.where((np.arange(64) % 2).reshape(8, 8) == 0, 1.0, -1.0)
+    x[0, 3] = 1000.0 * x[0, 0]
+    u = O.preactivation(x, O.sigma_mode("fp32", 2.0))
+    want = np.zeros_like(x)
+    clipped = A * (1.0 + 2.0 * np.sqrt(63.0)) / 64.0
+    want[0, 0, 2, 5] = clipped
+    want[0, 1, 7, 0] = -clipped
+    want[0, 2] = x[0, 2]
+    want[0, 3, 2, 5] = 1000.0 * clipped
+    g = O.preactivation_grad(x, O.sigma_mode("fp32", 2.0))
+    gwant = np.ones_like(x)
+    gwant[0, 0, 2, 5] = gwant[0, 1, 7, 0] = gwant[0, 3, 2, 5] = 0.0
+    return max(float(np.abs(u - want).max()) / 1000.0, float(np.abs(g - gwant).max()))
+
+
+def pin_sigma_fd_frozen():
+    """The data gradient through the 2-sigma clip equals central finite
+    differences of the layer whose clip bounds are held at the values the
+    statistics of x give (the reading: no gradient through the statistics),
+    for inside and clipped elements alike."""
+    rng = _rng(91)
+    n, modes = (8, 8), (2, 3)
+    kd = (4, 3)
+    x = rng.standard_normal((1, 2) + n)
+    x[0, 0, 0, 0] = 6.0
+    x[0, 1, 3, 3] = -7.0
+    w = _cplx(rng, (2, 2) + kd, 0.5)
+    gy = rng.standard_normal((1, 2) + n)
+    prec = O.sigma_mode("fp32", 2.0)
+    lo, hi = O.sigma_bounds(x, 2.0)
+
+    def loss(xx):
+        u = np.where(xx < lo, lo, np.where(xx > hi, hi, xx))
+        xh = O.forward_spectrum(u, n, modes)
+        y = O.inverse_spectrum(O.contract_dense(xh, w), n, modes)
+        return float(np.sum(gy * y))
+
+    gx = O.bwd_data(x, w, gy, n, modes, prec)
+    h = 1e-6
+    err = 0.0
+    for idx in [(0, 0, 0, 0), (0, 1, 3, 3), (0, 0, 4, 2), (0, 1, 6, 7), (0, 0, 7, 1)]:
+        xp, xm = x.copy(), x.copy()
+        xp[idx] += h
+        xm[idx] -= h
+        fd = (loss(xp) - loss(xm)) / (2 * h)
+        err = max(err, abs(fd - gx[idx]) / max(1.0, abs(gx[idx])))
+    return err
+
+
 ALL_PINS = {
+    "sigma_closed_form": (pin_sigma_closed_form, 1e-12),
+    "sigma_fd_frozen": (pin_sigma_fd_frozen, 1e-7),
     "rel_l2_hand": (pin_rel_l2_hand, 1e-15),
     "max_plane_hand": (pin_max_plane_hand, 1e-15),
     "cp_explicit": (pin_cp_explicit, 1e-13),
@@ -925,7 +987,29 @@ def _rel_l2_in_input_dtype(a, b):
     return float(num / den) if den else float(num)
 
 
+def _sigma_bounds_sample_std(x, k):
+    xf = np.asarray(x, dtype=np.float64)
+    axes = tuple(range(2, xf.ndim))
+    mu = xf.mean(axis=axes, keepdims=True)
+    sd = xf.std(axis=axes, ddof=1, keepdims=True)
+    return mu - k * sd, mu + k * sd
+
+
+def _sigma_bounds_whole_tensor(x, k):
+    xf = np.asarray(x, dtype=np.float64)
+    mu, sd = xf.mean(), xf.std()
+    shape = xf.shape[:2] + (1,) * (xf.ndim - 2)
+    return np.full(shape, mu - k * sd), np.full(shape, mu + k * sd)
+
+
 MUTATIONS = {
+    "sigma_sample_std": ("sigma_bounds", lambda orig: _sigma_bounds_sample_std),
+    "sigma_whole_tensor": ("sigma_bounds", lambda orig: _sigma_bounds_whole_tensor),
+    "sigma_one_sigma": ("sigma_bounds", lambda orig: (lambda x, k: orig(x, k / 2.0))),
+    "sigma_one_sided": ("sigma_bounds", lambda orig: (
+        lambda x, k: (np.full_like(orig(x, k)[0], -np.inf), orig(x, k)[1]))),
+    "sigma_grad_ones": ("preactivation_grad", lambda orig: (
+        lambda x, p: np.ones(np.shape(x)) if O.preact_kind(p)[0] == "sigma" else orig(x, p))),
     "rel_l2_divides_by_a": ("rel_l2", lambda orig: (lambda a, b: orig(b, a))),
     "rel_l2_no_sqrt": ("rel_l2", lambda orig: (lambda a, b: orig(a, b) ** 2)),
     "rel_l2_real_part_only": ("rel_l2", lambda orig: (
