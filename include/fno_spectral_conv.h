@@ -78,13 +78,28 @@ typedef enum {
  *   TANH      : f(x) = tanh(x),  f'(x) = 1 - tanh(x)^2
  *   HARD_CLIP : f(x) = min(max(x, -clip), clip),  f'(x) = 1 for |x| <= clip,
  *               0 otherwise (the bound's own point counts as inside)
+ *   SIGMA_CLIP: the statistics-based clip of App. B.6 (with clip = 2 its
+ *               2-sigma clip): every (batch, channel) plane of x is clipped
+ *               to [mu - clip sigma, mu + clip sigma], mu and sigma the mean
+ *               and the population standard deviation of that plane's N
+ *               values (computed in double); f'(x) = 1 inside the bounds
+ *               (their own points included), 0 outside: the bounds are held
+ *               constant in the gradient (no gradient through mu and sigma).
+ *               A plane holding a non-finite value has NaN bounds and gives
+ *               NaN throughout.  The comparisons with the bounds are made in
+ *               double.  The forward, data-gradient and (without caches)
+ *               weight-gradient calls compute the statistics themselves
+ *               (one extra read of x); their workspaces grow by 16 bytes per
+ *               (batch, input channel) plane.  The plane transforms then run
+ *               on the table-free kernels.
  * NaN inputs give NaN in f and f'.  In fp16 storage f(x) is rounded once to
  * fp16 before the transform. */
 typedef enum {
   FNO_PREACT_DEFAULT = 0,   /* TANH for FNO_PREC_FP16_TANH, NONE for FNO_PREC_FP32 */
   FNO_PREACT_NONE = 1,
   FNO_PREACT_TANH = 2,
-  FNO_PREACT_HARD_CLIP = 3
+  FNO_PREACT_HARD_CLIP = 3,
+  FNO_PREACT_SIGMA_CLIP = 4 /* clip each (batch, channel) plane to mean +- clip * sigma */
 } fno_preactivation;
 
 /* Spectral weight parameterisation: dense, Tucker (the tensorised FNO of
@@ -129,7 +144,8 @@ typedef struct {
   int64_t modes[3];
   int64_t rank[5];
   int32_t preact;        /* fno_preactivation              */
-  float clip;            /* bound of FNO_PREACT_HARD_CLIP  */
+  float clip;            /* bound of FNO_PREACT_HARD_CLIP; number of standard
+                            deviations of FNO_PREACT_SIGMA_CLIP (both > 0) */
 } fno_conv_desc;
 
 /* Spectral weights R (device pointers, element type of the precision mode).

@@ -27,6 +27,7 @@ FNO_PREACT_DEFAULT = 0
 FNO_PREACT_NONE = 1
 FNO_PREACT_TANH = 2
 FNO_PREACT_HARD_CLIP = 3
+FNO_PREACT_SIGMA_CLIP = 4
 FNO_WEIGHT_DENSE = 0
 FNO_WEIGHT_TUCKER = 1
 FNO_WEIGHT_CP = 2

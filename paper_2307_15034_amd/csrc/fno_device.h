@@ -108,6 +108,20 @@ __device__ __forceinline__ float preact_grad_f32(float x, int act, float clip) {
   return 1.0f - t * t;
 }
 
+// The statistics-based clip (act 3) with its plane's bounds [lo, hi],
+// compared in double; NaN bounds (a plane with a non-finite value) give NaN.
+__device__ __forceinline__ float preact_sigma_f32(float x, double lo, double hi) {
+  const double xd = (double)x;
+  if (lo != lo) return __builtin_nanf("");
+  return xd < lo ? (float)lo : (xd > hi ? (float)hi : x);
+}
+
+__device__ __forceinline__ float preact_sigma_grad_f32(float x, double lo, double hi) {
+  const double xd = (double)x;
+  if (lo != lo || x != x) return __builtin_nanf("");
+  return (xd >= lo && xd <= hi) ? 1.0f : 0.0f;
+}
+
 // Round-to-nearest-even conversions to the storage type.
 __device__ __forceinline__ _Float16 to_h(float v) { return (_Float16)v; }
 
@@ -155,12 +169,13 @@ __device__ __forceinline__ void wave_lds_sync() {
 template <typename T>
 __device__ __forceinline__ typename MM<T>::frag load_row_frag(const T* row, int n0, int Nb,
                                                               bool vrow, int act,
-                                                              float clip, int vec);
+                                                              float clip, int vec,
+                                                              double lo, double hi);
 
 template <>
 __device__ __forceinline__ h8 load_row_frag<_Float16>(const _Float16* row, int n0, int Nb,
                                                       bool vrow, int act, float clip,
-                                                      int vec) {
+                                                      int vec, double lo, double hi) {
   h8 v = MM<_Float16>::zero();
   if (vrow) {
     if (vec) {
@@ -170,7 +185,10 @@ __device__ __forceinline__ h8 load_row_frag<_Float16>(const _Float16* row, int n
       for (int i = 0; i < 8; ++i)
         if (n0 + i < Nb) v[i] = row[n0 + i];
     }
-    if (act) {
+    if (act == 3) {
+#pragma unroll
+      for (int i = 0; i < 8; ++i) v[i] = to_h(preact_sigma_f32((float)v[i], lo, hi));
+    } else if (act) {
 #pragma unroll
       for (int i = 0; i < 8; ++i) v[i] = to_h(preact_f32((float)v[i], act, clip));
     }
@@ -180,7 +198,8 @@ __device__ __forceinline__ h8 load_row_frag<_Float16>(const _Float16* row, int n
 
 template <>
 __device__ __forceinline__ f4 load_row_frag<float>(const float* row, int n0, int Nb,
-                                                   bool vrow, int act, float clip, int vec) {
+                                                   bool vrow, int act, float clip, int vec,
+                                                   double lo, double hi) {
   f4 v = f4{0.0f, 0.0f, 0.0f, 0.0f};
   if (vrow) {
     if (vec) {
@@ -190,7 +209,10 @@ __device__ __forceinline__ f4 load_row_frag<float>(const float* row, int n0, int
       for (int i = 0; i < 4; ++i)
         if (n0 + i < Nb) v[i] = row[n0 + i];
     }
-    if (act) {
+    if (act == 3) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) v[i] = preact_sigma_f32(v[i], lo, hi);
+    } else if (act) {
 #pragma unroll
       for (int i = 0; i < 4; ++i) v[i] = preact_f32(v[i], act, clip);
     }

@@ -9,7 +9,7 @@ namespace fno {
 
 enum Elem { ELEM_F32 = 0, ELEM_F16 = 1 };
 // Pre-activation of a plan (the `act` codes of the kernel arguments).
-enum Act { ACT_NONE = 0, ACT_TANH = 1, ACT_CLIP = 2 };
+enum Act { ACT_NONE = 0, ACT_TANH = 1, ACT_CLIP = 2, ACT_SIGMA = 3 };
 
 // Truncated real-to-complex transform of the last two axes of every plane
 // [planes][Na][Nb] -> spectrum [planes][Ka][Kb] (complex).  Step A runs the
@@ -41,6 +41,10 @@ struct R2CArgs {
   int NaC;          // Na padded to 32
   const void* lut;  // fp16 f(x) of every non-negative fp16 code (32768 entries; f odd)
   int lut_sat;      // first code from which f stays at its +inf value
+  // ACT_SIGMA (table-free kernels only): per statistics group (batch x
+  // channel) the clip bounds (lo, hi) in double; plane p uses group p / bgroup
+  const double* bounds;
+  int bgroup;
 };
 
 // Inverse of the above: spectrum [planes][Ka][Kb] -> y [planes][Na][Nb],
@@ -72,7 +76,15 @@ struct C2RArgs {
   const void* sIc;  //   t = 32 ks + 4 q + e (e < 4) or 32 ks + 16 + 4 q + e - 4
   const void* lut;  // fp16 f'(x) of every non-negative fp16 code (32768 entries; f' even)
   int lut_sat;      // first code from which f' stays at its +inf value
+  const double* bounds;  // ACT_SIGMA: as in R2CArgs
+  int bgroup;
 };
+
+// Clip bounds of the statistics-based pre-activation: for each of `groups`
+// contiguous groups of n values of x (fp16 or fp32), mean -/+ k population
+// standard deviations, in double (NaN when not finite).
+hipError_t launch_sigma_stats(int elem, const void* x, int64_t groups, int64_t n, double k,
+                              double* bounds, hipStream_t s);
 
 // Complex DFT along a middle axis: in [outer][Lin][inner] -> out
 // [outer][Lout][inner], out[o][t][j] = scale * sum_l E[t][l] in[o][l][j].

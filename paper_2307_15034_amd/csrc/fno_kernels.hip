@@ -48,6 +48,12 @@ __global__ __launch_bounds__(256) void r2c_plane_kernel(R2CArgs a) {
   const T* cB = reinterpret_cast<const T*>(a.cB);
   const T* sB = reinterpret_cast<const T*>(a.sB);
   const int nta = a.Kap16 >> 4;
+  // statistics-based clip: this plane's bounds
+  double slo = 0.0, shi = 0.0;
+  if (a.act == ACT_SIGMA) {
+    slo = a.bounds[2 * (p / a.bgroup)];
+    shi = a.bounds[2 * (p / a.bgroup) + 1];
+  }
 
   f4 accR[2][NTB], accI[2][NTB];
 #pragma unroll
@@ -78,7 +84,7 @@ __global__ __launch_bounds__(256) void r2c_plane_kernel(R2CArgs a) {
         for (int u = 0; u < R2C_NRT; ++u)
           if (rt0 + 4 * u < nrt)
             af[u] = load_row_frag<T>(rp[u], k0 + g * KPL, a.Nb, vrow[u], a.act, a.clip,
-                                    a.vec);
+                                    a.vec, slo, shi);
 #pragma unroll
         for (int ct = 0; ct < NCT; ++ct) {
           frag bf = M::ld(twA + (int64_t)(ct * 16 + r16) * a.Nbp + k0 + g * KPL);
@@ -359,8 +365,15 @@ __global__ __launch_bounds__(256) void c2r_plane_kernel(C2RArgs a) {
             if (a.epilogue) {
               float xv[16];
               load16<T>(xin + off, xv, nval, a.vec);
+              if (a.act == ACT_SIGMA) {
+                const int64_t grp = p / a.bgroup;
+                const double lo = a.bounds[2 * grp], hi = a.bounds[2 * grp + 1];
 #pragma unroll
-              for (int i = 0; i < 16; ++i) v[i] *= preact_grad_f32(xv[i], a.act, a.clip);
+                for (int i = 0; i < 16; ++i) v[i] *= preact_sigma_grad_f32(xv[i], lo, hi);
+              } else {
+#pragma unroll
+                for (int i = 0; i < 16; ++i) v[i] *= preact_grad_f32(xv[i], a.act, a.clip);
+              }
             }
             store16<T>(yout + off, v, nval, a.vec);
           }
@@ -1107,6 +1120,75 @@ __global__ void scale_kernel(float* p, int64_t n, float s) {
   if (i < n) p[i] *= s;
 }
 
+// Clip bounds of the statistics-based pre-activation, one work-group per
+// group of n contiguous values.  The sums run in double over the values
+// shifted by the group's first one (which keeps the sum of squares from
+// cancelling when the mean is large against the spread); a non-finite value
+// anywhere in the group makes both bounds NaN.
+template <typename T>
+__global__ __launch_bounds__(256) void sigma_stats_kernel(const T* x, int64_t n, double k,
+                                                          double* bounds) {
+  __shared__ double red[2][4];
+  __shared__ int redb[4];
+  const int64_t gi = blockIdx.x;
+  const T* xg = x + gi * n;
+  const double shift = (double)xg[0];
+  double s1 = 0.0, s2 = 0.0;
+  int bad = 0;
+  constexpr int V = 16 / (int)sizeof(T);
+  if (((n * (int64_t)sizeof(T)) & 15) == 0) {
+    using vec = u32x4;
+    const vec* xv = reinterpret_cast<const vec*>(xg);
+    const int64_t nv = n / V;
+    for (int64_t i = threadIdx.x; i < nv; i += 256) {
+      const vec w = xv[i];
+      const T* e = reinterpret_cast<const T*>(&w);
+#pragma unroll
+      for (int j = 0; j < V; ++j) {
+        const double v = (double)e[j];
+        bad |= !__builtin_isfinite(v);
+        const double dv = v - shift;
+        s1 += dv;
+        s2 = __builtin_fma(dv, dv, s2);
+      }
+    }
+  } else {
+    for (int64_t i = threadIdx.x; i < n; i += 256) {
+      const double v = (double)xg[i];
+      bad |= !__builtin_isfinite(v);
+      const double dv = v - shift;
+      s1 += dv;
+      s2 = __builtin_fma(dv, dv, s2);
+    }
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    s1 += __shfl_xor(s1, o);
+    s2 += __shfl_xor(s2, o);
+    bad |= __shfl_xor(bad, o);
+  }
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  if (lane == 0) {
+    red[0][wave] = s1;
+    red[1][wave] = s2;
+    redb[wave] = bad;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    const double t1 = (red[0][0] + red[0][1]) + (red[0][2] + red[0][3]);
+    const double t2 = (red[1][0] + red[1][1]) + (red[1][2] + red[1][3]);
+    const int b = redb[0] | redb[1] | redb[2] | redb[3];
+    const double m1 = t1 / (double)n;
+    const double var = t2 / (double)n - m1 * m1;
+    const double sd = __builtin_sqrt(var > 0.0 ? var : 0.0);
+    const double mu = shift + m1;
+    double lo = mu - k * sd, hi = mu + k * sd;
+    if (b || !__builtin_isfinite(lo) || !__builtin_isfinite(hi)) lo = hi = __builtin_nan("");
+    bounds[2 * gi] = lo;
+    bounds[2 * gi + 1] = hi;
+  }
+}
+
 // ---------------------------------------------------------------------------
 // Launchers
 // ---------------------------------------------------------------------------
@@ -1157,6 +1239,20 @@ static hipError_t c2r_dispatch(int nct, const C2RArgs& a, size_t lds, hipStream_
 hipError_t launch_c2r(int elem, int nct, const C2RArgs& a, size_t lds, hipStream_t s) {
   return elem == ELEM_F16 ? c2r_dispatch<_Float16>(nct, a, lds, s)
                           : c2r_dispatch<float>(nct, a, lds, s);
+}
+
+hipError_t launch_sigma_stats(int elem, const void* x, int64_t groups, int64_t n, double k,
+                              double* bounds, hipStream_t s) {
+  if (groups == 0) return hipSuccess;
+  if (groups < 0 || groups > 0x7fffffff || n < 1) return hipErrorInvalidValue;
+  dim3 grid((unsigned)groups), block(256);
+  if (elem == ELEM_F16)
+    hipLaunchKernelGGL(sigma_stats_kernel<_Float16>, grid, block, 0, s,
+                       reinterpret_cast<const _Float16*>(x), n, k, bounds);
+  else
+    hipLaunchKernelGGL(sigma_stats_kernel<float>, grid, block, 0, s,
+                       reinterpret_cast<const float*>(x), n, k, bounds);
+  return hipGetLastError();
 }
 
 hipError_t launch_axis(int elem, const AxisArgs& a, size_t lds, hipStream_t s) {

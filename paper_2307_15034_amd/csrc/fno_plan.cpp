@@ -42,6 +42,7 @@ int act_of(const fno_conv_desc* d) {
     case FNO_PREACT_NONE: return ACT_NONE;
     case FNO_PREACT_TANH: return ACT_TANH;
     case FNO_PREACT_HARD_CLIP: return ACT_CLIP;
+    case FNO_PREACT_SIGMA_CLIP: return ACT_SIGMA;
     default: return d->precision == FNO_PREC_FP16_TANH ? ACT_TANH : ACT_NONE;
   }
 }
@@ -51,8 +52,10 @@ fno_status check_desc(const fno_conv_desc* d) {
   if (d->ndim < 1 || d->ndim > 3) return FNO_ERR_INVALID_ARGUMENT;
   if (d->precision != FNO_PREC_FP32 && d->precision != FNO_PREC_FP16_TANH)
     return FNO_ERR_INVALID_ARGUMENT;
-  if (d->preact < FNO_PREACT_DEFAULT || d->preact > FNO_PREACT_HARD_CLIP)
+  if (d->preact < FNO_PREACT_DEFAULT || d->preact > FNO_PREACT_SIGMA_CLIP)
     return FNO_ERR_INVALID_ARGUMENT;
+  if (d->preact == FNO_PREACT_SIGMA_CLIP && !(d->clip > 0.0f && d->clip <= 3.4028235e38f))
+    return FNO_ERR_INVALID_ARGUMENT;  // a positive finite number of deviations
   if (d->preact == FNO_PREACT_HARD_CLIP) {
     // a positive finite bound, one that fp16 storage can hold in fp16 mode
     const float lim = d->precision == FNO_PREC_FP16_TANH ? 65504.0f : 3.4028235e38f;
@@ -324,8 +327,8 @@ struct Geo {
   int nd;
   int elem;          // ELEM_F16 / ELEM_F32
   int es;            // element bytes
-  int act;           // pre-activation: ACT_NONE / ACT_TANH / ACT_CLIP
-  float clip;        // bound of ACT_CLIP
+  int act;           // pre-activation: ACT_NONE / ACT_TANH / ACT_CLIP / ACT_SIGMA
+  float clip;        // bound of ACT_CLIP; deviations of ACT_SIGMA
   int64_t B, Cin, Cout;
   int64_t N;         // prod n
   int64_t K;         // prod K_j
@@ -384,7 +387,7 @@ Geo make_geo(const fno_conv_desc* d) {
   g.elem = d->precision == FNO_PREC_FP16_TANH ? ELEM_F16 : ELEM_F32;
   g.es = g.elem == ELEM_F16 ? 2 : 4;
   g.act = act_of(d);
-  g.clip = g.act == ACT_CLIP ? d->clip : 0.0f;
+  g.clip = g.act == ACT_CLIP || g.act == ACT_SIGMA ? d->clip : 0.0f;
   g.B = d->batch;
   g.Cin = d->c_in;
   g.Cout = d->c_out;
@@ -686,7 +689,7 @@ PlanKey key_of(const fno_conv_desc* d, int device) {
   if (d->weight_kind == FNO_WEIGHT_CP) k.v[14] = d->rank[0];
   const int act = act_of(d);
   k.v[19] = act;
-  if (act == ACT_CLIP) {
+  if (act == ACT_CLIP || act == ACT_SIGMA) {
     uint32_t bits;
     std::memcpy(&bits, &d->clip, 4);
     k.v[20] = bits;
@@ -854,7 +857,11 @@ size_t tucker_path_bytes(const fno_conv_desc* d, const std::vector<PStep>& path)
 size_t tucker_wgrad_bytes(const fno_conv_desc* d, const Plan* pl);
 size_t cp_wgrad_bytes(const fno_conv_desc* d, const Plan* pl);
 
-size_t ws_bytes(const fno_conv_desc* d, const Plan* pl, fno_op op, bool caches) {
+size_t ws_bytes(const fno_conv_desc* d, const Plan* pl, fno_op op, bool caches);
+
+// The workspace without the clip bounds of the statistics-based
+// pre-activation (a multiple of 256 bytes; the bounds follow it).
+size_t ws_core(const fno_conv_desc* d, const Plan* pl, fno_op op, bool caches) {
   const Geo& g = pl->g;
   WsLayout w;
   const bool tucker = factorized(d);
@@ -883,8 +890,26 @@ size_t ws_bytes(const fno_conv_desc* d, const Plan* pl, fno_op op, bool caches) 
     w.add(ws_bytes(d, pl, FNO_OP_BWD_DATA, true));
     if (tucker) w.add(ws_bytes(d, pl, FNO_OP_BWD_WEIGHT, true));
   }
-  return std::max<size_t>(w.total, 256);
+  return std::max<size_t>((size_t)round_up((int64_t)w.total, 256), 256);
 }
+
+// Clip bounds (lo, hi in double) of every (batch, input channel) plane: held
+// by the forward, data-gradient and cache-less weight-gradient workspaces
+// (the combined backward uses its data part's).
+size_t bounds_bytes(const Plan* pl, fno_op op, bool caches) {
+  const Geo& g = pl->g;
+  if (g.act != ACT_SIGMA) return 0;
+  if (op == FNO_OP_BWD || (op == FNO_OP_BWD_WEIGHT && caches)) return 0;
+  return (size_t)round_up(g.B * g.Cin * 16, 256);
+}
+
+size_t ws_bytes(const fno_conv_desc* d, const Plan* pl, fno_op op, bool caches) {
+  return ws_core(d, pl, op, caches) + bounds_bytes(pl, op, caches);
+}
+
+// Computes the clip bounds of x into `bounds` when the plan's pre-activation
+// is the statistics-based clip (nothing otherwise).
+fno_status run_sigma_stats(const Plan* pl, const void* x, double* bounds, hipStream_t s);
 
 // --------------------------------------------------------------------------
 // Kernel sequences
@@ -965,8 +990,19 @@ void prof_drain() {
 // Forward truncated transform of planes -> spectrum [B][C][K...].
 // scale_mode 0: 1/N normalisation (input spectrum), 1: 1/sqrt(N) (gradient).
 // pre: apply the plan's pre-activation (if it has one) to the input.
+fno_status run_sigma_stats(const Plan* pl, const void* x, double* bounds, hipStream_t s) {
+  const Geo& g = pl->g;
+  if (g.act != ACT_SIGMA) return FNO_OK;
+  FNO_HIP(timed("sigma_stats", s, [&] {
+    return launch_sigma_stats(g.elem, x, g.B * g.Cin, g.N, (double)g.clip, bounds, s);
+  }));
+  return FNO_OK;
+}
+
+// bounds: the clip bounds of the statistics-based pre-activation (read when
+// it is applied to the input).
 fno_status run_r2c(const Plan* pl, const void* in, void* spec, void* inter, int64_t C,
-                   int pre, int scale_mode, hipStream_t s) {
+                   int pre, int scale_mode, hipStream_t s, const double* bounds = nullptr) {
   const Geo& g = pl->g;
   R2CArgs a{};
   a.zeros = pl->t.zeros;
@@ -996,16 +1032,27 @@ fno_status run_r2c(const Plan* pl, const void* in, void* spec, void* inter, int6
   a.act = a.do_tanh ? g.act : ACT_NONE;
   a.clip = g.clip;
   const bool do_tanh = a.do_tanh;
-  const char* kname = !do_tanh ? "r2c_plane" : g.act == ACT_TANH ? "r2c_plane_tanh" : "r2c_plane_clip";
+  const char* kname = !do_tanh                ? "r2c_plane"
+                      : g.act == ACT_TANH      ? "r2c_plane_tanh"
+                      : g.act == ACT_CLIP      ? "r2c_plane_clip"
+                                               : "r2c_plane_sigma";
   a.vec = (g.Nb % 8) == 0;
+  // the statistics-based clip has per-plane bounds, no table: the
+  // table-free kernel only
+  const bool sigma = do_tanh && g.act == ACT_SIGMA;
+  if (sigma) {
+    if (!bounds) return FNO_ERR_INTERNAL;
+    a.bounds = bounds;
+    a.bgroup = g.nd == 3 ? g.N1 : 1;
+  }
   a.twAc = pl->t.twAc;
   a.cBc = pl->t.cBc;
   a.sBc = pl->t.sBc;
   a.NaC = g.NaC;
   a.lut = pl->t.lutAct;
   if (a.planes > 0x7fffffff || (g.nd == 3 && g.B * C > 65535)) return FNO_ERR_UNSUPPORTED;
-  bool done = false;
-  if (g.elem == ELEM_F16 && a.vec && g.Kb % 4 == 0 && g.Nb <= 256 && g.Na <= 128) {
+  bool done = sigma;
+  if (!done && g.elem == ELEM_F16 && a.vec && g.Kb % 4 == 0 && g.Nb <= 256 && g.Na <= 128) {
     const int nka = g.Nbp / 32, ntb = g.Kbp / 16, nta = g.Kap16 / 16;
     const size_t lds = r2c_chain_lds_bytes(nka, ntb, nta, g.NaC, do_tanh);
     const int64_t waves = (int64_t)kChainWaves;
@@ -1060,7 +1107,7 @@ fno_status run_r2c(const Plan* pl, const void* in, void* spec, void* inter, int6
     if (e == hipSuccess) done = true;
     else if (e != hipErrorNotSupported) return hip_fail(e, kname);
   }
-  if (!done) FNO_HIP(timed(kname, s, [&] { return launch_r2c(g.elem, g.nct, a, r2c_lds_bytes(g.elem, g.Kbp, g.R_f), s); }));
+  if (!done || sigma) FNO_HIP(timed(kname, s, [&] { return launch_r2c(g.elem, g.nct, a, r2c_lds_bytes(g.elem, g.Kbp, g.R_f), s); }));
   if (g.nd == 3) {
     AxisArgs x{};
     x.in = inter;
@@ -1081,7 +1128,8 @@ fno_status run_r2c(const Plan* pl, const void* in, void* spec, void* inter, int6
 
 // Inverse: spectrum [B][C][K...] -> planes, out = scale * sum Re(Z e^{+i theta}).
 fno_status run_c2r(const Plan* pl, const void* spec, void* out, void* inter, int64_t C,
-                   float scale, const void* x_epi, hipStream_t s) {
+                   float scale, const void* x_epi, hipStream_t s,
+                   const double* bounds = nullptr) {
   const Geo& g = pl->g;
   const void* src = spec;
   if (g.nd == 3 && g.B * C > 65535) return FNO_ERR_UNSUPPORTED;
@@ -1128,8 +1176,18 @@ fno_status run_c2r(const Plan* pl, const void* spec, void* out, void* inter, int
   a.cIc = pl->t.cIc;
   a.sIc = pl->t.sIc;
   a.lut = pl->t.lutGrad;
-  const char* kname = !x_epi ? "c2r_plane"
-                      : g.act == ACT_TANH ? "c2r_plane_tanh_grad" : "c2r_plane_clip_grad";
+  const char* kname = !x_epi              ? "c2r_plane"
+                      : g.act == ACT_TANH ? "c2r_plane_tanh_grad"
+                      : g.act == ACT_CLIP ? "c2r_plane_clip_grad"
+                                          : "c2r_plane_sigma_grad";
+  if (x_epi && g.act == ACT_SIGMA) {
+    // per-plane bounds, no table: the table-free kernel only
+    if (!bounds) return FNO_ERR_INTERNAL;
+    a.bounds = bounds;
+    a.bgroup = g.nd == 3 ? g.N1 : 1;
+    FNO_HIP(timed(kname, s, [&] { return launch_c2r(g.elem, g.nct, a, c2r_lds_bytes(g.elem, g.Kbp, g.Kap, g.R_i), s); }));
+    return FNO_OK;
+  }
   if (g.elem == ELEM_F16 && g.Nb % 16 == 0 && g.Kb % 4 == 0 && g.Nb <= 256 && g.Na <= 128) {
     const int ng = g.Nb64 / 64, ntb = g.Kbp / 16, nkz = g.Kap / 32;
     const size_t lds = c2r_chain_lds_bytes(ng, ntb, g.Kap, g.Na, x_epi != nullptr);
@@ -1644,13 +1702,15 @@ fno_status fwd_impl(const fno_conv_desc* d, const void* x, const fno_weights* w,
   char* ys = base + L.add(spec_bytes(g, g.Cout));
   char* inter = base + L.add(std::max(inter3d_bytes(g, g.Cin), inter3d_bytes(g, g.Cout)));
   char* tsc = base + L.total;
+  double* bounds = (double*)(base + ws_core(d, pl, FNO_OP_FWD, true));
   void* xh = x_hat_out ? x_hat_out : (void*)xs;
   struct Flag {  // profiler events stay off for an allocation-free call
     bool prev;
     explicit Flag(bool on) : prev(g_no_alloc_call) { g_no_alloc_call = on; }
     ~Flag() { g_no_alloc_call = prev; }
   } flag(!build_plan);
-  if ((st = run_r2c(pl, x, xh, inter, g.Cin, 1, 0, s)) != FNO_OK) return st;
+  if ((st = run_sigma_stats(pl, x, bounds, s)) != FNO_OK) return st;
+  if ((st = run_r2c(pl, x, xh, inter, g.Cin, 1, 0, s, bounds)) != FNO_OK) return st;
   if (d->weight_kind == FNO_WEIGHT_DENSE) {
     if ((st = run_contract(pl, xh, w->dense, ys, false, s)) != FNO_OK) return st;
   } else {
@@ -1812,7 +1872,9 @@ fno_status fno_spectral_conv_bwd_data(const fno_conv_desc* d, const void* x,
   char* gxs = base + L.add(spec_bytes(g, g.Cin));
   char* inter = base + L.add(std::max(inter3d_bytes(g, g.Cin), inter3d_bytes(g, g.Cout)));
   char* tsc = base + L.total;
+  double* bounds = (double*)(base + ws_core(d, pl, FNO_OP_BWD_DATA, true));
   void* gh = gy_hat_out ? gy_hat_out : (void*)gs;
+  if ((st = run_sigma_stats(pl, x, bounds, s)) != FNO_OK) return st;
   if ((st = run_r2c(pl, gy, gh, inter, g.Cout, 0, 1, s)) != FNO_OK) return st;
   if (d->weight_kind == FNO_WEIGHT_DENSE) {
     if ((st = run_contract(pl, gh, w->dense, gxs, true, s)) != FNO_OK) return st;
@@ -1820,7 +1882,7 @@ fno_status fno_spectral_conv_bwd_data(const fno_conv_desc* d, const void* x,
     if ((st = run_tucker_path(d, pl, true, gh, w, gxs, tsc, s)) != FNO_OK) return st;
   }
   const float sc = (float)(1.0 / std::sqrt((double)g.N));
-  return run_c2r(pl, gxs, gx, inter, g.Cin, sc, pre_on ? x : nullptr, s);
+  return run_c2r(pl, gxs, gx, inter, g.Cin, sc, pre_on ? x : nullptr, s, bounds);
 }
 
 fno_status fno_spectral_conv_bwd_weight(const fno_conv_desc* d, const void* x, const void* gy,
@@ -1857,9 +1919,9 @@ fno_status fno_spectral_conv_bwd_weight(const fno_conv_desc* d, const void* x, c
     char* gs = base + L.add(spec_bytes(g, g.Cout));
     char* inter = base + L.add(std::max(inter3d_bytes(g, g.Cin), inter3d_bytes(g, g.Cout)));
     if (!xh) {
-      if ((st = run_r2c(pl, x, xs, inter, g.Cin, 1, 0, s)) !=
-          FNO_OK)
-        return st;
+      double* bounds = (double*)(base + ws_core(d, pl, FNO_OP_BWD_WEIGHT, false));
+      if ((st = run_sigma_stats(pl, x, bounds, s)) != FNO_OK) return st;
+      if ((st = run_r2c(pl, x, xs, inter, g.Cin, 1, 0, s, bounds)) != FNO_OK) return st;
       xh = xs;
     }
     if (!gh) {
@@ -1936,7 +1998,9 @@ fno_status fno_spectral_conv_bwd(const fno_conv_desc* d, const void* x, const fn
       (void)Ld.add(spec_bytes(g, g.Cout));
       (void)Ld.add(spec_bytes(g, g.Cin));
       char* inter = wsd + Ld.add(std::max(inter3d_bytes(g, g.Cin), inter3d_bytes(g, g.Cout)));
-      if ((st = run_r2c(pl, x, xs, inter, g.Cin, 1, 0, s)) != FNO_OK) return st;
+      // the data part has left the clip bounds in its workspace
+      const double* bounds = (const double*)(wsd + ws_core(d, pl, FNO_OP_BWD_DATA, true));
+      if ((st = run_r2c(pl, x, xs, inter, g.Cin, 1, 0, s, bounds)) != FNO_OK) return st;
     }
     return fno_spectral_conv_bwd_weight(d, x, gy, w, cache ? x_hat : xs, gh, gw, wsw, nw, s);
   }
@@ -1946,9 +2010,11 @@ fno_status fno_spectral_conv_bwd(const fno_conv_desc* d, const void* x, const fn
   (void)Ld.add(spec_bytes(g, g.Cout));
   char* gxs = wsd + Ld.add(spec_bytes(g, g.Cin));
   char* inter = wsd + Ld.add(std::max(inter3d_bytes(g, g.Cin), inter3d_bytes(g, g.Cout)));
+  double* bounds = (double*)(wsd + ws_core(d, pl, FNO_OP_BWD_DATA, true));
+  if (pre_on && (st = run_sigma_stats(pl, x, bounds, s)) != FNO_OK) return st;
   const void* xh = x_hat;
   if (!cache) {
-    if ((st = run_r2c(pl, x, xs, inter, g.Cin, 1, 0, s)) != FNO_OK) return st;
+    if ((st = run_r2c(pl, x, xs, inter, g.Cin, 1, 0, s, bounds)) != FNO_OK) return st;
     xh = xs;
   }
   if ((st = run_r2c(pl, gy, gh, inter, g.Cout, 0, 1, s)) != FNO_OK) return st;
@@ -1989,7 +2055,7 @@ fno_status fno_spectral_conv_bwd(const fno_conv_desc* d, const void* x, const fn
     }));
   }
   const float sc = (float)(1.0 / std::sqrt((double)g.N));
-  return run_c2r(pl, gxs, gx, inter, g.Cin, sc, pre_on ? x : nullptr, s);
+  return run_c2r(pl, gxs, gx, inter, g.Cin, sc, pre_on ? x : nullptr, s, bounds);
 }
 
 fno_status fno_profile_enable(int32_t enable) {

@@ -27,8 +27,9 @@ def say(msg: str) -> None:
 
 def prec_codes(prec: str):
     """(library precision code, numpy storage dtype, oracle mode) of a mode
-    name: "fp32", "fp16_tanh", "fp32_tanh", "fp16" or "fp16_clip:<c>" /
-    "fp32_clip:<c>" (the oracle's mode strings)."""
+    name: "fp32", "fp16_tanh", "fp32_tanh", "fp16", "fp16_clip:<c>" /
+    "fp32_clip:<c>" or "fp16_sigma:<k>" / "fp32_sigma:<k>" (the oracle's mode
+    strings)."""
     from paper_2307_15034_amd import binding as B
     O.preact_kind(prec)  # rejects unknown names
     if prec.startswith("fp32"):
@@ -44,6 +45,8 @@ def preact_codes(prec: str):
         return B.FNO_PREACT_DEFAULT, 0.0
     if kind == "clip":
         return B.FNO_PREACT_HARD_CLIP, float(c)
+    if kind == "sigma":
+        return B.FNO_PREACT_SIGMA_CLIP, float(c)
     return (B.FNO_PREACT_TANH if kind == "tanh" else B.FNO_PREACT_NONE), 0.0
 
 

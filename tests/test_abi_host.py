@@ -264,7 +264,10 @@ def test_invalid_enums_and_counts():
 
 def test_preactivation_descriptor_checks():
     P16, P32 = B.FNO_PREC_FP16_TANH, B.FNO_PREC_FP32
-    bad = [(P16, 4, 1.0), (P16, -1, 1.0), (P16, B.FNO_PREACT_HARD_CLIP, 0.0),
+    SIG = B.FNO_PREACT_SIGMA_CLIP
+    bad = [(P16, 5, 1.0), (P16, -1, 1.0), (P16, B.FNO_PREACT_HARD_CLIP, 0.0),
+           (P16, SIG, 0.0), (P32, SIG, -2.0), (P16, SIG, float("nan")),
+           (P32, SIG, float("inf")),
            (P16, B.FNO_PREACT_HARD_CLIP, -1.0), (P16, B.FNO_PREACT_HARD_CLIP, float("nan")),
            (P32, B.FNO_PREACT_HARD_CLIP, float("inf")),
            (P16, B.FNO_PREACT_HARD_CLIP, 70000.0)]       # beyond fp16's largest value
@@ -275,10 +278,32 @@ def test_preactivation_descriptor_checks():
         assert e.value.status == B.FNO_ERR_INVALID_ARGUMENT, (prec, pa, clip)
     good = [(P32, B.FNO_PREACT_HARD_CLIP, 70000.0), (P16, B.FNO_PREACT_HARD_CLIP, 65504.0),
             (P16, B.FNO_PREACT_TANH, float("nan")), (P32, B.FNO_PREACT_NONE, -3.0),
-            (P32, B.FNO_PREACT_TANH, 0.0)]             # the bound is ignored unless clipping
+            (P32, B.FNO_PREACT_TANH, 0.0),             # the bound is ignored unless clipping
+            (P16, SIG, 2.0), (P32, SIG, 1e30)]
     for prec, pa, clip in good:
         d = B.make_desc((16, 16), (4, 4), 2, 4, 4, prec, preact=pa, clip=clip)
         assert B.fno_spectral_conv_workspace_size(d, B.FNO_OP_FWD) > 0
+
+
+def test_sigma_clip_workspace_holds_the_bounds():
+    """The statistics-based clip adds 16 bytes (lo, hi in double) per (batch,
+    input channel) plane, rounded up to 256, to the workspaces of the calls
+    that apply it to x: the forward, the data gradient and the weight
+    gradient without caches (the combined backward through its data part)."""
+    for n, modes, bt, ci in [((32, 32), (4, 4), 3, 5), ((6, 10, 12), (2, 3, 4), 2, 37),
+                             ((96,), (17,), 40, 9)]:
+        for prec in (B.FNO_PREC_FP16_TANH, B.FNO_PREC_FP32):
+            t = B.make_desc(n, modes, bt, ci, 4, prec, preact=B.FNO_PREACT_TANH)
+            s = B.make_desc(n, modes, bt, ci, 4, prec, preact=B.FNO_PREACT_SIGMA_CLIP, clip=2.0)
+            extra = (bt * ci * 16 + 255) // 256 * 256
+            for op in (B.FNO_OP_FWD, B.FNO_OP_BWD_DATA, B.FNO_OP_BWD):
+                assert (B.fno_spectral_conv_workspace_size(s, op)
+                        == B.fno_spectral_conv_workspace_size(t, op) + extra), (n, prec, op)
+            assert (B.fno_spectral_conv_workspace_size(s, B.FNO_OP_BWD_WEIGHT)
+                    == B.fno_spectral_conv_workspace_size(t, B.FNO_OP_BWD_WEIGHT))
+            assert (B.fno_spectral_conv_workspace_size(s, B.FNO_OP_BWD_WEIGHT, caches=False)
+                    == B.fno_spectral_conv_workspace_size(t, B.FNO_OP_BWD_WEIGHT, caches=False)
+                    + extra)
 
 
 def test_preactivation_decides_whether_bwd_data_reads_x():
@@ -286,6 +311,7 @@ def test_preactivation_decides_whether_bwd_data_reads_x():
     w = B.weights_struct(dense=FAKE)
     for prec, pa, needs_x in [(B.FNO_PREC_FP32, B.FNO_PREACT_TANH, True),
                               (B.FNO_PREC_FP32, B.FNO_PREACT_HARD_CLIP, True),
+                              (B.FNO_PREC_FP16_TANH, B.FNO_PREACT_SIGMA_CLIP, True),
                               (B.FNO_PREC_FP16_TANH, B.FNO_PREACT_NONE, False),
                               (B.FNO_PREC_FP32, B.FNO_PREACT_DEFAULT, False)]:
         d = B.make_desc((32, 32), (4, 4), 2, 4, 4, prec, preact=pa, clip=1.0)

@@ -1,8 +1,10 @@
 """GPU parity of the pre-activation variants against the float64 oracle:
 tanh in fp32 storage (the full-precision + tanh ablation, App. B.8), fp16
-storage without pre-activation (the unstabilised baseline), and the hard clip
+storage without pre-activation (the unstabilised baseline), the hard clip
 of the pre-FFT comparison (App. B.6), also at the FP8-E5M2 bound 57344 (the
-clipping of Sec. 4.6).
+clipping of Sec. 4.6), and the statistics-based 2-sigma clip of App. B.6
+(each (batch, channel) plane clipped to its mean +- 2 population standard
+deviations, the bounds held constant in the gradient).
 
 Tolerances (relative L2): 1e-5 for fp32 storage, 3e-3 for fp16.  In the clip
 modes some inputs sit exactly on +-c, where the derivative counts the point as
@@ -21,7 +23,8 @@ import synth  # noqa: E402
 from tests import gpu_util as U  # noqa: E402
 from tests.test_gpu_parity import EDGE, SPECIAL_SHAPES  # noqa: E402
 
-MODES = ["fp32_tanh", "fp16", "fp16_clip:0.75", "fp32_clip:1.0"]
+MODES = ["fp32_tanh", "fp16", "fp16_clip:0.75", "fp32_clip:1.0", "fp16_sigma:2",
+         "fp32_sigma:2"]
 
 
 def _check(name, got, ref, prec):
@@ -64,7 +67,7 @@ def test_preact_edge_cases(case, prec):
     _check("gW", U.cplx(gw), rgw, prec)
 
 
-@pytest.mark.parametrize("prec", ["fp16_clip:0.7", "fp32_tanh"])
+@pytest.mark.parametrize("prec", ["fp16_clip:0.7", "fp32_tanh", "fp16_sigma:2"])
 def test_preact_workload_128(prec):
     """The 128^2 workload (B32 C64, 32x32 modes) at full size; 0.7 is not an
     fp16 value, so clipped inputs become fp16(0.7) on the GPU."""
@@ -119,3 +122,65 @@ def test_preact_nan(shape, prec):
     gx = U.host(layer.bwd_data(xd, wd, gyd))
     assert np.isnan(y[0]).any() and np.isfinite(y[1]).all()
     assert np.array_equal(np.isnan(gx), np.isnan(x))
+
+
+SIGMA_SHAPES = [((32, 32), (8, 8)), ((256, 256), (32, 32)), ((6, 10, 12), (2, 3, 4)),
+                ((96,), (17,))]
+
+
+@pytest.mark.parametrize("prec", ["fp16_sigma:2", "fp32_sigma:1.5"])
+@pytest.mark.parametrize("shape", range(len(SIGMA_SHAPES)))
+def test_sigma_clip_special_planes(shape, prec):
+    """Planes whose statistics are extreme: a constant plane (deviation 0:
+    every value sits on both bounds and passes with derivative 1), a plane
+    with a large offset (mean far from 0 against its spread) and one with a
+    few large outliers (clipped, derivative 0), beside ordinary planes; the
+    combined backward with and without the input-spectrum cache agrees with
+    the separate calls."""
+    n, modes = SIGMA_SHAPES[shape]
+    Bt, ci, co = 2, 4, 3
+    _, npdt, oprec = U.prec_codes(prec)
+    U.say(f"sigma clip special planes n={n} {prec}")
+    x, w, gy = synth.random_dense_case(83, Bt, ci, co, n, modes, npdt)
+    x[0, 1] = npdt(0.625)
+    x[1, 2] = (x[1, 2].astype(np.float64) * 2.0 + 300.0).astype(npdt)
+    flat = x[1, 3].reshape(-1)
+    flat[::37] = npdt(40.0)
+    layer = U.make_layer(n, modes, Bt, ci, co, prec)
+    y, gx, gw = U.run_all(layer, x, w, gy)
+    ry, rgx, rgw = _oracle(x, w, gy, n, modes, oprec)
+    _check("y", y, ry, prec)
+    _check("gx", gx, rgx, prec)
+    _check("gW", U.cplx(gw), rgw, prec)
+    fp = O.preactivation_grad(x, oprec)
+    assert np.all(fp[0, 1] == 1.0)
+    assert np.all(gx[fp == 0.0] == 0)
+    assert np.any(fp[1, 3] == 0.0)
+    xd, wd, gyd = U.dev(x), U.dev(w), U.dev(gy)
+    for cache in (True, False):
+        xh = layer.spectrum_buffer(0)
+        layer.fwd(xd, wd, x_hat=xh)
+        gxc, gwc = layer.bwd(xd, wd, gyd, x_hat=xh if cache else None)
+        assert np.array_equal(U.host(gxc), gx), cache
+        assert np.array_equal(U.host(gwc), gw), cache
+
+
+@pytest.mark.parametrize("shape", range(len(SIGMA_SHAPES)))
+def test_sigma_clip_nan_plane(shape):
+    """A NaN makes its plane's statistics NaN: that whole plane of f(x) and
+    f'(x) is NaN (its sample's output and exactly its plane of the data
+    gradient), every other plane stays finite."""
+    n, modes = SIGMA_SHAPES[shape]
+    Bt, ci, co = 2, 3, 3
+    prec = "fp16_sigma:2"
+    U.say(f"sigma clip nan n={n}")
+    x, w, gy = synth.random_dense_case(84, Bt, ci, co, n, modes, np.float16)
+    x[0, 1].reshape(-1)[5] = np.nan
+    layer = U.make_layer(n, modes, Bt, ci, co, prec)
+    xd, wd, gyd = U.dev(x), U.dev(w), U.dev(gy)
+    y = U.host(layer.fwd(xd, wd))
+    gx = U.host(layer.bwd_data(xd, wd, gyd))
+    assert np.isnan(y[0]).any() and np.isfinite(y[1]).all()
+    mask = np.zeros(x.shape, dtype=bool)
+    mask[0, 1] = True
+    assert np.array_equal(np.isnan(gx), mask)
