@@ -35,6 +35,9 @@ Mixed-Precision Neural Operators", ICLR 2024):
   order a greedy rule picks (Sec. 4.2: the next step is the one whose intermediate is
   smallest).
 * Gradients use the real-gradient convention g = dL/dRe + i dL/dIm.
+* The rest of the FNO block (Sec. 2): the pointwise channel-mixing skip with
+  bias, the activation (GELU) and an optional residual connection, applied
+  to the block input and the spectral output, with their gradients.
 
 Everything runs in float64/complex128 on the exact stored input values.
 
@@ -592,6 +595,109 @@ def cp_bwd_weight(x, gy, lam, u_in, u_out, u_mode, n, modes, precision):
         spec = ",".join([gw_l, r, "i" + r, "o" + r] + others)
         g_mode.append(np.einsum(f"{spec}->{sp[j]}{r}", gw, clam, cu_in, cu_out, *arrs, **opt))
     return g_lam, g_in, g_out, g_mode
+
+
+# ---------------------------------------------------------------------------
+# The rest of the FNO block (Sec. 2; Sec. 4.2 leaves these real-valued
+# operations to automatic mixed precision)
+# ---------------------------------------------------------------------------
+#
+# One FNO block maps v to act(W v + b + K v) (+ v with a residual connection):
+# K is the spectral convolution above, W v + b a pointwise linear map over the
+# channels (a 1x1 convolution with bias, the "skip" path), act a pointwise
+# nonlinearity.  The epilogue below is everything after K: it takes the
+# block input x and the spectral output y = K x.
+
+EPI_ACT_NONE = "none"
+EPI_ACT_GELU = "gelu"
+
+
+def gelu(z: np.ndarray) -> np.ndarray:
+    """GELU, the Gaussian error linear unit z Phi(z) with the exact normal
+    distribution function Phi(z) = (1 + erf(z / sqrt 2)) / 2."""
+    from scipy.special import erf
+    z = np.asarray(z, dtype=np.float64)
+    return 0.5 * z * (1.0 + erf(z / np.sqrt(2.0)))
+
+
+def gelu_grad(z: np.ndarray) -> np.ndarray:
+    """d/dz z Phi(z) = Phi(z) + z phi(z), phi the standard normal density."""
+    from scipy.special import erf
+    z = np.asarray(z, dtype=np.float64)
+    return 0.5 * (1.0 + erf(z / np.sqrt(2.0))) + z * np.exp(-0.5 * z * z) / np.sqrt(2.0 * np.pi)
+
+
+def _epi_act(z, act):
+    if act == EPI_ACT_GELU:
+        return gelu(z)
+    if act == EPI_ACT_NONE:
+        return np.asarray(z, dtype=np.float64)
+    raise ValueError(act)
+
+
+def _epi_act_grad(z, act):
+    if act == EPI_ACT_GELU:
+        return gelu_grad(z)
+    if act == EPI_ACT_NONE:
+        return np.ones(np.shape(z))
+    raise ValueError(act)
+
+
+def channel_mix(w: np.ndarray, v: np.ndarray) -> np.ndarray:
+    """(W v)[b, o, x] = sum_i W[o, i] v[b, i, x]: the 1x1 convolution."""
+    return np.einsum("oi,bi...->bo...", np.asarray(w, dtype=np.float64),
+                     np.asarray(v, dtype=np.float64))
+
+
+def block_epilogue_fwd(x, y, w_skip, bias, act: str, residual: bool):
+    """z = W_skip x + b + y (b broadcast over batch and space, absent when
+    None), out = act(z) (+ x when residual, which needs C_in = C_out).
+    Returns (out, z)."""
+    z = channel_mix(w_skip, x) + np.asarray(y, dtype=np.float64)
+    if bias is not None:
+        z = z + np.asarray(bias, dtype=np.float64).reshape((1, -1) + (1,) * (z.ndim - 2))
+    out = _epi_act(z, act)
+    if residual:
+        if np.shape(x) != np.shape(out):
+            raise ValueError("the residual connection needs C_in = C_out")
+        out = out + np.asarray(x, dtype=np.float64)
+    return out, z
+
+
+def block_epilogue_bwd(x, z, g_out, w_skip, act: str, residual: bool):
+    """Gradients of the epilogue given dL/d out (chain rule):
+    g_z = g_out act'(z) (also the gradient of y, so the spectral convolution's
+    backward takes it as its output gradient), the skip path's share of the
+    input gradient W_skip^T g_z (+ g_out when residual), and the parameter
+    gradients g_W[o, i] = sum_{b, x} g_z[b, o, x] x[b, i, x] and
+    g_b[o] = sum_{b, x} g_z[b, o, x].  Returns (g_z, g_x_skip, g_w, g_b)."""
+    g_out = np.asarray(g_out, dtype=np.float64)
+    g_z = g_out * _epi_act_grad(z, act)
+    g_x = np.einsum("oi,bo...->bi...", np.asarray(w_skip, dtype=np.float64), g_z)
+    if residual:
+        g_x = g_x + g_out
+    xf = np.asarray(x, dtype=np.float64)
+    g_w = np.einsum("bop,bip->oi", g_z.reshape(g_z.shape[:2] + (-1,)),
+                    xf.reshape(xf.shape[:2] + (-1,)))
+    g_b = g_z.sum(axis=(0,) + tuple(range(2, g_z.ndim)))
+    return g_z, g_x, g_w, g_b
+
+
+def block_fwd(x, w, w_skip, bias, n, modes, precision, act, residual):
+    """The whole block with a dense spectral weight w: act(W_skip x + b + K x)
+    (+ x).  Returns (out, z)."""
+    return block_epilogue_fwd(x, fwd(x, w, n, modes, precision), w_skip, bias, act, residual)
+
+
+def block_bwd(x, w, w_skip, bias, g_out, n, modes, precision, act, residual):
+    """Gradients of block_fwd: (g_x, g_w_spectral, g_w_skip, g_b).  The input
+    gradient adds the spectral path's data gradient (taken at g_z) to the
+    skip path's."""
+    _, z = block_fwd(x, w, w_skip, bias, n, modes, precision, act, residual)
+    g_z, g_x_skip, g_ws, g_b = block_epilogue_bwd(x, z, g_out, w_skip, act, residual)
+    g_x = bwd_data(x, w, g_z, n, modes, precision) + g_x_skip
+    g_w = bwd_weight(x, g_z, n, modes, precision)
+    return g_x, g_w, g_ws, g_b
 
 
 # ---------------------------------------------------------------------------

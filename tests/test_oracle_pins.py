@@ -456,7 +456,126 @@ def pin_sigma_fd_frozen():
     return err
 
 
+def pin_gelu_values():
+    """GELU against values fixed by the normal distribution: Phi(1) and
+    phi(1) from the standard normal table (so GELU(1) = Phi(1),
+    GELU(-1) = -(1 - Phi(1)), GELU'(1) = Phi(1) + phi(1)), GELU(0) = 0,
+    GELU'(0) = 1/2, z Phi(z) on a grid against scipy.stats.norm.cdf, and the
+    derivative against central differences of the function."""
+    from scipy.stats import norm
+    phi1, dens1 = 0.8413447460685429, 0.24197072451914337
+    errs = [abs(O.gelu(np.array([1.0]))[0] - phi1),
+            abs(O.gelu(np.array([-1.0]))[0] + (1.0 - phi1)),
+            abs(O.gelu(np.array([0.0]))[0]),
+            abs(O.gelu_grad(np.array([0.0]))[0] - 0.5),
+            abs(O.gelu_grad(np.array([1.0]))[0] - (phi1 + dens1))]
+    z = np.linspace(-7.0, 7.0, 141)
+    errs.append(float(np.abs(O.gelu(z) - z * norm.cdf(z)).max()))
+    h = 1e-5
+    fd = (O.gelu(z + h) - O.gelu(z - h)) / (2 * h)
+    errs.append(float(np.abs(fd - O.gelu_grad(z)).max()) * 1e-3)
+    return max(errs)
+
+
+def _torch_epilogue(x, y, w, b, act, residual):
+    """The epilogue and its gradients through torch's own 1x1 convolution,
+    GELU and autograd (CPU, float64)."""
+    import torch
+    import torch.nn.functional as F
+    d = x.ndim - 2
+    conv = {1: F.conv1d, 2: F.conv2d, 3: F.conv3d}[d]
+    xt = torch.tensor(x, dtype=torch.float64, requires_grad=True)
+    yt = torch.tensor(y, dtype=torch.float64, requires_grad=True)
+    wt = torch.tensor(w, dtype=torch.float64, requires_grad=True)
+    bt = torch.tensor(b, dtype=torch.float64, requires_grad=True)
+    z = conv(xt, wt.reshape(wt.shape + (1,) * d), bt) + yt
+    out = F.gelu(z, approximate="none") if act == O.EPI_ACT_GELU else z
+    if residual:
+        out = out + xt
+    g = torch.tensor(_rng(95).standard_normal(out.shape), dtype=torch.float64)
+    out.backward(g)
+    return (out.detach().numpy(), g.numpy(), yt.grad.numpy(), xt.grad.numpy(),
+            wt.grad.numpy(), bt.grad.numpy())
+
+
+def pin_epilogue_torch():
+    """The block epilogue (1x1 skip with bias, activation, residual) and its
+    gradients against torch's convolution, GELU and autograd in float64, in
+    1-D, 2-D and 3-D, with and without GELU and the residual, C_in != C_out
+    where there is no residual."""
+    err = 0.0
+    cases = [((7,), 3, 5, O.EPI_ACT_GELU, False), ((5, 6), 4, 4, O.EPI_ACT_GELU, True),
+             ((3, 4, 5), 2, 3, O.EPI_ACT_NONE, False), ((6, 5), 3, 3, O.EPI_ACT_NONE, True)]
+    for k, (sp, ci, co, act, res) in enumerate(cases):
+        rng = _rng(96 + k)
+        x = rng.standard_normal((2, ci) + sp)
+        y = rng.standard_normal((2, co) + sp)
+        w = rng.standard_normal((co, ci))
+        b = rng.standard_normal(co)
+        out_t, g, gy_t, gx_t, gw_t, gb_t = _torch_epilogue(x, y, w, b, act, res)
+        out, z = O.block_epilogue_fwd(x, y, w, b, act, res)
+        g_z, g_x, g_w, g_b = O.block_epilogue_bwd(x, z, g, w, act, res)
+        for a, t in [(out, out_t), (g_z, gy_t), (g_x, gx_t), (g_w, gw_t), (g_b, gb_t)]:
+            err = max(err, float(np.abs(a - t).max()) / max(1.0, float(np.abs(t).max())))
+    return err
+
+
+def pin_block_fd():
+    """Gradients of the whole block act(W_skip x + b + K x) + x (spectral
+    path in tanh mode) against central differences of its loss
+    sum(g_out * out), for entries of x, W_skip, b and the real and imaginary
+    parts of the spectral weight."""
+    rng = _rng(97)
+    n, modes = (8, 6), (2, 3)
+    kd = (4, 3)
+    c = 3
+    x = rng.standard_normal((2, c) + n)
+    w = _cplx(rng, (c, c) + kd, 0.4)
+    ws = rng.standard_normal((c, c)) * 0.5
+    b = rng.standard_normal(c) * 0.3
+    g = rng.standard_normal((2, c) + n)
+    args = (n, modes, F16T, O.EPI_ACT_GELU, True)
+
+    def loss(x_, w_, ws_, b_):
+        out, _ = O.block_fwd(x_, w_, ws_, b_, *args)
+        return float(np.sum(g * out))
+
+    gx, gw, gws, gb = O.block_bwd(x, w, ws, b, g, *args)
+    h = 1e-6
+    err = 0.0
+
+    def check(fd, an):
+        return abs(fd - an) / max(1.0, abs(an))
+
+    for idx in [(0, 0, 0, 0), (1, 2, 5, 3), (0, 1, 7, 5)]:
+        xp, xm = x.copy(), x.copy()
+        xp[idx] += h
+        xm[idx] -= h
+        err = max(err, check((loss(xp, w, ws, b) - loss(xm, w, ws, b)) / (2 * h), gx[idx]))
+    for idx in [(0, 1), (2, 0), (1, 1)]:
+        wp, wm = ws.copy(), ws.copy()
+        wp[idx] += h
+        wm[idx] -= h
+        err = max(err, check((loss(x, w, wp, b) - loss(x, w, wm, b)) / (2 * h), gws[idx]))
+    for o in range(c):
+        bp, bm = b.copy(), b.copy()
+        bp[o] += h
+        bm[o] -= h
+        err = max(err, check((loss(x, w, ws, bp) - loss(x, w, ws, bm)) / (2 * h), gb[o]))
+    for idx in [(0, 1, 1, 2), (2, 2, 3, 0)]:
+        for unit, part in [(1.0, np.real), (1j, np.imag)]:
+            wp, wm = w.copy(), w.copy()
+            wp[idx] += h * unit
+            wm[idx] -= h * unit
+            fd = (loss(x, wp, ws, b) - loss(x, wm, ws, b)) / (2 * h)
+            err = max(err, check(fd, part(gw[idx])))
+    return err
+
+
 ALL_PINS = {
+    "gelu_values": (pin_gelu_values, 1e-12),
+    "epilogue_torch": (pin_epilogue_torch, 1e-12),
+    "block_fd": (pin_block_fd, 1e-6),
     "sigma_closed_form": (pin_sigma_closed_form, 1e-12),
     "sigma_fd_frozen": (pin_sigma_fd_frozen, 1e-7),
     "rel_l2_hand": (pin_rel_l2_hand, 1e-15),
@@ -1002,7 +1121,53 @@ def _sigma_bounds_whole_tensor(x, k):
     return np.full(shape, mu - k * sd), np.full(shape, mu + k * sd)
 
 
+def _gelu_tanh_form(z):
+    z = np.asarray(z, dtype=np.float64)
+    return 0.5 * z * (1.0 + np.tanh(np.sqrt(2.0 / np.pi) * (z + 0.044715 * z ** 3)))
+
+
+def _epi_fwd_residual_inside(orig):
+    def f(x, y, w, b, act, residual):
+        if not residual:
+            return orig(x, y, w, b, act, residual)
+        yy = np.asarray(y, dtype=np.float64) + np.asarray(x, dtype=np.float64)
+        return orig(x, yy, w, b, act, False)
+    return f
+
+
+def _epi_bwd_variant(kind):
+    def make(orig):
+        def f(x, z, g_out, w, act, residual):
+            g_z, g_x, g_w, g_b = orig(x, z, g_out, w, act, residual)
+            if kind == "no_act_grad":
+                g_z2, g_x2, g_w2, g_b2 = orig(x, np.zeros_like(z), g_out, w, O.EPI_ACT_NONE,
+                                              residual)
+                return g_z2, g_x2, g_w2, g_b2
+            if kind == "no_residual" and residual:
+                g_x = g_x - np.asarray(g_out, dtype=np.float64)
+            if kind == "gw_transposed":
+                g_w = g_w.T
+            if kind == "gb_mean":
+                g_b = g_b / np.prod(np.shape(g_z)[2:])
+            return g_z, g_x, g_w, g_b
+        return f
+    return make
+
+
 MUTATIONS = {
+    "gelu_tanh_approximation": ("gelu", lambda orig: _gelu_tanh_form),
+    "gelu_grad_no_density": ("gelu_grad", lambda orig: (
+        lambda z: 0.5 * (1.0 + __import__("scipy.special").special.erf(
+            np.asarray(z, dtype=np.float64) / np.sqrt(2.0))))),
+    "epi_bias_dropped": ("block_epilogue_fwd", lambda orig: (
+        lambda x, y, w, b, act, res: orig(x, y, w, None, act, res))),
+    "epi_skip_transposed": ("channel_mix", lambda orig: (
+        lambda w, v: orig(np.asarray(w).T, v))),
+    "epi_residual_before_activation": ("block_epilogue_fwd", _epi_fwd_residual_inside),
+    "epi_gz_without_act_grad": ("block_epilogue_bwd", _epi_bwd_variant("no_act_grad")),
+    "epi_gx_without_residual": ("block_epilogue_bwd", _epi_bwd_variant("no_residual")),
+    "epi_gw_transposed": ("block_epilogue_bwd", _epi_bwd_variant("gw_transposed")),
+    "epi_gb_mean": ("block_epilogue_bwd", _epi_bwd_variant("gb_mean")),
     "sigma_sample_std": ("sigma_bounds", lambda orig: _sigma_bounds_sample_std),
     "sigma_whole_tensor": ("sigma_bounds", lambda orig: _sigma_bounds_whole_tensor),
     "sigma_one_sigma": ("sigma_bounds", lambda orig: (lambda x, k: orig(x, k / 2.0))),
