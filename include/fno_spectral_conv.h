@@ -283,6 +283,84 @@ fno_status fno_contraction_path(const fno_conv_desc *desc, fno_op op, int32_t *s
 fno_status fno_contraction_path_cost(const fno_conv_desc *desc, fno_op op,
                                      int64_t *macs, int64_t *peak_elems);
 
+/* ------------------------------------------------------------------------
+ * The rest of the FNO block (Sec. 2): one block maps v to
+ *
+ *     out = act( W_skip v + b + K v )  (+ v with a residual connection)
+ *
+ * with K the spectral convolution above, W_skip v + b a pointwise linear map
+ * over the channels (a 1x1 convolution with bias: the skip path) and act a
+ * pointwise nonlinearity.  Sec. 4.2 leaves these real-valued operations to
+ * automatic mixed precision; here they are one fused pass after K (and two
+ * around K's backward) instead of separate convolution, add, activation and
+ * residual kernels.  In fp16 mode the channel mix multiplies fp16 operands
+ * with fp32 accumulation (as mixed precision runs a 1x1 convolution); the
+ * sums, the activation and the residual stay in fp32 registers and the
+ * results are rounded once to fp16.
+ *
+ * Layouts: x [batch][c_in][points], y and out [batch][c_out][points] (points
+ * = the product of the spatial extents, the layout of the spectral
+ * convolution's tensors), w_skip [c_out][c_in], b [c_out], all of the
+ * precision's element type; the parameter gradients g_w_skip [c_out][c_in]
+ * and g_b [c_out] are fp32 and overwritten (not accumulated).
+ *
+ * One block's training step:
+ *   fno_spectral_conv_fwd(x -> y);  fno_block_epilogue_fwd(x, y -> out, z)
+ *   fno_block_epilogue_bwd_weight(x, z, g_out -> g_z, g_w_skip, g_b)
+ *   fno_spectral_conv_bwd(x, gy = g_z -> gx_spec, g_w)
+ *   fno_block_epilogue_bwd_data(g_z, w_skip, gx_spec, g_out -> gx)
+ * ------------------------------------------------------------------------ */
+typedef enum {
+  FNO_EPI_ACT_NONE = 0,
+  FNO_EPI_ACT_GELU = 1  /* z Phi(z), Phi the exact normal distribution function */
+} fno_epi_activation;
+
+typedef struct {
+  int32_t precision;   /* FNO_PREC_FP16_TANH: fp16 tensors; FNO_PREC_FP32: fp32 */
+  int64_t batch, c_in, c_out;
+  int64_t points;      /* grid points of one channel, >= 1 */
+  int32_t activation;  /* fno_epi_activation */
+  int32_t residual;    /* 1: add x after the activation (needs c_in == c_out) */
+} fno_block_desc;
+
+/* Workspace bytes of an epilogue call: FNO_OP_BWD_WEIGHT needs one (the
+ * partial sums of the parameter gradients, reduced in a fixed order so that
+ * results are bit-identical from run to run); FNO_OP_FWD and
+ * FNO_OP_BWD_DATA need none (0).  FNO_ERR_INVALID_ARGUMENT for a malformed
+ * descriptor (c_in, c_out up to 65536 with c_out (c_in + 1) <= 65535 x 256;
+ * batch x points x channels up to 2^38; a residual with c_in != c_out) or
+ * another op. */
+fno_status fno_block_epilogue_workspace_size(const fno_block_desc *desc, fno_op op,
+                                             size_t *bytes);
+
+/* Forward (Sec. 2, the FNO block after K): z = W_skip x + b + y and
+ * out = act(z) (+ x).  b may be null (no bias).  z_out, if not null,
+ * receives z (the backward's input when act is GELU; may be null for
+ * act NONE or for inference).  out must not alias x or y. */
+fno_status fno_block_epilogue_fwd(const fno_block_desc *desc, const void *x, const void *y,
+                                  const void *w_skip, const void *b, void *out, void *z_out,
+                                  hipStream_t stream);
+
+/* First backward step (chain rule through the epilogue): g_z = g_out act'(z),
+ * which is also dL/dy and so the spectral convolution's output gradient, and
+ * the parameter gradients g_w_skip[o][i] = sum over batch and points of
+ * g_z[o] x[i], g_b[o] = sum of g_z[o].  With act GELU, z (from the forward)
+ * and g_z are required; with act NONE g_z equals g_out, z and g_z may be null
+ * and nothing is written there.  g_b may be null (no bias).  The workspace
+ * is the size fno_block_epilogue_workspace_size gives for FNO_OP_BWD_WEIGHT. */
+fno_status fno_block_epilogue_bwd_weight(const fno_block_desc *desc, const void *x,
+                                         const void *z, const void *g_out, void *g_z,
+                                         float *g_w_skip, float *g_b, void *ws, size_t ws_len,
+                                         hipStream_t stream);
+
+/* Last backward step: gx = gx_spec + W_skip^T g_z (+ g_out with a residual),
+ * gx_spec the spectral convolution's input gradient (taken at g_z).  g_out
+ * is read only with a residual (may be null otherwise).  gx may be the same
+ * buffer as gx_spec (in place). */
+fno_status fno_block_epilogue_bwd_data(const fno_block_desc *desc, const void *g_z,
+                                       const void *w_skip, const void *gx_spec,
+                                       const void *g_out, void *gx, hipStream_t stream);
+
 /* Per-kernel timing with HIP events (a profiling aid, off by default).
  * While enabled, every kernel the library launches is bracketed by a pair of
  * HIP events recorded on the launch stream (events are created per launch, so

@@ -644,9 +644,12 @@ def _epi_act_grad(z, act):
 
 
 def channel_mix(w: np.ndarray, v: np.ndarray) -> np.ndarray:
-    """(W v)[b, o, x] = sum_i W[o, i] v[b, i, x]: the 1x1 convolution."""
-    return np.einsum("oi,bi...->bo...", np.asarray(w, dtype=np.float64),
-                     np.asarray(v, dtype=np.float64))
+    """(W v)[b, o, x] = sum_i W[o, i] v[b, i, x]: the 1x1 convolution (one
+    matrix product per batch item over the flattened grid)."""
+    w = np.asarray(w, dtype=np.float64)
+    v = np.asarray(v, dtype=np.float64)
+    out = np.matmul(w, v.reshape(v.shape[:2] + (-1,)))
+    return out.reshape((v.shape[0], w.shape[0]) + v.shape[2:])
 
 
 def block_epilogue_fwd(x, y, w_skip, bias, act: str, residual: bool):
@@ -673,12 +676,12 @@ def block_epilogue_bwd(x, z, g_out, w_skip, act: str, residual: bool):
     g_b[o] = sum_{b, x} g_z[b, o, x].  Returns (g_z, g_x_skip, g_w, g_b)."""
     g_out = np.asarray(g_out, dtype=np.float64)
     g_z = g_out * _epi_act_grad(z, act)
-    g_x = np.einsum("oi,bo...->bi...", np.asarray(w_skip, dtype=np.float64), g_z)
+    g_x = channel_mix(np.asarray(w_skip, dtype=np.float64).T, g_z)
     if residual:
         g_x = g_x + g_out
     xf = np.asarray(x, dtype=np.float64)
-    g_w = np.einsum("bop,bip->oi", g_z.reshape(g_z.shape[:2] + (-1,)),
-                    xf.reshape(xf.shape[:2] + (-1,)))
+    gz2 = g_z.reshape(g_z.shape[:2] + (-1,))
+    g_w = np.matmul(gz2, xf.reshape(xf.shape[:2] + (-1,)).transpose(0, 2, 1)).sum(axis=0)
     g_b = g_z.sum(axis=(0,) + tuple(range(2, g_z.ndim)))
     return g_z, g_x, g_w, g_b
 

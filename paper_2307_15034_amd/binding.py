@@ -68,6 +68,22 @@ class FnoConvDesc(ctypes.Structure):
     ]
 
 
+FNO_EPI_ACT_NONE = 0
+FNO_EPI_ACT_GELU = 1
+
+
+class FnoBlockDesc(ctypes.Structure):
+    _fields_ = [
+        ("precision", ctypes.c_int32),
+        ("batch", ctypes.c_int64),
+        ("c_in", ctypes.c_int64),
+        ("c_out", ctypes.c_int64),
+        ("points", ctypes.c_int64),
+        ("activation", ctypes.c_int32),
+        ("residual", ctypes.c_int32),
+    ]
+
+
 class FnoWeights(ctypes.Structure):
     _fields_ = [
         ("dense", ctypes.c_void_p),
@@ -99,6 +115,7 @@ def _load() -> ctypes.CDLL:
     P = ctypes.POINTER
     D = P(FnoConvDesc)
     vp, sz, i32, i64 = ctypes.c_void_p, ctypes.c_size_t, ctypes.c_int32, ctypes.c_int64
+    BD = P(FnoBlockDesc)
     sig = {
         "fno_status_string": (ctypes.c_char_p, [ctypes.c_int]),
         "fno_last_error": (ctypes.c_char_p, []),
@@ -118,6 +135,11 @@ def _load() -> ctypes.CDLL:
         "fno_spectral_conv_bwd": (ctypes.c_int,
                                   [D, vp, P(FnoWeights), vp, vp, vp, P(FnoWeightGrads), vp, vp,
                                    sz, vp]),
+        "fno_block_epilogue_workspace_size": (ctypes.c_int, [BD, ctypes.c_int, P(sz)]),
+        "fno_block_epilogue_fwd": (ctypes.c_int, [BD, vp, vp, vp, vp, vp, vp, vp]),
+        "fno_block_epilogue_bwd_weight": (ctypes.c_int,
+                                          [BD, vp, vp, vp, vp, vp, vp, vp, sz, vp]),
+        "fno_block_epilogue_bwd_data": (ctypes.c_int, [BD, vp, vp, vp, vp, vp, vp]),
         "fno_release_caches": (ctypes.c_int, []),
         "fno_profile_enable": (ctypes.c_int, [i32]),
         "fno_profile_reset": (ctypes.c_int, []),
@@ -141,6 +163,8 @@ EXPORTED = [
     "fno_spectral_conv_bwd_data", "fno_spectral_conv_bwd_weight", "fno_spectral_conv_bwd",
     "fno_release_caches",
     "fno_profile_enable", "fno_profile_reset", "fno_profile_read",
+    "fno_block_epilogue_workspace_size", "fno_block_epilogue_fwd",
+    "fno_block_epilogue_bwd_weight", "fno_block_epilogue_bwd_data",
 ]
 
 
@@ -289,6 +313,54 @@ def fno_spectral_conv_bwd(desc, x: int, w: FnoWeights, gy: int, x_hat: int, gx: 
                                     gy_hat_out or None, ws or None, ws_bytes, stream or None)
     if check:
         _check(st, "fno_spectral_conv_bwd")
+    return st
+
+
+def make_block_desc(batch: int, c_in: int, c_out: int, points: int,
+                    precision: int = FNO_PREC_FP16_TANH, activation: int = FNO_EPI_ACT_GELU,
+                    residual: bool = False) -> FnoBlockDesc:
+    d = FnoBlockDesc()
+    d.precision = precision
+    d.batch, d.c_in, d.c_out, d.points = batch, c_in, c_out, points
+    d.activation = activation
+    d.residual = 1 if residual else 0
+    return d
+
+
+def fno_block_epilogue_workspace_size(desc: FnoBlockDesc, op: int) -> int:
+    b = ctypes.c_size_t()
+    _check(_lib.fno_block_epilogue_workspace_size(ctypes.byref(desc), op, ctypes.byref(b)),
+           "fno_block_epilogue_workspace_size")
+    return b.value
+
+
+def fno_block_epilogue_fwd(desc, x: int, y: int, w_skip: int, b: int, out: int, z_out: int,
+                           stream: int, check: bool = True) -> int:
+    st = _lib.fno_block_epilogue_fwd(ctypes.byref(desc), x or None, y or None, w_skip or None,
+                                     b or None, out or None, z_out or None, stream or None)
+    if check:
+        _check(st, "fno_block_epilogue_fwd")
+    return st
+
+
+def fno_block_epilogue_bwd_weight(desc, x: int, z: int, g_out: int, g_z: int, g_w_skip: int,
+                                  g_b: int, ws: int, ws_bytes: int, stream: int,
+                                  check: bool = True) -> int:
+    st = _lib.fno_block_epilogue_bwd_weight(ctypes.byref(desc), x or None, z or None,
+                                            g_out or None, g_z or None, g_w_skip or None,
+                                            g_b or None, ws or None, ws_bytes, stream or None)
+    if check:
+        _check(st, "fno_block_epilogue_bwd_weight")
+    return st
+
+
+def fno_block_epilogue_bwd_data(desc, g_z: int, w_skip: int, gx_spec: int, g_out: int, gx: int,
+                                stream: int, check: bool = True) -> int:
+    st = _lib.fno_block_epilogue_bwd_data(ctypes.byref(desc), g_z or None, w_skip or None,
+                                          gx_spec or None, g_out or None, gx or None,
+                                          stream or None)
+    if check:
+        _check(st, "fno_block_epilogue_bwd_data")
     return st
 
 

@@ -19,7 +19,7 @@ ROOT = os.path.dirname(HERE)
 LIB = os.path.join(HERE, "libfno_spectral_conv.so")
 OBJ = os.path.join(HERE, "_build")
 SOURCES = ["fno_kernels.hip", "fno_fast.hip", "fno_chain.hip", "fno_slab.hip", "fno_gemm.hip",
-           "fno_wide.hip", "fno_wide2.hip", "fno_noalloc.hip", "fno_plan.cpp"]
+           "fno_wide.hip", "fno_wide2.hip", "fno_noalloc.hip", "fno_block.hip", "fno_plan.cpp"]
 ARCH = "gfx950"
 
 

@@ -1678,6 +1678,12 @@ fno_status check_ws(const fno_conv_desc* d, fno_op op, bool caches, const void* 
 using namespace fno;
 
 namespace fno {
+fno_status report_hip_error(hipError_t e, const char* what) { return hip_fail(e, what); }
+
+hipError_t timed_launch(const char* name, hipStream_t s, hipError_t (*launch)(void*), void* ctx) {
+  return timed(name, s, [&] { return launch(ctx); });
+}
+
 // The forward call.  build_plan = false: the plan must already exist (no
 // device allocation, no blocking upload; the allocation-free entry point).
 fno_status fwd_impl(const fno_conv_desc* d, const void* x, const fno_weights* w, void* y,

@@ -225,3 +225,89 @@ class SpectralConv:
                                 self._x(gx, "gx", self.c_in), self.grads_struct(gw),
                                 self._spec(gy_hat, "gy_hat", 1), _addr(ws), ws.numel(), s)
         return gx, gw
+
+
+class BlockEpilogue:
+    """The rest of one FNO block after the spectral convolution K (the
+    fno_block_epilogue_* calls): out = act(W_skip x + b + y) (+ x).
+
+    x [batch, c_in, *grid], y and out [batch, c_out, *grid] in the
+    precision's dtype (float16 in fp16 mode, float32 in fp32 mode); w_skip
+    [c_out, c_in] and b [c_out] in the same dtype; the parameter gradients are
+    float32.  `grid` is the spatial shape (its product is the descriptor's
+    points).
+    """
+
+    def __init__(self, grid: Sequence[int], batch: int, c_in: int, c_out: int,
+                 precision: int = B.FNO_PREC_FP16_TANH, activation: int = B.FNO_EPI_ACT_GELU,
+                 residual: bool = False, device: str = "cuda"):
+        self.grid = tuple(int(v) for v in grid)
+        points = 1
+        for v in self.grid:
+            points *= v
+        self.batch, self.c_in, self.c_out = batch, c_in, c_out
+        self.activation, self.residual = activation, residual
+        self.desc = B.make_block_desc(batch, c_in, c_out, points, precision, activation,
+                                      residual)
+        self.dtype = torch.float16 if precision == B.FNO_PREC_FP16_TANH else torch.float32
+        self.device = torch.device(device)
+        # descriptor checks run in the library
+        self.ws_bytes = B.fno_block_epilogue_workspace_size(self.desc, B.FNO_OP_BWD_WEIGHT)
+
+    def _t(self, t, c, name, optional=False):
+        if t is None and optional:
+            return 0
+        if t is None:
+            raise ValueError(f"{name} is required")
+        return _addr(t, (self.batch, c) + self.grid, self.dtype, name, self.device)
+
+    def _new(self, c):
+        return torch.empty((self.batch, c) + self.grid, dtype=self.dtype, device=self.device)
+
+    def fwd(self, x, y, w_skip, b=None, out=None, z_out=None, keep_z: bool = True,
+            stream: Optional[int] = None):
+        """Returns (out, z); z is None unless kept (needed by the backward
+        with GELU)."""
+        ax, ay = self._t(x, self.c_in, "x"), self._t(y, self.c_out, "y")
+        aw = _addr(w_skip, (self.c_out, self.c_in), self.dtype, "w_skip", self.device)
+        ab = _addr(b, (self.c_out,), self.dtype, "b", self.device)
+        out = self._new(self.c_out) if out is None else out
+        if z_out is None and keep_z and self.activation != B.FNO_EPI_ACT_NONE:
+            z_out = self._new(self.c_out)
+        ao = self._t(out, self.c_out, "out")
+        az = self._t(z_out, self.c_out, "z_out", optional=True)
+        s = torch.cuda.current_stream().cuda_stream if stream is None else stream
+        B.fno_block_epilogue_fwd(self.desc, ax, ay, aw, ab, ao, az, s)
+        return out, z_out
+
+    def bwd_weight(self, x, z, g_out, g_z=None, bias: bool = True,
+                   stream: Optional[int] = None):
+        """Returns (g_z, g_w_skip, g_b); with activation NONE g_z is g_out
+        itself."""
+        gelu = self.activation != B.FNO_EPI_ACT_NONE
+        ax, ago = self._t(x, self.c_in, "x"), self._t(g_out, self.c_out, "g_out")
+        az = self._t(z, self.c_out, "z", optional=not gelu)
+        if gelu and g_z is None:
+            g_z = self._new(self.c_out)
+        agz = self._t(g_z, self.c_out, "g_z", optional=not gelu) if gelu else 0
+        gw = torch.empty((self.c_out, self.c_in), dtype=torch.float32, device=self.device)
+        gb = torch.empty((self.c_out,), dtype=torch.float32, device=self.device) if bias else None
+        ws = torch.empty(max(self.ws_bytes, 1), dtype=torch.uint8, device=self.device)
+        s = torch.cuda.current_stream().cuda_stream if stream is None else stream
+        B.fno_block_epilogue_bwd_weight(self.desc, ax, az if gelu else 0, ago, agz,
+                                        gw.data_ptr(), gb.data_ptr() if bias else 0,
+                                        ws.data_ptr(), self.ws_bytes, s)
+        return (g_z if gelu else g_out), gw, gb
+
+    def bwd_data(self, g_z, w_skip, gx_spec, g_out=None, gx=None,
+                 stream: Optional[int] = None):
+        """gx = gx_spec + W_skip^T g_z (+ g_out); gx may be gx_spec (in place)."""
+        agz = self._t(g_z, self.c_out, "g_z")
+        aw = _addr(w_skip, (self.c_out, self.c_in), self.dtype, "w_skip", self.device)
+        ags = self._t(gx_spec, self.c_in, "gx_spec")
+        ago = self._t(g_out, self.c_out, "g_out", optional=not self.residual)
+        gx = self._new(self.c_in) if gx is None else gx
+        agx = self._t(gx, self.c_in, "gx")
+        s = torch.cuda.current_stream().cuda_stream if stream is None else stream
+        B.fno_block_epilogue_bwd_data(self.desc, agz, aw, ags, ago, agx, s)
+        return gx

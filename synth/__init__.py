@@ -50,6 +50,7 @@ import numpy as np
 import scipy.fft
 
 STREAM_X, STREAM_W, STREAM_GY, STREAM_M = 0, 1, 2, 3
+STREAM_SKIP = 4  # the block's skip weight and bias
 
 GRF_SHIFT = 49.0
 GRF_POWER = 2.5
@@ -222,6 +223,30 @@ def make_weight(wl: Workload, dtype=np.float16):
     if wl.weight == "cp":
         return make_cp_weight(wl, dtype)
     return make_dense_weight(wl, dtype)
+
+
+def make_block_params(wl: Workload, dtype=np.float16):
+    """Skip weight w_skip[Cout, Cin] ~ N(0, 1/Cin) and bias b[Cout] ~ N(0, 0.1^2)
+    of one FNO block, in the storage dtype."""
+    rng = rng_for(wl.wid, STREAM_SKIP)
+    w = _round(rng.standard_normal((wl.c_out, wl.c_in)) / np.sqrt(wl.c_in), dtype)
+    b = _round(rng.standard_normal(wl.c_out) * 0.1, dtype)
+    return w, b
+
+
+def random_block_case(seed: int, batch: int, c_in: int, c_out: int, grid: Sequence[int],
+                      dtype=np.float16):
+    """Small iid-normal case for the block epilogue: x[B, Cin, *grid],
+    y[B, Cout, *grid] (standing in for the spectral output), w_skip[Cout, Cin]
+    ~ N(0, 1/Cin), b[Cout] ~ N(0, 0.1^2) and g_out[B, Cout, *grid]."""
+    rng = np.random.default_rng(np.random.SeedSequence([2000 + int(seed)]))
+    grid = tuple(grid)
+    x = _round(rng.standard_normal((batch, c_in) + grid), dtype)
+    y = _round(rng.standard_normal((batch, c_out) + grid), dtype)
+    w = _round(rng.standard_normal((c_out, c_in)) / np.sqrt(c_in), dtype)
+    b = _round(rng.standard_normal(c_out) * 0.1, dtype)
+    g = _round(rng.standard_normal((batch, c_out) + grid), dtype)
+    return x, y, w, b, g
 
 
 def pairs_to_complex(a: np.ndarray) -> np.ndarray:

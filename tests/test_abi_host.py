@@ -482,3 +482,59 @@ def test_layer_rejects_host_tensors_and_short_spectra():
         layer.fwd(x.transpose(2, 3), w)
     with pytest.raises(ValueError, match="bytes"):
         layer.fwd(x, w, x_hat=torch.zeros(16, dtype=torch.uint8))
+
+
+def test_block_epilogue_descriptor_checks():
+    """The block epilogue's descriptor: sizes, enums, the residual's channel
+    condition and the parameter-gradient limit are checked on the host."""
+    ok = B.make_block_desc(2, 4, 4, 64, B.FNO_PREC_FP16_TANH, B.FNO_EPI_ACT_GELU, True)
+    assert B.fno_block_epilogue_workspace_size(ok, B.FNO_OP_FWD) == 0
+    assert B.fno_block_epilogue_workspace_size(ok, B.FNO_OP_BWD_DATA) == 0
+    assert B.fno_block_epilogue_workspace_size(ok, B.FNO_OP_BWD_WEIGHT) > 0
+    bad = [dict(residual=True, c_out=5), dict(activation=2), dict(precision=3), dict(batch=0),
+           dict(points=0), dict(c_in=0), dict(c_out=70000), dict(c_in=65536, c_out=300)]
+    for kw in bad:
+        args = dict(batch=2, c_in=4, c_out=4, points=64, precision=B.FNO_PREC_FP16_TANH,
+                    activation=B.FNO_EPI_ACT_GELU, residual=False)
+        args.update(kw)
+        d = B.make_block_desc(**args)
+        with pytest.raises(B.FnoError) as e:
+            B.fno_block_epilogue_workspace_size(d, B.FNO_OP_BWD_WEIGHT)
+        assert e.value.status == B.FNO_ERR_INVALID_ARGUMENT, kw
+    with pytest.raises(B.FnoError):
+        B.fno_block_epilogue_workspace_size(ok, B.FNO_OP_BWD)
+
+
+def test_block_epilogue_workspace_is_the_partial_sums():
+    """One fp32 partial sum of (c_out x c_in + c_out) values per work-group of
+    the parameter-gradient kernel, at most 512 of them, rounded to 256
+    bytes."""
+    # 512-point tiles per work-group round (four waves of 128 points) on the
+    # matrix-core path, 4096-point slices on the generic one (255 points)
+    for bt, ci, co, pts, expect_g in [(8, 64, 64, 1 << 20, 512), (1, 16, 16, 256, 1),
+                                      (2, 5, 7, 480, 2), (3, 16, 16, 1536, 9),
+                                      (40, 6, 6, 255, 3)]:
+        d = B.make_block_desc(bt, ci, co, pts)
+        e = co * ci + co
+        got = B.fno_block_epilogue_workspace_size(d, B.FNO_OP_BWD_WEIGHT)
+        assert got == (expect_g * e * 4 + 255) // 256 * 256, (bt, ci, co, pts)
+
+
+def test_block_epilogue_rejects_bad_pointers_on_the_host():
+    """Misaligned or missing pointers are refused before anything is
+    enqueued (no GPU needed)."""
+    d = B.make_block_desc(2, 4, 4, 64, B.FNO_PREC_FP16_TANH, B.FNO_EPI_ACT_GELU, False)
+    st = B.fno_block_epilogue_fwd(d, FAKE, FAKE + 2, FAKE, 0, FAKE + 256, 0, 0, check=False)
+    assert st == B.FNO_ERR_INVALID_ARGUMENT
+    st = B.fno_block_epilogue_fwd(d, FAKE, FAKE + 512, FAKE, 0, FAKE, 0, 0, check=False)
+    assert st == B.FNO_ERR_INVALID_ARGUMENT          # out aliases x
+    st = B.fno_block_epilogue_bwd_weight(d, FAKE, 0, FAKE, FAKE + 256, FAKE + 512, 0, FAKE,
+                                         1 << 20, 0, check=False)
+    assert st == B.FNO_ERR_INVALID_ARGUMENT          # GELU needs z
+    st = B.fno_block_epilogue_bwd_weight(d, FAKE, FAKE + 768, FAKE + 256, FAKE + 1024,
+                                         FAKE + 512, 0, FAKE + 4096, 16, 0, check=False)
+    assert st == B.FNO_ERR_WORKSPACE_TOO_SMALL
+    r = B.make_block_desc(2, 4, 4, 64, B.FNO_PREC_FP32, B.FNO_EPI_ACT_NONE, True)
+    st = B.fno_block_epilogue_bwd_data(r, FAKE, FAKE + 256, FAKE + 512, 0, FAKE + 768, 0,
+                                       check=False)
+    assert st == B.FNO_ERR_INVALID_ARGUMENT          # the residual needs g_out
