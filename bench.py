@@ -55,6 +55,9 @@ def parse():
     p.add_argument("--separate-bwd", action="store_true",
                    help="bwd_data and bwd_weight as two calls instead of the combined one")
     p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--block", action="store_true",
+                   help="time the whole FNO block (spectral layer + skip/GELU/residual "
+                        "epilogue, forward and backward) instead of the layer alone")
     p.add_argument("--cpu-seconds", type=float, default=12.0)
     p.add_argument("--profile-steps", type=int, default=20)
     p.add_argument("--summarize", metavar="DIR",
@@ -100,6 +103,21 @@ def kernel_bytes(wl, es, preact="tanh"):
         out["r2c_plane"] += out["r2c_plane_tanh"]
         out["c2r_plane"] += spec_in + B * Ci * N * es
     return out
+
+
+def block_kernel_bytes(wl, es, residual=True):
+    """Algorithmic bytes of the block epilogue's launches: the forward reads x
+    and y and writes out and z; the parameter-gradient pass reads x, z and
+    g_out and writes g_z (plus W_skip / b and the fp32 parameter gradients);
+    the data-gradient pass reads g_z and gx_spec (and g_out with the
+    residual) and writes gx."""
+    B, Ci, Co = wl.batch, wl.c_in, wl.c_out
+    N = int(np.prod(wl.n))
+    S_in, S_out = B * Ci * N * es, B * Co * N * es
+    P = Co * Ci * es + Co * es
+    return {"block_epilogue_fwd": S_in + 3 * S_out + P,
+            "block_epilogue_bwd_weight": S_in + 3 * S_out + (Co * Ci + Co) * 4,
+            "block_epilogue_bwd_data": 2 * S_in + S_out + (S_out if residual else 0) + P}
 
 
 def step_bytes(wl, es, caches=True, preact="tanh"):
@@ -241,6 +259,9 @@ def copy_bandwidth(torch, nbytes=1 << 30, reps=10):
 # (first match wins; the template flag "true" marks the pre-activation
 # variant of a transform)
 KERNEL_NAMES = [
+    (r"epi_mix_kernel<[^>]*true>", "block_epilogue_fwd"),
+    (r"epi_mix_kernel<", "block_epilogue_bwd_data"),
+    (r"epi_wgrad_kernel<", "block_epilogue_bwd_weight"),
     (r"r2c_\w+<[^>]*true>", "r2c_plane_tanh"),
     (r"r2c_\w+<", "r2c_plane"),
     (r"slab_adj_wgrad_kernel", "contract_adjoint_wgrad"),
@@ -310,6 +331,8 @@ def summarize(args):
             (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3)
     es = 2 if args.precision == "fp16_tanh" else 4
     kb = kernel_bytes(wl, es)
+    if args.block:
+        kb.update(block_kernel_bytes(wl, es, wl.c_in == wl.c_out))
     tr = {"workload": wl.name, "src_hash": kernel_sources_hash(),
           "calibration": {"fetch": f_cal, "write": w_cal}, "kernels": {}}
     rows = []
@@ -333,12 +356,15 @@ def summarize(args):
                     f"{kb[name] / avg / 1e3 / HBM_PEAK_GBS:.3f} | {fb / 1e6:.1f} | "
                     f"{wb / 1e6:.1f} | {(fb + wb) / kb[name]:.2f} |")
     os.makedirs(os.path.join(ROOT, "profiles"), exist_ok=True)
+    tag = "block_" if args.block else ""
     if have_pmc:
-        with open(os.path.join(ROOT, "profiles", f"traffic_{wl.name}.json"), "w") as f:
+        with open(os.path.join(ROOT, "profiles", f"traffic_{tag}{wl.name}.json"), "w") as f:
             json.dump(tr, f, indent=1)
     cmd = ("cd /tmp && export TMPDIR=/tmp && rocprofv3 {what} --output-format csv "
            "-d <out>/{sub} -o run -- python3 /root/repo/bench.py {extra}")
     wk = f"--workload {args.workload} " if args.workload != 3 else ""
+    if args.block:
+        wk += "--block "
     if wl.weight != "dense":
         wk += f"--policy {args.policy} "
     cmds = [
@@ -356,8 +382,10 @@ def summarize(args):
         cmds = [cmds[0], cmds[-1]]
     total_avg = sum(sum(ds) / len(ds) for k, ds in dur.items() if _logical(k) in kb)
     pol = f", {args.policy} path" if wl.weight != "dense" else ""
+    title = ("FNO block step kernels (spectral layer + skip/GELU/residual epilogue)"
+             if args.block else "Layer step kernels")
     lines = [
-        f"# Layer step kernels, workload {wl.name} (fp16+tanh, {wl.weight}{pol}, spectral "
+        f"# {title}, workload {wl.name} (fp16+tanh, {wl.weight}{pol}, spectral "
         "caches, combined backward)", "",
         "MI355X, one GPU. Durations from the rocprofv3 kernel trace of the timed benchmark",
         "(kernel begin/end timestamps, all dispatches of the run)" + (
@@ -388,7 +416,8 @@ def summarize(args):
                      f"{float(r['MinNs']):.0f} | {float(r['MaxNs']):.0f} | "
                      f"{float(r['Percentage']):.2f} |")
     suffix = f"_{args.policy}" if wl.weight != "dense" else ""
-    with open(os.path.join(ROOT, "profiles", f"layer_step_{wl.name}{suffix}.md"), "w") as f:
+    stem = "block_step" if args.block else "layer_step"
+    with open(os.path.join(ROOT, "profiles", f"{stem}_{wl.name}{suffix}.md"), "w") as f:
         f.write("\n".join(lines) + "\n")
     print(json.dumps(tr))
 
@@ -520,6 +549,17 @@ def main():
     wd = ({"core": dev(w["core"]), "u_in": dev(w["u_in"]), "u_out": dev(w["u_out"]),
            "u_mode": [dev(u) for u in w["u_mode"]]} if isinstance(w, dict) else dev(w))
     caches = not args.no_caches
+    if args.block:
+        from paper_2307_15034_amd.layer import BlockEpilogue
+        if caches is False or args.separate_bwd:
+            raise SystemExit("--block times the combined backward with the spectral cache")
+        epi = BlockEpilogue(wl.n, wl.batch, wl.c_in, wl.c_out, pc, B.FNO_EPI_ACT_GELU,
+                            residual=wl.c_in == wl.c_out)
+        wsk, bsk = synth.make_block_params(wl, npdt)
+        wskd, bskd = dev(wsk), dev(bsk)
+        bout = torch.empty((wl.batch, wl.c_out) + wl.n, dtype=layer.dtype, device="cuda")
+        bz = torch.empty_like(bout)
+        bgz = torch.empty_like(bout)
     xh = layer.spectrum_buffer(0) if caches else None
     gh = layer.spectrum_buffer(1) if caches else None
     y = torch.empty((wl.batch, wl.c_out) + wl.n, dtype=layer.dtype, device="cuda")
@@ -532,8 +572,21 @@ def main():
     layer.workspace(B.FNO_OP_BWD_WEIGHT, caches)
     layer.workspace(B.FNO_OP_BWD, caches)
 
+    def block_step(s):
+        # y = K x; out = GELU(W_skip x + b + y) + x; then the backward with
+        # g_out = gy: g_z and the skip gradients, K's backward at g_z, and
+        # gx = gx_spec + W_skip^T g_z + g_out (in place)
+        layer.fwd(xd, wd, y=y, x_hat=xh, stream=s)
+        epi.fwd(xd, y, wskd, bskd, out=bout, z_out=bz, stream=s)
+        gzz, _, _ = epi.bwd_weight(xd, bz, gyd, g_z=bgz, stream=s)
+        layer.bwd(xd, wd, gzz, x_hat=xh, gx=gx, gw=gw, stream=s)
+        epi.bwd_data(gzz, wskd, gx, gyd if epi.residual else None, gx=gx, stream=s)
+
     def step(s=None):
         s = sh if s is None else s
+        if args.block:
+            block_step(s)
+            return
         layer.fwd(xd, wd, y=y, x_hat=xh, stream=s)
         if not args.separate_bwd:
             # data and weight gradient in one call (the layer's backward)
@@ -577,6 +630,8 @@ def main():
     ms_step = ev0.elapsed_time(ev1) / args.steps
     value = wl.batch / (ms_step / 1e3)
     sbytes = step_bytes(wl, es, caches, preact)
+    if args.block:
+        sbytes += sum(block_kernel_bytes(wl, es, epi.residual).values())
 
     # per-kernel durations: the library brackets each launch with HIP events
     B.fno_profile_reset()
@@ -588,6 +643,8 @@ def main():
     B.fno_profile_enable(False)
     B.fno_profile_reset()
     kb = kernel_bytes(wl, es, preact)
+    if args.block:
+        kb.update(block_kernel_bytes(wl, es, epi.residual))
     kernels = {}
     for name, (n, tot) in prof.items():
         avg = tot / max(n, 1)
@@ -627,6 +684,9 @@ def main():
                    "backward": "separate" if args.separate_bwd else "combined",
                    "launch": "stream" if args.no_graph else "hip_graph",
                    "path_policy": args.policy if wl.weight != "dense" else None},
+        **({"block": {"activation": "gelu", "residual": bool(epi.residual), "bias": True,
+                      "note": "whole FNO block: spectral layer + fused skip/GELU/residual "
+                              "epilogue, forward and backward"}} if args.block else {}),
         "step_alg_bytes": sbytes,
         "step_hbm_gbs": round(sbytes / (ms_step / 1e3) / 1e9, 1),
         "step_hbm_frac": round(sbytes / (ms_step / 1e3) / 1e9 / HBM_PEAK_GBS, 4),
@@ -636,7 +696,9 @@ def main():
                         for kk, vv in v.items()} for k, v in kernels.items()},
         "wall_s_timed": round(wall, 3),
     }
-    if not args.no_cpu_baseline:
+    if args.block:
+        out["metric"] = "FNO block fwd+bwd samples/s (fp16+tanh spectral layer, GELU, residual)"
+    if not args.no_cpu_baseline and not args.block:
         out["cpu_baseline"] = cpu_baseline(wl, x, w, gy, omode, args.cpu_seconds)
     print(json.dumps(out), flush=True)
 

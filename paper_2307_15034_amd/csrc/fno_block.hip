@@ -29,7 +29,7 @@ namespace {
 
 constexpr int kMixP = 128;          // grid points per tile of the channel mix
 constexpr int kWaveP = 128;         // grid points per wave and tile of the weight gradient
-constexpr int kMaxPartials = 512;   // work-groups (partial sums) of the weight gradient
+constexpr int kMaxPartials = 1024;  // work-groups (partial sums) of the weight gradient
 constexpr int64_t kPartialBytesCap = (int64_t)256 << 20;
 
 inline int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
@@ -78,7 +78,9 @@ size_t mix_lds_bytes(int ntt, int Kp) {
   return (size_t)(ntt * 16 + kMixP) * (Kp + kpl) * sizeof(T);
 }
 
-template <typename T, int NT>
+// FWD: the forward (activation, z, bias, residual; add2 unused); otherwise
+// the data gradient (W transposed, two addends, nothing else).
+template <typename T, int NT, bool FWD>
 __global__ __launch_bounds__(256) void epi_mix_kernel(EpiMixArgs a) {
   using M = MM<T>;
   using frag = typename M::frag;
@@ -93,17 +95,20 @@ __global__ __launch_bounds__(256) void epi_mix_kernel(EpiMixArgs a) {
   const T* in = reinterpret_cast<const T*>(a.in);
   const T* w = reinterpret_cast<const T*>(a.w);
   const T* add1 = reinterpret_cast<const T*>(a.add1);
-  const T* add2 = reinterpret_cast<const T*>(a.add2);
-  const T* bias = reinterpret_cast<const T*>(a.bias);
+  const T* add2 = FWD ? nullptr : reinterpret_cast<const T*>(a.add2);
+  const T* bias = FWD ? reinterpret_cast<const T*>(a.bias) : nullptr;
   T* out = reinterpret_cast<T*>(a.out);
-  T* zout = reinterpret_cast<T*>(a.zout);
+  T* zout = FWD ? reinterpret_cast<T*>(a.zout) : nullptr;
+  const bool gelu = FWD && a.act == FNO_EPI_ACT_GELU;
+  const bool resid = FWD && a.residual;
+  const int wt = FWD ? 0 : 1;
 
   // W once per work-group, zero beyond N rows and K columns; the input tile's
   // padding columns (k >= K) are zeroed once and never written again
   for (int e = tid; e < a.ntt * 16 * ld; e += 256) {
     const int n = e / ld, k = e - (e / ld) * ld;
     T v = (T)0.0f;
-    if (n < a.N && k < a.K) v = a.wt ? w[(int64_t)k * a.N + n] : w[(int64_t)n * a.K + k];
+    if (n < a.N && k < a.K) v = wt ? w[(int64_t)k * a.N + n] : w[(int64_t)n * a.K + k];
     WS[e] = v;
   }
   for (int e = tid; e < kMixP * ld; e += 256) XT[e] = (T)0.0f;
@@ -174,14 +179,199 @@ __global__ __launch_bounds__(256) void epi_mix_kernel(EpiMixArgs a) {
           for (int i = 0; i < 4; ++i) {
             const float z = acc[mt][j][i];
             zv[i] = (T)z;
-            float o = a.act == FNO_EPI_ACT_GELU ? gelu_f(z) : z;
-            if (a.residual) o += (float)XT[(prow + i) * ld + n];
+            float o = gelu ? gelu_f(z) : z;
+            if (resid) o += (float)XT[(prow + i) * ld + n];
             ov[i] = (T)o;
           }
           if (zout) *reinterpret_cast<V4*>(zout + off) = zv;
           *reinterpret_cast<V4*>(out + off) = ov;
         }
     }
+  }
+}
+
+// Software-pipelined fp16 channel mix for the common shapes (at most NT*16
+// output channels, at most 128 input channels), 64-point tiles.  Every
+// global access is a 16-byte vector of a channel row, eight lanes covering
+// a row's 128 bytes: the input rows are transposed into LDS (channel pairs
+// (k, k+1) travel together so that the transposing writes are 32-bit, and
+// the 16-byte column blocks of a transposed row are XOR-swizzled by the
+// row's 8-row group, when the number of blocks is a power of two, to spread
+// those writes over the banks); the addends and the results pass through
+// row-major LDS tiles between the row-wise global accesses and the
+// matrix-core layout.  The next tile's loads are in flight while the
+// current tile is multiplied and stored.
+constexpr int kPipeP = 64;  // grid points per tile of the pipelined channel mix
+
+template <int NT>
+size_t pipe_lds_bytes(int Kp) {
+  const int ld = Kp + 8, lda = kPipeP + 8;
+  return (size_t)((NT * 16 + kPipeP) * ld + 2 * NT * 16 * lda) * 2;
+}
+
+template <int NT, bool FWD>
+__global__ __launch_bounds__(256) void epi_mix_pipe_kernel(EpiMixArgs a) {
+  using T = _Float16;
+  using M = MM<T>;
+  using frag = typename M::frag;
+  constexpr int KPL = 8, KS = 32;
+  constexpr int VPR = kPipeP / 8;            // 16-byte vectors per channel row of a tile
+  constexpr int XV = 128 / 2 * VPR / 256;    // channel-pair vectors per thread (K <= 128)
+  constexpr int AV = NT * 16 * VPR / 256 > 0 ? NT * 16 * VPR / 256 : 1;  // addend vectors
+  constexpr int LDA = kPipeP + 8;
+  extern __shared__ __align__(16) unsigned char smem[];
+  const int ld = a.Kp + KPL;
+  const int nkb = a.Kp / KPL;
+  const int smask = (nkb & (nkb - 1)) == 0 ? nkb - 1 : 0;
+  T* WS = reinterpret_cast<T*>(smem);
+  T* XT = WS + (size_t)NT * 16 * ld;
+  T* A1 = XT + (size_t)kPipeP * ld;   // addend y / gx_spec, then out / gx
+  T* A2 = A1 + (size_t)NT * 16 * LDA; // FWD: z; otherwise the addend g_out
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int r16 = lane & 15, g = lane >> 4;
+  const T* in = reinterpret_cast<const T*>(a.in);
+  const T* w = reinterpret_cast<const T*>(a.w);
+  const T* add1 = reinterpret_cast<const T*>(a.add1);
+  const T* add2 = FWD ? nullptr : reinterpret_cast<const T*>(a.add2);
+  const T* bias = FWD ? reinterpret_cast<const T*>(a.bias) : nullptr;
+  T* out = reinterpret_cast<T*>(a.out);
+  T* zout = FWD ? reinterpret_cast<T*>(a.zout) : nullptr;
+  const bool gelu = FWD && a.act == FNO_EPI_ACT_GELU;
+  const bool resid = FWD && a.residual;
+
+  for (int e = tid; e < NT * 16 * ld; e += 256) {
+    const int n = e / ld, k = e - (e / ld) * ld;
+    T v = (T)0.0f;
+    if (n < a.N && k < a.K) v = FWD ? w[(int64_t)n * a.K + k] : w[(int64_t)k * a.N + n];
+    WS[e] = v;
+  }
+  for (int e = tid; e < kPipeP * ld; e += 256) XT[e] = (T)0.0f;
+  float bv[NT];
+#pragma unroll
+  for (int j = 0; j < NT; ++j) {
+    const int n = j * 16 + r16;
+    bv[j] = (bias && n < a.N) ? (float)bias[n] : 0.0f;
+  }
+  // swizzled position of channel k in transposed row p
+  auto xt_at = [&](int p, int k) {
+    return p * ld + ((((k >> 3) ^ ((p >> 3) & smask))) << 3) + (k & 7);
+  };
+
+  const int npv = ((a.K + 1) / 2) * VPR;  // channel-pair vectors of a tile
+  const int nav = a.N * VPR;              // addend / result vectors of a tile
+  u32x4 xr[XV][2], ar1[AV], ar2[AV];
+  auto load = [&](int64_t t) {
+    const int64_t b = t / a.ptiles;
+    const int64_t p0 = (t - b * a.ptiles) * kPipeP;
+#pragma unroll
+    for (int i = 0; i < XV; ++i) {
+      const int v = tid + 256 * i;
+      const int kp = v / VPR, c = v - (v / VPR) * VPR;
+      const int64_t p = p0 + (int64_t)c * 8;
+      xr[i][0] = xr[i][1] = u32x4{0u, 0u, 0u, 0u};
+      if (v < npv && p < a.P) {
+        const T* src = in + ((b * a.K + 2 * kp) * a.P + p);
+        xr[i][0] = *reinterpret_cast<const u32x4*>(src);
+        if (2 * kp + 1 < a.K) xr[i][1] = *reinterpret_cast<const u32x4*>(src + a.P);
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < AV; ++i) {
+      const int v = tid + 256 * i;
+      const int n = v / VPR, c = v - (v / VPR) * VPR;
+      const int64_t p = p0 + (int64_t)c * 8;
+      ar1[i] = ar2[i] = u32x4{0u, 0u, 0u, 0u};
+      if (v < nav && p < a.P) {
+        const int64_t off = (b * a.N + n) * a.P + p;
+        if (add1) ar1[i] = *reinterpret_cast<const u32x4*>(add1 + off);
+        if (add2) ar2[i] = *reinterpret_cast<const u32x4*>(add2 + off);
+      }
+    }
+  };
+
+  int64_t t = blockIdx.x;
+  if (t < a.tiles) load(t);
+  const int prow = 16 * wave + 4 * g;  // first of this lane's four points in the tile
+  while (t < a.tiles) {
+    const int64_t b = t / a.ptiles;
+    const int64_t p0 = (t - b * a.ptiles) * kPipeP;
+    __syncthreads();  // the previous tile is out of XT, A1 and A2
+#pragma unroll
+    for (int i = 0; i < XV; ++i) {
+      const int v = tid + 256 * i;
+      if (v < npv) {
+        const int kp = v / VPR, c = v - (v / VPR) * VPR;
+        uint16_t lo[8], hi[8];
+        __builtin_memcpy(lo, &xr[i][0], 16);
+        __builtin_memcpy(hi, &xr[i][1], 16);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const uint32_t pr = (uint32_t)lo[e] | ((uint32_t)hi[e] << 16);
+          *reinterpret_cast<uint32_t*>(XT + xt_at(c * 8 + e, 2 * kp)) = pr;
+        }
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < AV; ++i) {
+      const int v = tid + 256 * i;
+      if (v < nav) {
+        const int n = v / VPR, c = v - (v / VPR) * VPR;
+        *reinterpret_cast<u32x4*>(A1 + n * LDA + c * 8) = ar1[i];
+        if (!FWD) *reinterpret_cast<u32x4*>(A2 + n * LDA + c * 8) = ar2[i];
+      }
+    }
+    __syncthreads();
+    const int64_t tn = t + gridDim.x;
+    if (tn < a.tiles) load(tn);  // in flight during this tile's products and stores
+    f4 acc[NT];
+#pragma unroll
+    for (int j = 0; j < NT; ++j) {
+      const int n = j * 16 + r16;
+      const h4 u1 = *reinterpret_cast<const h4*>(A1 + n * LDA + prow);
+      h4 u2 = h4{};
+      if (!FWD) u2 = *reinterpret_cast<const h4*>(A2 + n * LDA + prow);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) acc[j][i] = bv[j] + (float)u1[i] + (float)u2[i];
+    }
+    for (int k0 = 0; k0 < a.Kp; k0 += KS) {
+      const frag af = M::ld(XT + xt_at(16 * wave + r16, k0 + g * KPL));
+#pragma unroll
+      for (int j = 0; j < NT; ++j) {
+        const frag bf = M::ld(WS + (j * 16 + r16) * ld + k0 + g * KPL);
+        acc[j] = M::mma(af, bf, acc[j]);
+      }
+    }
+    // results back into the row-major tiles at this lane's own positions
+#pragma unroll
+    for (int j = 0; j < NT; ++j) {
+      const int n = j * 16 + r16;
+      h4 zv, ov;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const float z = acc[j][i];
+        zv[i] = (T)z;
+        float o = gelu ? gelu_f(z) : z;
+        if (resid && n < a.K) o += (float)XT[xt_at(prow + i, n)];
+        ov[i] = (T)o;
+      }
+      *reinterpret_cast<h4*>(A1 + n * LDA + prow) = ov;
+      if (FWD) *reinterpret_cast<h4*>(A2 + n * LDA + prow) = zv;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int i = 0; i < AV; ++i) {
+      const int v = tid + 256 * i;
+      const int n = v / VPR, c = v - (v / VPR) * VPR;
+      const int64_t p = p0 + (int64_t)c * 8;
+      if (v < nav && p < a.P) {
+        const int64_t off = (b * a.N + n) * a.P + p;
+        *reinterpret_cast<u32x4*>(out + off) = *reinterpret_cast<const u32x4*>(A1 + n * LDA + c * 8);
+        if (zout)
+          *reinterpret_cast<u32x4*>(zout + off) =
+              *reinterpret_cast<const u32x4*>(A2 + n * LDA + c * 8);
+      }
+    }
+    t = tn;
   }
 }
 
@@ -350,6 +540,155 @@ __global__ __launch_bounds__(256) void epi_wgrad_kernel(EpiWgradArgs a) {
   for (int o = tid; o < a.Cout; o += 256) part[(int64_t)a.Cout * a.Cin + o] = bred[o];
 }
 
+// Software-pipelined fp16 parameter gradients for up to 128 x 128
+// channels, 64-point tiles: g_out, z and x rows arrive as 16-byte vectors
+// (eight lanes per 128-byte row segment), g_z is formed and stored in the
+// same layout and staged with x in row-major LDS tiles, from which the
+// matrix-core fragments (eight consecutive points per lane) are read.  Wave
+// w owns output-channel tiles w, w + 4 (OTW of them) by every input-channel
+// tile (IT); the next tile's loads are in flight during the products.
+constexpr int kWgP = 64;  // grid points per tile of the pipelined weight gradient
+
+template <int OTW, int IT>
+size_t wgrad_pipe_lds_bytes() {
+  return (size_t)(4 * OTW * 16 + IT * 16) * (kWgP + 8) * 2;
+}
+
+template <int OTW, int IT>
+__global__ __launch_bounds__(256) void epi_wgrad_pipe_kernel(EpiWgradArgs a) {
+  using T = _Float16;
+  using M = MM<T>;
+  using frag = typename M::frag;
+  constexpr int VPR = kWgP / 8;          // 16-byte vectors per channel row of a tile
+  constexpr int OROWS = 4 * OTW * 16;    // output-channel rows held (padded)
+  constexpr int GV = OROWS * VPR / 256;  // g_z vectors per thread
+  constexpr int XVN = IT * 16 * VPR / 256 > 0 ? IT * 16 * VPR / 256 : 1;
+  constexpr int LDA = kWgP + 8;
+  extern __shared__ __align__(16) unsigned char smem[];
+  T* GZ = reinterpret_cast<T*>(smem);  // [OROWS][LDA]
+  T* XS = GZ + OROWS * LDA;            // [IT*16][LDA]
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int r16 = lane & 15, g = lane >> 4;
+  const T* x = reinterpret_cast<const T*>(a.x);
+  const T* z = reinterpret_cast<const T*>(a.z);
+  const T* gout = reinterpret_cast<const T*>(a.gout);
+  T* gz = reinterpret_cast<T*>(a.gz);
+  const bool gelu = a.act == FNO_EPI_ACT_GELU;
+  const int ngv = a.Cout * VPR, nxv = a.Cin * VPR;
+
+  u32x4 gr[GV], zr[GV], xr[XVN];
+  float bs[GV];
+#pragma unroll
+  for (int i = 0; i < GV; ++i) bs[i] = 0.0f;
+  auto load = [&](int64_t t) {
+    const int64_t b = t / a.ptiles;
+    const int64_t p0 = (t - b * a.ptiles) * kWgP;
+#pragma unroll
+    for (int i = 0; i < GV; ++i) {
+      const int v = tid + 256 * i;
+      const int o = v / VPR, c = v - (v / VPR) * VPR;
+      const int64_t p = p0 + (int64_t)c * 8;
+      gr[i] = zr[i] = u32x4{0u, 0u, 0u, 0u};
+      if (v < ngv && p < a.P) {
+        const int64_t off = (b * a.Cout + o) * a.P + p;
+        gr[i] = *reinterpret_cast<const u32x4*>(gout + off);
+        if (gelu) zr[i] = *reinterpret_cast<const u32x4*>(z + off);
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < XVN; ++i) {
+      const int v = tid + 256 * i;
+      const int ic = v / VPR, c = v - (v / VPR) * VPR;
+      const int64_t p = p0 + (int64_t)c * 8;
+      xr[i] = u32x4{0u, 0u, 0u, 0u};
+      if (v < nxv && p < a.P) xr[i] = *reinterpret_cast<const u32x4*>(x + (b * a.Cin + ic) * a.P + p);
+    }
+  };
+
+  f4 acc[OTW][IT];
+#pragma unroll
+  for (int u = 0; u < OTW; ++u)
+#pragma unroll
+    for (int it = 0; it < IT; ++it) acc[u][it] = f4zero();
+  // rows beyond the channel counts stay zero in LDS
+  for (int e = tid; e < (OROWS + IT * 16) * LDA; e += 256) GZ[e] = (T)0.0f;
+
+  int64_t t = blockIdx.x;
+  if (t < a.tiles) load(t);
+  while (t < a.tiles) {
+    const int64_t b = t / a.ptiles;
+    const int64_t p0 = (t - b * a.ptiles) * kWgP;
+    __syncthreads();  // the previous tile's fragments are read
+#pragma unroll
+    for (int i = 0; i < GV; ++i) {
+      const int v = tid + 256 * i;
+      if (v < ngv) {
+        const int o = v / VPR, c = v - (v / VPR) * VPR;
+        h8 gv = w_as_h8(gr[i]);
+        const int64_t p = p0 + (int64_t)c * 8;
+        if (gelu) {
+          const h8 zv = w_as_h8(zr[i]);
+#pragma unroll
+          for (int e = 0; e < 8; ++e) gv[e] = (T)((float)gv[e] * gelu_grad_f((float)zv[e]));
+          if (p < a.P) *reinterpret_cast<h8*>(gz + (b * a.Cout + o) * a.P + p) = gv;
+        }
+        float sum = 0.0f;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) sum += (float)gv[e];
+        bs[i] += sum;
+        *reinterpret_cast<h8*>(GZ + o * LDA + c * 8) = gv;
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < XVN; ++i) {
+      const int v = tid + 256 * i;
+      if (v < nxv) {
+        const int ic = v / VPR, c = v - (v / VPR) * VPR;
+        *reinterpret_cast<u32x4*>(XS + ic * LDA + c * 8) = xr[i];
+      }
+    }
+    __syncthreads();
+    const int64_t tn = t + gridDim.x;
+    if (tn < a.tiles) load(tn);  // in flight during the products
+#pragma unroll
+    for (int k0 = 0; k0 < kWgP; k0 += 32) {
+      frag af[OTW], bf[IT];
+#pragma unroll
+      for (int u = 0; u < OTW; ++u)
+        af[u] = M::ld(GZ + ((wave + 4 * u) * 16 + r16) * LDA + k0 + g * 8);
+#pragma unroll
+      for (int it = 0; it < IT; ++it) bf[it] = M::ld(XS + (it * 16 + r16) * LDA + k0 + g * 8);
+#pragma unroll
+      for (int u = 0; u < OTW; ++u)
+#pragma unroll
+        for (int it = 0; it < IT; ++it) acc[u][it] = M::mma(af[u], bf[it], acc[u][it]);
+    }
+    t = tn;
+  }
+  // this work-group's partial sums: each (o, i) element belongs to one lane
+  const int64_t E = (int64_t)a.Cout * a.Cin + a.Cout;
+  float* part = a.part + (int64_t)blockIdx.x * E;
+#pragma unroll
+  for (int u = 0; u < OTW; ++u)
+#pragma unroll
+    for (int it = 0; it < IT; ++it)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int o = (wave + 4 * u) * 16 + 4 * g + q, ic = it * 16 + r16;
+        if (o < a.Cout && ic < a.Cin) part[(int64_t)o * a.Cin + ic] = acc[u][it][q];
+      }
+  // bias sums: the eight lanes of a row segment hold parts of one channel
+#pragma unroll
+  for (int i = 0; i < GV; ++i) {
+    float v = bs[i];
+    v += __shfl_xor(v, 1);
+    v += __shfl_xor(v, 2);
+    v += __shfl_xor(v, 4);
+    const int vv = tid + 256 * i;
+    if ((vv & (VPR - 1)) == 0 && vv < ngv) part[(int64_t)a.Cout * a.Cin + vv / VPR] = v;
+  }
+}
+
 // Any shape: g_z elementwise (act GELU) ...
 template <typename T>
 __global__ __launch_bounds__(256) void epi_gz_generic_kernel(const T* gout, const T* z, T* gz,
@@ -387,14 +726,25 @@ __global__ __launch_bounds__(256) void epi_wgrad_generic_kernel(const T* x, cons
   part[j * E + e] = s;
 }
 
+// 32 elements per work-group; the eight thread rows sum the partials
+// j = r, r + 8, ... and are then added in row order (a fixed order).
 __global__ __launch_bounds__(256) void epi_reduce_kernel(const float* part, int G, int64_t E,
                                                          int64_t Ew, float* gw, float* gb) {
-  const int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (e >= E) return;
+  __shared__ float red[8][32];
+  const int c = threadIdx.x & 31, r = threadIdx.x >> 5;
+  const int64_t e = (int64_t)blockIdx.x * 32 + c;
   float s = 0.0f;
-  for (int j = 0; j < G; ++j) s += part[(int64_t)j * E + e];
-  if (e < Ew) gw[e] = s;
-  else if (gb) gb[e - Ew] = s;
+  if (e < E)
+    for (int j = r; j < G; j += 8) s += part[(int64_t)j * E + e];
+  red[r][c] = s;
+  __syncthreads();
+  if (r == 0 && e < E) {
+    float t = red[0][c];
+#pragma unroll
+    for (int i = 1; i < 8; ++i) t += red[i][c];
+    if (e < Ew) gw[e] = t;
+    else if (gb) gb[e - Ew] = t;
+  }
 }
 
 // --------------------------------------------------------------------------
@@ -460,12 +810,21 @@ bool wgrad_fast(const EpiGeo& g, int* it, int* og, int* wpr) {
   return true;
 }
 
+// The pipelined fp16 weight gradient: points a multiple of 8, at most 128
+// channels each way.
+bool wgrad_pipe(const EpiGeo& g) {
+  return g.es == 2 && g.P % 8 == 0 && g.Cin <= 128 && g.Cout <= 128;
+}
+
 // Partial sums of the weight gradient: count and bytes.
 int wgrad_partials(const EpiGeo& g, int64_t* tiles, int64_t* ptiles) {
   const int64_t E = (int64_t)g.Cout * g.Cin + g.Cout;
   int it, og, wpr;
   int64_t cap = std::max<int64_t>(1, kPartialBytesCap / (E * 4));
-  if (wgrad_fast(g, &it, &og, &wpr)) {
+  if (wgrad_pipe(g)) {
+    *ptiles = cdiv(g.P, kWgP);
+    *tiles = g.B * *ptiles;
+  } else if (wgrad_fast(g, &it, &og, &wpr)) {
     const int ranges = 4 / wpr;
     *ptiles = cdiv(g.P, (int64_t)kWaveP * ranges);
     *tiles = g.B * *ptiles;
@@ -503,25 +862,57 @@ struct EpiMixLaunch {
   bool fast;
 };
 
+template <typename T, int NT, bool FWD>
+hipError_t launch_mix_nt(const EpiMixArgs& a, int grid, size_t lds, hipStream_t s) {
+  hipError_t e = allow_lds(reinterpret_cast<const void*>(&epi_mix_kernel<T, NT, FWD>), lds);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL((epi_mix_kernel<T, NT, FWD>), dim3(grid), dim3(256), lds, s, a);
+  return hipSuccess;
+}
+
+template <typename T, bool FWD>
+hipError_t launch_mix_fast(const EpiMixArgs& a, int grid, size_t lds, hipStream_t s) {
+  if (a.ntt >= 8) return launch_mix_nt<T, 8, FWD>(a, grid, lds, s);
+  if (a.ntt >= 4) return launch_mix_nt<T, 4, FWD>(a, grid, lds, s);
+  if (a.ntt >= 2) return launch_mix_nt<T, 2, FWD>(a, grid, lds, s);
+  return launch_mix_nt<T, 1, FWD>(a, grid, lds, s);
+}
+
+template <int NT, bool FWD>
+hipError_t launch_pipe_nt(const EpiMixArgs& a, int grid, size_t lds, hipStream_t s) {
+  hipError_t e = allow_lds(reinterpret_cast<const void*>(&epi_mix_pipe_kernel<NT, FWD>), lds);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL((epi_mix_pipe_kernel<NT, FWD>), dim3(grid), dim3(256), lds, s, a);
+  return hipSuccess;
+}
+
+template <bool FWD>
+hipError_t launch_pipe(const EpiMixArgs& a, int grid, hipStream_t s) {
+  const int nt = a.ntt <= 1 ? 1 : a.ntt <= 2 ? 2 : a.ntt <= 4 ? 4 : 8;
+  switch (nt) {
+    case 1: return launch_pipe_nt<1, FWD>(a, grid, pipe_lds_bytes<1>(a.Kp), s);
+    case 2: return launch_pipe_nt<2, FWD>(a, grid, pipe_lds_bytes<2>(a.Kp), s);
+    case 4: return launch_pipe_nt<4, FWD>(a, grid, pipe_lds_bytes<4>(a.Kp), s);
+    default: return launch_pipe_nt<8, FWD>(a, grid, pipe_lds_bytes<8>(a.Kp), s);
+  }
+}
+
 template <typename T>
 hipError_t launch_mix_t(EpiMixLaunch* L) {
   EpiMixArgs& a = L->a;
-  if (L->fast) {
-    const int nt = a.ntt >= 8 ? 8 : a.ntt >= 4 ? 4 : a.ntt >= 2 ? 2 : 1;
+  if (L->fast && sizeof(T) == 2 && a.ntt <= 8 && a.K <= 128) {
+    const int64_t tiles = a.B * cdiv(a.P, kPipeP);
+    a.ptiles = cdiv(a.P, kPipeP);
+    a.tiles = tiles;
+    const int grid = (int)std::min<int64_t>(tiles, (int64_t)4 * num_cus());
+    const hipError_t e = a.wt ? launch_pipe<false>(a, grid, L->s) : launch_pipe<true>(a, grid, L->s);
+    if (e != hipSuccess) return e;
+  } else if (L->fast) {
     const size_t lds = mix_lds_bytes<T>(a.ntt, a.Kp);
     const int grid = (int)std::min<int64_t>(a.tiles, (int64_t)4 * num_cus());
-    const void* k = nt == 8   ? reinterpret_cast<const void*>(&epi_mix_kernel<T, 8>)
-                    : nt == 4 ? reinterpret_cast<const void*>(&epi_mix_kernel<T, 4>)
-                    : nt == 2 ? reinterpret_cast<const void*>(&epi_mix_kernel<T, 2>)
-                              : reinterpret_cast<const void*>(&epi_mix_kernel<T, 1>);
-    hipError_t e = allow_lds(k, lds);
+    const hipError_t e = a.wt ? launch_mix_fast<T, false>(a, grid, lds, L->s)
+                              : launch_mix_fast<T, true>(a, grid, lds, L->s);
     if (e != hipSuccess) return e;
-    switch (nt) {
-      case 8: hipLaunchKernelGGL((epi_mix_kernel<T, 8>), dim3(grid), dim3(256), lds, L->s, a); break;
-      case 4: hipLaunchKernelGGL((epi_mix_kernel<T, 4>), dim3(grid), dim3(256), lds, L->s, a); break;
-      case 2: hipLaunchKernelGGL((epi_mix_kernel<T, 2>), dim3(grid), dim3(256), lds, L->s, a); break;
-      default: hipLaunchKernelGGL((epi_mix_kernel<T, 1>), dim3(grid), dim3(256), lds, L->s, a); break;
-    }
   } else {
     const dim3 grid((unsigned)cdiv(a.B * a.P, 256), (unsigned)cdiv(a.N, 8));
     hipLaunchKernelGGL(epi_mix_generic_kernel<T>, grid, dim3(256), 0, L->s, a);
@@ -567,7 +958,7 @@ fno_status run_mix(const EpiGeo& g, const char* name, const void* in, int K, con
 struct EpiWgradLaunch {
   EpiWgradArgs a;
   int es, G, it, og;
-  bool fast;
+  bool fast, pipe;
   const void* gz_src;  // generic path: the gradient the sums read
   float *gw, *gb;
   hipStream_t s;
@@ -577,7 +968,16 @@ template <typename T>
 hipError_t launch_wgrad_t(EpiWgradLaunch* L) {
   EpiWgradArgs& a = L->a;
   const int64_t E = (int64_t)a.Cout * a.Cin + a.Cout;
-  if (L->fast) {
+  if (L->pipe) {
+    const int cit = (int)cdiv(a.Cin, 16);
+    const int itp = cit <= 1 ? 1 : cit <= 2 ? 2 : cit <= 4 ? 4 : 8;
+    const int otw = a.Cout <= 64 ? 1 : 2;
+#define FNO_WGP(OTWV, ITV)                                                                     if (otw == OTWV && itp == ITV) {                                                               const size_t lds = wgrad_pipe_lds_bytes<OTWV, ITV>();                                        hipError_t e = allow_lds(reinterpret_cast<const void*>(&epi_wgrad_pipe_kernel<OTWV, ITV>), lds);     if (e != hipSuccess) return e;                                                               hipLaunchKernelGGL((epi_wgrad_pipe_kernel<OTWV, ITV>), dim3(L->G), dim3(256), lds, L->s, a);   }
+    FNO_WGP(1, 1) else FNO_WGP(1, 2) else FNO_WGP(1, 4) else FNO_WGP(1, 8)
+    else FNO_WGP(2, 1) else FNO_WGP(2, 2) else FNO_WGP(2, 4) else FNO_WGP(2, 8)
+    else return hipErrorInvalidValue;
+#undef FNO_WGP
+  } else if (L->fast) {
     const size_t lds = wgrad_lds_bytes<T>(a.wpr * L->og * 16, L->it * 16);
 #define FNO_WG(OGV, ITV)                                                                     \
   if (L->og == OGV && L->it == ITV) {                                                        \
@@ -605,7 +1005,7 @@ hipError_t launch_wgrad_t(EpiWgradLaunch* L) {
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(epi_reduce_kernel, dim3((unsigned)cdiv(E, 256)), dim3(256), 0, L->s, a.part,
+  hipLaunchKernelGGL(epi_reduce_kernel, dim3((unsigned)cdiv(E, 32)), dim3(256), 0, L->s, a.part,
                      L->G, E, (int64_t)a.Cout * a.Cin, L->gw, L->gb);
   return hipGetLastError();
 }
@@ -679,7 +1079,8 @@ extern "C" fno_status fno_block_epilogue_bwd_weight(const fno_block_desc* d, con
   a.act = g.act;
   L.es = g.es;
   L.G = wgrad_partials(g, &a.tiles, &a.ptiles);
-  L.fast = wgrad_fast(g, &L.it, &L.og, &a.wpr);
+  L.pipe = wgrad_pipe(g);
+  L.fast = !L.pipe && wgrad_fast(g, &L.it, &L.og, &a.wpr);
   a.ranges = L.fast ? 4 / a.wpr : 0;
   L.gw = g_w_skip;
   L.gb = g_b;

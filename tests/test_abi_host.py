@@ -507,17 +507,20 @@ def test_block_epilogue_descriptor_checks():
 
 def test_block_epilogue_workspace_is_the_partial_sums():
     """One fp32 partial sum of (c_out x c_in + c_out) values per work-group of
-    the parameter-gradient kernel, at most 512 of them, rounded to 256
+    the parameter-gradient kernel, at most 1024 of them, rounded to 256
     bytes."""
-    # 512-point tiles per work-group round (four waves of 128 points) on the
-    # matrix-core path, 4096-point slices on the generic one (255 points)
-    for bt, ci, co, pts, expect_g in [(8, 64, 64, 1 << 20, 512), (1, 16, 16, 256, 1),
-                                      (2, 5, 7, 480, 2), (3, 16, 16, 1536, 9),
-                                      (40, 6, 6, 255, 3)]:
-        d = B.make_block_desc(bt, ci, co, pts)
+    # fp16: 64-point tiles; fp32: 512-point tiles per work-group round (four
+    # waves of 128 points); the generic kernels (points not a multiple of 8)
+    # take 4096-point slices
+    P16, P32 = B.FNO_PREC_FP16_TANH, B.FNO_PREC_FP32
+    for bt, ci, co, pts, prec, expect_g in [(8, 64, 64, 1 << 20, P16, 1024),
+                                            (1, 16, 16, 256, P16, 4), (2, 5, 7, 480, P16, 16),
+                                            (3, 16, 16, 1536, P32, 9), (2, 5, 7, 480, P32, 2),
+                                            (40, 6, 6, 255, P16, 3)]:
+        d = B.make_block_desc(bt, ci, co, pts, prec)
         e = co * ci + co
         got = B.fno_block_epilogue_workspace_size(d, B.FNO_OP_BWD_WEIGHT)
-        assert got == (expect_g * e * 4 + 255) // 256 * 256, (bt, ci, co, pts)
+        assert got == (expect_g * e * 4 + 255) // 256 * 256, (bt, ci, co, pts, prec)
 
 
 def test_block_epilogue_rejects_bad_pointers_on_the_host():
