@@ -35,13 +35,36 @@ constexpr int64_t kPartialBytesCap = (int64_t)256 << 20;
 inline int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
 inline int64_t rup(int64_t a, int64_t b) { return cdiv(a, b) * b; }
 
+// The normal distribution function Phi(z) = (1 + erf(z / sqrt 2)) / 2 with
+// erf from Abramowitz & Stegun, Handbook of Mathematical Functions, formula
+// 7.1.26 (absolute error at most 1.5e-7): for x >= 0,
+//   erf(x) = 1 - t (a1 + t (a2 + t (a3 + t (a4 + t a5)))) exp(-x^2),
+//   t = 1 / (1 + p x),
+// odd in x.  exp(-x^2) at x = |z| / sqrt 2 is also sqrt(2 pi) phi(z), the
+// normal density the derivative needs.
+struct NormalCdf {
+  float cdf, e;  // Phi(z) and exp(-z^2 / 2)
+};
+__device__ __forceinline__ NormalCdf normal_cdf(float z) {
+  const float x = __builtin_fabsf(z) * 0.70710678118654752f;
+  const float t = __builtin_amdgcn_rcpf(__builtin_fmaf(0.3275911f, x, 1.0f));
+  float poly = __builtin_fmaf(1.061405429f, t, -1.453152027f);
+  poly = __builtin_fmaf(poly, t, 1.421413741f);
+  poly = __builtin_fmaf(poly, t, -0.284496736f);
+  poly = __builtin_fmaf(poly, t, 0.254829592f);
+  const float e = __expf(-x * x);
+  const float erfc_half = 0.5f * poly * t * e;  // (1 - erf(x)) / 2
+  return NormalCdf{z >= 0.0f ? 1.0f - erfc_half : erfc_half, e};
+}
 __device__ __forceinline__ float gelu_f(float z) {
-  return 0.5f * z * (1.0f + erff(z * 0.70710678118654752f));
+  if (z != z) return z;
+  return z * normal_cdf(z).cdf;
 }
 // d/dz z Phi(z) = Phi(z) + z phi(z)
 __device__ __forceinline__ float gelu_grad_f(float z) {
-  return 0.5f * (1.0f + erff(z * 0.70710678118654752f)) +
-         z * 0.39894228040143268f * expf(-0.5f * z * z);
+  if (z != z) return z;
+  const NormalCdf n = normal_cdf(z);
+  return __builtin_fmaf(z * 0.39894228040143268f, n.e, n.cdf);
 }
 
 template <typename T>
