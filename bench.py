@@ -259,9 +259,9 @@ def copy_bandwidth(torch, nbytes=1 << 30, reps=10):
 # (first match wins; the template flag "true" marks the pre-activation
 # variant of a transform)
 KERNEL_NAMES = [
-    (r"epi_mix_kernel<[^>]*true>", "block_epilogue_fwd"),
-    (r"epi_mix_kernel<", "block_epilogue_bwd_data"),
-    (r"epi_wgrad_kernel<", "block_epilogue_bwd_weight"),
+    (r"epi_mix\w*<[^>]*true>", "block_epilogue_fwd"),
+    (r"epi_mix\w*<", "block_epilogue_bwd_data"),
+    (r"epi_wgrad\w*<", "block_epilogue_bwd_weight"),
     (r"r2c_\w+<[^>]*true>", "r2c_plane_tanh"),
     (r"r2c_\w+<", "r2c_plane"),
     (r"slab_adj_wgrad_kernel", "contract_adjoint_wgrad"),
@@ -406,8 +406,9 @@ def summarize(args):
               "| kernel | dispatches | avg us | events us | min us | max us | alg MB | "
               "alg GB/s (avg) | frac | HBM fetch MB | HBM write MB | traffic / alg |",
               "|---|---|---|---|---|---|---|---|---|---|---|---|"] + rows
+    whole = wl.weight == "dense" and wl.ndim < 3 and not args.block
     lines += ["", f"Sum of the averages of the kernels in the table: {total_avg:.1f} us"
-                  + (" (the whole step)." if wl.weight == "dense" and wl.ndim < 3 else
+                  + (" (the whole step)." if whole else
                      " (the other kernels of the step are in the summary below)."), "",
               "rocprofv3 --stats summary (all dispatches):", "",
               "| name | calls | avg ns | min ns | max ns | % |", "|---|---|---|---|---|---|"]
