@@ -344,14 +344,16 @@ __device__ __forceinline__ uint32_t lut2(const _Float16* tab, uint32_t w, us2 sa
   const uint32_t aw = w & 0x7fff7fffu;
   us2 ax;
   __builtin_memcpy(&ax, &aw, 4);
-  const us2 nan = __builtin_elementwise_min(
-      __builtin_elementwise_sub_sat(ax, (us2){0x7c00, 0x7c00}), (us2){1, 1});
-  const us2 idx = __builtin_elementwise_min(ax, sat) + nan;
-  h2 r;
-  r[0] = tab[idx[0]];
-  r[1] = tab[idx[1]];
-  uint32_t u;
-  __builtin_memcpy(&u, &r, 4);
+  // 1 for the NaN codes (above 0x7c00): bit 15 of ax + 0x3ff (no overflow,
+  // ax <= 0x7fff); all on packed 16-bit operations
+  const us2 nan = (ax + (us2){0x3ff, 0x3ff}) >> (us2){15, 15};
+  const us2 off = (__builtin_elementwise_min(ax, sat) + nan) << (us2){1, 1};  // byte offsets
+  uint32_t o;
+  __builtin_memcpy(&o, &off, 4);
+  const unsigned char* base = reinterpret_cast<const unsigned char*>(tab);
+  const uint32_t r0 = *reinterpret_cast<const uint16_t*>(base + (o & 0xffffu));
+  const uint32_t r1 = *reinterpret_cast<const uint16_t*>(base + (o >> 16));
+  const uint32_t u = r0 | (r1 << 16);
   return ODD ? (u | (w & 0x80008000u)) : u;
 }
 

@@ -46,6 +46,10 @@ constexpr int W2_NTS = 2;          // cache policy of the inverse's stores: stre
 constexpr int W2_MB = 64;          // output columns per block of the inverse's last stage
 constexpr int W2_LDO = 68;         // transpose buffer row stride (floats)
 
+// LDS bytes of a lookup table of codes 0..sat plus the NaN entry, rounded
+// up to 256 (the regions after it stay aligned)
+__host__ __device__ __forceinline__ int w2_lut_bytes(int sat) { return ((sat + 2) * 2 + 255) & ~255; }
+
 // column x of a 64-wide row of the transpose buffer, stored with the two
 // 4-float halves of each 8-float group swapped in the upper 32 columns: the
 // eight lanes that read one row (8 floats each) then hit 32 distinct banks
@@ -77,9 +81,12 @@ __global__ __launch_bounds__(W2_NT, 1) void r2c_wide2_kernel(R2CArgs a) {
   constexpr int NKB = W2_H / W2_KS;            // step-B k-steps per item
   static_assert(TWP >= 1, "slice pieces");
   extern __shared__ __align__(16) unsigned char smem[];
-  _Float16* AT = reinterpret_cast<_Float16*>(smem);   // [2 rc][2 cls][2 KBPC][LDR]
+  // the lookup table first, so that a lookup address is the byte offset of
+  // the code itself (no base to add)
+  _Float16* lut = reinterpret_cast<_Float16*>(smem);
+  _Float16* AT = reinterpret_cast<_Float16*>(smem + (PRE ? w2_lut_bytes(a.lut_sat) : 0));
+  // [2 rc][2 cls][2 KBPC][LDR]
   _Float16* TWb = AT + 4 * 2 * KBPC * W2_LDR;           // [2][NROW][LDT]
-  _Float16* lut = TWb + 2 * NROW * W2_LDT;
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int r16 = lane & 15, g = lane >> 4;
@@ -368,12 +375,14 @@ __global__ __launch_bounds__(W2_NT, 1) void c2r_wide2_kernel(C2RArgs a) {
   constexpr int PPR = 4 * KBPC / 8;    // pieces per twiddle row
   static_assert(TWP >= 1, "block pieces");
   extern __shared__ __align__(16) unsigned char smem[];
-  _Float16* ZT = reinterpret_cast<_Float16*>(smem);      // [2][2][2 KBPC][LDZ]
-  unsigned char* reg = smem + L::zt_bytes;
+  // the lookup table first (a lookup address is the code's byte offset)
+  _Float16* lut = reinterpret_cast<_Float16*>(smem);
+  _Float16* ZT = reinterpret_cast<_Float16*>(smem + (EPI ? w2_lut_bytes(a.lut_sat) : 0));
+  // [2][2][2 KBPC][LDZ]
+  unsigned char* reg = reinterpret_cast<unsigned char*>(ZT) + L::zt_bytes;
   _Float16* VL = reinterpret_cast<_Float16*>(reg);       // [2 W2_H][LDV]
   _Float16* TW = reinterpret_cast<_Float16*>(reg);       // [2][W2_MB][LDT]
   float* OB = reinterpret_cast<float*>(reg + L::tw_bytes);  // [8][16][W2_LDO]
-  _Float16* lut = reinterpret_cast<_Float16*>(reg + L::reg_bytes);
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int r16 = lane & 15, g = lane >> 4;
@@ -632,7 +641,7 @@ size_t r2c_wide2_lds_bytes(int nctc, bool pre, int lut_sat) {
   const int kbpc = nctc * 8;
   const size_t at = (size_t)4 * 2 * kbpc * W2_LDR * 2;
   const size_t tw = (size_t)2 * 4 * kbpc * W2_LDT * 2;
-  return at + tw + (pre ? (size_t)(lut_sat + 2) * 2 : 0);
+  return at + tw + (pre ? (size_t)w2_lut_bytes(lut_sat) : 0);
 }
 
 size_t c2r_wide2_lds_bytes(int nctc, int nkzh, bool epi, int lut_sat) {
@@ -642,7 +651,7 @@ size_t c2r_wide2_lds_bytes(int nctc, int nkzh, bool epi, int lut_sat) {
   FNO_C2RW2_BYTES(2, 1) FNO_C2RW2_BYTES(2, 2) FNO_C2RW2_BYTES(4, 1) FNO_C2RW2_BYTES(4, 2)
 #undef FNO_C2RW2_BYTES
   if (base == 0) return (size_t)1 << 30;  // not a shape of this path
-  return base + (epi ? (size_t)(lut_sat + 2) * 2 : 0);
+  return base + (epi ? (size_t)w2_lut_bytes(lut_sat) : 0);
 }
 
 template <int NCTC, bool PRE>
