@@ -559,6 +559,12 @@ __global__ __launch_bounds__(W2_NT, 1) void c2r_wide2_kernel(C2RArgs a) {
       const _Float16* tb = TW + par * (W2_MB * LDT) + r16 * LDT + g * 8;
 #pragma unroll
       for (int u = 0; u < 2; ++u) {
+        // x of both segments of this half, requested before its products
+        u32x4 xs2[2][2];
+        if (EPI) {
+          ldX(rx, c0, b, 2 * u, xs2[0]);
+          ldX(rx, c0, b, 2 * u + 1, xs2[1]);
+        }
         f4 ae[4], ao[4];
 #pragma unroll
         for (int c = 0; c < 4; ++c) {
@@ -571,9 +577,7 @@ __global__ __launch_bounds__(W2_NT, 1) void c2r_wide2_kernel(C2RArgs a) {
         }
 #pragma unroll
         for (int hf = 0; hf < 2; ++hf) {
-          const int sg = 2 * u + hf;
-          u32x4 xs[2];
-          if (EPI) ldX(rx, c0, b, sg, xs);
+          const u32x4 (&xs)[2] = xs2[hf];
           // D: lane holds row r16 of the tile, columns m = c 16 + 4 g + i
 #pragma unroll
           for (int c = 0; c < 4; ++c) {
