@@ -465,6 +465,243 @@ int64_t max_offset(const GemmArgs& g, int which) {
 // (an index in the result only, sizes past 32-bit offsets, no room for the
 // split-K partial sums) or wastes most of a tile on it; the caller then uses
 // the generic kernels.
+// ---------------------------------------------------------------------------
+// Mode products with a small factor: R(pre, r, post) = s c(t) sum_k
+// A(pre, k, post) U(k, r), where the post indices are innermost and
+// contiguous in both A and R and U is the small operand (at most 16 columns
+// r, indices k and r only); pre, k and r have any strides (pre and k in A,
+// pre and r in R).  These are the
+// steps that apply u_in or u_out to a spectrum (forward, adjoint and the
+// weight gradient's first two).  As a GEMM they have 16 rows at most and a
+// long streaming operand; here a work-group takes up to 64 consecutive post
+// positions of one pre index, stages the K x 64 block of A in LDS with all
+// of its loads issued at once, and each thread forms four consecutive
+// positions of one column r in fp32 (VALU).
+constexpr int MP_T = 64;
+constexpr int MP_PRE = 6;
+
+struct ModeProdArgs {
+  const void* a;
+  const void* u;
+  void* out;
+  int a_elem, u_elem, out_elem, conj_a, conj_u;
+  int K, R;
+  int64_t T, P;              // post positions, pre positions
+  int tt;                    // post positions per work-group (T, or 64)
+  int n_pre;                 // pre indices (innermost last)
+  int64_t pre_ext[MP_PRE], pre_sa[MP_PRE], pre_so[MP_PRE];  // extents, strides in A and R
+  int64_t sa_k;              // stride of k in A
+  int64_t so_r;              // stride of r in R
+  int64_t su_k, su_r;        // element strides of U
+  int vec;                   // 16-byte loads of A rows
+  float scale;
+  int c_ext;                 // extent of the innermost post index carrying c(t) (0: none)
+  int Nb;
+};
+
+template <typename TA>
+__global__ __launch_bounds__(256) void pair_modeprod_kernel(ModeProdArgs m) {
+  extern __shared__ __align__(16) unsigned char smem[];
+  typedef typename std::conditional<std::is_same<TA, _Float16>::value, h2, f2>::type CA;
+  CA* As = reinterpret_cast<CA*>(smem);                   // [K][MP_T]
+  f2* Us = reinterpret_cast<f2*>(As + (size_t)m.K * MP_T);  // [K][16]
+  const int tid = threadIdx.x;
+  const int tt = m.tt;
+  const int64_t t0 = (int64_t)blockIdx.x * tt;
+  const int64_t p = blockIdx.y;
+  int64_t aoff = 0, ooff = 0;
+  {
+    int64_t q = p;
+    for (int j = m.n_pre - 1; j >= 0; --j) {
+      const int64_t dgt = q % m.pre_ext[j];
+      q /= m.pre_ext[j];
+      aoff += dgt * m.pre_sa[j];
+      ooff += dgt * m.pre_so[j];
+    }
+  }
+  const CA* a = reinterpret_cast<const CA*>(m.a) + aoff;
+  // A block: all loads in flight at once
+  constexpr int CPV = 16 / (int)sizeof(CA);  // complex values per 16-byte vector
+  if (m.vec) {
+    const int vpr = tt / CPV;  // vectors per row
+    for (int v = tid; v < m.K * vpr; v += 256) {
+      const int k = v / vpr, c = v - (v / vpr) * vpr;
+      const int64_t t = t0 + (int64_t)c * CPV;
+      u32x4 val = {0u, 0u, 0u, 0u};
+      if (t < m.T) val = *reinterpret_cast<const u32x4*>(a + k * m.sa_k + t);
+      *reinterpret_cast<u32x4*>(As + k * MP_T + c * CPV) = val;
+    }
+  } else {
+    for (int v = tid; v < m.K * tt; v += 256) {
+      const int k = v / tt, c = v - (v / tt) * tt;
+      const int64_t t = t0 + c;
+      CA val{};
+      if (t < m.T) val = a[k * m.sa_k + t];
+      As[k * MP_T + c] = val;
+    }
+  }
+  for (int e = tid; e < m.K * 16; e += 256) {
+    const int k = e >> 4, r = e & 15;
+    f2 uv = f2{0.0f, 0.0f};
+    if (r < m.R) {
+      const int64_t off = k * m.su_k + r * m.su_r;
+      if (m.u_elem == ELEM_F16) {
+        const h2 h = reinterpret_cast<const h2*>(m.u)[off];
+        uv = f2{(float)h[0], (float)h[1]};
+      } else {
+        uv = reinterpret_cast<const f2*>(m.u)[off];
+      }
+      if (m.conj_u) uv[1] = -uv[1];
+    }
+    Us[e] = uv;
+  }
+  __syncthreads();
+  const int tq = tid & 15, r = tid >> 4;
+  if (r >= m.R || 4 * tq >= tt) return;
+  float ar[4] = {0.0f, 0.0f, 0.0f, 0.0f}, ai[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+  const float sa = m.conj_a ? -1.0f : 1.0f;
+  for (int k = 0; k < m.K; ++k) {
+    const f2 uv = Us[k * 16 + r];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const CA av = As[k * MP_T + 4 * tq + i];
+      const float xr = (float)av[0], xi = sa * (float)av[1];
+      ar[i] = __builtin_fmaf(xr, uv[0], __builtin_fmaf(-xi, uv[1], ar[i]));
+      ai[i] = __builtin_fmaf(xr, uv[1], __builtin_fmaf(xi, uv[0], ai[i]));
+    }
+  }
+  const int64_t obase = ooff + r * m.so_r;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int64_t t = t0 + 4 * tq + i;
+    if (t >= m.T || 4 * tq + i >= tt) continue;
+    float sc = m.scale;
+    if (m.c_ext) {
+      const int64_t ci = t % m.c_ext;
+      sc *= (ci == 0 || 2 * ci == m.Nb) ? 1.0f : 2.0f;
+    }
+    if (m.out_elem == ELEM_F16)
+      reinterpret_cast<h2*>(m.out)[obase + t] = h2{to_h(ar[i] * sc), to_h(ai[i] * sc)};
+    else
+      reinterpret_cast<f2*>(m.out)[obase + t] = f2{ar[i] * sc, ai[i] * sc};
+  }
+}
+
+// The mode-product form of a step, if it has one (hipErrorNotSupported
+// otherwise): one contracted index k, one result index r carried by the
+// smaller operand only (with k), every other result index carried by the
+// larger operand only, which is laid out [pre][k][post] densely with the
+// result's order of pre and post.
+hipError_t launch_pair_modeprod(const PairArgs& p, hipStream_t s) {
+  if (p.n_red != 1 || p.a_stride_red[0] == 0 || p.b_stride_red[0] == 0) return hipErrorNotSupported;
+  int rpos = -1;
+  for (int k = 0; k < p.n_out; ++k) {
+    const bool ina = p.a_stride_out[k] != 0, inb = p.b_stride_out[k] != 0;
+    if (ina == inb) return hipErrorNotSupported;  // batch-like or absent index
+    if (inb) {
+      if (rpos >= 0) return hipErrorNotSupported;
+      rpos = k;
+    }
+  }
+  if (rpos < 0) return hipErrorNotSupported;
+  const int64_t K = p.red_ext[0], R = p.out_ext[rpos];
+  if (R > 16 || K < 1) return hipErrorNotSupported;
+  // result strides (dense in result order)
+  int64_t os[PW_MAXIDX];
+  {
+    int64_t st = 1;
+    for (int k = p.n_out - 1; k >= 0; --k) {
+      os[k] = st;
+      st *= p.out_ext[k];
+    }
+  }
+  // post: the longest innermost run of result indices that is also
+  // innermost and contiguous in A
+  int64_t st = 1, T = 1;
+  int ps = p.n_out;
+  while (ps > 0 && ps - 1 != rpos && p.a_stride_out[ps - 1] == st) {
+    --ps;
+    st *= p.out_ext[ps];
+    T *= p.out_ext[ps];
+  }
+  if (ps == p.n_out) return hipErrorNotSupported;
+  // pre: every other result index but r
+  int n_pre = 0;
+  int64_t P = 1;
+  int64_t pe[PW_MAXIDX], pa[PW_MAXIDX], po[PW_MAXIDX];
+  for (int k = 0; k < ps; ++k) {
+    if (k == rpos) continue;
+    if (n_pre >= MP_PRE) return hipErrorNotSupported;
+    pe[n_pre] = p.out_ext[k];
+    pa[n_pre] = p.a_stride_out[k];
+    po[n_pre] = os[k];
+    P *= p.out_ext[k];
+    ++n_pre;
+  }
+  // c(t) only along the innermost post index
+  int c_ext = 0;
+  if (p.scale_c_axis >= 0) {
+    if (p.scale_c_axis != p.n_out - 1) return hipErrorNotSupported;
+    c_ext = (int)p.out_ext[p.n_out - 1];
+  }
+  const bool ah = p.a_elem == ELEM_F16;
+  if (K > (ah ? 256 : 128) || P > 65535 || T / MP_T >= 0x7fffffffll) return hipErrorNotSupported;
+  ModeProdArgs m{};
+  m.a = p.a;
+  m.u = p.b;
+  m.out = p.out;
+  m.a_elem = p.a_elem;
+  m.u_elem = p.b_elem;
+  m.out_elem = p.out_elem;
+  m.conj_a = p.conj_a;
+  m.conj_u = p.conj_b;
+  m.K = (int)K;
+  m.R = (int)R;
+  m.T = T;
+  m.P = P;
+  m.su_k = p.b_stride_red[0];
+  m.su_r = p.b_stride_out[rpos];
+  m.sa_k = p.a_stride_red[0];
+  m.so_r = os[rpos];
+  m.n_pre = n_pre;
+  for (int k = 0; k < n_pre; ++k) {
+    m.pre_ext[k] = pe[k];
+    m.pre_sa[k] = pa[k];
+    m.pre_so[k] = po[k];
+  }
+  m.tt = (int)std::min<int64_t>(T, MP_T);
+  const int esz = ah ? 4 : 8;  // bytes per complex value of A
+  // 16-byte row pieces: every row start (pre and k strides, the tile
+  // starts) a multiple of 16 bytes
+  bool vec = ((uintptr_t)p.a & 15u) == 0 && (m.tt * esz) % 16 == 0 && (T * esz) % 16 == 0 &&
+             (m.sa_k * esz) % 16 == 0;
+  for (int k = 0; k < n_pre; ++k) vec = vec && (m.pre_sa[k] * esz) % 16 == 0;
+  m.vec = vec;
+  m.scale = p.scale;
+  m.c_ext = c_ext;
+  m.Nb = p.Nb;
+  const size_t lds = (size_t)K * MP_T * esz + (size_t)K * 16 * 8;
+  dim3 grid((unsigned)((T + m.tt - 1) / m.tt), (unsigned)P), block(256);
+  if (ah) {
+    if (lds > 65536) {
+      const hipError_t e = hipFuncSetAttribute(
+          reinterpret_cast<const void*>(&pair_modeprod_kernel<_Float16>),
+          hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+      if (e != hipSuccess) return e;
+    }
+    hipLaunchKernelGGL(pair_modeprod_kernel<_Float16>, grid, block, lds, s, m);
+  } else {
+    if (lds > 65536) {
+      const hipError_t e = hipFuncSetAttribute(
+          reinterpret_cast<const void*>(&pair_modeprod_kernel<float>),
+          hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+      if (e != hipSuccess) return e;
+    }
+    hipLaunchKernelGGL(pair_modeprod_kernel<float>, grid, block, lds, s, m);
+  }
+  return hipGetLastError();
+}
+
 hipError_t launch_pair_gemm(const PairArgs& p, hipStream_t s) {
   GemmArgs g{};
   g.a = p.a;

@@ -189,6 +189,9 @@ hipError_t launch_contract(int elem, const ContractArgs& a, hipStream_t s);
 hipError_t launch_wgrad(int elem, const WgradArgs& a, hipStream_t s);
 hipError_t launch_pair(const PairArgs& a, hipStream_t s);
 hipError_t launch_pair_gemm(const PairArgs& a, hipStream_t s);
+// The mode-product form (a small factor applied along one index of a large
+// dense operand); hipErrorNotSupported when the step is not of that form.
+hipError_t launch_pair_modeprod(const PairArgs& a, hipStream_t s);
 size_t r2c_wide_lds_bytes(int nct, bool pre, int lut_sat);
 size_t c2r_wide_lds_bytes(int nct, int Kap, bool epi, int lut_sat);
 hipError_t launch_r2c_wide(const R2CArgs& a, int nct, int grid, size_t lds, hipStream_t s);

@@ -1322,6 +1322,10 @@ hipError_t launch_pair(const PairArgs& a_in, hipStream_t s) {
   PairArgs a = a_in;
   if (a.out_size <= 0) return hipSuccess;
   {
+    const hipError_t e = launch_pair_modeprod(a, s);
+    if (e != hipErrorNotSupported) return e;
+  }
+  {
     const hipError_t e = launch_pair_gemm(a, s);
     if (e != hipErrorNotSupported) return e;
   }
