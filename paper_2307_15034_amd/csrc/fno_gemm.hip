@@ -587,6 +587,109 @@ __global__ __launch_bounds__(256) void pair_modeprod_kernel(ModeProdArgs m) {
   }
 }
 
+// Both operands in fp16: the products on the matrix cores, four real
+// v_mfma_f32_16x16x16_f16 per complex product (M = r, N = post positions,
+// K = k).  The block of A is staged transposed (position-major, k
+// contiguous) and split into real and imaginary planes, so that a lane's
+// four consecutive k are one 8-byte LDS read; wave w takes positions
+// 16 w .. 16 w + 15 of the tile.
+__host__ __device__ inline int mp_kp(int K) { return ((K + 15) / 16) * 16 + 4; }
+
+__global__ __launch_bounds__(256) void pair_modeprod_h_kernel(ModeProdArgs m) {
+  extern __shared__ __align__(16) unsigned char smem[];
+  const int KP = mp_kp(m.K), Kp = KP - 4;
+  _Float16* Ar = reinterpret_cast<_Float16*>(smem);  // [MP_T][KP]
+  _Float16* Ai = Ar + MP_T * KP;
+  _Float16* Ur = Ai + MP_T * KP;                     // [16][KP]
+  _Float16* Ui = Ur + 16 * KP;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int r16 = lane & 15, g = lane >> 4;
+  const int tt = m.tt;
+  const int64_t t0 = (int64_t)blockIdx.x * tt;
+  const int64_t p = blockIdx.y;
+  int64_t aoff = 0, ooff = 0;
+  {
+    int64_t q = p;
+    for (int j = m.n_pre - 1; j >= 0; --j) {
+      const int64_t dgt = q % m.pre_ext[j];
+      q /= m.pre_ext[j];
+      aoff += dgt * m.pre_sa[j];
+      ooff += dgt * m.pre_so[j];
+    }
+  }
+  const h2* a = reinterpret_cast<const h2*>(m.a) + aoff;
+  const _Float16 sa = m.conj_a ? (_Float16)-1.0f : (_Float16)1.0f;
+  // zero the padding rows k in [K, Kp) of the A planes
+  for (int e = tid; e < MP_T * (Kp - m.K); e += 256) {
+    const int t = e / (Kp - m.K), k = m.K + e % (Kp - m.K);
+    Ar[t * KP + k] = Ai[t * KP + k] = (_Float16)0.0f;
+  }
+  if (m.vec) {
+    const int vpr = tt / 4;  // 16-byte pieces (four complex values) per row
+    for (int v = tid; v < m.K * vpr; v += 256) {
+      const int k = v / vpr, c = v - (v / vpr) * vpr;
+      const int64_t t = t0 + (int64_t)c * 4;
+      u32x4 val = {0u, 0u, 0u, 0u};
+      if (t < m.T) val = *reinterpret_cast<const u32x4*>(a + k * m.sa_k + t);
+      const h8 hv = w_as_h8(val);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        Ar[(4 * c + i) * KP + k] = hv[2 * i];
+        Ai[(4 * c + i) * KP + k] = hv[2 * i + 1] * sa;
+      }
+    }
+  } else {
+    for (int v = tid; v < m.K * tt; v += 256) {
+      const int k = v / tt, c = v - (v / tt) * tt;
+      const int64_t t = t0 + c;
+      h2 val = h2{(_Float16)0.0f, (_Float16)0.0f};
+      if (t < m.T) val = a[k * m.sa_k + t];
+      Ar[c * KP + k] = val[0];
+      Ai[c * KP + k] = val[1] * sa;
+    }
+  }
+  // positions of the tile past tt stay unread (their columns are not stored)
+  for (int e = tid; e < 16 * Kp; e += 256) {
+    const int r = e / Kp, k = e - (e / Kp) * Kp;
+    h2 uv = h2{(_Float16)0.0f, (_Float16)0.0f};
+    if (r < m.R && k < m.K) uv = reinterpret_cast<const h2*>(m.u)[k * m.su_k + r * m.su_r];
+    Ur[r * KP + k] = uv[0];
+    Ui[r * KP + k] = m.conj_u ? -uv[1] : uv[1];
+  }
+  __syncthreads();
+  if (16 * wave >= tt) return;
+  f4 re = f4zero(), im = f4zero();
+  for (int k0 = 0; k0 < Kp; k0 += 16) {
+    const h4 ur = *reinterpret_cast<const h4*>(Ur + r16 * KP + k0 + 4 * g);
+    const h4 ui = *reinterpret_cast<const h4*>(Ui + r16 * KP + k0 + 4 * g);
+    const h4 br = *reinterpret_cast<const h4*>(Ar + (16 * wave + r16) * KP + k0 + 4 * g);
+    const h4 bi = *reinterpret_cast<const h4*>(Ai + (16 * wave + r16) * KP + k0 + 4 * g);
+    re = __builtin_amdgcn_mfma_f32_16x16x16f16(ur, br, re, 0, 0, 0);
+    re = __builtin_amdgcn_mfma_f32_16x16x16f16(-ui, bi, re, 0, 0, 0);
+    im = __builtin_amdgcn_mfma_f32_16x16x16f16(ur, bi, im, 0, 0, 0);
+    im = __builtin_amdgcn_mfma_f32_16x16x16f16(ui, br, im, 0, 0, 0);
+  }
+  // D: lane holds r = 4 g + i, position 16 wave + r16
+  const int tl = 16 * wave + r16;
+  const int64_t t = t0 + tl;
+  if (tl >= tt || t >= m.T) return;
+  float sc = m.scale;
+  if (m.c_ext) {
+    const int64_t ci = t % m.c_ext;
+    sc *= (ci == 0 || 2 * ci == m.Nb) ? 1.0f : 2.0f;
+  }
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int r = 4 * g + i;
+    if (r >= m.R) continue;
+    const int64_t o = ooff + r * m.so_r + t;
+    if (m.out_elem == ELEM_F16)
+      reinterpret_cast<h2*>(m.out)[o] = h2{to_h(re[i] * sc), to_h(im[i] * sc)};
+    else
+      reinterpret_cast<f2*>(m.out)[o] = f2{re[i] * sc, im[i] * sc};
+  }
+}
+
 // The mode-product form of a step, if it has one (hipErrorNotSupported
 // otherwise): one contracted index k, one result index r carried by the
 // smaller operand only (with k), every other result index carried by the
@@ -682,7 +785,16 @@ hipError_t launch_pair_modeprod(const PairArgs& p, hipStream_t s) {
   m.Nb = p.Nb;
   const size_t lds = (size_t)K * MP_T * esz + (size_t)K * 16 * 8;
   dim3 grid((unsigned)((T + m.tt - 1) / m.tt), (unsigned)P), block(256);
-  if (ah) {
+  if (ah && p.b_elem == ELEM_F16) {
+    const size_t ldsh = (size_t)(2 * MP_T + 2 * 16) * mp_kp((int)K) * 2;
+    if (ldsh > 65536) {
+      const hipError_t e = hipFuncSetAttribute(
+          reinterpret_cast<const void*>(&pair_modeprod_h_kernel),
+          hipFuncAttributeMaxDynamicSharedMemorySize, (int)ldsh);
+      if (e != hipSuccess) return e;
+    }
+    hipLaunchKernelGGL(pair_modeprod_h_kernel, grid, block, ldsh, s, m);
+  } else if (ah) {
     if (lds > 65536) {
       const hipError_t e = hipFuncSetAttribute(
           reinterpret_cast<const void*>(&pair_modeprod_kernel<_Float16>),
