@@ -741,5 +741,8 @@ def max_plane_rel_l2(a, b, nlead: int = 2) -> float:
     lead = a.shape[:nlead]
     worst = 0.0
     for idx in itertools.product(*[range(s) for s in lead]):
-        worst = max(worst, rel_l2(a[idx], b[idx]))
+        r = rel_l2(a[idx], b[idx])
+        if np.isnan(r):
+            return r  # a non-finite plane is the worst plane
+        worst = max(worst, r)
     return worst

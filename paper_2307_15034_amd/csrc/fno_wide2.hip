@@ -615,7 +615,11 @@ __global__ __launch_bounds__(W2_NT, 1) void c2r_wide2_kernel(C2RArgs a) {
             for (int e = 0; e < 8; ++e) w[e] = to_h(v[e]);
             u32x4 wv;
             __builtin_memcpy(&wv, &w, 16);
-            __builtin_amdgcn_raw_buffer_store_b128(wv, ry, xoff(c0, b, hf, h), u * hiA, W2_NTS);
+            // the whole offset in the vector operand: with an SGPR offset
+            // the compiler leaves no wait states between this store and a
+            // VALU write of its data registers, and the store has then been
+            // seen to take the new values of some lanes
+            __builtin_amdgcn_raw_buffer_store_b128(wv, ry, xoff(c0, b, hf, h) + u * hiA, 0, W2_NTS);
           }
           wave_lds_sync();  // the buffer is written again by the next segment
         }

@@ -109,6 +109,19 @@ def rel(a, b) -> float:
     return O.rel_l2(a, b)
 
 
+def nonfinite_report(got, ref, nlead: int = 2, show: int = 8) -> str:
+    """Where the non-finite values of got and of ref are: their counts and
+    the first few (leading-index plane, position) of each."""
+    out = []
+    for name, arr in (("got", np.asarray(got)), ("ref", np.asarray(ref))):
+        bad = ~np.isfinite(arr)
+        idx = np.argwhere(bad)[:show]
+        planes = sorted({tuple(int(v) for v in i[:nlead]) for i in np.argwhere(bad)})
+        out.append(f"{name}: {int(bad.sum())} non-finite in planes {planes[:show]}"
+                   f"{' ...' if len(planes) > show else ''} first {idx.tolist()}")
+    return "; ".join(out)
+
+
 def gw_complex(gw):
     if isinstance(gw, dict):
         return {"core": cplx(gw["core"]), "u_in": cplx(gw["u_in"]),

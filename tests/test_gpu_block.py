@@ -28,6 +28,8 @@ def _close(name, got, ref, prec, planes=True):
     rp = O.max_plane_rel_l2(got, ref) if planes and np.ndim(ref) >= 3 else None
     extra = f", max per plane {rp:.3e}" if rp is not None else ""
     U.say(f"  {name}: rel_l2 = {r:.3e}{extra} (tol {U.TOL[prec]:.0e})")
+    if not np.isfinite(r):
+        U.say("  " + U.nonfinite_report(got, ref))
     assert np.isfinite(r) and r <= U.TOL[prec], f"{name}: {r:.3e}"
     if rp is not None:
         assert np.isfinite(rp) and rp <= U.TOL[prec], f"{name} (worst plane): {rp:.3e}"

@@ -265,6 +265,46 @@ def test_deterministic_repeat(prec):
         assert np.array_equal(u, v)
 
 
+@pytest.mark.timeout(300)
+@pytest.mark.parametrize("wid,reps", [(3, 24), (5, 6)])
+def test_deterministic_repeat_workloads(wid, reps):
+    """Repeated calls on a benchmark workload in its launch configuration are
+    bit-identical to the first call: the 1024^2 layer's forward and data
+    gradient (radix-2 transforms), and the Tucker layer's combined backward
+    (its weight gradient on the side stream).  A race in a kernel, such as a
+    store handed another segment's values in a few lanes now and then, shows
+    as a difference between repetitions."""
+    wl = synth.WORKLOADS[wid]
+    prec = "fp16_tanh"
+    _, npdt, _ = U.prec_codes(prec)
+    U.say(f"repeat {wl.name} x{reps}")
+    x, w, gy = _workload_inputs(wid, prec)
+    tucker = isinstance(w, dict)
+    layer = (U.make_layer(wl.n, wl.modes, wl.batch, wl.c_in, wl.c_out, prec, wl.rank, 1)
+             if tucker else U.make_layer(wl.n, wl.modes, wl.batch, wl.c_in, wl.c_out, prec))
+    xd, gyd = U.dev(x), U.dev(gy)
+    wd = ({"core": U.dev(w["core"]), "u_in": U.dev(w["u_in"]), "u_out": U.dev(w["u_out"]),
+           "u_mode": [U.dev(u) for u in w["u_mode"]]} if tucker else U.dev(w))
+    y, gx = torch.empty_like(xd), torch.empty_like(xd)
+    xh = layer.spectrum_buffer(0)
+    gw = layer.alloc_grads()
+
+    def outputs():
+        layer.fwd(xd, wd, y=y, x_hat=xh)
+        if tucker:
+            layer.bwd(xd, wd, gyd, x_hat=xh, gx=gx, gw=gw)
+            return [y, gx, gw["core"], gw["u_in"], gw["u_out"]] + list(gw["u_mode"])
+        layer.bwd_data(xd, wd, gyd, gx=gx)
+        return [y, gx]
+
+    first = [t.clone() for t in outputs()]
+    for r in range(1, reps):
+        cur = outputs()
+        for k, (a, b) in enumerate(zip(cur, first)):
+            assert torch.equal(a, b), f"repetition {r}: output {k} differs"
+    torch.cuda.synchronize()
+
+
 @pytest.mark.parametrize("prec", PRECS)
 def test_caches_match_recompute(prec):
     n, modes, Bt, ci, co = (20, 24), (3, 5), 3, 5, 7

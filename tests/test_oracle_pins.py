@@ -387,13 +387,18 @@ def pin_rel_l2_hand():
 def pin_max_plane_hand():
     """max_plane_rel_l2 on a [2, 2, 3] tensor of ones with one element of
     plane (1, 0) off by 3: that plane's error is 3 / sqrt(3) = sqrt(3), while
-    the whole-tensor figure is only 3 / sqrt(12)."""
+    the whole-tensor figure is only 3 / sqrt(12).  A NaN in any plane makes
+    the worst plane NaN, wherever the plane comes in the scan."""
     b = np.ones((2, 2, 3))
     a = b.copy()
     a[1, 0, 2] += 3.0
+    n = a.copy()
+    n[0, 0, 1] = np.nan
+    nan_ok = np.isnan(O.max_plane_rel_l2(n, b)) and np.isnan(O.max_plane_rel_l2(n[::-1], b))
     return max(abs(O.max_plane_rel_l2(a, b) - np.sqrt(3.0)),
                abs(O.max_plane_rel_l2(b, b) - 0.0),
-               abs(O.rel_l2(a, b) - 3.0 / np.sqrt(12.0)))
+               abs(O.rel_l2(a, b) - 3.0 / np.sqrt(12.0)),
+               0.0 if nan_ok else np.inf)
 
 
 def pin_sigma_closed_form():
