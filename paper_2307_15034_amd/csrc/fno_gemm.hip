@@ -690,6 +690,173 @@ __global__ __launch_bounds__(256) void pair_modeprod_h_kernel(ModeProdArgs m) {
   }
 }
 
+// ---------------------------------------------------------------------------
+// Batches of small products with the batch innermost: R(m, n, t) = s c(t)
+// sum_k A(m, k, t) B(n, k, t) with one index each for m (<= 16), n (<= 16)
+// and k, and the batch indices t innermost and contiguous in A, B and R (the
+// weight-gradient steps R = sum_b P Q, Q conj(S), P S of the factorised
+// weights, batched over the modes).  As GEMMs these waste most of a tile or
+// run a thread per result with each operand element loaded once per result
+// that uses it.  Here a work-group stages the A and B rows of BT_T
+// consecutive batch positions in LDS (fp32 complex, every load issued
+// before the first is waited for), and thread (t, m, half) forms the n
+// results of its half of the row.
+constexpr int BT_T = 8;
+constexpr int BT_ROWS = 1024;  // (M + N) K rows of BT_T values: 64 KiB of LDS
+constexpr int BT_LD = BT_ROWS / (256 / BT_T);
+
+struct BtArgs {
+  const void* a;
+  const void* b;
+  void* out;
+  int out_elem, conj_a, conj_b;
+  int M, N, K;
+  int64_t T;
+  int64_t sa_m, sa_k, sb_n, sb_k, so_m, so_n;
+  float scale;
+  int c_ext, Nb;
+};
+
+template <typename TE>
+__device__ __forceinline__ f2 bt_load(const void* p, int64_t off) {
+  if constexpr (sizeof(TE) == 2) {
+    const h2 h = reinterpret_cast<const h2*>(p)[off];
+    return f2{(float)h[0], (float)h[1]};
+  } else {
+    return reinterpret_cast<const f2*>(p)[off];
+  }
+}
+
+template <typename TE>
+__global__ __launch_bounds__(256) void pair_bt_kernel(BtArgs g) {
+  extern __shared__ __align__(16) unsigned char smem[];
+  f2* S = reinterpret_cast<f2*>(smem);  // rows [A: m K + k][B: M K + n K + k] x BT_T
+  const int tid = threadIdx.x;
+  const int tl = tid % BT_T;
+  const int64_t t = (int64_t)blockIdx.x * BT_T + tl;
+  const int64_t tc = t < g.T ? t : g.T - 1;  // in-bounds stand-in past the end
+  const int arows = g.M * g.K, rows = (g.M + g.N) * g.K;
+  const int nld = (rows + 256 / BT_T - 1) / (256 / BT_T);
+  // Every load unconditional (rows clamped into range) so that none waits
+  // for another.
+  f2 v[BT_LD];
+#pragma unroll
+  for (int i = 0; i < BT_LD; ++i) {
+    if (i < nld) {
+      const int r = min(tid / BT_T + i * (256 / BT_T), rows - 1);
+      const bool isa = r < arows;
+      const int rr = isa ? r : r - arows;
+      const int q = rr / g.K, k = rr - q * g.K;
+      const int64_t off = (isa ? q * g.sa_m + k * g.sa_k : q * g.sb_n + k * g.sb_k) + tc;
+      v[i] = bt_load<TE>(isa ? g.a : g.b, off);
+    }
+  }
+#pragma unroll
+  for (int i = 0; i < BT_LD; ++i) {
+    if (i < nld) {
+      const int r = tid / BT_T + i * (256 / BT_T);
+      if (r < rows) {
+        const int cj = r < arows ? g.conj_a : g.conj_b;
+        S[r * BT_T + tl] = f2{v[i][0], cj ? -v[i][1] : v[i][1]};
+      }
+    }
+  }
+  __syncthreads();
+  const int m = (tid / BT_T) % 16, n0 = (tid / 128) * 8;
+  if (m >= g.M || n0 >= g.N || t >= g.T) return;
+  const int nn = min(8, g.N - n0);
+  float cr[8], ci[8];
+#pragma unroll
+  for (int j = 0; j < 8; ++j) cr[j] = ci[j] = 0.0f;
+  const f2* Ar = S + (size_t)m * g.K * BT_T + tl;
+  const f2* Br = S + ((size_t)arows + (size_t)n0 * g.K) * BT_T + tl;
+  for (int k = 0; k < g.K; ++k) {
+    const f2 av = Ar[k * BT_T];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      if (j < nn) {
+        const f2 bv = Br[(j * g.K + k) * BT_T];
+        cr[j] = __builtin_fmaf(av[0], bv[0], __builtin_fmaf(-av[1], bv[1], cr[j]));
+        ci[j] = __builtin_fmaf(av[0], bv[1], __builtin_fmaf(av[1], bv[0], ci[j]));
+      }
+    }
+  }
+  float sc = g.scale;
+  if (g.c_ext) {
+    const int64_t c = t % g.c_ext;
+    sc *= (c == 0 || 2 * c == g.Nb) ? 1.0f : 2.0f;
+  }
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    if (j >= nn) continue;
+    const int64_t o = m * g.so_m + (n0 + j) * g.so_n + t;
+    if (g.out_elem == ELEM_F16)
+      reinterpret_cast<h2*>(g.out)[o] = h2{to_h(cr[j] * sc), to_h(ci[j] * sc)};
+    else
+      reinterpret_cast<f2*>(g.out)[o] = f2{cr[j] * sc, ci[j] * sc};
+  }
+}
+
+// The batch-innermost form of a step, if it has one (hipErrorNotSupported
+// otherwise): the result's innermost indices are carried by both operands
+// with the same dense strides, one other result index by each operand alone,
+// one contracted index.
+hipError_t launch_pair_bt(const PairArgs& p, hipStream_t s) {
+  if (p.n_red != 1 || p.a_stride_red[0] == 0 || p.b_stride_red[0] == 0 || p.a_elem != p.b_elem)
+    return hipErrorNotSupported;
+  int64_t st = 1, T = 1;
+  int bs = p.n_out;
+  while (bs > 0 && p.a_stride_out[bs - 1] == st && p.b_stride_out[bs - 1] == st) {
+    --bs;
+    st *= p.out_ext[bs];
+    T *= p.out_ext[bs];
+  }
+  if (bs == p.n_out || bs != 2) return hipErrorNotSupported;
+  // the two outer result indices: one in A only (m), one in B only (n)
+  int im = -1, in_ = -1;
+  for (int k = 0; k < 2; ++k) {
+    const bool ina = p.a_stride_out[k] != 0, inb = p.b_stride_out[k] != 0;
+    if (ina && !inb) im = k;
+    else if (inb && !ina) in_ = k;
+  }
+  if (im < 0 || in_ < 0) return hipErrorNotSupported;
+  const int64_t M = p.out_ext[im], N = p.out_ext[in_], K = p.red_ext[0];
+  if (M > 16 || N > 16) return hipErrorNotSupported;
+  int c_ext = 0;
+  if (p.scale_c_axis >= 0) {
+    if (p.scale_c_axis != p.n_out - 1) return hipErrorNotSupported;
+    c_ext = (int)p.out_ext[p.n_out - 1];
+  }
+  BtArgs g{};
+  g.a = p.a;
+  g.b = p.b;
+  g.out = p.out;
+  g.out_elem = p.out_elem;
+  g.conj_a = p.conj_a;
+  g.conj_b = p.conj_b;
+  g.M = (int)M;
+  g.N = (int)N;
+  g.K = (int)K;
+  g.T = T;
+  g.sa_m = p.a_stride_out[im];
+  g.sa_k = p.a_stride_red[0];
+  g.sb_n = p.b_stride_out[in_];
+  g.sb_k = p.b_stride_red[0];
+  // result strides (dense in result order): the two outer indices
+  g.so_m = (im == 0 ? p.out_ext[1] : 1) * T;
+  g.so_n = (in_ == 0 ? p.out_ext[1] : 1) * T;
+  g.scale = p.scale;
+  g.c_ext = c_ext;
+  g.Nb = p.Nb;
+  if ((M + N) * K > BT_ROWS) return hipErrorNotSupported;
+  const size_t lds = (size_t)(M + N) * K * BT_T * sizeof(f2);
+  const int64_t blocks = (T + BT_T - 1) / BT_T;
+  if (blocks > 0x7fffffff) return hipErrorNotSupported;
+  auto kern = p.a_elem == ELEM_F16 ? pair_bt_kernel<_Float16> : pair_bt_kernel<float>;
+  hipLaunchKernelGGL(kern, dim3((unsigned)blocks), dim3(256), lds, s, g);
+  return hipGetLastError();
+}
+
 // The mode-product form of a step, if it has one (hipErrorNotSupported
 // otherwise): one contracted index k, one result index r carried by the
 // smaller operand only (with k), every other result index carried by the

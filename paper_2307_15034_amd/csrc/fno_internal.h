@@ -192,6 +192,9 @@ hipError_t launch_pair_gemm(const PairArgs& a, hipStream_t s);
 // The mode-product form (a small factor applied along one index of a large
 // dense operand); hipErrorNotSupported when the step is not of that form.
 hipError_t launch_pair_modeprod(const PairArgs& a, hipStream_t s);
+// The batch-innermost form (small products batched over the modes);
+// hipErrorNotSupported when the step is not of that form.
+hipError_t launch_pair_bt(const PairArgs& a, hipStream_t s);
 size_t r2c_wide_lds_bytes(int nct, bool pre, int lut_sat);
 size_t c2r_wide_lds_bytes(int nct, int Kap, bool epi, int lut_sat);
 hipError_t launch_r2c_wide(const R2CArgs& a, int nct, int grid, size_t lds, hipStream_t s);

@@ -1326,6 +1326,10 @@ hipError_t launch_pair(const PairArgs& a_in, hipStream_t s) {
     if (e != hipErrorNotSupported) return e;
   }
   {
+    const hipError_t e = launch_pair_bt(a, s);
+    if (e != hipErrorNotSupported) return e;
+  }
+  {
     const hipError_t e = launch_pair_gemm(a, s);
     if (e != hipErrorNotSupported) return e;
   }

@@ -1684,6 +1684,69 @@ hipError_t timed_launch(const char* name, hipStream_t s, hipError_t (*launch)(vo
   return timed(name, s, [&] { return launch(ctx); });
 }
 
+// A second stream per device for work of one call that needs none of the
+// other part's results: the factorised weight gradient of the combined
+// backward (a chain of small, latency-bound contractions) runs on it while
+// the caller's stream carries the adjoint path and the inverse transform.
+// The fork and the join are event waits, so the call stays ordered on the
+// caller's stream as a whole (and a stream capture records both branches);
+// calls that enqueue forks on one device take turns under a mutex.  Created
+// on first use outside a stream capture and kept until the process ends.
+struct SideStream {
+  hipStream_t s = nullptr;
+  hipEvent_t fork = nullptr, join = nullptr;
+};
+std::mutex g_side_mutex;
+std::map<int, SideStream> g_side;
+
+// The device's side stream, or null (the caller then runs both parts on its
+// own stream): when it cannot be created, or must not be because `s` is
+// being captured.  Call with g_side_mutex held.
+SideStream* side_stream_locked(hipStream_t s) {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return nullptr;
+  auto it = g_side.find(dev);
+  if (it != g_side.end()) return &it->second;
+  hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+  if (hipStreamIsCapturing(s, &cs) != hipSuccess || cs != hipStreamCaptureStatusNone) return nullptr;
+  SideStream ss;
+  if (hipStreamCreateWithFlags(&ss.s, hipStreamNonBlocking) != hipSuccess) return nullptr;
+  if (hipEventCreateWithFlags(&ss.fork, hipEventDisableTiming) != hipSuccess ||
+      hipEventCreateWithFlags(&ss.join, hipEventDisableTiming) != hipSuccess) {
+    if (ss.fork) (void)hipEventDestroy(ss.fork);
+    (void)hipStreamDestroy(ss.s);
+    return nullptr;
+  }
+  return &(g_side[dev] = ss);
+}
+
+// Runs side(stream) and main() as two branches after the work already on
+// `s`; everything enqueued on `s` afterwards follows both.  The join is
+// enqueued whatever either branch returns.
+template <typename FS, typename FM>
+fno_status run_forked(hipStream_t s, FS side, FM main_part) {
+  std::unique_lock<std::mutex> lk(g_side_mutex);
+  SideStream* ss = side_stream_locked(s);
+  if (!ss) {
+    lk.unlock();
+    const fno_status st = main_part();
+    return st != FNO_OK ? st : side(s);
+  }
+  // the caller's branch is enqueued first: launched from the host one by
+  // one, its few large kernels then start while the side's many small ones
+  // are still being enqueued
+  const hipError_t e = hipEventRecord(ss->fork, s);
+  if (e != hipSuccess) return hip_fail(e, "fork to the side stream");
+  const fno_status st_main = main_part();
+  const hipError_t ef = hipStreamWaitEvent(ss->s, ss->fork, 0);
+  const fno_status st_side = ef == hipSuccess ? side(ss->s) : FNO_OK;
+  const hipError_t ej = ef == hipSuccess ? hipEventRecord(ss->join, ss->s) : ef;
+  const hipError_t ew = ej == hipSuccess ? hipStreamWaitEvent(s, ss->join, 0) : ej;
+  if (st_side != FNO_OK) return st_side;
+  if (st_main != FNO_OK) return st_main;
+  return ew == hipSuccess ? FNO_OK : hip_fail(ew, "join of the side stream");
+}
+
 // The forward call.  build_plan = false: the plan must already exist (no
 // device allocation, no blocking upload; the allocation-free entry point).
 fno_status fwd_impl(const fno_conv_desc* d, const void* x, const fno_weights* w, void* y,
@@ -1993,22 +2056,36 @@ fno_status fno_spectral_conv_bwd(const fno_conv_desc* d, const void* x, const fn
   char* wsd = base + L.add(ws_bytes(d, pl, FNO_OP_BWD_DATA, true));
   void* gh = gy_hat_out ? gy_hat_out : (void*)gs;
   if (tucker) {
+    // the data part's regions inside wsd, laid out as in bwd_data (its first
+    // region, the gradient spectrum, is unused: gh holds it), then the
+    // weight part's scratch
     char* wsw = base + L.add(ws_bytes(d, pl, FNO_OP_BWD_WEIGHT, true));
-    const size_t nd = ws_bytes(d, pl, FNO_OP_BWD_DATA, true);
-    const size_t nw = ws_bytes(d, pl, FNO_OP_BWD_WEIGHT, true);
-    if ((st = fno_spectral_conv_bwd_data(d, x, w, gy, gx, gh, wsd, nd, s)) != FNO_OK) return st;
+    WsLayout Ld;
+    (void)Ld.add(spec_bytes(g, g.Cout));
+    char* gxs = wsd + Ld.add(spec_bytes(g, g.Cin));
+    char* inter = wsd + Ld.add(std::max(inter3d_bytes(g, g.Cin), inter3d_bytes(g, g.Cout)));
+    char* tsc = wsd + Ld.total;
+    double* bounds = (double*)(wsd + ws_core(d, pl, FNO_OP_BWD_DATA, true));
+    if ((st = run_sigma_stats(pl, x, bounds, s)) != FNO_OK) return st;
+    if ((st = run_r2c(pl, gy, gh, inter, g.Cout, 0, 1, s)) != FNO_OK) return st;
+    const void* xh = x_hat;
     if (!cache) {
-      // the input spectrum, recomputed into its own region (the 3-D
-      // intermediate is the third region of the data part's workspace)
-      WsLayout Ld;
-      (void)Ld.add(spec_bytes(g, g.Cout));
-      (void)Ld.add(spec_bytes(g, g.Cin));
-      char* inter = wsd + Ld.add(std::max(inter3d_bytes(g, g.Cin), inter3d_bytes(g, g.Cout)));
-      // the data part has left the clip bounds in its workspace
-      const double* bounds = (const double*)(wsd + ws_core(d, pl, FNO_OP_BWD_DATA, true));
       if ((st = run_r2c(pl, x, xs, inter, g.Cin, 1, 0, s, bounds)) != FNO_OK) return st;
+      xh = xs;
     }
-    return fno_spectral_conv_bwd_weight(d, x, gy, w, cache ? x_hat : xs, gh, gw, wsw, nw, s);
+    // The weight gradient reads only the two spectra and the weights and
+    // writes only its own scratch and gw: it runs beside the data part.
+    auto weight_part = [&](hipStream_t st_) {
+      return d->weight_kind == FNO_WEIGHT_CP ? run_cp_wgrad(d, pl, xh, gh, w, gw, wsw, st_)
+                                             : run_tucker_wgrad(d, pl, xh, gh, w, gw, wsw, st_);
+    };
+    auto data_part = [&]() -> fno_status {
+      fno_status r = run_tucker_path(d, pl, true, gh, w, gxs, tsc, s);
+      if (r != FNO_OK) return r;
+      const float sc = (float)(1.0 / std::sqrt((double)g.N));
+      return run_c2r(pl, gxs, gx, inter, g.Cin, sc, pre_on ? x : nullptr, s, bounds);
+    };
+    return run_forked(s, weight_part, data_part);
   }
   // dense: the data part's regions inside wsd, laid out as in bwd_data (its
   // first region, the gradient spectrum, is unused: gh holds it)
