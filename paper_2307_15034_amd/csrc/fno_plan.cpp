@@ -1404,14 +1404,22 @@ fno_status run_tucker_path(const fno_conv_desc* d, const Plan* pl, bool adjoint,
 // R = sum_b P Q, S = core x u_1 .. x u_d; g_core = R x conj(u_j)...,
 // g_u_j = R . conj(core x_{q != j} u_q), g_u_in = conj(Xhat) . (Q conj S),
 // g_u_out = (sqrt(N) c G) . (P conj S).
+// Phases of the factorised weight gradients: the steps that read only the
+// weights (partial products of the core and the mode factors), and the
+// steps that read the spectra.  Every phase lays out the scratch the same
+// way, so the two may run as separate calls in order.
+constexpr int WG_WEIGHTS = 1, WG_SPECTRA = 2, WG_ALL = 3;
+
 fno_status run_tucker_wgrad(const fno_conv_desc* d, const Plan* pl, const void* xh,
                             const void* gh, const fno_weights* w, fno_weight_grads* gw,
-                            char* scratch, hipStream_t s, size_t* scratch_used = nullptr) {
+                            char* scratch, hipStream_t s, size_t* scratch_used = nullptr,
+                            int phases = WG_ALL) {
   const bool dry = scratch_used != nullptr;
+  int phase = WG_SPECTRA;  // the phase of the steps that follow
   auto run_pair = [&](const Sizes& sz_, const Opnd& A, const Opnd& Bo, const std::string& res,
                       void* out, int out_elem, float scale, int c_axis_char, int Nb,
                       hipStream_t st) -> fno_status {
-    if (dry) return FNO_OK;
+    if (dry || !(phases & phase)) return FNO_OK;
     return fno::run_pair(sz_, A, Bo, res, out, out_elem, scale, c_axis_char, Nb, st, scratch);
   };
   const Geo& g = pl->g;
@@ -1474,6 +1482,7 @@ fno_status run_tucker_wgrad(const fno_conv_desc* d, const Plan* pl, const void* 
     Opnd cur = Wt(w->core, "ae" + rk, 0);
     std::string lab = "ae" + rk;
     bool first = true;
+    phase = WG_WEIGHTS;
     for (int q = 0; q < nd; ++q) {
       if (q == j) continue;
       std::string nl;
@@ -1486,6 +1495,7 @@ fno_status run_tucker_wgrad(const fno_conv_desc* d, const Plan* pl, const void* 
       lab = nl;
       first = false;
     }
+    phase = WG_SPECTRA;
     // g_u_j[x_j, r_j] = sum R[a,e,sp] conj(C_j[a,e,.., r_j, ..])
     std::string res = std::string(1, kSpatial[j]) + kRank[j];
     Opnd cj = first ? Wt(w->core, "ae" + rk, 1) : Opnd{cur.ptr, cur.lab, cur.elem, 1};
@@ -1494,6 +1504,7 @@ fno_status run_tucker_wgrad(const fno_conv_desc* d, const Plan* pl, const void* 
   }
   // S[a,e,sp] = core x all u_j
   void* S;
+  phase = WG_WEIGHTS;
   {
     Opnd cur = Wt(w->core, "ae" + rk, 0);
     std::string lab = "ae" + rk;
@@ -1509,6 +1520,7 @@ fno_status run_tucker_wgrad(const fno_conv_desc* d, const Plan* pl, const void* 
     }
     S = const_cast<void*>(cur.ptr);
   }
+  phase = WG_SPECTRA;
   const std::string lS = "ae" + sp;
   // Z1[b,a,sp] = sum_e Q[b,e,sp] conj(S[a,e,sp]);  g_u_in = sum conj(Xhat) Z1
   void* Z1 = buf("ba" + sp);
@@ -1546,11 +1558,12 @@ size_t tucker_wgrad_bytes(const fno_conv_desc* d, const Plan* pl) {
 //   g_u_in = sum_{b,sp} conj(Xhat) (Q conj(S)),  g_u_out = sum_{b,sp} G' (P conj(S)).
 fno_status run_cp_wgrad(const fno_conv_desc* d, const Plan* pl, const void* xh, const void* gh,
                         const fno_weights* w, fno_weight_grads* gw, char* scratch,
-                        hipStream_t s, size_t* scratch_used = nullptr) {
+                        hipStream_t s, size_t* scratch_used = nullptr, int phases = WG_ALL) {
   const bool dry = scratch_used != nullptr;
+  int phase = WG_SPECTRA;  // the phase of the steps that follow
   auto pair = [&](const Sizes& sz_, const Opnd& A, const Opnd& Bo, const std::string& res,
                   void* out, float scale, int c_axis_char) -> fno_status {
-    if (dry) return FNO_OK;
+    if (dry || !(phases & phase)) return FNO_OK;
     return run_pair(sz_, A, Bo, res, out, ELEM_F32, scale, c_axis_char, pl->g.Nb, s, scratch);
   };
   const Geo& g = pl->g;
@@ -1616,6 +1629,7 @@ fno_status run_cp_wgrad(const fno_conv_desc* d, const Plan* pl, const void* xh, 
   }
   // S[r, sp] = lambda[r] prod_j u_j[sp_j, r]
   Opnd S = Wt(w->core, "r", 0);
+  phase = WG_WEIGHTS;
   {
     std::string lab = "r";
     for (int j = 0; j < nd; ++j) {
@@ -1626,6 +1640,7 @@ fno_status run_cp_wgrad(const fno_conv_desc* d, const Plan* pl, const void* xh, 
       lab = nl;
     }
   }
+  phase = WG_SPECTRA;
   const Opnd Sc{S.ptr, S.lab, S.elem, 1};
   void* Z1 = buf(lP);
   if ((r = pair(sz, F(Q, lP, 0), Sc, lP, Z1, 1.0f, 0))) return r;
@@ -1687,14 +1702,14 @@ hipError_t timed_launch(const char* name, hipStream_t s, hipError_t (*launch)(vo
 // A second stream per device for work of one call that needs none of the
 // other part's results: the factorised weight gradient of the combined
 // backward (a chain of small, latency-bound contractions) runs on it while
-// the caller's stream carries the adjoint path and the inverse transform.
-// The fork and the join are event waits, so the call stays ordered on the
+// the caller's stream carries the transforms and the adjoint path.  The
+// forks and the join are event waits, so the call stays ordered on the
 // caller's stream as a whole (and a stream capture records both branches);
 // calls that enqueue forks on one device take turns under a mutex.  Created
 // on first use outside a stream capture and kept until the process ends.
 struct SideStream {
   hipStream_t s = nullptr;
-  hipEvent_t fork = nullptr, join = nullptr;
+  hipEvent_t fork = nullptr, fork2 = nullptr, join = nullptr;
 };
 std::mutex g_side_mutex;
 std::map<int, SideStream> g_side;
@@ -1711,40 +1726,54 @@ SideStream* side_stream_locked(hipStream_t s) {
   if (hipStreamIsCapturing(s, &cs) != hipSuccess || cs != hipStreamCaptureStatusNone) return nullptr;
   SideStream ss;
   if (hipStreamCreateWithFlags(&ss.s, hipStreamNonBlocking) != hipSuccess) return nullptr;
-  if (hipEventCreateWithFlags(&ss.fork, hipEventDisableTiming) != hipSuccess ||
-      hipEventCreateWithFlags(&ss.join, hipEventDisableTiming) != hipSuccess) {
-    if (ss.fork) (void)hipEventDestroy(ss.fork);
-    (void)hipStreamDestroy(ss.s);
-    return nullptr;
+  hipEvent_t* ev[3] = {&ss.fork, &ss.fork2, &ss.join};
+  for (hipEvent_t* e : ev) {
+    if (hipEventCreateWithFlags(e, hipEventDisableTiming) != hipSuccess) {
+      for (hipEvent_t* f : ev)
+        if (*f) (void)hipEventDestroy(*f);
+      (void)hipStreamDestroy(ss.s);
+      return nullptr;
+    }
   }
   return &(g_side[dev] = ss);
 }
 
-// Runs side(stream) and main() as two branches after the work already on
-// `s`; everything enqueued on `s` afterwards follows both.  The join is
-// enqueued whatever either branch returns.
-template <typename FS, typename FM>
-fno_status run_forked(hipStream_t s, FS side, FM main_part) {
+// Two branches after the work already on `s`: on the caller's stream
+// first() then second(); on the side stream side_a(stream), which reads
+// nothing first() writes, and then side_b(stream), which reads first()'s
+// results and nothing second() writes.  Everything enqueued on `s`
+// afterwards follows both branches; the join is enqueued whatever the
+// branches return.  The caller's work is enqueued before the side's, so
+// that, launched from the host one by one, its few large kernels start
+// while the side's many small ones are still being enqueued.
+template <typename FA, typename F1, typename FB, typename F2>
+fno_status run_forked(hipStream_t s, FA side_a, F1 first, FB side_b, F2 second) {
   std::unique_lock<std::mutex> lk(g_side_mutex);
   SideStream* ss = side_stream_locked(s);
+  fno_status st;
   if (!ss) {
     lk.unlock();
-    const fno_status st = main_part();
-    return st != FNO_OK ? st : side(s);
+    if ((st = first()) != FNO_OK || (st = second()) != FNO_OK || (st = side_a(s)) != FNO_OK)
+      return st;
+    return side_b(s);
   }
-  // the caller's branch is enqueued first: launched from the host one by
-  // one, its few large kernels then start while the side's many small ones
-  // are still being enqueued
-  const hipError_t e = hipEventRecord(ss->fork, s);
+  hipError_t e = hipEventRecord(ss->fork, s);
   if (e != hipSuccess) return hip_fail(e, "fork to the side stream");
-  const fno_status st_main = main_part();
-  const hipError_t ef = hipStreamWaitEvent(ss->s, ss->fork, 0);
-  const fno_status st_side = ef == hipSuccess ? side(ss->s) : FNO_OK;
+  if ((st = first()) != FNO_OK) return st;  // nothing waits on the fork yet
+  e = hipEventRecord(ss->fork2, s);
+  if (e != hipSuccess) return hip_fail(e, "fork to the side stream");
+  const fno_status st_main = second();
+  hipError_t ef = hipStreamWaitEvent(ss->s, ss->fork, 0);
+  fno_status st_side = ef == hipSuccess ? side_a(ss->s) : FNO_OK;
+  if (ef == hipSuccess && st_side == FNO_OK) {
+    ef = hipStreamWaitEvent(ss->s, ss->fork2, 0);
+    if (ef == hipSuccess) st_side = side_b(ss->s);
+  }
   const hipError_t ej = ef == hipSuccess ? hipEventRecord(ss->join, ss->s) : ef;
   const hipError_t ew = ej == hipSuccess ? hipStreamWaitEvent(s, ss->join, 0) : ej;
   if (st_side != FNO_OK) return st_side;
   if (st_main != FNO_OK) return st_main;
-  return ew == hipSuccess ? FNO_OK : hip_fail(ew, "join of the side stream");
+  return ew == hipSuccess ? FNO_OK : hip_fail(ew, "side stream");
 }
 
 // The forward call.  build_plan = false: the plan must already exist (no
@@ -2066,18 +2095,22 @@ fno_status fno_spectral_conv_bwd(const fno_conv_desc* d, const void* x, const fn
     char* inter = wsd + Ld.add(std::max(inter3d_bytes(g, g.Cin), inter3d_bytes(g, g.Cout)));
     char* tsc = wsd + Ld.total;
     double* bounds = (double*)(wsd + ws_core(d, pl, FNO_OP_BWD_DATA, true));
-    if ((st = run_sigma_stats(pl, x, bounds, s)) != FNO_OK) return st;
-    if ((st = run_r2c(pl, gy, gh, inter, g.Cout, 0, 1, s)) != FNO_OK) return st;
-    const void* xh = x_hat;
-    if (!cache) {
-      if ((st = run_r2c(pl, x, xs, inter, g.Cin, 1, 0, s, bounds)) != FNO_OK) return st;
-      xh = xs;
-    }
-    // The weight gradient reads only the two spectra and the weights and
-    // writes only its own scratch and gw: it runs beside the data part.
-    auto weight_part = [&](hipStream_t st_) {
-      return d->weight_kind == FNO_WEIGHT_CP ? run_cp_wgrad(d, pl, xh, gh, w, gw, wsw, st_)
-                                             : run_tucker_wgrad(d, pl, xh, gh, w, gw, wsw, st_);
+    const void* xh = x_hat ? x_hat : (const void*)xs;
+    // The weight gradient writes only its own scratch and gw; its steps
+    // that read only the weights run beside the transforms of gy (and x),
+    // the rest beside the adjoint path and the inverse transform.
+    auto weight_part = [&](int phases) {
+      return [&, phases](hipStream_t st_) {
+        return d->weight_kind == FNO_WEIGHT_CP
+                   ? run_cp_wgrad(d, pl, xh, gh, w, gw, wsw, st_, nullptr, phases)
+                   : run_tucker_wgrad(d, pl, xh, gh, w, gw, wsw, st_, nullptr, phases);
+      };
+    };
+    auto spectra = [&]() -> fno_status {
+      fno_status r = run_sigma_stats(pl, x, bounds, s);
+      if (r == FNO_OK) r = run_r2c(pl, gy, gh, inter, g.Cout, 0, 1, s);
+      if (r == FNO_OK && !cache) r = run_r2c(pl, x, xs, inter, g.Cin, 1, 0, s, bounds);
+      return r;
     };
     auto data_part = [&]() -> fno_status {
       fno_status r = run_tucker_path(d, pl, true, gh, w, gxs, tsc, s);
@@ -2085,7 +2118,7 @@ fno_status fno_spectral_conv_bwd(const fno_conv_desc* d, const void* x, const fn
       const float sc = (float)(1.0 / std::sqrt((double)g.N));
       return run_c2r(pl, gxs, gx, inter, g.Cin, sc, pre_on ? x : nullptr, s, bounds);
     };
-    return run_forked(s, weight_part, data_part);
+    return run_forked(s, weight_part(WG_WEIGHTS), spectra, weight_part(WG_SPECTRA), data_part);
   }
   // dense: the data part's regions inside wsd, laid out as in bwd_data (its
   // first region, the gradient spectrum, is unused: gh holds it)
