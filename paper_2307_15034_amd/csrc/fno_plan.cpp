@@ -1339,9 +1339,33 @@ fno_status run_pair(const Sizes& sz, const Opnd& A0, const Opnd& B0, const std::
 
 // Evaluate a Tucker or CP path: operands [spec, core (CP: lambda), u_in,
 // u_out, u_1..u_d].
+// Which steps of a factorised path a call runs: all of them; only those
+// whose operands all come from the weights (no spectrum), which then take no
+// split-K partial sums so that they may run beside the other steps; or the
+// others, the first of them that reads a weights-only result waiting for the
+// event `ready` (recorded after the weights-only steps on their stream).
+enum PathSteps { PATH_ALL = 0, PATH_WEIGHTS = 1, PATH_REST = 2 };
+
+// Whether a path has a step of the weights alone (operand 0 is the spectrum).
+bool path_has_weight_steps(const std::vector<PStep>& path, size_t nops) {
+  std::vector<char> wonly(nops, 1);
+  wonly[0] = 0;
+  for (const PStep& ps : path) {
+    const char both = wonly[ps.p] && wonly[ps.q];
+    if (both) return true;
+    std::vector<char> next;
+    for (int k = 0; k < (int)wonly.size(); ++k)
+      if (k != ps.p && k != ps.q) next.push_back(wonly[k]);
+    next.push_back(both);
+    wonly.swap(next);
+  }
+  return false;
+}
+
 fno_status run_tucker_path(const fno_conv_desc* d, const Plan* pl, bool adjoint,
                            const void* spec, const fno_weights* w, void* out_spec,
-                           char* scratch, hipStream_t s) {
+                           char* scratch, hipStream_t s, int which = PATH_ALL,
+                           hipEvent_t ready = nullptr) {
   const Geo& g = pl->g;
   Sizes sz = weight_sizes(d);
   const std::vector<PStep>& path = adjoint ? pl->path_adj : pl->path_fwd;
@@ -1361,9 +1385,24 @@ fno_status run_tucker_path(const fno_conv_desc* d, const Plan* pl, bool adjoint,
   void* part = scratch;
   size_t off = kPairPartBytes;
   const char clast = kSpatial[d->ndim - 1];
+  // per operand: derived from the weights alone; produced by a weights-only
+  // step (on the other stream when which == PATH_REST)
+  std::vector<char> wonly(ops.size(), 1), made(ops.size(), 0);
+  wonly[0] = 0;
+  bool waited = ready == nullptr || which != PATH_REST;
+  struct Join {  // the wait is enqueued on every way out
+    bool& done;
+    hipEvent_t ev;
+    hipStream_t st;
+    ~Join() {
+      if (!done) (void)hipStreamWaitEvent(st, ev, 0);
+    }
+  } join{waited, ready, s};
   for (size_t st = 0; st < path.size(); ++st) {
     const PStep& ps = path[st];
     const bool last = st + 1 == path.size();
+    const char wstep = wonly[ps.p] && wonly[ps.q];
+    const bool run = which == PATH_ALL || (which == PATH_WEIGHTS) == (wstep != 0);
     void* dst;
     int oelem;
     if (last) {
@@ -1387,14 +1426,30 @@ fno_status run_tucker_path(const fno_conv_desc* d, const Plan* pl, bool adjoint,
         store += clast;
       }
     }
-    fno_status r = run_pair(sz, ops[ps.p], ops[ps.q], store, dst, oelem, 1.0f,
-                            last ? clast : 0, g.Nb, s, part);
-    if (r != FNO_OK) return r;
+    if (run) {
+      if (!waited && (made[ps.p] || made[ps.q])) {
+        const hipError_t e = hipStreamWaitEvent(s, ready, 0);
+        waited = true;
+        if (e != hipSuccess) return hip_fail(e, "wait for the weights-only steps");
+      }
+      fno_status r = run_pair(sz, ops[ps.p], ops[ps.q], store, dst, oelem, 1.0f,
+                              last ? clast : 0, g.Nb, s, which == PATH_WEIGHTS ? nullptr : part);
+      if (r != FNO_OK) return r;
+    }
     std::vector<Opnd> next;
+    std::vector<char> nw, nm;
     for (int k = 0; k < (int)ops.size(); ++k)
-      if (k != ps.p && k != ps.q) next.push_back(ops[k]);
+      if (k != ps.p && k != ps.q) {
+        next.push_back(ops[k]);
+        nw.push_back(wonly[k]);
+        nm.push_back(made[k]);
+      }
     next.push_back({dst, store, oelem, 0});
+    nw.push_back(wstep);
+    nm.push_back(wstep);
     ops.swap(next);
+    wonly.swap(nw);
+    made.swap(nm);
   }
   return FNO_OK;
 }
@@ -1709,7 +1764,7 @@ hipError_t timed_launch(const char* name, hipStream_t s, hipError_t (*launch)(vo
 // on first use outside a stream capture and kept until the process ends.
 struct SideStream {
   hipStream_t s = nullptr;
-  hipEvent_t fork = nullptr, fork2 = nullptr, join = nullptr;
+  hipEvent_t fork = nullptr, fork2 = nullptr, join = nullptr, ready = nullptr;
 };
 std::mutex g_side_mutex;
 std::map<int, SideStream> g_side;
@@ -1726,7 +1781,7 @@ SideStream* side_stream_locked(hipStream_t s) {
   if (hipStreamIsCapturing(s, &cs) != hipSuccess || cs != hipStreamCaptureStatusNone) return nullptr;
   SideStream ss;
   if (hipStreamCreateWithFlags(&ss.s, hipStreamNonBlocking) != hipSuccess) return nullptr;
-  hipEvent_t* ev[3] = {&ss.fork, &ss.fork2, &ss.join};
+  hipEvent_t* ev[4] = {&ss.fork, &ss.fork2, &ss.join, &ss.ready};
   for (hipEvent_t* e : ev) {
     if (hipEventCreateWithFlags(e, hipEventDisableTiming) != hipSuccess) {
       for (hipEvent_t* f : ev)
@@ -1739,13 +1794,15 @@ SideStream* side_stream_locked(hipStream_t s) {
 }
 
 // Two branches after the work already on `s`: on the caller's stream
-// first() then second(); on the side stream side_a(stream), which reads
-// nothing first() writes, and then side_b(stream), which reads first()'s
-// results and nothing second() writes.  Everything enqueued on `s`
-// afterwards follows both branches; the join is enqueued whatever the
-// branches return.  The caller's work is enqueued before the side's, so
-// that, launched from the host one by one, its few large kernels start
-// while the side's many small ones are still being enqueued.
+// first() then second(side); on the side stream side_a(side, stream), which
+// reads nothing first() writes, and then side_b(stream), which reads
+// first()'s results and nothing second() writes (second may wait for an
+// event side_a records on the side stream; side is null when everything
+// runs on `s`).  Everything enqueued on `s` afterwards follows both
+// branches; the join is enqueued whatever the branches return.  Each part
+// of the caller's work is enqueued before the side's, so that, launched
+// from the host one by one, its few large kernels start while the side's
+// many small ones are still being enqueued.
 template <typename FA, typename F1, typename FB, typename F2>
 fno_status run_forked(hipStream_t s, FA side_a, F1 first, FB side_b, F2 second) {
   std::unique_lock<std::mutex> lk(g_side_mutex);
@@ -1753,7 +1810,8 @@ fno_status run_forked(hipStream_t s, FA side_a, F1 first, FB side_b, F2 second) 
   fno_status st;
   if (!ss) {
     lk.unlock();
-    if ((st = first()) != FNO_OK || (st = second()) != FNO_OK || (st = side_a(s)) != FNO_OK)
+    if ((st = first()) != FNO_OK || (st = second(nullptr)) != FNO_OK ||
+        (st = side_a(nullptr, s)) != FNO_OK)
       return st;
     return side_b(s);
   }
@@ -1762,9 +1820,10 @@ fno_status run_forked(hipStream_t s, FA side_a, F1 first, FB side_b, F2 second) 
   if ((st = first()) != FNO_OK) return st;  // nothing waits on the fork yet
   e = hipEventRecord(ss->fork2, s);
   if (e != hipSuccess) return hip_fail(e, "fork to the side stream");
-  const fno_status st_main = second();
+  // side_a before second(): second() may wait on an event side_a records
   hipError_t ef = hipStreamWaitEvent(ss->s, ss->fork, 0);
-  fno_status st_side = ef == hipSuccess ? side_a(ss->s) : FNO_OK;
+  fno_status st_side = ef == hipSuccess ? side_a(ss, ss->s) : FNO_OK;
+  const fno_status st_main = second(ef == hipSuccess ? ss : nullptr);
   if (ef == hipSuccess && st_side == FNO_OK) {
     ef = hipStreamWaitEvent(ss->s, ss->fork2, 0);
     if (ef == hipSuccess) st_side = side_b(ss->s);
@@ -1774,6 +1833,57 @@ fno_status run_forked(hipStream_t s, FA side_a, F1 first, FB side_b, F2 second) 
   if (st_side != FNO_OK) return st_side;
   if (st_main != FNO_OK) return st_main;
   return ew == hipSuccess ? FNO_OK : hip_fail(ew, "side stream");
+}
+
+// The weights-only steps of a factorised path on the side stream (recording
+// ss->ready after them) when there are any; returns the event the rest of
+// the path waits for, or null (then the caller's stream runs every step).
+hipEvent_t path_weights_on_side(const fno_conv_desc* d, const Plan* pl, bool adjoint,
+                                const fno_weights* w, char* scratch, SideStream* ss,
+                                fno_status* st) {
+  *st = FNO_OK;
+  const std::vector<PStep>& path = adjoint ? pl->path_adj : pl->path_fwd;
+  if (!ss || !path_has_weight_steps(path, 4 + (size_t)d->ndim)) return nullptr;
+  *st = run_tucker_path(d, pl, adjoint, nullptr, w, nullptr, scratch, ss->s, PATH_WEIGHTS);
+  const hipError_t e = hipEventRecord(ss->ready, ss->s);
+  if (*st == FNO_OK && e != hipSuccess) *st = hip_fail(e, "side stream event");
+  return *st == FNO_OK ? ss->ready : nullptr;
+}
+
+// A factorised path after its input transform(s): first() (the transforms)
+// on the caller's stream, the path's weights-only steps on the side stream
+// beside them, then the other steps on the caller's stream, waiting for the
+// side before the first step that reads its results.  Everything on one
+// stream when `allow_side` is false or the path has no weights-only step.
+template <typename F1>
+fno_status run_path_forked(const fno_conv_desc* d, const Plan* pl, bool adjoint,
+                           const void* spec, const fno_weights* w, void* out, char* tsc,
+                           hipStream_t s, bool allow_side, F1 first) {
+  const std::vector<PStep>& path = adjoint ? pl->path_adj : pl->path_fwd;
+  std::unique_lock<std::mutex> lk(g_side_mutex, std::defer_lock);
+  SideStream* ss = nullptr;
+  if (allow_side && path_has_weight_steps(path, 4 + (size_t)d->ndim)) {
+    lk.lock();
+    ss = side_stream_locked(s);
+    if (!ss) lk.unlock();
+  }
+  hipError_t e = ss ? hipEventRecord(ss->fork, s) : hipSuccess;
+  if (e != hipSuccess) return hip_fail(e, "fork to the side stream");
+  fno_status st = first();
+  if (st != FNO_OK) return st;  // nothing waits on the fork yet
+  hipEvent_t ready = nullptr;
+  if (ss) {
+    e = hipStreamWaitEvent(ss->s, ss->fork, 0);
+    if (e != hipSuccess) return hip_fail(e, "fork to the side stream");
+    ready = path_weights_on_side(d, pl, adjoint, w, tsc, ss, &st);
+    if (st != FNO_OK) {  // the side joins the caller's stream all the same
+      if (hipEventRecord(ss->join, ss->s) == hipSuccess)
+        (void)hipStreamWaitEvent(s, ss->join, 0);
+      return st;
+    }
+  }
+  return run_tucker_path(d, pl, adjoint, spec, w, out, tsc, s, ready ? PATH_REST : PATH_ALL,
+                         ready);
 }
 
 // The forward call.  build_plan = false: the plan must already exist (no
@@ -1807,12 +1917,17 @@ fno_status fwd_impl(const fno_conv_desc* d, const void* x, const fno_weights* w,
     explicit Flag(bool on) : prev(g_no_alloc_call) { g_no_alloc_call = on; }
     ~Flag() { g_no_alloc_call = prev; }
   } flag(!build_plan);
-  if ((st = run_sigma_stats(pl, x, bounds, s)) != FNO_OK) return st;
-  if ((st = run_r2c(pl, x, xh, inter, g.Cin, 1, 0, s, bounds)) != FNO_OK) return st;
+  auto spectra = [&]() -> fno_status {
+    fno_status r = run_sigma_stats(pl, x, bounds, s);
+    return r != FNO_OK ? r : run_r2c(pl, x, xh, inter, g.Cin, 1, 0, s, bounds);
+  };
   if (d->weight_kind == FNO_WEIGHT_DENSE) {
+    if ((st = spectra()) != FNO_OK) return st;
     if ((st = run_contract(pl, xh, w->dense, ys, false, s)) != FNO_OK) return st;
   } else {
-    if ((st = run_tucker_path(d, pl, false, xh, w, ys, tsc, s)) != FNO_OK) return st;
+    // (the allocation-free call keeps to the caller's stream)
+    st = run_path_forked(d, pl, false, xh, w, ys, tsc, s, build_plan, spectra);
+    if (st != FNO_OK) return st;
   }
   return run_c2r(pl, ys, y, inter, g.Cout, 1.0f, nullptr, s);
 }
@@ -1972,12 +2087,16 @@ fno_status fno_spectral_conv_bwd_data(const fno_conv_desc* d, const void* x,
   char* tsc = base + L.total;
   double* bounds = (double*)(base + ws_core(d, pl, FNO_OP_BWD_DATA, true));
   void* gh = gy_hat_out ? gy_hat_out : (void*)gs;
-  if ((st = run_sigma_stats(pl, x, bounds, s)) != FNO_OK) return st;
-  if ((st = run_r2c(pl, gy, gh, inter, g.Cout, 0, 1, s)) != FNO_OK) return st;
+  auto spectra = [&]() -> fno_status {
+    fno_status r = run_sigma_stats(pl, x, bounds, s);
+    return r != FNO_OK ? r : run_r2c(pl, gy, gh, inter, g.Cout, 0, 1, s);
+  };
   if (d->weight_kind == FNO_WEIGHT_DENSE) {
+    if ((st = spectra()) != FNO_OK) return st;
     if ((st = run_contract(pl, gh, w->dense, gxs, true, s)) != FNO_OK) return st;
   } else {
-    if ((st = run_tucker_path(d, pl, true, gh, w, gxs, tsc, s)) != FNO_OK) return st;
+    if ((st = run_path_forked(d, pl, true, gh, w, gxs, tsc, s, true, spectra)) != FNO_OK)
+      return st;
   }
   const float sc = (float)(1.0 / std::sqrt((double)g.N));
   return run_c2r(pl, gxs, gx, inter, g.Cin, sc, pre_on ? x : nullptr, s, bounds);
@@ -2099,26 +2218,34 @@ fno_status fno_spectral_conv_bwd(const fno_conv_desc* d, const void* x, const fn
     // The weight gradient writes only its own scratch and gw; its steps
     // that read only the weights run beside the transforms of gy (and x),
     // the rest beside the adjoint path and the inverse transform.
-    auto weight_part = [&](int phases) {
-      return [&, phases](hipStream_t st_) {
-        return d->weight_kind == FNO_WEIGHT_CP
-                   ? run_cp_wgrad(d, pl, xh, gh, w, gw, wsw, st_, nullptr, phases)
-                   : run_tucker_wgrad(d, pl, xh, gh, w, gw, wsw, st_, nullptr, phases);
-      };
+    auto wgrad = [&](int phases, hipStream_t st_) {
+      return d->weight_kind == FNO_WEIGHT_CP
+                 ? run_cp_wgrad(d, pl, xh, gh, w, gw, wsw, st_, nullptr, phases)
+                 : run_tucker_wgrad(d, pl, xh, gh, w, gw, wsw, st_, nullptr, phases);
     };
+    // the side first takes the adjoint path's weights-only steps, which the
+    // caller's stream waits for before the first step that reads them
+    hipEvent_t ready = nullptr;
+    auto side_a = [&](SideStream* ss, hipStream_t st_) {
+      fno_status r;
+      ready = path_weights_on_side(d, pl, true, w, tsc, ss, &r);
+      return r != FNO_OK ? r : wgrad(WG_WEIGHTS, st_);
+    };
+    auto side_b = [&](hipStream_t st_) { return wgrad(WG_SPECTRA, st_); };
     auto spectra = [&]() -> fno_status {
       fno_status r = run_sigma_stats(pl, x, bounds, s);
       if (r == FNO_OK) r = run_r2c(pl, gy, gh, inter, g.Cout, 0, 1, s);
       if (r == FNO_OK && !cache) r = run_r2c(pl, x, xs, inter, g.Cin, 1, 0, s, bounds);
       return r;
     };
-    auto data_part = [&]() -> fno_status {
-      fno_status r = run_tucker_path(d, pl, true, gh, w, gxs, tsc, s);
+    auto data_part = [&](SideStream*) -> fno_status {
+      fno_status r = run_tucker_path(d, pl, true, gh, w, gxs, tsc, s,
+                                     ready ? PATH_REST : PATH_ALL, ready);
       if (r != FNO_OK) return r;
       const float sc = (float)(1.0 / std::sqrt((double)g.N));
       return run_c2r(pl, gxs, gx, inter, g.Cin, sc, pre_on ? x : nullptr, s, bounds);
     };
-    return run_forked(s, weight_part(WG_WEIGHTS), spectra, weight_part(WG_SPECTRA), data_part);
+    return run_forked(s, side_a, spectra, side_b, data_part);
   }
   // dense: the data part's regions inside wsd, laid out as in bwd_data (its
   // first region, the gradient spectrum, is unused: gh holds it)
