@@ -1454,28 +1454,72 @@ fno_status run_tucker_path(const fno_conv_desc* d, const Plan* pl, bool adjoint,
   return FNO_OK;
 }
 
-// Fixed schedule of the Tucker weight gradient (chain rule through the
-// multilinear map): P = conj(Xhat u_in), Q = sqrt(N) c G conj(u_out),
-// R = sum_b P Q, S = core x u_1 .. x u_d; g_core = R x conj(u_j)...,
-// g_u_j = R . conj(core x_{q != j} u_q), g_u_in = conj(Xhat) . (Q conj S),
-// g_u_out = (sqrt(N) c G) . (P conj S).
 // Phases of the factorised weight gradients: the steps that read only the
 // weights (partial products of the core and the mode factors), and the
 // steps that read the spectra.  Every phase lays out the scratch the same
 // way, so the two may run as separate calls in order.
 constexpr int WG_WEIGHTS = 1, WG_SPECTRA = 2, WG_ALL = 3;
 
+// Extra streams of the spectrum phase.  After P and Q the chains of R (the
+// core and mode-factor gradients), Z1 (g_u_in) and Z2 (g_u_out) read
+// nothing the others write; with two more streams given, the Z1 and Z2
+// chains run on them beside the R chain (forked on event pq after P and Q,
+// joined back by d1 and d2).  Each chain has split-K partial sums of its
+// own at the start of the scratch.
+struct WgradBranches {
+  hipStream_t z1, z2;
+  hipEvent_t pq, d1, d2;
+};
+constexpr int kWgradChains = 3;
+
+// Runs the Z1 and Z2 chains of a weight gradient on the streams of `br`
+// (after the work already on s), or on s itself when br is null; joins them
+// back to s when it goes out of scope.
+struct WgradFork {
+  hipStream_t s, z1, z2;
+  const WgradBranches* br = nullptr;
+  WgradFork(hipStream_t s_) : s(s_), z1(s_), z2(s_) {}
+  fno_status fork(const WgradBranches* b) {
+    if (!b) return FNO_OK;
+    hipError_t e = hipEventRecord(b->pq, s);
+    if (e == hipSuccess) e = hipStreamWaitEvent(b->z1, b->pq, 0);
+    if (e != hipSuccess) return hip_fail(e, "fork of the weight-gradient chains");
+    br = b;
+    z1 = b->z1;
+    e = hipStreamWaitEvent(b->z2, b->pq, 0);
+    if (e != hipSuccess) return hip_fail(e, "fork of the weight-gradient chains");
+    z2 = b->z2;
+    return FNO_OK;
+  }
+  ~WgradFork() {
+    if (z1 != s && hipEventRecord(br->d1, z1) == hipSuccess) (void)hipStreamWaitEvent(s, br->d1, 0);
+    if (z2 != s && hipEventRecord(br->d2, z2) == hipSuccess) (void)hipStreamWaitEvent(s, br->d2, 0);
+  }
+  // split-K partial sums of the chain a step runs in
+  char* part(char* scratch, hipStream_t st) const {
+    return scratch + (st == z1 && z1 != s ? 1 : st == z2 && z2 != s ? 2 : 0) * kPairPartBytes;
+  }
+};
+
+// Fixed schedule of the Tucker weight gradient (chain rule through the
+// multilinear map): P = conj(Xhat u_in), Q = sqrt(N) c G conj(u_out),
+// R = sum_b P Q, S = core x u_1 .. x u_d; g_core = R x conj(u_j)...,
+// g_u_j = R . conj(core x_{q != j} u_q), g_u_in = conj(Xhat) . (Q conj S),
+// g_u_out = (sqrt(N) c G) . (P conj S).  The weights-only steps (C_j, S)
+// come first, then P and Q, then the three chains.
 fno_status run_tucker_wgrad(const fno_conv_desc* d, const Plan* pl, const void* xh,
                             const void* gh, const fno_weights* w, fno_weight_grads* gw,
                             char* scratch, hipStream_t s, size_t* scratch_used = nullptr,
-                            int phases = WG_ALL) {
+                            int phases = WG_ALL, const WgradBranches* br = nullptr) {
   const bool dry = scratch_used != nullptr;
-  int phase = WG_SPECTRA;  // the phase of the steps that follow
+  int phase = WG_WEIGHTS;  // the phase of the steps that follow
+  WgradFork fk(s);
   auto run_pair = [&](const Sizes& sz_, const Opnd& A, const Opnd& Bo, const std::string& res,
                       void* out, int out_elem, float scale, int c_axis_char, int Nb,
                       hipStream_t st) -> fno_status {
     if (dry || !(phases & phase)) return FNO_OK;
-    return fno::run_pair(sz_, A, Bo, res, out, out_elem, scale, c_axis_char, Nb, st, scratch);
+    return fno::run_pair(sz_, A, Bo, res, out, out_elem, scale, c_axis_char, Nb, st,
+                         fk.part(scratch, st));
   };
   const Geo& g = pl->g;
   const int nd = d->ndim;
@@ -1487,7 +1531,7 @@ fno_status run_tucker_wgrad(const fno_conv_desc* d, const Plan* pl, const void* 
   }
   const char clast = kSpatial[nd - 1];
   const float sqN = (float)std::sqrt((double)g.N);
-  size_t off = kPairPartBytes;  // split-K partial sums at the start
+  size_t off = kWgradChains * kPairPartBytes;  // split-K partial sums at the start
   auto buf = [&](const std::string& lab) {
     void* p = scratch + off;
     off += (size_t)round_up(label_size(lab, sz) * 8, 256);
@@ -1499,17 +1543,70 @@ fno_status run_tucker_wgrad(const fno_conv_desc* d, const Plan* pl, const void* 
   auto Wt = [&](const void* p, const std::string& lab, int conj) {
     return Opnd{p, lab, g.elem, conj};
   };
+  auto U = [&](int j, int conj) {
+    return Wt(w->u_mode[j], std::string(1, kSpatial[j]) + kRank[j], conj);
+  };
   fno_status r;
+  // ---- weights only ----
+  // per-axis partial cores C_j = core x_{q != j} u_q, labels (a,e, r_j, sp\j)
+  std::vector<Opnd> cj(nd);
+  for (int j = 0; j < nd; ++j) {
+    Opnd cur = Wt(w->core, "ae" + rk, 0);
+    std::string lab = "ae" + rk;
+    for (int q = 0; q < nd; ++q) {
+      if (q == j) continue;
+      std::string nl;
+      for (char c : lab) nl += (c == kRank[q]) ? kSpatial[q] : c;
+      void* dst = buf(nl);
+      if ((r = run_pair(sz, cur, U(q, 0), nl, dst, ELEM_F32, 1.0f, 0, g.Nb, s))) return r;
+      cur = F(dst, nl, 0);
+      lab = nl;
+    }
+    cj[j] = Opnd{cur.ptr, cur.lab, cur.elem, 1};  // conjugated where it is read
+  }
+  // S[a,e,sp] = core x all u_j
+  const std::string lS = "ae" + sp;
+  void* S;
+  {
+    Opnd cur = Wt(w->core, "ae" + rk, 0);
+    std::string lab = "ae" + rk;
+    for (int q = 0; q < nd; ++q) {
+      std::string nl;
+      for (char c : lab) nl += (c == kRank[q]) ? kSpatial[q] : c;
+      void* dst = buf(nl);
+      if ((r = run_pair(sz, cur, U(q, 0), nl, dst, ELEM_F32, 1.0f, 0, g.Nb, s))) return r;
+      cur = F(dst, nl, 0);
+      lab = nl;
+    }
+    S = const_cast<void*>(cur.ptr);
+  }
+  // ---- spectra ----
+  phase = WG_SPECTRA;
   const std::string lP = "ba" + sp, lQ = "be" + sp, lR = "ae" + sp;
   void* P = buf(lP);
   void* Q = buf(lQ);
   void* Rb = buf(lR);
+  void* Z1 = buf("ba" + sp);
+  void* Z2 = buf("be" + sp);
   // P[b,a,sp] = sum_i conj(Xhat[b,i,sp]) conj(u_in[i,a])
   r = run_pair(sz, Wt(xh, "bi" + sp, 1), Wt(w->u_in, "ia", 1), lP, P, ELEM_F32, 1.0f, 0, g.Nb, s);
   if (r) return r;
   // Q[b,e,sp] = sqrt(N) c(t) sum_o G[b,o,sp] conj(u_out[o,e])
   r = run_pair(sz, Wt(gh, "bo" + sp, 0), Wt(w->u_out, "oe", 1), lQ, Q, ELEM_F32, sqN, clast,
                g.Nb, s);
+  if (r) return r;
+  if (!dry && (phases & WG_SPECTRA) && (r = fk.fork(br))) return r;
+  // Z1[b,a,sp] = sum_e Q[b,e,sp] conj(S[a,e,sp]);  g_u_in = sum conj(Xhat) Z1
+  r = run_pair(sz, F(Q, lQ, 0), F(S, lS, 1), "ba" + sp, Z1, ELEM_F32, 1.0f, 0, g.Nb, fk.z1);
+  if (r) return r;
+  r = run_pair(sz, Wt(xh, "bi" + sp, 1), F(Z1, "ba" + sp, 0), "ia", gw->u_in, ELEM_F32, 1.0f, 0,
+               g.Nb, fk.z1);
+  if (r) return r;
+  // Z2[b,e,sp] = sqrt(N) c(t) sum_a P[b,a,sp] conj(S[a,e,sp]); g_u_out = sum G Z2
+  r = run_pair(sz, F(P, lP, 0), F(S, lS, 1), "be" + sp, Z2, ELEM_F32, sqN, clast, g.Nb, fk.z2);
+  if (r) return r;
+  r = run_pair(sz, Wt(gh, "bo" + sp, 0), F(Z2, "be" + sp, 0), "oe", gw->u_out, ELEM_F32, 1.0f,
+               0, g.Nb, fk.z2);
   if (r) return r;
   // R[a,e,sp] = sum_b P Q
   r = run_pair(sz, F(P, lP, 0), F(Q, lQ, 0), lR, Rb, ELEM_F32, 1.0f, 0, g.Nb, s);
@@ -1525,72 +1622,17 @@ fno_status run_tucker_wgrad(const fno_conv_desc* d, const Plan* pl, const void* 
       void* dst = last ? gw->core : buf(nl);
       // reorder the final result to (a, e, rk)
       std::string res = last ? ("ae" + rk) : nl;
-      r = run_pair(sz, cur, Wt(w->u_mode[j], std::string(1, kSpatial[j]) + kRank[j], 1), res,
-                   dst, ELEM_F32, 1.0f, 0, g.Nb, s);
-      if (r) return r;
+      if ((r = run_pair(sz, cur, U(j, 1), res, dst, ELEM_F32, 1.0f, 0, g.Nb, s))) return r;
       cur = F(dst, res, 0);
       lab = res;
     }
   }
-  // Per-axis partial cores C_j = core x_{q != j} u_q, labels (a,e, r_j, sp\j)
+  // g_u_j[x_j, r_j] = sum R[a,e,sp] conj(C_j[a,e,.., r_j, ..])
   for (int j = 0; j < nd; ++j) {
-    Opnd cur = Wt(w->core, "ae" + rk, 0);
-    std::string lab = "ae" + rk;
-    bool first = true;
-    phase = WG_WEIGHTS;
-    for (int q = 0; q < nd; ++q) {
-      if (q == j) continue;
-      std::string nl;
-      for (char c : lab) nl += (c == kRank[q]) ? kSpatial[q] : c;
-      void* dst = buf(nl);
-      r = run_pair(sz, cur, Wt(w->u_mode[q], std::string(1, kSpatial[q]) + kRank[q], 0), nl,
-                   dst, ELEM_F32, 1.0f, 0, g.Nb, s);
-      if (r) return r;
-      cur = F(dst, nl, 0);
-      lab = nl;
-      first = false;
-    }
-    phase = WG_SPECTRA;
-    // g_u_j[x_j, r_j] = sum R[a,e,sp] conj(C_j[a,e,.., r_j, ..])
     std::string res = std::string(1, kSpatial[j]) + kRank[j];
-    Opnd cj = first ? Wt(w->core, "ae" + rk, 1) : Opnd{cur.ptr, cur.lab, cur.elem, 1};
-    r = run_pair(sz, F(Rb, lR, 0), cj, res, gw->u_mode[j], ELEM_F32, 1.0f, 0, g.Nb, s);
-    if (r) return r;
+    if ((r = run_pair(sz, F(Rb, lR, 0), cj[j], res, gw->u_mode[j], ELEM_F32, 1.0f, 0, g.Nb, s)))
+      return r;
   }
-  // S[a,e,sp] = core x all u_j
-  void* S;
-  phase = WG_WEIGHTS;
-  {
-    Opnd cur = Wt(w->core, "ae" + rk, 0);
-    std::string lab = "ae" + rk;
-    for (int q = 0; q < nd; ++q) {
-      std::string nl;
-      for (char c : lab) nl += (c == kRank[q]) ? kSpatial[q] : c;
-      void* dst = buf(nl);
-      r = run_pair(sz, cur, Wt(w->u_mode[q], std::string(1, kSpatial[q]) + kRank[q], 0), nl,
-                   dst, ELEM_F32, 1.0f, 0, g.Nb, s);
-      if (r) return r;
-      cur = F(dst, nl, 0);
-      lab = nl;
-    }
-    S = const_cast<void*>(cur.ptr);
-  }
-  phase = WG_SPECTRA;
-  const std::string lS = "ae" + sp;
-  // Z1[b,a,sp] = sum_e Q[b,e,sp] conj(S[a,e,sp]);  g_u_in = sum conj(Xhat) Z1
-  void* Z1 = buf("ba" + sp);
-  r = run_pair(sz, F(Q, lQ, 0), F(S, lS, 1), "ba" + sp, Z1, ELEM_F32, 1.0f, 0, g.Nb, s);
-  if (r) return r;
-  r = run_pair(sz, Wt(xh, "bi" + sp, 1), F(Z1, "ba" + sp, 0), "ia", gw->u_in, ELEM_F32, 1.0f, 0,
-               g.Nb, s);
-  if (r) return r;
-  // Z2[b,e,sp] = sqrt(N) c(t) sum_a P[b,a,sp] conj(S[a,e,sp]); g_u_out = sum G Z2
-  void* Z2 = buf("be" + sp);
-  r = run_pair(sz, F(P, lP, 0), F(S, lS, 1), "be" + sp, Z2, ELEM_F32, sqN, clast, g.Nb, s);
-  if (r) return r;
-  r = run_pair(sz, Wt(gh, "bo" + sp, 0), F(Z2, "be" + sp, 0), "oe", gw->u_out, ELEM_F32, 1.0f,
-               0, g.Nb, s);
-  if (r) return r;
   if (dry) *scratch_used = off;
   return FNO_OK;
 }
@@ -1613,13 +1655,16 @@ size_t tucker_wgrad_bytes(const fno_conv_desc* d, const Plan* pl) {
 //   g_u_in = sum_{b,sp} conj(Xhat) (Q conj(S)),  g_u_out = sum_{b,sp} G' (P conj(S)).
 fno_status run_cp_wgrad(const fno_conv_desc* d, const Plan* pl, const void* xh, const void* gh,
                         const fno_weights* w, fno_weight_grads* gw, char* scratch,
-                        hipStream_t s, size_t* scratch_used = nullptr, int phases = WG_ALL) {
+                        hipStream_t s, size_t* scratch_used = nullptr, int phases = WG_ALL,
+                        const WgradBranches* br = nullptr) {
   const bool dry = scratch_used != nullptr;
-  int phase = WG_SPECTRA;  // the phase of the steps that follow
+  int phase = WG_WEIGHTS;  // the phase of the steps that follow
+  WgradFork fk(s);
   auto pair = [&](const Sizes& sz_, const Opnd& A, const Opnd& Bo, const std::string& res,
-                  void* out, float scale, int c_axis_char) -> fno_status {
+                  void* out, float scale, int c_axis_char, hipStream_t st) -> fno_status {
     if (dry || !(phases & phase)) return FNO_OK;
-    return run_pair(sz_, A, Bo, res, out, ELEM_F32, scale, c_axis_char, pl->g.Nb, s, scratch);
+    return run_pair(sz_, A, Bo, res, out, ELEM_F32, scale, c_axis_char, pl->g.Nb, st,
+                    fk.part(scratch, st));
   };
   const Geo& g = pl->g;
   const int nd = d->ndim;
@@ -1628,7 +1673,7 @@ fno_status run_cp_wgrad(const fno_conv_desc* d, const Plan* pl, const void* xh, 
   for (int j = 0; j < nd; ++j) sp += kSpatial[j];
   const char clast = kSpatial[nd - 1];
   const float sqN = (float)std::sqrt((double)g.N);
-  size_t off = kPairPartBytes;  // split-K partial sums at the start
+  size_t off = kWgradChains * kPairPartBytes;  // split-K partial sums at the start
   auto buf = [&](const std::string& lab) {
     void* p = scratch + off;
     off += (size_t)round_up(label_size(lab, sz) * 8, 256);
@@ -1642,13 +1687,36 @@ fno_status run_cp_wgrad(const fno_conv_desc* d, const Plan* pl, const void* xh, 
   };
   auto U = [&](int j, int conj) { return Wt(w->u_mode[j], std::string(1, kSpatial[j]) + "r", conj); };
   fno_status r;
+  // ---- weights only: S[r, sp] = lambda[r] prod_j u_j[sp_j, r] ----
+  Opnd S = Wt(w->core, "r", 0);
+  {
+    std::string lab = "r";
+    for (int j = 0; j < nd; ++j) {
+      const std::string nl = lab + kSpatial[j];
+      void* dst = buf(nl);
+      if ((r = pair(sz, S, U(j, 0), nl, dst, 1.0f, 0, s))) return r;
+      S = F(dst, nl, 0);
+      lab = nl;
+    }
+  }
+  const Opnd Sc{S.ptr, S.lab, S.elem, 1};
+  // ---- spectra ----
+  phase = WG_SPECTRA;
   const std::string lP = "br" + sp, lR = "r" + sp;
   void* P = buf(lP);
   void* Q = buf(lP);
   void* Rb = buf(lR);
-  if ((r = pair(sz, Wt(xh, "bi" + sp, 1), Wt(w->u_in, "ir", 1), lP, P, 1.0f, 0))) return r;
-  if ((r = pair(sz, Wt(gh, "bo" + sp, 0), Wt(w->u_out, "or", 1), lP, Q, sqN, clast))) return r;
-  if ((r = pair(sz, F(P, lP, 0), F(Q, lP, 0), lR, Rb, 1.0f, 0))) return r;
+  void* Z1 = buf(lP);
+  void* Z2 = buf(lP);
+  if ((r = pair(sz, Wt(xh, "bi" + sp, 1), Wt(w->u_in, "ir", 1), lP, P, 1.0f, 0, s))) return r;
+  if ((r = pair(sz, Wt(gh, "bo" + sp, 0), Wt(w->u_out, "or", 1), lP, Q, sqN, clast, s))) return r;
+  if (!dry && (phases & WG_SPECTRA) && (r = fk.fork(br))) return r;
+  if ((r = pair(sz, F(Q, lP, 0), Sc, lP, Z1, 1.0f, 0, fk.z1))) return r;
+  if ((r = pair(sz, Wt(xh, "bi" + sp, 1), F(Z1, lP, 0), "ir", gw->u_in, 1.0f, 0, fk.z1))) return r;
+  if ((r = pair(sz, F(P, lP, 0), Sc, lP, Z2, sqN, clast, fk.z2))) return r;
+  if ((r = pair(sz, Wt(gh, "bo" + sp, 0), F(Z2, lP, 0), "or", gw->u_out, 1.0f, 0, fk.z2)))
+    return r;
+  if ((r = pair(sz, F(P, lP, 0), F(Q, lP, 0), lR, Rb, 1.0f, 0, s))) return r;
   // g_lambda: contract R with conj(u_j) along every spatial axis
   {
     Opnd cur = F(Rb, lR, 0);
@@ -1659,7 +1727,7 @@ fno_status run_cp_wgrad(const fno_conv_desc* d, const Plan* pl, const void* xh, 
         if (c != kSpatial[j]) nl += c;
       const bool last = j == nd - 1;
       void* dst = last ? gw->core : buf(nl);
-      if ((r = pair(sz, cur, U(j, 1), nl, dst, 1.0f, 0))) return r;
+      if ((r = pair(sz, cur, U(j, 1), nl, dst, 1.0f, 0, s))) return r;
       cur = F(dst, nl, 0);
       lab = nl;
     }
@@ -1674,35 +1742,14 @@ fno_status run_cp_wgrad(const fno_conv_desc* d, const Plan* pl, const void* xh, 
       for (char c : lab)
         if (c != kSpatial[q]) nl += c;
       void* dst = buf(nl);
-      if ((r = pair(sz, cur, U(q, 1), nl, dst, 1.0f, 0))) return r;
+      if ((r = pair(sz, cur, U(q, 1), nl, dst, 1.0f, 0, s))) return r;
       cur = F(dst, nl, 0);
       lab = nl;
     }
     if ((r = pair(sz, cur, Wt(w->core, "r", 1), std::string(1, kSpatial[j]) + "r",
-                  gw->u_mode[j], 1.0f, 0)))
+                  gw->u_mode[j], 1.0f, 0, s)))
       return r;
   }
-  // S[r, sp] = lambda[r] prod_j u_j[sp_j, r]
-  Opnd S = Wt(w->core, "r", 0);
-  phase = WG_WEIGHTS;
-  {
-    std::string lab = "r";
-    for (int j = 0; j < nd; ++j) {
-      const std::string nl = lab + kSpatial[j];
-      void* dst = buf(nl);
-      if ((r = pair(sz, S, U(j, 0), nl, dst, 1.0f, 0))) return r;
-      S = F(dst, nl, 0);
-      lab = nl;
-    }
-  }
-  phase = WG_SPECTRA;
-  const Opnd Sc{S.ptr, S.lab, S.elem, 1};
-  void* Z1 = buf(lP);
-  if ((r = pair(sz, F(Q, lP, 0), Sc, lP, Z1, 1.0f, 0))) return r;
-  if ((r = pair(sz, Wt(xh, "bi" + sp, 1), F(Z1, lP, 0), "ir", gw->u_in, 1.0f, 0))) return r;
-  void* Z2 = buf(lP);
-  if ((r = pair(sz, F(P, lP, 0), Sc, lP, Z2, sqN, clast))) return r;
-  if ((r = pair(sz, Wt(gh, "bo" + sp, 0), F(Z2, lP, 0), "or", gw->u_out, 1.0f, 0))) return r;
   if (dry) *scratch_used = off;
   return FNO_OK;
 }
@@ -1765,9 +1812,19 @@ hipError_t timed_launch(const char* name, hipStream_t s, hipError_t (*launch)(vo
 struct SideStream {
   hipStream_t s = nullptr;
   hipEvent_t fork = nullptr, fork2 = nullptr, join = nullptr, ready = nullptr;
+  // the weight gradient's own two extra chains
+  hipStream_t z1 = nullptr, z2 = nullptr;
+  hipEvent_t pq = nullptr, d1 = nullptr, d2 = nullptr;
+  WgradBranches branches() const { return WgradBranches{z1, z2, pq, d1, d2}; }
 };
 std::mutex g_side_mutex;
 std::map<int, SideStream> g_side;
+
+// Whether work enqueued on `s` is being recorded into a graph.
+bool capturing(hipStream_t s) {
+  hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+  return hipStreamIsCapturing(s, &cs) != hipSuccess || cs != hipStreamCaptureStatusNone;
+}
 
 // The device's side stream, or null (the caller then runs both parts on its
 // own stream): when it cannot be created, or must not be because `s` is
@@ -1780,15 +1837,17 @@ SideStream* side_stream_locked(hipStream_t s) {
   hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
   if (hipStreamIsCapturing(s, &cs) != hipSuccess || cs != hipStreamCaptureStatusNone) return nullptr;
   SideStream ss;
-  if (hipStreamCreateWithFlags(&ss.s, hipStreamNonBlocking) != hipSuccess) return nullptr;
-  hipEvent_t* ev[4] = {&ss.fork, &ss.fork2, &ss.join, &ss.ready};
-  for (hipEvent_t* e : ev) {
-    if (hipEventCreateWithFlags(e, hipEventDisableTiming) != hipSuccess) {
-      for (hipEvent_t* f : ev)
-        if (*f) (void)hipEventDestroy(*f);
-      (void)hipStreamDestroy(ss.s);
-      return nullptr;
-    }
+  hipStream_t* st[3] = {&ss.s, &ss.z1, &ss.z2};
+  hipEvent_t* ev[7] = {&ss.fork, &ss.fork2, &ss.join, &ss.ready, &ss.pq, &ss.d1, &ss.d2};
+  bool ok = true;
+  for (hipStream_t* p : st) ok = ok && hipStreamCreateWithFlags(p, hipStreamNonBlocking) == hipSuccess;
+  for (hipEvent_t* e : ev) ok = ok && hipEventCreateWithFlags(e, hipEventDisableTiming) == hipSuccess;
+  if (!ok) {
+    for (hipEvent_t* e : ev)
+      if (*e) (void)hipEventDestroy(*e);
+    for (hipStream_t* p : st)
+      if (*p) (void)hipStreamDestroy(*p);
+    return nullptr;
   }
   return &(g_side[dev] = ss);
 }
@@ -2166,8 +2225,15 @@ fno_status fno_spectral_conv_bwd_weight(const fno_conv_desc* d, const void* x, c
     }));
     return FNO_OK;
   }
-  if (d->weight_kind == FNO_WEIGHT_CP) return run_cp_wgrad(d, pl, xh, gh, w, gw, tsc, s);
-  return run_tucker_wgrad(d, pl, xh, gh, w, gw, tsc, s);
+  // the chains after P and Q on the side streams when they exist
+  std::unique_lock<std::mutex> lk(g_side_mutex);
+  SideStream* ss = capturing(s) ? nullptr : side_stream_locked(s);
+  WgradBranches wb{};
+  if (ss) wb = ss->branches();
+  const WgradBranches* b = ss ? &wb : nullptr;
+  if (d->weight_kind == FNO_WEIGHT_CP)
+    return run_cp_wgrad(d, pl, xh, gh, w, gw, tsc, s, nullptr, WG_ALL, b);
+  return run_tucker_wgrad(d, pl, xh, gh, w, gw, tsc, s, nullptr, WG_ALL, b);
 }
 
 fno_status fno_spectral_conv_bwd(const fno_conv_desc* d, const void* x, const fno_weights* w,
@@ -2218,20 +2284,29 @@ fno_status fno_spectral_conv_bwd(const fno_conv_desc* d, const void* x, const fn
     // The weight gradient writes only its own scratch and gw; its steps
     // that read only the weights run beside the transforms of gy (and x),
     // the rest beside the adjoint path and the inverse transform.
-    auto wgrad = [&](int phases, hipStream_t st_) {
+    WgradBranches wb{};
+    auto wgrad = [&](int phases, hipStream_t st_, const WgradBranches* b) {
       return d->weight_kind == FNO_WEIGHT_CP
-                 ? run_cp_wgrad(d, pl, xh, gh, w, gw, wsw, st_, nullptr, phases)
-                 : run_tucker_wgrad(d, pl, xh, gh, w, gw, wsw, st_, nullptr, phases);
+                 ? run_cp_wgrad(d, pl, xh, gh, w, gw, wsw, st_, nullptr, phases, b)
+                 : run_tucker_wgrad(d, pl, xh, gh, w, gw, wsw, st_, nullptr, phases, b);
     };
     // the side first takes the adjoint path's weights-only steps, which the
     // caller's stream waits for before the first step that reads them
     hipEvent_t ready = nullptr;
+    const WgradBranches* pwb = nullptr;
     auto side_a = [&](SideStream* ss, hipStream_t st_) {
       fno_status r;
       ready = path_weights_on_side(d, pl, true, w, tsc, ss, &r);
-      return r != FNO_OK ? r : wgrad(WG_WEIGHTS, st_);
+      // the weight gradient's own extra chains only outside a stream
+      // capture: capturing that second-level fork ended the process inside
+      // the runtime's end-of-capture call, cause not found
+      if (ss && !capturing(s)) {
+        wb = ss->branches();
+        pwb = &wb;
+      }
+      return r != FNO_OK ? r : wgrad(WG_WEIGHTS, st_, nullptr);
     };
-    auto side_b = [&](hipStream_t st_) { return wgrad(WG_SPECTRA, st_); };
+    auto side_b = [&](hipStream_t st_) { return wgrad(WG_SPECTRA, st_, pwb); };
     auto spectra = [&]() -> fno_status {
       fno_status r = run_sigma_stats(pl, x, bounds, s);
       if (r == FNO_OK) r = run_r2c(pl, gy, gh, inter, g.Cout, 0, 1, s);
