@@ -552,6 +552,15 @@ __global__ __launch_bounds__(W2_NT, 1) void c2r_wide2_kernel(C2RArgs a) {
     // ---- step A' (last axis, radix-2) ------------------------------------------
     const __amdgpu_buffer_rsrc_t ry = plane_rsrc(a.out, p, plane_bytes);
     const __amdgpu_buffer_rsrc_t rx = plane_rsrc(EPI ? a.x : a.out, p, plane_bytes);
+    // x of the epilogue, one half of a block ahead: slot u holds half u of
+    // the current block; half 1's x is requested before half 0's products,
+    // the next block's half 0 before half 1's (the item's first half before
+    // its first block)
+    u32x4 xr[2][2][2];
+    if (EPI) {
+      ldX(rx, c0, 0, 0, xr[0][0]);
+      ldX(rx, c0, 0, 1, xr[0][1]);
+    }
     auto block = [&](int b, int par) {
       // twiddles requested two blocks ahead (the sequence wraps at the item
       // boundary: every item walks the same blocks)
@@ -559,12 +568,14 @@ __global__ __launch_bounds__(W2_NT, 1) void c2r_wide2_kernel(C2RArgs a) {
       const _Float16* tb = TW + par * (W2_MB * LDT) + r16 * LDT + g * 8;
 #pragma unroll
       for (int u = 0; u < 2; ++u) {
-        // x of both segments of this half, requested before its products
-        u32x4 xs2[2][2];
         if (EPI) {
-          ldX(rx, c0, b, 2 * u, xs2[0]);
-          ldX(rx, c0, b, 2 * u + 1, xs2[1]);
+          const int nb = u == 0 ? b : b + 1;
+          if (nb < nmb) {
+            ldX(rx, c0, nb, 2 * (1 - u), xr[1 - u][0]);
+            ldX(rx, c0, nb, 2 * (1 - u) + 1, xr[1 - u][1]);
+          }
         }
+        const u32x4 (&xs2)[2][2] = xr[u];
         f4 ae[4], ao[4];
 #pragma unroll
         for (int c = 0; c < 4; ++c) {
