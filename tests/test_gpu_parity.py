@@ -266,22 +266,28 @@ def test_deterministic_repeat(prec):
 
 
 @pytest.mark.timeout(300)
-@pytest.mark.parametrize("wid,reps", [(3, 24), (5, 6)])
+@pytest.mark.parametrize("wid,reps", [(3, 24), (5, 6), (2, 12), (4, 12), (6, 8)])
 def test_deterministic_repeat_workloads(wid, reps):
     """Repeated calls on a benchmark workload in its launch configuration are
-    bit-identical to the first call: the 1024^2 layer's forward and data
-    gradient (radix-2 transforms), and the Tucker layer's combined backward
-    (its weight gradient on the side stream).  A race in a kernel, such as a
-    store handed another segment's values in a few lanes now and then, shows
-    as a difference between repetitions."""
+    bit-identical to the first call: the forward and data gradient of the
+    dense layers (chained, leading-axis and radix-2 transforms), and the
+    Tucker and CP layers' combined backward (their weight gradients on the
+    side streams).  A race in a kernel, such as a store handed another
+    segment's values in a few lanes now and then, shows as a difference
+    between repetitions."""
     wl = synth.WORKLOADS[wid]
     prec = "fp16_tanh"
     _, npdt, _ = U.prec_codes(prec)
     U.say(f"repeat {wl.name} x{reps}")
     x, w, gy = _workload_inputs(wid, prec)
     tucker = isinstance(w, dict)
-    layer = (U.make_layer(wl.n, wl.modes, wl.batch, wl.c_in, wl.c_out, prec, wl.rank, 1)
-             if tucker else U.make_layer(wl.n, wl.modes, wl.batch, wl.c_in, wl.c_out, prec))
+    if wl.weight == "cp":
+        layer = U.make_layer(wl.n, wl.modes, wl.batch, wl.c_in, wl.c_out, prec, policy=1,
+                             cp_rank=wl.rank[0])
+    elif tucker:
+        layer = U.make_layer(wl.n, wl.modes, wl.batch, wl.c_in, wl.c_out, prec, wl.rank, 1)
+    else:
+        layer = U.make_layer(wl.n, wl.modes, wl.batch, wl.c_in, wl.c_out, prec)
     xd, gyd = U.dev(x), U.dev(gy)
     wd = ({"core": U.dev(w["core"]), "u_in": U.dev(w["u_in"]), "u_out": U.dev(w["u_out"]),
            "u_mode": [U.dev(u) for u in w["u_mode"]]} if tucker else U.dev(w))
