@@ -797,6 +797,100 @@ __global__ __launch_bounds__(256) void pair_bt_kernel(BtArgs g) {
   }
 }
 
+// ---------------------------------------------------------------------------
+// The three per-mode products of the Tucker weight gradient in one launch:
+// with P[b][a][t], Q[b][e][t], S[a][e][t] (fp32 complex, the mode index t
+// innermost),
+//   R[a][e][t]  = sum_b P[b][a][t] Q[b][e][t],
+//   Z1[b][a][t] = sum_e Q[b][e][t] conj(S[a][e][t]),
+//   Z2[b][e][t] = s c(t) sum_a P[b][a][t] conj(S[a][e][t]).
+// A work-group stages the three operands of TR_T consecutive modes in LDS
+// (every load issued before the first is waited for) and its threads form
+// the results of those modes, TR_T consecutive modes per result row.
+constexpr int TR_T = 8;
+constexpr int TR_ROWS = 1024;  // B A + B E + A E rows of TR_T values: 64 KiB of LDS
+
+__global__ __launch_bounds__(256) void tucker_tri_kernel(TriArgs g) {
+  extern __shared__ __align__(16) unsigned char smem[];
+  f2* L = reinterpret_cast<f2*>(smem);  // rows [P: b A + a][Q: b E + e][S: a E + e] x TR_T
+  const f2* gP = reinterpret_cast<const f2*>(g.P);
+  const f2* gQ = reinterpret_cast<const f2*>(g.Q);
+  const f2* gS = reinterpret_cast<const f2*>(g.S);
+  const int tid = threadIdx.x;
+  const int tl = tid % TR_T;
+  const int64_t t = (int64_t)blockIdx.x * TR_T + tl;
+  const int64_t tc = t < g.T ? t : g.T - 1;  // in-bounds stand-in past the end
+  const int np = g.B * g.A, nq = g.B * g.E, ns = g.A * g.E;
+  const int rows = np + nq + ns;
+  constexpr int RPI = 256 / TR_T;  // rows per pass of the work-group
+  for (int r0 = 0; r0 < rows; r0 += 8 * RPI) {
+    f2 v[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const int r = min(r0 + tid / TR_T + i * RPI, rows - 1);
+      const f2* src = r < np ? gP + (int64_t)r * g.T
+                    : r < np + nq ? gQ + (int64_t)(r - np) * g.T
+                                  : gS + (int64_t)(r - np - nq) * g.T;
+      v[i] = src[tc];
+    }
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const int r = r0 + tid / TR_T + i * RPI;
+      if (r < rows) L[r * TR_T + tl] = v[i];
+    }
+  }
+  __syncthreads();
+  if (t >= g.T) return;
+  const f2* Pl = L + tl;
+  const f2* Ql = L + (size_t)np * TR_T + tl;
+  const f2* Sl = L + (size_t)(np + nq) * TR_T + tl;
+  float cz = g.scale;
+  if (g.c_ext) {
+    const int64_t c = t % g.c_ext;
+    cz *= (c == 0 || 2 * c == g.Nb) ? 1.0f : 2.0f;
+  }
+  const int nres = ns + np + nq;  // R, then Z1 (B A), then Z2 (B E)
+  for (int j = tid / TR_T; j < nres; j += RPI) {
+    float sr = 0.0f, si = 0.0f;
+    if (j < ns) {
+      const int a = j / g.E, e = j - (j / g.E) * g.E;
+      for (int b = 0; b < g.B; ++b) {
+        const f2 p = Pl[(b * g.A + a) * TR_T], q = Ql[(b * g.E + e) * TR_T];
+        sr = __builtin_fmaf(p[0], q[0], __builtin_fmaf(-p[1], q[1], sr));
+        si = __builtin_fmaf(p[0], q[1], __builtin_fmaf(p[1], q[0], si));
+      }
+      reinterpret_cast<f2*>(g.R)[((int64_t)a * g.E + e) * g.T + t] = f2{sr, si};
+    } else if (j < ns + np) {
+      const int k = j - ns, b = k / g.A, a = k - (k / g.A) * g.A;
+      for (int e = 0; e < g.E; ++e) {  // q conj(s)
+        const f2 q = Ql[(b * g.E + e) * TR_T], sv = Sl[(a * g.E + e) * TR_T];
+        sr = __builtin_fmaf(q[0], sv[0], __builtin_fmaf(q[1], sv[1], sr));
+        si = __builtin_fmaf(q[1], sv[0], __builtin_fmaf(-q[0], sv[1], si));
+      }
+      reinterpret_cast<f2*>(g.Z1)[((int64_t)b * g.A + a) * g.T + t] = f2{sr, si};
+    } else {
+      const int k = j - ns - np, b = k / g.E, e = k - (k / g.E) * g.E;
+      for (int a = 0; a < g.A; ++a) {  // p conj(s)
+        const f2 p = Pl[(b * g.A + a) * TR_T], sv = Sl[(a * g.E + e) * TR_T];
+        sr = __builtin_fmaf(p[0], sv[0], __builtin_fmaf(p[1], sv[1], sr));
+        si = __builtin_fmaf(p[1], sv[0], __builtin_fmaf(-p[0], sv[1], si));
+      }
+      reinterpret_cast<f2*>(g.Z2)[((int64_t)b * g.E + e) * g.T + t] = f2{sr * cz, si * cz};
+    }
+  }
+}
+
+hipError_t launch_tucker_tri(const TriArgs& g, hipStream_t s) {
+  if (g.B < 1 || g.A < 1 || g.E < 1 || g.T < 1) return hipErrorInvalidValue;
+  const int64_t rows = (int64_t)g.B * g.A + (int64_t)g.B * g.E + (int64_t)g.A * g.E;
+  if (rows > TR_ROWS) return hipErrorNotSupported;
+  const int64_t blocks = (g.T + TR_T - 1) / TR_T;
+  if (blocks > 0x7fffffff) return hipErrorNotSupported;
+  const size_t lds = (size_t)rows * TR_T * sizeof(f2);
+  hipLaunchKernelGGL(tucker_tri_kernel, dim3((unsigned)blocks), dim3(256), lds, s, g);
+  return hipGetLastError();
+}
+
 // The batch-innermost form of a step, if it has one (hipErrorNotSupported
 // otherwise): the result's innermost indices are carried by both operands
 // with the same dense strides, one other result index by each operand alone,

@@ -195,6 +195,27 @@ hipError_t launch_pair_modeprod(const PairArgs& a, hipStream_t s);
 // The batch-innermost form (small products batched over the modes);
 // hipErrorNotSupported when the step is not of that form.
 hipError_t launch_pair_bt(const PairArgs& a, hipStream_t s);
+
+// The Tucker weight gradient's three per-mode products in one launch (all
+// fp32 complex, mode index t innermost, T modes):
+//   R[a][e][t] = sum_b P[b][a][t] Q[b][e][t],
+//   Z1[b][a][t] = sum_e Q[b][e][t] conj(S[a][e][t]),
+//   Z2[b][e][t] = scale c(t) sum_a P[b][a][t] conj(S[a][e][t]),
+// c(t) of the last axis index t % c_ext (1 at 0 and Nb/2, else 2; c_ext 0:
+// none).  hipErrorNotSupported when B A + B E + A E > 1024.
+struct TriArgs {
+  const void* P;  // fp32 complex
+  const void* Q;
+  const void* S;
+  void* R;
+  void* Z1;
+  void* Z2;
+  int B, A, E;
+  int64_t T;
+  float scale;
+  int c_ext, Nb;
+};
+hipError_t launch_tucker_tri(const TriArgs& g, hipStream_t s);
 size_t r2c_wide_lds_bytes(int nct, bool pre, int lut_sat);
 size_t c2r_wide_lds_bytes(int nct, int Kap, bool epi, int lut_sat);
 hipError_t launch_r2c_wide(const R2CArgs& a, int nct, int grid, size_t lds, hipStream_t s);

@@ -1595,22 +1595,45 @@ fno_status run_tucker_wgrad(const fno_conv_desc* d, const Plan* pl, const void* 
   r = run_pair(sz, Wt(gh, "bo" + sp, 0), Wt(w->u_out, "oe", 1), lQ, Q, ELEM_F32, sqN, clast,
                g.Nb, s);
   if (r) return r;
+  // R, Z1 and Z2 (below) in one launch where the ranks allow it
+  bool tri = false;
+  if (!dry && (phases & WG_SPECTRA)) {
+    TriArgs ta{};
+    ta.P = P;
+    ta.Q = Q;
+    ta.S = S;
+    ta.R = Rb;
+    ta.Z1 = Z1;
+    ta.Z2 = Z2;
+    ta.B = (int)sz['b'];
+    ta.A = (int)sz['a'];
+    ta.E = (int)sz['e'];
+    ta.T = label_size(sp, sz);
+    ta.scale = sqN;
+    ta.c_ext = (int)sz[clast];
+    ta.Nb = g.Nb;
+    const hipError_t e = timed("tucker_pair", s, [&] { return launch_tucker_tri(ta, s); });
+    if (e == hipSuccess) tri = true;
+    else if (e != hipErrorNotSupported) return hip_fail(e, "tucker_tri");
+  }
   if (!dry && (phases & WG_SPECTRA) && (r = fk.fork(br))) return r;
   // Z1[b,a,sp] = sum_e Q[b,e,sp] conj(S[a,e,sp]);  g_u_in = sum conj(Xhat) Z1
-  r = run_pair(sz, F(Q, lQ, 0), F(S, lS, 1), "ba" + sp, Z1, ELEM_F32, 1.0f, 0, g.Nb, fk.z1);
-  if (r) return r;
+  if (!tri && (r = run_pair(sz, F(Q, lQ, 0), F(S, lS, 1), "ba" + sp, Z1, ELEM_F32, 1.0f, 0, g.Nb,
+                            fk.z1)))
+    return r;
   r = run_pair(sz, Wt(xh, "bi" + sp, 1), F(Z1, "ba" + sp, 0), "ia", gw->u_in, ELEM_F32, 1.0f, 0,
                g.Nb, fk.z1);
   if (r) return r;
   // Z2[b,e,sp] = sqrt(N) c(t) sum_a P[b,a,sp] conj(S[a,e,sp]); g_u_out = sum G Z2
-  r = run_pair(sz, F(P, lP, 0), F(S, lS, 1), "be" + sp, Z2, ELEM_F32, sqN, clast, g.Nb, fk.z2);
-  if (r) return r;
+  if (!tri && (r = run_pair(sz, F(P, lP, 0), F(S, lS, 1), "be" + sp, Z2, ELEM_F32, sqN, clast,
+                            g.Nb, fk.z2)))
+    return r;
   r = run_pair(sz, Wt(gh, "bo" + sp, 0), F(Z2, "be" + sp, 0), "oe", gw->u_out, ELEM_F32, 1.0f,
                0, g.Nb, fk.z2);
   if (r) return r;
   // R[a,e,sp] = sum_b P Q
-  r = run_pair(sz, F(P, lP, 0), F(Q, lQ, 0), lR, Rb, ELEM_F32, 1.0f, 0, g.Nb, s);
-  if (r) return r;
+  if (!tri && (r = run_pair(sz, F(P, lP, 0), F(Q, lQ, 0), lR, Rb, ELEM_F32, 1.0f, 0, g.Nb, s)))
+    return r;
   // g_core[a,e,rk] = R contracted with conj(u_j) along every spatial axis
   {
     Opnd cur = F(Rb, lR, 0);
