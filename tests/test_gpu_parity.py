@@ -191,6 +191,9 @@ TUCKER_EDGE = [
     # are staged as 16-byte quads of contiguous contracted elements, with
     # contractions that end in a partial stage
     ((16, 24), (4, 5), 3, 12, 20, (4, 8, 2, 4)),
+    # B r_in + B r_out + r_in r_out > 1024: the weight gradient's R, Z1 and
+    # Z2 as three launches instead of the fused one
+    ((8, 8), (2, 3), 40, 16, 16, (14, 14, 2, 2)),
 ]
 
 
