@@ -39,6 +39,15 @@
  *     rejected call enqueues nothing.  Calls are asynchronous on `stream`.
  *   - The plan cache is mutex-guarded; concurrent calls on different streams
  *     are safe as long as their workspaces and outputs do not overlap.
+ *   - Calls run on the current device, whose stream `stream` must be.  With
+ *     Tucker or CP weights the forward, data-gradient, weight-gradient and
+ *     combined backward calls run part of their steps on up to three more
+ *     streams of the library's own (default priority, one set per device,
+ *     created on the first such call outside a stream capture and kept until
+ *     the process ends).  Those streams fork from and join `stream` through
+ *     events, so the whole call stays ordered on `stream`: work enqueued on
+ *     `stream` afterwards sees every result, and a stream capture records
+ *     every branch.
  */
 #ifndef FNO_SPECTRAL_CONV_H_
 #define FNO_SPECTRAL_CONV_H_
