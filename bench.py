@@ -513,7 +513,7 @@ def main():
         return
     if args.gpus != 1:
         print(json.dumps({"error": "this layer runs on one GPU; multi-GPU runs are not "
-                                   "part of this build (see the sharding design)",
+                                   "supported (the sharding is a documented design only)",
                           "n_gpus": args.gpus}))
         sys.exit(2)
     import torch
