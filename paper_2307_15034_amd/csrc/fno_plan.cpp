@@ -2320,11 +2320,15 @@ fno_status fno_spectral_conv_bwd(const fno_conv_desc* d, const void* x, const fn
     auto side_a = [&](SideStream* ss, hipStream_t st_) {
       fno_status r;
       ready = path_weights_on_side(d, pl, true, w, tsc, ss, &r);
-      // the weight gradient's own extra chains only outside a stream
-      // capture: capturing that second-level fork ended the process inside
-      // the runtime's end-of-capture call, cause not found
-      if (ss && !capturing(s)) {
+      // The weight gradient's Z1 and Z2 chains: on their own two streams
+      // outside a stream capture; under a capture on the caller's stream
+      // (after its inverse transform, which it enqueues first), since
+      // capturing the second-level fork ended the process inside the
+      // runtime's end-of-capture call (cause not found), while the caller's
+      // stream waiting for the side stream and back is an ordinary fork.
+      if (ss) {
         wb = ss->branches();
+        if (capturing(s)) wb.z1 = wb.z2 = s;
         pwb = &wb;
       }
       return r != FNO_OK ? r : wgrad(WG_WEIGHTS, st_, nullptr);
