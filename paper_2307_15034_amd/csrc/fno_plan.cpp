@@ -2320,15 +2320,17 @@ fno_status fno_spectral_conv_bwd(const fno_conv_desc* d, const void* x, const fn
     auto side_a = [&](SideStream* ss, hipStream_t st_) {
       fno_status r;
       ready = path_weights_on_side(d, pl, true, w, tsc, ss, &r);
-      // The weight gradient's Z1 and Z2 chains: on their own two streams
-      // outside a stream capture; under a capture on the caller's stream
-      // (after its inverse transform, which it enqueues first), since
-      // capturing the second-level fork ended the process inside the
-      // runtime's end-of-capture call (cause not found), while the caller's
-      // stream waiting for the side stream and back is an ordinary fork.
+      // The weight gradient's Z1 and Z2 chains run on the caller's stream
+      // after its inverse transform (which it enqueues first), beside the
+      // side stream's R chain: the caller's stream waits for P, Q and the
+      // fused products on the side stream, and the side stream for the
+      // chains.  (Forking the chains off the side stream onto two more
+      // streams instead ended the process inside the runtime's
+      // end-of-capture call under a stream capture, cause not found, and
+      // was no faster when launched from the host.)
       if (ss) {
         wb = ss->branches();
-        if (capturing(s)) wb.z1 = wb.z2 = s;
+        wb.z1 = wb.z2 = s;
         pwb = &wb;
       }
       return r != FNO_OK ? r : wgrad(WG_WEIGHTS, st_, nullptr);
