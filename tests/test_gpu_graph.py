@@ -106,14 +106,17 @@ def _flat(t):
     return [t]
 
 
+@pytest.mark.parametrize("separate", [False, True])
 @pytest.mark.parametrize("policy", [0, 1])
 @pytest.mark.parametrize("kind", ["tucker", "cp"])
-def test_graph_replay_factorized(kind, policy):
+def test_graph_replay_factorized(kind, policy, separate):
+    """separate: the backward as bwd_data (keeping the gradient spectrum) and
+    bwd_weight from the two spectra, instead of the combined call."""
     n, modes, Bt, ci, co, rank = FACTOR_CASES[kind]
     prec = "fp16_tanh"
     _, npdt, oprec = U.prec_codes(prec)
     U.say(f"graph replay {kind} policy {policy}: n={n} modes={modes} B={Bt} C={ci}->{co} "
-          f"rank={rank}")
+          f"rank={rank} separate={separate}")
     kd = tuple(2 * m if j < len(n) - 1 else m for j, m in enumerate(modes))
     if kind == "tucker":
         layer = U.make_layer(n, modes, Bt, ci, co, prec, rank, policy)
@@ -131,9 +134,19 @@ def test_graph_replay_factorized(kind, policy):
     gx = torch.empty((Bt, ci) + n, dtype=layer.dtype, device="cuda")
     gw = layer.alloc_grads()
 
+    gh = layer.spectrum_buffer(1)
+
+    def backward(x_, w_, gy_, xh_, gx_=None, gw_=None, gh_=None, stream=None):
+        if not separate:
+            return layer.bwd(x_, w_, gy_, x_hat=xh_, gx=gx_, gw=gw_, stream=stream)
+        gh_ = layer.spectrum_buffer(1) if gh_ is None else gh_
+        gx_ = layer.bwd_data(x_, w_, gy_, gx=gx_, gy_hat=gh_, stream=stream)
+        gw_ = layer.bwd_weight(None, None, w_, x_hat=xh_, gy_hat=gh_, gw=gw_, stream=stream)
+        return gx_, gw_
+
     def step(stream=None):
         layer.fwd(xs, ws, y=y, x_hat=xh, stream=stream)
-        layer.bwd(xs, ws, gys, x_hat=xh, gx=gx, gw=gw, stream=stream)
+        backward(xs, ws, gys, xh, gx_=gx, gw_=gw, gh_=gh, stream=stream)
 
     step()  # plans, tables and workspaces exist before the capture
     torch.cuda.synchronize()
@@ -161,7 +174,7 @@ def test_graph_replay_factorized(kind, policy):
               "u_mode": [U.dev(u) for u in w["u_mode"]]}
         xh_e = layer.spectrum_buffer(0)
         ye = layer.fwd(xd, wd, x_hat=xh_e)
-        gxe, gwe = layer.bwd(xd, wd, gd, x_hat=xh_e)
+        gxe, gwe = backward(xd, wd, gd, xh_e)
         torch.cuda.synchronize()
         ref = [U.host(t) for t in [ye, gxe] + _flat(gwe)]
         assert len(got) == len(ref)
