@@ -357,6 +357,77 @@ __device__ __forceinline__ uint32_t lut2(const _Float16* tab, uint32_t w, us2 sa
   return ODD ? (u | (w & 0x80008000u)) : u;
 }
 
+// A second table layout for kernels whose dynamic LDS starts with the table
+// (LDS byte address 0, no static LDS in the kernel): f of the codes 0..sat
+// followed by LUTN_NANS NaN entries.  With o = 2 |code| (the sign shifted out
+// of each 16-bit half) the byte address of a code's entry is
+//   min(o, 2 sat) + max(o - 0xf800, 0),
+// whose second term is 0 for every finite code and for inf (o <= 0xf800)
+// and 2..0x7fe for the NaN codes, which land in the NaN entries: three
+// packed 16-bit operations and two zero-extending adds form both addresses
+// of a word, with no base to add.  Entry sat + 1 is NaN as in the first
+// layout, so lut2 reads this layout too.
+constexpr int LUTN_NANS = 1023;
+
+// f(|x|) with the sign of x restored (odd f) for the four words of v
+// through such a table, in one asm block: the eight addresses, the eight LDS
+// reads in flight together, one wait, then the halves joined and the signs
+// put back.  The block waits for every LDS read of the wave (lgkmcnt(0)), so
+// the compiler's own outstanding LDS reads are complete after it too.
+// s2 holds 2 sat in both halves.
+__device__ __forceinline__ void lutn_odd4(u32x4& v, uint32_t s2) {
+  uint32_t w0 = v[0], w1 = v[1], w2 = v[2], w3 = v[3];
+  uint32_t a0, a1, a2, a3, t0, t1, t2, t3, r0, r1, r2, r3;
+#define FNO_LUTN_ADDR(W, A, T, R)                                                        \
+  "v_pk_lshlrev_b16 " R ", 1, " W " op_sel_hi:[0,1]\n\t"                                \
+  "v_pk_sub_u16 " A ", " R ", %[cn] clamp\n\t"                                          \
+  "v_pk_min_u16 " R ", " R ", %[s2]\n\t"                                                \
+  "v_add_u32_sdwa " T ", " R ", " A                                                     \
+  " dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:WORD_1 src1_sel:WORD_1\n\t"            \
+  "v_add_u32_sdwa " A ", " R ", " A                                                     \
+  " dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:WORD_0 src1_sel:WORD_0\n\t"
+#define FNO_LUTN_READ(A, T) "ds_read_u16 " A ", " A "\n\tds_read_u16 " T ", " T "\n\t"
+#define FNO_LUTN_JOIN(W, A, T) \
+  "v_lshl_or_b32 " T ", " T ", 16, " A "\n\tv_and_or_b32 " W ", " W ", %[sm], " T "\n\t"
+  asm volatile(
+      FNO_LUTN_ADDR("%[w0]", "%[a0]", "%[t0]", "%[r0]")
+      FNO_LUTN_ADDR("%[w1]", "%[a1]", "%[t1]", "%[r1]")
+      FNO_LUTN_ADDR("%[w2]", "%[a2]", "%[t2]", "%[r2]")
+      FNO_LUTN_ADDR("%[w3]", "%[a3]", "%[t3]", "%[r3]")
+      FNO_LUTN_READ("%[a0]", "%[t0]") FNO_LUTN_READ("%[a1]", "%[t1]")
+      FNO_LUTN_READ("%[a2]", "%[t2]") FNO_LUTN_READ("%[a3]", "%[t3]")
+      "s_waitcnt lgkmcnt(0)\n\t"
+      FNO_LUTN_JOIN("%[w0]", "%[a0]", "%[t0]") FNO_LUTN_JOIN("%[w1]", "%[a1]", "%[t1]")
+      FNO_LUTN_JOIN("%[w2]", "%[a2]", "%[t2]") FNO_LUTN_JOIN("%[w3]", "%[a3]", "%[t3]")
+      : [w0] "+v"(w0), [w1] "+v"(w1), [w2] "+v"(w2), [w3] "+v"(w3),
+        [a0] "=&v"(a0), [a1] "=&v"(a1), [a2] "=&v"(a2), [a3] "=&v"(a3),
+        [t0] "=&v"(t0), [t1] "=&v"(t1), [t2] "=&v"(t2), [t3] "=&v"(t3),
+        [r0] "=&v"(r0), [r1] "=&v"(r1), [r2] "=&v"(r2), [r3] "=&v"(r3)
+      : [cn] "s"(0xf800f800u), [s2] "s"(s2), [sm] "s"(0x80008000u));
+#undef FNO_LUTN_ADDR
+#undef FNO_LUTN_READ
+#undef FNO_LUTN_JOIN
+  v[0] = w0;
+  v[1] = w1;
+  v[2] = w2;
+  v[3] = w3;
+}
+
+// LDS bytes of such a table (codes 0..sat, the NaN entries), rounded up to
+// 256 so that the regions after it stay aligned.
+__host__ __device__ __forceinline__ int lutn_bytes(int sat) {
+  return ((sat + 1 + LUTN_NANS) * 2 + 255) & ~255;
+}
+
+// Stage tab[0..sat] of a global table and the NaN entries (NT threads).
+template <int NT>
+__device__ __forceinline__ void stage_lutn(_Float16* dst, const void* src, int sat) {
+  const _Float16* s = reinterpret_cast<const _Float16*>(src);
+  for (int i = threadIdx.x; i <= sat; i += NT) dst[i] = s[i];
+  const uint16_t qnan = 0x7e00;
+  for (int i = threadIdx.x; i < LUTN_NANS; i += NT) __builtin_memcpy(&dst[sat + 1 + i], &qnan, 2);
+}
+
 // Stage tab[0..sat] of a global table and the NaN entry (NT threads).
 template <int NT>
 __device__ __forceinline__ void stage_lut(_Float16* dst, const void* src, int sat) {

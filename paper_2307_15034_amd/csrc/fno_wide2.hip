@@ -22,9 +22,13 @@
 // each of the eight waves owns the 16-row tiles c0 + 16 w + [0, 16) and
 // c0 + Na/2 + 16 w + [0, 16), so the leading-axis butterfly pairs registers
 // of the same lane.  Persistent work-groups (one per compute unit) walk the
-// items; the twiddle staging through LDS and the tanh / tanh' lookup are as
-// in the one-stage wide kernels.  The LDS layouts below are chosen so that
-// the 16-byte accesses of each group of eight lanes hit 32 distinct banks.
+// items; the twiddle staging through LDS and the tanh' lookup of the
+// inverse are as in the one-stage wide kernels, the forward's tanh lookup
+// batches eight table reads per wait.  The padded LDS layouts below give
+// 16-byte accesses without bank conflicts beyond the half rate that gfx950
+// applies to any 16-byte read whose 16-lane groups do not each cover one
+// aligned 256-byte block (measured: such reads take twice the cycles of
+// block-aligned ones, with or without padding).
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -46,9 +50,6 @@ constexpr int W2_NTS = 2;          // cache policy of the inverse's stores: stre
 constexpr int W2_MB = 64;          // output columns per block of the inverse's last stage
 constexpr int W2_LDO = 68;         // transpose buffer row stride (floats)
 
-// LDS bytes of a lookup table of codes 0..sat plus the NaN entry, rounded
-// up to 256 (the regions after it stay aligned)
-__host__ __device__ __forceinline__ int w2_lut_bytes(int sat) { return ((sat + 2) * 2 + 255) & ~255; }
 
 // column x of a 64-wide row of the transpose buffer, stored with the two
 // 4-float halves of each 8-float group swapped in the upper 32 columns: the
@@ -84,7 +85,7 @@ __global__ __launch_bounds__(W2_NT, 1) void r2c_wide2_kernel(R2CArgs a) {
   // the lookup table first, so that a lookup address is the byte offset of
   // the code itself (no base to add)
   _Float16* lut = reinterpret_cast<_Float16*>(smem);
-  _Float16* AT = reinterpret_cast<_Float16*>(smem + (PRE ? w2_lut_bytes(a.lut_sat) : 0));
+  _Float16* AT = reinterpret_cast<_Float16*>(smem + (PRE ? lutn_bytes(a.lut_sat) : 0));
   // [2 rc][2 cls][2 KBPC][LDR]
   _Float16* TWb = AT + 4 * 2 * KBPC * W2_LDR;           // [2][NROW][LDT]
   const int tid = threadIdx.x, lane = tid & 63;
@@ -92,8 +93,8 @@ __global__ __launch_bounds__(W2_NT, 1) void r2c_wide2_kernel(R2CArgs a) {
   const int r16 = lane & 15, g = lane >> 4;
   const _Float16* cB = reinterpret_cast<const _Float16*>(a.cB);
   const _Float16* sB = reinterpret_cast<const _Float16*>(a.sB);
-  const us2 sat = {(unsigned short)a.lut_sat, (unsigned short)a.lut_sat};
-  if (PRE) stage_lut<W2_NT>(lut, a.lut, a.lut_sat);
+  const uint32_t sat2 = (uint32_t)(2 * a.lut_sat) * 0x10001u;
+  if (PRE) stage_lutn<W2_NT>(lut, a.lut, a.lut_sat);
 
   const int Nh = a.Nb >> 1, NhA = a.Na >> 1;
   const int64_t plane_bytes = (int64_t)a.Na * a.Nb * 2;
@@ -191,11 +192,8 @@ __global__ __launch_bounds__(W2_NT, 1) void r2c_wide2_kernel(R2CArgs a) {
       for (int u = 0; u < 2; ++u) {
         u32x4 lo = v[u][0], hi = v[u][1];
         if (PRE) {
-#pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            lo[e] = lut2<true>(lut, lo[e], sat);
-            hi[e] = lut2<true>(lut, hi[e], sat);
-          }
+          lutn_odd4(lo, sat2);
+          lutn_odd4(hi, sat2);
         }
         // half sums and half differences: fp16 cannot overflow here (large
         // pre-activation bounds reach 65504), and halving is exact; the
@@ -377,7 +375,7 @@ __global__ __launch_bounds__(W2_NT, 1) void c2r_wide2_kernel(C2RArgs a) {
   extern __shared__ __align__(16) unsigned char smem[];
   // the lookup table first (a lookup address is the code's byte offset)
   _Float16* lut = reinterpret_cast<_Float16*>(smem);
-  _Float16* ZT = reinterpret_cast<_Float16*>(smem + (EPI ? w2_lut_bytes(a.lut_sat) : 0));
+  _Float16* ZT = reinterpret_cast<_Float16*>(smem + (EPI ? lutn_bytes(a.lut_sat) : 0));
   // [2][2][2 KBPC][LDZ]
   unsigned char* reg = reinterpret_cast<unsigned char*>(ZT) + L::zt_bytes;
   _Float16* VL = reinterpret_cast<_Float16*>(reg);       // [2 W2_H][LDV]
@@ -405,7 +403,7 @@ __global__ __launch_bounds__(W2_NT, 1) void c2r_wide2_kernel(C2RArgs a) {
 
   // the padding of ZT stays zero: every plane writes the same positions
   for (int i = tid; i < 2 * 2 * 2 * KBPC * LDZ; i += W2_NT) ZT[i] = (_Float16)0.0f;
-  if (EPI) stage_lut<W2_NT>(lut, a.lut, a.lut_sat);
+  if (EPI) stage_lutn<W2_NT>(lut, a.lut, a.lut_sat);
 
   auto ldZ = [&](int64_t p, u32x4 (&zq)[ZQ]) {
     const __amdgpu_buffer_rsrc_t rz = plane_rsrc(a.in, p, spec_bytes);
@@ -421,15 +419,20 @@ __global__ __launch_bounds__(W2_NT, 1) void c2r_wide2_kernel(C2RArgs a) {
     for (int q = 0; q < ZQ; ++q) {
       const int i = tid + q * W2_NT;
       if (i < nq) {
-        const int t_a = i / qpr, kb0 = (i - t_a * qpr) * 4;
+        // kb0 is a multiple of 4: slot kb0 + e sits in column (e & 1) KBPC +
+        // kb0 / 2 + e / 2 of its class, a constant step from the first (one
+        // address per piece, formed per item rather than held live)
+        int t_a = i / qpr;
+        asm volatile("" : "+v"(t_a));
+        const int kb0 = (i - t_a * qpr) * 4;
         const int ca = t_a & 1, tq = t_a >> 1;
+        _Float16* z0 = ZT + (ca * 2 * 2 * KBPC + (kb0 >> 1)) * LDZ + tq;
         const h8 v = w_as_h8(zq[q]);
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-          const int kb = kb0 + e;
-          const int pcol = (kb & 1) * KBPC + (kb >> 1);
-          ZT[((ca * 2 + 0) * 2 * KBPC + pcol) * LDZ + tq] = v[2 * e];
-          ZT[((ca * 2 + 1) * 2 * KBPC + pcol) * LDZ + tq] = v[2 * e + 1];
+          const int pc = ((e & 1) * KBPC + (e >> 1)) * LDZ;
+          z0[pc] = v[2 * e];                       // real part
+          z0[2 * KBPC * LDZ + pc] = v[2 * e + 1];  // imaginary part
         }
       }
     }
@@ -660,7 +663,7 @@ size_t r2c_wide2_lds_bytes(int nctc, bool pre, int lut_sat) {
   const int kbpc = nctc * 8;
   const size_t at = (size_t)4 * 2 * kbpc * W2_LDR * 2;
   const size_t tw = (size_t)2 * 4 * kbpc * W2_LDT * 2;
-  return at + tw + (pre ? (size_t)w2_lut_bytes(lut_sat) : 0);
+  return at + tw + (pre ? (size_t)lutn_bytes(lut_sat) : 0);
 }
 
 size_t c2r_wide2_lds_bytes(int nctc, int nkzh, bool epi, int lut_sat) {
@@ -670,7 +673,7 @@ size_t c2r_wide2_lds_bytes(int nctc, int nkzh, bool epi, int lut_sat) {
   FNO_C2RW2_BYTES(2, 1) FNO_C2RW2_BYTES(2, 2) FNO_C2RW2_BYTES(4, 1) FNO_C2RW2_BYTES(4, 2)
 #undef FNO_C2RW2_BYTES
   if (base == 0) return (size_t)1 << 30;  // not a shape of this path
-  return base + (epi ? (size_t)w2_lut_bytes(lut_sat) : 0);
+  return base + (epi ? (size_t)lutn_bytes(lut_sat) : 0);
 }
 
 template <int NCTC, bool PRE>
