@@ -257,11 +257,14 @@ def copy_bandwidth(torch, nbytes=1 << 30, reps=10):
 
 # rocprofv3 kernel symbols -> the names the library times its launches under
 # (first match wins; the template flag "true" marks the pre-activation
-# variant of a transform)
+# variant of a transform: the last flag, the second argument of the radix-2
+# wide-plane forward)
 KERNEL_NAMES = [
     (r"epi_mix\w*<[^>]*true>", "block_epilogue_fwd"),
     (r"epi_mix\w*<", "block_epilogue_bwd_data"),
     (r"epi_wgrad\w*<", "block_epilogue_bwd_weight"),
+    (r"r2c_wide2_kernel<\d+, true", "r2c_plane_tanh"),
+    (r"r2c_wide2_kernel<", "r2c_plane"),
     (r"r2c_\w+<[^>]*true>", "r2c_plane_tanh"),
     (r"r2c_\w+<", "r2c_plane"),
     (r"slab_adj_wgrad_kernel", "contract_adjoint_wgrad"),

@@ -45,6 +45,10 @@ struct R2CArgs {
   // channel) the clip bounds (lo, hi) in double; plane p uses group p / bgroup
   const double* bounds;
   int bgroup;
+  // radix-2 wide-plane forward, narrow variant: 1 requests a work item's
+  // step-B tables at its start and the next item's rows during its last two
+  // slices (more registers held per wave)
+  int early;
 };
 
 // Inverse of the above: spectrum [planes][Ka][Kb] -> y [planes][Na][Nb],

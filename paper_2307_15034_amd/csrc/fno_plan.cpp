@@ -366,6 +366,8 @@ struct Plan {
   std::vector<std::string> labels_fwd, labels_adj;
   std::string out_fwd, out_adj;
   int device = 0;
+  // early requests in the narrow wide-plane forward (see host_plan)
+  bool r2c_early = true;
   Plan() = default;
   Plan(const Plan&) = delete;
   Plan& operator=(const Plan&) = delete;
@@ -775,6 +777,12 @@ fno_status build_tables(const fno_conv_desc* d, Plan* pl) {
 // Geometry and Tucker paths: host-only, no device calls.
 void host_plan(const fno_conv_desc* d, Plan* pl) {
   pl->g = make_geo(d);
+  // The early-request forward holds 32 more registers per wave.  The
+  // MIN_RESULT factorised paths run their longest weights-only products on a
+  // side stream beside the forward transform, and those slow down more
+  // (fewer registers left on each SIMD) than the transform gains; with
+  // MIN_NET and dense weights the early requests are faster.
+  pl->r2c_early = !(factorized(d) && d->path_policy == FNO_PATH_MIN_RESULT);
   if (factorized(d)) {
     Sizes sz = weight_sizes(d);
     weight_labels(d, false, &pl->labels_fwd, &pl->out_fwd);
@@ -1088,6 +1096,7 @@ fno_status run_r2c(const Plan* pl, const void* in, void* spec, void* inter, int6
     b.sB = pl->t.sB2;
     b.Kap16 = g.w2_nta * 16;
     b.lut_sat = pl->t.actSat;
+    b.early = pl->r2c_early ? 1 : 0;
     const size_t lds = r2c_wide2_lds_bytes(g.w2_nctc, do_tanh, b.lut_sat);
     const int grid = (int)std::min<int64_t>(a.planes, (int64_t)pl->num_cu);
     hipError_t e = timed(kname, s, [&] { return launch_r2c_wide2(b, g.w2_nctc, grid, lds, s); });

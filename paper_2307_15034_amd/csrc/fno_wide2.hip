@@ -71,7 +71,7 @@ __device__ __forceinline__ int ob_col(int x) { return x ^ ((x & 32) >> 3); }
 // X[t_a][t_b] += sum_r (cB - i sB)[rc][t][r] Y_rc[r][t_b] over the items of
 // the plane, t_a = 2t + rc, t_b = 2 t' + cls.
 // ---------------------------------------------------------------------------
-template <int NCTC, bool PRE>
+template <int NCTC, bool PRE, bool EARLY>
 __global__ __launch_bounds__(W2_NT, 1) void r2c_wide2_kernel(R2CArgs a) {
   typedef MM<_Float16> M;
   constexpr int KBPC = NCTC * 8;               // complex columns per class (padded)
@@ -81,6 +81,11 @@ __global__ __launch_bounds__(W2_NT, 1) void r2c_wide2_kernel(R2CArgs a) {
   constexpr int TWP = NROW * W2_SK / 8 / W2_NT;  // 16-byte slice pieces per thread
   constexpr int NKB = W2_H / W2_KS;            // step-B k-steps per item
   static_assert(TWP >= 1, "slice pieces");
+  // EARLY: an item's step-B tables are requested at its start and the next
+  // item's rows during its last two slices, so that short items (one chunk
+  // per plane) do not wait for the next rows after step B; it holds the
+  // tables' 32 registers through step A
+  static_assert(!EARLY || NCTC == 2, "early requests: narrow variant only");
   extern __shared__ __align__(16) unsigned char smem[];
   // the lookup table first, so that a lookup address is the byte offset of
   // the code itself (no base to add)
@@ -177,6 +182,16 @@ __global__ __launch_bounds__(W2_NT, 1) void r2c_wide2_kernel(R2CArgs a) {
     const bool more = it + 1 < nitems;
     const __amdgpu_buffer_rsrc_t rsn = more ? plane_rsrc(a.in, item_plane(it + 1), plane_bytes) : rs;
     const int cn = more ? item_chunk(it + 1) : c0;
+    h8 cfs[NKB], sfs[NKB];
+    auto ld_tables = [&] {
+#pragma unroll
+      for (int k = 0; k < NKB; ++k) {
+        const int64_t toff = (int64_t)(rc * nta * 16 + ta * 16 + r16) * NhA + c0 + k * W2_KS + g * 8;
+        cfs[k] = M::ld(cB + toff);
+        sfs[k] = M::ld(sB + toff);
+      }
+    };
+    if (EARLY) ld_tables();
 
     // ---- step A (last axis, radix-2) ----------------------------------------
     f4 accE[2][NCTC], accO[2][NCTC];
@@ -222,6 +237,11 @@ __global__ __launch_bounds__(W2_NT, 1) void r2c_wide2_kernel(R2CArgs a) {
       for (int k = 0; k < 2; ++k) {
         mul(va[2 * par + k], par, k);
         if (rows) ldA(rs, rb, 2 * gs + k + 4, va[2 * par + k]);
+        // EARLY: the last two slices request the next item's k-steps into
+        // the slots they free (the last k-step of this plane, in range, when
+        // there is no next item: one load sequence)
+        if (EARLY && !rows)
+          ldA(more ? rsn : rs, row_lane(cn), more ? 2 * gs + k + 4 - nks : nks - 1, va[2 * par + k]);
       }
       stTW(twr[1 - par], 1 - par);
       __syncthreads();
@@ -263,14 +283,8 @@ __global__ __launch_bounds__(W2_NT, 1) void r2c_wide2_kernel(R2CArgs a) {
     __builtin_amdgcn_sched_barrier(0);  // accumulators dead before the tables load
     // step-B tables of this item, then the next item's first row fragments
     // (operands selected, not branched on: one load sequence, exact waits)
-    h8 cfs[NKB], sfs[NKB];
-#pragma unroll
-    for (int k = 0; k < NKB; ++k) {
-      const int64_t toff = (int64_t)(rc * nta * 16 + ta * 16 + r16) * NhA + c0 + k * W2_KS + g * 8;
-      cfs[k] = M::ld(cB + toff);
-      sfs[k] = M::ld(sB + toff);
-    }
-    {
+    if (!EARLY) {
+      ld_tables();
       const int rb = row_lane(cn);
 #pragma unroll
       for (int d = 0; d < 4; ++d) ldA(more ? rsn : rs, rb, more ? d : nks - 1, va[d]);
@@ -564,6 +578,11 @@ __global__ __launch_bounds__(W2_NT, 1) void c2r_wide2_kernel(C2RArgs a) {
       ldX(rx, c0, 0, 0, xr[0][0]);
       ldX(rx, c0, 0, 1, xr[0][1]);
     }
+    // planes of one item (narrow variant): the next plane's spectrum is
+    // requested a whole item before it is staged (zq is free: this plane's
+    // staging has read it)
+    const bool z_early = NCTC == 2 && nch == 1;
+    if (more && z_early) ldZ(pn, zq);
     auto block = [&](int b, int par) {
       // twiddles requested two blocks ahead (the sequence wraps at the item
       // boundary: every item walks the same blocks)
@@ -651,8 +670,8 @@ __global__ __launch_bounds__(W2_NT, 1) void c2r_wide2_kernel(C2RArgs a) {
     // (registers free during the other blocks)
     ldC(cn, cf, sf);
     block(nmb - 1, 1);
-    // the next plane's spectrum (its latency is exposed once per plane)
-    if (more && cn == 0) ldZ(pn, zq);
+    // otherwise after the plane's last block
+    if (more && cn == 0 && !z_early) ldZ(pn, zq);
   }
 }
 
@@ -676,26 +695,31 @@ size_t c2r_wide2_lds_bytes(int nctc, int nkzh, bool epi, int lut_sat) {
   return base + (epi ? (size_t)lutn_bytes(lut_sat) : 0);
 }
 
-template <int NCTC, bool PRE>
+template <int NCTC, bool PRE, bool EARLY>
 static hipError_t r2c_wide2_go(const R2CArgs& a, int grid, size_t lds, hipStream_t s) {
-  const void* k = (const void*)&r2c_wide2_kernel<NCTC, PRE>;
+  const void* k = (const void*)&r2c_wide2_kernel<NCTC, PRE, EARLY>;
   hipError_t e = hipFuncSetAttribute(k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL((r2c_wide2_kernel<NCTC, PRE>), dim3(grid), dim3(W2_NT), lds, s, a);
+  hipLaunchKernelGGL((r2c_wide2_kernel<NCTC, PRE, EARLY>), dim3(grid), dim3(W2_NT), lds, s, a);
   return hipGetLastError();
 }
 
 // a.twA, a.cB, a.sB: the radix-2 tables; a.Kap16: leading-axis rows per
-// class padded to a tile count of 1, 2 or 4.  Shapes: nctc in {2, 4}, Na and
-// Nb multiples of 256.
+// class padded to a tile count of 1, 2 or 4; a.early: the early requests of
+// the narrow variant (ignored for nctc 4).  Shapes: nctc in {2, 4}, Na and Nb
+// multiples of 256.
 hipError_t launch_r2c_wide2(const R2CArgs& a, int nctc, int grid, size_t lds, hipStream_t s) {
   const int nta = a.Kap16 / 16;
   if (lds > 160 * 1024 || a.Na % 256 != 0 || a.Nb % 256 != 0 || a.Kap16 % 16 != 0 ||
       (nta != 1 && nta != 2 && nta != 4) || grid <= 0)
     return hipErrorNotSupported;
   const bool t = a.do_tanh != 0;
-  if (nctc == 2) return t ? r2c_wide2_go<2, true>(a, grid, lds, s) : r2c_wide2_go<2, false>(a, grid, lds, s);
-  if (nctc == 4) return t ? r2c_wide2_go<4, true>(a, grid, lds, s) : r2c_wide2_go<4, false>(a, grid, lds, s);
+  if (nctc == 2 && a.early)
+    return t ? r2c_wide2_go<2, true, true>(a, grid, lds, s) : r2c_wide2_go<2, false, true>(a, grid, lds, s);
+  if (nctc == 2)
+    return t ? r2c_wide2_go<2, true, false>(a, grid, lds, s) : r2c_wide2_go<2, false, false>(a, grid, lds, s);
+  if (nctc == 4)
+    return t ? r2c_wide2_go<4, true, false>(a, grid, lds, s) : r2c_wide2_go<4, false, false>(a, grid, lds, s);
   return hipErrorNotSupported;
 }
 
