@@ -81,10 +81,11 @@ __global__ __launch_bounds__(W2_NT, 1) void r2c_wide2_kernel(R2CArgs a) {
   constexpr int TWP = NROW * W2_SK / 8 / W2_NT;  // 16-byte slice pieces per thread
   constexpr int NKB = W2_H / W2_KS;            // step-B k-steps per item
   static_assert(TWP >= 1, "slice pieces");
-  // EARLY: an item's step-B tables are requested at its start and the next
-  // item's rows during its last two slices, so that short items (one chunk
-  // per plane) do not wait for the next rows after step B; it holds the
-  // tables' 32 registers through step A
+  // The next item's first four k-steps are requested during this item's
+  // last two slices.  Its step-B tables then complete behind them (loads
+  // complete in order), unless EARLY requests them at the item's start,
+  // which holds their 32 registers through step A: for short items (one
+  // chunk per plane) waiting for the rows at step B costs more than that.
   static_assert(!EARLY || NCTC == 2, "early requests: narrow variant only");
   extern __shared__ __align__(16) unsigned char smem[];
   // the lookup table first, so that a lookup address is the byte offset of
@@ -237,10 +238,10 @@ __global__ __launch_bounds__(W2_NT, 1) void r2c_wide2_kernel(R2CArgs a) {
       for (int k = 0; k < 2; ++k) {
         mul(va[2 * par + k], par, k);
         if (rows) ldA(rs, rb, 2 * gs + k + 4, va[2 * par + k]);
-        // EARLY: the last two slices request the next item's k-steps into
-        // the slots they free (the last k-step of this plane, in range, when
-        // there is no next item: one load sequence)
-        if (EARLY && !rows)
+        // the last two slices request the next item's k-steps into the
+        // slots they free (operands selected, not branched on: the last
+        // k-step of this plane, in range, when there is no next item)
+        if (!rows)
           ldA(more ? rsn : rs, row_lane(cn), more ? 2 * gs + k + 4 - nks : nks - 1, va[2 * par + k]);
       }
       stTW(twr[1 - par], 1 - par);
@@ -252,8 +253,7 @@ __global__ __launch_bounds__(W2_NT, 1) void r2c_wide2_kernel(R2CArgs a) {
       slice(gs, 0, rb, true);
       slice(gs + 1, 1, rb, true);
     }
-    // last two slices: the next item's rows are requested after the step-B
-    // tables
+    // last two slices: the next item's rows
     slice(ngr - 2, 0, 0, false);
     slice(ngr - 1, 1, 0, false);
     {
@@ -281,14 +281,7 @@ __global__ __launch_bounds__(W2_NT, 1) void r2c_wide2_kernel(R2CArgs a) {
         }
     }
     __builtin_amdgcn_sched_barrier(0);  // accumulators dead before the tables load
-    // step-B tables of this item, then the next item's first row fragments
-    // (operands selected, not branched on: one load sequence, exact waits)
-    if (!EARLY) {
-      ld_tables();
-      const int rb = row_lane(cn);
-#pragma unroll
-      for (int d = 0; d < 4; ++d) ldA(more ? rsn : rs, rb, more ? d : nks - 1, va[d]);
-    }
+    if (!EARLY) ld_tables();  // this item's step-B tables
     __syncthreads();
 
     // ---- step B (leading axis, the rc class of this wave's tile) -------------
