@@ -493,11 +493,21 @@ __global__ __launch_bounds__(W2_NT, 1) void c2r_wide2_kernel(C2RArgs a) {
   u32x4 zq[ZQ];
   h8 cf[2][NKZH], sf[2][NKZH];
   u32x4 twr[2][TWP];     // twiddle blocks b + 1, b + 2 in flight
+  // x of the epilogue, one half of a block ahead: slot u holds half u of
+  // the current block; half 1's x is requested before half 0's products,
+  // the next block's half 0 before half 1's, and the next item's first
+  // half during this item's last block (the first item's before the loop)
+  u32x4 xr[2][2][2];
   if (nitems > 0) {
     ldZ(item_plane(0), zq);
     ldC(0, cf, sf);
     ldTW(0, twr[0]);
     ldTW(1, twr[1]);
+    if (EPI) {
+      const __amdgpu_buffer_rsrc_t rx0 = plane_rsrc(a.x, item_plane(0), plane_bytes);
+      ldX(rx0, item_chunk(0), 0, 0, xr[0][0]);
+      ldX(rx0, item_chunk(0), 0, 1, xr[0][1]);
+    }
   }
   __syncthreads();  // ZT cleared, table staged
 
@@ -562,15 +572,7 @@ __global__ __launch_bounds__(W2_NT, 1) void c2r_wide2_kernel(C2RArgs a) {
     // ---- step A' (last axis, radix-2) ------------------------------------------
     const __amdgpu_buffer_rsrc_t ry = plane_rsrc(a.out, p, plane_bytes);
     const __amdgpu_buffer_rsrc_t rx = plane_rsrc(EPI ? a.x : a.out, p, plane_bytes);
-    // x of the epilogue, one half of a block ahead: slot u holds half u of
-    // the current block; half 1's x is requested before half 0's products,
-    // the next block's half 0 before half 1's (the item's first half before
-    // its first block)
-    u32x4 xr[2][2][2];
-    if (EPI) {
-      ldX(rx, c0, 0, 0, xr[0][0]);
-      ldX(rx, c0, 0, 1, xr[0][1]);
-    }
+    const __amdgpu_buffer_rsrc_t rxn = more ? plane_rsrc(EPI ? a.x : a.out, pn, plane_bytes) : rx;
     // planes of one item (narrow variant): the next plane's spectrum is
     // requested a whole item before it is staged (zq is free: this plane's
     // staging has read it)
@@ -588,6 +590,11 @@ __global__ __launch_bounds__(W2_NT, 1) void c2r_wide2_kernel(C2RArgs a) {
           if (nb < nmb) {
             ldX(rx, c0, nb, 2 * (1 - u), xr[1 - u][0]);
             ldX(rx, c0, nb, 2 * (1 - u) + 1, xr[1 - u][1]);
+          } else {
+            // the next item's first half (this item's again, in range,
+            // when there is none: one load sequence)
+            ldX(rxn, more ? cn : c0, 0, 0, xr[0][0]);
+            ldX(rxn, more ? cn : c0, 0, 1, xr[0][1]);
           }
         }
         const u32x4 (&xs2)[2][2] = xr[u];
