@@ -151,6 +151,29 @@ def test_workload_hires_sampled(prec):
     _assert_close("gW", U.cplx(gw), rgw, prec)
 
 
+def test_wide_narrow_multi_item():
+    """1024^2 planes through the narrow radix-2 wide-plane transforms (24 x 24
+    modes: two column tiles per class, ragged leading-axis tiles) with four
+    work items per plane and more planes (3 x 96 = 288) than work-groups, so
+    that the early step-B tables, the next item's rows and the inverse's
+    next-item epilogue inputs all cross item and plane boundaries.  y and gx
+    of the last batch sample (planes 192..287, the second plane of the first
+    work-groups among them) against the oracle; gW over every mode."""
+    n, modes, Bt, ci, co, prec = (1024, 1024), (24, 24), 3, 96, 96, "fp16_tanh"
+    _, _, oprec = U.prec_codes(prec)
+    U.say(f"narrow wide-plane transforms n={n} modes={modes} B={Bt} C={ci}->{co}")
+    x, w, gy = synth.random_dense_case(81, Bt, ci, co, n, modes, np.float16)
+    layer = U.make_layer(n, modes, Bt, ci, co, prec)
+    y, gx, gw = U.run_all(layer, x, w, gy)
+    wc = U.cplx(w)
+    b = Bt - 1
+    _assert_close(f"y[b={b}]", y[b:b + 1], O.fwd(x[b:b + 1], wc, n, modes, oprec), prec)
+    _assert_close(f"gx[b={b}]", gx[b:b + 1],
+                  O.bwd_data(x[b:b + 1], wc, gy[b:b + 1], n, modes, oprec), prec)
+    xs, gs = _spectra_by_sample(x, gy, n, modes, oprec)
+    _assert_close("gW", U.cplx(gw), np.einsum("bi...,bo...->io...", np.conj(xs), gs), prec)
+
+
 @pytest.mark.parametrize("policy", ["min_result", "min_net"])
 @pytest.mark.parametrize("prec", PRECS)
 def test_workload_tucker(prec, policy):
