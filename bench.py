@@ -257,8 +257,8 @@ def copy_bandwidth(torch, nbytes=1 << 30, reps=10):
 
 # rocprofv3 kernel symbols -> the names the library times its launches under
 # (first match wins; the template flag "true" marks the pre-activation
-# variant of a transform: the last flag, the second argument of the radix-2
-# wide-plane forward)
+# variant of a transform: the last flag; the second argument of the radix-2
+# wide-plane forward, the third of its inverse)
 KERNEL_NAMES = [
     (r"epi_mix\w*<[^>]*true>", "block_epilogue_fwd"),
     (r"epi_mix\w*<", "block_epilogue_bwd_data"),
@@ -269,6 +269,8 @@ KERNEL_NAMES = [
     (r"r2c_\w+<", "r2c_plane"),
     (r"slab_adj_wgrad_kernel", "contract_adjoint_wgrad"),
     (r"slab_kernel<", "contract"),
+    (r"c2r_wide2_kernel<\d+, \d+, true", "c2r_plane_tanh_grad"),
+    (r"c2r_wide2_kernel<", "c2r_plane"),
     (r"c2r_\w+<[^>]*true>", "c2r_plane_tanh_grad"),
     (r"c2r_\w+<", "c2r_plane"),
 ]

@@ -351,7 +351,7 @@ __global__ __launch_bounds__(W2_NT, 1) void r2c_wide2_kernel(R2CArgs a) {
 // (16 rows x 64 columns) requests its x at its start, after the previous
 // segment's stores, and uses it after its transpose.
 // ---------------------------------------------------------------------------
-template <int NCTC, int NKZH>
+template <int NCTC, int NKZH, int MB = W2_MB>
 struct C2RWide2 {
   static constexpr int KBPC = NCTC * 8;
   static constexpr int LDZ = NKZH * 32 + 8;
@@ -359,16 +359,22 @@ struct C2RWide2 {
   static constexpr int LDT = 4 * KBPC + 8;
   static constexpr size_t zt_bytes = (size_t)2 * 2 * (2 * KBPC) * LDZ * 2;
   static constexpr size_t vl_bytes = (size_t)2 * W2_H * LDV * 2;
-  static constexpr size_t tw_bytes = (size_t)2 * W2_MB * LDT * 2;
+  static constexpr size_t tw_bytes = (size_t)2 * MB * LDT * 2;
   static constexpr size_t ob_bytes = (size_t)W2_WAVES * 16 * W2_LDO * 4;
   static constexpr size_t reg_bytes =
       vl_bytes > tw_bytes + ob_bytes ? vl_bytes : tw_bytes + ob_bytes;
 };
 
-template <int NCTC, int NKZH, bool EPI>
+template <int NCTC, int NKZH, bool EPI, int MB = W2_MB>
 __global__ __launch_bounds__(W2_NT, 1) void c2r_wide2_kernel(C2RArgs a) {
   typedef MM<_Float16> M;
-  typedef C2RWide2<NCTC, NKZH> L;
+  typedef C2RWide2<NCTC, NKZH, MB> L;
+  // MB 128 (the plain inverse of the wide variant on planes with Nb / 2 a
+  // multiple of 256): half the blocks per item, so half the block barriers
+  // and twiddle stagings; each block's results still go out through the
+  // 64-column transpose buffer, one 64-column chunk at a time
+  static_assert(!EPI || MB == W2_MB, "wide blocks: plain inverse only");
+  constexpr int NCB = MB / 16;         // 16-column tiles per block
   constexpr int KBPC = L::KBPC;
   constexpr int NTB = NCTC;            // p tiles (both step-A' classes)
   constexpr int NTBC = NCTC / 2;
@@ -376,7 +382,7 @@ __global__ __launch_bounds__(W2_NT, 1) void c2r_wide2_kernel(C2RArgs a) {
   constexpr int LDZ = L::LDZ, LDV = L::LDV, LDT = L::LDT;
   constexpr int KAH = NKZH * 32;
   constexpr int ZQ = 4;                // 16-byte spectrum pieces per thread
-  constexpr int TWP = W2_MB * 4 * KBPC / 8 / W2_NT;  // twiddle pieces per thread
+  constexpr int TWP = MB * 4 * KBPC / 8 / W2_NT;  // twiddle pieces per thread
   constexpr int PPR = 4 * KBPC / 8;    // pieces per twiddle row
   static_assert(TWP >= 1, "block pieces");
   extern __shared__ __align__(16) unsigned char smem[];
@@ -400,7 +406,7 @@ __global__ __launch_bounds__(W2_NT, 1) void c2r_wide2_kernel(C2RArgs a) {
   const int64_t plane_bytes = (int64_t)a.Na * a.Nb * 2;
   const int spec_bytes = a.Ka * a.Kb * 4;
   const int nch = NhA / W2_H;
-  const int nmb = Nh / W2_MB;          // even on this path
+  const int nmb = Nh / MB;             // even on this path
   const int nq = a.Ka * a.Kb / 4;      // 16-byte spectrum pieces
   const int64_t nitems = a.planes > (int64_t)blockIdx.x
                              ? ((a.planes - 1 - blockIdx.x) / gridDim.x + 1) * nch
@@ -463,11 +469,11 @@ __global__ __launch_bounds__(W2_NT, 1) void c2r_wide2_kernel(C2RArgs a) {
     for (int e = 0; e < TWP; ++e) {
       const int pc = tid + e * W2_NT;
       v[e] = __builtin_amdgcn_raw_buffer_load_b128(
-          rt, ((pc / PPR) * 4 * KBPC + (pc % PPR) * 8) * 2, b * W2_MB * 4 * KBPC * 2, 0);
+          rt, ((pc / PPR) * 4 * KBPC + (pc % PPR) * 8) * 2, b * MB * 4 * KBPC * 2, 0);
     }
   };
   auto stTW = [&](const u32x4 (&v)[TWP], int buf) {
-    _Float16* d = TW + buf * (W2_MB * LDT);
+    _Float16* d = TW + buf * (MB * LDT);
 #pragma unroll
     for (int e = 0; e < TWP; ++e) {
       const int pc = tid + e * W2_NT;
@@ -481,7 +487,7 @@ __global__ __launch_bounds__(W2_NT, 1) void c2r_wide2_kernel(C2RArgs a) {
   const int hiA = NhA * a.Nb * 2;
   auto xoff = [&](int c0, int b, int half, int h) {
     return (c0 + wave * 16 + (lane >> 3) + 8 * h) * a.Nb * 2 +
-           (half * Nh + b * W2_MB + (lane & 7) * 8) * 2;
+           (half * Nh + b * MB + (lane & 7) * 8) * 2;
   };
   // x of output segment sg = 2 u + half of block b (both row groups h)
   auto ldX = [&](const __amdgpu_buffer_rsrc_t& rx, int c0, int b, int sg, u32x4 (&v)[2]) {
@@ -582,7 +588,7 @@ __global__ __launch_bounds__(W2_NT, 1) void c2r_wide2_kernel(C2RArgs a) {
       // twiddles requested two blocks ahead (the sequence wraps at the item
       // boundary: every item walks the same blocks)
       ldTW(b + 2 < nmb ? b + 2 : b + 2 - nmb, twr[par]);
-      const _Float16* tb = TW + par * (W2_MB * LDT) + r16 * LDT + g * 8;
+      const _Float16* tb = TW + par * (MB * LDT) + r16 * LDT + g * 8;
 #pragma unroll
       for (int u = 0; u < 2; ++u) {
         if (EPI) {
@@ -598,9 +604,9 @@ __global__ __launch_bounds__(W2_NT, 1) void c2r_wide2_kernel(C2RArgs a) {
           }
         }
         const u32x4 (&xs2)[2][2] = xr[u];
-        f4 ae[4], ao[4];
+        f4 ae[NCB], ao[NCB];
 #pragma unroll
-        for (int c = 0; c < 4; ++c) {
+        for (int c = 0; c < NCB; ++c) {
           ae[c] = ao[c] = f4zero();
 #pragma unroll
           for (int k = 0; k < NKVC; ++k) {
@@ -609,16 +615,18 @@ __global__ __launch_bounds__(W2_NT, 1) void c2r_wide2_kernel(C2RArgs a) {
           }
         }
 #pragma unroll
-        for (int hf = 0; hf < 2; ++hf) {
+        for (int hq = 0; hq < 2 * (MB / 64); ++hq) {
+          const int hf = hq / (MB / 64), q = hq % (MB / 64);  // half, 64-column chunk
           const u32x4 (&xs)[2] = xs2[hf];
           // D: lane holds row r16 of the tile, columns m = c 16 + 4 g + i
 #pragma unroll
-          for (int c = 0; c < 4; ++c) {
+          for (int c4 = 0; c4 < 4; ++c4) {
+            const int c = q * 4 + c4;
             f4 v;
 #pragma unroll
             for (int i = 0; i < 4; ++i)
               v[i] = (hf == 0 ? ae[c][i] + ao[c][i] : ae[c][i] - ao[c][i]) * a.scale;
-            *reinterpret_cast<f4*>(ob + r16 * W2_LDO + ob_col(c * 16 + 4 * g)) = v;
+            *reinterpret_cast<f4*>(ob + r16 * W2_LDO + ob_col(c4 * 16 + 4 * g)) = v;
           }
           wave_lds_sync();
           // one row group h (row lane / 8 + 8 h, columns (lane % 8) 8 + e) at
@@ -652,7 +660,7 @@ __global__ __launch_bounds__(W2_NT, 1) void c2r_wide2_kernel(C2RArgs a) {
             // the compiler leaves no wait states between this store and a
             // VALU write of its data registers, and the store has then been
             // seen to take the new values of some lanes
-            __builtin_amdgcn_raw_buffer_store_b128(wv, ry, xoff(c0, b, hf, h) + u * hiA, 0, W2_NTS);
+            __builtin_amdgcn_raw_buffer_store_b128(wv, ry, xoff(c0, b, hf, h) + q * 128 + u * hiA, 0, W2_NTS);
           }
           wave_lds_sync();  // the buffer is written again by the next segment
         }
@@ -689,6 +697,9 @@ size_t c2r_wide2_lds_bytes(int nctc, int nkzh, bool epi, int lut_sat) {
   size_t base = 0;
 #define FNO_C2RW2_BYTES(N, K) \
   if (nctc == N && nkzh == K) base = C2RWide2<N, K>::zt_bytes + C2RWide2<N, K>::reg_bytes;
+  // the plain wide inverse may take 128-column blocks (enough for both)
+  if (!epi && nctc == 4 && nkzh == 2)
+    return C2RWide2<4, 2, 128>::zt_bytes + C2RWide2<4, 2, 128>::reg_bytes;
   FNO_C2RW2_BYTES(2, 1) FNO_C2RW2_BYTES(2, 2) FNO_C2RW2_BYTES(4, 1) FNO_C2RW2_BYTES(4, 2)
 #undef FNO_C2RW2_BYTES
   if (base == 0) return (size_t)1 << 30;  // not a shape of this path
@@ -746,6 +757,15 @@ hipError_t launch_c2r_wide2(const C2RArgs& a, int nctc, int grid, size_t lds, hi
   if (nctc == 2 && nkzh == 1) return c2r_wide2_go<2, 1>(a, grid, lds, s);
   if (nctc == 2 && nkzh == 2) return c2r_wide2_go<2, 2>(a, grid, lds, s);
   if (nctc == 4 && nkzh == 1) return c2r_wide2_go<4, 1>(a, grid, lds, s);
+  // plain wide inverse, Nb / 2 a multiple of 256 (an even count of
+  // 128-column blocks): 128-column blocks
+  if (nctc == 4 && nkzh == 2 && !a.epilogue && (a.Nb / 2) % 256 == 0) {
+    const void* k = (const void*)&c2r_wide2_kernel<4, 2, false, 128>;
+    hipError_t e = hipFuncSetAttribute(k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL((c2r_wide2_kernel<4, 2, false, 128>), dim3(grid), dim3(W2_NT), lds, s, a);
+    return hipGetLastError();
+  }
   if (nctc == 4 && nkzh == 2) return c2r_wide2_go<4, 2>(a, grid, lds, s);
   return hipErrorNotSupported;
 }
