@@ -72,6 +72,10 @@ EDGE = [
     ((512, 256), (20, 20), 2, 3, 2),    # 10 + 10 last-axis slots, 2 x 20 leading
     ((256, 512), (40, 36), 1, 2, 3),    # 18 + 18 last-axis slots (four column tiles)
     ((1024, 256), (8, 12), 3, 2, 2),    # four items per plane, 6 + 6 slots
+    # four column tiles: the plain inverse's 64-column blocks (Nb / 2 not a
+    # multiple of 256) beside the 128-column ones of (256, 512) above
+    ((256, 256), (40, 36), 1, 2, 3),    # two 64-column blocks
+    ((768, 768), (40, 40), 1, 2, 2),    # six 64-column blocks, three chunks
 ]
 
 
