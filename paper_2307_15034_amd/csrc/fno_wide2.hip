@@ -351,7 +351,14 @@ __global__ __launch_bounds__(W2_NT, 1) void r2c_wide2_kernel(R2CArgs a) {
 // (16 rows x 64 columns) requests its x at its start, after the previous
 // segment's stores, and uses it after its transpose.
 // ---------------------------------------------------------------------------
-template <int NCTC, int NKZH, int MB = W2_MB>
+constexpr int W2_LDOH = 72;        // fp16 transpose buffer row stride (halves)
+
+// LDS bytes of the inverse's table of codes 0..sat plus one NaN entry (its
+// lookups index at most sat + 1), rounded up to 256 (the regions after it
+// stay aligned)
+__host__ __device__ __forceinline__ int w2_lut_bytes(int sat) { return ((sat + 2) * 2 + 255) & ~255; }
+
+template <int NCTC, int NKZH, int MB = W2_MB, bool OB16 = false>
 struct C2RWide2 {
   static constexpr int KBPC = NCTC * 8;
   static constexpr int LDZ = NKZH * 32 + 8;
@@ -360,7 +367,8 @@ struct C2RWide2 {
   static constexpr size_t zt_bytes = (size_t)2 * 2 * (2 * KBPC) * LDZ * 2;
   static constexpr size_t vl_bytes = (size_t)2 * W2_H * LDV * 2;
   static constexpr size_t tw_bytes = (size_t)2 * MB * LDT * 2;
-  static constexpr size_t ob_bytes = (size_t)W2_WAVES * 16 * W2_LDO * 4;
+  static constexpr size_t ob_bytes =
+      OB16 ? (size_t)W2_WAVES * 16 * W2_LDOH * 2 : (size_t)W2_WAVES * 16 * W2_LDO * 4;
   static constexpr size_t reg_bytes =
       vl_bytes > tw_bytes + ob_bytes ? vl_bytes : tw_bytes + ob_bytes;
 };
@@ -368,13 +376,16 @@ struct C2RWide2 {
 template <int NCTC, int NKZH, bool EPI, int MB = W2_MB>
 __global__ __launch_bounds__(W2_NT, 1) void c2r_wide2_kernel(C2RArgs a) {
   typedef MM<_Float16> M;
-  typedef C2RWide2<NCTC, NKZH, MB> L;
-  // MB 128 (the plain inverse of the wide variant on planes with Nb / 2 a
-  // multiple of 256): half the blocks per item, so half the block barriers
-  // and twiddle stagings; each block's results still go out through the
-  // 64-column transpose buffer, one 64-column chunk at a time
-  static_assert(!EPI || MB == W2_MB, "wide blocks: plain inverse only");
-  constexpr int NCB = MB / 16;         // 16-column tiles per block
+  // MB 128 (the wide variant on planes with Nb / 2 a multiple of 256): half
+  // the blocks per item, so half the block barriers and twiddle stagings;
+  // each block's results still go out through the transpose buffer one
+  // 64-column chunk at a time.  With the epilogue the buffer then holds fp16
+  // (the table leaves no room for fp32): the products are rounded to fp16
+  // before the multiplication by f'(x), as an unfused epilogue would read
+  // them.
+  constexpr bool OB16 = EPI && MB == 128;
+  typedef C2RWide2<NCTC, NKZH, MB, OB16> L;
+  constexpr int NQ = MB / 64;          // 64-column chunks per block
   constexpr int KBPC = L::KBPC;
   constexpr int NTB = NCTC;            // p tiles (both step-A' classes)
   constexpr int NTBC = NCTC / 2;
@@ -388,7 +399,7 @@ __global__ __launch_bounds__(W2_NT, 1) void c2r_wide2_kernel(C2RArgs a) {
   extern __shared__ __align__(16) unsigned char smem[];
   // the lookup table first (a lookup address is the code's byte offset)
   _Float16* lut = reinterpret_cast<_Float16*>(smem);
-  _Float16* ZT = reinterpret_cast<_Float16*>(smem + (EPI ? lutn_bytes(a.lut_sat) : 0));
+  _Float16* ZT = reinterpret_cast<_Float16*>(smem + (EPI ? w2_lut_bytes(a.lut_sat) : 0));
   // [2][2][2 KBPC][LDZ]
   unsigned char* reg = reinterpret_cast<unsigned char*>(ZT) + L::zt_bytes;
   _Float16* VL = reinterpret_cast<_Float16*>(reg);       // [2 W2_H][LDV]
@@ -401,6 +412,7 @@ __global__ __launch_bounds__(W2_NT, 1) void c2r_wide2_kernel(C2RArgs a) {
   const _Float16* sI = reinterpret_cast<const _Float16*>(a.sI);
   const us2 sat = {(unsigned short)a.lut_sat, (unsigned short)a.lut_sat};
   float* ob = OB + wave * 16 * W2_LDO;
+  _Float16* obh = reinterpret_cast<_Float16*>(OB) + wave * 16 * W2_LDOH;
 
   const int Nh = a.Nb >> 1, NhA = a.Na >> 1;
   const int64_t plane_bytes = (int64_t)a.Na * a.Nb * 2;
@@ -416,7 +428,7 @@ __global__ __launch_bounds__(W2_NT, 1) void c2r_wide2_kernel(C2RArgs a) {
 
   // the padding of ZT stays zero: every plane writes the same positions
   for (int i = tid; i < 2 * 2 * 2 * KBPC * LDZ; i += W2_NT) ZT[i] = (_Float16)0.0f;
-  if (EPI) stage_lutn<W2_NT>(lut, a.lut, a.lut_sat);
+  if (EPI) stage_lut<W2_NT>(lut, a.lut, a.lut_sat);
 
   auto ldZ = [&](int64_t p, u32x4 (&zq)[ZQ]) {
     const __amdgpu_buffer_rsrc_t rz = plane_rsrc(a.in, p, spec_bytes);
@@ -489,30 +501,38 @@ __global__ __launch_bounds__(W2_NT, 1) void c2r_wide2_kernel(C2RArgs a) {
     return (c0 + wave * 16 + (lane >> 3) + 8 * h) * a.Nb * 2 +
            (half * Nh + b * MB + (lane & 7) * 8) * 2;
   };
-  // x of output segment sg = 2 u + half of block b (both row groups h)
-  auto ldX = [&](const __amdgpu_buffer_rsrc_t& rx, int c0, int b, int sg, u32x4 (&v)[2]) {
+  // x of unit (u, q) of block b: 64-column chunk q of the rows of tile u,
+  // both halves hf and both row groups h
+  auto ldX = [&](const __amdgpu_buffer_rsrc_t& rx, int c0, int b, int u, int q,
+                 u32x4 (&v)[2][2]) {
 #pragma unroll
-    for (int h = 0; h < 2; ++h)
-      v[h] = __builtin_amdgcn_raw_buffer_load_b128(rx, xoff(c0, b, sg & 1, h), (sg >> 1) * hiA, 0);
+    for (int hf = 0; hf < 2; ++hf)
+#pragma unroll
+      for (int h = 0; h < 2; ++h)
+        v[hf][h] = __builtin_amdgcn_raw_buffer_load_b128(rx, xoff(c0, b, hf, h) + q * 128, u * hiA, 0);
   };
 
   u32x4 zq[ZQ];
   h8 cf[2][NKZH], sf[2][NKZH];
-  u32x4 twr[2][TWP];     // twiddle blocks b + 1, b + 2 in flight
-  // x of the epilogue, one half of a block ahead: slot u holds half u of
-  // the current block; half 1's x is requested before half 0's products,
-  // the next block's half 0 before half 1's, and the next item's first
-  // half during this item's last block (the first item's before the loop)
+  // twiddle blocks in flight: b + 1 and b + 2, or, with 128-column blocks
+  // (each as long as two 64-column ones), b + 1
+  constexpr int TWA = MB == 128 ? 1 : 2;
+  u32x4 twr[TWA][TWP];
+  // x of the epilogue, one unit ahead: a block's units are (u, q), u the
+  // row tile and q the 64-column chunk, in that order; unit t of a block
+  // (t = u NQ + q) sits in slot t % 2.  Each unit's x is requested before
+  // the products of the unit before it, the next block's first unit before
+  // those of the last one, and the next item's first during this item's
+  // last block (the first item's before the loop)
   u32x4 xr[2][2][2];
   if (nitems > 0) {
     ldZ(item_plane(0), zq);
     ldC(0, cf, sf);
     ldTW(0, twr[0]);
-    ldTW(1, twr[1]);
+    if (TWA == 2) ldTW(1, twr[TWA - 1]);
     if (EPI) {
       const __amdgpu_buffer_rsrc_t rx0 = plane_rsrc(a.x, item_plane(0), plane_bytes);
-      ldX(rx0, item_chunk(0), 0, 0, xr[0][0]);
-      ldX(rx0, item_chunk(0), 0, 1, xr[0][1]);
+      ldX(rx0, item_chunk(0), 0, 0, 0, xr[0]);
     }
   }
   __syncthreads();  // ZT cleared, table staged
@@ -584,88 +604,103 @@ __global__ __launch_bounds__(W2_NT, 1) void c2r_wide2_kernel(C2RArgs a) {
     // staging has read it)
     const bool z_early = NCTC == 2 && nch == 1;
     if (more && z_early) ldZ(pn, zq);
+    // request the unit after unit t of block b (operands selected where
+    // there is no next item: this item's first unit again, in range)
+    auto req = [&](int b, int t) {
+      const int t1 = t + 1;
+      if (t1 < 2 * NQ) ldX(rx, c0, b, t1 / NQ, t1 % NQ, xr[t1 & 1]);
+      else if (b + 1 < nmb) ldX(rx, c0, b + 1, 0, 0, xr[0]);
+      else ldX(rxn, more ? cn : c0, 0, 0, 0, xr[0]);
+    };
     auto block = [&](int b, int par) {
-      // twiddles requested two blocks ahead (the sequence wraps at the item
-      // boundary: every item walks the same blocks)
-      ldTW(b + 2 < nmb ? b + 2 : b + 2 - nmb, twr[par]);
+      // twiddles requested two blocks (one 128-column block) ahead; the
+      // sequence wraps at the item boundary: every item walks the same blocks
+      if (TWA == 2) ldTW(b + 2 < nmb ? b + 2 : b + 2 - nmb, twr[par & (TWA - 1)]);
+      else ldTW(b + 1 < nmb ? b + 1 : 0, twr[0]);
       const _Float16* tb = TW + par * (MB * LDT) + r16 * LDT + g * 8;
 #pragma unroll
       for (int u = 0; u < 2; ++u) {
-        if (EPI) {
-          const int nb = u == 0 ? b : b + 1;
-          if (nb < nmb) {
-            ldX(rx, c0, nb, 2 * (1 - u), xr[1 - u][0]);
-            ldX(rx, c0, nb, 2 * (1 - u) + 1, xr[1 - u][1]);
-          } else {
-            // the next item's first half (this item's again, in range,
-            // when there is none: one load sequence)
-            ldX(rxn, more ? cn : c0, 0, 0, xr[0][0]);
-            ldX(rxn, more ? cn : c0, 0, 1, xr[0][1]);
-          }
-        }
-        const u32x4 (&xs2)[2][2] = xr[u];
-        f4 ae[NCB], ao[NCB];
 #pragma unroll
-        for (int c = 0; c < NCB; ++c) {
-          ae[c] = ao[c] = f4zero();
-#pragma unroll
-          for (int k = 0; k < NKVC; ++k) {
-            ae[c] = M::mma(M::ld(tb + c * 16 * LDT + k * W2_KS), vf[u][0][k], ae[c]);
-            ao[c] = M::mma(M::ld(tb + c * 16 * LDT + 2 * KBPC + k * W2_KS), vf[u][1][k], ao[c]);
-          }
-        }
-#pragma unroll
-        for (int hq = 0; hq < 2 * (MB / 64); ++hq) {
-          const int hf = hq / (MB / 64), q = hq % (MB / 64);  // half, 64-column chunk
-          const u32x4 (&xs)[2] = xs2[hf];
-          // D: lane holds row r16 of the tile, columns m = c 16 + 4 g + i
+        for (int q = 0; q < NQ; ++q) {
+          const int t = u * NQ + q;
+          if (EPI) req(b, t);  // before this unit's products
+          // the unit's four 16-column tiles
+          f4 ae[4], ao[4];
 #pragma unroll
           for (int c4 = 0; c4 < 4; ++c4) {
             const int c = q * 4 + c4;
-            f4 v;
+            ae[c4] = ao[c4] = f4zero();
 #pragma unroll
-            for (int i = 0; i < 4; ++i)
-              v[i] = (hf == 0 ? ae[c][i] + ao[c][i] : ae[c][i] - ao[c][i]) * a.scale;
-            *reinterpret_cast<f4*>(ob + r16 * W2_LDO + ob_col(c4 * 16 + 4 * g)) = v;
-          }
-          wave_lds_sync();
-          // one row group h (row lane / 8 + 8 h, columns (lane % 8) 8 + e) at
-          // a time: read, epilogue, store
-#pragma unroll
-          for (int h = 0; h < 2; ++h) {
-            float v[8];
-#pragma unroll
-            for (int e0 = 0; e0 < 8; e0 += 4) {
-              const f4 t = *reinterpret_cast<const f4*>(
-                  ob + ((lane >> 3) + 8 * h) * W2_LDO + ob_col((lane & 7) * 8 + e0));
-#pragma unroll
-              for (int i = 0; i < 4; ++i) v[e0 + i] = t[i];
+            for (int k = 0; k < NKVC; ++k) {
+              ae[c4] = M::mma(M::ld(tb + c * 16 * LDT + k * W2_KS), vf[u][0][k], ae[c4]);
+              ao[c4] = M::mma(M::ld(tb + c * 16 * LDT + 2 * KBPC + k * W2_KS), vf[u][1][k], ao[c4]);
             }
-            if (EPI) {
+          }
+          const u32x4 (&xs2)[2][2] = xr[t & 1];
 #pragma unroll
-              for (int e = 0; e < 4; ++e) {
-                const uint32_t sw = lut2<false>(lut, xs[h][e], sat);
-                h2 s2;
-                __builtin_memcpy(&s2, &sw, 4);
-                v[2 * e] *= (float)s2[0];
-                v[2 * e + 1] *= (float)s2[1];
+          for (int hf = 0; hf < 2; ++hf) {
+            const u32x4 (&xs)[2] = xs2[hf];
+            // D: lane holds row r16 of the tile, columns m = c 16 + 4 g + i
+#pragma unroll
+            for (int c4 = 0; c4 < 4; ++c4) {
+              f4 v;
+#pragma unroll
+              for (int i = 0; i < 4; ++i)
+                v[i] = (hf == 0 ? ae[c4][i] + ao[c4][i] : ae[c4][i] - ao[c4][i]) * a.scale;
+              if (OB16) {
+                const h4 hv = {to_h(v[0]), to_h(v[1]), to_h(v[2]), to_h(v[3])};
+                *reinterpret_cast<h4*>(obh + r16 * W2_LDOH + c4 * 16 + 4 * g) = hv;
+              } else {
+                *reinterpret_cast<f4*>(ob + r16 * W2_LDO + ob_col(c4 * 16 + 4 * g)) = v;
               }
             }
-            h8 w;
+            wave_lds_sync();
+            // one row group h (row lane / 8 + 8 h, columns (lane % 8) 8 + e) at
+            // a time: read, epilogue, store
 #pragma unroll
-            for (int e = 0; e < 8; ++e) w[e] = to_h(v[e]);
-            u32x4 wv;
-            __builtin_memcpy(&wv, &w, 16);
-            // the whole offset in the vector operand: with an SGPR offset
-            // the compiler leaves no wait states between this store and a
-            // VALU write of its data registers, and the store has then been
-            // seen to take the new values of some lanes
-            __builtin_amdgcn_raw_buffer_store_b128(wv, ry, xoff(c0, b, hf, h) + q * 128 + u * hiA, 0, W2_NTS);
+            for (int h = 0; h < 2; ++h) {
+              float v[8];
+              if (OB16) {
+                const h8 t8 = *reinterpret_cast<const h8*>(obh + ((lane >> 3) + 8 * h) * W2_LDOH +
+                                                           (lane & 7) * 8);
+#pragma unroll
+                for (int e = 0; e < 8; ++e) v[e] = (float)t8[e];
+              } else {
+#pragma unroll
+                for (int e0 = 0; e0 < 8; e0 += 4) {
+                  const f4 t4 = *reinterpret_cast<const f4*>(
+                      ob + ((lane >> 3) + 8 * h) * W2_LDO + ob_col((lane & 7) * 8 + e0));
+#pragma unroll
+                  for (int i = 0; i < 4; ++i) v[e0 + i] = t4[i];
+                }
+              }
+              if (EPI) {
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                  const uint32_t sw = lut2<false>(lut, xs[h][e], sat);
+                  h2 s2;
+                  __builtin_memcpy(&s2, &sw, 4);
+                  v[2 * e] *= (float)s2[0];
+                  v[2 * e + 1] *= (float)s2[1];
+                }
+              }
+              h8 w;
+#pragma unroll
+              for (int e = 0; e < 8; ++e) w[e] = to_h(v[e]);
+              u32x4 wv;
+              __builtin_memcpy(&wv, &w, 16);
+              // the whole offset in the vector operand: with an SGPR offset
+              // the compiler leaves no wait states between this store and a
+              // VALU write of its data registers, and the store has then
+              // been seen to take the new values of some lanes
+              __builtin_amdgcn_raw_buffer_store_b128(wv, ry, xoff(c0, b, hf, h) + q * 128 + u * hiA,
+                                                     0, W2_NTS);
+            }
+            wave_lds_sync();  // the buffer is written again by the next segment
           }
-          wave_lds_sync();  // the buffer is written again by the next segment
         }
       }
-      stTW(twr[1 - par], 1 - par);
+      stTW(twr[(1 - par) & (TWA - 1)], 1 - par);
       __syncthreads();
     };
 #pragma nounroll
@@ -697,13 +732,15 @@ size_t c2r_wide2_lds_bytes(int nctc, int nkzh, bool epi, int lut_sat) {
   size_t base = 0;
 #define FNO_C2RW2_BYTES(N, K) \
   if (nctc == N && nkzh == K) base = C2RWide2<N, K>::zt_bytes + C2RWide2<N, K>::reg_bytes;
-  // the plain wide inverse may take 128-column blocks (enough for both)
-  if (!epi && nctc == 4 && nkzh == 2)
-    return C2RWide2<4, 2, 128>::zt_bytes + C2RWide2<4, 2, 128>::reg_bytes;
+  // the wide variant may take 128-column blocks (enough for both)
+  if (nctc == 4 && nkzh == 2)
+    return epi ? C2RWide2<4, 2, 128, true>::zt_bytes + C2RWide2<4, 2, 128, true>::reg_bytes +
+                     (size_t)w2_lut_bytes(lut_sat)
+               : C2RWide2<4, 2, 128>::zt_bytes + C2RWide2<4, 2, 128>::reg_bytes;
   FNO_C2RW2_BYTES(2, 1) FNO_C2RW2_BYTES(2, 2) FNO_C2RW2_BYTES(4, 1) FNO_C2RW2_BYTES(4, 2)
 #undef FNO_C2RW2_BYTES
   if (base == 0) return (size_t)1 << 30;  // not a shape of this path
-  return base + (epi ? (size_t)lutn_bytes(lut_sat) : 0);
+  return base + (epi ? (size_t)w2_lut_bytes(lut_sat) : 0);
 }
 
 template <int NCTC, bool PRE, bool EARLY>
@@ -757,13 +794,17 @@ hipError_t launch_c2r_wide2(const C2RArgs& a, int nctc, int grid, size_t lds, hi
   if (nctc == 2 && nkzh == 1) return c2r_wide2_go<2, 1>(a, grid, lds, s);
   if (nctc == 2 && nkzh == 2) return c2r_wide2_go<2, 2>(a, grid, lds, s);
   if (nctc == 4 && nkzh == 1) return c2r_wide2_go<4, 1>(a, grid, lds, s);
-  // plain wide inverse, Nb / 2 a multiple of 256 (an even count of
-  // 128-column blocks): 128-column blocks
-  if (nctc == 4 && nkzh == 2 && !a.epilogue && (a.Nb / 2) % 256 == 0) {
-    const void* k = (const void*)&c2r_wide2_kernel<4, 2, false, 128>;
+  // wide variant, Nb / 2 a multiple of 256 (an even count of 128-column
+  // blocks): 128-column blocks
+  if (nctc == 4 && nkzh == 2 && (a.Nb / 2) % 256 == 0) {
+    const void* k = a.epilogue ? (const void*)&c2r_wide2_kernel<4, 2, true, 128>
+                               : (const void*)&c2r_wide2_kernel<4, 2, false, 128>;
     hipError_t e = hipFuncSetAttribute(k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL((c2r_wide2_kernel<4, 2, false, 128>), dim3(grid), dim3(W2_NT), lds, s, a);
+    if (a.epilogue)
+      hipLaunchKernelGGL((c2r_wide2_kernel<4, 2, true, 128>), dim3(grid), dim3(W2_NT), lds, s, a);
+    else
+      hipLaunchKernelGGL((c2r_wide2_kernel<4, 2, false, 128>), dim3(grid), dim3(W2_NT), lds, s, a);
     return hipGetLastError();
   }
   if (nctc == 4 && nkzh == 2) return c2r_wide2_go<4, 2>(a, grid, lds, s);
